@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the SpotAttention hot path on one MI355X.
+
+One step = selector scoring of every KV block + dual top-p/top-K selection +
+block-sparse GQA decode attention, for all sequences of one layer, on the
+Qwen3-8B-shaped 128K-token workload (batch 4, 32 query / 8 KV heads, d = 128,
+2048 blocks of 64 tokens, p = 0.95, K_max = 128, 1 sink + 2 recent blocks).
+
+Inputs are resident in HBM before timing starts.  The timed loop rotates
+over NCOPY distinct copies of the KV cache and selector cache so that the
+256 MB last-level cache cannot serve repeated steps.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "decode steps/s at L=128K (selector+sparse attn), % of HBM peak GB/s"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--copies", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--dense", action="store_true", help="also time the dense decode baseline")
+    ap.add_argument("--fmt", default="bf16", choices=["bf16", "int4", "mxfp4"])
+    return ap.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the decode path "
+              "needs no cross-GPU exchange and this build measures a single device.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_22874_amd import spot, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    spot.load()
+
+    log("[bench] generating the 128K-token decode workload")
+    t0 = time.time()
+    wl = synth.decode_config(3)
+    log(f"[bench] generated in {time.time() - t0:.1f}s")
+    B, Hq, Hkv, d, L = wl.B, wl.Hq, wl.Hkv, wl.d, wl.L
+    nblk, rule = wl.nblk, wl.rule
+
+    def bf(a):
+        return spot.to_device_bf16(a, dev)
+
+    # Selector cache in the requested storage format.
+    if args.fmt == "bf16":
+        ksel_host, kscale_host = wl.k_sel, None
+        sel_bytes = wl.k_sel.nbytes
+    elif args.fmt == "int4":
+        ksel_host, kscale_host = synth.quantize_int4_g32(wl.k_sel)
+        sel_bytes = ksel_host.nbytes + kscale_host.nbytes
+    else:
+        ksel_host, kscale_host = synth.quantize_mxfp4_g32(wl.k_sel)
+        sel_bytes = ksel_host.nbytes + kscale_host.nbytes
+
+    def dev_sel():
+        if args.fmt == "bf16":
+            return bf(ksel_host), None
+        ks = torch.from_numpy(np.ascontiguousarray(ksel_host)).to(dev)
+        sc = kscale_host.view(np.int16) if args.fmt == "int4" else kscale_host
+        return ks, torch.from_numpy(np.ascontiguousarray(sc)).to(dev)
+
+    q = bf(wl.q)
+    q_sel = bf(wl.q_sel)
+    w = torch.from_numpy(wl.w).to(dev)
+    seq_len = torch.from_numpy(wl.seq_len).to(dev)
+    n_valid = torch.from_numpy(wl.n_valid).to(dev)
+    k0, v0 = bf(wl.k), bf(wl.v)
+    copies = []
+    for c in range(args.copies):
+        ks, sc = dev_sel()
+        copies.append((k0 if c == 0 else k0.clone(), v0 if c == 0 else v0.clone(), ks, sc))
+    torch.cuda.synchronize()
+
+    scores = torch.empty((B, nblk), dtype=torch.float32, device=dev)
+    idx = torch.empty((B, rule.k_max), dtype=torch.int32, device=dev)
+    cnt = torch.empty(B, dtype=torch.int32, device=dev)
+    mass = torch.empty(B, dtype=torch.float32, device=dev)
+    out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    ws = spot.decode_workspace(B, Hq, Hkv, d, rule.k_max, dev)
+    stream = torch.cuda.current_stream()
+
+    def step(c, ev=None):
+        k, v, ks, sc = copies[c % len(copies)]
+        spot.spot_selector_score(q_sel, w, ks, sc, args.fmt, B, 1, nblk, wl.Hs, wl.ds, n_valid,
+                                 scores, stream)
+        spot.spot_select_blocks(scores, B, nblk, n_valid, rule.top_p, rule.k_max, rule.k_min,
+                                rule.n_sink, rule.n_recent, idx, cnt, mass, stream)
+        if ev is not None:
+            ev[0].record(stream)
+        spot.spot_sparse_decode(q, k, v, seq_len, idx, cnt, rule.k_max, B, Hq, Hkv, d, L,
+                                wl.sm_scale, out, lse, ws, stream)
+        if ev is not None:
+            ev[1].record(stream)
+
+    log(f"[bench] warmup {args.warmup} steps")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    counts = cnt.cpu().numpy()
+
+    # Timed region: K steps, events around the attention call of every step.
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        step(i, evs[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    log(f"[bench] {ms * 1e3:.1f} us/step, attention call {attn_ms * 1e3:.1f} us")
+
+    kv_block_bytes = kBlkBytes = 64 * Hkv * d * 2 * 2          # K and V of one block
+    attn_bytes = int(counts.sum()) * kv_block_bytes
+    step_bytes = sel_bytes + attn_bytes
+    steps_per_s = 1e3 / ms
+    step_gbs = step_bytes / (ms * 1e-3) / 1e9
+    attn_gbs = attn_bytes / (attn_ms * 1e-3) / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": round(steps_per_s, 1),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "decode L=131072 B=4 (Qwen3-8B-shaped layer: 32 q / 8 kv heads, d=128; "
+                        "selector 8x64 pooled per 64-token block; p=0.95 K_max=128 sink 1 recent 2)",
+            "selector_cache": args.fmt,
+            "copies_rotated": args.copies,
+            "mean_selected_blocks": float(counts.mean()),
+            "bytes_per_step": step_bytes,
+            "step_hbm_gbs": round(step_gbs, 1),
+            "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "spot_sparse_decode (split + merge)",
+            "achieved": round(attn_gbs, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "bytes_per_launch": attn_bytes,
+            "avg_launch_us": round(attn_ms * 1e3, 2),
+        },
+    }
+
+    if args.dense:
+        wsd = spot.decode_workspace(B, Hq, Hkv, d, nblk, dev)
+        for i in range(3):
+            k, v, _, _ = copies[i % len(copies)]
+            spot.spot_dense_decode(q, k, v, seq_len, B, Hq, Hkv, d, L, wl.sm_scale, out, lse, wsd,
+                                   stream)
+        torch.cuda.synchronize()
+        n_d = 20
+        start.record(stream)
+        for i in range(n_d):
+            k, v, _, _ = copies[i % len(copies)]
+            spot.spot_dense_decode(q, k, v, seq_len, B, Hq, Hkv, d, L, wl.sm_scale, out, lse, wsd,
+                                   stream)
+        end.record(stream)
+        torch.cuda.synchronize()
+        dms = start.elapsed_time(end) / n_d
+        dbytes = B * Hkv * L * d * 2 * 2
+        result["dense_baseline"] = {
+            "value": round(1e3 / dms, 1), "unit": "steps/s", "ms_per_step": round(dms, 4),
+            "hbm_gbs": round(dbytes / (dms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(dbytes / (dms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(wl, budget_s):
+    """The FP64 oracle timed on the host cores over whole decode steps."""
+    import oracle
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    oracle.set_threads(cores)
+    log(f"[bench] cpu baseline: oracle on {cores} threads for ~{budget_s:.0f}s")
+    n, t0 = 0, time.time()
+    while True:
+        s = oracle.selector_score(wl.q_sel, wl.w, wl.k_sel, n_valid=wl.n_valid)
+        idx, cnt, _ = oracle.select_blocks(s.astype(np.float32), wl.rule, wl.n_valid)
+        oracle.sparse_decode(wl.q, wl.k, wl.v, wl.seq_len, idx, cnt, wl.sm_scale)
+        n += 1
+        el = time.time() - t0
+        if el >= budget_s or (n >= 1 and el * (n + 1) / n > 30.0):
+            break
+    return {"value": round(n / el, 4), "unit": "steps/s", "cores": oracle.get_threads(),
+            "kind": "oracle",
+            "sample": f"{n} full decode steps (score + select + sparse attention, all 4 "
+                      f"sequences) of the same workload, FP64 C with OpenMP"}
+
+
+if __name__ == "__main__":
+    main()

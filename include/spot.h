@@ -1,0 +1,197 @@
+/*
+ * spot.h -- C ABI of the SpotAttention hot path for MI355X (gfx950).
+ *
+ * One decode step of a full-attention layer is
+ *   spot_selector_score  -> block scores of every KV block       (Section 2.1)
+ *   spot_select_blocks   -> dual top-p / top-K block set          (Section 2.3)
+ *   spot_sparse_decode   -> GQA attention over the chosen blocks  (Section 2)
+ * with spot_dense_decode as the full-attention baseline and
+ * spot_sparse_prefill as the block-sparse causal prefill over query blocks.
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers named as device arrays are caller-owned device memory; the
+ *    library never allocates, frees, or synchronises, and keeps no state
+ *    between calls.  Arrays are C-contiguous.  BF16 arrays hold bfloat16
+ *    values (2 bytes each).  A KV block is 64 consecutive tokens; the
+ *    selector key cache holds one pooled key per block.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *    enqueues work on it and returns; the returned status covers argument
+ *    validation and the launch itself.  A fault inside a kernel surfaces at
+ *    the caller's next synchronisation.
+ *  - Arguments are validated before anything is enqueued.  On any non-zero
+ *    status nothing was enqueued and no output was touched.
+ *  - Calls are re-entrant; calls on different streams may run concurrently
+ *    as long as they do not share output or workspace buffers.
+ */
+#ifndef SPOT_H
+#define SPOT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t spot_status;
+
+#define SPOT_OK 0
+#define SPOT_ERR_NULL 1        /* a required pointer is NULL                      */
+#define SPOT_ERR_SHAPE 2       /* a size or shape is out of range / inconsistent  */
+#define SPOT_ERR_UNSUPPORTED 3 /* a valid but unimplemented size or format        */
+#define SPOT_ERR_RULE 4        /* selection rule parameters are invalid           */
+#define SPOT_ERR_WORKSPACE 5   /* the workspace is missing or too small           */
+#define SPOT_ERR_HIP 6         /* the HIP runtime reported a launch error         */
+
+/* Storage formats of the selector key cache (Section 5.3, Appendix G:
+ * group-32 microscale 4-bit formats alongside BF16). */
+#define SPOT_KFMT_BF16 0
+#define SPOT_KFMT_INT4_G32 1  /* signed 4-bit codes, FP16 scale per 32 elements */
+#define SPOT_KFMT_MXFP4_G32 2 /* OCP MXFP4: E2M1 codes, E8M0 scale per 32       */
+
+/* Human-readable name of a status code (static storage). */
+const char *spot_status_str(spot_status s);
+
+/* Library version string (static storage). */
+const char *spot_version(void);
+
+/*
+ * spot_selector_score -- block scores of the learned selector.
+ *
+ * Section 2.1: the selector's score of a key for a query is the head-weighted
+ * ReLU score  s = sum_h w_h * ReLU(q_h . k_h), computed once per
+ * query-block x key-block tile.  Here the key side of a tile is the block's
+ * pooled selector key k_bar[b, j, h, :], so
+ *     scores[r, j] = sum_{h < h_s} w[r, h] * max(0, sum_{i < d_s} q_sel[r, h, i] * k_bar[seq(r), j, h, i])
+ * with no 1/sqrt(d_s) factor (temperature 1).  Rows r = 0 .. n_seq*rows_per_seq-1
+ * and seq(r) = r / rows_per_seq: decode uses rows_per_seq = 1 (one query per
+ * sequence); prefill uses rows_per_seq = number of query blocks, with q_sel
+ * and w holding query-block pooled selector queries and weights.
+ *
+ *  q_sel    device, BF16 [n_seq*rows_per_seq, h_s, d_s]
+ *  w        device, float [n_seq*rows_per_seq, h_s]
+ *  k_sel    device, selector key cache, [n_seq, nblk, h_s, d_s] BF16 for
+ *           SPOT_KFMT_BF16; for the 4-bit formats uint8 [n_seq, nblk, h_s, d_s/2]
+ *           with element 2i in the low nibble of byte i
+ *  k_scale  device, NULL for BF16; else [n_seq, nblk, h_s, d_s/32] of FP16
+ *           (INT4: value = code * scale, code the nibble as two's complement)
+ *           or uint8 E8M0 (MXFP4: value = E2M1(code) * 2^(e - 127))
+ *  n_valid  device int32 [rows] (blocks j >= n_valid[r] do not exist and score
+ *           -inf) or NULL (every block valid)
+ *  scores   device, float [rows, nblk]  (output)
+ *
+ * Supported: h_s * d_s == 512 with d_s in {64, 128} (decode, any format);
+ * rows_per_seq > 1 requires SPOT_KFMT_BF16, h_s <= 16 and d_s == 64.
+ */
+spot_status spot_selector_score(const void *q_sel, const float *w, const void *k_sel,
+                                const void *k_scale, int kfmt, int n_seq, int rows_per_seq,
+                                int nblk, int h_s, int d_s, const int32_t *n_valid,
+                                float *scores, void *stream);
+
+/*
+ * spot_select_blocks -- dual top-p / static top-K block selection.
+ *
+ * Section 2.3 (Eqs. select-topk, select-nucleus, select-topp).  Per row r,
+ * over the valid blocks [0, nv) with nv = n_valid[r] (or nblk):
+ *  1. reserved R = sink prefix [0, n_sink) u recency suffix [nv-n_recent, nv);
+ *  2. residual softmax p~ over B_res = [0, nv) \ R (reserved blocks excluded);
+ *  3. nucleus = the smallest prefix of B_res in descending score order (equal
+ *     scores: lower block id first) whose cumulative p~ reaches top_p
+ *     (inclusive); top_p >= 1 takes all of B_res, top_p <= 0 none;
+ *  4. cap |R| + |nucleus| <= k_max, then floor |S| >= k_min by extending the
+ *     nucleus along the same order (never past k_max or |B_res|).
+ * Static top-K is top_p = 1, n_sink = n_recent = 0, k_max = K.
+ *
+ *  scores    device float [rows, nblk] (entries j >= nv are ignored)
+ *  n_valid   device int32 [rows] or NULL
+ *  idx       device int32 [rows, k_max] (output): S in ascending block id,
+ *            padded with -1
+ *  count     device int32 [rows] (output): |S|
+ *  nuc_mass  device float [rows] (output, may be NULL): p~-mass of the nucleus
+ *
+ * Errors: SPOT_ERR_RULE if top_p is NaN, k_max < 1, k_min > k_max,
+ * n_sink < 0, n_recent < 0 or k_max < n_sink + n_recent; SPOT_ERR_UNSUPPORTED
+ * if nblk > 16384 or k_max > 4096.  Deterministic: the same scores give the
+ * same outputs bit for bit.
+ */
+spot_status spot_select_blocks(const float *scores, int rows, int nblk, const int32_t *n_valid,
+                               float top_p, int k_max, int k_min, int n_sink, int n_recent,
+                               int32_t *idx, int32_t *count, float *nuc_mass, void *stream);
+
+/*
+ * Workspace bytes that spot_sparse_decode (max_blocks = k_max) and
+ * spot_dense_decode (max_blocks = ceil(l_cap / 64)) need for these sizes.
+ */
+size_t spot_decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_blocks);
+
+/*
+ * spot_sparse_decode -- GQA decode attention over the selected blocks only.
+ *
+ * Section 2 and the method figure: the layer attends only to the keys and
+ * values of the selected block set S (one set per sequence, shared by every
+ * head).  For sequence b and query head h with KV head g = h / (h_q / h_kv):
+ *     out[b, h] = sum_{t in T} softmax_t(sm_scale * q[b,h] . k[b,g,t]) v[b,g,t],
+ *     T = { t < seq_len[b] : t / 64 in S_b },  lse[b, h] = log sum_{t in T} exp(.)
+ * Entries of idx that are negative or whose block starts at or past seq_len
+ * are skipped, so a bad index cannot cause an out-of-bounds read.  An empty
+ * T gives out = 0 and lse = -inf.
+ *
+ *  q        device BF16 [batch, h_q, d]
+ *  k, v     device BF16 [batch, h_kv, l_cap, d]  (l_cap a multiple of 64)
+ *  seq_len  device int32 [batch] (values above l_cap are clamped to l_cap)
+ *  idx      device int32 [batch, k_max] distinct block ids, any order
+ *  count    device int32 [batch] number of leading entries of idx to use
+ *  out      device BF16 [batch, h_q, d] (output, round to nearest even)
+ *  lse      device float [batch, h_q] (output, may be NULL)
+ *  ws       device workspace of at least
+ *           spot_decode_workspace_bytes(batch, h_q, h_kv, d, k_max) bytes
+ *
+ * Supported: d == 128, h_q / h_kv in {1, 2, 4, 8}.
+ */
+spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
+                               const int32_t *seq_len, const int32_t *idx, const int32_t *count,
+                               int k_max, int batch, int h_q, int h_kv, int d, int l_cap,
+                               float sm_scale, void *out, float *lse, void *ws, size_t ws_bytes,
+                               void *stream);
+
+/*
+ * spot_dense_decode -- the dense decode baseline: spot_sparse_decode with
+ * every block < ceil(seq_len / 64) selected (full attention over the cache).
+ * Same layouts; ws of spot_decode_workspace_bytes(batch, h_q, h_kv, d,
+ * l_cap / 64) bytes.
+ */
+spot_status spot_dense_decode(const void *q, const void *k, const void *v,
+                              const int32_t *seq_len, int batch, int h_q, int h_kv, int d,
+                              int l_cap, float sm_scale, void *out, float *lse, void *ws,
+                              size_t ws_bytes, void *stream);
+
+/*
+ * spot_sparse_prefill -- block-sparse causal prefill.
+ *
+ * The paper's selector runs in the prefill regime with one selected key-block
+ * set per query block (Section 2.1: one score per query-block x key-block
+ * tile; Appendix B: the selector and block-sparse kernels run in prefill).
+ * Query token i of query block qb (position p = 64*qb + i) attends to the
+ * tokens t <= p of the key blocks selected for row (b, qb):
+ *     out[b, h, p] = sum_t softmax_t(sm_scale * q[b,h,p] . k[b,g,t]) v[b,g,t]
+ * with g = h / (h_q / h_kv).  Selected ids > qb contribute nothing (causal);
+ * negative ids are skipped.
+ *
+ *  q        device BF16 [batch, h_q, L, d]
+ *  k, v     device BF16 [batch, h_kv, L, d]   (L a multiple of 64)
+ *  idx      device int32 [batch * L/64, k_max] distinct ids, ascending
+ *  count    device int32 [batch * L/64]
+ *  out      device BF16 [batch, h_q, L, d] (output)
+ *  lse      device float [batch, h_q, L] (output, may be NULL)
+ *
+ * Supported: d == 128, h_q / h_kv in {1, 2, 4, 8}.
+ */
+spot_status spot_sparse_prefill(const void *q, const void *k, const void *v, int L,
+                                const int32_t *idx, const int32_t *count, int k_max, int batch,
+                                int h_q, int h_kv, int d, float sm_scale, void *out, float *lse,
+                                void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPOT_H */

@@ -1,0 +1,126 @@
+// C ABI of libspot: argument validation, then kernel launches.  Nothing is
+// enqueued unless every argument check passes.
+#include "spot_internal.h"
+
+#define SPOT_VERSION_STR "spot-mi355x 0.1 (gfx950)"
+
+using namespace spot;
+
+namespace {
+
+spot_status from_hip(hipError_t e) { return e == hipSuccess ? SPOT_OK : SPOT_ERR_HIP; }
+
+bool supported_group(int h_q, int h_kv) {
+  if (h_kv < 1 || h_q < h_kv || h_q % h_kv) return false;
+  const int g = h_q / h_kv;
+  return g == 1 || g == 2 || g == 4 || g == 8;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* spot_status_str(spot_status s) {
+  switch (s) {
+    case SPOT_OK: return "ok";
+    case SPOT_ERR_NULL: return "null pointer";
+    case SPOT_ERR_SHAPE: return "invalid shape";
+    case SPOT_ERR_UNSUPPORTED: return "unsupported size or format";
+    case SPOT_ERR_RULE: return "invalid selection rule";
+    case SPOT_ERR_WORKSPACE: return "workspace missing or too small";
+    case SPOT_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+const char* spot_version(void) { return SPOT_VERSION_STR; }
+
+spot_status spot_selector_score(const void* q_sel, const float* w, const void* k_sel,
+                                const void* k_scale, int kfmt, int n_seq, int rows_per_seq,
+                                int nblk, int h_s, int d_s, const int32_t* n_valid,
+                                float* scores, void* stream) {
+  if (!q_sel || !w || !k_sel || !scores) return SPOT_ERR_NULL;
+  if (n_seq < 0 || rows_per_seq < 1 || nblk < 0 || h_s < 1 || d_s < 1) return SPOT_ERR_SHAPE;
+  if (kfmt != SPOT_KFMT_BF16 && kfmt != SPOT_KFMT_INT4_G32 && kfmt != SPOT_KFMT_MXFP4_G32)
+    return SPOT_ERR_UNSUPPORTED;
+  if (kfmt != SPOT_KFMT_BF16 && !k_scale) return SPOT_ERR_NULL;
+  if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
+  if ((long long)n_seq * rows_per_seq > 0x7fffffffLL) return SPOT_ERR_SHAPE;
+  if (n_seq == 0 || nblk == 0) return SPOT_OK;
+  return from_hip(launch_selector_score(q_sel, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq,
+                                        nblk, h_s, d_s, n_valid, scores,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+spot_status spot_select_blocks(const float* scores, int rows, int nblk, const int32_t* n_valid,
+                               float top_p, int k_max, int k_min, int n_sink, int n_recent,
+                               int32_t* idx, int32_t* count, float* nuc_mass, void* stream) {
+  if (!scores || !idx || !count) return SPOT_ERR_NULL;
+  if (rows < 0 || nblk < 0) return SPOT_ERR_SHAPE;
+  if (top_p != top_p || k_max < 1 || k_min > k_max || n_sink < 0 || n_recent < 0 ||
+      k_max < n_sink + n_recent)
+    return SPOT_ERR_RULE;
+  if (nblk > 16384 || k_max > 4096) return SPOT_ERR_UNSUPPORTED;
+  if (rows == 0) return SPOT_OK;
+  return from_hip(launch_select_blocks(scores, rows, nblk, n_valid, top_p, k_max, k_min, n_sink,
+                                       n_recent, idx, count, nuc_mass,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+size_t spot_decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_blocks) {
+  if (batch < 1 || h_q < 1 || h_kv < 1 || d < 1 || max_blocks < 1) return 0;
+  return decode_workspace_bytes(batch, h_q, h_kv, d, max_blocks);
+}
+
+static spot_status check_decode(const void* q, const void* k, const void* v,
+                                const int32_t* seq_len, const void* out, int batch, int h_q,
+                                int h_kv, int d, int l_cap) {
+  if (!q || !k || !v || !seq_len || !out) return SPOT_ERR_NULL;
+  if (batch < 0 || h_q < 1 || h_kv < 1 || l_cap < 0 || l_cap % kBlk) return SPOT_ERR_SHAPE;
+  if (d != 128 || !supported_group(h_q, h_kv)) return SPOT_ERR_UNSUPPORTED;
+  return SPOT_OK;
+}
+
+spot_status spot_sparse_decode(const void* q, const void* k, const void* v,
+                               const int32_t* seq_len, const int32_t* idx, const int32_t* count,
+                               int k_max, int batch, int h_q, int h_kv, int d, int l_cap,
+                               float sm_scale, void* out, float* lse, void* ws, size_t ws_bytes,
+                               void* stream) {
+  spot_status st = check_decode(q, k, v, seq_len, out, batch, h_q, h_kv, d, l_cap);
+  if (st != SPOT_OK) return st;
+  if (!idx || !count) return SPOT_ERR_NULL;
+  if (k_max < 1) return SPOT_ERR_SHAPE;
+  if (batch == 0) return SPOT_OK;
+  if (!ws || ws_bytes < decode_workspace_bytes(batch, h_q, h_kv, d, k_max))
+    return SPOT_ERR_WORKSPACE;
+  return from_hip(launch_decode(false, q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv,
+                                l_cap, sm_scale, out, lse, ws, static_cast<hipStream_t>(stream)));
+}
+
+spot_status spot_dense_decode(const void* q, const void* k, const void* v,
+                              const int32_t* seq_len, int batch, int h_q, int h_kv, int d,
+                              int l_cap, float sm_scale, void* out, float* lse, void* ws,
+                              size_t ws_bytes, void* stream) {
+  spot_status st = check_decode(q, k, v, seq_len, out, batch, h_q, h_kv, d, l_cap);
+  if (st != SPOT_OK) return st;
+  if (l_cap == 0) return SPOT_ERR_SHAPE;
+  if (batch == 0) return SPOT_OK;
+  if (!ws || ws_bytes < decode_workspace_bytes(batch, h_q, h_kv, d, l_cap / kBlk))
+    return SPOT_ERR_WORKSPACE;
+  return from_hip(launch_decode(true, q, k, v, seq_len, nullptr, nullptr, 0, batch, h_q, h_kv,
+                                l_cap, sm_scale, out, lse, ws, static_cast<hipStream_t>(stream)));
+}
+
+spot_status spot_sparse_prefill(const void* q, const void* k, const void* v, int L,
+                                const int32_t* idx, const int32_t* count, int k_max, int batch,
+                                int h_q, int h_kv, int d, float sm_scale, void* out, float* lse,
+                                void* stream) {
+  if (!q || !k || !v || !idx || !count || !out) return SPOT_ERR_NULL;
+  if (L < 0 || L % kBlk || batch < 0 || k_max < 1 || h_q < 1 || h_kv < 1) return SPOT_ERR_SHAPE;
+  if (d != 128 || !supported_group(h_q, h_kv)) return SPOT_ERR_UNSUPPORTED;
+  if (batch == 0 || L == 0) return SPOT_OK;
+  return from_hip(launch_sparse_prefill(q, k, v, L, idx, count, k_max, batch, h_q, h_kv,
+                                        sm_scale, out, lse, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,351 @@
+// Dual top-p / top-K block selection (paper Section 2.3, Eqs. select-topk,
+// select-nucleus and select-topp) with a cap k_max on the set size.
+//
+// One workgroup (256 threads) per row.  Thread t owns the EPT consecutive
+// block ids [t*EPT, (t+1)*EPT) in registers.  Per row:
+//  1. reserved blocks (sink prefix, recency suffix) are set aside; the
+//     residual candidates get an order-preserving 32-bit key of their score;
+//  2. residual softmax statistics: max and Z = sum exp(s - max) with a fixed
+//     reduction tree (deterministic);
+//  3. only the best C = min(k_max - |R|, |B_res|) candidates can ever be
+//     chosen, so a fixed 4-pass 8-bit radix select finds the C-th largest key;
+//     equal keys at the threshold are taken in ascending block id;
+//  4. the C survivors are bitonic-sorted in LDS by (score desc, id asc), their
+//     probabilities prefix-summed in that order (fixed tree, FP32), and the
+//     nucleus length n is the first prefix reaching top_p * Z, then capped
+//     and floored by k_min;
+//  5. reserved + the first n survivors are written in ascending block id.
+#include "spot_internal.h"
+
+namespace spot {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+__device__ __forceinline__ uint32_t order_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float order_key_inv(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+struct Scratch {
+  int wave_i[kWaves];
+  float wave_f[kWaves];
+  uint32_t wave_u[kWaves];
+  uint32_t hist[256];
+  int digit;
+  int need;
+};
+
+// Block-wide exclusive prefix sum of one int per thread (thread order).
+__device__ __forceinline__ int block_excl_scan(int v, int& total, Scratch& sc) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
+  }
+  if (lane == 63) sc.wave_i[wave] = incl;
+  __syncthreads();
+  int base = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int t = sc.wave_i[w];
+    base += (w < wave) ? t : 0;
+    total += t;
+  }
+  __syncthreads();
+  return base + incl - v;
+}
+
+// Block-wide exclusive prefix sum of one float per thread; fixed order.
+__device__ __forceinline__ float block_excl_scan_f(float v, Scratch& sc) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
+  }
+  if (lane == 63) sc.wave_f[wave] = incl;
+  __syncthreads();
+  float base = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) base += (w < wave) ? sc.wave_f[w] : 0.f;
+  __syncthreads();
+  return base + (incl - v);
+}
+
+__device__ __forceinline__ float block_sum_f(float v, Scratch& sc) {
+  v = wave_sum(v);
+  if ((threadIdx.x & 63) == 0) sc.wave_f[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) t += sc.wave_f[w];
+  __syncthreads();
+  return t;
+}
+
+__device__ __forceinline__ int block_sum_i(int v, Scratch& sc) {
+  int total;
+  block_excl_scan(v, total, sc);
+  return total;
+}
+
+__device__ __forceinline__ uint32_t block_max_u(uint32_t v, Scratch& sc) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off, 64));
+  if ((threadIdx.x & 63) == 0) sc.wave_u[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint32_t t = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) t = max(t, sc.wave_u[w]);
+  __syncthreads();
+  return t;
+}
+
+// "a ranks before b": higher key, then lower id.
+__device__ __forceinline__ bool ranks_before(uint32_t ka, int ia, uint32_t kb, int ib) {
+  return ka > kb || (ka == kb && ia < ib);
+}
+
+template <int EPT>
+__global__ __launch_bounds__(kThreads) void select_kernel(
+    const float* __restrict__ scores, int nblk, const int32_t* __restrict__ n_valid,
+    float top_p, int k_max, int k_min, int n_sink, int n_recent, int P,
+    int32_t* __restrict__ idx_out, int32_t* __restrict__ count_out,
+    float* __restrict__ mass_out) {
+  __shared__ Scratch sc;
+  extern __shared__ uint32_t dyn[];  // [P] keys, [P] ids, [P] probs, [nblk/32+1] bitmap
+  uint32_t* s_key = dyn;
+  int* s_id = reinterpret_cast<int*>(dyn + P);
+  float* s_p = reinterpret_cast<float*>(dyn + 2 * P);
+  uint32_t* s_bits = dyn + 3 * P;
+
+  const int row = blockIdx.x;
+  const int tid = threadIdx.x;
+  int nv = n_valid ? n_valid[row] : nblk;
+  nv = nv < 0 ? 0 : (nv > nblk ? nblk : nv);
+
+  // Reserved tier (sink prefix + recency suffix of the valid blocks).
+  const int sink_end = min(n_sink, nv);
+  const int rec_start = max(0, nv - n_recent);
+  const int n_reserved = sink_end + (nv - rec_start) - max(0, sink_end - rec_start);
+  const int n_res = nv - n_reserved;
+  const int cap = min(k_max - n_reserved, n_res);
+
+  const float* srow = scores + (size_t)row * nblk;
+  uint32_t key[EPT];
+  float sv[EPT];
+  bool cand[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int j = tid * EPT + e;
+    cand[e] = j < nv && j >= sink_end && j < rec_start;
+    sv[e] = cand[e] ? srow[j] : -INFINITY;
+    key[e] = cand[e] ? order_key(sv[e]) : 0u;
+  }
+  for (int i = tid; i <= (nblk >> 5); i += kThreads) s_bits[i] = 0u;
+
+  int n = 0;
+  float mass = 0.f;
+  if (cap > 0) {
+    // ---- residual softmax statistics (Eq. select-nucleus) ----
+    uint32_t kmax = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) kmax = max(kmax, key[e]);
+    const float m = order_key_inv(block_max_u(kmax, sc));
+    float pe[EPT];
+    float zpart = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      pe[e] = cand[e] ? expf(sv[e] - m) : 0.f;
+      zpart += pe[e];
+    }
+    const float Z = block_sum_f(zpart, sc);
+
+    // ---- radix select of the cap-th largest key ----
+    uint32_t prefix = 0, pmask = 0;
+    int need = cap;
+    if (cap < n_res) {
+      for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        sc.hist[tid] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+          if (cand[e] && (key[e] & pmask) == prefix)
+            atomicAdd(&sc.hist[(key[e] >> shift) & 255u], 1u);
+        __syncthreads();
+        if (tid < 64) {
+          // lane l holds digits 255-4l .. 252-4l (descending)
+          int c[4], tot = 0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            c[i] = (int)sc.hist[255 - 4 * tid - i];
+            tot += c[i];
+          }
+          int incl = tot;
+#pragma unroll
+          for (int off = 1; off < 64; off <<= 1) {
+            const int o = __shfl_up(incl, off, 64);
+            if (tid >= off) incl += o;
+          }
+          int before = incl - tot;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (before < need && need <= before + c[i]) {
+              sc.digit = 255 - 4 * tid - i;
+              sc.need = need - before;
+            }
+            before += c[i];
+          }
+        }
+        __syncthreads();
+        prefix |= (uint32_t)sc.digit << shift;
+        pmask |= 255u << shift;
+        need = sc.need;
+        __syncthreads();
+      }
+    }
+    const uint32_t thr = prefix;  // cap == n_res: every candidate passes (thr = 0)
+
+    // ---- survivors: key > thr, or key == thr among the first `need` ids ----
+    int n_eq = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) n_eq += (cand[e] && key[e] == thr) ? 1 : 0;
+    int eq_total;
+    int eq_rank = block_excl_scan(n_eq, eq_total, sc);
+    bool sel[EPT];
+    int n_sel = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const bool eq = cand[e] && key[e] == thr;
+      sel[e] = cand[e] && (key[e] > thr || (eq && eq_rank < need));
+      eq_rank += eq ? 1 : 0;
+      n_sel += sel[e] ? 1 : 0;
+    }
+    int sel_total;
+    int pos = block_excl_scan(n_sel, sel_total, sc);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      if (sel[e]) {
+        s_key[pos] = key[e];
+        s_id[pos] = tid * EPT + e;
+        s_p[pos] = pe[e];
+        ++pos;
+      }
+    }
+    for (int i = cap + tid; i < P; i += kThreads) {
+      s_key[i] = 0u;
+      s_id[i] = 0x7fffffff;
+      s_p[i] = 0.f;
+    }
+    __syncthreads();
+
+    // ---- bitonic sort of the P slots by (key desc, id asc) ----
+    for (int kk = 2; kk <= P; kk <<= 1) {
+      for (int jj = kk >> 1; jj > 0; jj >>= 1) {
+        for (int i = tid; i < P; i += kThreads) {
+          const int ixj = i ^ jj;
+          if (ixj > i) {
+            const uint32_t ka = s_key[i], kb = s_key[ixj];
+            const int ia = s_id[i], ib = s_id[ixj];
+            const bool a_first = ranks_before(ka, ia, kb, ib);
+            const bool up = (i & kk) == 0;
+            if (up != a_first) {
+              s_key[i] = kb; s_key[ixj] = ka;
+              s_id[i] = ib; s_id[ixj] = ia;
+              const float pa = s_p[i];
+              s_p[i] = s_p[ixj]; s_p[ixj] = pa;
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
+
+    // ---- prefix mass in sorted order (thread t owns a contiguous run) ----
+    const int per = (P + kThreads - 1) / kThreads;
+    const int r0 = min(tid * per, P), r1 = min(r0 + per, P);
+    float run = 0.f;
+    for (int r = r0; r < r1; ++r) run += s_p[r];
+    float acc = block_excl_scan_f(run, sc);
+    const float pz = top_p * Z;
+    int below = 0;
+    for (int r = r0; r < r1; ++r) {
+      acc += s_p[r];
+      s_p[r] = acc;  // inclusive cumulative mass (unnormalised)
+      below += (r < cap && acc < pz) ? 1 : 0;
+    }
+    const int n_below = block_sum_i(below, sc);  // also orders the s_p writes
+    if (top_p >= 1.f)
+      n = cap;
+    else if (top_p <= 0.f)
+      n = 0;
+    else
+      n = min(cap, n_below + 1);
+    if (n_reserved + n < k_min) n = min(k_min - n_reserved, cap);
+    mass = n > 0 ? s_p[n - 1] / Z : 0.f;
+    for (int r = tid; r < n; r += kThreads) atomicOr(&s_bits[s_id[r] >> 5], 1u << (s_id[r] & 31));
+  }
+  __syncthreads();
+
+  // ---- write S = reserved u nucleus in ascending block id ----
+  bool fin[EPT];
+  int n_fin = 0;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int j = tid * EPT + e;
+    const bool reserved = j < nv && (j < sink_end || j >= rec_start);
+    fin[e] = reserved || (j < nv && ((s_bits[j >> 5] >> (j & 31)) & 1u));
+    n_fin += fin[e] ? 1 : 0;
+  }
+  int total;
+  int pos = block_excl_scan(n_fin, total, sc);
+  int32_t* out = idx_out + (size_t)row * k_max;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e)
+    if (fin[e]) out[pos++] = tid * EPT + e;
+  for (int i = total + tid; i < k_max; i += kThreads) out[i] = -1;
+  if (tid == 0) {
+    count_out[row] = total;
+    if (mass_out) mass_out[row] = mass;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const int32_t* n_valid,
+                                float top_p, int k_max, int k_min, int n_sink, int n_recent,
+                                int32_t* idx, int32_t* count, float* nuc_mass, hipStream_t s) {
+  int P = 1;
+  const int cap = min(k_max, nblk);
+  while (P < cap) P <<= 1;
+  const size_t shm = (size_t)(3 * P + (nblk >> 5) + 1) * 4;
+  const int ept_needed = (nblk + kThreads - 1) / kThreads;
+  dim3 grid(rows), block(kThreads);
+#define SPOT_SELECT_CASE(E)                                                                   \
+  if (ept_needed <= E) {                                                                    \
+    hipLaunchKernelGGL((select_kernel<E>), grid, block, shm, s, scores, nblk, n_valid, top_p, \
+                       k_max, k_min, n_sink, n_recent, P, idx, count, nuc_mass);            \
+    return hipGetLastError();                                                                \
+  }
+  SPOT_SELECT_CASE(1)
+  SPOT_SELECT_CASE(2)
+  SPOT_SELECT_CASE(4)
+  SPOT_SELECT_CASE(8)
+  SPOT_SELECT_CASE(16)
+  SPOT_SELECT_CASE(32)
+  SPOT_SELECT_CASE(64)
+#undef SPOT_SELECT_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace spot

@@ -1,0 +1,296 @@
+"""ctypes binding of libspot (include/spot.h).
+
+The functions ``spot_*`` mirror the C ABI one to one: they take torch tensors
+(device memory), check dtype / device / contiguity / size, and pass raw
+pointers plus the current HIP stream.  Every step of the path runs in the HIP
+kernels of libspot.so; there is no fallback: if the library cannot be loaded
+on a machine with a GPU, the first call raises.
+
+Convenience wrappers without the ``spot_`` prefix allocate outputs with torch.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import sys
+import threading
+from typing import Optional
+
+import torch
+
+from . import build as _build
+
+SPOT_OK = 0
+STATUS = {0: "ok", 1: "null pointer", 2: "invalid shape", 3: "unsupported", 4: "invalid rule",
+          5: "workspace", 6: "HIP launch error"}
+KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2}
+BLK = 64
+
+SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score", "spot_select_blocks",
+           "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
+           "spot_sparse_prefill"]
+
+
+class SpotError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: status {status} ({STATUS.get(status, '?')})")
+        self.status = status
+
+
+_lock = threading.Lock()
+_lib = None
+
+
+def load(path: Optional[str] = None):
+    """Load libspot.so, building it first only if it does not exist."""
+    global _lib
+    with _lock:
+        if _lib is not None and path is None:
+            return _lib
+        so = path or _build.SO
+        if not os.path.exists(so):
+            _build.build()
+        elif path is None and _build.stale():
+            print(f"warning: {so} is older than its sources; rebuild with "
+                  "`python -m paper_2606_22874_amd.build`", file=sys.stderr)
+        L = ctypes.CDLL(so)
+        P, I, F, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+        L.spot_status_str.argtypes = [I]
+        L.spot_status_str.restype = ctypes.c_char_p
+        L.spot_version.restype = ctypes.c_char_p
+        L.spot_selector_score.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P, P]
+        L.spot_select_blocks.argtypes = [P, I, I, P, F, I, I, I, I, P, P, P, P]
+        L.spot_decode_workspace_bytes.argtypes = [I, I, I, I, I]
+        L.spot_decode_workspace_bytes.restype = Z
+        L.spot_sparse_decode.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, P, P, P, Z, P]
+        L.spot_dense_decode.argtypes = [P, P, P, P, I, I, I, I, I, F, P, P, P, Z, P]
+        L.spot_sparse_prefill.argtypes = [P, P, P, I, P, P, I, I, I, I, I, F, P, P, P]
+        for name in ("spot_selector_score", "spot_select_blocks", "spot_sparse_decode",
+                     "spot_dense_decode", "spot_sparse_prefill"):
+            getattr(L, name).restype = ctypes.c_int32
+        if path is None:
+            _lib = L
+        return L
+
+
+# ------------------------------------------------------------- marshalling
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dev(t: torch.Tensor, name: str, dtypes, numel: Optional[int] = None):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise ValueError(f"{name}: dtype {t.dtype} not in {dtypes}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name}: {t.numel()} elements, need {numel}")
+    return t
+
+
+BF16 = (torch.bfloat16, torch.int16)
+I32 = (torch.int32,)
+F32 = (torch.float32,)
+U8 = (torch.uint8,)
+
+
+def _check(fn: str, st: int):
+    if st != SPOT_OK:
+        raise SpotError(fn, st)
+
+
+# ------------------------------------------------------------- C ABI calls
+def spot_selector_score(q_sel, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq, nblk, h_s, d_s,
+                        n_valid, scores, stream=None):
+    rows = n_seq * rows_per_seq
+    f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
+    _dev(q_sel, "q_sel", BF16, rows * h_s * d_s)
+    _dev(w, "w", F32, rows * h_s)
+    if f == 0:
+        _dev(k_sel, "k_sel", BF16, n_seq * nblk * h_s * d_s)
+    else:
+        _dev(k_sel, "k_sel", U8, n_seq * nblk * h_s * d_s // 2)
+        _dev(k_scale, "k_scale", (torch.float16, torch.int16) if f == 1 else U8,
+             n_seq * nblk * h_s * d_s // 32)
+    if n_valid is not None:
+        _dev(n_valid, "n_valid", I32, rows)
+    _dev(scores, "scores", F32, rows * nblk)
+    _check("spot_selector_score", load().spot_selector_score(
+        _ptr(q_sel), _ptr(w), _ptr(k_sel), _ptr(k_scale), f, n_seq, rows_per_seq, nblk, h_s,
+        d_s, _ptr(n_valid), _ptr(scores), _stream(stream)))
+
+
+def spot_select_blocks(scores, rows, nblk, n_valid, top_p, k_max, k_min, n_sink, n_recent, idx,
+                       count, nuc_mass=None, stream=None):
+    _dev(scores, "scores", F32, rows * nblk)
+    if n_valid is not None:
+        _dev(n_valid, "n_valid", I32, rows)
+    _dev(idx, "idx", I32, rows * k_max)
+    _dev(count, "count", I32, rows)
+    if nuc_mass is not None:
+        _dev(nuc_mass, "nuc_mass", F32, rows)
+    _check("spot_select_blocks", load().spot_select_blocks(
+        _ptr(scores), rows, nblk, _ptr(n_valid), float(top_p), k_max, k_min, n_sink, n_recent,
+        _ptr(idx), _ptr(count), _ptr(nuc_mass), _stream(stream)))
+
+
+def spot_decode_workspace_bytes(batch, h_q, h_kv, d, max_blocks) -> int:
+    return int(load().spot_decode_workspace_bytes(batch, h_q, h_kv, d, max_blocks))
+
+
+def spot_sparse_decode(q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, d, l_cap,
+                       sm_scale, out, lse, ws, stream=None):
+    _dev(q, "q", BF16, batch * h_q * d)
+    _dev(k, "k", BF16, batch * h_kv * l_cap * d)
+    _dev(v, "v", BF16, batch * h_kv * l_cap * d)
+    _dev(seq_len, "seq_len", I32, batch)
+    _dev(idx, "idx", I32, batch * k_max)
+    _dev(count, "count", I32, batch)
+    _dev(out, "out", BF16, batch * h_q * d)
+    if lse is not None:
+        _dev(lse, "lse", F32, batch * h_q)
+    _dev(ws, "ws", None)
+    _check("spot_sparse_decode", load().spot_sparse_decode(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(seq_len), _ptr(idx), _ptr(count), k_max, batch, h_q,
+        h_kv, d, l_cap, float(sm_scale), _ptr(out), _ptr(lse), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def spot_dense_decode(q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale, out, lse, ws,
+                      stream=None):
+    _dev(q, "q", BF16, batch * h_q * d)
+    _dev(k, "k", BF16, batch * h_kv * l_cap * d)
+    _dev(v, "v", BF16, batch * h_kv * l_cap * d)
+    _dev(seq_len, "seq_len", I32, batch)
+    _dev(out, "out", BF16, batch * h_q * d)
+    if lse is not None:
+        _dev(lse, "lse", F32, batch * h_q)
+    _dev(ws, "ws", None)
+    _check("spot_dense_decode", load().spot_dense_decode(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(seq_len), batch, h_q, h_kv, d, l_cap, float(sm_scale),
+        _ptr(out), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def spot_sparse_prefill(q, k, v, L, idx, count, k_max, batch, h_q, h_kv, d, sm_scale, out, lse,
+                        stream=None):
+    nqb = L // BLK
+    _dev(q, "q", BF16, batch * h_q * L * d)
+    _dev(k, "k", BF16, batch * h_kv * L * d)
+    _dev(v, "v", BF16, batch * h_kv * L * d)
+    _dev(idx, "idx", I32, batch * nqb * k_max)
+    _dev(count, "count", I32, batch * nqb)
+    _dev(out, "out", BF16, batch * h_q * L * d)
+    if lse is not None:
+        _dev(lse, "lse", F32, batch * h_q * L)
+    _check("spot_sparse_prefill", load().spot_sparse_prefill(
+        _ptr(q), _ptr(k), _ptr(v), L, _ptr(idx), _ptr(count), k_max, batch, h_q, h_kv, d,
+        float(sm_scale), _ptr(out), _ptr(lse), _stream(stream)))
+
+
+# --------------------------------------------------- allocating wrappers
+def selector_score(q_sel, w, k_sel, k_scale=None, kfmt="bf16", rows_per_seq=1, n_valid=None,
+                   nblk=None, out=None, stream=None):
+    """Block scores [rows, nblk] float32 for q_sel [rows, h_s, d_s]."""
+    h_s, d_s = q_sel.shape[-2], q_sel.shape[-1]
+    rows = q_sel.numel() // (h_s * d_s)
+    n_seq = rows // rows_per_seq
+    if nblk is None:
+        per = h_s * d_s if KFMT.get(kfmt, kfmt) == 0 else h_s * d_s // 2
+        nblk = k_sel.numel() // (n_seq * per)
+    if out is None:
+        out = torch.empty((rows, nblk), dtype=torch.float32, device=q_sel.device)
+    spot_selector_score(q_sel, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq, nblk, h_s, d_s,
+                        n_valid, out, stream)
+    return out
+
+
+def select_blocks(scores, rule, n_valid=None, idx=None, count=None, nuc_mass=None, stream=None):
+    rows, nblk = scores.shape
+    dev = scores.device
+    if idx is None:
+        idx = torch.empty((rows, rule.k_max), dtype=torch.int32, device=dev)
+    if count is None:
+        count = torch.empty(rows, dtype=torch.int32, device=dev)
+    if nuc_mass is None:
+        nuc_mass = torch.empty(rows, dtype=torch.float32, device=dev)
+    spot_select_blocks(scores, rows, nblk, n_valid, rule.top_p, rule.k_max, rule.k_min,
+                       rule.n_sink, rule.n_recent, idx, count, nuc_mass, stream)
+    return idx, count, nuc_mass
+
+
+def decode_workspace(batch, h_q, h_kv, d, max_blocks, device="cuda"):
+    n = spot_decode_workspace_bytes(batch, h_q, h_kv, d, max_blocks)
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=device)
+
+
+def sparse_decode(q, k, v, seq_len, idx, count, sm_scale=None, out=None, lse=None, ws=None,
+                  stream=None):
+    batch, h_q, d = q.shape
+    _, h_kv, l_cap, _ = k.shape
+    k_max = idx.shape[-1]
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    if out is None:
+        out = torch.empty((batch, h_q, d), dtype=torch.bfloat16, device=q.device)
+    if lse is None:
+        lse = torch.empty((batch, h_q), dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = decode_workspace(batch, h_q, h_kv, d, k_max, q.device)
+    spot_sparse_decode(q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, d, l_cap,
+                       sm_scale, out, lse, ws, stream)
+    return out, lse
+
+
+def dense_decode(q, k, v, seq_len, sm_scale=None, out=None, lse=None, ws=None, stream=None):
+    batch, h_q, d = q.shape
+    _, h_kv, l_cap, _ = k.shape
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    if out is None:
+        out = torch.empty((batch, h_q, d), dtype=torch.bfloat16, device=q.device)
+    if lse is None:
+        lse = torch.empty((batch, h_q), dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = decode_workspace(batch, h_q, h_kv, d, l_cap // BLK, q.device)
+    spot_dense_decode(q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale, out, lse, ws,
+                      stream)
+    return out, lse
+
+
+def sparse_prefill(q, k, v, idx, count, sm_scale=None, out=None, lse=None, stream=None):
+    batch, h_q, L, d = q.shape
+    h_kv = k.shape[1]
+    k_max = idx.shape[-1]
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    if out is None:
+        out = torch.empty_like(q, dtype=torch.bfloat16)
+    if lse is None:
+        lse = torch.empty((batch, h_q, L), dtype=torch.float32, device=q.device)
+    spot_sparse_prefill(q, k, v, L, idx, count, k_max, batch, h_q, h_kv, d, sm_scale, out, lse,
+                        stream)
+    return out, lse
+
+
+# ------------------------------------------------------- host helpers
+def to_device_bf16(a, device="cuda") -> torch.Tensor:
+    """uint16 BF16 bit patterns (numpy) -> torch.bfloat16 device tensor."""
+    import numpy as np
+    t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16))
+    return t.to(device).view(torch.bfloat16)
+
+
+def bf16_to_float_host(t: torch.Tensor):
+    return t.detach().float().cpu().numpy()

@@ -1,0 +1,91 @@
+"""The C-ABI library builds, loads and exports every declared entry point.
+
+No kernel is launched here: the calls below fail argument validation, which
+the library performs before touching the HIP runtime.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2606_22874_amd import build, spot
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = []
+    for fn in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names += re.findall(r"\b(spot_\w+)\s*\(", text)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(build.SO):
+        build.build()
+    return spot.load()
+
+
+def test_header_declares_the_five_calls():
+    names = declared_functions()
+    for n in ("spot_selector_score", "spot_select_blocks", "spot_sparse_decode",
+              "spot_sparse_prefill", "spot_dense_decode"):
+        assert n in names
+
+
+def test_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", build.SO], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (\w+)$", out, flags=re.M))
+    for n in declared_functions():
+        assert n in exported, n
+        assert hasattr(lib, n)
+    assert set(spot.SYMBOLS) == set(declared_functions())
+
+
+def test_version_and_status_strings(lib):
+    assert b"gfx950" in lib.spot_version()
+    for s in range(7):
+        assert lib.spot_status_str(s)
+
+
+def test_validation_errors_before_launch(lib):
+    P = ctypes.c_void_p
+    nz = P(16)  # never dereferenced: each call below fails validation first
+    # NULL pointers
+    assert lib.spot_selector_score(None, nz, nz, None, 0, 1, 1, 4, 8, 64, None, nz, None) == 1
+    # h_s * d_s != 512 is unsupported
+    assert lib.spot_selector_score(nz, nz, nz, None, 0, 1, 1, 4, 8, 32, None, nz, None) == 3
+    # quantized format without scales
+    assert lib.spot_selector_score(nz, nz, nz, None, 1, 1, 1, 4, 8, 64, None, nz, None) == 1
+    # rules: NaN p, k_min > k_max, k_max < n_sink + n_recent, k_max < 1
+    sel = lib.spot_select_blocks
+    assert sel(nz, 1, 8, None, float("nan"), 4, 0, 1, 2, nz, nz, None, None) == 4
+    assert sel(nz, 1, 8, None, 0.9, 4, 5, 1, 2, nz, nz, None, None) == 4
+    assert sel(nz, 1, 8, None, 0.9, 2, 0, 1, 2, nz, nz, None, None) == 4
+    assert sel(nz, 1, 8, None, 0.9, 0, 0, 0, 0, nz, nz, None, None) == 4
+    assert sel(nz, 1, 20000, None, 0.9, 4, 0, 1, 2, nz, nz, None, None) == 3
+    # decode: d != 128, bad GQA group, l_cap not a multiple of 64, no workspace
+    dec = lib.spot_sparse_decode
+    assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 32, 8, 64, 4096, 0.1, nz, None, nz, 1 << 20, None) == 3
+    assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 24, 8, 128, 4096, 0.1, nz, None, nz, 1 << 20, None) == 3
+    assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 32, 8, 128, 4000, 0.1, nz, None, nz, 1 << 20, None) == 2
+    assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 32, 8, 128, 4096, 0.1, nz, None, nz, 0, None) == 5
+    assert dec(nz, nz, nz, nz, None, nz, 4, 1, 32, 8, 128, 4096, 0.1, nz, None, nz, 1 << 20, None) == 1
+    den = lib.spot_dense_decode
+    assert den(nz, nz, nz, nz, 1, 32, 8, 128, 4096, 0.1, nz, None, nz, 16, None) == 5
+    pre = lib.spot_sparse_prefill
+    assert pre(nz, nz, nz, 100, nz, nz, 4, 1, 64, 8, 128, 0.1, nz, None, None) == 2
+    assert pre(nz, nz, nz, 128, nz, nz, 4, 1, 64, 8, 96, 0.1, nz, None, None) == 3
+
+
+def test_workspace_size_query(lib):
+    n = lib.spot_decode_workspace_bytes(4, 32, 8, 128, 128)
+    assert n > 0 and n % 4 == 0
+    assert lib.spot_decode_workspace_bytes(0, 32, 8, 128, 128) == 0
