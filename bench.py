@@ -110,18 +110,35 @@ def main():
     ws = spot.decode_workspace(B, Hq, Hkv, d, rule.k_max, dev)
     stream = torch.cuda.current_stream()
 
-    def step(c, ev=None):
-        k, v, ks, sc = copies[c % len(copies)]
+    def score(c):
+        _, _, ks, sc = copies[c % len(copies)]
         spot.spot_selector_score(q_sel, w, ks, sc, args.fmt, B, 1, nblk, wl.Hs, wl.ds, n_valid,
                                  scores, stream)
+
+    def select(c):
         spot.spot_select_blocks(scores, B, nblk, n_valid, rule.top_p, rule.k_max, rule.k_min,
                                 rule.n_sink, rule.n_recent, idx, cnt, mass, stream)
-        if ev is not None:
-            ev[0].record(stream)
+
+    def attend(c):
+        k, v, _, _ = copies[c % len(copies)]
         spot.spot_sparse_decode(q, k, v, seq_len, idx, cnt, rule.k_max, B, Hq, Hkv, d, L,
                                 wl.sm_scale, out, lse, ws, stream)
-        if ev is not None:
-            ev[1].record(stream)
+
+    def step(c):
+        score(c)
+        select(c)
+        attend(c)
+
+    def timed(fn, n):
+        """Average time of n back-to-back calls, HIP events on the launch stream."""
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for i in range(n):
+            fn(i)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
 
     log(f"[bench] warmup {args.warmup} steps")
     for i in range(args.warmup):
@@ -129,24 +146,26 @@ def main():
     torch.cuda.synchronize()
     counts = cnt.cpu().numpy()
 
-    # Timed region: K steps, events around the attention call of every step.
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     log(f"[bench] timing {args.steps} steps")
-    torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(args.steps):
-        step(i, evs[i])
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
-    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
-    log(f"[bench] {ms * 1e3:.1f} us/step, attention call {attn_ms * 1e3:.1f} us")
+    ms = timed(step, args.steps)
+    # Per-stage averages (same launch stream, back to back, rotating copies).
+    attn_ms = timed(attend, args.steps)
+    score_ms = timed(score, args.steps)
+    select_ms = timed(select, args.steps)
+    log(f"[bench] {ms * 1e3:.1f} us/step; score {score_ms * 1e3:.1f} us, select "
+        f"{select_ms * 1e3:.1f} us, attention {attn_ms * 1e3:.1f} us")
 
-    kv_block_bytes = kBlkBytes = 64 * Hkv * d * 2 * 2          # K and V of one block
+    # Practical read ceiling: the same byte count streamed by a plain kernel.
+    kv_block_bytes = 64 * Hkv * d * 2 * 2          # K and V of one 64-token block
     attn_bytes = int(counts.sum()) * kv_block_bytes
     step_bytes = sel_bytes + attn_bytes
+    sink = torch.empty(spot.load().spot_probe_sink_words(), dtype=torch.float32, device=dev)
+    n_el = step_bytes // 2
+    bufs = [copies[c][0].view(-1)[:n_el] for c in range(len(copies))]
+    stream_ms = timed(lambda i: spot.spot_probe_stream_read(bufs[i % len(bufs)], sink, stream),
+                      args.steps)
+    stream_gbs = step_bytes / (stream_ms * 1e-3) / 1e9
+
     steps_per_s = 1e3 / ms
     step_gbs = step_bytes / (ms * 1e-3) / 1e9
     attn_gbs = attn_bytes / (attn_ms * 1e-3) / 1e9
@@ -173,10 +192,13 @@ def main():
             "bytes_per_step": step_bytes,
             "step_hbm_gbs": round(step_gbs, 1),
             "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
+            "stage_us": {"score": round(score_ms * 1e3, 2), "select": round(select_ms * 1e3, 2),
+                         "attention": round(attn_ms * 1e3, 2)},
+            "stream_read_ceiling_gbs": round(stream_gbs, 1),
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "spot_sparse_decode (split + merge)",
+            "kernel": "decode_split_kernel (spot_sparse_decode)",
             "achieved": round(attn_gbs, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
@@ -189,20 +211,15 @@ def main():
 
     if args.dense:
         wsd = spot.decode_workspace(B, Hq, Hkv, d, nblk, dev)
+
+        def dense(i):
+            k, v, _, _ = copies[i % len(copies)]
+            spot.spot_dense_decode(q, k, v, seq_len, B, Hq, Hkv, d, L, wl.sm_scale, out, lse,
+                                   wsd, stream)
+
         for i in range(3):
-            k, v, _, _ = copies[i % len(copies)]
-            spot.spot_dense_decode(q, k, v, seq_len, B, Hq, Hkv, d, L, wl.sm_scale, out, lse, wsd,
-                                   stream)
-        torch.cuda.synchronize()
-        n_d = 20
-        start.record(stream)
-        for i in range(n_d):
-            k, v, _, _ = copies[i % len(copies)]
-            spot.spot_dense_decode(q, k, v, seq_len, B, Hq, Hkv, d, L, wl.sm_scale, out, lse, wsd,
-                                   stream)
-        end.record(stream)
-        torch.cuda.synchronize()
-        dms = start.elapsed_time(end) / n_d
+            dense(i)
+        dms = timed(dense, 20)
         dbytes = B * Hkv * L * d * 2 * 2
         result["dense_baseline"] = {
             "value": round(1e3 / dms, 1), "unit": "steps/s", "ms_per_step": round(dms, 4),

@@ -10,8 +10,9 @@
  *
  * Conventions shared by every entry point:
  *  - Pointers named as device arrays are caller-owned device memory; the
- *    library never allocates, frees, or synchronises, and keeps no state
- *    between calls.  Arrays are C-contiguous.  BF16 arrays hold bfloat16
+ *    library never allocates, frees, or synchronises, and keeps no state of
+ *    its own between calls (the decode workspace carries completion counters
+ *    that each call returns to zero).  Arrays are C-contiguous.  BF16 arrays hold bfloat16
  *    values (2 bytes each).  A KV block is 64 consecutive tokens; the
  *    selector key cache holds one pooled key per block.
  *  - `stream` is a hipStream_t (NULL = the default stream).  Every call only
@@ -120,7 +121,9 @@ spot_status spot_select_blocks(const float *scores, int rows, int nblk, const in
 
 /*
  * Workspace bytes that spot_sparse_decode (max_blocks = k_max) and
- * spot_dense_decode (max_blocks = ceil(l_cap / 64)) need for these sizes.
+ * spot_dense_decode (max_blocks = l_cap / 64) need for these sizes: split
+ * partials (float) followed by one completion counter per (sequence, KV
+ * head).  Returns 0 for non-positive sizes.
  */
 size_t spot_decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_blocks);
 
@@ -144,7 +147,10 @@ size_t spot_decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_
  *  out      device BF16 [batch, h_q, d] (output, round to nearest even)
  *  lse      device float [batch, h_q] (output, may be NULL)
  *  ws       device workspace of at least
- *           spot_decode_workspace_bytes(batch, h_q, h_kv, d, k_max) bytes
+ *           spot_decode_workspace_bytes(batch, h_q, h_kv, d, k_max) bytes.
+ *           It must be zero-filled before its first use; every call leaves
+ *           it ready for the next one (its completion counters return to
+ *           zero).  Calls that may overlap in time need separate workspaces.
  *
  * Supported: d == 128, h_q / h_kv in {1, 2, 4, 8}.
  */
@@ -190,6 +196,18 @@ spot_status spot_sparse_prefill(const void *q, const void *k, const void *v, int
                                 const int32_t *idx, const int32_t *count, int k_max, int batch,
                                 int h_q, int h_kv, int d, float sm_scale, void *out, float *lse,
                                 void *stream);
+
+/*
+ * spot_probe_stream_read -- measurement helper, not part of the attention
+ * path: reads `bytes` bytes of device memory at `buf` once with 16-byte
+ * coalesced loads (the access pattern of the decode kernels) and writes one
+ * checksum word per workgroup to `sink` (device, at least
+ * spot_probe_sink_words() floats) so the loads cannot be elided.  Used to
+ * measure the practical HBM read ceiling.  `buf` must be 16-byte aligned and
+ * `bytes` a multiple of 16.
+ */
+spot_status spot_probe_stream_read(const void *buf, size_t bytes, float *sink, void *stream);
+int spot_probe_sink_words(void);
 
 #ifdef __cplusplus
 }

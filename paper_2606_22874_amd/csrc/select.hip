@@ -1,8 +1,9 @@
 // Dual top-p / top-K block selection (paper Section 2.3, Eqs. select-topk,
 // select-nucleus and select-topp) with a cap k_max on the set size.
 //
-// One workgroup (256 threads) per row.  Thread t owns the EPT consecutive
-// block ids [t*EPT, (t+1)*EPT) in registers.  Per row:
+// Rows of up to 4096 blocks use the single-wavefront kernel further down.
+// Larger rows use one workgroup (256 threads) per row; thread t owns the EPT
+// consecutive block ids [t*EPT, (t+1)*EPT) in registers.  Per row:
 //  1. reserved blocks (sink prefix, recency suffix) are set aside; the
 //     residual candidates get an order-preserving 32-bit key of their score;
 //  2. residual softmax statistics: max and Z = sum exp(s - max) with a fixed
@@ -235,7 +236,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
     int pos = block_excl_scan(n_sel, sel_total, sc);
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
-      if (sel[e]) {
+      if (sel[e] && pos < P) {
         s_key[pos] = key[e];
         s_id[pos] = tid * EPT + e;
         s_p[pos] = pe[e];
@@ -312,10 +313,260 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
   int32_t* out = idx_out + (size_t)row * k_max;
 #pragma unroll
   for (int e = 0; e < EPT; ++e)
-    if (fin[e]) out[pos++] = tid * EPT + e;
+    if (fin[e] && pos < k_max) out[pos++] = tid * EPT + e;
   for (int i = total + tid; i < k_max; i += kThreads) out[i] = -1;
   if (tid == 0) {
-    count_out[row] = total;
+    count_out[row] = min(total, k_max);
+    if (mass_out) mass_out[row] = mass;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// One wavefront per row (rows of up to 4096 blocks).  Lane l owns the EPT
+// consecutive block ids [l*EPT, (l+1)*EPT).  No workgroup barriers and no sort:
+//  1. candidates' order keys, residual max m and Z = sum exp(s - m);
+//  2. if the cap C = min(k_max - |R|, |B_res|) binds, a radix select by count
+//     (8-bit digits, LDS histogram, starting at the highest bit where the
+//     candidate keys differ) finds the C-th largest key; equal keys at the
+//     threshold are taken in ascending block id.  These C survivors are the
+//     only blocks the rule can pick;
+//  3. the survivors are compacted (id order) and the nucleus length is found
+//     by bisection on the key: the largest threshold T whose mass
+//     sum_{key >= T} exp(s - m) still reaches top_p * Z, plus as many blocks
+//     tied at T (lowest ids first) as are needed to reach it;
+//  4. the k_min floor and the cap give the final n; the top-n survivors (by
+//     count bisection, ties by id) plus the reserved blocks are written in
+//     ascending block id.
+template <int EPT>
+__global__ __launch_bounds__(64) void select_wave_kernel(
+    const float* __restrict__ scores, int nblk, const int32_t* __restrict__ n_valid,
+    float top_p, int k_max, int k_min, int n_sink, int n_recent, int P,
+    int32_t* __restrict__ idx_out, int32_t* __restrict__ count_out,
+    float* __restrict__ mass_out) {
+  constexpr int kMaxBlocks = 64 * EPT;
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t bits[kMaxBlocks / 32];
+  extern __shared__ uint32_t dyn[];  // staging [kMaxBlocks] | surv key [P] | id [P] | e [P]
+  float* stage = reinterpret_cast<float*>(dyn);
+  uint32_t* s_key = dyn + kMaxBlocks;
+  int* s_id = reinterpret_cast<int*>(s_key + P);
+  float* s_e = reinterpret_cast<float*>(s_id + P);
+
+  const int row = blockIdx.x;
+  const int lane = threadIdx.x;
+  int nv = n_valid ? n_valid[row] : nblk;
+  nv = nv < 0 ? 0 : (nv > nblk ? nblk : nv);
+  const int sink_end = min(n_sink, nv);
+  const int rec_start = max(0, nv - n_recent);
+  const int n_reserved = sink_end + (nv - rec_start) - max(0, sink_end - rec_start);
+  const int n_res = nv - n_reserved;
+  const int cap = min(k_max - n_reserved, n_res);
+
+  // Coalesced load into LDS, then each lane takes its consecutive run.
+  const float* srow = scores + (size_t)row * nblk;
+  for (int j = lane; j < nv; j += 64) stage[j] = srow[j];
+  for (int i = lane; i < kMaxBlocks / 32; i += 64) bits[i] = 0u;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+  uint32_t key[EPT];
+  float sv[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int j = lane * EPT + e;
+    const bool c = j < nv && j >= sink_end && j < rec_start;
+    sv[e] = c ? stage[j] : -INFINITY;
+    key[e] = c ? order_key(sv[e]) : 0u;  // 0 marks "not a candidate"
+  }
+
+  int n = 0;
+  float mass = 0.f;
+  if (cap > 0) {
+    uint32_t kmax = 0u, kmin = 0xffffffffu;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      kmax = max(kmax, key[e]);
+      if (key[e]) kmin = min(kmin, key[e]);
+    }
+    kmax = wave_max_u(kmax);
+    kmin = wave_min_u(kmin);
+    const float m = order_key_inv(kmax);
+    float pe[EPT];
+    float zl = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      pe[e] = key[e] ? exp2f((sv[e] - m) * 1.4426950408889634f) : 0.f;
+      zl += pe[e];
+    }
+    const float Z = wave_sum(zl);
+
+    // ---- 2. radix select by count: the cap-th largest key ----
+    uint32_t thr = 0u;  // cap == n_res: every candidate survives (keys > 0)
+    int need = cap;
+    if (cap < n_res) {
+      const uint32_t diff = kmin ^ kmax;
+      int shift = diff ? 32 - __builtin_clz(diff) : 0;   // bits still to resolve
+      uint32_t prefix = shift >= 32 ? 0u : (kmax >> shift) << shift;
+      uint32_t pmask = shift >= 32 ? 0u : ~0u << shift;
+      while (shift > 0) {
+        const int width = shift < 8 ? shift : 8;
+        shift -= width;
+        const uint32_t dmask = (1u << width) - 1u;
+        for (int i = lane; i < 256; i += 64) hist[i] = 0u;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+          if (key[e] && (key[e] & pmask) == prefix) atomicAdd(&hist[(key[e] >> shift) & dmask], 1u);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // lane l holds digits 255-4l .. 252-4l (descending)
+        int c[4], tot = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          c[i] = (int)hist[255 - 4 * lane - i];
+          tot += c[i];
+        }
+        const int incl = wave_incl_scan_i(tot);
+        int before = incl - tot, digit = -1, left = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (before < need && need <= before + c[i]) {
+            digit = 255 - 4 * lane - i;
+            left = need - before;
+          }
+          before += c[i];
+        }
+        const unsigned long long who = __ballot(digit >= 0);
+        const int src = __ffsll((long long)who) - 1;
+        digit = __builtin_amdgcn_readlane(digit, src);
+        need = __builtin_amdgcn_readlane(left, src);
+        prefix |= (uint32_t)digit << shift;
+        pmask |= dmask << shift;
+      }
+      thr = prefix;
+    }
+
+    // survivors in id order: key > thr, or key == thr among the first `need`
+    int n_eq = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) n_eq += (key[e] && key[e] == thr) ? 1 : 0;
+    int eq_rank = wave_incl_scan_i(n_eq) - n_eq;
+    bool surv[EPT];
+    int n_sv = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const bool eq = key[e] && key[e] == thr;
+      surv[e] = key[e] && (key[e] > thr || (eq && eq_rank < need));
+      eq_rank += eq ? 1 : 0;
+      n_sv += surv[e] ? 1 : 0;
+    }
+    int pos = wave_incl_scan_i(n_sv) - n_sv;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      if (surv[e] && pos < P) {
+        s_key[pos] = key[e];
+        s_id[pos] = lane * EPT + e;
+        s_e[pos] = pe[e];
+        ++pos;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // ---- 3. work on the cap survivors, SP consecutive ones per lane ----
+    const int SP = (cap + 63) / 64;
+    const int i0 = min(lane * SP, cap), i1 = min(i0 + SP, cap);
+    auto mass_ge = [&](uint32_t T) {
+      float part = 0.f;
+      for (int i = i0; i < i1; ++i) part += s_key[i] >= T ? s_e[i] : 0.f;
+      return wave_sum(part);
+    };
+    auto count_ge = [&](uint32_t T) {
+      int part = 0;
+      for (int i = i0; i < i1; ++i) part += s_key[i] >= T ? 1 : 0;
+      return wave_sum_i(part);
+    };
+    // Largest T with f(T) >= target, for f non-increasing in T (bisection).
+    const float pz = top_p * Z;
+    int n_target;
+    if (top_p >= 1.f) {
+      n_target = cap;
+    } else if (top_p <= 0.f) {
+      n_target = 0;
+    } else if (mass_ge(0u) < pz) {
+      n_target = cap;  // the nucleus would need more than the cap allows
+    } else {
+      uint32_t T = 0u;
+      for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t Tc = T | (1u << bit);
+        if (mass_ge(Tc) >= pz) T = Tc;
+      }
+      const float mass_gt = T == 0xffffffffu ? 0.f : mass_ge(T + 1u);
+      const int n_gt = T == 0xffffffffu ? 0 : count_ge(T + 1u);
+      const int n_eqT = count_ge(T) - n_gt;
+      float eT = 0.f;
+      for (int i = i0; i < i1; ++i) eT = s_key[i] == T ? s_e[i] : eT;
+      eT = wave_max(eT);
+      int t = 1;
+      while (t < n_eqT && mass_gt + (float)t * eT < pz) ++t;
+      n_target = n_gt + t;
+    }
+    n = min(n_target, cap);
+    if (n_reserved + n < k_min) n = min(k_min - n_reserved, cap);
+
+    // ---- 4. the top-n survivors (count bisection, ties by lowest id) ----
+    uint32_t T2 = 0u;
+    int need2 = n;
+    if (n < cap) {
+      for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t Tc = T2 | (1u << bit);
+        if (count_ge(Tc) >= n) T2 = Tc;
+      }
+      need2 = n - (T2 == 0xffffffffu ? 0 : count_ge(T2 + 1u));
+    }
+    int q_eq = 0;
+    for (int i = i0; i < i1; ++i) q_eq += s_key[i] == T2 ? 1 : 0;
+    int r = wave_incl_scan_i(q_eq) - q_eq;
+    float ml = 0.f;
+    for (int i = i0; i < i1; ++i) {
+      const bool eq = s_key[i] == T2;
+      const bool take = n > 0 && (s_key[i] > T2 || (eq && r < need2));
+      r += eq ? 1 : 0;
+      if (take) {
+        atomicOr(&bits[s_id[i] >> 5], 1u << (s_id[i] & 31));
+        ml += s_e[i];
+      }
+    }
+    mass = n > 0 ? wave_sum(ml) / Z : 0.f;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+
+  // ---- write S = reserved u chosen, ascending ----
+  bool fin[EPT];
+  int n_fin = 0;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int j = lane * EPT + e;
+    const bool reserved = j < nv && (j < sink_end || j >= rec_start);
+    fin[e] = reserved || (j < nv && ((bits[j >> 5] >> (j & 31)) & 1u));
+    n_fin += fin[e] ? 1 : 0;
+  }
+  const int incl = wave_incl_scan_i(n_fin);
+  const int total = __builtin_amdgcn_readlane(incl, 63);
+  int pos = incl - n_fin;
+  int32_t* out = idx_out + (size_t)row * k_max;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e)
+    if (fin[e] && pos < k_max) out[pos++] = lane * EPT + e;
+  for (int i = total + lane; i < k_max; i += 64) out[i] = -1;
+  if (lane == 0) {
+    count_out[row] = min(total, k_max);
     if (mass_out) mass_out[row] = mass;
   }
 }
@@ -328,9 +579,30 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
   int P = 1;
   const int cap = min(k_max, nblk);
   while (P < cap) P <<= 1;
+  dim3 grid(rows);
+  const int ept = nblk <= 64 ? 1 : nblk <= 128 ? 2 : nblk <= 256 ? 4 : nblk <= 512 ? 8
+                : nblk <= 1024 ? 16 : nblk <= 2048 ? 32 : 64;
+  const size_t shm_w = (size_t)(64 * ept + 3 * P) * 4;
+  if (nblk <= 4096 && shm_w <= 56 * 1024) {
+#define SPOT_SELECT_WAVE(E)                                                                     \
+    if (ept == E) {                                                                           \
+      hipLaunchKernelGGL((select_wave_kernel<E>), grid, dim3(64), shm_w, s, scores, nblk,     \
+                         n_valid, top_p, k_max, k_min, n_sink, n_recent, P, idx, count,       \
+                         nuc_mass);                                                           \
+      return hipGetLastError();                                                                \
+    }
+    SPOT_SELECT_WAVE(1)
+    SPOT_SELECT_WAVE(2)
+    SPOT_SELECT_WAVE(4)
+    SPOT_SELECT_WAVE(8)
+    SPOT_SELECT_WAVE(16)
+    SPOT_SELECT_WAVE(32)
+    SPOT_SELECT_WAVE(64)
+#undef SPOT_SELECT_WAVE
+  }
   const size_t shm = (size_t)(3 * P + (nblk >> 5) + 1) * 4;
   const int ept_needed = (nblk + kThreads - 1) / kThreads;
-  dim3 grid(rows), block(kThreads);
+  dim3 block(kThreads);
 #define SPOT_SELECT_CASE(E)                                                                   \
   if (ept_needed <= E) {                                                                    \
     hipLaunchKernelGGL((select_kernel<E>), grid, block, shm, s, scores, nblk, n_valid, top_p, \

@@ -29,7 +29,7 @@ BLK = 64
 
 SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score", "spot_select_blocks",
            "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
-           "spot_sparse_prefill"]
+           "spot_sparse_prefill", "spot_probe_stream_read", "spot_probe_sink_words"]
 
 
 class SpotError(RuntimeError):
@@ -66,6 +66,9 @@ def load(path: Optional[str] = None):
         L.spot_sparse_decode.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, P, P, P, Z, P]
         L.spot_dense_decode.argtypes = [P, P, P, P, I, I, I, I, I, F, P, P, P, Z, P]
         L.spot_sparse_prefill.argtypes = [P, P, P, I, P, P, I, I, I, I, I, F, P, P, P]
+        L.spot_probe_stream_read.argtypes = [P, Z, P, P]
+        L.spot_probe_stream_read.restype = ctypes.c_int32
+        L.spot_probe_sink_words.restype = I
         for name in ("spot_selector_score", "spot_select_blocks", "spot_sparse_decode",
                      "spot_dense_decode", "spot_sparse_prefill"):
             getattr(L, name).restype = ctypes.c_int32
@@ -202,6 +205,13 @@ def spot_sparse_prefill(q, k, v, L, idx, count, k_max, batch, h_q, h_kv, d, sm_s
         float(sm_scale), _ptr(out), _ptr(lse), _stream(stream)))
 
 
+def spot_probe_stream_read(buf, sink, stream=None):
+    _dev(buf, "buf", None)
+    _dev(sink, "sink", F32, int(load().spot_probe_sink_words()))
+    _check("spot_probe_stream_read", load().spot_probe_stream_read(
+        _ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)))
+
+
 # --------------------------------------------------- allocating wrappers
 def selector_score(q_sel, w, k_sel, k_scale=None, kfmt="bf16", rows_per_seq=1, n_valid=None,
                    nblk=None, out=None, stream=None):
@@ -234,8 +244,9 @@ def select_blocks(scores, rule, n_valid=None, idx=None, count=None, nuc_mass=Non
 
 
 def decode_workspace(batch, h_q, h_kv, d, max_blocks, device="cuda"):
+    """Zero-filled decode workspace (the library keeps it zeroed between calls)."""
     n = spot_decode_workspace_bytes(batch, h_q, h_kv, d, max_blocks)
-    return torch.empty(max(n, 16), dtype=torch.uint8, device=device)
+    return torch.zeros(max(n, 16), dtype=torch.uint8, device=device)
 
 
 def sparse_decode(q, k, v, seq_len, idx, count, sm_scale=None, out=None, lse=None, ws=None,
