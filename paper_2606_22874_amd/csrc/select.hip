@@ -322,35 +322,109 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// One wavefront per row (rows of up to 4096 blocks).  Lane l owns the EPT
-// consecutive block ids [l*EPT, (l+1)*EPT).  No workgroup barriers and no sort:
-//  1. candidates' order keys, residual max m and Z = sum exp(s - m);
+// Single-wavefront selection (rows of up to 4096 blocks, cap up to 512).
+// Lane l owns the EPT consecutive block ids [l*EPT, (l+1)*EPT).  No workgroup
+// barriers:
+//  1. scores are loaded with coalesced loads (all issued before any use) and
+//     transposed through LDS; candidates get order-preserving keys; residual
+//     max m and Z = sum exp(s - m) with a fixed reduction tree;
 //  2. if the cap C = min(k_max - |R|, |B_res|) binds, a radix select by count
 //     (8-bit digits, LDS histogram, starting at the highest bit where the
 //     candidate keys differ) finds the C-th largest key; equal keys at the
-//     threshold are taken in ascending block id.  These C survivors are the
-//     only blocks the rule can pick;
-//  3. the survivors are compacted (id order) and the nucleus length is found
-//     by bisection on the key: the largest threshold T whose mass
-//     sum_{key >= T} exp(s - m) still reaches top_p * Z, plus as many blocks
-//     tied at T (lowest ids first) as are needed to reach it;
-//  4. the k_min floor and the cap give the final n; the top-n survivors (by
-//     count bisection, ties by id) plus the reserved blocks are written in
-//     ascending block id.
-template <int EPT>
+//     threshold go to the lowest block ids.  These C survivors are the only
+//     blocks the rule can pick;
+//  3. the survivors are bitonic-sorted in registers by (score desc, id asc),
+//     packed as 64-bit keys, SPL = P / 64 slots per lane, lane exchanges via
+//     DPP / swizzle / bpermute;
+//  4. their probabilities are prefix-summed in that order; the nucleus is the
+//     first prefix reaching top_p * Z, then capped and floored by k_min; the
+//     chosen ids plus the reserved blocks are written in ascending order.
+
+// Value of lane (lane ^ m); m is a power of two and a compile-time constant
+// after unrolling.  Needs the full wave active.
+__device__ __forceinline__ uint32_t xor_lane(uint32_t x, int m) {
+  switch (m) {
+    case 1: return (uint32_t)dpp_i<kDppQuadXor1>((int)x);
+    case 2: return (uint32_t)dpp_i<kDppQuadXor2>((int)x);
+    case 4: {
+      const uint32_t up = (uint32_t)dpp_i<0x104>((int)x);  // row_shl:4, lane i <- i + 4
+      const uint32_t dn = (uint32_t)dpp_i<0x114>((int)x);  // row_shr:4, lane i <- i - 4
+      return (__lane_id() & 4) ? dn : up;
+    }
+    case 8: return (uint32_t)dpp_i<0x128>((int)x);          // row_ror:8 == xor 8
+    case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x401F);  // xor 16
+    default: return (uint32_t)__builtin_amdgcn_ds_bpermute((__lane_id() ^ 32) << 2, (int)x);
+  }
+}
+__device__ __forceinline__ uint64_t xor_lane64(uint64_t x, int m) {
+  const uint32_t lo = xor_lane((uint32_t)x, m), hi = xor_lane((uint32_t)(x >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive float prefix sum over lanes (same tree as wave_incl_scan_i).
+__device__ __forceinline__ float wave_incl_scan_f(float x) {
+  const int lane = __lane_id();
+  x += dpp_f<0x111>(x);
+  x += dpp_f<0x112>(x);
+  x += dpp_f<0x114>(x);
+  x += dpp_f<0x118>(x);
+  const float r0 = readlane_f(x, 15), r1 = readlane_f(x, 31), r2 = readlane_f(x, 47);
+  const int row = lane >> 4;
+  if (row > 0) x += r0;
+  if (row > 1) x += r1;
+  if (row > 2) x += r2;
+  return x;
+}
+
+// Descending bitonic sort of 64 * SPL packed keys; slot i = lane * SPL + t.
+template <int SPL>
+__device__ __forceinline__ void bitonic_desc(uint64_t (&K)[SPL]) {
+  constexpr int P = 64 * SPL;
+  const int lane = __lane_id();
+#pragma unroll
+  for (int k = 2; k <= P; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (j < SPL) {
+#pragma unroll
+        for (int t = 0; t < SPL; ++t) {
+          const int u = t ^ j;
+          if (u > t) {
+            const bool up = (((lane * SPL + t) & k) == 0);
+            const uint64_t a = K[t], b = K[u];
+            const bool swap = up ? (a < b) : (a > b);
+            K[t] = swap ? b : a;
+            K[u] = swap ? a : b;
+          }
+        }
+      } else {
+        const int m = j / SPL;
+        const bool lower = (lane & m) == 0;
+#pragma unroll
+        for (int t = 0; t < SPL; ++t) {
+          const uint64_t o = xor_lane64(K[t], m);
+          const bool up = (((lane * SPL + t) & k) == 0);
+          const bool keep_max = up == lower;
+          K[t] = keep_max ? (K[t] > o ? K[t] : o) : (K[t] < o ? K[t] : o);
+        }
+      }
+    }
+  }
+}
+
+template <int EPT, int SPL>
 __global__ __launch_bounds__(64) void select_wave_kernel(
     const float* __restrict__ scores, int nblk, const int32_t* __restrict__ n_valid,
-    float top_p, int k_max, int k_min, int n_sink, int n_recent, int P,
+    float top_p, int k_max, int k_min, int n_sink, int n_recent,
     int32_t* __restrict__ idx_out, int32_t* __restrict__ count_out,
     float* __restrict__ mass_out) {
   constexpr int kMaxBlocks = 64 * EPT;
+  constexpr int P = 64 * SPL;
+  constexpr float kLog2e = 1.4426950408889634f;
   __shared__ uint32_t hist[256];
-  __shared__ uint32_t bits[kMaxBlocks / 32];
-  extern __shared__ uint32_t dyn[];  // staging [kMaxBlocks] | surv key [P] | id [P] | e [P]
-  float* stage = reinterpret_cast<float*>(dyn);
-  uint32_t* s_key = dyn + kMaxBlocks;
-  int* s_id = reinterpret_cast<int*>(s_key + P);
-  float* s_e = reinterpret_cast<float*>(s_id + P);
+  __shared__ uint32_t bits[(kMaxBlocks + 31) / 32];
+  __shared__ float stage[kMaxBlocks];
+  __shared__ uint64_t s_K[P];
 
   const int row = blockIdx.x;
   const int lane = threadIdx.x;
@@ -362,22 +436,37 @@ __global__ __launch_bounds__(64) void select_wave_kernel(
   const int n_res = nv - n_reserved;
   const int cap = min(k_max - n_reserved, n_res);
 
-  // Coalesced load into LDS, then each lane takes its consecutive run.
+  // 1. Coalesced loads, all in flight at once, then transpose via LDS.
   const float* srow = scores + (size_t)row * nblk;
-  for (int j = lane; j < nv; j += 64) stage[j] = srow[j];
-  for (int i = lane; i < kMaxBlocks / 32; i += 64) bits[i] = 0u;
+  float ld[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int j = e * 64 + lane;
+    ld[e] = j < nv ? srow[j] : -INFINITY;
+  }
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) stage[e * 64 + lane] = ld[e];
+  for (int i = lane; i < (kMaxBlocks + 31) / 32; i += 64) bits[i] = 0u;
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
+  // Candidates get a non-zero order key; reserved blocks are remembered in a
+  // per-lane bit word (VGPR) rather than as per-element lane masks.
   uint32_t key[EPT];
   float sv[EPT];
+  uint64_t resv = 0;
+  {
+    const int j0 = lane * EPT;
+    const int lo = max(sink_end - j0, 0), hi = min(rec_start - j0, EPT);  // candidate run
+    const int vend = min(nv - j0, EPT);                                   // valid run
 #pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    const int j = lane * EPT + e;
-    const bool c = j < nv && j >= sink_end && j < rec_start;
-    sv[e] = c ? stage[j] : -INFINITY;
-    key[e] = c ? order_key(sv[e]) : 0u;  // 0 marks "not a candidate"
+    for (int e = 0; e < EPT; ++e) {
+      const bool c = e >= lo && e < hi;
+      sv[e] = stage[j0 + e];
+      key[e] = c ? order_key(sv[e]) : 0u;  // 0 marks "not a candidate"
+      resv |= (uint64_t)(e < vend && !c) << e;
+    }
   }
 
   int n = 0;
@@ -392,13 +481,9 @@ __global__ __launch_bounds__(64) void select_wave_kernel(
     kmax = wave_max_u(kmax);
     kmin = wave_min_u(kmin);
     const float m = order_key_inv(kmax);
-    float pe[EPT];
     float zl = 0.f;
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      pe[e] = key[e] ? exp2f((sv[e] - m) * 1.4426950408889634f) : 0.f;
-      zl += pe[e];
-    }
+    for (int e = 0; e < EPT; ++e) zl += key[e] ? exp2f((sv[e] - m) * kLog2e) : 0.f;
     const float Z = wave_sum(zl);
 
     // ---- 2. radix select by count: the cap-th largest key ----
@@ -406,7 +491,7 @@ __global__ __launch_bounds__(64) void select_wave_kernel(
     int need = cap;
     if (cap < n_res) {
       const uint32_t diff = kmin ^ kmax;
-      int shift = diff ? 32 - __builtin_clz(diff) : 0;   // bits still to resolve
+      int shift = diff ? 32 - __builtin_clz(diff) : 0;  // low bits still to resolve
       uint32_t prefix = shift >= 32 ? 0u : (kmax >> shift) << shift;
       uint32_t pmask = shift >= 32 ? 0u : ~0u << shift;
       while (shift > 0) {
@@ -449,121 +534,107 @@ __global__ __launch_bounds__(64) void select_wave_kernel(
       thr = prefix;
     }
 
-    // survivors in id order: key > thr, or key == thr among the first `need`
+    // survivors (id order): key > thr, or key == thr among the first `need`
     int n_eq = 0;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) n_eq += (key[e] && key[e] == thr) ? 1 : 0;
     int eq_rank = wave_incl_scan_i(n_eq) - n_eq;
-    bool surv[EPT];
+    // Per-lane flag words live in VGPRs (bool arrays would become SGPR lane
+    // masks and spill).
+    uint64_t surv = 0;
     int n_sv = 0;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
       const bool eq = key[e] && key[e] == thr;
-      surv[e] = key[e] && (key[e] > thr || (eq && eq_rank < need));
+      const bool sv_e = key[e] && (key[e] > thr || (eq && eq_rank < need));
       eq_rank += eq ? 1 : 0;
-      n_sv += surv[e] ? 1 : 0;
+      n_sv += sv_e ? 1 : 0;
+      surv |= (uint64_t)sv_e << e;
     }
     int pos = wave_incl_scan_i(n_sv) - n_sv;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
-      if (surv[e] && pos < P) {
-        s_key[pos] = key[e];
-        s_id[pos] = lane * EPT + e;
-        s_e[pos] = pe[e];
+      if (((surv >> e) & 1u) && pos < P) {
+        // (key desc, id asc) == packed value desc
+        s_K[pos] = ((uint64_t)key[e] << 32) | (uint64_t)(0xffffffffu - (uint32_t)(lane * EPT + e));
         ++pos;
       }
     }
+    for (int i = cap + lane; i < P; i += 64) s_K[i] = 0ull;  // padding sorts last
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    // ---- 3. work on the cap survivors, SP consecutive ones per lane ----
-    const int SP = (cap + 63) / 64;
-    const int i0 = min(lane * SP, cap), i1 = min(i0 + SP, cap);
-    auto mass_ge = [&](uint32_t T) {
-      float part = 0.f;
-      for (int i = i0; i < i1; ++i) part += s_key[i] >= T ? s_e[i] : 0.f;
-      return wave_sum(part);
-    };
-    auto count_ge = [&](uint32_t T) {
-      int part = 0;
-      for (int i = i0; i < i1; ++i) part += s_key[i] >= T ? 1 : 0;
-      return wave_sum_i(part);
-    };
-    // Largest T with f(T) >= target, for f non-increasing in T (bisection).
-    const float pz = top_p * Z;
-    int n_target;
-    if (top_p >= 1.f) {
-      n_target = cap;
-    } else if (top_p <= 0.f) {
-      n_target = 0;
-    } else if (mass_ge(0u) < pz) {
-      n_target = cap;  // the nucleus would need more than the cap allows
-    } else {
-      uint32_t T = 0u;
-      for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t Tc = T | (1u << bit);
-        if (mass_ge(Tc) >= pz) T = Tc;
-      }
-      const float mass_gt = T == 0xffffffffu ? 0.f : mass_ge(T + 1u);
-      const int n_gt = T == 0xffffffffu ? 0 : count_ge(T + 1u);
-      const int n_eqT = count_ge(T) - n_gt;
-      float eT = 0.f;
-      for (int i = i0; i < i1; ++i) eT = s_key[i] == T ? s_e[i] : eT;
-      eT = wave_max(eT);
-      int t = 1;
-      while (t < n_eqT && mass_gt + (float)t * eT < pz) ++t;
-      n_target = n_gt + t;
-    }
-    n = min(n_target, cap);
-    if (n_reserved + n < k_min) n = min(k_min - n_reserved, cap);
+    // ---- 3. sort the survivors ----
+    uint64_t K[SPL];
+#pragma unroll
+    for (int t = 0; t < SPL; ++t) K[t] = s_K[lane * SPL + t];
+    bitonic_desc<SPL>(K);
 
-    // ---- 4. the top-n survivors (count bisection, ties by lowest id) ----
-    uint32_t T2 = 0u;
-    int need2 = n;
-    if (n < cap) {
-      for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t Tc = T2 | (1u << bit);
-        if (count_ge(Tc) >= n) T2 = Tc;
-      }
-      need2 = n - (T2 == 0xffffffffu ? 0 : count_ge(T2 + 1u));
+    // ---- 4. prefix mass in sorted order ----
+    float cum[SPL];
+    float run = 0.f;
+#pragma unroll
+    for (int t = 0; t < SPL; ++t) {
+      const bool real = lane * SPL + t < cap;
+      const float s = order_key_inv((uint32_t)(K[t] >> 32));
+      run += real ? exp2f((s - m) * kLog2e) : 0.f;
+      cum[t] = run;
     }
-    int q_eq = 0;
-    for (int i = i0; i < i1; ++i) q_eq += s_key[i] == T2 ? 1 : 0;
-    int r = wave_incl_scan_i(q_eq) - q_eq;
-    float ml = 0.f;
-    for (int i = i0; i < i1; ++i) {
-      const bool eq = s_key[i] == T2;
-      const bool take = n > 0 && (s_key[i] > T2 || (eq && r < need2));
-      r += eq ? 1 : 0;
-      if (take) {
-        atomicOr(&bits[s_id[i] >> 5], 1u << (s_id[i] & 31));
-        ml += s_e[i];
+    const float base = wave_incl_scan_f(run) - run;
+    const float pz = top_p * Z;
+    int below = 0;
+#pragma unroll
+    for (int t = 0; t < SPL; ++t) {
+      cum[t] += base;
+      below += (lane * SPL + t < cap && cum[t] < pz) ? 1 : 0;
+    }
+    if (top_p >= 1.f)
+      n = cap;
+    else if (top_p <= 0.f)
+      n = 0;
+    else
+      n = min(cap, wave_sum_i(below) + 1);
+    if (n_reserved + n < k_min) n = min(k_min - n_reserved, cap);
+#pragma unroll
+    for (int t = 0; t < SPL; ++t) {
+      if (lane * SPL + t < n) {
+        const int id = (int)(0xffffffffu - (uint32_t)K[t]);
+        atomicOr(&bits[id >> 5], 1u << (id & 31));
       }
     }
-    mass = n > 0 ? wave_sum(ml) / Z : 0.f;
+    if (n > 0) {
+      const int ln = (n - 1) / SPL, tn = (n - 1) % SPL;
+      float mine = 0.f;
+#pragma unroll
+      for (int t = 0; t < SPL; ++t) mine = t == tn ? cum[t] : mine;
+      mass = readlane_f(mine, ln) / Z;
+    }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 
   // ---- write S = reserved u chosen, ascending ----
-  bool fin[EPT];
-  int n_fin = 0;
+  // chosen bits of this lane's run [lane*EPT, lane*EPT + EPT) (EPT <= 64)
+  uint64_t fin = resv;
+  {
+    const int j0 = lane * EPT;
+    if (EPT >= 32) {
 #pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    const int j = lane * EPT + e;
-    const bool reserved = j < nv && (j < sink_end || j >= rec_start);
-    fin[e] = reserved || (j < nv && ((bits[j >> 5] >> (j & 31)) & 1u));
-    n_fin += fin[e] ? 1 : 0;
+      for (int w = 0; w < EPT / 32; ++w) fin |= (uint64_t)bits[j0 / 32 + w] << (32 * w);
+    } else {
+      fin |= (uint64_t)((bits[j0 >> 5] >> (j0 & 31)) & ((1u << EPT) - 1u));
+    }
   }
+  const int n_fin = __popcll(fin);
   const int incl = wave_incl_scan_i(n_fin);
   const int total = __builtin_amdgcn_readlane(incl, 63);
   int pos = incl - n_fin;
   int32_t* out = idx_out + (size_t)row * k_max;
 #pragma unroll
   for (int e = 0; e < EPT; ++e)
-    if (fin[e] && pos < k_max) out[pos++] = lane * EPT + e;
+    if (((fin >> e) & 1u) && pos < k_max) out[pos++] = lane * EPT + e;
   for (int i = total + lane; i < k_max; i += 64) out[i] = -1;
   if (lane == 0) {
     count_out[row] = min(total, k_max);
@@ -582,22 +653,25 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
   dim3 grid(rows);
   const int ept = nblk <= 64 ? 1 : nblk <= 128 ? 2 : nblk <= 256 ? 4 : nblk <= 512 ? 8
                 : nblk <= 1024 ? 16 : nblk <= 2048 ? 32 : 64;
-  const size_t shm_w = (size_t)(64 * ept + 3 * P) * 4;
-  if (nblk <= 4096 && shm_w <= 56 * 1024) {
-#define SPOT_SELECT_WAVE(E)                                                                     \
-    if (ept == E) {                                                                           \
-      hipLaunchKernelGGL((select_wave_kernel<E>), grid, dim3(64), shm_w, s, scores, nblk,     \
-                         n_valid, top_p, k_max, k_min, n_sink, n_recent, P, idx, count,       \
+  const int spl = P <= 64 ? 1 : P / 64;
+  if (nblk <= 4096 && spl <= 8) {
+#define SPOT_SELECT_WAVE(E, S)                                                                  \
+    if (ept == E && spl == S) {                                                               \
+      hipLaunchKernelGGL((select_wave_kernel<E, S>), grid, dim3(64), 0, s, scores, nblk,      \
+                         n_valid, top_p, k_max, k_min, n_sink, n_recent, idx, count,          \
                          nuc_mass);                                                           \
       return hipGetLastError();                                                                \
     }
-    SPOT_SELECT_WAVE(1)
-    SPOT_SELECT_WAVE(2)
-    SPOT_SELECT_WAVE(4)
-    SPOT_SELECT_WAVE(8)
-    SPOT_SELECT_WAVE(16)
-    SPOT_SELECT_WAVE(32)
-    SPOT_SELECT_WAVE(64)
+#define SPOT_SELECT_WAVE_E(E) \
+    SPOT_SELECT_WAVE(E, 1) SPOT_SELECT_WAVE(E, 2) SPOT_SELECT_WAVE(E, 4) SPOT_SELECT_WAVE(E, 8)
+    SPOT_SELECT_WAVE_E(1)
+    SPOT_SELECT_WAVE_E(2)
+    SPOT_SELECT_WAVE_E(4)
+    SPOT_SELECT_WAVE_E(8)
+    SPOT_SELECT_WAVE_E(16)
+    SPOT_SELECT_WAVE_E(32)
+    SPOT_SELECT_WAVE_E(64)
+#undef SPOT_SELECT_WAVE_E
 #undef SPOT_SELECT_WAVE
   }
   const size_t shm = (size_t)(3 * P + (nblk >> 5) + 1) * 4;

@@ -125,7 +125,7 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
                                 float top_p, int k_max, int k_min, int n_sink, int n_recent,
                                 int32_t* idx, int32_t* count, float* nuc_mass, hipStream_t s);
 
-int decode_num_splits(int batch, int h_kv, int max_blocks);
+int decode_num_splits(int batch, int h_kv, int max_blocks, int group);
 size_t decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_blocks);
 
 hipError_t launch_decode(bool dense, const void* q, const void* k, const void* v,
