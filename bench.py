@@ -15,9 +15,10 @@ over NCOPY distinct copies of the KV cache and selector cache so that the
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
-import math
 import os
+import re
 import sys
 import time
 
@@ -42,6 +43,32 @@ def parse():
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_sparse_L131072_B4.md")
+
+
+def decode_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("decode.hip", "spot_internal.h"):
+        with open(os.path.join(ROOT, "paper_2606_22874_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed rocprofv3 counter runs,
+    or None when the decode kernel source changed since they were taken."""
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    m = re.search(r"traffic_bytes_per_launch: (\d+)\s*\(source: .*? sha256 prefix (\w+)\)",
+                  text, re.S)
+    if not m or m.group(2) != decode_source_hash():
+        return None
+    return int(m.group(1))
 
 
 def main():
@@ -165,6 +192,11 @@ def main():
     stream_ms = timed(lambda i: spot.spot_probe_stream_read(bufs[i % len(bufs)], sink, stream),
                       args.steps)
     stream_gbs = step_bytes / (stream_ms * 1e-3) / 1e9
+    # Known-size write (64 MiB fill) for calibrating the WRITE_SIZE counter.
+    calib = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
+    calib.fill_(1)
+    torch.cuda.synchronize()
+    del calib
 
     steps_per_s = 1e3 / ms
     step_gbs = step_bytes / (ms * 1e-3) / 1e9
@@ -203,7 +235,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic() if args.fmt == "bf16" else None,
             "bytes_per_launch": attn_bytes,
             "avg_launch_us": round(attn_ms * 1e3, 2),
         },

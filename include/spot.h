@@ -137,10 +137,9 @@ size_t spot_decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_
  *     T = { t < seq_len[b] : t / 64 in S_b },  lse[b, h] = log sum_{t in T} exp(.)
  * Entries of idx that are negative or whose block starts at or past seq_len
  * are skipped, so a bad index cannot cause an out-of-bounds read.  An empty
- * T gives out = 0 and lse = -inf.  Blocks are shared out among workgroups at
- * run time (to absorb uneven workgroup start times), so the FP32 summation
- * order -- and hence the last bits of out and lse -- may differ between
- * calls on identical inputs.
+ * T gives out = 0 and lse = -inf.  The work split and every reduction order
+ * depend only on the sizes, so identical inputs give bitwise identical
+ * outputs.
  *
  *  q        device BF16 [batch, h_q, d]
  *  k, v     device BF16 [batch, h_kv, l_cap, d]  (l_cap a multiple of 64)

@@ -642,6 +642,291 @@ __global__ __launch_bounds__(64) void select_wave_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Workgroup (4 waves) selection for rows of 513 .. 4096 blocks, cap <= 512.
+// Same algorithm as the single-wave kernel, with the element-wise phases
+// spread over 256 threads (EPT <= 16 consecutive ids each):
+//  * max and Z in one barrier: each wave reduces its own max m_w and
+//    z_w = sum exp(s - m_w); then m = max_w m_w, Z = sum_w z_w exp(m_w - m);
+//  * radix select by count as before (block histogram, wave 0 scans);
+//  * one packed (greater, equal) exclusive scan gives every survivor its
+//    compaction slot;
+//  * wave 0 finishes on the survivors.  When the cap binds (the survivors'
+//    mass stays below top_p * Z) every survivor is chosen and no sort is
+//    needed; otherwise it sorts them and cuts the prefix as before.
+constexpr int kSelWG = 256;
+
+// Exclusive prefix over the 256 threads in thread order; `total` = sum.
+__device__ __forceinline__ int wg_excl_scan(int v, int* red, int& total) {
+  const int lane = __lane_id(), wave = threadIdx.x >> 6;
+  const int incl = wave_incl_scan_i(v);
+  if (lane == 63) red[wave] = incl;
+  __syncthreads();
+  int base = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < kSelWG / 64; ++w) {
+    const int t = red[w];
+    base += w < wave ? t : 0;
+    total += t;
+  }
+  __syncthreads();
+  return base + incl - v;
+}
+
+template <int EPT, int SPL>
+__global__ __launch_bounds__(kSelWG) void select_wg_kernel(
+    const float* __restrict__ scores, int nblk, const int32_t* __restrict__ n_valid,
+    float top_p, int k_max, int k_min, int n_sink, int n_recent,
+    int32_t* __restrict__ idx_out, int32_t* __restrict__ count_out,
+    float* __restrict__ mass_out) {
+  constexpr int NT = kSelWG, NW = NT / 64;
+  constexpr int kMaxBlocks = NT * EPT;
+  constexpr int P = 64 * SPL;
+  constexpr float kLog2e = 1.4426950408889634f;
+  static_assert(32 % EPT == 0, "a thread's ids must sit in one bit word");
+  __shared__ float stage[kMaxBlocks];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t bits[kMaxBlocks / 32];
+  __shared__ uint64_t s_K[P];
+  __shared__ uint32_t red_u[NW][2];
+  __shared__ float red_f[NW];
+  __shared__ int red_i[NW];
+  __shared__ int bc[4];
+
+  const int row = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int nv = n_valid ? n_valid[row] : nblk;
+  nv = nv < 0 ? 0 : (nv > nblk ? nblk : nv);
+  const int sink_end = min(n_sink, nv);
+  const int rec_start = max(0, nv - n_recent);
+  const int n_reserved = sink_end + (nv - rec_start) - max(0, sink_end - rec_start);
+  const int n_res = nv - n_reserved;
+  const int cap = min(k_max - n_reserved, n_res);
+
+  // 1. coalesced loads (all in flight), transposed through LDS
+  const float* srow = scores + (size_t)row * nblk;
+  float ld[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int j = e * NT + tid;
+    ld[e] = j < nv ? srow[j] : -INFINITY;
+  }
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) stage[e * NT + tid] = ld[e];
+  for (int i = tid; i < kMaxBlocks / 32; i += NT) bits[i] = 0u;
+  __syncthreads();
+
+  const int j0 = tid * EPT;
+  uint32_t key[EPT];
+  float sv[EPT];
+  uint32_t resv = 0;
+  {
+    const int lo = max(sink_end - j0, 0), hi = min(rec_start - j0, EPT);
+    const int vend = min(nv - j0, EPT);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const bool c = e >= lo && e < hi;
+      sv[e] = stage[j0 + e];
+      key[e] = c ? order_key(sv[e]) : 0u;  // 0 marks "not a candidate"
+      resv |= (uint32_t)(e < vend && !c) << e;
+    }
+  }
+
+  float mass = 0.f;
+  if (cap > 0) {
+    // 2. max, min and Z with one barrier
+    uint32_t kmax = 0u, kmin = 0xffffffffu;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      kmax = max(kmax, key[e]);
+      if (key[e]) kmin = min(kmin, key[e]);
+    }
+    kmax = wave_max_u(kmax);
+    kmin = wave_min_u(kmin);
+    float zw = 0.f;
+    if (kmax) {
+      const float mw = order_key_inv(kmax);
+      float zl = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) zl += key[e] ? exp2f((sv[e] - mw) * kLog2e) : 0.f;
+      zw = wave_sum(zl);
+    }
+    if (lane == 0) {
+      red_u[wave][0] = kmax;
+      red_u[wave][1] = kmin;
+      red_f[wave] = zw;
+    }
+    __syncthreads();
+    kmax = 0u;
+    kmin = 0xffffffffu;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      kmax = max(kmax, red_u[w][0]);
+      kmin = min(kmin, red_u[w][1]);
+    }
+    const float m = order_key_inv(kmax);
+    float Z = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+      if (red_u[w][0]) Z += red_f[w] * exp2f((order_key_inv(red_u[w][0]) - m) * kLog2e);
+
+    // 3. radix select by count: the cap-th largest key
+    uint32_t thr = 0u;  // cap == n_res: every candidate survives (keys > 0)
+    int need = cap;
+    if (cap < n_res) {
+      const uint32_t diff = kmin ^ kmax;
+      int shift = diff ? 32 - __builtin_clz(diff) : 0;  // low bits still to resolve
+      uint32_t prefix = shift >= 32 ? 0u : (kmax >> shift) << shift;
+      uint32_t pmask = shift >= 32 ? 0u : ~0u << shift;
+      while (shift > 0) {
+        const int width = shift < 8 ? shift : 8;
+        shift -= width;
+        const uint32_t dmask = (1u << width) - 1u;
+        hist[tid] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+          if (key[e] && (key[e] & pmask) == prefix) atomicAdd(&hist[(key[e] >> shift) & dmask], 1u);
+        __syncthreads();
+        if (wave == 0) {
+          // lane l holds digits 255-4l .. 252-4l (descending)
+          int c[4], tot = 0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            c[i] = (int)hist[255 - 4 * lane - i];
+            tot += c[i];
+          }
+          const int incl = wave_incl_scan_i(tot);
+          int before = incl - tot;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (before < need && need <= before + c[i]) {
+              bc[0] = 255 - 4 * lane - i;
+              bc[1] = need - before;
+            }
+            before += c[i];
+          }
+        }
+        __syncthreads();
+        prefix |= (uint32_t)bc[0] << shift;
+        pmask |= dmask << shift;
+        need = bc[1];
+      }
+      thr = prefix;
+    }
+
+    // 4. survivors and their slots from one packed (greater, equal) scan
+    int n_gt = 0, n_eq = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      n_gt += (key[e] && key[e] > thr) ? 1 : 0;
+      n_eq += (key[e] && key[e] == thr) ? 1 : 0;
+    }
+    int total;
+    const int pre = wg_excl_scan(n_gt | (n_eq << 16), red_i, total);
+    int gt_before = pre & 0xffff, eq_before = pre >> 16;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      if (!key[e]) continue;
+      const uint64_t K = ((uint64_t)key[e] << 32) | (uint64_t)(0xffffffffu - (uint32_t)(j0 + e));
+      if (key[e] > thr) {
+        const int pos = gt_before + min(eq_before, need);
+        if (pos < P) s_K[pos] = K;
+        ++gt_before;
+      } else if (key[e] == thr) {
+        if (eq_before < need && gt_before + eq_before < P) s_K[gt_before + eq_before] = K;
+        ++eq_before;
+      }
+    }
+    for (int i = cap + tid; i < P; i += NT) s_K[i] = 0ull;  // padding sorts last
+    __syncthreads();
+
+    // 5. wave 0 decides n and marks the chosen blocks
+    if (wave == 0) {
+      uint64_t K[SPL];
+      float ev[SPL];
+      float msum = 0.f;
+#pragma unroll
+      for (int t = 0; t < SPL; ++t) {
+        K[t] = s_K[lane * SPL + t];
+        const bool real = lane * SPL + t < cap;
+        ev[t] = real ? exp2f((order_key_inv((uint32_t)(K[t] >> 32)) - m) * kLog2e) : 0.f;
+        msum += ev[t];
+      }
+      msum = wave_sum(msum);
+      const float pz = top_p * Z;
+      int n;
+      bool sorted = false;
+      float cum[SPL];
+      auto sort_and_scan = [&]() {
+        bitonic_desc<SPL>(K);
+        float run = 0.f;
+#pragma unroll
+        for (int t = 0; t < SPL; ++t) {
+          const bool real = lane * SPL + t < cap;
+          run += real ? exp2f((order_key_inv((uint32_t)(K[t] >> 32)) - m) * kLog2e) : 0.f;
+          cum[t] = run;
+        }
+        const float base = wave_incl_scan_f(run) - run;
+#pragma unroll
+        for (int t = 0; t < SPL; ++t) cum[t] += base;
+        sorted = true;
+      };
+      if (top_p >= 1.f) {
+        n = cap;
+      } else if (top_p <= 0.f) {
+        n = 0;
+      } else if (msum < pz) {
+        n = cap;  // the cap binds before the nucleus reaches top_p
+      } else {
+        sort_and_scan();
+        int below = 0;
+#pragma unroll
+        for (int t = 0; t < SPL; ++t) below += (lane * SPL + t < cap && cum[t] < pz) ? 1 : 0;
+        n = min(cap, wave_sum_i(below) + 1);
+      }
+      if (n_reserved + n < k_min) n = min(k_min - n_reserved, cap);
+      if (n < cap && !sorted) sort_and_scan();
+      float mass_w = 0.f;
+      if (n == cap) {
+        mass_w = msum;
+      } else if (n > 0) {
+        const int ln = (n - 1) / SPL, tn = (n - 1) % SPL;
+        float mine = 0.f;
+#pragma unroll
+        for (int t = 0; t < SPL; ++t) mine = t == tn ? cum[t] : mine;
+        mass_w = readlane_f(mine, ln);
+      }
+#pragma unroll
+      for (int t = 0; t < SPL; ++t) {
+        if (lane * SPL + t < n) {
+          const int id = (int)(0xffffffffu - (uint32_t)K[t]);
+          atomicOr(&bits[id >> 5], 1u << (id & 31));
+        }
+      }
+      if (lane == 0) red_f[0] = n > 0 ? mass_w / Z : 0.f;
+    }
+    __syncthreads();
+    mass = red_f[0];
+  }
+
+  // 6. write S = reserved u chosen, ascending
+  uint32_t fin = resv;
+  fin |= (EPT == 32 ? bits[j0 >> 5] : (bits[j0 >> 5] >> (j0 & 31)) & ((1u << EPT) - 1u));
+  int total;
+  int pos = wg_excl_scan(__popc(fin), red_i, total);
+  int32_t* out = idx_out + (size_t)row * k_max;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e)
+    if (((fin >> e) & 1u) && pos < k_max) out[pos++] = j0 + e;
+  for (int i = total + tid; i < k_max; i += NT) out[i] = -1;
+  if (tid == 0) {
+    count_out[row] = min(total, k_max);
+    if (mass_out) mass_out[row] = mass;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const int32_t* n_valid,
@@ -654,6 +939,23 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
   const int ept = nblk <= 64 ? 1 : nblk <= 128 ? 2 : nblk <= 256 ? 4 : nblk <= 512 ? 8
                 : nblk <= 1024 ? 16 : nblk <= 2048 ? 32 : 64;
   const int spl = P <= 64 ? 1 : P / 64;
+  if (nblk > 512 && nblk <= 4096 && spl <= 8) {
+    const int e2 = nblk <= 1024 ? 4 : nblk <= 2048 ? 8 : 16;
+#define SPOT_SELECT_WG(E, S)                                                                    \
+    if (e2 == E && spl == S) {                                                                \
+      hipLaunchKernelGGL((select_wg_kernel<E, S>), grid, dim3(kSelWG), 0, s, scores, nblk,    \
+                         n_valid, top_p, k_max, k_min, n_sink, n_recent, idx, count,          \
+                         nuc_mass);                                                           \
+      return hipGetLastError();                                                                \
+    }
+#define SPOT_SELECT_WG_E(E) \
+    SPOT_SELECT_WG(E, 1) SPOT_SELECT_WG(E, 2) SPOT_SELECT_WG(E, 4) SPOT_SELECT_WG(E, 8)
+    SPOT_SELECT_WG_E(4)
+    SPOT_SELECT_WG_E(8)
+    SPOT_SELECT_WG_E(16)
+#undef SPOT_SELECT_WG_E
+#undef SPOT_SELECT_WG
+  }
   if (nblk <= 4096 && spl <= 8) {
 #define SPOT_SELECT_WAVE(E, S)                                                                  \
     if (ept == E && spl == S) {                                                               \

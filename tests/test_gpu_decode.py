@@ -279,10 +279,8 @@ def test_sparse_equals_dense_when_all_selected():
     assert torch.max(torch.abs(la - lb)).item() <= 1e-4
 
 
-def test_full_step_repeatable():
-    """Scores and the selection are bitwise repeatable.  Attention balances
-    blocks across workgroups at run time, so its FP32 summation order (not its
-    inputs) can change between runs: outputs agree to BF16 rounding."""
+def test_full_step_deterministic():
+    """Scores, selection and attention outputs are bitwise repeatable."""
     wl = workload(3)
     q_sel, w, k_sel, nv = bf(wl.q_sel), f32(wl.w), bf(wl.k_sel), i32(wl.n_valid)
     q, k, v, sl = bf(wl.q), bf(wl.k), bf(wl.v), i32(wl.seq_len)
@@ -294,11 +292,8 @@ def test_full_step_repeatable():
         res.append((s, idx, cnt, mass, out, lse))
     torch.cuda.synchronize()
     for r in res[1:]:
-        for x, y in zip(res[0][:4], r[:4]):
+        for x, y in zip(res[0], r):
             assert torch.equal(x, y)
-        o0, o1 = res[0][4].float(), r[4].float()
-        assert torch.all(torch.abs(o0 - o1) <= 2.0 ** -7 * torch.abs(o0) + 1e-6)
-        assert torch.max(torch.abs(res[0][5] - r[5])).item() <= 1e-5
 
 
 def test_error_paths_leave_outputs_untouched():
