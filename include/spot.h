@@ -187,12 +187,21 @@ spot_status spot_dense_decode(const void *q, const void *k, const void *v,
  *
  *  q        device BF16 [batch, h_q, L, d]
  *  k, v     device BF16 [batch, h_kv, L, d]   (L a multiple of 64)
- *  idx      device int32 [batch * L/64, k_max] distinct ids, ascending
- *  count    device int32 [batch * L/64]
+ *  idx      device int32 [batch * L/64, k_max]: the first min(count, k_max)
+ *           entries of row b*(L/64)+qb are the selected block ids, each at
+ *           most once (a repeated id is attended once per occurrence); ids
+ *           outside [0, qb] are skipped
+ *  count    device int32 [batch * L/64] (negative counts as 0)
  *  out      device BF16 [batch, h_q, L, d] (output)
- *  lse      device float [batch, h_q, L] (output, may be NULL)
+ *  lse      device float [batch, h_q, L] (output, natural log, may be NULL);
+ *           a query token that sees no key gets out = 0 and lse = -inf
  *
- * Supported: d == 128, h_q / h_kv in {1, 2, 4, 8}.
+ * Numerics: scores and the running softmax in FP32; the probabilities are
+ * rounded to BF16 for the P.V product (FP32 accumulation).  No atomics: the
+ * result is bitwise reproducible.
+ *
+ * Supported: d == 128, h_q / h_kv in {1, 2, 4, 8}, k_max <= 4096 and a
+ * finite sm_scale > 0 (otherwise SPOT_ERR_UNSUPPORTED).
  */
 spot_status spot_sparse_prefill(const void *q, const void *k, const void *v, int L,
                                 const int32_t *idx, const int32_t *count, int k_max, int batch,

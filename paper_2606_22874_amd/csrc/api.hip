@@ -117,7 +117,9 @@ spot_status spot_sparse_prefill(const void* q, const void* k, const void* v, int
                                 void* stream) {
   if (!q || !k || !v || !idx || !count || !out) return SPOT_ERR_NULL;
   if (L < 0 || L % kBlk || batch < 0 || k_max < 1 || h_q < 1 || h_kv < 1) return SPOT_ERR_SHAPE;
-  if (d != 128 || !supported_group(h_q, h_kv)) return SPOT_ERR_UNSUPPORTED;
+  if (d != 128 || !supported_group(h_q, h_kv) || k_max > 4096) return SPOT_ERR_UNSUPPORTED;
+  if (!(sm_scale > 0.f) || sm_scale > 3.0e38f) return SPOT_ERR_UNSUPPORTED;
+  if ((long long)batch * (L / kBlk) * h_kv > 0x0fffffffLL) return SPOT_ERR_SHAPE;
   if (batch == 0 || L == 0) return SPOT_OK;
   return from_hip(launch_sparse_prefill(q, k, v, L, idx, count, k_max, batch, h_q, h_kv,
                                         sm_scale, out, lse, static_cast<hipStream_t>(stream)));

@@ -83,6 +83,9 @@ def test_validation_errors_before_launch(lib):
     pre = lib.spot_sparse_prefill
     assert pre(nz, nz, nz, 100, nz, nz, 4, 1, 64, 8, 128, 0.1, nz, None, None) == 2
     assert pre(nz, nz, nz, 128, nz, nz, 4, 1, 64, 8, 96, 0.1, nz, None, None) == 3
+    assert pre(nz, nz, nz, 128, nz, nz, 5000, 1, 64, 8, 128, 0.1, nz, None, None) == 3
+    for bad_scale in (0.0, -0.1, float("nan"), float("inf")):
+        assert pre(nz, nz, nz, 128, nz, nz, 4, 1, 64, 8, 128, bad_scale, nz, None, None) == 3
 
 
 def test_workspace_size_query(lib):
