@@ -25,6 +25,7 @@ import time
 import numpy as np
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "decode steps/s at L=128K (selector+sparse attn), % of HBM peak GB/s"
 
 
@@ -38,6 +39,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--dense", action="store_true", help="also time the dense decode baseline")
     ap.add_argument("--fmt", default="bf16", choices=["bf16", "int4", "mxfp4"])
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the block-sparse prefill leg (32K-token layer)")
+    ap.add_argument("--prefill-iters", type=int, default=10)
     return ap.parse_args()
 
 
@@ -259,10 +263,89 @@ def main():
             "hbm_frac": round(dbytes / (dms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         }
 
+    if not args.no_prefill:
+        del copies, bufs
+        torch.cuda.empty_cache()
+        result["prefill"] = prefill_leg(args, torch, spot, synth, dev, timed)
+
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
+
+
+def prefill_leg(args, torch, spot, synth, dev, timed):
+    """Block-sparse causal prefill of one 32K-token Qwen3-32B-shaped layer
+    (64 query / 8 KV heads, d = 128): query-block selector scores, selection
+    (p = 0.9, K_max = 64) and the MFMA block-sparse attention."""
+    log("[bench] prefill: generating the 32K-token layer")
+    pw = synth.prefill_config()
+    nqb, rule = pw.nblk, pw.rule
+
+    def bf(a):
+        return spot.to_device_bf16(a, dev)
+
+    q, k, v = bf(pw.q), bf(pw.k), bf(pw.v)
+    q_sel, k_sel = bf(pw.q_sel), bf(pw.k_sel)
+    w = torch.from_numpy(pw.w).to(dev)
+    n_valid = torch.from_numpy(pw.n_valid).to(dev)
+    rows = pw.B * nqb
+    scores = torch.empty((rows, nqb), dtype=torch.float32, device=dev)
+    idx = torch.empty((rows, rule.k_max), dtype=torch.int32, device=dev)
+    cnt = torch.empty(rows, dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    lse = torch.empty((pw.B, pw.Hq, pw.L), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def score(i):
+        spot.spot_selector_score(q_sel, w, k_sel, None, "bf16", pw.B, nqb, nqb, pw.Hs, pw.ds,
+                                 n_valid, scores, stream)
+
+    def select(i):
+        spot.spot_select_blocks(scores, rows, nqb, n_valid, rule.top_p, rule.k_max, rule.k_min,
+                                rule.n_sink, rule.n_recent, idx, cnt, None, stream)
+
+    def attend(i):
+        spot.spot_sparse_prefill(q, k, v, pw.L, idx, cnt, rule.k_max, pw.B, pw.Hq, pw.Hkv, pw.d,
+                                 pw.sm_scale, out, lse, stream)
+
+    for i in range(2):
+        score(i), select(i), attend(i)
+    torch.cuda.synchronize()
+    n = args.prefill_iters
+    attn_ms = timed(attend, n)
+    score_ms = timed(score, n)
+    select_ms = timed(select, n)
+    step_ms = timed(lambda i: (score(i), select(i), attend(i)), n)
+
+    ids = idx.cpu().numpy()
+    c = cnt.cpu().numpy()
+    qb = np.arange(rows) % nqb
+    take = np.arange(rule.k_max)[None, :] < c[:, None]
+    n_tiles = int(take.sum())
+    n_diag = int((take & (ids == qb[:, None])).sum())
+    tile_flops = 4.0 * 64 * 64 * pw.d * pw.Hq          # QK^T and PV, all query heads
+    mfma_flops = n_tiles * tile_flops
+    useful_flops = (n_tiles - n_diag + n_diag * (64 * 65 / 2) / (64 * 64)) * tile_flops
+    tflops = mfma_flops / (attn_ms * 1e-3) / 1e12
+    log(f"[bench] prefill: {step_ms:.3f} ms/layer; attention {attn_ms:.3f} ms "
+        f"({tflops:.0f} TFLOP/s), score {score_ms * 1e3:.1f} us, select {select_ms * 1e3:.1f} us")
+    return {
+        "workload": "prefill L=32768 B=1 (Qwen3-32B-shaped layer: 64 q / 8 kv heads, d=128; "
+                    "selector 8x64 pooled per 64-token block; p=0.9 K_max=64 sink 1 recent 2)",
+        "value": round(pw.L / (step_ms * 1e-3), 1), "unit": "tokens/s",
+        "ms_per_layer": round(step_ms, 4),
+        "stage_us": {"score": round(score_ms * 1e3, 2), "select": round(select_ms * 1e3, 2),
+                     "attention": round(attn_ms * 1e3, 2)},
+        "selected_tiles": n_tiles, "diagonal_tiles": n_diag,
+        "roofline": {
+            "bound": "mfma", "kernel": "prefill_kernel (spot_sparse_prefill)",
+            "achieved": round(tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+            "useful_tflops": round(useful_flops / (attn_ms * 1e-3) / 1e12, 1),
+            "flops_per_launch": mfma_flops, "avg_launch_us": round(attn_ms * 1e3, 1),
+        },
+    }
 
 
 def cpu_baseline(wl, budget_s):

@@ -26,6 +26,8 @@
 // order, so the tile keeps 256-byte rows and bank conflicts are avoided by
 // XOR-swizzling the 16-byte chunks of a row instead of padding it.  Two tile
 // buffers alternate; the next tile's loads fly while the current one is used.
+#include <type_traits>
+
 #include "spot_internal.h"
 
 namespace spot {
@@ -42,13 +44,9 @@ constexpr int kTileBytes = kBlk * kRowBytes;    // 16 KiB
 constexpr int kPrefillMaxIds = 4096;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
+constexpr float kLazy = 8.f;
 
-struct PrefillSmem {
-  alignas(16) unsigned char k[2][kTileBytes];
-  alignas(16) unsigned char v[2][kTileBytes];
-  int ids[kPrefillMaxIds];
-  int n_local;
-};
+constexpr int kQWaveBytes = 32 * kRowBytes;     // 32 query rows of one wave
 
 // Physical 16-byte chunk of logical chunk c in tile row r.  K is read as 16
 // rows x one chunk per quarter wave, so rows must map one chunk to distinct
@@ -59,13 +57,14 @@ __device__ __forceinline__ int swz_v(int r, int c) { return c ^ ((r & 7) << 1); 
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Stage one 64 x 128 BF16 tile (16 KiB, contiguous in global memory) in LDS.
-template <int W, bool IS_K>
+// Stage one 64 x 128 BF16 tile (16 KiB, contiguous in global memory) in LDS,
+// shared out over waves 0..NW-1 (1 KiB per wave instruction).
+template <int NW, bool IS_K>
 __device__ __forceinline__ void stage_tile(const uint16_t* __restrict__ src, unsigned char* dst,
                                            int wave, int lane) {
 #pragma unroll
-  for (int u = 0; u < 16 / W; ++u) {
-    const int base = (u * W + wave) * kWave;  // first physical chunk of this wave's KiB
+  for (int u = 0; u < 16 / NW; ++u) {
+    const int base = (u * NW + wave) * kWave;  // first physical chunk of this wave's KiB
     const int p = base + lane;
     const int r = p >> 4, pc = p & 15;
     const int lc = IS_K ? swz_k(r, pc) : swz_v(r, pc);
@@ -76,11 +75,214 @@ __device__ __forceinline__ void stage_tile(const uint16_t* __restrict__ src, uns
 
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-__device__ __forceinline__ float xor_f(float x, int m) { return __shfl_xor(x, m, 64); }
-
+// Two floats -> packed BF16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  return (uint32_t)f32_to_bf16_rne(a) | ((uint32_t)f32_to_bf16_rne(b) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2_t));
 }
+
+// Cross-lane partner values within the wave without an LDS round trip:
+// v_permlane32_swap / v_permlane16_swap exchange the two halves / the
+// odd-even 16-lane rows of a register, so combining the swapped pair gives
+// every lane the value of lane l ^ 32 (resp. l ^ 16) alongside its own.
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ float max4(f32x4 x) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(x[0], x[1]),
+                                       __builtin_elementwise_maximum(x[2], x[3]));
+}
+
+// 16 bytes (8 BF16) of logical chunk c of row r of a swizzled LDS tile.
+__device__ __forceinline__ bf16x8 lds_frag(const unsigned char* base, int r, int c) {
+  return __builtin_bit_cast(
+      bf16x8, *reinterpret_cast<const u32x4*>(base + r * kRowBytes + (swz_k(r, c) << 4)));
+}
+
+// S^T[key][query] of one key block for the wave's 32 queries: 4 key tiles x
+// 2 query tiles, eight independent accumulation chains, head dim outermost.
+// The operands of step ks+1 are read from LDS before the MFMAs of step ks
+// are issued, so the read latency hides behind matrix work.
+__device__ __forceinline__ void qk_tile(const unsigned char* Kt, const unsigned char* Qw,
+                                        f32x4 (&s)[2][4], int G, int r16) {
+  bf16x8 a[2][4], bq[2][2];
+  auto load = [&](int ks, int slot) {
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) a[slot][kt] = lds_frag(Kt, kt * 16 + r16, ks * 4 + G);
+    bq[slot][0] = lds_frag(Qw, r16, ks * 4 + G);
+    bq[slot][1] = lds_frag(Qw, 16 + r16, ks * 4 + G);
+  };
+  load(0, 0);
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int cur = ks & 1;
+    if (ks + 1 < 4) load(ks + 1, cur ^ 1);
+    // Keep the reads of step ks+1 ahead of the MFMAs of step ks.
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      const f32x4 z = ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : s[0][kt];
+      const f32x4 z1 = ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : s[1][kt];
+      s[0][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cur][kt], bq[cur][0], z, 0, 0, 0);
+      s[1][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cur][kt], bq[cur][1], z1, 0, 0, 0);
+    }
+  }
+}
+
+// O^T[d][query] += V^T P^T over one key block.  The transposing read gives
+// lane (l/16, l%16) the four consecutive keys addressed by its 16-lane group
+// at column l%16: lane k of the group addresses key row 4(l/16) + k/4,
+// columns 4(k%4)..+3 of the 16-column d tile.  The 16 V^T fragments are
+// read in four groups of four, each group one group ahead of the MFMAs that
+// use it (at most 16 reads in flight, the LDS counter's range).
+__device__ __forceinline__ void pv_tile(const unsigned char* Vt, const bf16x8 (&pb)[2][2],
+                                        f32x4 (&o)[2][8], int G, int r16) {
+  bf16x8 a[2][8];
+  auto load = [&](int ks, int dt0) {
+    const int r0 = 32 * ks + 4 * G + (r16 >> 2);
+    const int lc = (r16 & 3) >> 1;
+    const int half = (r16 & 1) * 8;
+#pragma unroll
+    for (int dt = dt0; dt < dt0 + 4; ++dt) {
+      const int off = r0 * kRowBytes + (swz_v(r0, 2 * dt + lc) << 4) + half;
+      const s16x4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4*)(Vt + off));
+      const s16x4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4*)(Vt + off + 16 * kRowBytes));
+      const u32x2 y0 = __builtin_bit_cast(u32x2, x0), y1 = __builtin_bit_cast(u32x2, x1);
+      a[ks][dt] = __builtin_bit_cast(bf16x8, u32x4{y0[0], y0[1], y1[0], y1[1]});
+    }
+  };
+  auto mma = [&](int ks, int dt0) {
+#pragma unroll
+    for (int dt = dt0; dt < dt0 + 4; ++dt) {
+      o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][dt], pb[0][ks], o[0][dt], 0, 0, 0);
+      o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][dt], pb[1][ks], o[1][dt], 0, 0, 0);
+    }
+  };
+  load(0, 0);
+  load(0, 4);
+  __builtin_amdgcn_sched_barrier(0);
+  mma(0, 0);
+  load(1, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  mma(0, 4);
+  load(1, 4);
+  __builtin_amdgcn_sched_barrier(0);
+  mma(1, 0);
+  mma(1, 4);
+}
+
+template <int W>
+struct PrefillWave {
+  const unsigned char* qw;   // this wave's 32 query rows in LDS
+  f32x4 o[2][8];
+  f32x4 s[2][4];             // scores S^T of the current tile
+  float m_run[2], l_run[2];
+  float c;
+  int G, r16, qoff;
+
+  bf16x8 pb[2][2];           // probabilities of the last finished tile
+
+  // Matrix phase: O += P V of the previous tile, then S = K Q^T of the next.
+  __device__ __forceinline__ void matrix_phase(bool do_qk, const unsigned char* Kt, bool do_pv,
+                                               const unsigned char* Vp) {
+    if (do_pv) pv_tile(Vp, pb, o, G, r16);
+    if (do_qk) qk_tile(Kt, qw, s, G, r16);
+  }
+
+  // Vector phase: online softmax of the tile in s into pb.  DIAG masks keys
+  // after the query (the query block's own key block).
+  template <bool DIAG>
+  __device__ __forceinline__ void softmax_phase() {
+    if (DIAG) {
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        const int qrow = qoff + qt * 16 + r16;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (kt * 16 + 4 * G + i > qrow) s[qt][kt][i] = -INFINITY;
+      }
+    }
+    // Column max over the four 16-lane groups; the reference max only moves
+    // when a column's max grows by more than kLazy (log2 units): the
+    // probabilities then stay below 2^kLazy, far from FP32/BF16 overflow,
+    // and most tiles skip the rescale of O and l.  The final division by l
+    // uses the same reference, so the result is unchanged up to rounding.
+    float mt[2];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      float mx = __builtin_elementwise_maximum(
+          __builtin_elementwise_maximum(max4(s[qt][0]), max4(s[qt][1])),
+          __builtin_elementwise_maximum(max4(s[qt][2]), max4(s[qt][3])));
+      mt[qt] = max_xor16(max_xor32(mx)) * c;
+    }
+    if (__ballot(mt[0] > m_run[0] + kLazy || mt[1] > m_run[1] + kLazy)) {
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        const float m_new = fmaxf(m_run[qt], mt[qt]);
+        const float alpha =
+            __builtin_amdgcn_exp2f(m_run[qt] - (m_new == -INFINITY ? 0.f : m_new));
+        m_run[qt] = m_new;
+        l_run[qt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) o[qt][dt] *= alpha;
+      }
+    }
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      const float mu = m_run[qt] == -INFINITY ? 0.f : m_run[qt];
+      float ps[4];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          s[qt][kt][i] = __builtin_amdgcn_exp2f(fmaf(s[qt][kt][i], c, -mu));
+        ps[kt] = (s[qt][kt][0] + s[qt][kt][1]) + (s[qt][kt][2] + s[qt][kt][3]);
+      }
+      l_run[qt] += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+      // P^T as the B operand of the PV product: k entry 8(l/16)+i holds key
+      // 32 ks + 4(l/16) + i for i < 4 and key 32 ks + 16 + 4(l/16) + (i - 4)
+      // for i >= 4, matching the key order of the transposed V reads.
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        u32x4 w;
+        w[0] = pack_bf16(s[qt][2 * ks][0], s[qt][2 * ks][1]);
+        w[1] = pack_bf16(s[qt][2 * ks][2], s[qt][2 * ks][3]);
+        w[2] = pack_bf16(s[qt][2 * ks + 1][0], s[qt][2 * ks + 1][1]);
+        w[3] = pack_bf16(s[qt][2 * ks + 1][2], s[qt][2 * ks + 1][3]);
+        pb[qt][ks] = __builtin_bit_cast(bf16x8, w);
+      }
+    }
+  }
+
+  __device__ __forceinline__ void softmax_phase(bool diag) {
+    if (diag)
+      softmax_phase<true>();
+    else
+      softmax_phase<false>();
+  }
+};
 
 template <int W>
 __global__ __launch_bounds__(64 * W) void prefill_kernel(
@@ -88,7 +290,15 @@ __global__ __launch_bounds__(64 * W) void prefill_kernel(
     const uint16_t* __restrict__ v, int L, const int32_t* __restrict__ idx,
     const int32_t* __restrict__ count, int k_max, int batch, int h_q, int h_kv, int n_chunk,
     int n_pairs, float c, uint16_t* __restrict__ out, float* __restrict__ lse) {
-  __shared__ PrefillSmem sm;
+  // Each tile buffer is a variable of its own and every access names it at
+  // compile time (the loop below is unrolled by two), so the compiler can
+  // tell the direct global->LDS writes into one buffer from the reads of
+  // another and does not wait for the loads in flight before reading.
+  __shared__ __attribute__((aligned(16))) unsigned char sk0[kTileBytes], sk1[kTileBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char sv0[kTileBytes], sv1[kTileBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char sq[W][kQWaveBytes];
+  __shared__ int s_ids[kPrefillMaxIds];
+  __shared__ int s_n_local, s_has_diag;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // Workgroups of one (sequence, query block, KV head) pair differ by a
   // multiple of 8 in their id, so they are dispatched to the same XCD and
@@ -101,179 +311,141 @@ __global__ __launch_bounds__(64 * W) void prefill_kernel(
   const int b = rank % batch, qb = nqb - 1 - rank / batch;
   const int row = b * nqb + qb;
   const int h = g * (h_q / h_kv) + chunk * (W / 2) + (wave >> 1);
-  const int qoff = (wave & 1) * 32;
-  const int G = lane >> 4, r16 = lane & 15;
 
-  // Selected key blocks that exist for this query block (0 <= id <= qb), in
-  // list order, compacted into LDS.
+  // Selected key blocks that exist for this query block: ids in [0, qb) in
+  // list order, then the query block's own block qb (the only one that needs
+  // the causal mask) last if it was selected.
   if (wave == 0) {
     const int n_e = min(max(count[row], 0), k_max);
     const int32_t* ids_row = idx + (int64_t)row * k_max;
     int n = 0;
+    bool diag = false;
     for (int base = 0; base < n_e; base += kWave) {
       const int e = base + lane;
       const int j = e < n_e ? ids_row[e] : -1;
-      const bool ok = j >= 0 && j <= qb;
+      const bool ok = j >= 0 && j < qb;
       const uint64_t m = __ballot(ok);
       const int pos = n + __popcll(m & ((1ull << lane) - 1ull));
-      if (ok && pos < kPrefillMaxIds) sm.ids[pos] = j;
+      if (ok && pos < kPrefillMaxIds) s_ids[pos] = j;
       n += __popcll(m);
+      diag = diag || __ballot(j == qb) != 0;
     }
-    if (lane == 0) sm.n_local = min(n, kPrefillMaxIds);
+    if (lane == 0) {
+      n = min(n, kPrefillMaxIds - 1);
+      if (diag) s_ids[n++] = qb;
+      s_n_local = n;
+      s_has_diag = diag;
+    }
   }
 
-  // Q^T fragments (B operand): lane holds Q[row 16 qt + l%16][32 ks + 8(l/16) ..+7].
-  const uint16_t* qh = q + ((int64_t)(b * h_q + h) * L + qb * kBlk + qoff) * kD;
-  bf16x8 qf[2][4];
+  PrefillWave<W> wv;
+  wv.G = lane >> 4;
+  wv.r16 = lane & 15;
+  wv.qoff = (wave & 1) * 32;
+  wv.c = c;
+  // The wave's 32 query rows go to LDS (same chunk swizzle as K); the QK
+  // product reads them as the B operand: lane holds Q[16 qt + l%16][32 ks +
+  // 8(l/16) ..+7].
+  wv.qw = sq[wave];
+  {
+    const uint16_t* qh = q + ((int64_t)(b * h_q + h) * L + qb * kBlk + wv.qoff) * kD;
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt)
+    for (int u = 0; u < kQWaveBytes / (kWave * 16); ++u) {
+      const int p = u * kWave + lane;
+      const int r = p >> 4, lc = swz_k(r, p & 15);
+      __builtin_amdgcn_global_load_lds(qh + r * kD + lc * 8,
+                                       (lds_void*)(sq[wave] + u * kWave * 16), 16, 0, 0);
+    }
+  }
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-      qf[qt][ks] = __builtin_bit_cast(
-          bf16x8, *reinterpret_cast<const u32x4*>(qh + (qt * 16 + r16) * kD + ks * 32 + 8 * G));
+  for (int qt = 0; qt < 2; ++qt) {
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) wv.o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    wv.m_run[qt] = -INFINITY;
+    wv.l_run[qt] = 0.f;
+  }
 
   const uint16_t* kg = k + (int64_t)(b * h_kv + g) * L * kD;
   const uint16_t* vg = v + (int64_t)(b * h_kv + g) * L * kD;
+  auto blk = [](const uint16_t* base, int j) { return base + (int64_t)j * kBlk * kD; };
 
-  f32x4 o[2][8];
-#pragma unroll
-  for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
-
+  // Ping-pong schedule.  The waves form two groups, 0..W/2-1 and W/2..W-1,
+  // so the two waves sharing a SIMD belong to different groups.  Time is cut
+  // into half periods separated by workgroup barriers; in each, one group
+  // runs its matrix phase (P V of tile t-1, then S of tile t) while the
+  // other runs its vector phase (softmax), so MFMA work of one wave overlaps
+  // VALU work of the other.  Group 1 runs the same sequence one half period
+  // later.  Tile t (t = 0..n) takes half periods 2t and 2t+1:
+  //   2t:   loads K(t+1) -> K buffer (t+1)%2, V(t) -> V buffer t%2;
+  //         group 0 matrix(t), group 1 softmax(t-1)
+  //   2t+1: group 0 softmax(t), group 1 matrix(t); loads complete.
+  // Matrix(t) reads K buffer t%2 and V buffer (t-1)%2, never a buffer a load
+  // in flight writes to.  Buffer parity is a compile-time constant (the loop
+  // is unrolled by two, each buffer its own variable), which lets the
+  // compiler skip waiting on the loads before its LDS reads.
   __syncthreads();
-  const int n_local = sm.n_local;
-  if (n_local > 0) {
-    const int j0 = sm.ids[0];
-    stage_tile<W, true>(kg + (int64_t)j0 * kBlk * kD, sm.k[0], wave, lane);
-    stage_tile<W, false>(vg + (int64_t)j0 * kBlk * kD, sm.v[0], wave, lane);
-  }
+  const int n_local = s_n_local;
+  const bool has_diag = s_has_diag;
+  const bool grp1 = wave >= W / 2;
+  if (n_local > 0) stage_tile<W, true>(blk(kg, s_ids[0]), sk0, wave, lane);
   wait_vm();
   __syncthreads();
-
-  for (int t = 0; t < n_local; ++t) {
-    const int buf = t & 1;
-    const int j = sm.ids[t];
-    if (t + 1 < n_local) {
-      const int jn = sm.ids[t + 1];
-      stage_tile<W, true>(kg + (int64_t)jn * kBlk * kD, sm.k[buf ^ 1], wave, lane);
-      stage_tile<W, false>(vg + (int64_t)jn * kBlk * kD, sm.v[buf ^ 1], wave, lane);
+  auto tile = [&](auto parity, int t) {
+    constexpr int P = decltype(parity)::value;
+    unsigned char* kcur = P ? sk1 : sk0;
+    unsigned char* knext = P ? sk0 : sk1;
+    unsigned char* vcur = P ? sv1 : sv0;
+    unsigned char* vprev = P ? sv0 : sv1;
+    const bool do_qk = t < n_local, do_pv = t >= 1;
+    // The two groups run separate straight-line paths (the barrier counts
+    // match: one mid-period barrier and one end-of-period barrier each), so
+    // the compiler sees that group 1 never has a direct-to-LDS load in
+    // flight; a wave with one in flight only gets full LDS waits, which
+    // would serialise its matrix phase.  Group 0 therefore issues all tile
+    // loads, right after its own LDS reads.
+    if (!grp1) {
+      wv.matrix_phase(do_qk, kcur, do_pv, vprev);
+      if (t + 1 < n_local) stage_tile<W / 2, true>(blk(kg, s_ids[t + 1]), knext, wave, lane);
+      if (t < n_local) stage_tile<W / 2, false>(blk(vg, s_ids[t]), vcur, wave, lane);
+      // Phase switch only: no LDS data changes hands here, so no memory
+      // fence (a fence would also wait for the tile loads in flight).
+      __builtin_amdgcn_s_barrier();
+      if (do_qk) wv.softmax_phase(has_diag && t + 1 == n_local);
+      wait_vm();
+      __syncthreads();
+    } else {
+      if (do_pv) wv.softmax_phase(has_diag && t == n_local);
+      __builtin_amdgcn_s_barrier();
+      wv.matrix_phase(do_qk, kcur, do_pv, vprev);
+      __syncthreads();
     }
-    const unsigned char* Kt = sm.k[buf];
-    const unsigned char* Vt = sm.v[buf];
-
-    // S^T[key][query] for 4 key tiles x 2 query tiles.
-    f32x4 s[2][4];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-      s[0][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      s[1][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int r = kt * 16 + r16;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8 a = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(Kt + r * kRowBytes +
-                                                    (swz_k(r, ks * 4 + G) << 4)));
-        s[0][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][ks], s[0][kt], 0, 0, 0);
-        s[1][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][ks], s[1][kt], 0, 0, 0);
-      }
+  };
+  if (n_local > 0) {
+    for (int t = 0;; t += 2) {
+      tile(std::integral_constant<int, 0>(), t);
+      if (t + 1 > n_local) break;
+      tile(std::integral_constant<int, 1>(), t + 1);
+      if (t + 2 > n_local) break;
     }
-
-    // Online softmax per query column; P^T packed as the B operand of the
-    // PV product: k entry 8(l/16)+i <-> key 32 ks + 4(l/16) + i for i < 4 and
-    // key 32 ks + 16 + 4(l/16) + (i - 4) for i >= 4.
-    bf16x8 pb[2][2];
-    const bool diag = j == qb;
-#pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
-      if (diag) {
-        const int qrow = qoff + qt * 16 + r16;
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (kt * 16 + 4 * G + i > qrow) s[qt][kt][i] = -INFINITY;
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-        mx = fmaxf(mx, fmaxf(fmaxf(s[qt][kt][0], s[qt][kt][1]),
-                             fmaxf(s[qt][kt][2], s[qt][kt][3])));
-      mx = fmaxf(mx, xor_f(mx, 16));
-      mx = fmaxf(mx, xor_f(mx, 32));
-      const float m_new = fmaxf(m_run[qt], mx * c);
-      const float mu = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run[qt] - mu);
-      m_run[qt] = m_new;
-      float ps = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[qt][kt][i], c, -mu));
-          s[qt][kt][i] = p;
-          ps += p;
-        }
-      l_run[qt] = l_run[qt] * alpha + ps;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) o[qt][dt] *= alpha;
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        u32x4 w;
-        w[0] = pack_bf16(s[qt][2 * ks][0], s[qt][2 * ks][1]);
-        w[1] = pack_bf16(s[qt][2 * ks][2], s[qt][2 * ks][3]);
-        w[2] = pack_bf16(s[qt][2 * ks + 1][0], s[qt][2 * ks + 1][1]);
-        w[3] = pack_bf16(s[qt][2 * ks + 1][2], s[qt][2 * ks + 1][3]);
-        pb[qt][ks] = __builtin_bit_cast(bf16x8, w);
-      }
-    }
-
-    // O^T[d][query] += V^T P^T.  The transposing read gives lane (l/16, l%16)
-    // the four consecutive keys addressed by its 16-lane group, at column
-    // l%16: lane k of the group addresses key row 4(l/16) + k/4, columns
-    // 4(k%4)..+3 of the 16-column d tile.
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int r0 = 32 * ks + 4 * G + (r16 >> 2);
-      const int lc = ((r16 & 3) >> 1);  // + 2 dt
-      const int half = (r16 & 1) * 8;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        const int off = r0 * kRowBytes + (swz_v(r0, 2 * dt + lc) << 4) + half;
-        const s16x4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4*)(Vt + off));
-        const s16x4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4*)(Vt + off + 16 * kRowBytes));
-        const u32x2 y0 = __builtin_bit_cast(u32x2, x0), y1 = __builtin_bit_cast(u32x2, x1);
-        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{y0[0], y0[1], y1[0], y1[1]});
-        o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[0][ks], o[0][dt], 0, 0, 0);
-        o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[1][ks], o[1][dt], 0, 0, 0);
-      }
-    }
-    wait_vm();
-    __syncthreads();
   }
 
   // Normalise and store: lane holds O^T[16 dt + 4(l/16) + i][query l%16].
 #pragma unroll
   for (int qt = 0; qt < 2; ++qt) {
-    float lt = l_run[qt];
-    lt += xor_f(lt, 16);
-    lt += xor_f(lt, 32);
+    const float lt = sum_xor16(sum_xor32(wv.l_run[qt]));
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    const int qpos = qb * kBlk + qoff + qt * 16 + r16;
+    const int qpos = qb * kBlk + wv.qoff + qt * 16 + wv.r16;
     uint16_t* orow = out + ((int64_t)(b * h_q + h) * L + qpos) * kD;
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
       u32x2 w;
-      w[0] = pack_bf16(o[qt][dt][0] * inv, o[qt][dt][1] * inv);
-      w[1] = pack_bf16(o[qt][dt][2] * inv, o[qt][dt][3] * inv);
-      *reinterpret_cast<u32x2*>(orow + dt * 16 + 4 * G) = w;
+      w[0] = pack_bf16(wv.o[qt][dt][0] * inv, wv.o[qt][dt][1] * inv);
+      w[1] = pack_bf16(wv.o[qt][dt][2] * inv, wv.o[qt][dt][3] * inv);
+      *reinterpret_cast<u32x2*>(orow + dt * 16 + 4 * wv.G) = w;
     }
-    if (lse && G == 0)
+    if (lse && wv.G == 0)
       lse[(int64_t)(b * h_q + h) * L + qpos] =
-          lt > 0.f ? (m_run[qt] + __log2f(lt)) * kLn2 : -INFINITY;
+          lt > 0.f ? (wv.m_run[qt] + __log2f(lt)) * kLn2 : -INFINITY;
   }
 }
 
