@@ -5,8 +5,9 @@
  *   spot_selector_score  -> block scores of every KV block       (Section 2.1)
  *   spot_select_blocks   -> dual top-p / top-K block set          (Section 2.3)
  *   spot_sparse_decode   -> GQA attention over the chosen blocks  (Section 2)
- * with spot_dense_decode as the full-attention baseline and
- * spot_sparse_prefill as the block-sparse causal prefill over query blocks.
+ * with spot_decode_step running all three for every sequence in one launch,
+ * spot_dense_decode as the full-attention baseline and spot_sparse_prefill
+ * as the block-sparse causal prefill over query blocks.
  *
  * Conventions shared by every entry point:
  *  - Pointers named as device arrays are caller-owned device memory; the
@@ -161,6 +162,50 @@ spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
                                int k_max, int batch, int h_q, int h_kv, int d, int l_cap,
                                float sm_scale, void *out, float *lse, void *ws, size_t ws_bytes,
                                void *stream);
+
+/*
+ * spot_decode_step -- one decode step of the whole method for every sequence:
+ * spot_selector_score (rows = batch, one query row per sequence, nblk =
+ * l_cap / 64), spot_select_blocks on those scores, then spot_sparse_decode
+ * on the selected blocks (Section 2: score every KV block, select by the
+ * dual top-p / top-K rule with sink and recency reserved, attend to the
+ * selected blocks only).  The arguments mean exactly what they mean in those
+ * three calls, and the outputs (scores, idx, count, nuc_mass, out, lse) are
+ * the ones they would produce.
+ *
+ * When h_q == 4 * h_kv, nblk <= 4096 and min(k_max, nblk) <= 512, the three
+ * stages run as one launch whose grid fits the device at once: one
+ * workgroup per sequence selects its blocks as soon as the sequence's
+ * scores are in, and the attention workgroups start as soon as that
+ * selection is published, with no kernel boundary in between (hand-offs
+ * through flags in the workspace; every wait is bounded in time).  Otherwise
+ * (or when no such grid fits) the three stages are launched one after the
+ * other on `stream`.  Either way the results are deterministic; the fused
+ * path may split the attention over fewer workgroups when fewer fit, which
+ * changes the FP32 summation order (not the block set).
+ *
+ *  scores   device float [batch, nblk]          (output)
+ *  idx      device int32 [batch, k_max]         (output)
+ *  count    device int32 [batch]                (output)
+ *  nuc_mass device float [batch] or NULL        (output)
+ *  out, lse as spot_sparse_decode               (output; lse may be NULL)
+ *  ws       device, spot_decode_step_workspace_bytes(batch, h_q, h_kv, d,
+ *           k_max) bytes: the decode partials and counters laid out as for
+ *           spot_sparse_decode, then 66 flags per sequence.  It must
+ *           be zero-filled before its first use; every call leaves it ready
+ *           for the next one (all its counters return to zero).  Calls that
+ *           share a workspace must not overlap in time.
+ */
+size_t spot_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max);
+
+spot_status spot_decode_step(const void *q_sel, const float *w, const void *k_sel,
+                             const void *k_scale, int kfmt, int h_s, int d_s,
+                             const int32_t *n_valid, float top_p, int k_max, int k_min,
+                             int n_sink, int n_recent, const void *q, const void *k,
+                             const void *v, const int32_t *seq_len, int batch, int h_q,
+                             int h_kv, int d, int l_cap, float sm_scale, float *scores,
+                             int32_t *idx, int32_t *count, float *nuc_mass, void *out,
+                             float *lse, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * spot_dense_decode -- the dense decode baseline: spot_sparse_decode with

@@ -22,7 +22,8 @@ BUILD = os.path.join(ROOT, "_build")
 SO = os.path.join(PKG, "libspot.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "score.hip", "select.hip", "decode.hip", "prefill.hip", "probe.hip"]
+SOURCES = ["api.hip", "score.hip", "select.hip", "decode.hip", "step.hip", "prefill.hip",
+           "probe.hip"]
 
 HIPCC_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

@@ -111,6 +111,57 @@ spot_status spot_dense_decode(const void* q, const void* k, const void* v,
                                 l_cap, sm_scale, out, lse, ws, static_cast<hipStream_t>(stream)));
 }
 
+size_t spot_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max) {
+  if (batch < 1 || h_q < 1 || h_kv < 1 || d < 1 || k_max < 1) return 0;
+  return step_workspace_bytes(batch, h_q, h_kv, d, k_max);
+}
+
+spot_status spot_decode_step(const void* q_sel, const float* w, const void* k_sel,
+                             const void* k_scale, int kfmt, int h_s, int d_s,
+                             const int32_t* n_valid, float top_p, int k_max, int k_min,
+                             int n_sink, int n_recent, const void* q, const void* k,
+                             const void* v, const int32_t* seq_len, int batch, int h_q,
+                             int h_kv, int d, int l_cap, float sm_scale, float* scores,
+                             int32_t* idx, int32_t* count, float* nuc_mass, void* out,
+                             float* lse, void* ws, size_t ws_bytes, void* stream) {
+  spot_status st = check_decode(q, k, v, seq_len, out, batch, h_q, h_kv, d, l_cap);
+  if (st != SPOT_OK) return st;
+  if (!q_sel || !w || !k_sel || !scores || !idx || !count) return SPOT_ERR_NULL;
+  if (kfmt != SPOT_KFMT_BF16 && kfmt != SPOT_KFMT_INT4_G32 && kfmt != SPOT_KFMT_MXFP4_G32)
+    return SPOT_ERR_UNSUPPORTED;
+  if (kfmt != SPOT_KFMT_BF16 && !k_scale) return SPOT_ERR_NULL;
+  if (h_s < 1 || d_s < 1) return SPOT_ERR_SHAPE;
+  if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
+  if (l_cap == 0) return SPOT_ERR_SHAPE;
+  if (top_p != top_p || k_max < 1 || k_min > k_max || n_sink < 0 || n_recent < 0 ||
+      k_max < n_sink + n_recent)
+    return SPOT_ERR_RULE;
+  const int nblk = l_cap / kBlk;
+  if (nblk > 16384 || k_max > 4096) return SPOT_ERR_UNSUPPORTED;
+  if (batch == 0) return SPOT_OK;
+  if (!ws || ws_bytes < step_workspace_bytes(batch, h_q, h_kv, d, k_max))
+    return SPOT_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (step_fusable(h_q, h_kv, nblk, k_max)) {
+    const hipError_t e = launch_decode_step(q_sel, w, k_sel, k_scale, kfmt, d_s, n_valid, top_p,
+                                            k_max, k_min, n_sink, n_recent, q, k, v, seq_len,
+                                            batch, h_q, h_kv, l_cap, sm_scale, scores, idx,
+                                            count, nuc_mass, out, lse, ws, s);
+    if (e == hipSuccess) return SPOT_OK;
+    if (e != hipErrorCooperativeLaunchTooLarge) return SPOT_ERR_HIP;
+    (void)hipGetLastError();  // clear the refused launch; run the stages separately
+  }
+  hipError_t e = launch_selector_score(q_sel, w, k_sel, k_scale, kfmt, batch, 1, nblk, h_s, d_s,
+                                       n_valid, scores, s);
+  if (e == hipSuccess)
+    e = launch_select_blocks(scores, batch, nblk, n_valid, top_p, k_max, k_min, n_sink,
+                             n_recent, idx, count, nuc_mass, s);
+  if (e == hipSuccess)
+    e = launch_decode(false, q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, l_cap,
+                      sm_scale, out, lse, ws, s);
+  return from_hip(e);
+}
+
 spot_status spot_sparse_prefill(const void* q, const void* k, const void* v, int L,
                                 const int32_t* idx, const int32_t* count, int k_max, int batch,
                                 int h_q, int h_kv, int d, float sm_scale, void* out, float* lse,

@@ -1,15 +1,6 @@
-// Selector block scoring (paper Section 2.1): for each query row r and key
-// block j,  scores[r, j] = sum_h w[r,h] * ReLU(q_sel[r,h,:] . kbar[seq(r), j, h, :]).
-//
-// The pooled key of one block is h_s * d_s = 512 elements.  One wavefront
-// covers a whole block with one load per lane: lane l owns elements
-// 8l .. 8l+7 (BF16: 16 bytes; 4-bit formats: 4 bytes of codes plus the group
-// scale of its 32-element group), so consecutive lanes read consecutive
-// bytes.  The head dot products are reduced over the d_s/8 lanes of a head,
-// passed through ReLU and weighted, then summed over heads -- all with a fixed
-// butterfly so the result is deterministic.  Each wave handles kUnroll
-// consecutive blocks with all their loads issued before any arithmetic.
-#include "spot_internal.h"
+// Selector block scoring kernel (paper Section 2.1); the per-wavefront core
+// is in score_core.h.  Each wave handles kUnroll consecutive blocks.
+#include "score_core.h"
 
 namespace spot {
 namespace {
@@ -18,81 +9,8 @@ constexpr int kUnroll = 8;          // blocks per wavefront
 constexpr int kWavesPerWG = 4;
 constexpr int kBlocksPerWG = kUnroll * kWavesPerWG;
 
-// FP16 bits -> float (IEEE binary16, subnormals exact).
-__device__ __forceinline__ float f16_to_f32(uint16_t h) {
-  return (float)__builtin_bit_cast(_Float16, h);
-}
-
-// E2M1 magnitude code (0..7) -> float: 0, .5, 1, 1.5, 2, 3, 4, 6.
-__device__ __forceinline__ float e2m1_to_f32(uint32_t c) {
-  const uint32_t e = (c >> 1) & 3u, m = c & 1u;
-  // e == 0: subnormal 0 or 0.5; otherwise 2^(e-1) * (1 + m/2).
-  uint32_t bits = e ? (((e + 126u) << 23) | (m << 22)) : (m ? 0x3f000000u : 0u);
-  bits |= (c & 8u) << 28;  // sign
-  return __uint_as_float(bits);
-}
-
-// E8M0 -> 2^(e-127) as float (e = 0 gives the subnormal 2^-127).
-__device__ __forceinline__ float e8m0_to_f32(uint32_t e) {
-  return e ? __uint_as_float(e << 23) : __uint_as_float(0x00400000u);
-}
-
-template <int KFMT>
-struct KeyLoad;
-
-// BF16: 16 bytes per lane.
-template <>
-struct KeyLoad<SPOT_KFMT_BF16> {
-  uint4 raw;
-  __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t*, size_t blk, int lane) {
-    raw = *reinterpret_cast<const uint4*>(kb + blk * 1024 + lane * 16);
-  }
-  __device__ __forceinline__ float dot(const uint4& qraw, const float*) const {
-    float a = dot2_bf16(qraw.x, raw.x, 0.f);
-    a = dot2_bf16(qraw.y, raw.y, a);
-    a = dot2_bf16(qraw.z, raw.z, a);
-    return dot2_bf16(qraw.w, raw.w, a);
-  }
-};
-
-// INT4: 4 bytes of codes (element 2i in the low nibble) and one FP16 scale.
-template <>
-struct KeyLoad<SPOT_KFMT_INT4_G32> {
-  uint32_t codes;
-  uint16_t scale;
-  __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t* ks, size_t blk, int lane) {
-    codes = *reinterpret_cast<const uint32_t*>(kb + blk * 256 + lane * 4);
-    scale = *reinterpret_cast<const uint16_t*>(ks + (blk * 16 + (lane >> 2)) * 2);
-  }
-  __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
-    float a = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int code = (int)(codes << (28 - 4 * i)) >> 28;  // sign-extend nibble i
-      a = fmaf(qf[i], (float)code, a);
-    }
-    return a * f16_to_f32(scale);
-  }
-};
-
-// MXFP4: 4 bytes of E2M1 codes and one E8M0 scale.
-template <>
-struct KeyLoad<SPOT_KFMT_MXFP4_G32> {
-  uint32_t codes;
-  uint8_t scale;
-  __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t* ks, size_t blk, int lane) {
-    codes = *reinterpret_cast<const uint32_t*>(kb + blk * 256 + lane * 4);
-    scale = ks[blk * 16 + (lane >> 2)];
-  }
-  __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
-    float a = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) a = fmaf(qf[i], e2m1_to_f32((codes >> (4 * i)) & 15u), a);
-    return a * e8m0_to_f32(scale);
-  }
-};
-
-// grid: x = row (n_seq * rows_per_seq), y = chunk of kBlocksPerWG blocks.
+// grid: x = row (n_seq * rows_per_seq), y = chunk of kBlocksPerWG blocks;
+// wave w scores kUnroll consecutive blocks.
 template <int KFMT, int LPH>
 __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__ q_sel,
                                                     const float* __restrict__ w,
@@ -101,44 +19,13 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
                                                     int rows_per_seq, int nblk,
                                                     const int32_t* __restrict__ n_valid,
                                                     float* __restrict__ scores) {
-  constexpr int kHeads = 64 / LPH;
   const int row = blockIdx.x;
-  const int seq = row / rows_per_seq;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int j0 = blockIdx.y * kBlocksPerWG + wave * kUnroll;
+  const int j0 = blockIdx.y * kBlocksPerWG + (threadIdx.x >> 6) * kUnroll;
   int nv = n_valid ? n_valid[row] : nblk;
   nv = nv < 0 ? 0 : (nv > nblk ? nblk : nv);
   if (j0 >= nblk) return;
-
-  // This lane's 8 query elements (head lane / LPH, dims 8*(lane % LPH) ..).
-  const uint4 qraw = *reinterpret_cast<const uint4*>(q_sel + (size_t)row * 512 + lane * 8);
-  float qf[8];
-  qf[0] = bf16_lo(qraw.x); qf[1] = bf16_hi(qraw.x);
-  qf[2] = bf16_lo(qraw.y); qf[3] = bf16_hi(qraw.y);
-  qf[4] = bf16_lo(qraw.z); qf[5] = bf16_hi(qraw.z);
-  qf[6] = bf16_lo(qraw.w); qf[7] = bf16_hi(qraw.w);
-  const float wh = w[(size_t)row * kHeads + lane / LPH];
-
-  KeyLoad<KFMT> key[kUnroll];
-#pragma unroll
-  for (int u = 0; u < kUnroll; ++u) {
-    const int j = j0 + u;
-    if (j < nv) key[u].load(k_sel, k_scale, (size_t)seq * nblk + j, lane);
-  }
-  float res = 0.f;
-#pragma unroll
-  for (int u = 0; u < kUnroll; ++u) {
-    float part = key[u].dot(qraw, qf);
-#pragma unroll
-    for (int off = 1; off < LPH; off <<= 1) part += __shfl_xor(part, off, 64);
-    float v = wh * fmaxf(part, 0.f);
-#pragma unroll
-    for (int off = LPH; off < 64; off <<= 1) v += __shfl_xor(v, off, 64);
-    if (lane == u) res = v;
-  }
-  const int j = j0 + lane;
-  if (lane < kUnroll && j < nblk) scores[(size_t)row * nblk + j] = j < nv ? res : -INFINITY;
+  score_blocks<KFMT, LPH, kUnroll, false>(q_sel, w, k_sel, k_scale, row, row / rows_per_seq,
+                                          nblk, nv, j0, nblk, scores, threadIdx.x & 63);
 }
 
 template <int KFMT>

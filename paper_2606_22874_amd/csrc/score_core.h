@@ -1,0 +1,140 @@
+// Selector scoring core shared by the stand-alone scoring kernel and the
+// fused decode step (paper Section 2.1):
+//   scores[r, j] = sum_h w[r,h] * ReLU(q_sel[r,h,:] . kbar[seq(r), j, h, :]).
+// The pooled key of one block is h_s * d_s = 512 elements.  One wavefront
+// covers a whole block with one load per lane: lane l owns elements
+// 8l .. 8l+7 (BF16: 16 bytes; 4-bit formats: 4 bytes of codes plus the group
+// scale of its 32-element group), so consecutive lanes read consecutive
+// bytes.  The head dot products are reduced over the LPH = d_s/8 lanes of a
+// head, passed through ReLU and weighted, then summed over heads -- all with
+// a fixed butterfly, so the result is deterministic.
+#pragma once
+
+#include "spot_internal.h"
+
+namespace spot {
+
+// FP16 bits -> float (IEEE binary16, subnormals exact).
+__device__ __forceinline__ float f16_to_f32(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
+
+// E2M1 magnitude code (0..7) -> float: 0, .5, 1, 1.5, 2, 3, 4, 6.
+__device__ __forceinline__ float e2m1_to_f32(uint32_t c) {
+  const uint32_t e = (c >> 1) & 3u, m = c & 1u;
+  // e == 0: subnormal 0 or 0.5; otherwise 2^(e-1) * (1 + m/2).
+  uint32_t bits = e ? (((e + 126u) << 23) | (m << 22)) : (m ? 0x3f000000u : 0u);
+  bits |= (c & 8u) << 28;  // sign
+  return __uint_as_float(bits);
+}
+
+// E8M0 -> 2^(e-127) as float (e = 0 gives the subnormal 2^-127).
+__device__ __forceinline__ float e8m0_to_f32(uint32_t e) {
+  return e ? __uint_as_float(e << 23) : __uint_as_float(0x00400000u);
+}
+
+template <int KFMT>
+struct KeyLoad;
+
+// BF16: 16 bytes per lane.
+template <>
+struct KeyLoad<SPOT_KFMT_BF16> {
+  uint4 raw;
+  __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t*, size_t blk, int lane) {
+    raw = *reinterpret_cast<const uint4*>(kb + blk * 1024 + lane * 16);
+  }
+  __device__ __forceinline__ float dot(const uint4& qraw, const float*) const {
+    float a = dot2_bf16(qraw.x, raw.x, 0.f);
+    a = dot2_bf16(qraw.y, raw.y, a);
+    a = dot2_bf16(qraw.z, raw.z, a);
+    return dot2_bf16(qraw.w, raw.w, a);
+  }
+};
+
+// INT4: 4 bytes of codes (element 2i in the low nibble) and one FP16 scale.
+template <>
+struct KeyLoad<SPOT_KFMT_INT4_G32> {
+  uint32_t codes;
+  uint16_t scale;
+  __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t* ks, size_t blk, int lane) {
+    codes = *reinterpret_cast<const uint32_t*>(kb + blk * 256 + lane * 4);
+    scale = *reinterpret_cast<const uint16_t*>(ks + (blk * 16 + (lane >> 2)) * 2);
+  }
+  __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
+    float a = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int code = (int)(codes << (28 - 4 * i)) >> 28;  // sign-extend nibble i
+      a = fmaf(qf[i], (float)code, a);
+    }
+    return a * f16_to_f32(scale);
+  }
+};
+
+// MXFP4: 4 bytes of E2M1 codes and one E8M0 scale.
+template <>
+struct KeyLoad<SPOT_KFMT_MXFP4_G32> {
+  uint32_t codes;
+  uint8_t scale;
+  __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t* ks, size_t blk, int lane) {
+    codes = *reinterpret_cast<const uint32_t*>(kb + blk * 256 + lane * 4);
+    scale = ks[blk * 16 + (lane >> 2)];
+  }
+  __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
+    float a = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) a = fmaf(qf[i], e2m1_to_f32((codes >> (4 * i)) & 15u), a);
+    return a * e8m0_to_f32(scale);
+  }
+};
+
+// One wavefront scores blocks j0 .. min(j0 + U, jend) - 1 of query row `row`
+// (sequence `seq`), all key loads issued before any arithmetic; blocks at or
+// past nv score -inf.  COH stores the scores at device scope (for readers in
+// other workgroups of the same launch).
+template <int KFMT, int LPH, int U, bool COH>
+__device__ __forceinline__ void score_blocks(const uint16_t* __restrict__ q_sel,
+                                             const float* __restrict__ w,
+                                             const uint8_t* __restrict__ k_sel,
+                                             const uint8_t* __restrict__ k_scale, int row,
+                                             int seq, int nblk, int nv, int j0, int jend,
+                                             float* __restrict__ scores, int lane) {
+  constexpr int kHeads = 64 / LPH;
+  // This lane's 8 query elements (head lane / LPH, dims 8*(lane % LPH) ..).
+  const uint4 qraw = *reinterpret_cast<const uint4*>(q_sel + (size_t)row * 512 + lane * 8);
+  float qf[8];
+  qf[0] = bf16_lo(qraw.x); qf[1] = bf16_hi(qraw.x);
+  qf[2] = bf16_lo(qraw.y); qf[3] = bf16_hi(qraw.y);
+  qf[4] = bf16_lo(qraw.z); qf[5] = bf16_hi(qraw.z);
+  qf[6] = bf16_lo(qraw.w); qf[7] = bf16_hi(qraw.w);
+  const float wh = w[(size_t)row * kHeads + lane / LPH];
+
+  KeyLoad<KFMT> key[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int j = j0 + u;
+    if (j < nv && j < jend) key[u].load(k_sel, k_scale, (size_t)seq * nblk + j, lane);
+  }
+  float res = 0.f;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    float part = key[u].dot(qraw, qf);
+#pragma unroll
+    for (int off = 1; off < LPH; off <<= 1) part += __shfl_xor(part, off, 64);
+    float v = wh * fmaxf(part, 0.f);
+#pragma unroll
+    for (int off = LPH; off < 64; off <<= 1) v += __shfl_xor(v, off, 64);
+    if (lane == u) res = v;
+  }
+  const int j = j0 + lane;
+  if (lane < U && j < jend) {
+    float* dst = scores + (size_t)row * nblk + j;
+    const float val = j < nv ? res : -INFINITY;
+    if constexpr (COH)
+      __hip_atomic_store(dst, val, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      *dst = val;
+  }
+}
+
+}  // namespace spot

@@ -1,36 +1,32 @@
 // Dual top-p / top-K block selection (paper Section 2.3, Eqs. select-topk,
 // select-nucleus and select-topp) with a cap k_max on the set size.
 //
-// Rows of up to 4096 blocks use the single-wavefront kernel further down.
-// Larger rows use one workgroup (256 threads) per row; thread t owns the EPT
-// consecutive block ids [t*EPT, (t+1)*EPT) in registers.  Per row:
+// Three kernels, chosen by row length and cap (one row per workgroup):
+//  * rows of up to 512 blocks: one wavefront (select_wave_kernel);
+//  * 513 .. 4096 blocks: one 256-thread workgroup (select_wg_kernel, its body
+//    in select_core.h, shared with the fused decode step);
+//  * longer rows or caps above 512: the 256-thread sort-based select_kernel.
+// All follow the same steps per row:
 //  1. reserved blocks (sink prefix, recency suffix) are set aside; the
 //     residual candidates get an order-preserving 32-bit key of their score;
 //  2. residual softmax statistics: max and Z = sum exp(s - max) with a fixed
 //     reduction tree (deterministic);
 //  3. only the best C = min(k_max - |R|, |B_res|) candidates can ever be
-//     chosen, so a fixed 4-pass 8-bit radix select finds the C-th largest key;
-//     equal keys at the threshold are taken in ascending block id;
-//  4. the C survivors are bitonic-sorted in LDS by (score desc, id asc), their
-//     probabilities prefix-summed in that order (fixed tree, FP32), and the
-//     nucleus length n is the first prefix reaching top_p * Z, then capped
-//     and floored by k_min;
+//     chosen; a radix select by count finds the C-th largest key, and equal
+//     keys at the threshold are taken in ascending block id;
+//  4. the C survivors are sorted by (score desc, id asc), their probabilities
+//     prefix-summed in that order (fixed tree, FP32), and the nucleus length
+//     n is the first prefix reaching top_p * Z, then capped and floored by
+//     k_min (when the survivors' total mass stays below top_p * Z the cap
+//     binds and no sort is needed);
 //  5. reserved + the first n survivors are written in ascending block id.
-#include "spot_internal.h"
+#include "select_core.h"
 
 namespace spot {
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-
-__device__ __forceinline__ uint32_t order_key(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ float order_key_inv(uint32_t k) {
-  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
-}
 
 struct Scratch {
   int wave_i[kWaves];
@@ -340,78 +336,6 @@ __global__ __launch_bounds__(kThreads) void select_kernel(
 //     first prefix reaching top_p * Z, then capped and floored by k_min; the
 //     chosen ids plus the reserved blocks are written in ascending order.
 
-// Value of lane (lane ^ m); m is a power of two and a compile-time constant
-// after unrolling.  Needs the full wave active.
-__device__ __forceinline__ uint32_t xor_lane(uint32_t x, int m) {
-  switch (m) {
-    case 1: return (uint32_t)dpp_i<kDppQuadXor1>((int)x);
-    case 2: return (uint32_t)dpp_i<kDppQuadXor2>((int)x);
-    case 4: {
-      const uint32_t up = (uint32_t)dpp_i<0x104>((int)x);  // row_shl:4, lane i <- i + 4
-      const uint32_t dn = (uint32_t)dpp_i<0x114>((int)x);  // row_shr:4, lane i <- i - 4
-      return (__lane_id() & 4) ? dn : up;
-    }
-    case 8: return (uint32_t)dpp_i<0x128>((int)x);          // row_ror:8 == xor 8
-    case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x401F);  // xor 16
-    default: return (uint32_t)__builtin_amdgcn_ds_bpermute((__lane_id() ^ 32) << 2, (int)x);
-  }
-}
-__device__ __forceinline__ uint64_t xor_lane64(uint64_t x, int m) {
-  const uint32_t lo = xor_lane((uint32_t)x, m), hi = xor_lane((uint32_t)(x >> 32), m);
-  return ((uint64_t)hi << 32) | lo;
-}
-
-// Inclusive float prefix sum over lanes (same tree as wave_incl_scan_i).
-__device__ __forceinline__ float wave_incl_scan_f(float x) {
-  const int lane = __lane_id();
-  x += dpp_f<0x111>(x);
-  x += dpp_f<0x112>(x);
-  x += dpp_f<0x114>(x);
-  x += dpp_f<0x118>(x);
-  const float r0 = readlane_f(x, 15), r1 = readlane_f(x, 31), r2 = readlane_f(x, 47);
-  const int row = lane >> 4;
-  if (row > 0) x += r0;
-  if (row > 1) x += r1;
-  if (row > 2) x += r2;
-  return x;
-}
-
-// Descending bitonic sort of 64 * SPL packed keys; slot i = lane * SPL + t.
-template <int SPL>
-__device__ __forceinline__ void bitonic_desc(uint64_t (&K)[SPL]) {
-  constexpr int P = 64 * SPL;
-  const int lane = __lane_id();
-#pragma unroll
-  for (int k = 2; k <= P; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      if (j < SPL) {
-#pragma unroll
-        for (int t = 0; t < SPL; ++t) {
-          const int u = t ^ j;
-          if (u > t) {
-            const bool up = (((lane * SPL + t) & k) == 0);
-            const uint64_t a = K[t], b = K[u];
-            const bool swap = up ? (a < b) : (a > b);
-            K[t] = swap ? b : a;
-            K[u] = swap ? a : b;
-          }
-        }
-      } else {
-        const int m = j / SPL;
-        const bool lower = (lane & m) == 0;
-#pragma unroll
-        for (int t = 0; t < SPL; ++t) {
-          const uint64_t o = xor_lane64(K[t], m);
-          const bool up = (((lane * SPL + t) & k) == 0);
-          const bool keep_max = up == lower;
-          K[t] = keep_max ? (K[t] > o ? K[t] : o) : (K[t] < o ? K[t] : o);
-        }
-      }
-    }
-  }
-}
-
 template <int EPT, int SPL>
 __global__ __launch_bounds__(64) void select_wave_kernel(
     const float* __restrict__ scores, int nblk, const int32_t* __restrict__ n_valid,
@@ -642,289 +566,21 @@ __global__ __launch_bounds__(64) void select_wave_kernel(
   }
 }
 
-// ---------------------------------------------------------------------------
-// Workgroup (4 waves) selection for rows of 513 .. 4096 blocks, cap <= 512.
-// Same algorithm as the single-wave kernel, with the element-wise phases
-// spread over 256 threads (EPT <= 16 consecutive ids each):
-//  * max and Z in one barrier: each wave reduces its own max m_w and
-//    z_w = sum exp(s - m_w); then m = max_w m_w, Z = sum_w z_w exp(m_w - m);
-//  * radix select by count as before (block histogram, wave 0 scans);
-//  * one packed (greater, equal) exclusive scan gives every survivor its
-//    compaction slot;
-//  * wave 0 finishes on the survivors.  When the cap binds (the survivors'
-//    mass stays below top_p * Z) every survivor is chosen and no sort is
-//    needed; otherwise it sorts them and cuts the prefix as before.
-constexpr int kSelWG = 256;
-
-// Exclusive prefix over the 256 threads in thread order; `total` = sum.
-__device__ __forceinline__ int wg_excl_scan(int v, int* red, int& total) {
-  const int lane = __lane_id(), wave = threadIdx.x >> 6;
-  const int incl = wave_incl_scan_i(v);
-  if (lane == 63) red[wave] = incl;
-  __syncthreads();
-  int base = 0;
-  total = 0;
-#pragma unroll
-  for (int w = 0; w < kSelWG / 64; ++w) {
-    const int t = red[w];
-    base += w < wave ? t : 0;
-    total += t;
-  }
-  __syncthreads();
-  return base + incl - v;
-}
-
+// Workgroup selection kernel: one 256-thread workgroup per row (rows of
+// 513 .. 4096 blocks, cap <= 512).
 template <int EPT, int SPL>
 __global__ __launch_bounds__(kSelWG) void select_wg_kernel(
     const float* __restrict__ scores, int nblk, const int32_t* __restrict__ n_valid,
     float top_p, int k_max, int k_min, int n_sink, int n_recent,
     int32_t* __restrict__ idx_out, int32_t* __restrict__ count_out,
     float* __restrict__ mass_out) {
-  constexpr int NT = kSelWG, NW = NT / 64;
-  constexpr int kMaxBlocks = NT * EPT;
-  constexpr int P = 64 * SPL;
-  constexpr float kLog2e = 1.4426950408889634f;
-  static_assert(32 % EPT == 0, "a thread's ids must sit in one bit word");
-  __shared__ float stage[kMaxBlocks];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t bits[kMaxBlocks / 32];
-  __shared__ uint64_t s_K[P];
-  __shared__ uint32_t red_u[NW][2];
-  __shared__ float red_f[NW];
-  __shared__ int red_i[NW];
-  __shared__ int bc[4];
-
+  __shared__ SelWgSmem<EPT, SPL> sm;
   const int row = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int nv = n_valid ? n_valid[row] : nblk;
   nv = nv < 0 ? 0 : (nv > nblk ? nblk : nv);
-  const int sink_end = min(n_sink, nv);
-  const int rec_start = max(0, nv - n_recent);
-  const int n_reserved = sink_end + (nv - rec_start) - max(0, sink_end - rec_start);
-  const int n_res = nv - n_reserved;
-  const int cap = min(k_max - n_reserved, n_res);
-
-  // 1. coalesced loads (all in flight), transposed through LDS
-  const float* srow = scores + (size_t)row * nblk;
-  float ld[EPT];
-#pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    const int j = e * NT + tid;
-    ld[e] = j < nv ? srow[j] : -INFINITY;
-  }
-#pragma unroll
-  for (int e = 0; e < EPT; ++e) stage[e * NT + tid] = ld[e];
-  for (int i = tid; i < kMaxBlocks / 32; i += NT) bits[i] = 0u;
-  __syncthreads();
-
-  const int j0 = tid * EPT;
-  uint32_t key[EPT];
-  float sv[EPT];
-  uint32_t resv = 0;
-  {
-    const int lo = max(sink_end - j0, 0), hi = min(rec_start - j0, EPT);
-    const int vend = min(nv - j0, EPT);
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      const bool c = e >= lo && e < hi;
-      sv[e] = stage[j0 + e];
-      key[e] = c ? order_key(sv[e]) : 0u;  // 0 marks "not a candidate"
-      resv |= (uint32_t)(e < vend && !c) << e;
-    }
-  }
-
-  float mass = 0.f;
-  if (cap > 0) {
-    // 2. max, min and Z with one barrier
-    uint32_t kmax = 0u, kmin = 0xffffffffu;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      kmax = max(kmax, key[e]);
-      if (key[e]) kmin = min(kmin, key[e]);
-    }
-    kmax = wave_max_u(kmax);
-    kmin = wave_min_u(kmin);
-    float zw = 0.f;
-    if (kmax) {
-      const float mw = order_key_inv(kmax);
-      float zl = 0.f;
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) zl += key[e] ? exp2f((sv[e] - mw) * kLog2e) : 0.f;
-      zw = wave_sum(zl);
-    }
-    if (lane == 0) {
-      red_u[wave][0] = kmax;
-      red_u[wave][1] = kmin;
-      red_f[wave] = zw;
-    }
-    __syncthreads();
-    kmax = 0u;
-    kmin = 0xffffffffu;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      kmax = max(kmax, red_u[w][0]);
-      kmin = min(kmin, red_u[w][1]);
-    }
-    const float m = order_key_inv(kmax);
-    float Z = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w)
-      if (red_u[w][0]) Z += red_f[w] * exp2f((order_key_inv(red_u[w][0]) - m) * kLog2e);
-
-    // 3. radix select by count: the cap-th largest key
-    uint32_t thr = 0u;  // cap == n_res: every candidate survives (keys > 0)
-    int need = cap;
-    if (cap < n_res) {
-      const uint32_t diff = kmin ^ kmax;
-      int shift = diff ? 32 - __builtin_clz(diff) : 0;  // low bits still to resolve
-      uint32_t prefix = shift >= 32 ? 0u : (kmax >> shift) << shift;
-      uint32_t pmask = shift >= 32 ? 0u : ~0u << shift;
-      while (shift > 0) {
-        const int width = shift < 8 ? shift : 8;
-        shift -= width;
-        const uint32_t dmask = (1u << width) - 1u;
-        hist[tid] = 0u;
-        __syncthreads();
-#pragma unroll
-        for (int e = 0; e < EPT; ++e)
-          if (key[e] && (key[e] & pmask) == prefix) atomicAdd(&hist[(key[e] >> shift) & dmask], 1u);
-        __syncthreads();
-        if (wave == 0) {
-          // lane l holds digits 255-4l .. 252-4l (descending)
-          int c[4], tot = 0;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            c[i] = (int)hist[255 - 4 * lane - i];
-            tot += c[i];
-          }
-          const int incl = wave_incl_scan_i(tot);
-          int before = incl - tot;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if (before < need && need <= before + c[i]) {
-              bc[0] = 255 - 4 * lane - i;
-              bc[1] = need - before;
-            }
-            before += c[i];
-          }
-        }
-        __syncthreads();
-        prefix |= (uint32_t)bc[0] << shift;
-        pmask |= dmask << shift;
-        need = bc[1];
-      }
-      thr = prefix;
-    }
-
-    // 4. survivors and their slots from one packed (greater, equal) scan
-    int n_gt = 0, n_eq = 0;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      n_gt += (key[e] && key[e] > thr) ? 1 : 0;
-      n_eq += (key[e] && key[e] == thr) ? 1 : 0;
-    }
-    int total;
-    const int pre = wg_excl_scan(n_gt | (n_eq << 16), red_i, total);
-    int gt_before = pre & 0xffff, eq_before = pre >> 16;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      if (!key[e]) continue;
-      const uint64_t K = ((uint64_t)key[e] << 32) | (uint64_t)(0xffffffffu - (uint32_t)(j0 + e));
-      if (key[e] > thr) {
-        const int pos = gt_before + min(eq_before, need);
-        if (pos < P) s_K[pos] = K;
-        ++gt_before;
-      } else if (key[e] == thr) {
-        if (eq_before < need && gt_before + eq_before < P) s_K[gt_before + eq_before] = K;
-        ++eq_before;
-      }
-    }
-    for (int i = cap + tid; i < P; i += NT) s_K[i] = 0ull;  // padding sorts last
-    __syncthreads();
-
-    // 5. wave 0 decides n and marks the chosen blocks
-    if (wave == 0) {
-      uint64_t K[SPL];
-      float ev[SPL];
-      float msum = 0.f;
-#pragma unroll
-      for (int t = 0; t < SPL; ++t) {
-        K[t] = s_K[lane * SPL + t];
-        const bool real = lane * SPL + t < cap;
-        ev[t] = real ? exp2f((order_key_inv((uint32_t)(K[t] >> 32)) - m) * kLog2e) : 0.f;
-        msum += ev[t];
-      }
-      msum = wave_sum(msum);
-      const float pz = top_p * Z;
-      int n;
-      bool sorted = false;
-      float cum[SPL];
-      auto sort_and_scan = [&]() {
-        bitonic_desc<SPL>(K);
-        float run = 0.f;
-#pragma unroll
-        for (int t = 0; t < SPL; ++t) {
-          const bool real = lane * SPL + t < cap;
-          run += real ? exp2f((order_key_inv((uint32_t)(K[t] >> 32)) - m) * kLog2e) : 0.f;
-          cum[t] = run;
-        }
-        const float base = wave_incl_scan_f(run) - run;
-#pragma unroll
-        for (int t = 0; t < SPL; ++t) cum[t] += base;
-        sorted = true;
-      };
-      if (top_p >= 1.f) {
-        n = cap;
-      } else if (top_p <= 0.f) {
-        n = 0;
-      } else if (msum < pz) {
-        n = cap;  // the cap binds before the nucleus reaches top_p
-      } else {
-        sort_and_scan();
-        int below = 0;
-#pragma unroll
-        for (int t = 0; t < SPL; ++t) below += (lane * SPL + t < cap && cum[t] < pz) ? 1 : 0;
-        n = min(cap, wave_sum_i(below) + 1);
-      }
-      if (n_reserved + n < k_min) n = min(k_min - n_reserved, cap);
-      if (n < cap && !sorted) sort_and_scan();
-      float mass_w = 0.f;
-      if (n == cap) {
-        mass_w = msum;
-      } else if (n > 0) {
-        const int ln = (n - 1) / SPL, tn = (n - 1) % SPL;
-        float mine = 0.f;
-#pragma unroll
-        for (int t = 0; t < SPL; ++t) mine = t == tn ? cum[t] : mine;
-        mass_w = readlane_f(mine, ln);
-      }
-#pragma unroll
-      for (int t = 0; t < SPL; ++t) {
-        if (lane * SPL + t < n) {
-          const int id = (int)(0xffffffffu - (uint32_t)K[t]);
-          atomicOr(&bits[id >> 5], 1u << (id & 31));
-        }
-      }
-      if (lane == 0) red_f[0] = n > 0 ? mass_w / Z : 0.f;
-    }
-    __syncthreads();
-    mass = red_f[0];
-  }
-
-  // 6. write S = reserved u chosen, ascending
-  uint32_t fin = resv;
-  fin |= (EPT == 32 ? bits[j0 >> 5] : (bits[j0 >> 5] >> (j0 & 31)) & ((1u << EPT) - 1u));
-  int total;
-  int pos = wg_excl_scan(__popc(fin), red_i, total);
-  int32_t* out = idx_out + (size_t)row * k_max;
-#pragma unroll
-  for (int e = 0; e < EPT; ++e)
-    if (((fin >> e) & 1u) && pos < k_max) out[pos++] = j0 + e;
-  for (int i = total + tid; i < k_max; i += NT) out[i] = -1;
-  if (tid == 0) {
-    count_out[row] = min(total, k_max);
-    if (mass_out) mass_out[row] = mass;
-  }
+  select_row_wg<EPT, SPL, false>(sm, scores + (size_t)row * nblk, nblk, nv, top_p, k_max, k_min,
+                                 n_sink, n_recent, idx_out + (size_t)row * k_max,
+                                 count_out + row, mass_out ? mass_out + row : nullptr);
 }
 
 }  // namespace

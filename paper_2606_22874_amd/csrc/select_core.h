@@ -1,0 +1,505 @@
+// Selection cores shared by the stand-alone selection kernels and the fused
+// decode step: order-preserving score keys, cross-lane exchanges, a
+// descending bitonic sort of packed keys held in registers, and the
+// workgroup (256-thread) selection of one row.
+#pragma once
+
+#include "spot_internal.h"
+
+namespace spot {
+
+__device__ __forceinline__ uint32_t order_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float order_key_inv(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+
+// Value of lane (lane ^ m); m is a power of two and a compile-time constant
+// after unrolling.  Needs the full wave active.
+__device__ __forceinline__ uint32_t xor_lane(uint32_t x, int m) {
+  switch (m) {
+    case 1: return (uint32_t)dpp_i<kDppQuadXor1>((int)x);
+    case 2: return (uint32_t)dpp_i<kDppQuadXor2>((int)x);
+    case 4: {
+      const uint32_t up = (uint32_t)dpp_i<0x104>((int)x);  // row_shl:4, lane i <- i + 4
+      const uint32_t dn = (uint32_t)dpp_i<0x114>((int)x);  // row_shr:4, lane i <- i - 4
+      return (__lane_id() & 4) ? dn : up;
+    }
+    case 8: return (uint32_t)dpp_i<0x128>((int)x);          // row_ror:8 == xor 8
+    case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x401F);  // xor 16
+    default: return (uint32_t)__builtin_amdgcn_ds_bpermute((__lane_id() ^ 32) << 2, (int)x);
+  }
+}
+__device__ __forceinline__ uint64_t xor_lane64(uint64_t x, int m) {
+  const uint32_t lo = xor_lane((uint32_t)x, m), hi = xor_lane((uint32_t)(x >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive float prefix sum over lanes (same tree as wave_incl_scan_i).
+__device__ __forceinline__ float wave_incl_scan_f(float x) {
+  const int lane = __lane_id();
+  x += dpp_f<0x111>(x);
+  x += dpp_f<0x112>(x);
+  x += dpp_f<0x114>(x);
+  x += dpp_f<0x118>(x);
+  const float r0 = readlane_f(x, 15), r1 = readlane_f(x, 31), r2 = readlane_f(x, 47);
+  const int row = lane >> 4;
+  if (row > 0) x += r0;
+  if (row > 1) x += r1;
+  if (row > 2) x += r2;
+  return x;
+}
+
+// Descending bitonic sort of 64 * SPL packed keys; slot i = lane * SPL + t.
+template <int SPL>
+__device__ __forceinline__ void bitonic_desc(uint64_t (&K)[SPL]) {
+  constexpr int P = 64 * SPL;
+  const int lane = __lane_id();
+#pragma unroll
+  for (int k = 2; k <= P; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (j < SPL) {
+#pragma unroll
+        for (int t = 0; t < SPL; ++t) {
+          const int u = t ^ j;
+          if (u > t) {
+            const bool up = (((lane * SPL + t) & k) == 0);
+            const uint64_t a = K[t], b = K[u];
+            const bool swap = up ? (a < b) : (a > b);
+            K[t] = swap ? b : a;
+            K[u] = swap ? a : b;
+          }
+        }
+      } else {
+        const int m = j / SPL;
+        const bool lower = (lane & m) == 0;
+#pragma unroll
+        for (int t = 0; t < SPL; ++t) {
+          const uint64_t o = xor_lane64(K[t], m);
+          const bool up = (((lane * SPL + t) & k) == 0);
+          const bool keep_max = up == lower;
+          K[t] = keep_max ? (K[t] > o ? K[t] : o) : (K[t] < o ? K[t] : o);
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Workgroup (4 waves) selection for rows of 513 .. 4096 blocks, cap <= 512.
+// Same algorithm as the single-wave kernel, with the element-wise phases
+// spread over 256 threads (EPT <= 16 consecutive ids each):
+//  * max and Z in one barrier: each wave reduces its own max m_w and
+//    z_w = sum exp(s - m_w); then m = max_w m_w, Z = sum_w z_w exp(m_w - m);
+//  * radix select by count as before (block histogram, wave 0 scans);
+//  * one packed (greater, equal) exclusive scan gives every survivor its
+//    compaction slot;
+//  * wave 0 finishes on the survivors.  When the cap binds (the survivors'
+//    mass stays below top_p * Z) every survivor is chosen and no sort is
+//    needed; otherwise it sorts them and cuts the prefix as before.
+constexpr int kSelWG = 256;
+
+// Exclusive prefix over the 256 threads in thread order; `total` = sum.
+__device__ __forceinline__ int wg_excl_scan(int v, int* red, int& total) {
+  const int lane = __lane_id(), wave = threadIdx.x >> 6;
+  const int incl = wave_incl_scan_i(v);
+  if (lane == 63) red[wave] = incl;
+  __syncthreads();
+  int base = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < kSelWG / 64; ++w) {
+    const int t = red[w];
+    base += w < wave ? t : 0;
+    total += t;
+  }
+  __syncthreads();
+  return base + incl - v;
+}
+
+
+// Coherent (device-scope) or plain global accesses.  The fused decode step
+// reads scores written by other workgroups of the same launch and publishes
+// its selection to them, so it bypasses the per-XCD L2 caches.
+template <bool COH>
+__device__ __forceinline__ float load_score(const float* p) {
+  if constexpr (COH)
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    return *p;
+}
+template <bool COH>
+__device__ __forceinline__ void store_i32(int32_t* p, int32_t v) {
+  if constexpr (COH)
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    *p = v;
+}
+template <bool COH>
+__device__ __forceinline__ void store_f32(float* p, float v) {
+  if constexpr (COH)
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    *p = v;
+}
+
+constexpr int kValBins = 2048;   // value bins of the threshold search
+
+#ifndef SPOT_SEL_TS
+#define SPOT_SEL_TS(i) ((void)0)
+#endif
+
+template <int EPT, int SPL>
+struct SelWgSmem {
+  uint32_t hist[kValBins];        // value-bin counts (the fallback radix uses 256)
+  uint64_t s_K[64 * SPL];         // threshold-bin members, then sorted survivors
+  uint32_t red_u[kSelWG / 64][2];
+  float red_f[kSelWG / 64][2];
+  int red_i[kSelWG / 64];
+  int bc[4];
+  uint64_t cut;
+  float cut_mass;
+};
+
+// Packed rank key: higher score first, then lower block id; unique per id.
+__device__ __forceinline__ uint64_t rank_key(uint32_t key, int id) {
+  return ((uint64_t)key << 32) | (uint64_t)(0xffffffffu - (uint32_t)id);
+}
+
+// Selection of one row by the whole 256-thread workgroup: srow holds the
+// row's scores (the first nv valid), out its k_max id slots.  Every thread of
+// the workgroup must call it.  Thread t owns the EPT consecutive ids
+// [t*EPT, (t+1)*EPT).  Steps (barrier rounds in brackets):
+//  1. load; order-preserving keys for the residual candidates; residual max
+//     M, min and Z = sum exp(s - M) from per-wave partials [1];
+//  2. when the cap C binds, the C-th best candidate (score desc, id asc):
+//     a histogram over 2048 equal-width value bins between the candidate min
+//     and max finds the bin holding it [1], a scan over the bins its rank
+//     inside the bin [2]; the bin's members are sorted exactly in one wave
+//     [2].  A bin with more members than fit the sort (heavy ties) falls back
+//     to an 8-bit radix select on the keys.  The result is one packed cut
+//     key: the survivors are the candidates whose packed key reaches it;
+//  3. the survivors' mass [1] decides: below top_p * Z the cap binds and the
+//     survivors are the answer; otherwise they are compacted [2], sorted in
+//     one wave by (score desc, id asc), prefix-summed, and the nucleus cut
+//     where the prefix first reaches top_p * Z (then floored by k_min) [1];
+//  4. reserved + chosen ids are written in ascending order [2].
+// Every reduction has a fixed order, so the result is deterministic.
+template <int EPT, int SPL, bool COH>
+__device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
+                                              const float* __restrict__ srow, int nblk, int nv,
+                                              float top_p, int k_max, int k_min, int n_sink,
+                                              int n_recent, int32_t* __restrict__ out,
+                                              int32_t* __restrict__ count_out,
+                                              float* __restrict__ mass_out) {
+  constexpr int NT = kSelWG, NW = NT / 64;
+  constexpr int P = 64 * SPL;
+  constexpr int BPT = kValBins / NT;   // value bins per thread in the scan
+  constexpr float kLog2e = 1.4426950408889634f;
+  static_assert(EPT <= 32, "a thread's ids must fit one bit word");
+  (void)nblk;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sink_end = min(n_sink, nv);
+  const int rec_start = max(0, nv - n_recent);
+  const int n_reserved = sink_end + (nv - rec_start) - max(0, sink_end - rec_start);
+  const int n_res = nv - n_reserved;
+  const int cap = min(k_max - n_reserved, n_res);
+  const int j0 = tid * EPT;
+
+  // 1. scores, keys (0 = not a candidate), M, min and Z
+  float sv[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int j = j0 + e;
+    sv[e] = j < nv ? load_score<COH>(srow + j) : -INFINITY;
+  }
+  SPOT_SEL_TS(0);
+  for (int i = tid; i < kValBins; i += NT) sm.hist[i] = 0u;
+  uint32_t key[EPT];
+  uint32_t resv = 0;
+  {
+    const int lo = max(sink_end - j0, 0), hi = min(rec_start - j0, EPT);
+    const int vend = min(nv - j0, EPT);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const bool c = e >= lo && e < hi;
+      key[e] = c ? order_key(sv[e]) : 0u;
+      resv |= (uint32_t)(e < vend && !c) << e;
+    }
+  }
+  SPOT_SEL_TS(1);
+  uint32_t kmax = 0u, kmin = 0xffffffffu;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    kmax = max(kmax, key[e]);
+    if (key[e]) kmin = min(kmin, key[e]);
+  }
+  kmax = wave_max_u(kmax);
+  kmin = wave_min_u(kmin);
+  {
+    float zl = 0.f;
+    if (kmax) {
+      const float mw = order_key_inv(kmax);
+#pragma unroll
+      for (int e = 0; e < EPT; ++e)
+        zl += key[e] ? __builtin_amdgcn_exp2f((sv[e] - mw) * kLog2e) : 0.f;
+    }
+    const float zw = wave_sum(zl);
+    if (lane == 0) {
+      sm.red_u[wave][0] = kmax;
+      sm.red_u[wave][1] = kmin;
+      sm.red_f[wave][0] = zw;
+    }
+  }
+  __syncthreads();
+  kmax = 0u;
+  kmin = 0xffffffffu;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    kmax = max(kmax, sm.red_u[w][0]);
+    kmin = min(kmin, sm.red_u[w][1]);
+  }
+  const float M = order_key_inv(kmax);
+  float Z = 0.f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w)
+    if (sm.red_u[w][0])
+      Z += sm.red_f[w][0] * __builtin_amdgcn_exp2f((order_key_inv(sm.red_u[w][0]) - M) * kLog2e);
+
+  SPOT_SEL_TS(2);
+  // 2. the cut: survivors are the candidates with rank_key >= k_thr
+  uint64_t k_thr = 1ull;                       // every candidate (cap == n_res)
+  if (cap <= 0) {
+    k_thr = ~0ull;
+  } else if (cap < n_res) {
+    const float vhi = M, vlo = order_key_inv(kmin);
+    const float span = vhi - vlo;
+    bool crowded = !(span > 0.f) || !(span < INFINITY);
+    if (!crowded) {
+      const float inv_w = (float)kValBins / span * 0.99999f;
+      int bin[EPT];
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        // clamped in float first (non-candidates may hold -inf or NaN)
+        bin[e] = (int)fminf((vhi - sv[e]) * inv_w, (float)(kValBins - 1));
+        if (key[e]) atomicAdd(&sm.hist[bin[e]], 1u);
+      }
+      __syncthreads();
+      // bins ascend as values descend; thread t scans bins [BPT t, BPT t + BPT)
+      int c[BPT], tot = 0;
+#pragma unroll
+      for (int i = 0; i < BPT; ++i) {
+        c[i] = (int)sm.hist[BPT * tid + i];
+        tot += c[i];
+      }
+      SPOT_SEL_TS(6);
+      const int incl = wave_incl_scan_i(tot);
+      if (lane == 63) sm.red_i[wave] = incl;
+      __syncthreads();
+      int before = incl - tot;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) before += w < wave ? sm.red_i[w] : 0;
+#pragma unroll
+      for (int i = 0; i < BPT; ++i) {
+        if (before < cap && cap <= before + c[i]) {
+          sm.bc[0] = BPT * tid + i;
+          sm.bc[1] = cap - before;
+          sm.bc[2] = c[i];
+          sm.bc[3] = 0;
+        }
+        before += c[i];
+      }
+      __syncthreads();
+      SPOT_SEL_TS(7);
+      const int b_star = sm.bc[0], need = sm.bc[1], in_bin = sm.bc[2];
+      crowded = in_bin > P;
+      if (!crowded) {
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+          if (key[e] && bin[e] == b_star) sm.s_K[atomicAdd(&sm.bc[3], 1)] = rank_key(key[e], j0 + e);
+        for (int i = in_bin + tid; i < P; i += NT) sm.s_K[i] = 0ull;
+        __syncthreads();
+      SPOT_SEL_TS(8);
+        if (wave == 0) {
+          uint64_t K[SPL];
+#pragma unroll
+          for (int t = 0; t < SPL; ++t) K[t] = sm.s_K[lane * SPL + t];
+          bitonic_desc<SPL>(K);
+          const int ln = (need - 1) / SPL, tn = (need - 1) % SPL;
+          uint64_t mine = 0ull;
+#pragma unroll
+          for (int t = 0; t < SPL; ++t) mine = t == tn ? K[t] : mine;
+          const uint32_t lo32 = __builtin_amdgcn_readlane((uint32_t)mine, ln);
+          const uint32_t hi32 = __builtin_amdgcn_readlane((uint32_t)(mine >> 32), ln);
+          if (lane == 0) sm.cut = ((uint64_t)hi32 << 32) | lo32;
+        }
+        __syncthreads();
+        k_thr = sm.cut;
+      }
+    }
+    if (crowded) {
+      // 8-bit radix select by count on the keys, from the highest bit where
+      // the candidates differ; equal keys at the threshold go to lower ids.
+      const uint32_t diff = kmin ^ kmax;
+      int shift = diff ? 32 - __builtin_clz(diff) : 0;
+      uint32_t prefix = shift >= 32 ? 0u : (kmax >> shift) << shift;
+      uint32_t pmask = shift >= 32 ? 0u : ~0u << shift;
+      int need = cap;
+      while (shift > 0) {
+        const int width = shift < 8 ? shift : 8;
+        shift -= width;
+        const uint32_t dmask = (1u << width) - 1u;
+        sm.hist[tid] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+          if (key[e] && (key[e] & pmask) == prefix)
+            atomicAdd(&sm.hist[(key[e] >> shift) & dmask], 1u);
+        __syncthreads();
+        if (wave == 0) {
+          int c[4], tot = 0;                   // lane l: digits 255-4l .. 252-4l
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            c[i] = (int)sm.hist[255 - 4 * lane - i];
+            tot += c[i];
+          }
+          const int incl = wave_incl_scan_i(tot);
+          int before = incl - tot;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (before < need && need <= before + c[i]) {
+              sm.bc[0] = 255 - 4 * lane - i;
+              sm.bc[1] = need - before;
+            }
+            before += c[i];
+          }
+        }
+        __syncthreads();
+        prefix |= (uint32_t)sm.bc[0] << shift;
+        pmask |= dmask << shift;
+        need = sm.bc[1];
+      }
+      // the need-th lowest id among the keys equal to the threshold
+      int n_eq = 0;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) n_eq += key[e] == prefix ? 1 : 0;
+      int total;
+      int eq_before = wg_excl_scan(n_eq, sm.red_i, total);
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        if (key[e] == prefix) {
+          if (++eq_before == need) sm.cut = rank_key(prefix, j0 + e);
+        }
+      }
+      __syncthreads();
+      k_thr = sm.cut;
+    }
+  }
+
+  SPOT_SEL_TS(3);
+  // 3. survivors, their mass, and the nucleus
+  uint32_t surv = 0u;
+  float ms = 0.f;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    if (key[e] && rank_key(key[e], j0 + e) >= k_thr) {
+      surv |= 1u << e;
+      ms += __builtin_amdgcn_exp2f((sv[e] - M) * kLog2e);
+    }
+  }
+  {
+    const float mw = wave_sum(ms);
+    if (lane == 0) sm.red_f[wave][1] = mw;
+  }
+  __syncthreads();
+  float msum = 0.f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) msum += sm.red_f[w][1];
+  const float pz = top_p * Z;
+  int n;                                  // -1: the nucleus ends before the cap
+  if (cap <= 0) n = 0;
+  else if (top_p >= 1.f) n = cap;
+  else if (top_p <= 0.f) n = 0;
+  else if (msum < pz) n = cap;           // the cap binds before the nucleus reaches top_p
+  else n = -1;
+  if (n >= 0 && n_reserved + n < k_min) n = min(k_min - n_reserved, cap);
+  uint64_t k_cut = n == 0 ? ~0ull : k_thr;
+  float mass = n > 0 && Z > 0.f ? msum / Z : 0.f;
+  if (n < 0 || (n > 0 && n < cap)) {
+    // survivors in rank order: compact, sort in wave 0, cut the prefix
+    int total;
+    int pos = wg_excl_scan(__popc(surv), sm.red_i, total);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+      if ((surv >> e) & 1u) sm.s_K[pos++] = rank_key(key[e], j0 + e);
+    for (int i = total + tid; i < P; i += NT) sm.s_K[i] = 0ull;   // padding sorts last
+    __syncthreads();
+    if (wave == 0) {
+      uint64_t K[SPL];
+#pragma unroll
+      for (int t = 0; t < SPL; ++t) K[t] = sm.s_K[lane * SPL + t];
+      bitonic_desc<SPL>(K);
+      float cum[SPL], run = 0.f;
+#pragma unroll
+      for (int t = 0; t < SPL; ++t) {
+        const bool real = lane * SPL + t < cap;
+        run += real ? __builtin_amdgcn_exp2f((order_key_inv((uint32_t)(K[t] >> 32)) - M) * kLog2e)
+                    : 0.f;
+        cum[t] = run;
+      }
+      const float base = wave_incl_scan_f(run) - run;
+#pragma unroll
+      for (int t = 0; t < SPL; ++t) cum[t] += base;
+      int nn = n;
+      if (nn < 0) {
+        int below = 0;
+#pragma unroll
+        for (int t = 0; t < SPL; ++t) below += (lane * SPL + t < cap && cum[t] < pz) ? 1 : 0;
+        nn = min(cap, wave_sum_i(below) + 1);
+        if (n_reserved + nn < k_min) nn = min(k_min - n_reserved, cap);
+      }
+      const int ln = (nn - 1) / SPL, tn = (nn - 1) % SPL;
+      uint64_t mk = 0ull;
+      float mc = 0.f;
+#pragma unroll
+      for (int t = 0; t < SPL; ++t) {
+        mk = t == tn ? K[t] : mk;
+        mc = t == tn ? cum[t] : mc;
+      }
+      const uint32_t lo32 = __builtin_amdgcn_readlane((uint32_t)mk, ln);
+      const uint32_t hi32 = __builtin_amdgcn_readlane((uint32_t)(mk >> 32), ln);
+      const float m_at = readlane_f(mc, ln);
+      if (lane == 0) {
+        sm.cut = ((uint64_t)hi32 << 32) | lo32;
+        sm.cut_mass = Z > 0.f ? m_at / Z : 0.f;
+      }
+    }
+    __syncthreads();
+    k_cut = sm.cut;
+    mass = sm.cut_mass;
+  }
+
+  SPOT_SEL_TS(4);
+  // 4. write S = reserved u chosen, ascending
+  uint32_t fin = resv;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e)
+    if (key[e] && rank_key(key[e], j0 + e) >= k_cut) fin |= 1u << e;
+  int total;
+  int pos = wg_excl_scan(__popc(fin), sm.red_i, total);
+#pragma unroll
+  for (int e = 0; e < EPT; ++e)
+    if (((fin >> e) & 1u) && pos < k_max) store_i32<COH>(out + pos++, j0 + e);
+  for (int i = total + tid; i < k_max; i += NT) store_i32<COH>(out + i, -1);
+  if (tid == 0) {
+    store_i32<COH>(count_out, min(total, k_max));
+    if (mass_out) store_f32<COH>(mass_out, mass);
+  }
+  SPOT_SEL_TS(5);
+}
+
+}  // namespace spot

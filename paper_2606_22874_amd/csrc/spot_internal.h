@@ -128,6 +128,15 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
 int decode_num_splits(int batch, int h_kv, int max_blocks, int group);
 size_t decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_blocks);
 
+size_t step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max);
+bool step_fusable(int h_q, int h_kv, int nblk, int k_max);
+hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_sel,
+                              const void* k_scale, int kfmt, int d_s, const int32_t* n_valid,
+                              float top_p, int k_max, int k_min, int n_sink, int n_recent,
+                              const void* q, const void* k, const void* v,
+                              const int32_t* seq_len, int batch, int h_q, int h_kv, int l_cap,
+                              float sm_scale, float* scores, int32_t* idx, int32_t* count,
+                              float* nuc_mass, void* out, float* lse, void* ws, hipStream_t s);
 hipError_t launch_decode(bool dense, const void* q, const void* k, const void* v,
                          const int32_t* seq_len, const int32_t* idx, const int32_t* count,
                          int k_max, int batch, int h_q, int h_kv, int l_cap, float sm_scale,

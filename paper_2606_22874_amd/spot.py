@@ -29,7 +29,8 @@ BLK = 64
 
 SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score", "spot_select_blocks",
            "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
-           "spot_sparse_prefill", "spot_probe_stream_read", "spot_probe_sink_words"]
+           "spot_sparse_prefill", "spot_decode_step_workspace_bytes", "spot_decode_step",
+           "spot_probe_stream_read", "spot_probe_sink_words"]
 
 
 class SpotError(RuntimeError):
@@ -66,11 +67,15 @@ def load(path: Optional[str] = None):
         L.spot_sparse_decode.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, P, P, P, Z, P]
         L.spot_dense_decode.argtypes = [P, P, P, P, I, I, I, I, I, F, P, P, P, Z, P]
         L.spot_sparse_prefill.argtypes = [P, P, P, I, P, P, I, I, I, I, I, F, P, P, P]
+        L.spot_decode_step_workspace_bytes.argtypes = [I, I, I, I, I]
+        L.spot_decode_step_workspace_bytes.restype = Z
+        L.spot_decode_step.argtypes = [P, P, P, P, I, I, I, P, F, I, I, I, I, P, P, P, P, I, I,
+                                       I, I, I, F, P, P, P, P, P, P, P, Z, P]
         L.spot_probe_stream_read.argtypes = [P, Z, P, P]
         L.spot_probe_stream_read.restype = ctypes.c_int32
         L.spot_probe_sink_words.restype = I
         for name in ("spot_selector_score", "spot_select_blocks", "spot_sparse_decode",
-                     "spot_dense_decode", "spot_sparse_prefill"):
+                     "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step"):
             getattr(L, name).restype = ctypes.c_int32
         if path is None:
             _lib = L
@@ -205,6 +210,45 @@ def spot_sparse_prefill(q, k, v, L, idx, count, k_max, batch, h_q, h_kv, d, sm_s
         float(sm_scale), _ptr(out), _ptr(lse), _stream(stream)))
 
 
+def spot_decode_step_workspace_bytes(batch, h_q, h_kv, d, k_max) -> int:
+    return int(load().spot_decode_step_workspace_bytes(batch, h_q, h_kv, d, k_max))
+
+
+def spot_decode_step(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max, k_min,
+                     n_sink, n_recent, q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale,
+                     scores, idx, count, nuc_mass, out, lse, ws, stream=None):
+    nblk = l_cap // BLK
+    f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
+    _dev(q_sel, "q_sel", BF16, batch * h_s * d_s)
+    _dev(w, "w", F32, batch * h_s)
+    if f == 0:
+        _dev(k_sel, "k_sel", BF16, batch * nblk * h_s * d_s)
+    else:
+        _dev(k_sel, "k_sel", U8, batch * nblk * h_s * d_s // 2)
+        _dev(k_scale, "k_scale", None, batch * nblk * h_s * d_s // 32)
+    if n_valid is not None:
+        _dev(n_valid, "n_valid", I32, batch)
+    _dev(q, "q", BF16, batch * h_q * d)
+    _dev(k, "k", BF16, batch * h_kv * l_cap * d)
+    _dev(v, "v", BF16, batch * h_kv * l_cap * d)
+    _dev(seq_len, "seq_len", I32, batch)
+    _dev(scores, "scores", F32, batch * nblk)
+    _dev(idx, "idx", I32, batch * k_max)
+    _dev(count, "count", I32, batch)
+    if nuc_mass is not None:
+        _dev(nuc_mass, "nuc_mass", F32, batch)
+    _dev(out, "out", BF16, batch * h_q * d)
+    if lse is not None:
+        _dev(lse, "lse", F32, batch * h_q)
+    _dev(ws, "ws", None)
+    _check("spot_decode_step", load().spot_decode_step(
+        _ptr(q_sel), _ptr(w), _ptr(k_sel), _ptr(k_scale), f, h_s, d_s, _ptr(n_valid),
+        float(top_p), k_max, k_min, n_sink, n_recent, _ptr(q), _ptr(k), _ptr(v), _ptr(seq_len),
+        batch, h_q, h_kv, d, l_cap, float(sm_scale), _ptr(scores), _ptr(idx), _ptr(count),
+        _ptr(nuc_mass), _ptr(out), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
 def spot_probe_stream_read(buf, sink, stream=None):
     _dev(buf, "buf", None)
     _dev(sink, "sink", F32, int(load().spot_probe_sink_words()))
@@ -293,6 +337,35 @@ def sparse_prefill(q, k, v, idx, count, sm_scale=None, out=None, lse=None, strea
     spot_sparse_prefill(q, k, v, L, idx, count, k_max, batch, h_q, h_kv, d, sm_scale, out, lse,
                         stream)
     return out, lse
+
+
+def step_workspace(batch, h_q, h_kv, d, k_max, device="cuda"):
+    """Zero-filled workspace of spot_decode_step (kept zeroed between calls)."""
+    n = spot_decode_step_workspace_bytes(batch, h_q, h_kv, d, k_max)
+    return torch.zeros(max(n, 16), dtype=torch.uint8, device=device)
+
+
+def decode_step(q_sel, w, k_sel, q, k, v, seq_len, rule, k_scale=None, kfmt="bf16",
+                n_valid=None, sm_scale=None, ws=None, stream=None):
+    """One fused decode step: (scores, idx, count, nuc_mass, out, lse)."""
+    batch, h_q, d = q.shape
+    _, h_kv, l_cap, _ = k.shape
+    h_s, d_s = q_sel.shape[-2], q_sel.shape[-1]
+    nblk = l_cap // BLK
+    dev = q.device
+    sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
+    scores = torch.empty((batch, nblk), dtype=torch.float32, device=dev)
+    idx = torch.empty((batch, rule.k_max), dtype=torch.int32, device=dev)
+    count = torch.empty(batch, dtype=torch.int32, device=dev)
+    mass = torch.empty(batch, dtype=torch.float32, device=dev)
+    out = torch.empty((batch, h_q, d), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((batch, h_q), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = step_workspace(batch, h_q, h_kv, d, rule.k_max, dev)
+    spot_decode_step(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, rule.top_p, rule.k_max,
+                     rule.k_min, rule.n_sink, rule.n_recent, q, k, v, seq_len, batch, h_q, h_kv,
+                     d, l_cap, sm_scale, scores, idx, count, mass, out, lse, ws, stream)
+    return scores, idx, count, mass, out, lse
 
 
 # ------------------------------------------------------- host helpers

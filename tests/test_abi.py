@@ -86,6 +86,34 @@ def test_validation_errors_before_launch(lib):
     assert pre(nz, nz, nz, 128, nz, nz, 5000, 1, 64, 8, 128, 0.1, nz, None, None) == 3
     for bad_scale in (0.0, -0.1, float("nan"), float("inf")):
         assert pre(nz, nz, nz, 128, nz, nz, 4, 1, 64, 8, 128, bad_scale, nz, None, None) == 3
+    # fused step: (q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max, k_min,
+    # n_sink, n_recent, q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale, scores, idx,
+    # count, nuc_mass, out, lse, ws, ws_bytes, stream)
+    step = lib.spot_decode_step
+
+    def call(**kw):
+        a = dict(q_sel=nz, w=nz, k_sel=nz, k_scale=None, kfmt=0, h_s=8, d_s=64, n_valid=None,
+                 top_p=0.9, k_max=16, k_min=0, n_sink=1, n_recent=2, q=nz, k=nz, v=nz,
+                 seq_len=nz, batch=1, h_q=32, h_kv=8, d=128, l_cap=4096, sm_scale=0.1,
+                 scores=nz, idx=nz, count=nz, nuc_mass=None, out=nz, lse=None, ws=nz,
+                 ws_bytes=1 << 30, stream=None)
+        a.update(kw)
+        return step(*a.values())
+
+    assert call(q_sel=None) == 1
+    assert call(scores=None) == 1
+    assert call(kfmt=1) == 1                    # quantized without scales
+    assert call(kfmt=7) == 3
+    assert call(d_s=32) == 3
+    assert call(d=64) == 3
+    assert call(l_cap=4000) == 2
+    assert call(top_p=float("nan")) == 4
+    assert call(k_max=2) == 4
+    assert call(k_max=5000) == 3
+    assert call(ws_bytes=16) == 5
+    assert call(ws=None) == 5
+    assert lib.spot_decode_step_workspace_bytes(4, 32, 8, 128, 128) >= \
+        lib.spot_decode_workspace_bytes(4, 32, 8, 128, 128) + 4 * 66 * 4
 
 
 def test_workspace_size_query(lib):

@@ -1,0 +1,184 @@
+"""The fused decode step (spot_decode_step) against the three separate calls
+and against the FP64 oracle (needs an MI355X).
+
+The fused launch runs the same scoring, selection and attention cores as the
+separate kernels, so scores and block sets must match them exactly; the
+attention outputs must match to the decode tolerances (they are bitwise equal
+whenever both paths split the attention the same way).  End to end, the block
+sets are checked against the oracle's with the near-tie / mass-boundary
+exemptions of selcheck, and the outputs against the oracle run on the fused
+path's own block sets.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_22874_amd import spot, synth
+from paper_2606_22874_amd.synth import Rule
+
+from selcheck import check_all
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+DEV = "cuda:0"
+
+
+def bf(a):
+    return spot.to_device_bf16(a, DEV)
+
+
+def i32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(DEV)
+
+
+def f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+
+
+_cache = {}
+
+
+def workload(i, **kw):
+    key = (i, tuple(sorted(kw.items())))
+    if key not in _cache:
+        print(f"[gen] decode workload {i} {kw}", flush=True)
+        _cache[key] = synth.decode_config(i, **kw)
+    return _cache[key]
+
+
+def selector(wl, fmt):
+    if fmt == "bf16":
+        return bf(wl.k_sel), None
+    if fmt == "int4":
+        c, s = synth.quantize_int4_g32(wl.k_sel)
+        return (torch.from_numpy(c).to(DEV),
+                torch.from_numpy(s.view(np.uint16).view(np.int16)).to(DEV))
+    c, s = synth.quantize_mxfp4_g32(wl.k_sel)
+    return torch.from_numpy(c).to(DEV), torch.from_numpy(s).to(DEV)
+
+
+def inputs(wl, fmt):
+    k_sel, k_scale = selector(wl, fmt)
+    return dict(q_sel=bf(wl.q_sel), w=f32(wl.w), k_sel=k_sel, k_scale=k_scale, kfmt=fmt,
+                q=bf(wl.q), k=bf(wl.k), v=bf(wl.v), seq_len=i32(wl.seq_len),
+                n_valid=i32(wl.n_valid))
+
+
+def separate(x, wl):
+    s = spot.selector_score(x["q_sel"], x["w"], x["k_sel"], x["k_scale"], x["kfmt"],
+                            n_valid=x["n_valid"], nblk=wl.nblk)
+    idx, cnt, mass = spot.select_blocks(s, wl.rule, x["n_valid"])
+    out, lse = spot.sparse_decode(x["q"], x["k"], x["v"], x["seq_len"], idx, cnt, wl.sm_scale)
+    return s, idx, cnt, mass, out, lse
+
+
+def fused(x, wl, ws=None):
+    return spot.decode_step(x["q_sel"], x["w"], x["k_sel"], x["q"], x["k"], x["v"],
+                            x["seq_len"], wl.rule, k_scale=x["k_scale"], kfmt=x["kfmt"],
+                            n_valid=x["n_valid"], sm_scale=wl.sm_scale, ws=ws)
+
+
+def assert_same(sep, fus):
+    s0, i0, c0, m0, o0, l0 = sep
+    s1, i1, c1, m1, o1, l1 = fus
+    assert torch.equal(s0, s1), "scores differ"
+    assert torch.equal(c0, c1), "counts differ"
+    assert torch.equal(i0, i1), "block sets differ"
+    assert torch.allclose(m0, m1, rtol=1e-5, atol=1e-7), "nucleus mass differs"
+    assert torch.max(torch.abs(o0.float() - o1.float())).item() <= 1e-2
+    assert torch.max(torch.abs(l0 - l1)).item() <= 1e-4
+
+
+@pytest.mark.parametrize("cfg,fmt", [(1, "bf16"), (2, "bf16"), (3, "bf16"), (3, "int4"),
+                                     (3, "mxfp4")])
+def test_step_matches_separate_calls(cfg, fmt):
+    wl = workload(cfg)
+    x = inputs(wl, fmt)
+    print(f"[step] cfg {cfg} {fmt}", flush=True)
+    sep = separate(x, wl)
+    fus = fused(x, wl)
+    torch.cuda.synchronize()
+    assert_same(sep, fus)
+
+
+def test_step_end_to_end_vs_oracle():
+    wl = workload(3)
+    x = inputs(wl, "bf16")
+    s, idx, cnt, mass, out, lse = fused(x, wl)
+    torch.cuda.synchronize()
+    s_o = oracle.selector_score(wl.q_sel, wl.w, wl.k_sel, n_valid=wl.n_valid)
+    err = np.abs(s.cpu().numpy() - s_o)
+    fin = np.isfinite(s_o)
+    assert np.all(err[fin] <= 1e-4 * np.abs(s_o[fin]) + 1e-6)
+    idx_o, cnt_o, _ = oracle.select_blocks(s_o.astype(np.float32).astype(np.float64), wl.rule,
+                                           wl.n_valid)
+    idx_g, cnt_g = idx.cpu().numpy(), cnt.cpu().numpy()
+    print("[step] selection vs oracle:",
+          check_all(s_o.astype(np.float32), wl.n_valid, wl.rule, idx_o, cnt_o, idx_g, cnt_g))
+    out_o, lse_o = oracle.sparse_decode(wl.q, wl.k, wl.v, wl.seq_len, idx_g, cnt_g, wl.sm_scale)
+    g = out.float().cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(g - out_o)) <= 2e-2
+    assert np.linalg.norm(g - out_o) / np.linalg.norm(out_o) <= 1e-2
+    assert np.max(np.abs(lse.cpu().numpy() - lse_o)) <= 2e-3
+
+
+def test_step_repeated_calls_reset_workspace():
+    """Back-to-back steps on one workspace: every call right, counters zero after."""
+    wl = workload(3)
+    x = inputs(wl, "bf16")
+    ws = spot.step_workspace(wl.B, wl.Hq, wl.Hkv, wl.d, wl.rule.k_max, DEV)
+    qs = [x["q"], x["q"].flip(-1).contiguous(), (x["q"].float() * 0.5).to(torch.bfloat16)]
+    results = []
+    for qv in qs:
+        y = dict(x, q=qv)
+        results.append((separate(y, wl), fused(y, wl, ws)))
+    torch.cuda.synchronize()
+    for sep, fus in results:
+        assert_same(sep, fus)
+    # The counters (one per (sequence, KV head) pair, then 66 flags per
+    # sequence) sit at the end of the workspace and are all back to zero.
+    n_cnt = wl.B * wl.Hkv + 66 * wl.B
+    n_bytes = spot.spot_decode_step_workspace_bytes(wl.B, wl.Hq, wl.Hkv, wl.d, wl.rule.k_max)
+    counters = ws[:n_bytes].view(torch.int32)[-n_cnt:]
+    assert int(torch.count_nonzero(counters).item()) == 0
+
+
+def test_step_ragged_sequences():
+    wl = workload(2, B=5, L=8192, seq_len=(8192, 5000, 64, 1, 4097))
+    x = inputs(wl, "bf16")
+    sep = separate(x, wl)
+    fus = fused(x, wl)
+    torch.cuda.synchronize()
+    assert_same(sep, fus)
+
+
+def test_step_fallback_shapes():
+    """Shapes outside the fused path (GQA group 8, 8192 blocks) run the three
+    stages one after the other and give the separate calls' results."""
+    wl = workload(2, B=2, L=8192)
+    x = inputs(wl, "bf16")
+    # GQA group 8: 64 query heads over the same 8 KV heads.
+    x8 = dict(x, q=bf(synth.normal_bf16(77, 1, (wl.B, 64, wl.d))))
+    sep = separate(x8, wl)
+    fus = fused(x8, wl)
+    torch.cuda.synchronize()
+    assert_same(sep, fus)
+    # 8192 blocks (L = 524288) exceed the fused selection core: k_max 256.
+    wl_long = synth.decode_config(3, B=1, L=524288, backbone=False)
+    rule = Rule(0.95, 256, 0, 1, 2)
+    wl_long.rule = rule
+    nb = wl_long.nblk
+    q_sel, w, k_sel = bf(wl_long.q_sel), f32(wl_long.w), bf(wl_long.k_sel)
+    seq = i32(wl_long.seq_len)
+    nv = i32(wl_long.n_valid)
+    qq = bf(synth.normal_bf16(78, 1, (1, 32, 128)))
+    kk = torch.zeros((1, 8, 524288, 128), dtype=torch.bfloat16, device=DEV)
+    vv = torch.zeros_like(kk)
+    s0 = spot.selector_score(q_sel, w, k_sel, n_valid=nv, nblk=nb)
+    i0, c0, _ = spot.select_blocks(s0, rule, nv)
+    s1, i1, c1, _, o1, l1 = spot.decode_step(q_sel, w, k_sel, qq, kk, vv, seq, rule, n_valid=nv)
+    torch.cuda.synchronize()
+    assert torch.equal(s0, s1) and torch.equal(i0, i1) and torch.equal(c0, c1)
+    assert torch.all(o1.float() == 0)   # zero values give zero outputs
