@@ -96,6 +96,33 @@ __device__ __forceinline__ void merge_head(const float* __restrict__ ws_o,
                                            size_t bh, uint16_t* __restrict__ out,
                                            float* __restrict__ lse, int lane) {
   const float* ml = ws_ml + bh * n_split * 2;
+  if (n_split <= 16) {
+    // one round trip: every partial's (m, l) and o in flight together
+    const float2 t = lane < n_split ? load_coherent(ml + 2 * lane) : make_float2(-INFINITY, 0.f);
+    const float* ob = ws_o + bh * n_split * kD + 2 * lane;
+    float2 o[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (u < n_split) o[u] = load_coherent(ob + (size_t)u * kD);
+    const float M = wave_max(t.y > 0.f ? t.x : -INFINITY);
+    const float wgt = t.y > 0.f ? exp2f(t.x - M) : 0.f;
+    const float L = wave_sum(t.y * wgt);
+    float o0 = 0.f, o1 = 0.f;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      if (u < n_split) {
+        const float wt = readlane_f(wgt, u);
+        o0 = fmaf(o[u].x, wt, o0);
+        o1 = fmaf(o[u].y, wt, o1);
+      }
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    const uint32_t packed = (uint32_t)f32_to_bf16_rne(o0 * inv) |
+                            ((uint32_t)f32_to_bf16_rne(o1 * inv) << 16);
+    *reinterpret_cast<uint32_t*>(&out[bh * kD + 2 * lane]) = packed;
+    if (lse && lane == 0) lse[bh] = L > 0.f ? (M + log2f(L)) * 0.6931471805599453f : -INFINITY;
+    return;
+  }
   float M = -INFINITY;
   for (int s = lane; s < n_split; s += 64) {
     const float2 t = load_coherent(ml + 2 * s);

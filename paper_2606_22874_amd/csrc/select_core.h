@@ -156,9 +156,10 @@ constexpr int kValBins = 2048;   // value bins of the threshold search
 template <int EPT, int SPL>
 struct SelWgSmem {
   uint32_t hist[kValBins];        // value-bin counts (the fallback radix uses 256)
-  uint64_t s_K[64 * SPL];         // threshold-bin members, then sorted survivors
+  uint64_t s_K[64 * SPL];         // threshold-bin members / survivors
   uint32_t red_u[kSelWG / 64][2];
-  float red_f[kSelWG / 64][2];
+  float red_f[kSelWG / 64];
+  float red_m[kSelWG / 64];       // survivors' mass partials
   int red_i[kSelWG / 64];
   int bc[4];
   uint64_t cut;
@@ -169,25 +170,32 @@ struct SelWgSmem {
 __device__ __forceinline__ uint64_t rank_key(uint32_t key, int id) {
   return ((uint64_t)key << 32) | (uint64_t)(0xffffffffu - (uint32_t)id);
 }
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, l);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(x >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
 
 // Selection of one row by the whole 256-thread workgroup: srow holds the
 // row's scores (the first nv valid), out its k_max id slots.  Every thread of
 // the workgroup must call it.  Thread t owns the EPT consecutive ids
-// [t*EPT, (t+1)*EPT).  Steps (barrier rounds in brackets):
-//  1. load; order-preserving keys for the residual candidates; residual max
+// [t*EPT, (t+1)*EPT).  Steps, with the workgroup barriers in brackets:
+//  1. load; order-preserving keys of the residual candidates; residual max
 //     M, min and Z = sum exp(s - M) from per-wave partials [1];
-//  2. when the cap C binds, the C-th best candidate (score desc, id asc):
-//     a histogram over 2048 equal-width value bins between the candidate min
-//     and max finds the bin holding it [1], a scan over the bins its rank
-//     inside the bin [2]; the bin's members are sorted exactly in one wave
-//     [2].  A bin with more members than fit the sort (heavy ties) falls back
-//     to an 8-bit radix select on the keys.  The result is one packed cut
-//     key: the survivors are the candidates whose packed key reaches it;
-//  3. the survivors' mass [1] decides: below top_p * Z the cap binds and the
-//     survivors are the answer; otherwise they are compacted [2], sorted in
-//     one wave by (score desc, id asc), prefix-summed, and the nucleus cut
-//     where the prefix first reaches top_p * Z (then floored by k_min) [1];
-//  4. reserved + chosen ids are written in ascending order [2].
+//  2. when the cap C binds: a histogram over 2048 equal-width value bins
+//     between the candidate min and max [1]; a scan over the bins finds the
+//     bin holding the C-th best candidate (score desc, id asc) [2]; the
+//     bin's members are gathered while every thread sums the mass of its
+//     candidates in better bins [1]; wave 0 ranks the members by counting
+//     and publishes the packed cut key and the members' share of the mass
+//     [1].  The survivors are the candidates whose packed key reaches the
+//     cut.  A bin too crowded to rank (heavy ties) falls back to an 8-bit
+//     radix select on the keys;
+//  3. below top_p * Z the cap binds and the survivors are the answer;
+//     otherwise they are compacted [2], sorted in wave 0 by (score desc, id
+//     asc), prefix-summed and cut where the prefix first reaches top_p * Z,
+//     then floored by k_min [1];
+//  4. reserved + chosen ids are written in ascending order [1].
 // Every reduction has a fixed order, so the result is deterministic.
 template <int EPT, int SPL, bool COH>
 __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
@@ -200,7 +208,7 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
   constexpr int P = 64 * SPL;
   constexpr int BPT = kValBins / NT;   // value bins per thread in the scan
   constexpr float kLog2e = 1.4426950408889634f;
-  static_assert(EPT <= 32, "a thread's ids must fit one bit word");
+  static_assert(EPT <= 16, "a thread's ids must fit one bit word");
   (void)nblk;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sink_end = min(n_sink, nv);
@@ -211,16 +219,17 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
   const int j0 = tid * EPT;
 
   // 1. scores, keys (0 = not a candidate), M, min and Z
+  SPOT_SEL_TS(0);
   float sv[EPT];
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
     const int j = j0 + e;
     sv[e] = j < nv ? load_score<COH>(srow + j) : -INFINITY;
   }
-  SPOT_SEL_TS(0);
   for (int i = tid; i < kValBins; i += NT) sm.hist[i] = 0u;
+  if (tid == 0) sm.bc[3] = 0;
   uint32_t key[EPT];
-  uint32_t resv = 0;
+  uint32_t cand = 0, resv = 0;
   {
     const int lo = max(sink_end - j0, 0), hi = min(rec_start - j0, EPT);
     const int vend = min(nv - j0, EPT);
@@ -228,6 +237,7 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
     for (int e = 0; e < EPT; ++e) {
       const bool c = e >= lo && e < hi;
       key[e] = c ? order_key(sv[e]) : 0u;
+      cand |= (uint32_t)c << e;
       resv |= (uint32_t)(e < vend && !c) << e;
     }
   }
@@ -236,23 +246,23 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
     kmax = max(kmax, key[e]);
-    if (key[e]) kmin = min(kmin, key[e]);
+    kmin = min(kmin, key[e] ? key[e] : 0xffffffffu);
   }
   kmax = wave_max_u(kmax);
   kmin = wave_min_u(kmin);
   {
     float zl = 0.f;
-    if (kmax) {
-      const float mw = order_key_inv(kmax);
+    const float mw = order_key_inv(kmax);
 #pragma unroll
-      for (int e = 0; e < EPT; ++e)
-        zl += key[e] ? __builtin_amdgcn_exp2f((sv[e] - mw) * kLog2e) : 0.f;
+    for (int e = 0; e < EPT; ++e) {
+      const float x = __builtin_amdgcn_exp2f((sv[e] - mw) * kLog2e);
+      zl += ((cand >> e) & 1u) && kmax ? x : 0.f;
     }
     const float zw = wave_sum(zl);
     if (lane == 0) {
       sm.red_u[wave][0] = kmax;
       sm.red_u[wave][1] = kmin;
-      sm.red_f[wave][0] = zw;
+      sm.red_f[wave] = zw;
     }
   }
   __syncthreads();
@@ -268,35 +278,39 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
 #pragma unroll
   for (int w = 0; w < NW; ++w)
     if (sm.red_u[w][0])
-      Z += sm.red_f[w][0] * __builtin_amdgcn_exp2f((order_key_inv(sm.red_u[w][0]) - M) * kLog2e);
-
+      Z += sm.red_f[w] * __builtin_amdgcn_exp2f((order_key_inv(sm.red_u[w][0]) - M) * kLog2e);
+  float pe[EPT];                                 // exp(s - M) of the candidates
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) pe[e] = __builtin_amdgcn_exp2f((sv[e] - M) * kLog2e);
   SPOT_SEL_TS(2);
-  // 2. the cut: survivors are the candidates with rank_key >= k_thr
-  uint64_t k_thr = 1ull;                       // every candidate (cap == n_res)
-  if (cap <= 0) {
-    k_thr = ~0ull;
-  } else if (cap < n_res) {
+
+  // 2. the cut: survivors are the candidates with rank_key >= (kt, it)
+  const bool thresh = cap > 0 && cap < n_res;
+  uint32_t kt = cap <= 0 ? 0xffffffffu : 1u;     // threshold key
+  int it = cap <= 0 ? -1 : 0x7fffffff;            // largest id kept at the threshold key
+  float msum = 0.f;
+  bool have_msum = false;
+  bool crowded = thresh;
+  if (thresh) {
     const float vhi = M, vlo = order_key_inv(kmin);
     const float span = vhi - vlo;
-    bool crowded = !(span > 0.f) || !(span < INFINITY);
-    if (!crowded) {
+    if (span > 0.f && span < INFINITY) {
       const float inv_w = (float)kValBins / span * 0.99999f;
       int bin[EPT];
 #pragma unroll
       for (int e = 0; e < EPT; ++e) {
-        // clamped in float first (non-candidates may hold -inf or NaN)
+        // bins ascend as values descend; clamped in float first
         bin[e] = (int)fminf((vhi - sv[e]) * inv_w, (float)(kValBins - 1));
         if (key[e]) atomicAdd(&sm.hist[bin[e]], 1u);
       }
       __syncthreads();
-      // bins ascend as values descend; thread t scans bins [BPT t, BPT t + BPT)
+      SPOT_SEL_TS(6);
       int c[BPT], tot = 0;
 #pragma unroll
       for (int i = 0; i < BPT; ++i) {
         c[i] = (int)sm.hist[BPT * tid + i];
         tot += c[i];
       }
-      SPOT_SEL_TS(6);
       const int incl = wave_incl_scan_i(tot);
       if (lane == 63) sm.red_i[wave] = incl;
       __syncthreads();
@@ -309,128 +323,142 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
           sm.bc[0] = BPT * tid + i;
           sm.bc[1] = cap - before;
           sm.bc[2] = c[i];
-          sm.bc[3] = 0;
         }
         before += c[i];
       }
       __syncthreads();
       SPOT_SEL_TS(7);
       const int b_star = sm.bc[0], need = sm.bc[1], in_bin = sm.bc[2];
-      crowded = in_bin > P;
-      if (!crowded) {
+      if (in_bin <= 64) {
+        crowded = false;
+        // gather the bin's members; sum the mass of better bins
+        float ma = 0.f;
 #pragma unroll
-        for (int e = 0; e < EPT; ++e)
+        for (int e = 0; e < EPT; ++e) {
           if (key[e] && bin[e] == b_star) sm.s_K[atomicAdd(&sm.bc[3], 1)] = rank_key(key[e], j0 + e);
-        for (int i = in_bin + tid; i < P; i += NT) sm.s_K[i] = 0ull;
+          ma += key[e] && bin[e] < b_star ? pe[e] : 0.f;
+        }
+        const float mw = wave_sum(ma);
+        if (lane == 0) sm.red_m[wave] = mw;
         __syncthreads();
-      SPOT_SEL_TS(8);
+        SPOT_SEL_TS(8);
         if (wave == 0) {
-          uint64_t K[SPL];
-#pragma unroll
-          for (int t = 0; t < SPL; ++t) K[t] = sm.s_K[lane * SPL + t];
-          bitonic_desc<SPL>(K);
-          const int ln = (need - 1) / SPL, tn = (need - 1) % SPL;
-          uint64_t mine = 0ull;
-#pragma unroll
-          for (int t = 0; t < SPL; ++t) mine = t == tn ? K[t] : mine;
-          const uint32_t lo32 = __builtin_amdgcn_readlane((uint32_t)mine, ln);
-          const uint32_t hi32 = __builtin_amdgcn_readlane((uint32_t)(mine >> 32), ln);
-          if (lane == 0) sm.cut = ((uint64_t)hi32 << 32) | lo32;
+          // member j sits in lane j; its rank is the number of better members
+          const uint64_t mine = lane < in_bin ? sm.s_K[lane] : 0ull;
+          int better = 0;
+          for (int j = 0; j < in_bin; ++j) better += readlane_u64(mine, j) > mine ? 1 : 0;
+          const bool top = lane < in_bin && better < need;
+          const float x = top ? __builtin_amdgcn_exp2f(
+                                    (order_key_inv((uint32_t)(mine >> 32)) - M) * kLog2e)
+                              : 0.f;
+          const float m_in = wave_sum(x);
+          const int src = __builtin_ctzll(__ballot(lane < in_bin && better == need - 1));
+          if (lane == 0) {
+            sm.cut = readlane_u64(mine, src);
+            sm.cut_mass = m_in;
+          }
+          // (readlane above is wave-uniform; lane 0 stores it)
         }
         __syncthreads();
-        k_thr = sm.cut;
+        const uint64_t kc = sm.cut;
+        kt = (uint32_t)(kc >> 32);
+        it = (int)(0xffffffffu - (uint32_t)kc);
+        msum = sm.cut_mass;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) msum += sm.red_m[w];
+        have_msum = true;
       }
     }
-    if (crowded) {
-      // 8-bit radix select by count on the keys, from the highest bit where
-      // the candidates differ; equal keys at the threshold go to lower ids.
-      const uint32_t diff = kmin ^ kmax;
-      int shift = diff ? 32 - __builtin_clz(diff) : 0;
-      uint32_t prefix = shift >= 32 ? 0u : (kmax >> shift) << shift;
-      uint32_t pmask = shift >= 32 ? 0u : ~0u << shift;
-      int need = cap;
-      while (shift > 0) {
-        const int width = shift < 8 ? shift : 8;
-        shift -= width;
-        const uint32_t dmask = (1u << width) - 1u;
-        sm.hist[tid] = 0u;
-        __syncthreads();
+  }
+  if (crowded) {
+    // 8-bit radix select by count on the keys, from the highest bit where
+    // the candidates differ; equal keys at the threshold go to lower ids.
+    const uint32_t diff = kmin ^ kmax;
+    int shift = diff ? 32 - __builtin_clz(diff) : 0;
+    uint32_t prefix = shift >= 32 ? 0u : (kmax >> shift) << shift;
+    uint32_t pmask = shift >= 32 ? 0u : ~0u << shift;
+    int need = cap;
+    while (shift > 0) {
+      const int width = shift < 8 ? shift : 8;
+      shift -= width;
+      const uint32_t dmask = (1u << width) - 1u;
+      sm.hist[tid] = 0u;
+      __syncthreads();
 #pragma unroll
-        for (int e = 0; e < EPT; ++e)
-          if (key[e] && (key[e] & pmask) == prefix)
-            atomicAdd(&sm.hist[(key[e] >> shift) & dmask], 1u);
-        __syncthreads();
-        if (wave == 0) {
-          int c[4], tot = 0;                   // lane l: digits 255-4l .. 252-4l
+      for (int e = 0; e < EPT; ++e)
+        if (key[e] && (key[e] & pmask) == prefix) atomicAdd(&sm.hist[(key[e] >> shift) & dmask], 1u);
+      __syncthreads();
+      if (wave == 0) {
+        int c[4], tot = 0;                   // lane l: digits 255-4l .. 252-4l
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            c[i] = (int)sm.hist[255 - 4 * lane - i];
-            tot += c[i];
-          }
-          const int incl = wave_incl_scan_i(tot);
-          int before = incl - tot;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if (before < need && need <= before + c[i]) {
-              sm.bc[0] = 255 - 4 * lane - i;
-              sm.bc[1] = need - before;
-            }
-            before += c[i];
-          }
+        for (int i = 0; i < 4; ++i) {
+          c[i] = (int)sm.hist[255 - 4 * lane - i];
+          tot += c[i];
         }
-        __syncthreads();
-        prefix |= (uint32_t)sm.bc[0] << shift;
-        pmask |= dmask << shift;
-        need = sm.bc[1];
-      }
-      // the need-th lowest id among the keys equal to the threshold
-      int n_eq = 0;
+        const int incl = wave_incl_scan_i(tot);
+        int before = incl - tot;
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) n_eq += key[e] == prefix ? 1 : 0;
-      int total;
-      int eq_before = wg_excl_scan(n_eq, sm.red_i, total);
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) {
-        if (key[e] == prefix) {
-          if (++eq_before == need) sm.cut = rank_key(prefix, j0 + e);
+        for (int i = 0; i < 4; ++i) {
+          if (before < need && need <= before + c[i]) {
+            sm.bc[0] = 255 - 4 * lane - i;
+            sm.bc[1] = need - before;
+          }
+          before += c[i];
         }
       }
       __syncthreads();
-      k_thr = sm.cut;
+      prefix |= (uint32_t)sm.bc[0] << shift;
+      pmask |= dmask << shift;
+      need = sm.bc[1];
     }
+    // the need-th lowest id among the keys equal to the threshold
+    int n_eq = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) n_eq += key[e] == prefix ? 1 : 0;
+    int total;
+    int eq_before = wg_excl_scan(n_eq, sm.red_i, total);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      if (key[e] == prefix) {
+        if (++eq_before == need) sm.bc[2] = j0 + e;
+      }
+    }
+    __syncthreads();
+    kt = prefix;
+    it = sm.bc[2];
   }
-
-  SPOT_SEL_TS(3);
-  // 3. survivors, their mass, and the nucleus
+  // survivor bits (key > kt, or key == kt and id <= it)
   uint32_t surv = 0u;
-  float ms = 0.f;
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
-    if (key[e] && rank_key(key[e], j0 + e) >= k_thr) {
-      surv |= 1u << e;
-      ms += __builtin_amdgcn_exp2f((sv[e] - M) * kLog2e);
-    }
+    const bool sv_ = key[e] && (key[e] > kt || (key[e] == kt && j0 + e <= it));
+    surv |= (uint32_t)sv_ << e;
   }
-  {
-    const float mw = wave_sum(ms);
-    if (lane == 0) sm.red_f[wave][1] = mw;
-  }
-  __syncthreads();
-  float msum = 0.f;
+  if (!have_msum) {
+    float ms = 0.f;
 #pragma unroll
-  for (int w = 0; w < NW; ++w) msum += sm.red_f[w][1];
+    for (int e = 0; e < EPT; ++e) ms += ((surv >> e) & 1u) ? pe[e] : 0.f;
+    const float mw = wave_sum(ms);
+    if (lane == 0) sm.red_m[wave] = mw;
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < NW; ++w) msum += sm.red_m[w];
+  }
+  SPOT_SEL_TS(3);
+
+  // 3. the nucleus (the same decision in every thread)
   const float pz = top_p * Z;
   int n;                                  // -1: the nucleus ends before the cap
   if (cap <= 0) n = 0;
   else if (top_p >= 1.f) n = cap;
   else if (top_p <= 0.f) n = 0;
-  else if (msum < pz) n = cap;           // the cap binds before the nucleus reaches top_p
+  else if (msum < pz) n = cap;            // the cap binds before the nucleus reaches top_p
   else n = -1;
   if (n >= 0 && n_reserved + n < k_min) n = min(k_min - n_reserved, cap);
-  uint64_t k_cut = n == 0 ? ~0ull : k_thr;
+  uint32_t chosen = n == 0 ? 0u : surv;
   float mass = n > 0 && Z > 0.f ? msum / Z : 0.f;
   if (n < 0 || (n > 0 && n < cap)) {
-    // survivors in rank order: compact, sort in wave 0, cut the prefix
+    // survivors (exactly cap of them) in rank order: compact, sort, cut
     int total;
     int pos = wg_excl_scan(__popc(surv), sm.red_i, total);
 #pragma unroll
@@ -451,9 +479,9 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
                     : 0.f;
         cum[t] = run;
       }
-      const float base = wave_incl_scan_f(run) - run;
+      const float offs = wave_incl_scan_f(run) - run;
 #pragma unroll
-      for (int t = 0; t < SPL; ++t) cum[t] += base;
+      for (int t = 0; t < SPL; ++t) cum[t] += offs;
       int nn = n;
       if (nn < 0) {
         int below = 0;
@@ -470,27 +498,40 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
         mk = t == tn ? K[t] : mk;
         mc = t == tn ? cum[t] : mc;
       }
-      const uint32_t lo32 = __builtin_amdgcn_readlane((uint32_t)mk, ln);
-      const uint32_t hi32 = __builtin_amdgcn_readlane((uint32_t)(mk >> 32), ln);
+      const uint64_t kc = readlane_u64(mk, ln);
       const float m_at = readlane_f(mc, ln);
       if (lane == 0) {
-        sm.cut = ((uint64_t)hi32 << 32) | lo32;
+        sm.cut = kc;
         sm.cut_mass = Z > 0.f ? m_at / Z : 0.f;
       }
     }
     __syncthreads();
-    k_cut = sm.cut;
+    const uint64_t kc = sm.cut;
+    const uint32_t ck = (uint32_t)(kc >> 32);
+    const int ci = (int)(0xffffffffu - (uint32_t)kc);
     mass = sm.cut_mass;
-  }
-
-  SPOT_SEL_TS(4);
-  // 4. write S = reserved u chosen, ascending
-  uint32_t fin = resv;
+    chosen = 0u;
 #pragma unroll
-  for (int e = 0; e < EPT; ++e)
-    if (key[e] && rank_key(key[e], j0 + e) >= k_cut) fin |= 1u << e;
-  int total;
-  int pos = wg_excl_scan(__popc(fin), sm.red_i, total);
+    for (int e = 0; e < EPT; ++e) {
+      const bool ch = ((surv >> e) & 1u) && (key[e] > ck || (key[e] == ck && j0 + e <= ci));
+      chosen |= (uint32_t)ch << e;
+    }
+  }
+  SPOT_SEL_TS(4);
+
+  // 4. write S = reserved u chosen, ascending
+  const uint32_t fin = resv | chosen;
+  const int mine = __popc(fin);
+  const int incl = wave_incl_scan_i(mine);
+  if (lane == 63) sm.red_i[wave] = incl;
+  __syncthreads();
+  int pos = incl - mine, total = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int t = sm.red_i[w];
+    pos += w < wave ? t : 0;
+    total += t;
+  }
 #pragma unroll
   for (int e = 0; e < EPT; ++e)
     if (((fin >> e) & 1u) && pos < k_max) store_i32<COH>(out + pos++, j0 + e);
