@@ -5,6 +5,8 @@ One step = selector scoring of every KV block + dual top-p/top-K selection +
 block-sparse GQA decode attention, for all sequences of one layer, on the
 Qwen3-8B-shaped 128K-token workload (batch 4, 32 query / 8 KV heads, d = 128,
 2048 blocks of 64 tokens, p = 0.95, K_max = 128, 1 sink + 2 recent blocks).
+The headline value times spot_decode_step (all three stages in one launch);
+the three separate calls are timed too, with their per-stage times.
 
 Inputs are resident in HBM before timing starts.  The timed loop rotates
 over NCOPY distinct copies of the KV cache and selector cache so that the
@@ -50,27 +52,29 @@ def log(msg):
 
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_sparse_L131072_B4.md")
+STEP_PROFILE = os.path.join(ROOT, "profiles", "decode_step_L131072_B4.md")
+# Sources whose code the fused step kernel is built from.
+STEP_SOURCES = ("step.hip", "decode_core.h", "score_core.h", "select_core.h", "spot_internal.h")
 
 
-def decode_source_hash() -> str:
+def source_hash(files=STEP_SOURCES) -> str:
     h = hashlib.sha256()
-    for f in ("decode.hip", "spot_internal.h"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2606_22874_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per decode launch from the committed rocprofv3 counter runs,
-    or None when the decode kernel source changed since they were taken."""
+def measured_traffic(path=STEP_PROFILE, files=STEP_SOURCES):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, or
+    None when the kernel's sources changed since they were taken."""
     try:
-        text = open(TRAFFIC_PROFILE).read()
+        text = open(path).read()
     except OSError:
         return None
     m = re.search(r"traffic_bytes_per_launch: (\d+)\s*\(source: .*? sha256 prefix (\w+)\)",
                   text, re.S)
-    if not m or m.group(2) != decode_source_hash():
+    if not m or m.group(2) != source_hash(files):
         return None
     return int(m.group(1))
 
@@ -139,6 +143,7 @@ def main():
     out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
     ws = spot.decode_workspace(B, Hq, Hkv, d, rule.k_max, dev)
+    ws_step = spot.step_workspace(B, Hq, Hkv, d, rule.k_max, dev)
     stream = torch.cuda.current_stream()
 
     def score(c):
@@ -155,10 +160,17 @@ def main():
         spot.spot_sparse_decode(q, k, v, seq_len, idx, cnt, rule.k_max, B, Hq, Hkv, d, L,
                                 wl.sm_scale, out, lse, ws, stream)
 
-    def step(c):
+    def separate_step(c):
         score(c)
         select(c)
         attend(c)
+
+    def step(c):
+        k, v, ks, sc = copies[c % len(copies)]
+        spot.spot_decode_step(q_sel, w, ks, sc, args.fmt, wl.Hs, wl.ds, n_valid, rule.top_p,
+                              rule.k_max, rule.k_min, rule.n_sink, rule.n_recent, q, k, v,
+                              seq_len, B, Hq, Hkv, d, L, wl.sm_scale, scores, idx, cnt, mass,
+                              out, lse, ws_step, stream)
 
     def timed(fn, n):
         """Average time of n back-to-back calls, HIP events on the launch stream."""
@@ -173,18 +185,21 @@ def main():
 
     log(f"[bench] warmup {args.warmup} steps")
     for i in range(args.warmup):
+        separate_step(i)
         step(i)
     torch.cuda.synchronize()
     counts = cnt.cpu().numpy()
 
     log(f"[bench] timing {args.steps} steps")
     ms = timed(step, args.steps)
+    sep_ms = timed(separate_step, args.steps)
     # Per-stage averages (same launch stream, back to back, rotating copies).
     attn_ms = timed(attend, args.steps)
     score_ms = timed(score, args.steps)
     select_ms = timed(select, args.steps)
-    log(f"[bench] {ms * 1e3:.1f} us/step; score {score_ms * 1e3:.1f} us, select "
-        f"{select_ms * 1e3:.1f} us, attention {attn_ms * 1e3:.1f} us")
+    log(f"[bench] fused {ms * 1e3:.1f} us/step, separate {sep_ms * 1e3:.1f} us/step; score "
+        f"{score_ms * 1e3:.1f} us, select {select_ms * 1e3:.1f} us, attention "
+        f"{attn_ms * 1e3:.1f} us")
 
     # Practical read ceiling: the same byte count streamed by a plain kernel.
     kv_block_bytes = 64 * Hkv * d * 2 * 2          # K and V of one 64-token block
@@ -228,20 +243,29 @@ def main():
             "bytes_per_step": step_bytes,
             "step_hbm_gbs": round(step_gbs, 1),
             "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
+            "path": "spot_decode_step (score + select + attention in one launch)",
+            "separate_calls_us_per_step": round(sep_ms * 1e3, 2),
             "stage_us": {"score": round(score_ms * 1e3, 2), "select": round(select_ms * 1e3, 2),
                          "attention": round(attn_ms * 1e3, 2)},
             "stream_read_ceiling_gbs": round(stream_gbs, 1),
+            "attention_kernel": {
+                "kernel": "decode_split_kernel (spot_sparse_decode)",
+                "achieved_gbs": round(attn_gbs, 1),
+                "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
+                "bytes_per_launch": attn_bytes,
+                "avg_launch_us": round(attn_ms * 1e3, 2),
+            },
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "decode_split_kernel (spot_sparse_decode)",
-            "achieved": round(attn_gbs, 1),
+            "kernel": "step_kernel (spot_decode_step: scoring, selection, attention)",
+            "achieved": round(step_gbs, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
+            "frac": round(step_gbs / HBM_PEAK_GBS, 4),
             "traffic": measured_traffic() if args.fmt == "bf16" else None,
-            "bytes_per_launch": attn_bytes,
-            "avg_launch_us": round(attn_ms * 1e3, 2),
+            "bytes_per_launch": step_bytes,
+            "avg_launch_us": round(ms * 1e3, 2),
         },
     }
 
