@@ -42,7 +42,8 @@ typedef int32_t spot_status;
 #define SPOT_ERR_SHAPE 2       /* a size or shape is out of range / inconsistent  */
 #define SPOT_ERR_UNSUPPORTED 3 /* a valid but unimplemented size or format        */
 #define SPOT_ERR_RULE 4        /* selection rule parameters are invalid           */
-#define SPOT_ERR_WORKSPACE 5   /* the workspace is missing or too small           */
+#define SPOT_ERR_WORKSPACE 5   /* the workspace is missing, too small or not      */
+                               /* 16-byte aligned                                 */
 #define SPOT_ERR_HIP 6         /* the HIP runtime reported a launch error         */
 
 /* Storage formats of the selector key cache (Section 5.3, Appendix G:
@@ -150,10 +151,11 @@ size_t spot_decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_
  *  out      device BF16 [batch, h_q, d] (output, round to nearest even)
  *  lse      device float [batch, h_q] (output, may be NULL)
  *  ws       device workspace of at least
- *           spot_decode_workspace_bytes(batch, h_q, h_kv, d, k_max) bytes.
- *           It must be zero-filled before its first use; every call leaves
- *           it ready for the next one (its completion counters return to
- *           zero).  Calls that may overlap in time need separate workspaces.
+ *           spot_decode_workspace_bytes(batch, h_q, h_kv, d, k_max) bytes,
+ *           16-byte aligned.  It must be zero-filled before its first use;
+ *           every call leaves it ready for the next one (its completion
+ *           counters return to zero).  Calls that may overlap in time need
+ *           separate workspaces.
  *
  * Supported: d == 128, h_q / h_kv in {1, 2, 4, 8}.
  */
@@ -178,7 +180,8 @@ spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
  * workgroup per sequence selects its blocks as soon as the sequence's
  * scores are in, and the attention workgroups start as soon as that
  * selection is published, with no kernel boundary in between (hand-offs
- * through flags in the workspace; every wait is bounded in time).  Otherwise
+ * through self-flagging record words in the workspace, which each reader
+ * clears again; every wait is bounded in time).  Otherwise
  * (or when no such grid fits) the three stages are launched one after the
  * other on `stream`.  Either way the results are deterministic; the fused
  * path may split the attention over fewer workgroups when fewer fit, which
@@ -190,11 +193,13 @@ spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
  *  nuc_mass device float [batch] or NULL        (output)
  *  out, lse as spot_sparse_decode               (output; lse may be NULL)
  *  ws       device, spot_decode_step_workspace_bytes(batch, h_q, h_kv, d,
- *           k_max) bytes: the decode partials and counters laid out as for
- *           spot_sparse_decode, then 66 flags per sequence.  It must
- *           be zero-filled before its first use; every call leaves it ready
- *           for the next one (all its counters return to zero).  Calls that
- *           share a workspace must not overlap in time.
+ *           k_max) bytes, 16-byte aligned: the decode partials and counters
+ *           laid out as for spot_sparse_decode, then (from the next 16-byte
+ *           boundary) 4096 score record words per sequence and h_kv * k_max
+ *           block list record words per sequence.  It must be zero-filled
+ *           before its first use; every call leaves it ready for the next one
+ *           (its counters and records return to zero).  Calls that share a
+ *           workspace must not overlap in time.
  */
 size_t spot_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max);
 
@@ -211,7 +216,7 @@ spot_status spot_decode_step(const void *q_sel, const float *w, const void *k_se
  * spot_dense_decode -- the dense decode baseline: spot_sparse_decode with
  * every block < ceil(seq_len / 64) selected (full attention over the cache).
  * Same layouts; ws of spot_decode_workspace_bytes(batch, h_q, h_kv, d,
- * l_cap / 64) bytes.
+ * l_cap / 64) bytes, 16-byte aligned.
  */
 spot_status spot_dense_decode(const void *q, const void *k, const void *v,
                               const int32_t *seq_len, int batch, int h_q, int h_kv, int d,

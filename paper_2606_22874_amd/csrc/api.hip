@@ -72,6 +72,10 @@ size_t spot_decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_
   return decode_workspace_bytes(batch, h_q, h_kv, d, max_blocks);
 }
 
+// Workspaces hold 8-byte device-scope words; 16-byte alignment is required
+// (every hipMalloc allocation has it).
+static bool misaligned(const void* ws) { return (reinterpret_cast<uintptr_t>(ws) & 15u) != 0; }
+
 static spot_status check_decode(const void* q, const void* k, const void* v,
                                 const int32_t* seq_len, const void* out, int batch, int h_q,
                                 int h_kv, int d, int l_cap) {
@@ -91,7 +95,7 @@ spot_status spot_sparse_decode(const void* q, const void* k, const void* v,
   if (!idx || !count) return SPOT_ERR_NULL;
   if (k_max < 1) return SPOT_ERR_SHAPE;
   if (batch == 0) return SPOT_OK;
-  if (!ws || ws_bytes < decode_workspace_bytes(batch, h_q, h_kv, d, k_max))
+  if (!ws || ws_bytes < decode_workspace_bytes(batch, h_q, h_kv, d, k_max) || misaligned(ws))
     return SPOT_ERR_WORKSPACE;
   return from_hip(launch_decode(false, q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv,
                                 l_cap, sm_scale, out, lse, ws, static_cast<hipStream_t>(stream)));
@@ -105,7 +109,8 @@ spot_status spot_dense_decode(const void* q, const void* k, const void* v,
   if (st != SPOT_OK) return st;
   if (l_cap == 0) return SPOT_ERR_SHAPE;
   if (batch == 0) return SPOT_OK;
-  if (!ws || ws_bytes < decode_workspace_bytes(batch, h_q, h_kv, d, l_cap / kBlk))
+  if (!ws || ws_bytes < decode_workspace_bytes(batch, h_q, h_kv, d, l_cap / kBlk) ||
+      misaligned(ws))
     return SPOT_ERR_WORKSPACE;
   return from_hip(launch_decode(true, q, k, v, seq_len, nullptr, nullptr, 0, batch, h_q, h_kv,
                                 l_cap, sm_scale, out, lse, ws, static_cast<hipStream_t>(stream)));
@@ -139,7 +144,7 @@ spot_status spot_decode_step(const void* q_sel, const float* w, const void* k_se
   const int nblk = l_cap / kBlk;
   if (nblk > 16384 || k_max > 4096) return SPOT_ERR_UNSUPPORTED;
   if (batch == 0) return SPOT_OK;
-  if (!ws || ws_bytes < step_workspace_bytes(batch, h_q, h_kv, d, k_max))
+  if (!ws || ws_bytes < step_workspace_bytes(batch, h_q, h_kv, d, k_max) || misaligned(ws))
     return SPOT_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (step_fusable(h_q, h_kv, nblk, k_max)) {

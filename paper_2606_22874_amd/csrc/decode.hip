@@ -18,9 +18,9 @@ __global__ __launch_bounds__(64 * G, waves_per_eu(G)) void decode_split_kernel(
     float* __restrict__ ws_ml, unsigned* __restrict__ counters, uint16_t* __restrict__ out,
     float* __restrict__ lse) {
   __shared__ DecodeSmem<G> sm;
-  decode_body<G, DENSE, false>(sm, blockIdx.x / n_slot, blockIdx.x % n_slot, q, k, v, seq_len,
-                               idx, count, k_max, h_q, h_kv, l_cap, scale_log2, n_slot, ws_o,
-                               ws_ml, counters, out, lse);
+  decode_body<G, DENSE>(sm, ListFromIdx{idx, count, k_max}, blockIdx.x / n_slot,
+                        blockIdx.x % n_slot, q, k, v, seq_len, h_q, h_kv, l_cap, scale_log2,
+                        n_slot, ws_o, ws_ml, counters, out, lse);
 }
 
 }  // namespace

@@ -5,8 +5,8 @@
 // (paper Section 2 and the method figure: attention over the gathered K_I,
 // V_I; one block set per query, shared by every head).
 //
-// Work split: grid (n_split, h_kv, batch).  A workgroup owns a contiguous run
-// of entries of its sequence's block list and the whole GQA group of G query
+// Work split: grid (n_split, h_kv, batch).  A workgroup owns every n_split-th
+// entry of its sequence's block list and the whole GQA group of G query
 // heads of one KV head, so every K/V byte is read from HBM exactly once.  The
 // workgroup has G waves; wave w owns token rows [w*T, (w+1)*T) (T = 64/G) of
 // every 64-token block, and its lanes are (head h, token t) = (lane / T,
@@ -213,26 +213,50 @@ __device__ __forceinline__ unsigned* pair_counters(unsigned* counters, int pair)
   return counters + pair;
 }
 
-template <bool COH>
-__device__ __forceinline__ int32_t load_i32(const int32_t* p) {
-  if constexpr (COH)
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  else
-    return *p;
+// Appends the ids of wave 0's lanes that lie in [0, nb_valid) to ids[cnt ..]
+// in lane order and returns the new count (ids past kMaxIds are dropped).
+__device__ __forceinline__ int append_ids(int* ids, int cnt, int j, int nb_valid) {
+  const int lane = __lane_id();
+  const bool ok = j >= 0 && j < nb_valid;
+  const unsigned long long m = __ballot(ok);
+  const int pos = cnt + __popcll(m & ((1ull << lane) - 1ull));
+  if (ok && pos < kMaxIds) ids[pos] = j;
+  return cnt + __popcll(m);
 }
 
+// Block list source of decode_body: entries slot, slot + n_slot, slot +
+// 2 n_slot, ... of the sequence's list idx[b, 0 .. min(count[b], k_max)).
+// Interleaving keeps the workgroups' shares within one entry of each other
+// for any count.  Called by wave 0 only.
+struct ListFromIdx {
+  const int32_t* idx;
+  const int32_t* count;
+  int k_max;
+  __device__ __forceinline__ int operator()(int* ids, int b, int g, int slot, int n_slot,
+                                            int nb_valid) const {
+    (void)g;
+    const int lane = __lane_id();
+    const int n_entries = min(count[b], k_max);
+    const int32_t* lst = idx + (size_t)b * k_max;
+    int cnt = 0;
+    for (int base = slot; base < n_entries; base += 64 * n_slot) {
+      const int e = base + lane * n_slot;
+      cnt = append_ids(ids, cnt, e < n_entries ? lst[e] : -1, nb_valid);
+    }
+    return min(cnt, kMaxIds);
+  }
+};
+
 // ---------------------------------------------------------- the body
-// Workgroup (pair, slot): slot s takes the s-th contiguous run of the pair's
-// block list; wave w processes token rows [w*T, (w+1)*T) of each of those
-// blocks.  Returns true in the workgroup that merged the pair's slots (the
-// last one to finish).  COH reads the block list with device-scope loads
-// (it may have been written by another workgroup of the same launch).
-template <int G, bool DENSE, bool COH>
+// Workgroup (pair, slot): slot s takes its share of the pair's block list
+// (from `list`; DENSE: the s-th contiguous run of all valid blocks); wave w
+// processes token rows [w*T, (w+1)*T) of each of those blocks.  Returns true
+// in the workgroup that merged the pair's slots (the last one to finish).
+template <int G, bool DENSE, class List>
 __device__ __forceinline__ bool decode_body(
-    DecodeSmem<G>& sm, int pair, int slot, const uint16_t* __restrict__ q,
+    DecodeSmem<G>& sm, const List& list, int pair, int slot, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    const int32_t* __restrict__ seq_len, const int32_t* __restrict__ idx,
-    const int32_t* __restrict__ count, int k_max, int h_q, int h_kv, int l_cap,
+    const int32_t* __restrict__ seq_len, int h_q, int h_kv, int l_cap,
     float scale_log2, int n_slot, float* __restrict__ ws_o, float* __restrict__ ws_ml,
     unsigned* __restrict__ counters, uint16_t* __restrict__ out, float* __restrict__ lse) {
   constexpr int T = 64 / G;               // token rows per wave per block
@@ -243,30 +267,6 @@ __device__ __forceinline__ bool decode_body(
   const int hh = lane / T, tt = lane % T;  // this lane's (head, token row)
   unsigned* pc = pair_counters(counters, pair);
 
-  const int sl = min(seq_len[b], l_cap);
-  const int nb_valid = (sl + kBlk - 1) / kBlk;
-  const int n_entries = DENSE ? nb_valid : min(load_i32<COH>(count + b), k_max);
-  const int32_t* list = idx + (size_t)b * k_max;
-
-  // This workgroup's run of the list: entries [e0, e1), compacted into LDS
-  // (ids outside [0, nb_valid) are dropped, so no load can leave the cache).
-  const int bps = (n_entries + n_slot - 1) / n_slot;
-  const int e0 = slot * bps;
-  const int e1 = min(e0 + bps, n_entries);
-  if (!DENSE && wave == 0) {
-    int cnt = 0;
-    for (int base = e0; base < e1; base += 64) {
-      const int e = base + lane;
-      const int j = e < e1 ? load_i32<COH>(list + e) : -1;
-      const bool ok = j >= 0 && j < nb_valid;
-      const unsigned long long m = __ballot(ok);
-      const int pos = cnt + __popcll(m & ((1ull << lane) - 1ull));
-      if (ok && pos < kMaxIds) sm.ids[pos] = j;
-      cnt += __popcll(m);
-    }
-    if (lane == 0) sm.n_local = min(cnt, kMaxIds);
-  }
-
   // This lane's query head (g*G + hh): 128 dims as packed BF16 pairs.
   uint32_t qv[kD / 2];
   {
@@ -276,6 +276,17 @@ __device__ __forceinline__ bool decode_body(
       const u32x4 t = qp[i];
       qv[4 * i + 0] = t.x; qv[4 * i + 1] = t.y; qv[4 * i + 2] = t.z; qv[4 * i + 3] = t.w;
     }
+  }
+
+  const int sl = min(seq_len[b], l_cap);
+  const int nb_valid = (sl + kBlk - 1) / kBlk;
+  // DENSE: this workgroup's contiguous run [e0, e1) of the valid blocks.
+  const int bps = (nb_valid + n_slot - 1) / n_slot;
+  const int e0 = slot * bps;
+  const int e1 = min(e0 + bps, nb_valid);
+  if (!DENSE && wave == 0) {
+    const int n = list(sm.ids, b, g, slot, n_slot, nb_valid);
+    if (lane == 0) sm.n_local = n;
   }
 
   const size_t head_base = ((size_t)b * h_kv + g) * (size_t)l_cap * kD;

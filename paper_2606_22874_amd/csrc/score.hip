@@ -24,8 +24,8 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
   int nv = n_valid ? n_valid[row] : nblk;
   nv = nv < 0 ? 0 : (nv > nblk ? nblk : nv);
   if (j0 >= nblk) return;
-  score_blocks<KFMT, LPH, kUnroll, false>(q_sel, w, k_sel, k_scale, row, row / rows_per_seq,
-                                          nblk, nv, j0, nblk, scores, threadIdx.x & 63);
+  score_blocks<KFMT, LPH, kUnroll>(q_sel, w, k_sel, k_scale, row, row / rows_per_seq, nblk, nv,
+                                   j0, nblk, scores, nullptr, threadIdx.x & 63);
 }
 
 template <int KFMT>

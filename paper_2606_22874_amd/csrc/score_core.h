@@ -88,17 +88,30 @@ struct KeyLoad<SPOT_KFMT_MXFP4_G32> {
   }
 };
 
+// Self-flagging record of a score for readers in other workgroups: the bit
+// complement of the float, so that no score maps to the zero "not written"
+// word (the only float whose complement is zero, the NaN with every bit set,
+// is replaced by the canonical quiet NaN first).
+__device__ __forceinline__ uint32_t score_word(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return ~(u == 0xffffffffu ? 0x7fc00000u : u);
+}
+__device__ __forceinline__ float score_of_word(uint32_t w) { return __uint_as_float(~w); }
+
 // One wavefront scores blocks j0 .. min(j0 + U, jend) - 1 of query row `row`
 // (sequence `seq`), all key loads issued before any arithmetic; blocks at or
-// past nv score -inf.  COH stores the scores at device scope (for readers in
-// other workgroups of the same launch).
-template <int KFMT, int LPH, int U, bool COH>
+// past nv score -inf.  A non-null rec (the row's record words, indexed by
+// block) also receives score_word() of each valid block's score, stored at
+// device scope (a reader in another workgroup
+// of the same launch polls these words: zero means not written yet).
+template <int KFMT, int LPH, int U>
 __device__ __forceinline__ void score_blocks(const uint16_t* __restrict__ q_sel,
                                              const float* __restrict__ w,
                                              const uint8_t* __restrict__ k_sel,
                                              const uint8_t* __restrict__ k_scale, int row,
                                              int seq, int nblk, int nv, int j0, int jend,
-                                             float* __restrict__ scores, int lane) {
+                                             float* __restrict__ scores,
+                                             uint32_t* __restrict__ rec, int lane) {
   constexpr int kHeads = 64 / LPH;
   // This lane's 8 query elements (head lane / LPH, dims 8*(lane % LPH) ..).
   const uint4 qraw = *reinterpret_cast<const uint4*>(q_sel + (size_t)row * 512 + lane * 8);
@@ -130,10 +143,10 @@ __device__ __forceinline__ void score_blocks(const uint16_t* __restrict__ q_sel,
   if (lane < U && j < jend) {
     float* dst = scores + (size_t)row * nblk + j;
     const float val = j < nv ? res : -INFINITY;
-    if constexpr (COH)
-      __hip_atomic_store(dst, val, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else
-      *dst = val;
+    if (rec && j < nv)
+      __hip_atomic_store(rec + j, score_word(val), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    *dst = val;
   }
 }
 

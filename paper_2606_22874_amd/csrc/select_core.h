@@ -122,30 +122,26 @@ __device__ __forceinline__ int wg_excl_scan(int v, int* red, int& total) {
 }
 
 
-// Coherent (device-scope) or plain global accesses.  The fused decode step
-// reads scores written by other workgroups of the same launch and publishes
-// its selection to them, so it bypasses the per-XCD L2 caches.
-template <bool COH>
-__device__ __forceinline__ float load_score(const float* p) {
-  if constexpr (COH)
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  else
-    return *p;
-}
-template <bool COH>
-__device__ __forceinline__ void store_i32(int32_t* p, int32_t v) {
-  if constexpr (COH)
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  else
-    *p = v;
-}
-template <bool COH>
-__device__ __forceinline__ void store_f32(float* p, float v) {
-  if constexpr (COH)
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  else
-    *p = v;
-}
+// Score source of select_row_wg: plain loads of a row of scores.  The fused
+// decode step substitutes a source that polls records written by other
+// workgroups of the same launch.
+struct RowScores {
+  const float* srow;
+  template <int EPT>
+  __device__ __forceinline__ void operator()(float (&sv)[EPT], int j0, int nv) const {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) sv[e] = j0 + e < nv ? srow[j0 + e] : -INFINITY;
+  }
+};
+
+// Optional copies of the selection for readers in other workgroups of the
+// same launch: `copies` runs of `len` words, word i of each run = id + 1 of
+// entry i, or 0xffffffff past the last entry (zero means not written yet).
+// Stored at device scope; base == nullptr publishes nothing.
+struct IdRecords {
+  uint32_t* base;
+  int len, copies;
+};
 
 constexpr int kValBins = 2048;   // value bins of the threshold search
 
@@ -176,9 +172,10 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-// Selection of one row by the whole 256-thread workgroup: srow holds the
-// row's scores (the first nv valid), out its k_max id slots.  Every thread of
-// the workgroup must call it.  Thread t owns the EPT consecutive ids
+// Selection of one row by the whole 256-thread workgroup: src supplies the
+// row's scores (the first nv valid), out receives its k_max id slots, pub
+// optional device-scope copies.  Needs min(k_max, nblk) <= P = 64 * SPL
+// (<= 512).  Every thread of the workgroup must call it.  Thread t owns the EPT consecutive ids
 // [t*EPT, (t+1)*EPT).  Steps, with the workgroup barriers in brackets:
 //  1. load; order-preserving keys of the residual candidates; residual max
 //     M, min and Z = sum exp(s - M) from per-wave partials [1];
@@ -195,15 +192,14 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 //     otherwise they are compacted [2], sorted in wave 0 by (score desc, id
 //     asc), prefix-summed and cut where the prefix first reaches top_p * Z,
 //     then floored by k_min [1];
-//  4. reserved + chosen ids are written in ascending order [1].
+//  4. reserved + chosen ids are written in ascending order [2].
 // Every reduction has a fixed order, so the result is deterministic.
-template <int EPT, int SPL, bool COH>
-__device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
-                                              const float* __restrict__ srow, int nblk, int nv,
-                                              float top_p, int k_max, int k_min, int n_sink,
-                                              int n_recent, int32_t* __restrict__ out,
+template <int EPT, int SPL, class Src>
+__device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src& src, int nblk,
+                                              int nv, float top_p, int k_max, int k_min,
+                                              int n_sink, int n_recent, int32_t* __restrict__ out,
                                               int32_t* __restrict__ count_out,
-                                              float* __restrict__ mass_out) {
+                                              float* __restrict__ mass_out, IdRecords pub) {
   constexpr int NT = kSelWG, NW = NT / 64;
   constexpr int P = 64 * SPL;
   constexpr int BPT = kValBins / NT;   // value bins per thread in the scan
@@ -221,11 +217,7 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
   // 1. scores, keys (0 = not a candidate), M, min and Z
   SPOT_SEL_TS(0);
   float sv[EPT];
-#pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    const int j = j0 + e;
-    sv[e] = j < nv ? load_score<COH>(srow + j) : -INFINITY;
-  }
+  src(sv, j0, nv);
   for (int i = tid; i < kValBins; i += NT) sm.hist[i] = 0u;
   if (tid == 0) sm.bc[3] = 0;
   uint32_t key[EPT];
@@ -519,7 +511,9 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
   }
   SPOT_SEL_TS(4);
 
-  // 4. write S = reserved u chosen, ascending
+  // 4. write S = reserved u chosen, ascending: positions by a scan, the ids
+  // staged in LDS (at most 512 of them: min(k_max, nblk) <= P), then written
+  // out by all threads in order
   const uint32_t fin = resv | chosen;
   const int mine = __popc(fin);
   const int incl = wave_incl_scan_i(mine);
@@ -532,13 +526,23 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm,
     pos += w < wave ? t : 0;
     total += t;
   }
+  const int n_out = min(total, k_max);
 #pragma unroll
   for (int e = 0; e < EPT; ++e)
-    if (((fin >> e) & 1u) && pos < k_max) store_i32<COH>(out + pos++, j0 + e);
-  for (int i = total + tid; i < k_max; i += NT) store_i32<COH>(out + i, -1);
+    if (((fin >> e) & 1u) && pos < n_out && pos < kValBins) sm.hist[pos++] = (uint32_t)(j0 + e);
+  __syncthreads();
+  if (pub.base) {
+    const int n_pub = pub.len * pub.copies;
+    for (int t = tid; t < n_pub; t += NT) {
+      const int i = t % pub.len;
+      const uint32_t wd = i < n_out ? sm.hist[i] + 1u : 0xffffffffu;
+      __hip_atomic_store(pub.base + t, wd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  for (int i = tid; i < k_max; i += NT) out[i] = i < n_out ? (int32_t)sm.hist[i] : -1;
   if (tid == 0) {
-    store_i32<COH>(count_out, min(total, k_max));
-    if (mass_out) store_f32<COH>(mass_out, mass);
+    *count_out = n_out;
+    if (mass_out) *mass_out = mass;
   }
   SPOT_SEL_TS(5);
 }

@@ -1,25 +1,26 @@
 // Fused decode step: selector scoring, block selection and block-sparse
-// attention of every sequence in one cooperative launch (paper Section 2:
-// score every KV block, pick blocks by the dual top-p / top-K rule with sink
-// and recency reserved, attend to the chosen blocks only).
+// attention of every sequence in one launch (paper Section 2: score every KV
+// block, pick blocks by the dual top-p / top-K rule with sink and recency
+// reserved, attend to the chosen blocks only).
 //
 // Separate launches pay a kernel boundary (completion, cache maintenance and
 // dispatch of the next grid, a few microseconds each) twice per step, and the
 // attention grid only starts fetching once its dispatch is done.  Here one
 // grid of n_pairs * n_slot workgroups runs
 //   1. scoring: the first kMaxScorers workgroups of each row (workgroup i
-//      serves row i % batch) score a contiguous run of its blocks with
-//      device-scope stores, then raise their own done flag;
-//   2. selection: workgroup r (a scorer of row r) waits for the row's done
-//      flags, clears them, selects the row (the workgroup core shared with
-//      the stand-alone kernel, device-scope loads and stores) and raises the
-//      row's ready flag;
-//   3. attention: every workgroup takes its (pair, slot) of the split-KV
-//      decode (shared core) once its sequence's ready flag is up.
-// One flag per writer keeps the hand-offs free of contended atomics (a
-// counter bumped by every scorer serialises at the memory).  The last
-// workgroup of each sequence clears the ready flag, so all flags and counters
-// are zero again when the launch ends.
+//      serves row i % batch) score a contiguous run of its blocks; each
+//      score also goes out as a self-flagging record word;
+//   2. selection: workgroup r (a scorer of row r) polls the row's score
+//      records (each thread its own ids, as they land), clears them, selects
+//      the row (the workgroup core shared with the stand-alone kernel) and
+//      publishes the block list as record words, one copy per KV head;
+//   3. attention: every workgroup polls the list records of its (sequence,
+//      KV head) share, clears them and runs its (pair, slot) of the split-KV
+//      decode (shared core).
+// A record word is nonzero once written and its reader sets it back to zero,
+// so a hand-off costs one round trip to the device coherence point, there
+// are no flags or contended atomics, and the workspace is all zero again
+// when the launch ends.
 //
 // The waits need every workgroup of the grid to be resident at once: the
 // launcher sizes the grid to the occupancy-derived capacity of the device
@@ -27,7 +28,7 @@
 // start when it drains, since nothing else depends on this grid).  Each wait
 // is also bounded in time (kWaitTicks of the 100 MHz real-time counter), so
 // a wait can never hang the device; an expired wait lets the workgroup
-// finish with whatever the flag guarded.
+// finish with whatever the records held.
 #include "decode_core.h"
 #include "score_core.h"
 #include "select_core.h"
@@ -40,7 +41,8 @@ using namespace dec;
 constexpr int kStepG = 4;                 // GQA group of the fused path (256 threads)
 constexpr int kScoreRun = 8;              // blocks per scoring call of one wave (the
                                           // stand-alone kernel's run: same code, same bits)
-constexpr int kMaxScorers = 64;           // scoring workgroups per row (<= 64: one wave polls)
+constexpr int kMaxScorers = 64;           // scoring workgroups per row
+constexpr int kRecRow = 4096;             // score record words per row (the fused maximum)
 constexpr uint64_t kWaitTicks = 20000000; // 0.2 s of the 100 MHz real-time counter
 
 struct StepArgs {
@@ -67,18 +69,103 @@ struct StepArgs {
   float* ws_o;
   float* ws_ml;
   unsigned* pair_cnt;   // [batch * h_kv] split completion (decode merge)
-  unsigned* done;       // [batch, kMaxScorers] scorer finished
-  unsigned* ready;      // [batch] selection published
-  unsigned* row_done;   // [batch] pairs merged
+  uint32_t* srec;       // [batch, kRecRow] score records
+  uint32_t* irec;       // [batch, h_kv, rec_len] block list records
+  int rec_len;          // min(k_max, nblk)
 };
 
-__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+__device__ __forceinline__ uint64_t now() { return __builtin_amdgcn_s_memrealtime(); }
+
+template <typename W>
+__device__ __forceinline__ W load_rec(const W* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename W>
+__device__ __forceinline__ void store_rec(W* p, W v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Score source of the selector: thread t polls the records of its own ids
+// [j0, j0 + EPT) until every valid one is written (two words per load; the
+// words past nv stay zero all launch), then clears them for the next launch.
+struct PolledScores {
+  uint32_t* rec;   // the row's kRecRow record words
+  template <int EPT>
+  __device__ __forceinline__ void operator()(float (&sv)[EPT], int j0, int nv) const {
+    uint32_t wd[EPT];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) wd[e] = 0u;
+    const uint64_t deadline = now() + kWaitTicks;
+    for (;;) {
+      bool all = true;
+      if constexpr (EPT % 2 == 0) {
+#pragma unroll
+        for (int e = 0; e < EPT; e += 2) {
+          const bool need = (j0 + e < nv && wd[e] == 0u) || (j0 + e + 1 < nv && wd[e + 1] == 0u);
+          if (need) {
+            const uint64_t x = load_rec(reinterpret_cast<const uint64_t*>(rec + j0 + e));
+            wd[e] = (uint32_t)x;
+            wd[e + 1] = (uint32_t)(x >> 32);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+          if (j0 + e < nv && wd[e] == 0u) wd[e] = load_rec(rec + j0 + e);
+      }
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) all = all && (j0 + e >= nv || wd[e] != 0u);
+      if (all || now() > deadline) break;
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if constexpr (EPT % 2 == 0) {
+#pragma unroll
+      for (int e = 0; e < EPT; e += 2)
+        if (j0 + e < nv) store_rec(reinterpret_cast<uint64_t*>(rec + j0 + e), (uint64_t)0);
+    } else {
+#pragma unroll
+      for (int e = 0; e < EPT; ++e)
+        if (j0 + e < nv) store_rec(rec + j0 + e, 0u);
+    }
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) sv[e] = j0 + e < nv ? score_of_word(wd[e]) : -INFINITY;
+  }
+};
+
+// Block list source of an attention workgroup: entries slot, slot + n_slot,
+// ... of its (sequence, KV head) copy of the list records (the stand-alone
+// decode's share of the same list, in the same order), polled until written,
+// then cleared.  Called by wave 0.
+struct PolledList {
+  const uint32_t* irec;
+  int h_kv, rec_len;
+  __device__ __forceinline__ int operator()(int* ids, int b, int g, int slot, int n_slot,
+                                            int nb_valid) const {
+    const int lane = __lane_id();
+    uint32_t* rec = const_cast<uint32_t*>(irec) + ((size_t)b * h_kv + g) * rec_len;
+    const uint64_t deadline = now() + kWaitTicks;
+    int cnt = 0;
+    for (int base = slot; base < rec_len; base += 64 * n_slot) {
+      const int e = base + lane * n_slot;
+      uint32_t wd = e < rec_len ? 0u : 0xffffffffu;
+      for (;;) {
+        if (wd == 0u) wd = load_rec(rec + e);
+        if (__ballot(wd == 0u) == 0ull || now() > deadline) break;
+        __builtin_amdgcn_s_sleep(1);
+      }
+      if (e < rec_len) store_rec(rec + e, 0u);
+      const int j = wd == 0u || wd == 0xffffffffu ? -1 : (int)(wd - 1u);
+      cnt = append_ids(ids, cnt, j, nb_valid);
+    }
+    return min(cnt, kMaxIds);
+  }
+};
 
 template <int KFMT, int LPH>
 __device__ __forceinline__ void score_run(const StepArgs& a, int row, int nv, int j0, int jend,
                                           int lane) {
-  score_blocks<KFMT, LPH, kScoreRun, true>(a.q_sel, a.w, a.k_sel, a.k_scale, row, row, a.nblk,
-                                           nv, j0, jend, a.scores, lane);
+  score_blocks<KFMT, LPH, kScoreRun>(a.q_sel, a.w, a.k_sel, a.k_scale, row, row, a.nblk, nv, j0,
+                                     jend, a.scores, a.srec + (size_t)row * kRecRow, lane);
 }
 
 __device__ __forceinline__ void score_run_rt(const StepArgs& a, int row, int nv, int j0, int jend,
@@ -118,57 +205,23 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
     const int jb = c * per, je = min(jb + per, a.nblk);
     for (int j0 = jb + wave * kScoreRun; j0 < je; j0 += kStepG * kScoreRun)
       score_run_rt(a, r, nv, j0, je, lane);
-    wait_vm();  // this thread's score stores are visible device-wide
-    __syncthreads();
-    if (tid == 0)
-      __hip_atomic_store(&a.done[r * kMaxScorers + c], 1u, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
   }
 
   // ---- 2. selection of row wg by workgroup wg (wg < B is scorer 0 of it)
   if (wg < B) {
-    if (wave == 0) {
-      const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + kWaitTicks;
-      unsigned* flag = &a.done[wg * kMaxScorers + lane];
-      for (;;) {
-        const bool up = lane >= n_sc ||
-                        __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
-        if (__ballot(!up) == 0 || __builtin_amdgcn_s_memrealtime() > deadline) break;
-        __builtin_amdgcn_s_sleep(2);
-      }
-      if (lane < n_sc) __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    __syncthreads();
-    select_row_wg<EPT, SPL, true>(sm.sel, a.scores + (size_t)wg * a.nblk, a.nblk, nv, a.top_p,
-                                  a.k_max, a.k_min, a.n_sink, a.n_recent,
-                                  a.idx + (size_t)wg * a.k_max, a.count + wg,
-                                  a.mass ? a.mass + wg : nullptr);
-    wait_vm();
-    __syncthreads();
-    if (tid == 0) __hip_atomic_store(&a.ready[wg], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    select_row_wg<EPT, SPL>(sm.sel, PolledScores{a.srec + (size_t)wg * kRecRow}, a.nblk, nv,
+                            a.top_p, a.k_max, a.k_min, a.n_sink, a.n_recent,
+                            a.idx + (size_t)wg * a.k_max, a.count + wg,
+                            a.mass ? a.mass + wg : nullptr,
+                            IdRecords{a.irec + (size_t)wg * a.h_kv * a.rec_len, a.rec_len,
+                                      a.h_kv});
+    __syncthreads();   // the selection's LDS is reused below
   }
 
-  // ---- 3. attention for (pair, slot) once the sequence's selection is out
-  const int pair = wg / a.n_slot, slot = wg % a.n_slot;
-  const int b = pair / a.h_kv;
-  if (tid == 0) {
-    const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + kWaitTicks;
-    while (__hip_atomic_load(&a.ready[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u &&
-           __builtin_amdgcn_s_memrealtime() <= deadline)
-      __builtin_amdgcn_s_sleep(8);
-  }
-  __syncthreads();
-  const bool merged = decode_body<kStepG, false, true>(
-      sm.dec, pair, slot, a.q, a.k, a.v, a.seq_len, a.idx, a.count, a.k_max, a.h_q, a.h_kv,
-      a.l_cap, a.scale_log2, a.n_slot, a.ws_o, a.ws_ml, a.pair_cnt, a.out, a.lse);
-  if (merged && tid == 0) {
-    const unsigned prev =
-        __hip_atomic_fetch_add(&a.row_done[b], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (prev == (unsigned)(a.h_kv - 1)) {
-      __hip_atomic_store(&a.row_done[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&a.ready[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
+  // ---- 3. attention for (pair, slot) on the published block list
+  decode_body<kStepG, false>(sm.dec, PolledList{a.irec, a.h_kv, a.rec_len}, wg / a.n_slot,
+                             wg % a.n_slot, a.q, a.k, a.v, a.seq_len, a.h_q, a.h_kv, a.l_cap,
+                             a.scale_log2, a.n_slot, a.ws_o, a.ws_ml, a.pair_cnt, a.out, a.lse);
 }
 
 // Workgroups of one step kernel that can be resident at once (per CU times
@@ -202,13 +255,19 @@ hipError_t launch_step_t(StepArgs& a, int n_pairs, int n_slot_max, hipStream_t s
 
 }  // namespace
 
+// Workspace: the split-decode partials and pair counters, then (16-byte
+// aligned) the score records [batch, kRecRow] and the list records
+// [batch, h_kv, min(k_max, nblk)] (sized for k_max).
+static size_t step_records_offset(int batch, int h_q, int h_kv, int d, int k_max) {
+  return (decode_workspace_bytes(batch, h_q, h_kv, d, k_max) + 15) & ~(size_t)15;
+}
 size_t step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max) {
-  return decode_workspace_bytes(batch, h_q, h_kv, d, k_max) +
-         (size_t)batch * (kMaxScorers + 2) * sizeof(unsigned);
+  return step_records_offset(batch, h_q, h_kv, d, k_max) +
+         (size_t)batch * (kRecRow + (size_t)h_kv * k_max) * sizeof(uint32_t);
 }
 
 bool step_fusable(int h_q, int h_kv, int nblk, int k_max) {
-  if (h_q != kStepG * h_kv || nblk < 1 || nblk > 4096) return false;
+  if (h_q != kStepG * h_kv || nblk < 1 || nblk > kRecRow) return false;
   int P = 1;
   const int cap = k_max < nblk ? k_max : nblk;
   while (P < cap) P <<= 1;
@@ -256,9 +315,10 @@ hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_s
   a.ws_o = static_cast<float*>(ws);
   a.ws_ml = a.ws_o + (size_t)batch * h_q * n_slot_max * kD;
   a.pair_cnt = reinterpret_cast<unsigned*>(a.ws_ml + (size_t)batch * h_q * n_slot_max * 2);
-  a.done = a.pair_cnt + n_pairs;
-  a.ready = a.done + (size_t)batch * kMaxScorers;
-  a.row_done = a.ready + batch;
+  a.srec = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) +
+                                       step_records_offset(batch, h_q, h_kv, kD, k_max));
+  a.irec = a.srec + (size_t)batch * kRecRow;
+  a.rec_len = k_max < a.nblk ? k_max : a.nblk;
   // The partial buffers are laid out for n_slot_max; a smaller n_slot (when
   // fewer workgroups fit) uses a prefix of each head's run, indexed with the
   // actual n_slot -- the layout is [B, h_q, n_slot] either way.

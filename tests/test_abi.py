@@ -78,6 +78,9 @@ def test_validation_errors_before_launch(lib):
     assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 32, 8, 128, 4000, 0.1, nz, None, nz, 1 << 20, None) == 2
     assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 32, 8, 128, 4096, 0.1, nz, None, nz, 0, None) == 5
     assert dec(nz, nz, nz, nz, None, nz, 4, 1, 32, 8, 128, 4096, 0.1, nz, None, nz, 1 << 20, None) == 1
+    # a workspace that is not 16-byte aligned
+    assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 32, 8, 128, 4096, 0.1, nz, None, P(24), 1 << 20,
+               None) == 5
     den = lib.spot_dense_decode
     assert den(nz, nz, nz, nz, 1, 32, 8, 128, 4096, 0.1, nz, None, nz, 16, None) == 5
     pre = lib.spot_sparse_prefill
@@ -112,8 +115,11 @@ def test_validation_errors_before_launch(lib):
     assert call(k_max=5000) == 3
     assert call(ws_bytes=16) == 5
     assert call(ws=None) == 5
+    assert call(ws=P(24)) == 5                   # not 16-byte aligned
+    # decode partials and counters, then 4096 score records and h_kv * k_max
+    # list records per sequence
     assert lib.spot_decode_step_workspace_bytes(4, 32, 8, 128, 128) >= \
-        lib.spot_decode_workspace_bytes(4, 32, 8, 128, 128) + 4 * 66 * 4
+        lib.spot_decode_workspace_bytes(4, 32, 8, 128, 128) + 4 * (4096 + 8 * 128) * 4
 
 
 def test_workspace_size_query(lib):
