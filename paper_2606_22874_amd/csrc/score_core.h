@@ -102,10 +102,11 @@ __device__ __forceinline__ float score_of_word(uint32_t w) { return __uint_as_fl
 // (sequence `seq`), all key loads issued before any arithmetic; blocks at or
 // past nv score -inf.  A non-null rec (the row's record words, indexed by
 // block) also receives score_word() of each valid block's score, stored at
-// device scope (a reader in another workgroup
-// of the same launch polls these words: zero means not written yet).
+// device scope (a reader in another workgroup of the same launch polls these
+// words: zero means not written yet).  Returns, in lane u < U, the score of
+// block j0 + u (-inf in the other lanes and past jend).
 template <int KFMT, int LPH, int U>
-__device__ __forceinline__ void score_blocks(const uint16_t* __restrict__ q_sel,
+__device__ __forceinline__ float score_blocks(const uint16_t* __restrict__ q_sel,
                                              const float* __restrict__ w,
                                              const uint8_t* __restrict__ k_sel,
                                              const uint8_t* __restrict__ k_scale, int row,
@@ -140,14 +141,14 @@ __device__ __forceinline__ void score_blocks(const uint16_t* __restrict__ q_sel,
     if (lane == u) res = v;
   }
   const int j = j0 + lane;
+  const float val = lane < U && j < nv && j < jend ? res : -INFINITY;
   if (lane < U && j < jend) {
-    float* dst = scores + (size_t)row * nblk + j;
-    const float val = j < nv ? res : -INFINITY;
     if (rec && j < nv)
       __hip_atomic_store(rec + j, score_word(val), __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
-    *dst = val;
+    scores[(size_t)row * nblk + j] = val;
   }
+  return val;
 }
 
 }  // namespace spot

@@ -149,14 +149,18 @@ constexpr int kValBins = 2048;   // value bins of the threshold search
 #define SPOT_SEL_TS(i) ((void)0)
 #endif
 
+constexpr int kFine = kValBins / 64;   // value bins per coarse bin
+
 template <int EPT, int SPL>
 struct SelWgSmem {
   uint32_t hist[kValBins];        // value-bin counts (the fallback radix uses 256)
-  uint64_t s_K[64 * SPL];         // threshold-bin members / survivors
+  uint32_t hist2[64];             // coarse counts: kFine value bins each
+  uint64_t s_K[64 * (SPL > 4 ? SPL : 4)];   // threshold-bin members (64 per wave) / survivors
   uint32_t red_u[kSelWG / 64][2];
   float red_f[kSelWG / 64];
   float red_m[kSelWG / 64];       // survivors' mass partials
   int red_i[kSelWG / 64];
+  int gc[kSelWG / 64];            // threshold-bin members per wave
   int bc[4];
   uint64_t cut;
   float cut_mass;
@@ -175,19 +179,20 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 // Selection of one row by the whole 256-thread workgroup: src supplies the
 // row's scores (the first nv valid), out receives its k_max id slots, pub
 // optional device-scope copies.  Needs min(k_max, nblk) <= P = 64 * SPL
-// (<= 512).  Every thread of the workgroup must call it.  Thread t owns the EPT consecutive ids
-// [t*EPT, (t+1)*EPT).  Steps, with the workgroup barriers in brackets:
+// (<= 512).  Every thread of the workgroup must call it.  Thread t owns the
+// EPT consecutive ids [t*EPT, (t+1)*EPT).  Steps, with the workgroup barriers
+// in brackets:
 //  1. load; order-preserving keys of the residual candidates; residual max
 //     M, min and Z = sum exp(s - M) from per-wave partials [1];
 //  2. when the cap C binds: a histogram over 2048 equal-width value bins
-//     between the candidate min and max [1]; a scan over the bins finds the
-//     bin holding the C-th best candidate (score desc, id asc) [2]; the
-//     bin's members are gathered while every thread sums the mass of its
-//     candidates in better bins [1]; wave 0 ranks the members by counting
-//     and publishes the packed cut key and the members' share of the mass
-//     [1].  The survivors are the candidates whose packed key reaches the
-//     cut.  A bin too crowded to rank (heavy ties) falls back to an 8-bit
-//     radix select on the keys;
+//     between the candidate min and max, and over 64 coarse bins of 32 [1];
+//     every wave scans the coarse and then the fine counts for the bin
+//     holding the C-th best candidate (score desc, id asc); each wave packs
+//     its members of that bin and sums the mass of its candidates in better
+//     bins [1]; every wave ranks the members by counting and derives the
+//     packed cut key and the mass of the survivors.  The survivors are the
+//     candidates whose packed key reaches the cut.  A bin too crowded to
+//     rank (heavy ties) falls back to an 8-bit radix select on the keys;
 //  3. below top_p * Z the cap binds and the survivors are the answer;
 //     otherwise they are compacted [2], sorted in wave 0 by (score desc, id
 //     asc), prefix-summed and cut where the prefix first reaches top_p * Z,
@@ -218,8 +223,10 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   SPOT_SEL_TS(0);
   float sv[EPT];
   src(sv, j0, nv);
-  for (int i = tid; i < kValBins; i += NT) sm.hist[i] = 0u;
-  if (tid == 0) sm.bc[3] = 0;
+  static_assert(kValBins == NT * 8, "two 16-byte zero stores per thread");
+  reinterpret_cast<uint4*>(sm.hist)[2 * tid] = make_uint4(0u, 0u, 0u, 0u);
+  reinterpret_cast<uint4*>(sm.hist)[2 * tid + 1] = make_uint4(0u, 0u, 0u, 0u);
+  if (tid < 64) sm.hist2[tid] = 0u;
   uint32_t key[EPT];
   uint32_t cand = 0, resv = 0;
   {
@@ -293,69 +300,74 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
       for (int e = 0; e < EPT; ++e) {
         // bins ascend as values descend; clamped in float first
         bin[e] = (int)fminf((vhi - sv[e]) * inv_w, (float)(kValBins - 1));
-        if (key[e]) atomicAdd(&sm.hist[bin[e]], 1u);
+        if (key[e]) {
+          atomicAdd(&sm.hist[bin[e]], 1u);
+          atomicAdd(&sm.hist2[bin[e] / kFine], 1u);
+        }
       }
       __syncthreads();
       SPOT_SEL_TS(6);
-      int c[BPT], tot = 0;
-#pragma unroll
-      for (int i = 0; i < BPT; ++i) {
-        c[i] = (int)sm.hist[BPT * tid + i];
-        tot += c[i];
-      }
-      const int incl = wave_incl_scan_i(tot);
-      if (lane == 63) sm.red_i[wave] = incl;
-      __syncthreads();
-      int before = incl - tot;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) before += w < wave ? sm.red_i[w] : 0;
-#pragma unroll
-      for (int i = 0; i < BPT; ++i) {
-        if (before < cap && cap <= before + c[i]) {
-          sm.bc[0] = BPT * tid + i;
-          sm.bc[1] = cap - before;
-          sm.bc[2] = c[i];
-        }
-        before += c[i];
-      }
-      __syncthreads();
+      // Every wave finds the bin of the cap-th best candidate on its own: a
+      // scan over the 64 coarse bins, then over the 32 fine bins of the
+      // coarse bin that holds it (no barrier).
+      const int cc = (int)sm.hist2[lane];
+      const int c_incl = wave_incl_scan_i(cc);
+      const int cb = min(__builtin_ctzll(__ballot(c_incl >= cap)), 63);
+      const int c_before = __builtin_amdgcn_readlane(c_incl - cc, cb);
+      const int fc = lane < kFine ? (int)sm.hist[cb * kFine + lane] : 0;
+      const int f_incl = wave_incl_scan_i(fc) + c_before;
+      const int fb = min(__builtin_ctzll(__ballot(lane < kFine && f_incl >= cap)), kFine - 1);
+      const int b_star = cb * kFine + fb;
+      const int need = cap - __builtin_amdgcn_readlane(f_incl - fc, fb);
+      const int in_bin = __builtin_amdgcn_readlane(fc, fb);
       SPOT_SEL_TS(7);
-      const int b_star = sm.bc[0], need = sm.bc[1], in_bin = sm.bc[2];
       if (in_bin <= 64) {
         crowded = false;
-        // gather the bin's members; sum the mass of better bins
+        // each wave packs its members of the bin into its own run of s_K and
+        // sums the mass of its candidates in better bins
+        uint32_t mm = 0u;
         float ma = 0.f;
 #pragma unroll
         for (int e = 0; e < EPT; ++e) {
-          if (key[e] && bin[e] == b_star) sm.s_K[atomicAdd(&sm.bc[3], 1)] = rank_key(key[e], j0 + e);
+          mm |= (uint32_t)(key[e] && bin[e] == b_star) << e;
           ma += key[e] && bin[e] < b_star ? pe[e] : 0.f;
         }
+        const int nm = __popc(mm);
+        const int m_incl = wave_incl_scan_i(nm);
+        int slot = wave * 64 + m_incl - nm;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+          if ((mm >> e) & 1u) sm.s_K[slot++] = rank_key(key[e], j0 + e);
         const float mw = wave_sum(ma);
+        if (lane == 63) sm.gc[wave] = m_incl;
         if (lane == 0) sm.red_m[wave] = mw;
         __syncthreads();
         SPOT_SEL_TS(8);
-        if (wave == 0) {
-          // member j sits in lane j; its rank is the number of better members
-          const uint64_t mine = lane < in_bin ? sm.s_K[lane] : 0ull;
-          int better = 0;
-          for (int j = 0; j < in_bin; ++j) better += readlane_u64(mine, j) > mine ? 1 : 0;
-          const bool top = lane < in_bin && better < need;
-          const float x = top ? __builtin_amdgcn_exp2f(
-                                    (order_key_inv((uint32_t)(mine >> 32)) - M) * kLog2e)
-                              : 0.f;
-          const float m_in = wave_sum(x);
-          const int src = __builtin_ctzll(__ballot(lane < in_bin && better == need - 1));
-          if (lane == 0) {
-            sm.cut = readlane_u64(mine, src);
-            sm.cut_mass = m_in;
+        // every wave ranks the members (member l in lane l) by counting the
+        // better ones and derives the same cut and mass (no barrier)
+        int w_of = 0, base = 0, run = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+          const int n_w = sm.gc[w];
+          if (lane >= run) {
+            w_of = w;
+            base = run;
           }
-          // (readlane above is wave-uniform; lane 0 stores it)
+          run += n_w;
         }
-        __syncthreads();
-        const uint64_t kc = sm.cut;
+        const uint64_t mine = lane < in_bin ? sm.s_K[w_of * 64 + lane - base] : 0ull;
+        int better = 0;
+        for (int j = 0; j < in_bin; ++j) better += readlane_u64(mine, j) > mine ? 1 : 0;
+        const bool top = lane < in_bin && better < need;
+        const float x = top ? __builtin_amdgcn_exp2f(
+                                  (order_key_inv((uint32_t)(mine >> 32)) - M) * kLog2e)
+                            : 0.f;
+        const float m_in = wave_sum(x);
+        const int src = __builtin_ctzll(__ballot(lane < in_bin && better == need - 1));
+        const uint64_t kc = readlane_u64(mine, src);
         kt = (uint32_t)(kc >> 32);
         it = (int)(0xffffffffu - (uint32_t)kc);
-        msum = sm.cut_mass;
+        msum = m_in;
 #pragma unroll
         for (int w = 0; w < NW; ++w) msum += sm.red_m[w];
         have_msum = true;
@@ -365,6 +377,7 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   if (crowded) {
     // 8-bit radix select by count on the keys, from the highest bit where
     // the candidates differ; equal keys at the threshold go to lower ids.
+    __syncthreads();   // every wave is done reading the value histograms
     const uint32_t diff = kmin ^ kmax;
     int shift = diff ? 32 - __builtin_clz(diff) : 0;
     uint32_t prefix = shift >= 32 ? 0u : (kmax >> shift) << shift;
@@ -532,11 +545,11 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
     if (((fin >> e) & 1u) && pos < n_out && pos < kValBins) sm.hist[pos++] = (uint32_t)(j0 + e);
   __syncthreads();
   if (pub.base) {
-    const int n_pub = pub.len * pub.copies;
-    for (int t = tid; t < n_pub; t += NT) {
-      const int i = t % pub.len;
+    for (int i = tid; i < pub.len; i += NT) {
       const uint32_t wd = i < n_out ? sm.hist[i] + 1u : 0xffffffffu;
-      __hip_atomic_store(pub.base + t, wd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int c = 0; c < pub.copies; ++c)
+        __hip_atomic_store(pub.base + (size_t)c * pub.len + i, wd, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     }
   }
   for (int i = tid; i < k_max; i += NT) out[i] = i < n_out ? (int32_t)sm.hist[i] : -1;
