@@ -88,20 +88,10 @@ struct KeyLoad<SPOT_KFMT_MXFP4_G32> {
   }
 };
 
-// Self-flagging record of a score for readers in other workgroups: the bit
-// complement of the float, so that no score maps to the zero "not written"
-// word (the only float whose complement is zero, the NaN with every bit set,
-// is replaced by the canonical quiet NaN first).
-__device__ __forceinline__ uint32_t score_word(float v) {
-  const uint32_t u = __float_as_uint(v);
-  return ~(u == 0xffffffffu ? 0x7fc00000u : u);
-}
-__device__ __forceinline__ float score_of_word(uint32_t w) { return __uint_as_float(~w); }
-
 // One wavefront scores blocks j0 .. min(j0 + U, jend) - 1 of query row `row`
 // (sequence `seq`), all key loads issued before any arithmetic; blocks at or
 // past nv score -inf.  A non-null rec (the row's record words, indexed by
-// block) also receives score_word() of each valid block's score, stored at
+// block) also receives rec_word() of each valid block's score, stored at
 // device scope (a reader in another workgroup of the same launch polls these
 // words: zero means not written yet).  Returns, in lane u < U, the score of
 // block j0 + u (-inf in the other lanes and past jend).
@@ -144,7 +134,7 @@ __device__ __forceinline__ float score_blocks(const uint16_t* __restrict__ q_sel
   const float val = lane < U && j < nv && j < jend ? res : -INFINITY;
   if (lane < U && j < jend) {
     if (rec && j < nv)
-      __hip_atomic_store(rec + j, score_word(val), __ATOMIC_RELAXED,
+      __hip_atomic_store(rec + j, rec_word(val), __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     scores[(size_t)row * nblk + j] = val;
   }

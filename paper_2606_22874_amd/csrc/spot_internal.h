@@ -50,6 +50,16 @@ constexpr int kDppHalfMirror = 0x141;    // lane i <-> 7 - i within 8
 constexpr int kDppMirror = 0x140;        // lane i <-> 15 - i within 16
 constexpr int kDppRowShr1 = 0x111;
 
+// Self-flagging record word of a float for readers in other workgroups of
+// the same launch: the bit complement, so that no value maps to the zero
+// "not written yet" word (the only float whose complement is zero, the NaN
+// with every bit set, is replaced by the canonical quiet NaN first).
+__device__ __forceinline__ uint32_t rec_word(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return ~(u == 0xffffffffu ? 0x7fc00000u : u);
+}
+__device__ __forceinline__ float rec_value(uint32_t w) { return __uint_as_float(~w); }
+
 __device__ __forceinline__ float readlane_f(float x, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
 }

@@ -128,7 +128,7 @@ struct PolledScores {
         if (j0 + e < nv) store_rec(rec + j0 + e, 0u);
     }
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) sv[e] = j0 + e < nv ? score_of_word(wd[e]) : -INFINITY;
+    for (int e = 0; e < EPT; ++e) sv[e] = j0 + e < nv ? rec_value(wd[e]) : -INFINITY;
   }
 };
 
