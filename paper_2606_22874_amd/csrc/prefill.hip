@@ -9,8 +9,9 @@
 //
 // Per wave and key block (64 keys x 32 queries, head dim 128) the math runs
 // transposed so that no score ever leaves the registers:
-//   S^T = K Q^T       16 v_mfma_f32_16x16x32_bf16 tiles  (K from LDS as the
-//                     A operand, Q^T held in VGPRs as the B operand)
+//   S^T = K Q^T       32 v_mfma_f32_16x16x32_bf16 (K from LDS as the A
+//                     operand, Q^T held in VGPRs for the whole key loop as
+//                     the B operand)
 //   online softmax    per query = per lane column; column max over the four
 //                     16-lane groups with two cross-lane exchanges
 //   O^T += V^T P^T    P^T goes straight from the accumulators to the B
@@ -46,7 +47,6 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr float kLazy = 8.f;
 
-constexpr int kQWaveBytes = 32 * kRowBytes;     // 32 query rows of one wave
 
 // Physical 16-byte chunk of logical chunk c in tile row r.  K is read as 16
 // rows x one chunk per quarter wave, so rows must map one chunk to distinct
@@ -119,16 +119,16 @@ __device__ __forceinline__ bf16x8 lds_frag(const unsigned char* base, int r, int
 
 // S^T[key][query] of one key block for the wave's 32 queries: 4 key tiles x
 // 2 query tiles, eight independent accumulation chains, head dim outermost.
-// The operands of step ks+1 are read from LDS before the MFMAs of step ks
+// The K fragments of step ks+1 are read from LDS before the MFMAs of step ks
 // are issued, so the read latency hides behind matrix work.
-__device__ __forceinline__ void qk_tile(const unsigned char* Kt, const unsigned char* Qw,
+__device__ __forceinline__ void qk_tile(const unsigned char* Kt, const bf16x8 (&qf)[4][2],
                                         f32x4 (&s)[2][4], int G, int r16) {
   bf16x8 a[2][4], bq[2][2];
   auto load = [&](int ks, int slot) {
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) a[slot][kt] = lds_frag(Kt, kt * 16 + r16, ks * 4 + G);
-    bq[slot][0] = lds_frag(Qw, r16, ks * 4 + G);
-    bq[slot][1] = lds_frag(Qw, 16 + r16, ks * 4 + G);
+    bq[slot][0] = qf[ks][0];
+    bq[slot][1] = qf[ks][1];
   };
   load(0, 0);
 #pragma unroll
@@ -193,7 +193,7 @@ __device__ __forceinline__ void pv_tile(const unsigned char* Vt, const bf16x8 (&
 
 template <int W>
 struct PrefillWave {
-  const unsigned char* qw;   // this wave's 32 query rows in LDS
+  bf16x8 qf[4][2];           // Q^T B operand [ks][qt]
   f32x4 o[2][8];
   f32x4 s[2][4];             // scores S^T of the current tile
   float m_run[2], l_run[2];
@@ -206,7 +206,7 @@ struct PrefillWave {
   __device__ __forceinline__ void matrix_phase(bool do_qk, const unsigned char* Kt, bool do_pv,
                                                const unsigned char* Vp) {
     if (do_pv) pv_tile(Vp, pb, o, G, r16);
-    if (do_qk) qk_tile(Kt, qw, s, G, r16);
+    if (do_qk) qk_tile(Kt, qf, s, G, r16);
   }
 
   // Vector phase: online softmax of the tile in s into pb.  DIAG masks keys
@@ -296,7 +296,6 @@ __global__ __launch_bounds__(64 * W) void prefill_kernel(
   // another and does not wait for the loads in flight before reading.
   __shared__ __attribute__((aligned(16))) unsigned char sk0[kTileBytes], sk1[kTileBytes];
   __shared__ __attribute__((aligned(16))) unsigned char sv0[kTileBytes], sv1[kTileBytes];
-  __shared__ __attribute__((aligned(16))) unsigned char sq[W][kQWaveBytes];
   __shared__ int s_ids[kPrefillMaxIds];
   __shared__ int s_n_local, s_has_diag;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -343,19 +342,18 @@ __global__ __launch_bounds__(64 * W) void prefill_kernel(
   wv.r16 = lane & 15;
   wv.qoff = (wave & 1) * 32;
   wv.c = c;
-  // The wave's 32 query rows go to LDS (same chunk swizzle as K); the QK
-  // product reads them as the B operand: lane holds Q[16 qt + l%16][32 ks +
-  // 8(l/16) ..+7].
-  wv.qw = sq[wave];
+  // The wave's 32 query rows stay in registers as the QK product's B
+  // operand for the whole key loop: lane holds Q[16 qt + l%16][32 ks +
+  // 8(l/16) ..+7] in qf[ks][qt].
   {
     const uint16_t* qh = q + ((int64_t)(b * h_q + h) * L + qb * kBlk + wv.qoff) * kD;
 #pragma unroll
-    for (int u = 0; u < kQWaveBytes / (kWave * 16); ++u) {
-      const int p = u * kWave + lane;
-      const int r = p >> 4, lc = swz_k(r, p & 15);
-      __builtin_amdgcn_global_load_lds(qh + r * kD + lc * 8,
-                                       (lds_void*)(sq[wave] + u * kWave * 16), 16, 0, 0);
-    }
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt)
+        wv.qf[ks][qt] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(qh + (qt * 16 + wv.r16) * kD + ks * 32 +
+                                                    8 * wv.G));
   }
 #pragma unroll
   for (int qt = 0; qt < 2; ++qt) {
