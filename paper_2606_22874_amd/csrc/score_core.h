@@ -113,12 +113,14 @@ __device__ __forceinline__ float score_blocks(const uint16_t* __restrict__ q_sel
   qf[6] = bf16_lo(qraw.w); qf[7] = bf16_hi(qraw.w);
   const float wh = w[(size_t)row * kHeads + lane / LPH];
 
+  // Every slot loads (branch-free, so the loads of all U blocks fly
+  // together); a slot past the last valid block rereads that block (or
+  // block 0), which stays in bounds and in cache, and its score is dropped.
   KeyLoad<KFMT> key[U];
+  const int jlim = min(jend, max(nv, 1)) - 1;
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int j = j0 + u;
-    if (j < nv && j < jend) key[u].load(k_sel, k_scale, (size_t)seq * nblk + j, lane);
-  }
+  for (int u = 0; u < U; ++u)
+    key[u].load(k_sel, k_scale, (size_t)seq * nblk + min(j0 + u, jlim), lane);
   float res = 0.f;
 #pragma unroll
   for (int u = 0; u < U; ++u) {
