@@ -39,7 +39,10 @@ def parse():
     ap.add_argument("--copies", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--dense", action="store_true", help="also time the dense decode baseline")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense decode baseline")
+    ap.add_argument("--dense", action="store_true", help=argparse.SUPPRESS)   # the default
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the quantized-selector and smaller-workload decode timings")
     ap.add_argument("--fmt", default="bf16", choices=["bf16", "int4", "mxfp4"])
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the block-sparse prefill leg (32K-token layer)")
@@ -269,7 +272,36 @@ def main():
         },
     }
 
-    if args.dense:
+    if not args.no_extra and args.fmt == "bf16":
+        # The same step with the 4-bit selector caches (INT4-g32 / MXFP4-g32,
+        # quantized from the BF16 cache): fewer selector bytes, same K/V.
+        quant = {}
+        for fmt, qfn in (("int4", synth.quantize_int4_g32), ("mxfp4", synth.quantize_mxfp4_g32)):
+            codes, scales = qfn(wl.k_sel)
+            sc = scales.view(np.int16) if fmt == "int4" else scales
+            qsel = [(torch.from_numpy(np.ascontiguousarray(codes)).to(dev),
+                     torch.from_numpy(np.ascontiguousarray(sc)).to(dev))
+                    for _ in range(args.copies)]
+
+            def qstep(c, fmt=fmt, qsel=qsel):
+                k, v, _, _ = copies[c % len(copies)]
+                ks, sc_ = qsel[c % len(qsel)]
+                spot.spot_decode_step(q_sel, w, ks, sc_, fmt, wl.Hs, wl.ds, n_valid, rule.top_p,
+                                      rule.k_max, rule.k_min, rule.n_sink, rule.n_recent, q, k,
+                                      v, seq_len, B, Hq, Hkv, d, L, wl.sm_scale, scores, idx,
+                                      cnt, mass, out, lse, ws_step, stream)
+
+            for i in range(args.warmup):
+                qstep(i)
+            qms = timed(qstep, args.steps)
+            qbytes = codes.nbytes + scales.nbytes + attn_bytes
+            quant[fmt] = {"us_per_step": round(qms * 1e3, 2), "steps_per_s": round(1e3 / qms, 1),
+                          "bytes_per_step": int(qbytes),
+                          "hbm_frac": round(qbytes / (qms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            log(f"[bench] {fmt} selector cache: {qms * 1e3:.1f} us/step")
+        result["config"]["quantized_selector"] = quant
+
+    if not args.no_dense:
         wsd = spot.decode_workspace(B, Hq, Hkv, d, nblk, dev)
 
         def dense(i):
@@ -287,8 +319,14 @@ def main():
             "hbm_frac": round(dbytes / (dms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         }
 
-    if not args.no_prefill:
+    if not args.no_extra:
         del copies, bufs
+        torch.cuda.empty_cache()
+        result["config"]["smaller_workloads"] = small_decode_legs(args, torch, spot, synth, dev,
+                                                                  timed)
+
+    if not args.no_prefill:
+        copies = bufs = None
         torch.cuda.empty_cache()
         result["prefill"] = prefill_leg(args, torch, spot, synth, dev, timed)
 
@@ -296,6 +334,55 @@ def main():
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
+
+
+def small_decode_legs(args, torch, spot, synth, dev, timed):
+    """The fused decode step on the two smaller decode workloads (4K tokens,
+    batch 1, K_max 16; 32K tokens, batch 8, K_max 64): launch-bound sizes,
+    reported for context."""
+    res = {}
+    for i, name in ((1, "decode L=4096 B=1 p=0.9 K_max=16"),
+                    (2, "decode L=32768 B=8 p=0.9 K_max=64")):
+        wl = synth.decode_config(i)
+        rule = wl.rule
+
+        def bf(a):
+            return spot.to_device_bf16(a, dev)
+
+        q, q_sel, ks = bf(wl.q), bf(wl.q_sel), bf(wl.k_sel)
+        w = torch.from_numpy(wl.w).to(dev)
+        seq_len = torch.from_numpy(wl.seq_len).to(dev)
+        n_valid = torch.from_numpy(wl.n_valid).to(dev)
+        k0, v0 = bf(wl.k), bf(wl.v)
+        kv = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(args.copies - 1)]
+        scores = torch.empty((wl.B, wl.nblk), dtype=torch.float32, device=dev)
+        idx = torch.empty((wl.B, rule.k_max), dtype=torch.int32, device=dev)
+        cnt = torch.empty(wl.B, dtype=torch.int32, device=dev)
+        out = torch.empty((wl.B, wl.Hq, wl.d), dtype=torch.bfloat16, device=dev)
+        ws = spot.step_workspace(wl.B, wl.Hq, wl.Hkv, wl.d, rule.k_max, dev)
+        stream = torch.cuda.current_stream()
+
+        def step(c):
+            k, v = kv[c % len(kv)]
+            spot.spot_decode_step(q_sel, w, ks, None, "bf16", wl.Hs, wl.ds, n_valid, rule.top_p,
+                                  rule.k_max, rule.k_min, rule.n_sink, rule.n_recent, q, k, v,
+                                  seq_len, wl.B, wl.Hq, wl.Hkv, wl.d, wl.L, wl.sm_scale, scores,
+                                  idx, cnt, None, out, None, ws, stream)
+
+        for c in range(args.warmup):
+            step(c)
+        ms = timed(step, args.steps)
+        counts = cnt.cpu().numpy()
+        nbytes = wl.k_sel.nbytes + int(counts.sum()) * 64 * wl.Hkv * wl.d * 4
+        res[f"decode{i}"] = {"workload": name, "us_per_step": round(ms * 1e3, 2),
+                             "steps_per_s": round(1e3 / ms, 1),
+                             "mean_selected_blocks": float(counts.mean()),
+                             "bytes_per_step": int(nbytes),
+                             "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"[bench] {name}: {ms * 1e3:.1f} us/step")
+        del kv, k0, v0
+        torch.cuda.empty_cache()
+    return res
 
 
 def prefill_leg(args, torch, spot, synth, dev, timed):

@@ -19,19 +19,12 @@ __device__ __forceinline__ float f16_to_f32(uint16_t h) {
   return (float)__builtin_bit_cast(_Float16, h);
 }
 
-// E2M1 magnitude code (0..7) -> float: 0, .5, 1, 1.5, 2, 3, 4, 6.
-__device__ __forceinline__ float e2m1_to_f32(uint32_t c) {
-  const uint32_t e = (c >> 1) & 3u, m = c & 1u;
-  // e == 0: subnormal 0 or 0.5; otherwise 2^(e-1) * (1 + m/2).
-  uint32_t bits = e ? (((e + 126u) << 23) | (m << 22)) : (m ? 0x3f000000u : 0u);
-  bits |= (c & 8u) << 28;  // sign
-  return __uint_as_float(bits);
-}
-
 // E8M0 -> 2^(e-127) as float (e = 0 gives the subnormal 2^-127).
 __device__ __forceinline__ float e8m0_to_f32(uint32_t e) {
   return e ? __uint_as_float(e << 23) : __uint_as_float(0x00400000u);
 }
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 template <int KFMT>
 struct KeyLoad;
@@ -81,9 +74,21 @@ struct KeyLoad<SPOT_KFMT_MXFP4_G32> {
     scale = ks[blk * 16 + (lane >> 2)];
   }
   __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
-    float a = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) a = fmaf(qf[i], e2m1_to_f32((codes >> (4 * i)) & 15u), a);
+    // v_cvt_scalef32_pk_f32_fp4 (scale 1): byte b of the codes -> the exact
+    // E2M1 values of its low and high nibble (elements 2b, 2b+1); the E8M0
+    // scale is applied once to the sum, in FP32.
+    const f32x2 v0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, 1.0f, 0);
+    const f32x2 v1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, 1.0f, 1);
+    const f32x2 v2 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, 1.0f, 2);
+    const f32x2 v3 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, 1.0f, 3);
+    float a = fmaf(qf[0], v0[0], 0.f);
+    a = fmaf(qf[1], v0[1], a);
+    a = fmaf(qf[2], v1[0], a);
+    a = fmaf(qf[3], v1[1], a);
+    a = fmaf(qf[4], v2[0], a);
+    a = fmaf(qf[5], v2[1], a);
+    a = fmaf(qf[6], v3[0], a);
+    a = fmaf(qf[7], v3[1], a);
     return a * e8m0_to_f32(scale);
   }
 };
