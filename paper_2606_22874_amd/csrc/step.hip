@@ -87,7 +87,9 @@ __device__ __forceinline__ void store_rec(W* p, W v) {
 
 // Score source of the selector: thread t polls the records of its own ids
 // [j0, j0 + EPT) until every valid one is written (two words per load; the
-// words past nv stay zero all launch), then clears them for the next launch.
+// words past nv stay zero all launch).  clear_scores() zeroes them again
+// once the selection is done: a store issued here would hold up the
+// selection's next barrier until it completed.
 struct PolledScores {
   uint32_t* rec;   // the row's kRecRow record words
   template <int EPT>
@@ -118,24 +120,30 @@ struct PolledScores {
       if (all || now() > deadline) break;
       __builtin_amdgcn_s_sleep(1);
     }
-    if constexpr (EPT % 2 == 0) {
-#pragma unroll
-      for (int e = 0; e < EPT; e += 2)
-        if (j0 + e < nv) store_rec(reinterpret_cast<uint64_t*>(rec + j0 + e), (uint64_t)0);
-    } else {
-#pragma unroll
-      for (int e = 0; e < EPT; ++e)
-        if (j0 + e < nv) store_rec(rec + j0 + e, 0u);
-    }
 #pragma unroll
     for (int e = 0; e < EPT; ++e) sv[e] = j0 + e < nv ? rec_value(wd[e]) : -INFINITY;
   }
 };
 
+// Clears thread t's score records [j0, j0 + EPT) below nv (see PolledScores).
+template <int EPT>
+__device__ __forceinline__ void clear_scores(uint32_t* rec, int j0, int nv) {
+  if constexpr (EPT % 2 == 0) {
+#pragma unroll
+    for (int e = 0; e < EPT; e += 2)
+      if (j0 + e < nv) store_rec(reinterpret_cast<uint64_t*>(rec + j0 + e), (uint64_t)0);
+  } else {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+      if (j0 + e < nv) store_rec(rec + j0 + e, 0u);
+  }
+}
+
 // Block list source of an attention workgroup: entries slot, slot + n_slot,
 // ... of its (sequence, KV head) copy of the list records (the stand-alone
-// decode's share of the same list, in the same order), polled until written,
-// then cleared.  Called by wave 0.
+// decode's share of the same list, in the same order), polled until written.
+// Called by wave 0; clear_list() zeroes the same words after the attention
+// (a store here would hold up the next workgroup barrier).
 struct PolledList {
   const uint32_t* irec;
   int h_kv, rec_len;
@@ -153,13 +161,18 @@ struct PolledList {
         if (__ballot(wd == 0u) == 0ull || now() > deadline) break;
         __builtin_amdgcn_s_sleep(1);
       }
-      if (e < rec_len) store_rec(rec + e, 0u);
       const int j = wd == 0u || wd == 0xffffffffu ? -1 : (int)(wd - 1u);
       cnt = append_ids(ids, cnt, j, nb_valid);
     }
     return min(cnt, kMaxIds);
   }
 };
+
+__device__ __forceinline__ void clear_list(uint32_t* irec, int h_kv, int rec_len, int b, int g,
+                                           int slot, int n_slot) {
+  uint32_t* rec = irec + ((size_t)b * h_kv + g) * rec_len;
+  for (int e = slot + __lane_id() * n_slot; e < rec_len; e += 64 * n_slot) store_rec(rec + e, 0u);
+}
 
 template <int KFMT, int LPH>
 __device__ __forceinline__ void score_run(const StepArgs& a, int row, int nv, int j0, int jend,
@@ -215,13 +228,19 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
                             a.mass ? a.mass + wg : nullptr,
                             IdRecords{a.irec + (size_t)wg * a.h_kv * a.rec_len, a.rec_len,
                                       a.h_kv});
-    __syncthreads();   // the selection's LDS is reused below
+    clear_scores<EPT>(a.srec + (size_t)wg * kRecRow, tid * EPT, nv);
+    // The selection's LDS is reused below: every wave's LDS accesses are
+    // done; no wait for the stores in flight.
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
   }
 
   // ---- 3. attention for (pair, slot) on the published block list
-  decode_body<kStepG, false>(sm.dec, PolledList{a.irec, a.h_kv, a.rec_len}, wg / a.n_slot,
-                             wg % a.n_slot, a.q, a.k, a.v, a.seq_len, a.h_q, a.h_kv, a.l_cap,
-                             a.scale_log2, a.n_slot, a.ws_o, a.ws_ml, a.pair_cnt, a.out, a.lse);
+  const int pair = wg / a.n_slot, slot = wg % a.n_slot;
+  decode_body<kStepG, false>(sm.dec, PolledList{a.irec, a.h_kv, a.rec_len}, pair, slot, a.q, a.k,
+                             a.v, a.seq_len, a.h_q, a.h_kv, a.l_cap, a.scale_log2, a.n_slot,
+                             a.ws_o, a.ws_ml, a.pair_cnt, a.out, a.lse);
+  if (wave == 0) clear_list(a.irec, a.h_kv, a.rec_len, pair / a.h_kv, pair % a.h_kv, slot, a.n_slot);
 }
 
 // Workgroups of one step kernel that can be resident at once (per CU times
