@@ -181,11 +181,16 @@ spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
  * scores are in, and the attention workgroups start as soon as that
  * selection is published, with no kernel boundary in between (hand-offs
  * through self-flagging record words in the workspace, which each reader
- * clears again; every wait is bounded in time).  Otherwise
- * (or when no such grid fits) the three stages are launched one after the
- * other on `stream`.  Either way the results are deterministic; the fused
- * path may split the attention over fewer workgroups when fewer fit, which
- * changes the FP32 summation order (not the block set).
+ * clears again).  Otherwise (or when no such grid fits) the three stages are
+ * launched one after the other on `stream`.  Either way the results are
+ * deterministic; the fused path may split the attention over fewer
+ * workgroups when fewer fit, which changes the FP32 summation order (not
+ * the block set).  The fused grid is sized to the whole device: it assumes
+ * no other kernel holds compute units for long while it runs (workgroups
+ * that cannot start wait for others to drain).  Every wait inside it is
+ * bounded (0.2 s), so the device never hangs; if a wait does expire, that
+ * call's outputs are undefined and the workspace must be zero-filled again
+ * before the next call.
  *
  *  scores   device float [batch, nblk]          (output)
  *  idx      device int32 [batch, k_max]         (output)
