@@ -1,5 +1,11 @@
-// Selector block scoring kernel (paper Section 2.1); the per-wavefront core
-// is in score_core.h.  Each wave handles kUnroll consecutive blocks.
+// Selector block scoring kernels (paper Section 2.1).
+//  * score_kernel: one query row against a run of key blocks per wavefront
+//    (the per-wavefront core is in score_core.h) -- the decode case, a GEMV
+//    per sequence, and the 4-bit selector formats.
+//  * score_tile_kernel: many query rows per sequence (prefill: one row per
+//    query block) with a BF16 selector cache -- per head a GEMM
+//    S_h = Q_h K_h^T on the matrix cores, then sum_h w_h ReLU(S_h) per
+//    (query block, key block) tile (the query-block x key-block matmul).
 #include "score_core.h"
 
 namespace spot {
@@ -28,6 +34,84 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
                                    j0, nblk, scores, nullptr, threadIdx.x & 63);
 }
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// One 16 x 16 (query row x key block) tile per wavefront, a 2 x 2 group of
+// tiles per workgroup.  For head h, v_mfma_f32_16x16x32_bf16 with
+//   A = Q_h (16 rows x 32 dims): lane l holds row l%16, dims 8(l/16) ..+7,
+//   B = K_h^T (32 dims x 16 keys): lane l holds key l%16, dims 8(l/16) ..+7,
+// both 16 contiguous bytes of the row-major caches, read straight from
+// global memory; D gives lane l rows 4(l/16)+i of key column l%16.  The head
+// sum w_h ReLU(S_h) is accumulated in head order.  Keys at or past a row's
+// n_valid score -inf; a tile whose keys all lie past every row's n_valid
+// only writes -inf.
+template <int DS>
+__global__ __launch_bounds__(256) void score_tile_kernel(
+    const uint16_t* __restrict__ q_sel, const float* __restrict__ w,
+    const uint16_t* __restrict__ k_sel, int rows, int rows_per_seq, int nblk,
+    const int32_t* __restrict__ n_valid, float* __restrict__ scores) {
+  constexpr int HS = 512 / DS, KS = DS / 32;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r0 = blockIdx.x * 32 + (wave >> 1) * 16;    // first row of the tile
+  const int j0 = blockIdx.y * 32 + (wave & 1) * 16;     // first key block of the tile
+  const int r16 = lane & 15, G = lane >> 4;
+  // This lane's output rows 4G + i and key column r16.
+  int nv[4];
+  int nv_max = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = r0 + 4 * G + i;
+    int v = r < rows ? (n_valid ? n_valid[r] : nblk) : 0;
+    v = v < 0 ? 0 : (v > nblk ? nblk : v);
+    nv[i] = v;
+    nv_max = max(nv_max, v);
+  }
+  nv_max = (int)wave_max_u((uint32_t)nv_max);
+  const int key = j0 + r16;
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  if (j0 < nv_max) {
+    const int ra = r0 + r16;                            // A row of this lane
+    const bool a_ok = ra < rows, b_ok = key < nblk;
+    // The 16 rows of a tile share one sequence (the launcher requires
+    // rows_per_seq % 16 == 0), whose key cache is the B operand for all.
+    const int seq = min(r0, rows - 1) / rows_per_seq;
+    const uint16_t* qa = q_sel + (size_t)(a_ok ? ra : 0) * 512 + 8 * G;
+    const uint16_t* kb = k_sel + ((size_t)seq * nblk + (b_ok ? key : 0)) * 512 + 8 * G;
+    const float* wr = w + (size_t)(r0 + 4 * G) * HS;
+    u32x4 af[HS][KS], bfr[HS][KS];
+#pragma unroll
+    for (int h = 0; h < HS; ++h)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        af[h][ks] = a_ok ? *reinterpret_cast<const u32x4*>(qa + h * DS + ks * 32) : z;
+        bfr[h][ks] = b_ok ? *reinterpret_cast<const u32x4*>(kb + h * DS + ks * 32) : z;
+      }
+#pragma unroll
+    for (int h = 0; h < HS; ++h) {
+      f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, af[h][ks]),
+                                                    __builtin_bit_cast(bf16x8_t, bfr[h][ks]), s,
+                                                    0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float wi = r0 + 4 * G + i < rows ? wr[i * HS + h] : 0.f;
+        acc[i] = fmaf(wi, fmaxf(s[i], 0.f), acc[i]);
+      }
+    }
+  }
+  if (key < nblk) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = r0 + 4 * G + i;
+      if (r < rows) scores[(size_t)r * nblk + key] = key < nv[i] ? acc[i] : -INFINITY;
+    }
+  }
+}
+
 template <int KFMT>
 hipError_t launch_fmt(int lph, dim3 grid, hipStream_t s, const uint16_t* q, const float* w,
                       const uint8_t* k, const uint8_t* ks, int rows_per_seq, int nblk,
@@ -49,6 +133,19 @@ hipError_t launch_selector_score(const void* q_sel, const float* w, const void* 
                                  float* scores, hipStream_t s) {
   (void)h_s;
   const int rows = n_seq * rows_per_seq;
+  if (kfmt == SPOT_KFMT_BF16 && rows_per_seq > 1 && rows_per_seq % 16 == 0 &&
+      (d_s == 64 || d_s == 128)) {
+    const dim3 tgrid((rows + 31) / 32, (nblk + 31) / 32);
+    auto q = static_cast<const uint16_t*>(q_sel);
+    auto k = static_cast<const uint16_t*>(k_sel);
+    if (d_s == 64)
+      hipLaunchKernelGGL((score_tile_kernel<64>), tgrid, dim3(256), 0, s, q, w, k, rows,
+                         rows_per_seq, nblk, n_valid, scores);
+    else
+      hipLaunchKernelGGL((score_tile_kernel<128>), tgrid, dim3(256), 0, s, q, w, k, rows,
+                         rows_per_seq, nblk, n_valid, scores);
+    return hipGetLastError();
+  }
   dim3 grid(rows, (nblk + kBlocksPerWG - 1) / kBlocksPerWG);
   const int lph = d_s / 8;
   auto q = static_cast<const uint16_t*>(q_sel);

@@ -129,6 +129,23 @@ def test_selector_score_prefill_rows():
     assert_scores_close(s_g.cpu().numpy(), s_o)
 
 
+@pytest.mark.parametrize("B,nqb,Hs,ds", [(2, 48, 8, 64), (3, 32, 4, 128), (1, 20, 8, 64)])
+def test_selector_score_prefill_tiles(B, nqb, Hs, ds):
+    """Query-block x key-block scores on the matrix cores (rows_per_seq a
+    multiple of 16) and on the row kernel otherwise: several sequences,
+    a block count that is not a multiple of the 32-block workgroup tile,
+    both head splits of the 512-wide pooled key, a causal n_valid."""
+    rng = np.random.default_rng([B, nqb, Hs, ds])
+    q_sel, w, k_sel = synth.selector_prefill(rng, B, nqb, nqb, Hs, ds)
+    q_sel = q_sel.reshape(B * nqb, Hs, ds)
+    w = w.reshape(B * nqb, Hs)
+    n_valid = np.tile(np.arange(1, nqb + 1, dtype=np.int32), B)
+    s_o = oracle.selector_score(q_sel, w, k_sel, rows_per_seq=nqb, n_valid=n_valid)
+    s_g = spot.selector_score(bf(q_sel), f32(w), bf(k_sel), rows_per_seq=nqb,
+                              n_valid=i32(n_valid), nblk=nqb)
+    assert_scores_close(s_g.cpu().numpy(), s_o)
+
+
 # ---------------------------------------------------------------- selection
 SELECT_CASES = [
     # rows, nblk, rule, n_valid spec
