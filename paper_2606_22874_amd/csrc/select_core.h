@@ -90,17 +90,9 @@ __device__ __forceinline__ void bitonic_desc(uint64_t (&K)[SPL]) {
 }
 
 // ---------------------------------------------------------------------------
-// Workgroup (4 waves) selection for rows of 513 .. 4096 blocks, cap <= 512.
-// Same algorithm as the single-wave kernel, with the element-wise phases
-// spread over 256 threads (EPT <= 16 consecutive ids each):
-//  * max and Z in one barrier: each wave reduces its own max m_w and
-//    z_w = sum exp(s - m_w); then m = max_w m_w, Z = sum_w z_w exp(m_w - m);
-//  * radix select by count as before (block histogram, wave 0 scans);
-//  * one packed (greater, equal) exclusive scan gives every survivor its
-//    compaction slot;
-//  * wave 0 finishes on the survivors.  When the cap binds (the survivors'
-//    mass stays below top_p * Z) every survivor is chosen and no sort is
-//    needed; otherwise it sorts them and cuts the prefix as before.
+// Workgroup (4 waves) selection for rows of 513 .. 4096 blocks, cap <= 512
+// (select_row_wg below): the single-wave kernel's rule with the element-wise
+// phases spread over 256 threads (EPT <= 16 consecutive ids each).
 constexpr int kSelWG = 256;
 
 // Exclusive prefix over the 256 threads in thread order; `total` = sum.
@@ -183,7 +175,8 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 // EPT consecutive ids [t*EPT, (t+1)*EPT).  Steps, with the workgroup barriers
 // in brackets:
 //  1. load; order-preserving keys of the residual candidates; residual max
-//     M, min and Z = sum exp(s - M) from per-wave partials [1];
+//     M and min from per-wave partials [1]; Z = sum exp(s - M) per wave,
+//     combined after the next barrier;
 //  2. when the cap C binds: a histogram over 2048 equal-width value bins
 //     between the candidate min and max, and over 64 coarse bins of 32 [1];
 //     every wave scans the coarse and then the fine counts for the bin
@@ -219,7 +212,7 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   const int cap = min(k_max - n_reserved, n_res);
   const int j0 = tid * EPT;
 
-  // 1. scores, keys (0 = not a candidate), M, min and Z
+  // 1. scores, keys (0 = not a candidate), M and min
   SPOT_SEL_TS(0);
   float sv[EPT];
   src(sv, j0, nv);
@@ -249,20 +242,9 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   }
   kmax = wave_max_u(kmax);
   kmin = wave_min_u(kmin);
-  {
-    float zl = 0.f;
-    const float mw = order_key_inv(kmax);
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      const float x = __builtin_amdgcn_exp2f((sv[e] - mw) * kLog2e);
-      zl += ((cand >> e) & 1u) && kmax ? x : 0.f;
-    }
-    const float zw = wave_sum(zl);
-    if (lane == 0) {
-      sm.red_u[wave][0] = kmax;
-      sm.red_u[wave][1] = kmin;
-      sm.red_f[wave] = zw;
-    }
+  if (lane == 0) {
+    sm.red_u[wave][0] = kmax;
+    sm.red_u[wave][1] = kmin;
   }
   __syncthreads();
   kmax = 0u;
@@ -273,14 +255,18 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
     kmin = min(kmin, sm.red_u[w][1]);
   }
   const float M = order_key_inv(kmax);
-  float Z = 0.f;
-#pragma unroll
-  for (int w = 0; w < NW; ++w)
-    if (sm.red_u[w][0])
-      Z += sm.red_f[w] * __builtin_amdgcn_exp2f((order_key_inv(sm.red_u[w][0]) - M) * kLog2e);
   float pe[EPT];                                 // exp(s - M) of the candidates
 #pragma unroll
   for (int e = 0; e < EPT; ++e) pe[e] = __builtin_amdgcn_exp2f((sv[e] - M) * kLog2e);
+  {
+    // Z's per-wave partials, read after the next barrier (every path below
+    // has one before the nucleus decision)
+    float zl = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) zl += ((cand >> e) & 1u) ? pe[e] : 0.f;
+    const float zw = wave_sum(zl);
+    if (lane == 0) sm.red_f[wave] = zw;
+  }
   SPOT_SEL_TS(2);
 
   // 2. the cut: survivors are the candidates with rank_key >= (kt, it)
@@ -452,6 +438,9 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   SPOT_SEL_TS(3);
 
   // 3. the nucleus (the same decision in every thread)
+  float Z = 0.f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) Z += sm.red_f[w];
   const float pz = top_p * Z;
   int n;                                  // -1: the nucleus ends before the cap
   if (cap <= 0) n = 0;
