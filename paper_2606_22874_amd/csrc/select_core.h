@@ -145,8 +145,7 @@ constexpr int kFine = kValBins / 64;   // value bins per coarse bin
 
 template <int EPT, int SPL>
 struct SelWgSmem {
-  uint32_t hist[kValBins];        // value-bin counts (the fallback radix uses 256)
-  uint32_t hist2[64];             // coarse counts: kFine value bins each
+  alignas(16) uint32_t hist[kValBins];   // value-bin counts (the fallback radix uses 256)
   uint64_t s_K[64 * (SPL > 4 ? SPL : 4)];   // threshold-bin members (64 per wave) / survivors
   uint32_t red_u[kSelWG / 64][2];
   float red_f[kSelWG / 64];
@@ -178,11 +177,12 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 //     M and min from per-wave partials [1]; Z = sum exp(s - M) per wave,
 //     combined after the next barrier;
 //  2. when the cap C binds: a histogram over 2048 equal-width value bins
-//     between the candidate min and max, and over 64 coarse bins of 32 [1];
-//     every wave scans the coarse and then the fine counts for the bin
-//     holding the C-th best candidate (score desc, id asc); each wave packs
-//     its members of that bin and sums the mass of its candidates in better
-//     bins [1]; every wave ranks the members by counting and derives the
+//     between the candidate min and max [1]; every wave sums the bins into
+//     64 coarse bins of 32 and scans the coarse and then the fine counts
+//     for the bin holding the C-th best candidate (score desc, id asc); each
+//     wave packs its members of that bin and sums the mass of its
+//     candidates in better bins [1]; every wave ranks the members by
+//     counting and derives the
 //     packed cut key and the mass of the survivors.  The survivors are the
 //     candidates whose packed key reaches the cut.  A bin too crowded to
 //     rank (heavy ties) falls back to an 8-bit radix select on the keys;
@@ -219,7 +219,6 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   static_assert(kValBins == NT * 8, "two 16-byte zero stores per thread");
   reinterpret_cast<uint4*>(sm.hist)[2 * tid] = make_uint4(0u, 0u, 0u, 0u);
   reinterpret_cast<uint4*>(sm.hist)[2 * tid + 1] = make_uint4(0u, 0u, 0u, 0u);
-  if (tid < 64) sm.hist2[tid] = 0u;
   uint32_t key[EPT];
   uint32_t cand = 0, resv = 0;
   {
@@ -286,17 +285,22 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
       for (int e = 0; e < EPT; ++e) {
         // bins ascend as values descend; clamped in float first
         bin[e] = (int)fminf((vhi - sv[e]) * inv_w, (float)(kValBins - 1));
-        if (key[e]) {
-          atomicAdd(&sm.hist[bin[e]], 1u);
-          atomicAdd(&sm.hist2[bin[e] / kFine], 1u);
-        }
+        if (key[e]) atomicAdd(&sm.hist[bin[e]], 1u);
       }
       __syncthreads();
       SPOT_SEL_TS(6);
       // Every wave finds the bin of the cap-th best candidate on its own: a
       // scan over the 64 coarse bins, then over the 32 fine bins of the
       // coarse bin that holds it (no barrier).
-      const int cc = (int)sm.hist2[lane];
+      // lane l sums fine bins [32 l, 32 l + 32): eight 16-byte reads, the
+      // chunk order rotated by lane so a read spreads over the banks
+      int cc = 0;
+#pragma unroll
+      for (int k = 0; k < kFine / 4; ++k) {
+        const uint4 t = reinterpret_cast<const uint4*>(sm.hist)[lane * (kFine / 4) +
+                                                              ((k + (lane >> 1)) & (kFine / 4 - 1))];
+        cc += (int)(t.x + t.y + t.z + t.w);
+      }
       const int c_incl = wave_incl_scan_i(cc);
       const int cb = min(__builtin_ctzll(__ballot(c_incl >= cap)), 63);
       const int c_before = __builtin_amdgcn_readlane(c_incl - cc, cb);
