@@ -170,7 +170,7 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 // Selection of one row by the whole 256-thread workgroup: src supplies the
 // row's scores (the first nv valid), out receives its k_max id slots, pub
 // optional device-scope copies.  Needs min(k_max, nblk) <= P = 64 * SPL
-// (<= 512).  Every thread of the workgroup must call it.  Thread t owns the
+// (<= 512) and pub.len <= k_max.  Every thread of the workgroup must call it.  Thread t owns the
 // EPT consecutive ids [t*EPT, (t+1)*EPT).  Steps, with the workgroup barriers
 // in brackets:
 //  1. load; order-preserving keys of the residual candidates; residual max
@@ -190,7 +190,8 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 //     otherwise they are compacted [2], sorted in wave 0 by (score desc, id
 //     asc), prefix-summed and cut where the prefix first reaches top_p * Z,
 //     then floored by k_min [1];
-//  4. reserved + chosen ids are written in ascending order [2].
+//  4. reserved + chosen ids are written in ascending order [1] (with
+//     record copies: [2]).
 // Every reduction has a fixed order, so the result is deterministic.
 template <int EPT, int SPL, class Src>
 __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src& src, int nblk,
@@ -517,9 +518,10 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   }
   SPOT_SEL_TS(4);
 
-  // 4. write S = reserved u chosen, ascending: positions by a scan, the ids
-  // staged in LDS (at most 512 of them: min(k_max, nblk) <= P), then written
-  // out by all threads in order
+  // 4. write S = reserved u chosen, ascending: positions by a scan.  Each
+  // thread writes its own ids; with record copies to publish, the ids are
+  // staged in LDS first (at most 512: min(k_max, nblk) <= P) so that all
+  // threads share the copies' stores evenly.
   const uint32_t fin = resv | chosen;
   const int mine = __popc(fin);
   const int incl = wave_incl_scan_i(mine);
@@ -533,19 +535,24 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
     total += t;
   }
   const int n_out = min(total, k_max);
-#pragma unroll
-  for (int e = 0; e < EPT; ++e)
-    if (((fin >> e) & 1u) && pos < n_out && pos < kValBins) sm.hist[pos++] = (uint32_t)(j0 + e);
-  __syncthreads();
   if (pub.base) {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+      if (((fin >> e) & 1u) && pos < n_out && pos < kValBins) sm.hist[pos++] = (uint32_t)(j0 + e);
+    __syncthreads();
     for (int i = tid; i < pub.len; i += NT) {
       const uint32_t wd = i < n_out ? sm.hist[i] + 1u : 0xffffffffu;
       for (int c = 0; c < pub.copies; ++c)
         __hip_atomic_store(pub.base + (size_t)c * pub.len + i, wd, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     }
+    for (int i = tid; i < k_max; i += NT) out[i] = i < n_out ? (int32_t)sm.hist[i] : -1;
+  } else {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+      if (((fin >> e) & 1u) && pos < n_out) out[pos++] = j0 + e;
+    for (int i = n_out + tid; i < k_max; i += NT) out[i] = -1;
   }
-  for (int i = tid; i < k_max; i += NT) out[i] = i < n_out ? (int32_t)sm.hist[i] : -1;
   if (tid == 0) {
     *count_out = n_out;
     if (mass_out) *mass_out = mass;
