@@ -477,10 +477,25 @@ def cpu_baseline(wl, budget_s):
         el = time.time() - t0
         if el >= budget_s or (n >= 1 and el * (n + 1) / n > 30.0):
             break
-    return {"value": round(n / el, 4), "unit": "steps/s", "cores": oracle.get_threads(),
+    used = oracle.get_threads()
+    # The same steps on one thread, over a shorter sample.
+    oracle.set_threads(1)
+    n1, t1 = 0, time.time()
+    while True:
+        s = oracle.selector_score(wl.q_sel, wl.w, wl.k_sel, n_valid=wl.n_valid)
+        idx, cnt, _ = oracle.select_blocks(s.astype(np.float32), wl.rule, wl.n_valid)
+        oracle.sparse_decode(wl.q, wl.k, wl.v, wl.seq_len, idx, cnt, wl.sm_scale)
+        n1 += 1
+        el1 = time.time() - t1
+        if el1 >= budget_s / 4 or (n1 >= 1 and el1 * (n1 + 1) / n1 > 10.0):
+            break
+    oracle.set_threads(cores)
+    return {"value": round(n / el, 4), "unit": "steps/s", "cores": used,
             "kind": "oracle",
             "sample": f"{n} full decode steps (score + select + sparse attention, all 4 "
-                      f"sequences) of the same workload, FP64 C with OpenMP"}
+                      f"sequences) of the same workload, FP64 C with OpenMP",
+            "single_thread_value": round(n1 / el1, 4),
+            "single_thread_sample": f"{n1} of the same steps on 1 thread"}
 
 
 if __name__ == "__main__":
