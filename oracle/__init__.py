@@ -57,6 +57,7 @@ def lib():
             L.oracle_key_value.argtypes = [P, P, I, ctypes.c_int64]
             L.oracle_key_value.restype = D
             L.oracle_selector_score.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P]
+            L.oracle_selector_score_tokens.argtypes = [P, P, P, P, I, I, I, I, I, I, I, P, P]
             L.oracle_select_blocks.argtypes = [P, I, I, P, D, I, I, I, I, P, P, P]
             L.oracle_select_blocks.restype = I
             L.oracle_sparse_decode.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, I, D, P, P]
@@ -112,6 +113,29 @@ def selector_score(q_sel, w, k_sel, k_scale=None, kfmt="bf16", rows_per_seq=1,
     out = np.empty((rows, nblk), dtype=np.float64)
     lib().oracle_selector_score(_p(q_sel), _p(w), _p(k_sel), _p(sc), f, n_seq, rows_per_seq,
                                 nblk, h_s, d_s, _p(nv), _p(out))
+    return out
+
+
+def selector_score_tokens(q_sel, w, k_tok, k_scale=None, kfmt="bf16", rows_per_seq=1,
+                          seq_len=None, l_cap=None, blk=64, h_s=None, d_s=None) -> np.ndarray:
+    """Per-block maximum of per-token scores [rows, l_cap // blk] in float64
+    (Section 2.3 over the score of Section 2.1)."""
+    f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
+    q_sel = _c(q_sel, np.uint16)
+    w = _c(w, np.float32)
+    h_s = q_sel.shape[-2] if h_s is None else h_s
+    d_s = q_sel.shape[-1] if d_s is None else d_s
+    rows = q_sel.size // (h_s * d_s)
+    n_seq = rows // rows_per_seq
+    k_tok = np.ascontiguousarray(k_tok)
+    if l_cap is None:
+        per = h_s * d_s if f == 0 else h_s * d_s // 2
+        l_cap = k_tok.size // (n_seq * per)
+    sc = None if k_scale is None else np.ascontiguousarray(k_scale)
+    sl = None if seq_len is None else _c(seq_len, np.int32)
+    out = np.empty((rows, l_cap // blk), dtype=np.float64)
+    lib().oracle_selector_score_tokens(_p(q_sel), _p(w), _p(k_tok), _p(sc), f, n_seq,
+                                       rows_per_seq, l_cap, blk, h_s, d_s, _p(sl), _p(out))
     return out
 
 

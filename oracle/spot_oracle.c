@@ -8,6 +8,8 @@
  *
  *   selector score ....... Section 2.1: s = sum_h w_h ReLU(q_h . k_h), one
  *                          score per query-block x key-block tile
+ *   per-token selector ... Section 2.3: the block value is the maximum of
+ *                          the per-token scores of the block's tokens
  *   block selection ...... Section 2.3: Eq. select-topk (static top-K),
  *                          Eq. select-nucleus (softmax over the residual
  *                          blocks), Eq. select-topp (sink + recency + nucleus,
@@ -124,6 +126,40 @@ void oracle_selector_score(const uint16_t *q_sel, const float *w, const void *k_
                 s += (double)w[(int64_t)r * h_s + h] * (dot > 0.0 ? dot : 0.0);
             }
             scores[(int64_t)r * nblk + j] = s;
+        }
+    }
+}
+
+/* Per-token selector with a per-block maximum (Section 2.3): each visible
+ * token t gets the head-weighted ReLU score of Section 2.1 against its own
+ * selector key, and a block's value is the largest score among its visible
+ * tokens.  A block with no visible token does not exist (-inf). */
+void oracle_selector_score_tokens(const uint16_t *q_sel, const float *w, const void *k_tok,
+                                  const void *k_scale, int kfmt, int n_seq, int rows_per_seq,
+                                  int l_cap, int blk, int h_s, int d_s,
+                                  const int32_t *seq_len, double *scores) {
+    int rows = n_seq * rows_per_seq;
+    int nblk = l_cap / blk;
+#pragma omp parallel for schedule(dynamic) num_threads(oracle_get_threads())
+    for (int r = 0; r < rows; ++r) {
+        int seq = r / rows_per_seq;
+        int len = seq_len ? seq_len[r] : l_cap;
+        if (len > l_cap) len = l_cap;
+        for (int j = 0; j < nblk; ++j) {
+            double best = -INFINITY;
+            for (int t = j * blk; t < (j + 1) * blk && t < len; ++t) {
+                double s = 0.0;
+                for (int h = 0; h < h_s; ++h) {
+                    int64_t base = (((int64_t)seq * l_cap + t) * h_s + h) * d_s;
+                    double dot = 0.0;
+                    for (int i = 0; i < d_s; ++i)
+                        dot += bf16_to_double(q_sel[((int64_t)r * h_s + h) * d_s + i]) *
+                               oracle_key_value(k_tok, k_scale, kfmt, base + i);
+                    s += (double)w[(int64_t)r * h_s + h] * (dot > 0.0 ? dot : 0.0);
+                }
+                if (s > best) best = s;
+            }
+            scores[(int64_t)r * nblk + j] = best;
         }
     }
 }

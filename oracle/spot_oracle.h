@@ -39,6 +39,18 @@ void oracle_selector_score(const uint16_t *q_sel, const float *w, const void *k_
                            int nblk, int h_s, int d_s, const int32_t *n_valid,
                            double *scores);
 
+/* Per-token selector scores reduced to one value per block (Section 2.3:
+ * sbar[r, b] = max over the tokens t of block b of s[r, t], with s the score
+ * of Section 2.1 against each token's own selector key).
+ * k_tok [n_seq, l_cap, h_s, d_s] (BF16) or codes [n_seq, l_cap, h_s, d_s/2]
+ * with scales [n_seq, l_cap, h_s, d_s/32]; blocks of blk tokens, nblk =
+ * l_cap / blk.  Row r sees the tokens t < seq_len[r] (all l_cap if seq_len is
+ * NULL); a block with none of them is -inf.  scores [rows, nblk]. */
+void oracle_selector_score_tokens(const uint16_t *q_sel, const float *w, const void *k_tok,
+                                  const void *k_scale, int kfmt, int n_seq, int rows_per_seq,
+                                  int l_cap, int blk, int h_s, int d_s,
+                                  const int32_t *seq_len, double *scores);
+
 /* Dual top-p / top-K block selection (Section 2.3, Eqs. select-topk,
  * select-nucleus, select-topp) with a cap k_max on the total set size.
  * idx [rows, k_max] receives the chosen block ids ascending, padded with -1;

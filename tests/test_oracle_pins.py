@@ -116,6 +116,64 @@ def test_score_invariants():
     np.testing.assert_array_equal(s_pf[0], s[0])
 
 
+def test_score_tokens_closed_form(golden_dir):
+    g = json.load(open(os.path.join(golden_dir, "score_tokens_closed_form.json")))
+    keys = {n: np.array(v, dtype=np.float32) for n, v in g["keys"].items()}
+    for case in g["cases"]:
+        k = bf16_bits(np.stack([np.stack([keys[c] for c in seq]) for seq in case["tokens"]]))
+        rps = case["rows_per_seq"]
+        rows = len(case["tokens"]) * rps
+        q = np.broadcast_to(bf16_bits(np.array(g["q_sel"], np.float32)), (rows, 2, 4)).copy()
+        w = np.broadcast_to(np.array(g["w"], np.float32), (rows, 2)).copy()
+        s = oracle.selector_score_tokens(q, w, k, rows_per_seq=rps, blk=g["blk"],
+                                         seq_len=np.array(case["seq_len"], np.int32))
+        expected = np.array([[_num(x) for x in row] for row in case["expected"]])
+        np.testing.assert_array_equal(s, expected)
+
+
+@pytest.mark.parametrize("kfmt", ["bf16", "int4", "mxfp4"])
+def test_score_tokens_reduces_to_pooled_scores(kfmt):
+    """With one token per block the per-token selector is the pinned block
+    score with every token as its own block; a numpy maximum over groups of
+    tokens then gives the per-block value, with hidden tokens left out."""
+    rng = np.random.default_rng(23)
+    n_seq, rps, Hs, ds, L, blk = 2, 2, 4, 128, 320, 64
+    q = bf16_bits(rng.standard_normal((n_seq * rps, Hs, ds)).astype(np.float32))
+    w = rng.uniform(0, 1, (n_seq * rps, Hs)).astype(np.float32)
+    kb = bf16_bits(rng.standard_normal((n_seq, L, Hs, ds)).astype(np.float32))
+    k, sc = {"bf16": lambda b: (b, None), "int4": synth.quantize_int4_g32,
+             "mxfp4": synth.quantize_mxfp4_g32}[kfmt](kb)
+    per_tok = oracle.selector_score(q, w, k, sc, kfmt, rows_per_seq=rps, nblk=L, h_s=Hs, d_s=ds)
+    seq_len = np.array([L, 200, 129, 1], np.int32)
+    s = oracle.selector_score_tokens(q, w, k, sc, kfmt, rows_per_seq=rps, seq_len=seq_len,
+                                     l_cap=L, blk=blk, h_s=Hs, d_s=ds)
+    for r in range(n_seq * rps):
+        for j in range(L // blk):
+            lo, hi = j * blk, min((j + 1) * blk, int(seq_len[r]))
+            want = per_tok[r, lo:hi].max() if hi > lo else -np.inf
+            assert s[r, j] == want, (r, j)
+    # Shuffling the tokens inside each block leaves every block value as it was.
+    perm = np.concatenate([j * blk + rng.permutation(blk) for j in range(L // blk)])
+    s_p = oracle.selector_score_tokens(q, w, k[:, perm], None if sc is None else sc[:, perm],
+                                       kfmt, rows_per_seq=rps, l_cap=L, blk=blk, h_s=Hs, d_s=ds)
+    s_all = oracle.selector_score_tokens(q, w, k, sc, kfmt, rows_per_seq=rps, l_cap=L, blk=blk,
+                                         h_s=Hs, d_s=ds)
+    np.testing.assert_array_equal(s_p, s_all)
+
+
+def test_score_tokens_of_repeated_key_is_pooled_score():
+    """A block whose tokens all carry the key kbar scores exactly as the
+    pooled block kbar does."""
+    rng = np.random.default_rng(29)
+    Hs, ds, nblk, blk = 8, 64, 5, 64
+    q = bf16_bits(rng.standard_normal((1, Hs, ds)).astype(np.float32))
+    w = rng.uniform(0, 1, (1, Hs)).astype(np.float32)
+    kbar = bf16_bits(rng.standard_normal((1, nblk, Hs, ds)).astype(np.float32))
+    k_tok = np.repeat(kbar, blk, axis=1)
+    np.testing.assert_array_equal(oracle.selector_score_tokens(q, w, k_tok, blk=blk),
+                                  oracle.selector_score(q, w, kbar))
+
+
 # -------------------------------------------------------------- selection
 def _sel(scores, rule, n_valid=None):
     s = np.asarray(scores, dtype=np.float64)[None]
