@@ -8,6 +8,9 @@
  * with spot_decode_step running all three for every sequence in one launch,
  * spot_dense_decode as the full-attention baseline and spot_sparse_prefill
  * as the block-sparse causal prefill over query blocks.
+ * spot_selector_score_tokens replaces the first call when the selector cache
+ * holds one key per token (block value = maximum of per-token scores,
+ * Section 2.3).
  *
  * Conventions shared by every entry point:
  *  - Pointers named as device arrays are caller-owned device memory; the
@@ -15,7 +18,8 @@
  *    its own between calls (the decode workspace carries completion counters
  *    that each call returns to zero).  Arrays are C-contiguous.  BF16 arrays hold bfloat16
  *    values (2 bytes each).  A KV block is 64 consecutive tokens; the
- *    selector key cache holds one pooled key per block.
+ *    pooled selector key cache holds one key per block, the per-token cache
+ *    one key per token.
  *  - `stream` is a hipStream_t (NULL = the default stream).  Every call only
  *    enqueues work on it and returns; the returned status covers argument
  *    validation and the launch itself.  A fault inside a kernel surfaces at
@@ -83,13 +87,50 @@ const char *spot_version(void);
  *           -inf) or NULL (every block valid)
  *  scores   device, float [rows, nblk]  (output)
  *
- * Supported: h_s * d_s == 512 with d_s in {64, 128} (decode, any format);
- * rows_per_seq > 1 requires SPOT_KFMT_BF16, h_s <= 16 and d_s == 64.
+ * Supported: h_s * d_s == 512 with d_s in {64, 128}, any format and any
+ * rows_per_seq (BF16 keys with rows_per_seq a multiple of 16 run on the
+ * matrix cores, everything else on the vector units).
  */
 spot_status spot_selector_score(const void *q_sel, const float *w, const void *k_sel,
                                 const void *k_scale, int kfmt, int n_seq, int rows_per_seq,
                                 int nblk, int h_s, int d_s, const int32_t *n_valid,
                                 float *scores, void *stream);
+
+/*
+ * spot_selector_score_tokens -- per-token selector, one value per block.
+ *
+ * Section 2.3: both selection modes rank a block by the largest per-token
+ * selector score among its tokens.  With one selector key per token (the
+ * score of Section 2.1 against each token's own key) and blocks of 64 tokens:
+ *     scores[r, b] = max_{64b <= t < min(64b + 64, seq_len[r])}
+ *                    sum_{h < h_s} w[r, h] * max(0, q_sel[r, h, :] . k_tok[seq(r), t, h, :])
+ * and -inf for a block with no visible token.  Rows and seq(r) as in
+ * spot_selector_score.  The result feeds spot_select_blocks unchanged
+ * (n_valid[r] = ceil(seq_len[r] / 64)).
+ *
+ *  q_sel    device, BF16 [n_seq*rows_per_seq, h_s, d_s]
+ *  w        device, float [n_seq*rows_per_seq, h_s]
+ *  k_tok    device, per-token selector key cache, [n_seq, l_cap, h_s, d_s] BF16
+ *           for SPOT_KFMT_BF16; for the 4-bit formats uint8
+ *           [n_seq, l_cap, h_s, d_s/2], element 2i in the low nibble of byte i
+ *  k_scale  device, NULL for BF16; else [n_seq, l_cap, h_s, d_s/32] FP16 (INT4)
+ *           or uint8 E8M0 (MXFP4), as for spot_selector_score
+ *  l_cap    tokens per sequence in the cache, a multiple of 64; nblk = l_cap/64
+ *  seq_len  device int32 [rows]: row r sees tokens t < seq_len[r] (clamped to
+ *           [0, l_cap]); NULL means every token is visible
+ *  scores   device, float [rows, nblk] (output)
+ *
+ * Supported: h_s * d_s == 512 with d_s in {64, 128}, any format.  Rows of one
+ * sequence are scheduled on the same XCD so that they share its L2 for the
+ * key stream.  Errors: SPOT_ERR_NULL for a missing pointer (or missing scales
+ * of a 4-bit format), SPOT_ERR_SHAPE for negative sizes or l_cap not a
+ * multiple of 64, SPOT_ERR_UNSUPPORTED for other head shapes or formats.
+ * Nothing is written on an error.
+ */
+spot_status spot_selector_score_tokens(const void *q_sel, const float *w, const void *k_tok,
+                                       const void *k_scale, int kfmt, int n_seq,
+                                       int rows_per_seq, int l_cap, int h_s, int d_s,
+                                       const int32_t *seq_len, float *scores, void *stream);
 
 /*
  * spot_select_blocks -- dual top-p / static top-K block selection.

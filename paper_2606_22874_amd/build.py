@@ -22,7 +22,7 @@ BUILD = os.path.join(ROOT, "_build")
 SO = os.path.join(PKG, "libspot.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "score.hip", "select.hip", "decode.hip", "step.hip", "prefill.hip",
+SOURCES = ["api.hip", "score.hip", "score_tokens.hip", "select.hip", "decode.hip", "step.hip", "prefill.hip",
            "probe.hip"]
 
 HIPCC_FLAGS = [

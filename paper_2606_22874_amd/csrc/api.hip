@@ -52,6 +52,26 @@ spot_status spot_selector_score(const void* q_sel, const float* w, const void* k
                                         static_cast<hipStream_t>(stream)));
 }
 
+spot_status spot_selector_score_tokens(const void* q_sel, const float* w, const void* k_tok,
+                                       const void* k_scale, int kfmt, int n_seq,
+                                       int rows_per_seq, int l_cap, int h_s, int d_s,
+                                       const int32_t* seq_len, float* scores, void* stream) {
+  if (!q_sel || !w || !k_tok || !scores) return SPOT_ERR_NULL;
+  if (n_seq < 0 || rows_per_seq < 1 || l_cap < 0 || l_cap % kBlk || h_s < 1 || d_s < 1)
+    return SPOT_ERR_SHAPE;
+  if (kfmt != SPOT_KFMT_BF16 && kfmt != SPOT_KFMT_INT4_G32 && kfmt != SPOT_KFMT_MXFP4_G32)
+    return SPOT_ERR_UNSUPPORTED;
+  if (kfmt != SPOT_KFMT_BF16 && !k_scale) return SPOT_ERR_NULL;
+  if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
+  // Launch size: one workgroup per (row, run of 4 blocks), padded to 8 runs.
+  const long long runs = (l_cap / kBlk + 3) / 4;
+  if (((long long)n_seq * runs + 7) / 8 * 8 * rows_per_seq > 0x7fffffffLL) return SPOT_ERR_SHAPE;
+  if (n_seq == 0 || l_cap == 0) return SPOT_OK;
+  return from_hip(launch_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq,
+                                               rows_per_seq, l_cap, d_s, seq_len, scores,
+                                               static_cast<hipStream_t>(stream)));
+}
+
 spot_status spot_select_blocks(const float* scores, int rows, int nblk, const int32_t* n_valid,
                                float top_p, int k_max, int k_min, int n_sink, int n_recent,
                                int32_t* idx, int32_t* count, float* nuc_mass, void* stream) {

@@ -1,0 +1,186 @@
+// Per-token selector scores reduced to one value per block (paper Section
+// 2.3): the value of block b for query row r is the largest head-weighted
+// ReLU score (Section 2.1) of r against the selector keys of b's visible
+// tokens,
+//     sbar[r, b] = max_{t in b, t < seq_len[r]} sum_h w[r,h] ReLU(q[r,h,:] . k[seq(r), t, h, :]).
+//
+// The per-token cache is a streamed read (1 KiB per BF16 token), so the kernel
+// is bound by HBM and runs on the vector ALUs: one wavefront owns one 64-token
+// block.  Each lane reads the same 16 bytes (8 elements) of every token row,
+// so a load instruction moves one whole token row, coalesced.  Tokens are
+// taken 8 at a time; the 8 per-lane partial dot products are folded across
+// the LPH lanes of a head by a reduce-scatter (each butterfly step halves the
+// tokens a lane keeps and exchanges the other half with its partner), which
+// leaves every lane with the full head dot of one token in 7 exchanges where
+// per-token reductions would need 8 x log2(LPH).  The ReLU and weight follow,
+// then the head sum: inside a 16-lane row with one DPP move, across rows by a
+// second reduce-scatter over the block's 8 groups, once per block.  A final
+// wave maximum gives the block value.  Every exchange order is fixed, so the
+// result is deterministic.
+//
+// Token loads past the last visible token re-read that token (in bounds, in
+// cache); a duplicate of a visible token cannot change a maximum, so ragged
+// blocks need no masking.
+#include "score_core.h"
+
+namespace spot {
+namespace {
+
+constexpr int kTokWavesPerWG = 4;  // one 64-token block per wave
+
+// Butterfly exchange partner moves, all DPP inside a 16-lane row: the partner
+// differs from the lane in the bit being folded (half-mirror 7 - i flips bit
+// 2, mirror 15 - i flips bit 3, quad swaps flip bits 1 and 0); the other bits
+// it flips are folded later, so each lane still sums every lane of its head.
+template <int CTRL, int N>
+__device__ __forceinline__ void fold_half(const float (&in)[2 * N], float (&out)[N], bool hi) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const float keep = hi ? in[i + N] : in[i];
+    const float send = hi ? in[i] : in[i + N];
+    out[i] = keep + dpp_f<CTRL>(send);
+  }
+}
+
+// Same fold across 16-lane rows (partner lane ^ 16 or ^ 32).
+template <int XOR, int N>
+__device__ __forceinline__ void fold_half_rows(const float (&in)[2 * N], float (&out)[N],
+                                               bool hi) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const float keep = hi ? in[i + N] : in[i];
+    const float send = hi ? in[i] : in[i + N];
+    out[i] = keep + __shfl_xor(send, XOR, 64);
+  }
+}
+
+// Launch order: work units u = (sequence, run of 4 blocks) and the
+// rows_per_seq query rows of a sequence.  Workgroup ids go round-robin over
+// the 8 XCDs, so the rows that read the same keys are given ids 8 apart --
+// the same XCD, hence the same L2 -- and consecutive units alternate XCDs.
+template <int KFMT, int LPH>
+__global__ __launch_bounds__(256) void score_tokens_kernel(
+    const uint16_t* __restrict__ q_sel, const float* __restrict__ w,
+    const uint8_t* __restrict__ k_tok, const uint8_t* __restrict__ k_scale, int n_seq,
+    int rows_per_seq, int l_cap, int nblk, int runs, const int32_t* __restrict__ seq_len,
+    float* __restrict__ scores) {
+  constexpr int kHeads = 64 / LPH;
+  const int lane = threadIdx.x & 63;
+  const int gsize = 8 * rows_per_seq;
+  const int id = blockIdx.x;
+  const int unit = (id / gsize) * 8 + (id & 7);
+  const int rr = (id % gsize) >> 3;
+  if (unit >= n_seq * runs) return;
+  const int seq = unit / runs;
+  const int j = (unit % runs) * kTokWavesPerWG + (threadIdx.x >> 6);
+  if (j >= nblk) return;
+  const int row = seq * rows_per_seq + rr;
+  int len = seq_len ? seq_len[row] : l_cap;
+  len = len < 0 ? 0 : (len > l_cap ? l_cap : len);
+  const int t0 = j * 64;
+  float* dst = scores + (size_t)row * nblk + j;
+  if (t0 >= len) {
+    if (lane == 0) *dst = -INFINITY;
+    return;
+  }
+  const int tlim = min(t0 + 64, len) - 1;
+  const size_t base = (size_t)seq * l_cap;
+
+  const uint4 qraw = *reinterpret_cast<const uint4*>(q_sel + (size_t)row * 512 + lane * 8);
+  float qf[8];
+  qf[0] = bf16_lo(qraw.x); qf[1] = bf16_hi(qraw.x);
+  qf[2] = bf16_lo(qraw.y); qf[3] = bf16_hi(qraw.y);
+  qf[4] = bf16_lo(qraw.z); qf[5] = bf16_hi(qraw.z);
+  qf[6] = bf16_lo(qraw.w); qf[7] = bf16_hi(qraw.w);
+  const float wh = w[(size_t)row * kHeads + lane / LPH];
+
+  // y[g]: the in-row head sum of this lane's token of group g (tokens
+  // t0 + 8g .. t0 + 8g + 7; lane holds token (LPH == 8 ? lane : lane >> 1) & 7).
+  float y[8];
+  KeyLoad<KFMT> key[2][8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+    key[0][u].load(k_tok, k_scale, base + min(t0 + u, tlim), lane);
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    if (g + 1 < 8) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        key[(g + 1) & 1][u].load(k_tok, k_scale, base + min(t0 + 8 * (g + 1) + u, tlim), lane);
+    }
+    float p[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) p[u] = key[g & 1][u].dot(qraw, qf);
+    float d;
+    if constexpr (LPH == 8) {
+      // Head lanes are lane bits 0..2.
+      float a[4], c[2];
+      fold_half<kDppHalfMirror, 4>(p, a, lane & 4);
+      fold_half<kDppQuadXor2, 2>(a, c, lane & 2);
+      float c1[1];
+      fold_half<kDppQuadXor1, 1>(c, c1, lane & 1);
+      d = wh * fmaxf(c1[0], 0.f);
+      d += dpp_f<0x128>(d);  // row_ror:8 -- the other head of this 16-lane row
+    } else {
+      // Head lanes are lane bits 0..3.
+      float a[4], c[2], e[1];
+      fold_half<kDppMirror, 4>(p, a, lane & 8);
+      fold_half<kDppHalfMirror, 2>(a, c, lane & 4);
+      fold_half<kDppQuadXor2, 1>(c, e, lane & 2);
+      const float h = e[0] + dpp_f<kDppQuadXor1>(e[0]);
+      d = wh * fmaxf(h, 0.f);
+    }
+    y[g] = d;
+  }
+  // Sum over the 4 rows of the wave: fold the groups over lane bits 4 and 5.
+  float z[4], v[2];
+  fold_half_rows<16, 4>(y, z, lane & 16);
+  fold_half_rows<32, 2>(z, v, lane & 32);
+  const float m = wave_max(fmaxf(v[0], v[1]));
+  if (lane == 0) *dst = m;
+}
+
+template <int KFMT>
+hipError_t launch_tokens_fmt(int lph, dim3 grid, hipStream_t s, const uint16_t* q,
+                             const float* w, const uint8_t* k, const uint8_t* ks, int n_seq,
+                             int rows_per_seq, int l_cap, int nblk, int runs,
+                             const int32_t* seq_len, float* out) {
+  if (lph == 8)
+    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 8>), grid, dim3(256), 0, s, q, w, k, ks,
+                       n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+  else
+    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 16>), grid, dim3(256), 0, s, q, w, k, ks,
+                       n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_selector_score_tokens(const void* q_sel, const float* w, const void* k_tok,
+                                        const void* k_scale, int kfmt, int n_seq,
+                                        int rows_per_seq, int l_cap, int d_s,
+                                        const int32_t* seq_len, float* scores, hipStream_t s) {
+  const int nblk = l_cap / kBlk;
+  const int runs = (nblk + kTokWavesPerWG - 1) / kTokWavesPerWG;
+  const long long units = (long long)n_seq * runs;
+  const dim3 grid((unsigned)(((units + 7) / 8) * 8 * rows_per_seq));
+  const int lph = d_s / 8;
+  auto q = static_cast<const uint16_t*>(q_sel);
+  auto k = static_cast<const uint8_t*>(k_tok);
+  auto ks = static_cast<const uint8_t*>(k_scale);
+  switch (kfmt) {
+    case SPOT_KFMT_BF16:
+      return launch_tokens_fmt<SPOT_KFMT_BF16>(lph, grid, s, q, w, k, ks, n_seq, rows_per_seq,
+                                               l_cap, nblk, runs, seq_len, scores);
+    case SPOT_KFMT_INT4_G32:
+      return launch_tokens_fmt<SPOT_KFMT_INT4_G32>(lph, grid, s, q, w, k, ks, n_seq,
+                                                   rows_per_seq, l_cap, nblk, runs, seq_len,
+                                                   scores);
+    default:
+      return launch_tokens_fmt<SPOT_KFMT_MXFP4_G32>(lph, grid, s, q, w, k, ks, n_seq,
+                                                    rows_per_seq, l_cap, nblk, runs, seq_len,
+                                                    scores);
+  }
+}
+
+}  // namespace spot

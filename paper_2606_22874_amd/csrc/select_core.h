@@ -201,7 +201,6 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
                                               float* __restrict__ mass_out, IdRecords pub) {
   constexpr int NT = kSelWG, NW = NT / 64;
   constexpr int P = 64 * SPL;
-  constexpr int BPT = kValBins / NT;   // value bins per thread in the scan
   constexpr float kLog2e = 1.4426950408889634f;
   static_assert(EPT <= 16, "a thread's ids must fit one bit word");
   (void)nblk;

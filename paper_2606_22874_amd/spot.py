@@ -27,7 +27,8 @@ STATUS = {0: "ok", 1: "null pointer", 2: "invalid shape", 3: "unsupported", 4: "
 KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2}
 BLK = 64
 
-SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score", "spot_select_blocks",
+SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score",
+           "spot_selector_score_tokens", "spot_select_blocks",
            "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
            "spot_sparse_prefill", "spot_decode_step_workspace_bytes", "spot_decode_step",
            "spot_probe_stream_read", "spot_probe_sink_words"]
@@ -61,6 +62,7 @@ def load(path: Optional[str] = None):
         L.spot_status_str.restype = ctypes.c_char_p
         L.spot_version.restype = ctypes.c_char_p
         L.spot_selector_score.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P, P]
+        L.spot_selector_score_tokens.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P, P]
         L.spot_select_blocks.argtypes = [P, I, I, P, F, I, I, I, I, P, P, P, P]
         L.spot_decode_workspace_bytes.argtypes = [I, I, I, I, I]
         L.spot_decode_workspace_bytes.restype = Z
@@ -74,7 +76,7 @@ def load(path: Optional[str] = None):
         L.spot_probe_stream_read.argtypes = [P, Z, P, P]
         L.spot_probe_stream_read.restype = ctypes.c_int32
         L.spot_probe_sink_words.restype = I
-        for name in ("spot_selector_score", "spot_select_blocks", "spot_sparse_decode",
+        for name in ("spot_selector_score", "spot_selector_score_tokens", "spot_select_blocks", "spot_sparse_decode",
                      "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step"):
             getattr(L, name).restype = ctypes.c_int32
         if path is None:
@@ -141,6 +143,26 @@ def spot_selector_score(q_sel, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq, nbl
     _check("spot_selector_score", load().spot_selector_score(
         _ptr(q_sel), _ptr(w), _ptr(k_sel), _ptr(k_scale), f, n_seq, rows_per_seq, nblk, h_s,
         d_s, _ptr(n_valid), _ptr(scores), _stream(stream)))
+
+
+def spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, h_s,
+                               d_s, seq_len, scores, stream=None):
+    rows = n_seq * rows_per_seq
+    f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
+    _dev(q_sel, "q_sel", BF16, rows * h_s * d_s)
+    _dev(w, "w", F32, rows * h_s)
+    if f == 0:
+        _dev(k_tok, "k_tok", BF16, n_seq * l_cap * h_s * d_s)
+    else:
+        _dev(k_tok, "k_tok", U8, n_seq * l_cap * h_s * d_s // 2)
+        _dev(k_scale, "k_scale", (torch.float16, torch.int16) if f == 1 else U8,
+             n_seq * l_cap * h_s * d_s // 32)
+    if seq_len is not None:
+        _dev(seq_len, "seq_len", I32, rows)
+    _dev(scores, "scores", F32, rows * (l_cap // 64))
+    _check("spot_selector_score_tokens", load().spot_selector_score_tokens(
+        _ptr(q_sel), _ptr(w), _ptr(k_tok), _ptr(k_scale), f, n_seq, rows_per_seq, l_cap, h_s,
+        d_s, _ptr(seq_len), _ptr(scores), _stream(stream)))
 
 
 def spot_select_blocks(scores, rows, nblk, n_valid, top_p, k_max, k_min, n_sink, n_recent, idx,
@@ -270,6 +292,22 @@ def selector_score(q_sel, w, k_sel, k_scale=None, kfmt="bf16", rows_per_seq=1, n
         out = torch.empty((rows, nblk), dtype=torch.float32, device=q_sel.device)
     spot_selector_score(q_sel, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq, nblk, h_s, d_s,
                         n_valid, out, stream)
+    return out
+
+
+def selector_score_tokens(q_sel, w, k_tok, k_scale=None, kfmt="bf16", rows_per_seq=1,
+                          seq_len=None, l_cap=None, out=None, stream=None):
+    """Per-block maximum of per-token scores [rows, l_cap // 64] float32."""
+    h_s, d_s = q_sel.shape[-2], q_sel.shape[-1]
+    rows = q_sel.numel() // (h_s * d_s)
+    n_seq = rows // rows_per_seq
+    if l_cap is None:
+        per = h_s * d_s if KFMT.get(kfmt, kfmt) == 0 else h_s * d_s // 2
+        l_cap = k_tok.numel() // (n_seq * per)
+    if out is None:
+        out = torch.empty((rows, l_cap // 64), dtype=torch.float32, device=q_sel.device)
+    spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, h_s,
+                               d_s, seq_len, out, stream)
     return out
 
 

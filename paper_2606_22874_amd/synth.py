@@ -217,6 +217,32 @@ def selector_planted(rng, B, L, Hs, ds, seq_len, n_planted=4, cosine=0.8):
     return q_sel, w, k_sel
 
 
+def selector_tokens(seed, B, L, Hs, ds, seq_len, n_planted=4, gain=3.0):
+    """Per-token selector inputs: q_sel [B, Hs, ds], w [B, Hs], k_tok
+    [B, L, Hs, ds] (BF16 bits).
+
+    Token keys are N(0, 1) draws (filled in parallel in runs of up to 4096
+    tokens); ``n_planted`` visible tokens per sequence, at random positions,
+    get gain * sqrt(ds) times the unit selector query of every head added, so
+    a few blocks stand out the way relevant context does.  w ~ U(0, 1).
+    """
+    rng = np.random.default_rng([seed, 91])
+    q_sel = bf16_bits(rng.standard_normal((B, Hs, ds), dtype=np.float32))
+    w = rng.uniform(0.0, 1.0, (B, Hs)).astype(np.float32)
+    run = min(L, 4096)
+    assert L % run == 0
+    k_tok = normal_bf16(seed, 4, (B, L // run, run * Hs * ds)).reshape(B, L, Hs, ds)
+    qhat = _unit(bf16_value(q_sel).astype(np.float64))
+    for b in range(B):
+        n = int(min(max(int(seq_len[b]), 0), L))
+        if n == 0:
+            continue
+        for t in rng.choice(n, size=min(n_planted, n), replace=False):
+            kt = bf16_value(k_tok[b, t]).astype(np.float64) + gain * math.sqrt(ds) * qhat[b]
+            k_tok[b, t] = bf16_bits(kt.astype(np.float32))
+    return q_sel, w, k_tok
+
+
 def selector_zipf(rng, B, nblk, Hs, ds, n_valid, rule: Rule, n_spikes=0,
                   zipf_a=1.1, t0=16.0, noise=0.06):
     """Pooled selector keys with a Zipf(zipf_a) relevance profile over blocks.

@@ -64,6 +64,17 @@ def test_validation_errors_before_launch(lib):
     assert lib.spot_selector_score(nz, nz, nz, None, 0, 1, 1, 4, 8, 32, None, nz, None) == 3
     # quantized format without scales
     assert lib.spot_selector_score(nz, nz, nz, None, 1, 1, 1, 4, 8, 64, None, nz, None) == 1
+    # per-token scorer: (q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, h_s, d_s,
+    # seq_len, scores, stream)
+    tok = lib.spot_selector_score_tokens
+    assert tok(nz, nz, None, None, 0, 1, 1, 4096, 8, 64, None, nz, None) == 1
+    assert tok(nz, nz, nz, None, 1, 1, 1, 4096, 8, 64, None, nz, None) == 1   # no scales
+    assert tok(nz, nz, nz, None, 0, 1, 1, 4000, 8, 64, None, nz, None) == 2   # l_cap % 64
+    assert tok(nz, nz, nz, None, 0, 1, 0, 4096, 8, 64, None, nz, None) == 2
+    assert tok(nz, nz, nz, None, 0, 1, 1, 4096, 8, 32, None, nz, None) == 3
+    assert tok(nz, nz, nz, None, 0, 1, 1, 4096, 16, 32, None, nz, None) == 3
+    assert tok(nz, nz, nz, None, 5, 1, 1, 4096, 8, 64, None, nz, None) == 3
+    assert tok(nz, nz, nz, None, 0, 0, 1, 4096, 8, 64, None, nz, None) == 0   # nothing to do
     # rules: NaN p, k_min > k_max, k_max < n_sink + n_recent, k_max < 1
     sel = lib.spot_select_blocks
     assert sel(nz, 1, 8, None, float("nan"), 4, 0, 1, 2, nz, nz, None, None) == 4
