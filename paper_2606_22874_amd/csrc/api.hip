@@ -63,9 +63,9 @@ spot_status spot_selector_score_tokens(const void* q_sel, const float* w, const 
     return SPOT_ERR_UNSUPPORTED;
   if (kfmt != SPOT_KFMT_BF16 && !k_scale) return SPOT_ERR_NULL;
   if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
-  // Launch size: one workgroup per (row, run of 4 blocks), padded to 8 runs.
-  const long long runs = (l_cap / kBlk + 3) / 4;
-  if (((long long)n_seq * runs + 7) / 8 * 8 * rows_per_seq > 0x7fffffffLL) return SPOT_ERR_SHAPE;
+  // Launch size: at most one workgroup per (row, block), padded to 8 blocks.
+  if (((long long)n_seq * (l_cap / kBlk) + 7) / 8 * 8 * rows_per_seq > 0x7fffffffLL)
+    return SPOT_ERR_SHAPE;
   if (n_seq == 0 || l_cap == 0) return SPOT_OK;
   return from_hip(launch_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq,
                                                rows_per_seq, l_cap, d_s, seq_len, scores,

@@ -26,6 +26,17 @@ __device__ __forceinline__ float e8m0_to_f32(uint32_t e) {
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
+// Global loads, optionally non-temporal (NT: the line is not kept in the
+// caches -- for data streamed exactly once, which then does not evict
+// anything reused).
+template <bool NT, class T>
+__device__ __forceinline__ T ld(const void* p) {
+  if constexpr (NT)
+    return __builtin_nontemporal_load(reinterpret_cast<const T*>(p));
+  else
+    return *reinterpret_cast<const T*>(p);
+}
+
 template <int KFMT>
 struct KeyLoad;
 
@@ -33,8 +44,10 @@ struct KeyLoad;
 template <>
 struct KeyLoad<SPOT_KFMT_BF16> {
   uint4 raw;
+  template <bool NT = false>
   __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t*, size_t blk, int lane) {
-    raw = *reinterpret_cast<const uint4*>(kb + blk * 1024 + lane * 16);
+    const u32x4 t = ld<NT, u32x4>(kb + blk * 1024 + lane * 16);
+    raw = make_uint4(t[0], t[1], t[2], t[3]);
   }
   __device__ __forceinline__ float dot(const uint4& qraw, const float*) const {
     float a = dot2_bf16(qraw.x, raw.x, 0.f);
@@ -49,9 +62,10 @@ template <>
 struct KeyLoad<SPOT_KFMT_INT4_G32> {
   uint32_t codes;
   uint16_t scale;
+  template <bool NT = false>
   __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t* ks, size_t blk, int lane) {
-    codes = *reinterpret_cast<const uint32_t*>(kb + blk * 256 + lane * 4);
-    scale = *reinterpret_cast<const uint16_t*>(ks + (blk * 16 + (lane >> 2)) * 2);
+    codes = ld<NT, uint32_t>(kb + blk * 256 + lane * 4);
+    scale = ld<NT, uint16_t>(ks + (blk * 16 + (lane >> 2)) * 2);
   }
   __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
     float a = 0.f;
@@ -69,9 +83,10 @@ template <>
 struct KeyLoad<SPOT_KFMT_MXFP4_G32> {
   uint32_t codes;
   uint8_t scale;
+  template <bool NT = false>
   __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t* ks, size_t blk, int lane) {
-    codes = *reinterpret_cast<const uint32_t*>(kb + blk * 256 + lane * 4);
-    scale = ks[blk * 16 + (lane >> 2)];
+    codes = ld<NT, uint32_t>(kb + blk * 256 + lane * 4);
+    scale = ld<NT, uint8_t>(ks + blk * 16 + (lane >> 2));
   }
   __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
     // v_cvt_scalef32_pk_f32_fp4 (scale 1): byte b of the codes -> the exact

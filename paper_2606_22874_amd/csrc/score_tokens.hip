@@ -26,7 +26,8 @@
 namespace spot {
 namespace {
 
-constexpr int kTokWavesPerWG = 4;  // one 64-token block per wave
+constexpr int kTokWavesPerWG = 4;
+constexpr int kTokTPW = 32;         // tokens per wave (two waves per block)
 
 // Butterfly exchange partner moves, all DPP inside a 16-lane row: the partner
 // differs from the lane in the bit being folded (half-mirror 7 - i flips bit
@@ -54,90 +55,126 @@ __device__ __forceinline__ void fold_half_rows(const float (&in)[2 * N], float (
   }
 }
 
-// Launch order: work units u = (sequence, run of 4 blocks) and the
-// rows_per_seq query rows of a sequence.  Workgroup ids go round-robin over
-// the 8 XCDs, so the rows that read the same keys are given ids 8 apart --
-// the same XCD, hence the same L2 -- and consecutive units alternate XCDs.
-template <int KFMT, int LPH>
+// Cross-row head sum of the G group values of a lane (G = 2, 4 or 8) and the
+// maximum over them: after the folds over lane bits 4 and 5 each lane holds
+// complete scores (G/4 of them, or one for G = 2), covering every token of
+// the wave between the lanes.
+template <int G>
+__device__ __forceinline__ float rows_sum_max(const float (&y)[G], int lane) {
+  if constexpr (G == 8) {
+    float z[4], v[2];
+    fold_half_rows<16, 4>(y, z, lane & 16);
+    fold_half_rows<32, 2>(z, v, lane & 32);
+    return fmaxf(v[0], v[1]);
+  } else if constexpr (G == 4) {
+    float z[2], v[1];
+    fold_half_rows<16, 2>(y, z, lane & 16);
+    fold_half_rows<32, 1>(z, v, lane & 32);
+    return v[0];
+  } else {
+    float z[1];
+    fold_half_rows<16, 1>(y, z, lane & 16);
+    return z[0] + __shfl_xor(z[0], 32, 64);
+  }
+}
+
+// TPW tokens per wavefront (16, 32 or 64): a block is shared by 64 / TPW
+// waves of one workgroup, whose partial maxima meet in LDS.
+//
+// Launch order: work units u = (sequence, run of the 4 * TPW / 64 blocks of
+// one workgroup) and the rows_per_seq query rows of a sequence.  Workgroup
+// ids go round-robin over the 8 XCDs, so the rows that read the same keys
+// are given ids 8 apart -- the same XCD, hence the same L2 -- and
+// consecutive units alternate XCDs.
+template <int KFMT, int LPH, int TPW>
 __global__ __launch_bounds__(256) void score_tokens_kernel(
     const uint16_t* __restrict__ q_sel, const float* __restrict__ w,
     const uint8_t* __restrict__ k_tok, const uint8_t* __restrict__ k_scale, int n_seq,
     int rows_per_seq, int l_cap, int nblk, int runs, const int32_t* __restrict__ seq_len,
     float* __restrict__ scores) {
   constexpr int kHeads = 64 / LPH;
-  const int lane = threadIdx.x & 63;
+  constexpr int G = TPW / 8;                 // groups of 8 tokens per wave
+  constexpr int WPB = 64 / TPW;              // waves per block
+  constexpr int BPW = kTokWavesPerWG / WPB;  // blocks per workgroup
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gsize = 8 * rows_per_seq;
   const int id = blockIdx.x;
   const int unit = (id / gsize) * 8 + (id & 7);
   const int rr = (id % gsize) >> 3;
   if (unit >= n_seq * runs) return;
   const int seq = unit / runs;
-  const int j = (unit % runs) * kTokWavesPerWG + (threadIdx.x >> 6);
-  if (j >= nblk) return;
+  const int j = (unit % runs) * BPW + wave / WPB;
   const int row = seq * rows_per_seq + rr;
   int len = seq_len ? seq_len[row] : l_cap;
   len = len < 0 ? 0 : (len > l_cap ? l_cap : len);
-  const int t0 = j * 64;
+  const int t0 = j * 64 + (wave % WPB) * TPW;  // this wave's first token
+
+  float m = -INFINITY;
+  if (j < nblk && t0 < len) {
+    const int tlim = min(j * 64 + 64, len) - 1;
+    const size_t base = (size_t)seq * l_cap;
+    const uint4 qraw = *reinterpret_cast<const uint4*>(q_sel + (size_t)row * 512 + lane * 8);
+    float qf[8];
+    qf[0] = bf16_lo(qraw.x); qf[1] = bf16_hi(qraw.x);
+    qf[2] = bf16_lo(qraw.y); qf[3] = bf16_hi(qraw.y);
+    qf[4] = bf16_lo(qraw.z); qf[5] = bf16_hi(qraw.z);
+    qf[6] = bf16_lo(qraw.w); qf[7] = bf16_hi(qraw.w);
+    const float wh = w[(size_t)row * kHeads + lane / LPH];
+
+    // y[g]: the in-row head sum of this lane's token of group g (tokens
+    // t0 + 8g .. t0 + 8g + 7; the lane holds token (LPH == 8 ? lane : lane >> 1) & 7).
+    float y[G];
+    KeyLoad<KFMT> key[2][8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      key[0][u].template load<true>(k_tok, k_scale, base + min(t0 + u, tlim), lane);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      if (g + 1 < G) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          key[(g + 1) & 1][u].template load<true>(k_tok, k_scale,
+                                                  base + min(t0 + 8 * (g + 1) + u, tlim), lane);
+      }
+      float p[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) p[u] = key[g & 1][u].dot(qraw, qf);
+      float d;
+      if constexpr (LPH == 8) {
+        // Head lanes are lane bits 0..2.
+        float a[4], c[2], e[1];
+        fold_half<kDppHalfMirror, 4>(p, a, lane & 4);
+        fold_half<kDppQuadXor2, 2>(a, c, lane & 2);
+        fold_half<kDppQuadXor1, 1>(c, e, lane & 1);
+        d = wh * fmaxf(e[0], 0.f);
+        d += dpp_f<0x128>(d);  // row_ror:8 -- the other head of this 16-lane row
+      } else {
+        // Head lanes are lane bits 0..3.
+        float a[4], c[2], e[1];
+        fold_half<kDppMirror, 4>(p, a, lane & 8);
+        fold_half<kDppHalfMirror, 2>(a, c, lane & 4);
+        fold_half<kDppQuadXor2, 1>(c, e, lane & 2);
+        const float h = e[0] + dpp_f<kDppQuadXor1>(e[0]);
+        d = wh * fmaxf(h, 0.f);
+      }
+      y[g] = d;
+    }
+    m = wave_max(rows_sum_max<G>(y, lane));
+  }
   float* dst = scores + (size_t)row * nblk + j;
-  if (t0 >= len) {
-    if (lane == 0) *dst = -INFINITY;
-    return;
-  }
-  const int tlim = min(t0 + 64, len) - 1;
-  const size_t base = (size_t)seq * l_cap;
-
-  const uint4 qraw = *reinterpret_cast<const uint4*>(q_sel + (size_t)row * 512 + lane * 8);
-  float qf[8];
-  qf[0] = bf16_lo(qraw.x); qf[1] = bf16_hi(qraw.x);
-  qf[2] = bf16_lo(qraw.y); qf[3] = bf16_hi(qraw.y);
-  qf[4] = bf16_lo(qraw.z); qf[5] = bf16_hi(qraw.z);
-  qf[6] = bf16_lo(qraw.w); qf[7] = bf16_hi(qraw.w);
-  const float wh = w[(size_t)row * kHeads + lane / LPH];
-
-  // y[g]: the in-row head sum of this lane's token of group g (tokens
-  // t0 + 8g .. t0 + 8g + 7; lane holds token (LPH == 8 ? lane : lane >> 1) & 7).
-  float y[8];
-  KeyLoad<KFMT> key[2][8];
+  if constexpr (WPB == 1) {
+    if (lane == 0 && j < nblk) *dst = m;
+  } else {
+    __shared__ float part[kTokWavesPerWG];
+    if (lane == 0) part[wave] = m;
+    __syncthreads();
+    if (lane == 0 && wave % WPB == 0 && j < nblk) {
+      float b = part[wave];
 #pragma unroll
-  for (int u = 0; u < 8; ++u)
-    key[0][u].load(k_tok, k_scale, base + min(t0 + u, tlim), lane);
-#pragma unroll
-  for (int g = 0; g < 8; ++g) {
-    if (g + 1 < 8) {
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        key[(g + 1) & 1][u].load(k_tok, k_scale, base + min(t0 + 8 * (g + 1) + u, tlim), lane);
+      for (int i = 1; i < WPB; ++i) b = fmaxf(b, part[wave + i]);
+      *dst = b;
     }
-    float p[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) p[u] = key[g & 1][u].dot(qraw, qf);
-    float d;
-    if constexpr (LPH == 8) {
-      // Head lanes are lane bits 0..2.
-      float a[4], c[2];
-      fold_half<kDppHalfMirror, 4>(p, a, lane & 4);
-      fold_half<kDppQuadXor2, 2>(a, c, lane & 2);
-      float c1[1];
-      fold_half<kDppQuadXor1, 1>(c, c1, lane & 1);
-      d = wh * fmaxf(c1[0], 0.f);
-      d += dpp_f<0x128>(d);  // row_ror:8 -- the other head of this 16-lane row
-    } else {
-      // Head lanes are lane bits 0..3.
-      float a[4], c[2], e[1];
-      fold_half<kDppMirror, 4>(p, a, lane & 8);
-      fold_half<kDppHalfMirror, 2>(a, c, lane & 4);
-      fold_half<kDppQuadXor2, 1>(c, e, lane & 2);
-      const float h = e[0] + dpp_f<kDppQuadXor1>(e[0]);
-      d = wh * fmaxf(h, 0.f);
-    }
-    y[g] = d;
   }
-  // Sum over the 4 rows of the wave: fold the groups over lane bits 4 and 5.
-  float z[4], v[2];
-  fold_half_rows<16, 4>(y, z, lane & 16);
-  fold_half_rows<32, 2>(z, v, lane & 32);
-  const float m = wave_max(fmaxf(v[0], v[1]));
-  if (lane == 0) *dst = m;
 }
 
 template <int KFMT>
@@ -146,10 +183,10 @@ hipError_t launch_tokens_fmt(int lph, dim3 grid, hipStream_t s, const uint16_t* 
                              int rows_per_seq, int l_cap, int nblk, int runs,
                              const int32_t* seq_len, float* out) {
   if (lph == 8)
-    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 8>), grid, dim3(256), 0, s, q, w, k, ks,
+    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 8, kTokTPW>), grid, dim3(256), 0, s, q, w, k, ks,
                        n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
   else
-    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 16>), grid, dim3(256), 0, s, q, w, k, ks,
+    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 16, kTokTPW>), grid, dim3(256), 0, s, q, w, k, ks,
                        n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
   return hipGetLastError();
 }
@@ -161,7 +198,8 @@ hipError_t launch_selector_score_tokens(const void* q_sel, const float* w, const
                                         int rows_per_seq, int l_cap, int d_s,
                                         const int32_t* seq_len, float* scores, hipStream_t s) {
   const int nblk = l_cap / kBlk;
-  const int runs = (nblk + kTokWavesPerWG - 1) / kTokWavesPerWG;
+  constexpr int kBlocksPerWG = kTokWavesPerWG * kTokTPW / 64;
+  const int runs = (nblk + kBlocksPerWG - 1) / kBlocksPerWG;
   const long long units = (long long)n_seq * runs;
   const dim3 grid((unsigned)(((units + 7) / 8) * 8 * rows_per_seq));
   const int lph = d_s / 8;
