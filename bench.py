@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--dense", action="store_true", help=argparse.SUPPRESS)   # the default
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the quantized-selector and smaller-workload decode timings")
+    ap.add_argument("--tokens", action="store_true",
+                    help="run the per-token selector leg even with --no-extra")
     ap.add_argument("--fmt", default="bf16", choices=["bf16", "int4", "mxfp4"])
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the block-sparse prefill leg (32K-token layer)")
@@ -58,6 +60,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 STEP_PROFILE = os.path.join(ROOT, "profiles", "decode_step_L131072_B4.md")
 # Sources whose code the fused step kernel is built from.
 STEP_SOURCES = ("step.hip", "decode_core.h", "score_core.h", "select_core.h", "spot_internal.h")
+TOKENS_PROFILE = os.path.join(ROOT, "profiles", "score_tokens_L131072_B4.md")
+TOKENS_SOURCES = ("score_tokens.hip", "score_core.h", "spot_internal.h")
+SEED_TOKENS = 20260611
 
 
 def source_hash(files=STEP_SOURCES) -> str:
@@ -319,6 +324,11 @@ def main():
             "hbm_frac": round(dbytes / (dms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         }
 
+    if (args.tokens or not args.no_extra) and args.fmt == "bf16":
+        result["per_token_selector"] = per_token_leg(args, torch, spot, synth, dev, timed, wl,
+                                                     copies, q, seq_len, n_valid, idx, cnt,
+                                                     mass, out, lse, ws, stream)
+
     if not args.no_extra:
         del copies, bufs
         torch.cuda.empty_cache()
@@ -334,6 +344,65 @@ def main():
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
+
+
+def per_token_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, n_valid, idx,
+                  cnt, mass, out, lse, ws, stream):
+    """The decode step with the paper's own selector cache -- one 4 x 128
+    selector key per token, block value = maximum of its tokens' scores --
+    on the same 128K-token, batch-4 layer: spot_selector_score_tokens, then
+    selection and sparse attention as separate launches."""
+    B, L, rule = wl.B, wl.L, wl.rule
+    Hs, ds = 4, 128
+    log("[bench] per-token selector: generating the 4 x 128 per-token cache")
+    q_tok, w_tok, k_tok = synth.selector_tokens(SEED_TOKENS, B, L, Hs, ds, wl.seq_len)
+    qs = spot.to_device_bf16(q_tok, dev)
+    ws_ = torch.from_numpy(w_tok).to(dev)
+    ktoks = [spot.to_device_bf16(k_tok, dev) for _ in range(2)]
+    tok_bytes = k_tok.nbytes
+    del k_tok
+    nblk = L // 64
+    scores = torch.empty((B, nblk), dtype=torch.float32, device=dev)
+
+    def score(c):
+        spot.spot_selector_score_tokens(qs, ws_, ktoks[c % 2], None, "bf16", B, 1, L, Hs, ds,
+                                        seq_len, scores, stream)
+
+    def step(c):
+        score(c)
+        k, v, _, _ = copies[c % len(copies)]
+        spot.spot_select_blocks(scores, B, nblk, n_valid, rule.top_p, rule.k_max, rule.k_min,
+                                rule.n_sink, rule.n_recent, idx, cnt, mass, stream)
+        spot.spot_sparse_decode(q, k, v, seq_len, idx, cnt, rule.k_max, B, wl.Hq, wl.Hkv, wl.d,
+                                L, wl.sm_scale, out, lse, ws, stream)
+
+    for i in range(args.warmup):
+        step(i)
+    sms = timed(score, args.steps)
+    ms = timed(step, args.steps)
+    counts = cnt.cpu().numpy()
+    attn_bytes = int(counts.sum()) * 64 * wl.Hkv * wl.d * 4
+    gbs = tok_bytes / (sms * 1e-3) / 1e9
+    log(f"[bench] per-token selector: score {sms * 1e3:.1f} us ({gbs:.0f} GB/s), "
+        f"step {ms * 1e3:.1f} us")
+    del ktoks
+    return {
+        "workload": f"decode L={L} B={B}, per-token selector cache {Hs}x{ds} BF16 "
+                    f"({tok_bytes >> 20} MiB), block value = max over its 64 tokens; "
+                    f"p={rule.top_p} K_max={rule.k_max}",
+        "us_per_step": round(ms * 1e3, 2),
+        "steps_per_s": round(1e3 / ms, 1),
+        "mean_selected_blocks": float(counts.mean()),
+        "bytes_per_step": int(tok_bytes + attn_bytes),
+        "hbm_frac": round((tok_bytes + attn_bytes) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "scorer_roofline": {
+            "bound": "hbm", "kernel": "score_tokens_kernel (spot_selector_score_tokens)",
+            "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes_per_launch": int(tok_bytes),
+            "avg_launch_us": round(sms * 1e3, 2),
+            "traffic": measured_traffic(TOKENS_PROFILE, TOKENS_SOURCES),
+        },
+    }
 
 
 def small_decode_legs(args, torch, spot, synth, dev, timed):

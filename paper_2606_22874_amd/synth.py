@@ -217,29 +217,49 @@ def selector_planted(rng, B, L, Hs, ds, seq_len, n_planted=4, cosine=0.8):
     return q_sel, w, k_sel
 
 
-def selector_tokens(seed, B, L, Hs, ds, seq_len, n_planted=4, gain=3.0):
-    """Per-token selector inputs: q_sel [B, Hs, ds], w [B, Hs], k_tok
-    [B, L, Hs, ds] (BF16 bits).
+def selector_tokens(seed, B, L, Hs, ds, seq_len, rule=None, zipf_a=1.1, t0=16.0,
+                    noise=0.06):
+    """Per-token selector inputs with the Zipf relevance profile of
+    ``selector_zipf`` carried by one token per block.
 
-    Token keys are N(0, 1) draws (filled in parallel in runs of up to 4096
-    tokens); ``n_planted`` visible tokens per sequence, at random positions,
-    get gain * sqrt(ds) times the unit selector query of every head added, so
-    a few blocks stand out the way relevant context does.  w ~ U(0, 1).
+    Returns q_sel [B, Hs, ds] (N(0, I/ds) draws, so |q_h| is about 1),
+    w [B, Hs] ~ U(0, 1) and k_tok [B, L, Hs, ds] (BF16 bits).  Every token key
+    is N(0, I) (filled in parallel in runs of up to 4096 tokens), which gives
+    background token scores of order sum_h w_h.  In each residual block (not
+    a sink or recency block of ``rule``) one visible "lead" token, at a random
+    position, is replaced by a key whose dot product with each head's query is
+    T_j / sum_h w_h + N(0, noise^2), with T_j = t0 - zipf_a * ln(rank_j) for a
+    random permutation rank of 1..n_res; its other directions are N(0, I).
+    The lead token's score is then T_j, so block values follow a Zipf law
+    under the residual softmax, as in the pooled-key workloads.
     """
+    rule = Rule(0.95, 128, 0, 1, 2) if rule is None else rule
     rng = np.random.default_rng([seed, 91])
-    q_sel = bf16_bits(rng.standard_normal((B, Hs, ds), dtype=np.float32))
+    q = rng.standard_normal((B, Hs, ds)) / math.sqrt(ds)
+    q_sel = bf16_bits(q.astype(np.float32))
     w = rng.uniform(0.0, 1.0, (B, Hs)).astype(np.float32)
+    qf = bf16_value(q_sel).astype(np.float64)
+    qn = np.linalg.norm(qf, axis=-1)                          # [B, Hs]
+    qhat = qf / qn[..., None]
     run = min(L, 4096)
     assert L % run == 0
     k_tok = normal_bf16(seed, 4, (B, L // run, run * Hs * ds)).reshape(B, L, Hs, ds)
-    qhat = _unit(bf16_value(q_sel).astype(np.float64))
     for b in range(B):
         n = int(min(max(int(seq_len[b]), 0), L))
-        if n == 0:
+        nv = (n + BLK - 1) // BLK
+        res = np.flatnonzero(~_reserved_mask(nv, rule.n_sink, rule.n_recent))
+        if len(res) == 0:
             continue
-        for t in rng.choice(n, size=min(n_planted, n), replace=False):
-            kt = bf16_value(k_tok[b, t]).astype(np.float64) + gain * math.sqrt(ds) * qhat[b]
-            k_tok[b, t] = bf16_bits(kt.astype(np.float32))
+        T = t0 - zipf_a * np.log(rng.permutation(len(res)) + 1.0)
+        lo = res * BLK
+        pos = lo + (rng.random(len(res)) * (np.minimum(lo + BLK, n) - lo)).astype(np.int64)
+        z = rng.standard_normal((len(res), Hs, ds))
+        along = np.sum(z * qhat[b][None], axis=-1)
+        perp = z - along[..., None] * qhat[b][None]
+        t = T[:, None] / float(np.sum(w[b], dtype=np.float64)) + \
+            rng.standard_normal((len(res), Hs)) * noise
+        lead = perp + (t / qn[b][None])[..., None] * qhat[b][None]
+        k_tok[b, pos] = bf16_bits(lead.astype(np.float32))
     return q_sel, w, k_tok
 
 
