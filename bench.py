@@ -324,6 +324,10 @@ def main():
             "hbm_frac": round(dbytes / (dms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         }
 
+    if not args.no_extra and args.fmt == "bf16":
+        result["static_topk"] = static_topk_leg(args, torch, spot, dev, timed, wl, copies, q,
+                                                q_sel, w, seq_len, n_valid, out, lse, stream)
+
     if (args.tokens or not args.no_extra) and args.fmt == "bf16":
         result["per_token_selector"] = per_token_leg(args, torch, spot, synth, dev, timed, wl,
                                                      copies, q, seq_len, n_valid, idx, cnt,
@@ -344,6 +348,43 @@ def main():
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
+
+
+def static_topk_leg(args, torch, spot, dev, timed, wl, copies, q, q_sel, w, seq_len, n_valid,
+                    out, lse, stream):
+    """Static top-K (Eq. select-topk) at large budgets on the 128K-token,
+    batch-4 workload: K = 0.25, 0.5 and 0.75 of the 2048 blocks, no reserved
+    blocks, through spot_decode_step (fused for K <= 512, three stages
+    above)."""
+    B, L, nblk = wl.B, wl.L, wl.nblk
+    res = {}
+    for frac in (0.25, 0.5, 0.75):
+        K = int(frac * nblk)
+        ws_k = spot.step_workspace(B, wl.Hq, wl.Hkv, wl.d, K, dev)
+        scores = torch.empty((B, nblk), dtype=torch.float32, device=dev)
+        idx = torch.empty((B, K), dtype=torch.int32, device=dev)
+        cnt = torch.empty(B, dtype=torch.int32, device=dev)
+
+        def step(c, K=K, ws_k=ws_k, scores=scores, idx=idx, cnt=cnt):
+            k, v, ks, sc = copies[c % len(copies)]
+            spot.spot_decode_step(q_sel, w, ks, sc, "bf16", wl.Hs, wl.ds, n_valid, 1.0, K, 0,
+                                  0, 0, q, k, v, seq_len, B, wl.Hq, wl.Hkv, wl.d, L,
+                                  wl.sm_scale, scores, idx, cnt, None, out, lse, ws_k, stream)
+
+        for i in range(3):
+            step(i)
+        n = max(5, args.steps // 10)
+        ms = timed(step, n)
+        counts = cnt.cpu().numpy()
+        nbytes = wl.k_sel.nbytes + int(counts.sum()) * 64 * wl.Hkv * wl.d * 4
+        res[f"K={K}"] = {"fraction_of_blocks": frac, "us_per_step": round(ms * 1e3, 2),
+                         "steps_per_s": round(1e3 / ms, 1), "bytes_per_step": int(nbytes),
+                         "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                         "path": "fused" if K <= 512 else "three launches"}
+        log(f"[bench] static top-K K={K}: {ms * 1e3:.1f} us/step")
+        del ws_k
+    return {"workload": f"decode L={L} B={B}, static top-K (p >= 1, no reserved blocks)",
+            "budgets": res}
 
 
 def per_token_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, n_valid, idx,

@@ -4,8 +4,9 @@
 // Three kernels, chosen by row length and cap (one row per workgroup):
 //  * rows of up to 512 blocks: one wavefront (select_wave_kernel);
 //  * 513 .. 4096 blocks: one 256-thread workgroup (select_wg_kernel, its body
-//    in select_core.h, shared with the fused decode step);
-//  * longer rows or caps above 512: the 256-thread sort-based select_kernel.
+//    in select_core.h, shared with the fused decode step), for caps up to
+//    1024 and, when top_p >= 1 (static top-K: no survivor sort), any cap;
+//  * longer rows or larger caps: the 256-thread sort-based select_kernel.
 // All follow the same steps per row:
 //  1. reserved blocks (sink prefix, recency suffix) are set aside; the
 //     residual candidates get an order-preserving 32-bit key of their score;
@@ -595,17 +596,22 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
   const int ept = nblk <= 64 ? 1 : nblk <= 128 ? 2 : nblk <= 256 ? 4 : nblk <= 512 ? 8
                 : nblk <= 1024 ? 16 : nblk <= 2048 ? 32 : 64;
   const int spl = P <= 64 ? 1 : P / 64;
-  if (nblk > 512 && nblk <= 4096 && spl <= 8) {
+  // With top_p >= 1 every candidate up to the cap is kept, so the survivors
+  // are never sorted and the survivor buffer (64 * SPL keys) does not bound
+  // the cap: static top-K at any budget runs on the 512-key instantiation.
+  const int spl_wg = top_p >= 1.f && spl > 8 ? 8 : spl;
+  if (nblk > 512 && nblk <= 4096 && spl_wg <= 16) {
     const int e2 = nblk <= 1024 ? 4 : nblk <= 2048 ? 8 : 16;
 #define SPOT_SELECT_WG(E, S)                                                                    \
-    if (e2 == E && spl == S) {                                                                \
+    if (e2 == E && spl_wg == S) {                                                             \
       hipLaunchKernelGGL((select_wg_kernel<E, S>), grid, dim3(kSelWG), 0, s, scores, nblk,    \
                          n_valid, top_p, k_max, k_min, n_sink, n_recent, idx, count,          \
                          nuc_mass);                                                           \
       return hipGetLastError();                                                                \
     }
-#define SPOT_SELECT_WG_E(E) \
-    SPOT_SELECT_WG(E, 1) SPOT_SELECT_WG(E, 2) SPOT_SELECT_WG(E, 4) SPOT_SELECT_WG(E, 8)
+#define SPOT_SELECT_WG_E(E)                                                      \
+    SPOT_SELECT_WG(E, 1) SPOT_SELECT_WG(E, 2) SPOT_SELECT_WG(E, 4) SPOT_SELECT_WG(E, 8) \
+    SPOT_SELECT_WG(E, 16)
     SPOT_SELECT_WG_E(4)
     SPOT_SELECT_WG_E(8)
     SPOT_SELECT_WG_E(16)

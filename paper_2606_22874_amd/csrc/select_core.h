@@ -9,7 +9,8 @@
 namespace spot {
 
 __device__ __forceinline__ uint32_t order_key(float f) {
-  const uint32_t u = __float_as_uint(f);
+  uint32_t u = __float_as_uint(f);
+  u = u == 0x80000000u ? 0u : u;   // -0 and +0 are the same score (a tie)
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 __device__ __forceinline__ float order_key_inv(uint32_t k) {

@@ -158,6 +158,10 @@ SELECT_CASES = [
     (8, 100, Rule(0.9, 200, 0, 1, 2), None),            # k_max > nblk
     (16, 5, Rule(0.7, 4, 0, 1, 2), "tiny"),              # nblk <= sink + recent
     (4, 16384, Rule(0.99, 4096, 0, 4, 4), None),         # largest supported sizes
+    (8, 2048, Rule(1.0, 1536, 0, 1, 2), None),          # static top-K, cap above 512
+    (8, 4096, Rule(1.0, 3000, 0, 0, 0), "ragged"),      # static top-K, cap above 2048
+    (8, 2048, Rule(0.999, 1000, 0, 1, 2), None),        # nucleus under a 1000-block cap
+    (4, 2048, Rule(0.0, 900, 600, 1, 2), None),         # k_min floor of 600 blocks
 ]
 
 
@@ -200,6 +204,24 @@ def test_select_deterministic_and_ties():
         assert torch.equal(x, y)
     np.testing.assert_array_equal(a[0].cpu().numpy(), idx_o)
     np.testing.assert_array_equal(a[1].cpu().numpy(), cnt_o)
+
+
+@pytest.mark.parametrize("nblk,k_max", [(300, 100), (2048, 100), (2048, 1500), (8192, 700)])
+def test_select_negative_zero_ties_positive_zero(nblk, k_max):
+    """-0.0 and +0.0 are the same score: a cut through a run of zeros of
+    both signs takes the lower ids, whatever their sign (every selection
+    kernel: one wave, one workgroup, the sort-based kernel)."""
+    rng = np.random.default_rng(nblk + k_max)
+    rows = 8
+    s = np.where(rng.random((rows, nblk)) < 0.5, np.float32(0.0), np.float32(-0.0))
+    s[:, rng.choice(nblk, size=k_max // 3, replace=False)] = 1.0   # the cut falls in the zeros
+    s = s.astype(np.float32)
+    for rule in (Rule(1.0, k_max, 0, 1, 2), Rule(0.5, k_max, 0, 1, 2)):
+        idx_o, cnt_o, _ = oracle.select_blocks(s.astype(np.float64), rule)
+        idx_g, cnt_g, _ = spot.select_blocks(f32(s), rule)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(cnt_g.cpu().numpy(), cnt_o)
+        np.testing.assert_array_equal(idx_g.cpu().numpy(), idx_o)
 
 
 @pytest.mark.parametrize("cfg,fmt", [(1, "bf16"), (2, "bf16"), (3, "bf16"), (3, "int4"),

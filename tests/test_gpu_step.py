@@ -9,6 +9,8 @@ sets are checked against the oracle's with the near-tie / mass-boundary
 exemptions of selcheck, and the outputs against the oracle run on the fused
 path's own block sets.
 """
+import copy
+
 import numpy as np
 import pytest
 import torch
@@ -122,6 +124,36 @@ def test_step_end_to_end_vs_oracle():
     assert np.max(np.abs(g - out_o)) <= 2e-2
     assert np.linalg.norm(g - out_o) / np.linalg.norm(out_o) <= 1e-2
     assert np.max(np.abs(lse.cpu().numpy() - lse_o)) <= 2e-3
+
+
+@pytest.mark.parametrize("frac", [0.25, 0.5, 0.75])
+def test_static_topk_large_budgets(frac):
+    """Static top-K (Eq. select-topk: p >= 1 keeps every block, no reserved
+    blocks, the cap K_max = K picks the top K) at a quarter, half and three
+    quarters of the 2048 blocks of the 128K-token workload.  K = 512 runs in
+    the fused launch, 1024 and 1536 as three stages.  The sets must equal the
+    oracle's top-K of the same FP32 scores (unique: ties go to the lower id);
+    the outputs are checked against the oracle on two sequences."""
+    wl = copy.copy(workload(3))
+    K = int(frac * wl.nblk)
+    wl.rule = Rule(1.0, K, 0, 0, 0)
+    print(f"[step] static top-K K={K}", flush=True)
+    x = inputs(wl, "bf16")
+    s, idx, cnt, mass, out, lse = fused(x, wl)
+    torch.cuda.synchronize()
+    s_g = s.cpu().numpy().astype(np.float64)
+    idx_o, cnt_o, _ = oracle.select_blocks(s_g, wl.rule, wl.n_valid)
+    idx_g, cnt_g = idx.cpu().numpy(), cnt.cpu().numpy()
+    assert np.all(cnt_g == K)
+    np.testing.assert_array_equal(cnt_g, cnt_o)
+    np.testing.assert_array_equal(idx_g, idx_o)
+    pick = [0, 3]
+    out_o, lse_o = oracle.sparse_decode(wl.q[pick], wl.k[pick], wl.v[pick], wl.seq_len[pick],
+                                        idx_g[pick], cnt_g[pick], wl.sm_scale)
+    g = out.float().cpu().numpy().astype(np.float64)[pick]
+    assert np.max(np.abs(g - out_o)) <= 2e-2
+    assert np.linalg.norm(g - out_o) / np.linalg.norm(out_o) <= 1e-2
+    assert np.max(np.abs(lse.cpu().numpy()[pick] - lse_o)) <= 2e-3
 
 
 def test_step_repeated_calls_reset_workspace():
