@@ -58,6 +58,8 @@ def lib():
             L.oracle_key_value.restype = D
             L.oracle_selector_score.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P]
             L.oracle_selector_score_tokens.argtypes = [P, P, P, P, I, I, I, I, I, I, I, P, P]
+            L.oracle_selector_project.argtypes = [P, P, P, P, P, I, I, I, I, I, D, P, P, P]
+            L.oracle_selector_pool.argtypes = [P, I, I, I, I, P, P]
             L.oracle_select_blocks.argtypes = [P, I, I, P, D, I, I, I, I, P, P, P]
             L.oracle_select_blocks.restype = I
             L.oracle_sparse_decode.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, I, D, P, P]
@@ -136,6 +138,34 @@ def selector_score_tokens(q_sel, w, k_tok, k_scale=None, kfmt="bf16", rows_per_s
     out = np.empty((rows, l_cap // blk), dtype=np.float64)
     lib().oracle_selector_score_tokens(_p(q_sel), _p(w), _p(k_tok), _p(sc), f, n_seq,
                                        rows_per_seq, l_cap, blk, h_s, d_s, _p(sl), _p(out))
+    return out
+
+
+def selector_project(h, w_q, w_k, w_w, pos, h_s, d_s, rope_dim=64, rope_base=1.0e6):
+    """(q [rows, h_s, d_s], k [rows, h_s, d_s], w [rows, h_s]) in float64:
+    the selector projections of hidden states h [rows, d_model] with rotary
+    embedding at positions pos (Section 2.1, Appendix A)."""
+    h = _c(h, np.uint16)
+    rows, d_model = h.shape
+    w_q, w_k, w_w = _c(w_q, np.uint16), _c(w_k, np.uint16), _c(w_w, np.uint16)
+    pos = _c(pos, np.int32)
+    q = np.empty((rows, h_s, d_s))
+    k = np.empty((rows, h_s, d_s))
+    w = np.empty((rows, h_s))
+    lib().oracle_selector_project(_p(h), _p(w_q), _p(w_k), _p(w_w), _p(pos), rows, d_model,
+                                  h_s, d_s, rope_dim, float(rope_base), _p(q), _p(k), _p(w))
+    return q, k, w
+
+
+def selector_pool(k_tok, seq_len=None, blk=64):
+    """Pooled keys [n_seq, l_cap // blk, ...] in float64: the mean of each
+    block's existing tokens (0 where there are none)."""
+    k_tok = _c(k_tok, np.uint16)
+    n_seq, l_cap = k_tok.shape[:2]
+    width = k_tok.size // (n_seq * l_cap)
+    sl = None if seq_len is None else _c(seq_len, np.int32)
+    out = np.empty((n_seq, l_cap // blk) + k_tok.shape[2:])
+    lib().oracle_selector_pool(_p(k_tok), n_seq, l_cap, blk, width, _p(sl), _p(out))
     return out
 
 

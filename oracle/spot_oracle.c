@@ -10,6 +10,12 @@
  *                          score per query-block x key-block tile
  *   per-token selector ... Section 2.3: the block value is the maximum of
  *                          the per-token scores of the block's tokens
+ *   selector front end ... Section 2.1: per-head query / key projections of
+ *                          the hidden state and the weight map W_w, with
+ *                          rotary position embedding on part of each head
+ *                          (Appendix A: RoPE head dim 64 of 128); block
+ *                          pooling of the selector keys (mean of the block's
+ *                          tokens) for the pooled cache
  *   block selection ...... Section 2.3: Eq. select-topk (static top-K),
  *                          Eq. select-nucleus (softmax over the residual
  *                          blocks), Eq. select-topp (sink + recency + nucleus,
@@ -29,6 +35,11 @@
  * "reaches p" is an inclusive >=; ties in score rank the lower block id first;
  * p >= 1 keeps every residual block and p <= 0 none; k_max caps the total set
  * size (reserved blocks included) and is applied before the k_min floor.
+ * Front end: the rotary part is the first rope_dim dimensions of each head,
+ * rotated in pairs (i, i + rope_dim/2) by the angle pos * base^(-2i/rope_dim)
+ * (the rotate-half convention of the Qwen3 backbones); w = W_w h with no
+ * further scaling; a pooled key is the mean over the block's tokens that
+ * exist (t < seq_len).
  */
 #include "spot_oracle.h"
 
@@ -380,5 +391,72 @@ void oracle_sparse_prefill(const uint16_t *q, const uint16_t *k, const uint16_t 
         free(logit);
         free(tok);
         free(in_set);
+    }
+}
+
+/* ------------------------------------------------------------ front end */
+void oracle_selector_project(const uint16_t *h, const uint16_t *w_q, const uint16_t *w_k,
+                             const uint16_t *w_w, const int32_t *pos, int rows, int d_model,
+                             int h_s, int d_s, int rope_dim, double rope_base, double *q_out,
+                             double *k_out, double *w_out) {
+    int n_out = h_s * d_s;
+    int half = rope_dim / 2;
+#pragma omp parallel for schedule(dynamic) num_threads(oracle_get_threads())
+    for (int r = 0; r < rows; ++r) {
+        const uint16_t *hr = h + (int64_t)r * d_model;
+        double *qr = q_out + (int64_t)r * n_out, *kr = k_out + (int64_t)r * n_out;
+        /* the linear maps: out[j] = sum_i W[j, i] h[i] */
+        for (int j = 0; j < n_out; ++j) {
+            double aq = 0.0, ak = 0.0;
+            for (int i = 0; i < d_model; ++i) {
+                double x = bf16_to_double(hr[i]);
+                aq += bf16_to_double(w_q[(int64_t)j * d_model + i]) * x;
+                ak += bf16_to_double(w_k[(int64_t)j * d_model + i]) * x;
+            }
+            qr[j] = aq;
+            kr[j] = ak;
+        }
+        for (int hh = 0; hh < h_s; ++hh) {
+            double a = 0.0;
+            for (int i = 0; i < d_model; ++i)
+                a += bf16_to_double(w_w[(int64_t)hh * d_model + i]) * bf16_to_double(hr[i]);
+            w_out[(int64_t)r * h_s + hh] = a;
+        }
+        /* rotary position embedding on the first rope_dim dims of each head */
+        for (int hh = 0; hh < h_s; ++hh) {
+            for (int i = 0; i < half; ++i) {
+                double ang = (double)pos[r] * pow(rope_base, -2.0 * i / rope_dim);
+                double c = cos(ang), sn = sin(ang);
+                double *v[2] = {qr + hh * d_s, kr + hh * d_s};
+                for (int m = 0; m < 2; ++m) {
+                    double x1 = v[m][i], x2 = v[m][i + half];
+                    v[m][i] = x1 * c - x2 * sn;
+                    v[m][i + half] = x2 * c + x1 * sn;
+                }
+            }
+        }
+    }
+}
+
+void oracle_selector_pool(const uint16_t *k_tok, int n_seq, int l_cap, int blk, int width,
+                          const int32_t *seq_len, double *k_pool) {
+    int nblk = l_cap / blk;
+#pragma omp parallel for schedule(dynamic) num_threads(oracle_get_threads())
+    for (int task = 0; task < n_seq * nblk; ++task) {
+        int b = task / nblk, j = task % nblk;
+        int len = seq_len ? seq_len[b] : l_cap;
+        if (len > l_cap) len = l_cap;
+        int lo = j * blk, hi = (j + 1) * blk < len ? (j + 1) * blk : len;
+        double *o = k_pool + (int64_t)task * width;
+        for (int e = 0; e < width; ++e) {
+            if (hi <= lo) {
+                o[e] = 0.0;
+                continue;
+            }
+            double acc = 0.0;
+            for (int t = lo; t < hi; ++t)
+                acc += bf16_to_double(k_tok[((int64_t)b * l_cap + t) * width + e]);
+            o[e] = acc / (hi - lo);
+        }
     }
 }

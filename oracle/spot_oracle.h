@@ -86,6 +86,25 @@ void oracle_sparse_prefill(const uint16_t *q, const uint16_t *k, const uint16_t 
                            int h_q, int h_kv, int d, int blk, double sm_scale,
                            const int32_t *qrows, int n_q, double *out, double *lse);
 
+/* Selector front end for rows of hidden states (Section 2.1: per-head query
+ * and key projections q^I = W_q h, k^I = W_k h and the weight map w = W_w h;
+ * Appendix A: rotary position embedding on 64 of the 128 head dims).
+ * h [rows, d_model] bf16; w_q, w_k [h_s*d_s, d_model] and w_w [h_s, d_model]
+ * bf16 (output-major); pos [rows].  q_out, k_out [rows, h_s, d_s] and
+ * w_out [rows, h_s] in double, after the rotation of the pairs
+ * (i, i + rope_dim/2), i < rope_dim/2, of every head by pos * base^(-2i/rope_dim). */
+void oracle_selector_project(const uint16_t *h, const uint16_t *w_q, const uint16_t *w_k,
+                             const uint16_t *w_w, const int32_t *pos, int rows, int d_model,
+                             int h_s, int d_s, int rope_dim, double rope_base, double *q_out,
+                             double *k_out, double *w_out);
+
+/* Pooled selector keys: k_pool[b, j, :] = mean of k_tok[b, t, :] over the
+ * tokens t of block j (blk tokens each) with t < seq_len[b] (all l_cap if
+ * seq_len is NULL); 0 for a block with none.  k_tok [n_seq, l_cap, width]
+ * bf16, k_pool [n_seq, l_cap/blk, width] double. */
+void oracle_selector_pool(const uint16_t *k_tok, int n_seq, int l_cap, int blk, int width,
+                          const int32_t *seq_len, double *k_pool);
+
 #ifdef __cplusplus
 }
 #endif

@@ -174,6 +174,113 @@ def test_score_tokens_of_repeated_key_is_pooled_score():
                                   oracle.selector_score(q, w, kbar))
 
 
+# ------------------------------------------------------------ front end
+def _onehot_rows(idx, d_model, scale=1.0):
+    m = np.zeros((len(idx), d_model), np.float32)
+    m[np.arange(len(idx)), idx] = scale
+    return bf16_bits(m)
+
+
+def test_project_selects_hidden_dims_at_position_zero():
+    """Weights that copy chosen hidden dims give exactly those dims (no
+    rotation at position 0): pins the output-major weight layout and the
+    three maps apart."""
+    rng = np.random.default_rng(31)
+    rows, d_model, Hs, ds = 3, 96, 2, 16
+    h = bf16_bits(rng.standard_normal((rows, d_model)).astype(np.float32))
+    iq = rng.permutation(d_model)[:Hs * ds]
+    ik = rng.permutation(d_model)[:Hs * ds]
+    iw = rng.permutation(d_model)[:Hs]
+    q, k, w = oracle.selector_project(h, _onehot_rows(iq, d_model), _onehot_rows(ik, d_model, 2.0),
+                                      _onehot_rows(iw, d_model, -0.5), np.zeros(rows, np.int32),
+                                      Hs, ds, rope_dim=8, rope_base=1e4)
+    hv = bf16_value(h).astype(np.float64)
+    np.testing.assert_array_equal(q.reshape(rows, -1), hv[:, iq])
+    np.testing.assert_array_equal(k.reshape(rows, -1), 2.0 * hv[:, ik])
+    np.testing.assert_array_equal(w, -0.5 * hv[:, iw])
+
+
+def test_rope_quarter_and_half_turn():
+    """With base 4/pi^2 and 4 rotary dims the pair (1, 3) turns by pi/2 per
+    position: (x1, x3) -> (-x3, x1) at position 1 and -> (-x1, -x3) at 2.
+    The pair (0, 2) turns by 1 radian per position; its length is kept."""
+    rng = np.random.default_rng(37)
+    d_model, ds = 4, 4
+    h = bf16_bits(rng.standard_normal((3, d_model)).astype(np.float32))
+    eye = bf16_bits(np.eye(4, dtype=np.float32))
+    ww = bf16_bits(np.ones((1, d_model), np.float32))
+    base = 4.0 / math.pi ** 2
+    q, k, _ = oracle.selector_project(h, eye, eye, ww, np.array([0, 1, 2], np.int32), 1, ds,
+                                      rope_dim=4, rope_base=base)
+    x = bf16_value(h).astype(np.float64)
+    np.testing.assert_allclose(q[0, 0], x[0], rtol=0, atol=0)
+    np.testing.assert_allclose([q[1, 0, 1], q[1, 0, 3]], [-x[1, 3], x[1, 1]], atol=1e-15)
+    np.testing.assert_allclose([q[2, 0, 1], q[2, 0, 3]], [-x[2, 1], -x[2, 3]], atol=1e-15)
+    np.testing.assert_allclose(k, q, atol=0)
+    for r in range(3):
+        assert math.isclose(math.hypot(q[r, 0, 0], q[r, 0, 2]), math.hypot(x[r, 0], x[r, 2]),
+                            rel_tol=1e-14)
+    # pair (0, 2) at position 1 is a 1-radian turn: the angle between them
+    ang = math.atan2(q[1, 0, 2], q[1, 0, 0]) - math.atan2(x[1, 2], x[1, 0])
+    assert math.isclose(math.remainder(ang, 2 * math.pi), 1.0, rel_tol=1e-12)
+
+
+def test_rope_frequency_schedule():
+    """Pair i turns by base^(-2i/rope_dim) per position: with base 1e6 and
+    64 rotary dims the pair 16 turns by exactly 1e-3 and the pair 0 by 1."""
+    d_model, ds, r = 128, 128, 64
+    eye = bf16_bits(np.eye(128, dtype=np.float32))
+    h = np.zeros((1, d_model), np.float32)
+    h[0, 0] = 1.0
+    h[0, 16] = 1.0
+    hb = bf16_bits(h)
+    ww = bf16_bits(np.ones((1, d_model), np.float32))
+    q, _, _ = oracle.selector_project(hb, eye, eye, ww, np.array([1], np.int32), 1, ds,
+                                      rope_dim=r, rope_base=1.0e6)
+    assert math.isclose(math.atan2(q[0, 0, 32], q[0, 0, 0]), 1.0, rel_tol=1e-12)
+    assert math.isclose(math.atan2(q[0, 0, 48], q[0, 0, 16]), 1e-3, rel_tol=1e-9)
+
+
+def test_rope_scores_depend_on_relative_position():
+    """q(m) . k(n) over each head depends only on m - n, and the dims past
+    rope_dim do not move with the position."""
+    rng = np.random.default_rng(41)
+    d_model, Hs, ds = 64, 4, 128
+    h = bf16_bits(rng.standard_normal((2, d_model)).astype(np.float32))
+    wq = bf16_bits(rng.standard_normal((Hs * ds, d_model)).astype(np.float32) * 0.1)
+    wk = bf16_bits(rng.standard_normal((Hs * ds, d_model)).astype(np.float32) * 0.1)
+    ww = bf16_bits(rng.standard_normal((Hs, d_model)).astype(np.float32))
+
+    def dots(m, n):
+        q, _, _ = oracle.selector_project(h[:1], wq, wk, ww, np.array([m], np.int32), Hs, ds)
+        _, k, _ = oracle.selector_project(h[1:], wq, wk, ww, np.array([n], np.int32), Hs, ds)
+        return np.sum(q[0] * k[0], axis=-1)
+
+    np.testing.assert_allclose(dots(7, 3), dots(100007, 100003), rtol=1e-9)
+    np.testing.assert_allclose(dots(0, 0), dots(5000, 5000), rtol=1e-9)
+    assert not np.allclose(dots(7, 3), dots(3, 7), rtol=1e-6)
+    q0, k0, _ = oracle.selector_project(h, wq, wk, ww, np.array([0, 0], np.int32), Hs, ds)
+    q1, k1, _ = oracle.selector_project(h, wq, wk, ww, np.array([9999, 123], np.int32), Hs, ds)
+    np.testing.assert_array_equal(q0[..., 64:], q1[..., 64:])
+    np.testing.assert_array_equal(k0[..., 64:], k1[..., 64:])
+
+
+def test_pool_is_block_mean_of_existing_tokens():
+    rng = np.random.default_rng(43)
+    n_seq, L, width, blk = 3, 320, 16, 64
+    k = bf16_bits(rng.standard_normal((n_seq, L, width)).astype(np.float32))
+    seq_len = np.array([320, 130, 0], np.int32)
+    pooled = oracle.selector_pool(k, seq_len, blk)
+    kv = bf16_value(k).astype(np.float64)
+    for b in range(n_seq):
+        for j in range(L // blk):
+            lo, hi = j * blk, min((j + 1) * blk, int(seq_len[b]))
+            want = kv[b, lo:hi].mean(axis=0) if hi > lo else np.zeros(width)
+            np.testing.assert_allclose(pooled[b, j], want, rtol=1e-15, atol=1e-15)
+    same = np.repeat(k[:, :1], L, axis=1)
+    np.testing.assert_allclose(oracle.selector_pool(same)[:, 2], kv[:, 0], rtol=1e-15)
+
+
 # -------------------------------------------------------------- selection
 def _sel(scores, rule, n_valid=None):
     s = np.asarray(scores, dtype=np.float64)[None]
