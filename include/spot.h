@@ -10,7 +10,9 @@
  * as the block-sparse causal prefill over query blocks.
  * spot_selector_score_tokens replaces the first call when the selector cache
  * holds one key per token (block value = maximum of per-token scores,
- * Section 2.3).
+ * Section 2.3).  Before them, spot_selector_project produces the step's
+ * selector query, weights and new cache key from the hidden state, and
+ * spot_selector_pool refreshes the pooled key of the block it landed in.
  *
  * Conventions shared by every entry point:
  *  - Pointers named as device arrays are caller-owned device memory; the
@@ -61,6 +63,72 @@ const char *spot_status_str(spot_status s);
 
 /* Library version string (static storage). */
 const char *spot_version(void);
+
+/*
+ * spot_selector_project -- the selector's query, key and weight projections.
+ *
+ * Section 2.1: the selector projects the hidden state h of a token into
+ * per-head query and key vectors q^I = W_q h, k^I = W_k h (h_s heads of d_s
+ * dims) and per-head mixing weights w = W_w h.  Appendix A: rotary position
+ * embedding covers rope_dim (64) of the head dims; here the first rope_dim
+ * dims of every head, rotated in pairs (i, i + rope_dim/2) by the angle
+ * pos * rope_base^(-2i / rope_dim) (the rotate-half convention), after the
+ * projection and before rounding.  For each row r:
+ *     q_out[r]  = RoPE(W_q h[r], pos[r])               (BF16, round to nearest even)
+ *     w_out[r]  = W_w h[r]                             (FP32)
+ *     k_cache[r / rows_per_seq, pos[r]] = RoPE(W_k h[r], pos[r])  (BF16), the
+ *     append to the per-token selector cache; a row with pos outside
+ *     [0, l_cap) stores no key.
+ * Decode passes one row per sequence (rows_per_seq = 1, pos = the new
+ * token's position); prefill may pass every token of a sequence
+ * (rows_per_seq = L, pos = 0 .. L-1).
+ *
+ *  h        device BF16 [rows, d_model], 16-byte aligned, d_model % 8 == 0
+ *  w_q, w_k device BF16 [h_s*d_s, d_model] (output-major, as a linear layer
+ *           stores its weight), 16-byte aligned
+ *  w_w      device BF16 [h_s, d_model], 16-byte aligned
+ *  pos      device int32 [rows]
+ *  q_out    device BF16 [rows, h_s, d_s] (output)
+ *  w_out    device float [rows, h_s] (output)
+ *  k_cache  device BF16 [rows/rows_per_seq, l_cap, h_s, d_s] (the rows at pos
+ *           are written)
+ *
+ * Supported: h_s * d_s == 512 with d_s in {64, 128}; rope_dim even, 0 <=
+ * rope_dim <= d_s; rope_base > 0.  The arithmetic is FP32 (products of
+ * BF16, fixed summation order) with the rotation angle in FP64.  Errors:
+ * SPOT_ERR_NULL, SPOT_ERR_SHAPE (sizes, rows % rows_per_seq, alignment),
+ * SPOT_ERR_UNSUPPORTED (head shape, rope_dim, rope_base).
+ */
+spot_status spot_selector_project(const void *h, const void *w_q, const void *w_k,
+                                  const void *w_w, const int32_t *pos, int rows, int d_model,
+                                  int h_s, int d_s, int rope_dim, float rope_base, void *q_out,
+                                  float *w_out, void *k_cache, int rows_per_seq, int l_cap,
+                                  void *stream);
+
+/*
+ * spot_selector_pool -- block-pooled selector keys from the per-token cache.
+ *
+ * The pooled cache (one key per 64-token block, the key side of the
+ * query-block x key-block tiles of Section 2.1) holds the mean of the block's
+ * token keys: for each sequence b and block j = first_block[b] + y,
+ * y = 0 .. max_blocks-1,
+ *     k_pool[b, j] = BF16( (sum over t in block j, t < seq_len[b], in token
+ *                           order, of k_tok[b, t], in FP32) / count )
+ * Blocks with no token below seq_len, or outside [0, l_cap/64), are left
+ * untouched.  Decode re-pools only the block the new token fell in
+ * (first_block = (seq_len - 1) / 64, max_blocks = 1); prefill pools all
+ * (first_block NULL = 0, max_blocks = l_cap / 64).
+ *
+ *  k_tok        device BF16 [n_seq, l_cap, h_s, d_s], 16-byte aligned
+ *  k_pool       device BF16 [n_seq, l_cap/64, h_s, d_s] (output), 16-byte aligned
+ *  seq_len      device int32 [n_seq] or NULL (all l_cap tokens exist)
+ *  first_block  device int32 [n_seq] or NULL (0)
+ *
+ * Supported: h_s * d_s == 512, max_blocks <= 65535.
+ */
+spot_status spot_selector_pool(const void *k_tok, void *k_pool, int n_seq, int l_cap, int h_s,
+                               int d_s, const int32_t *seq_len, const int32_t *first_block,
+                               int max_blocks, void *stream);
 
 /*
  * spot_selector_score -- block scores of the learned selector.

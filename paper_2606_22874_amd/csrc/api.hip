@@ -35,6 +35,43 @@ const char* spot_status_str(spot_status s) {
 
 const char* spot_version(void) { return SPOT_VERSION_STR; }
 
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+spot_status spot_selector_project(const void* h, const void* w_q, const void* w_k,
+                                  const void* w_w, const int32_t* pos, int rows, int d_model,
+                                  int h_s, int d_s, int rope_dim, float rope_base, void* q_out,
+                                  float* w_out, void* k_cache, int rows_per_seq, int l_cap,
+                                  void* stream) {
+  if (!h || !w_q || !w_k || !w_w || !pos || !q_out || !w_out || !k_cache) return SPOT_ERR_NULL;
+  if (rows < 0 || d_model < 8 || d_model % 8 || h_s < 1 || d_s < 1 || rows_per_seq < 1 ||
+      rows % rows_per_seq || l_cap < 0)
+    return SPOT_ERR_SHAPE;
+  if (!aligned16(h) || !aligned16(w_q) || !aligned16(w_k) || !aligned16(w_w))
+    return SPOT_ERR_SHAPE;
+  if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
+  if (rope_dim < 0 || rope_dim > d_s || rope_dim % 2 || !(rope_base > 0.f) ||
+      rope_base > 3.0e38f)
+    return SPOT_ERR_UNSUPPORTED;
+  if (rows == 0) return SPOT_OK;
+  return from_hip(launch_selector_project(h, w_q, w_k, w_w, pos, rows, d_model, h_s, d_s,
+                                          rope_dim, rope_base, q_out, w_out, k_cache,
+                                          rows_per_seq, l_cap, static_cast<hipStream_t>(stream)));
+}
+
+spot_status spot_selector_pool(const void* k_tok, void* k_pool, int n_seq, int l_cap, int h_s,
+                               int d_s, const int32_t* seq_len, const int32_t* first_block,
+                               int max_blocks, void* stream) {
+  if (!k_tok || !k_pool) return SPOT_ERR_NULL;
+  if (n_seq < 0 || l_cap < 0 || l_cap % kBlk || max_blocks < 0 || h_s < 1 || d_s < 1)
+    return SPOT_ERR_SHAPE;
+  if (!aligned16(k_tok) || !aligned16(k_pool)) return SPOT_ERR_SHAPE;
+  if (h_s * d_s != 512) return SPOT_ERR_UNSUPPORTED;
+  if (max_blocks > 65535) return SPOT_ERR_UNSUPPORTED;
+  if (n_seq == 0 || l_cap == 0 || max_blocks == 0) return SPOT_OK;
+  return from_hip(launch_selector_pool(k_tok, k_pool, n_seq, l_cap, seq_len, first_block,
+                                       max_blocks, static_cast<hipStream_t>(stream)));
+}
+
 spot_status spot_selector_score(const void* q_sel, const float* w, const void* k_sel,
                                 const void* k_scale, int kfmt, int n_seq, int rows_per_seq,
                                 int nblk, int h_s, int d_s, const int32_t* n_valid,

@@ -136,6 +136,15 @@ hipError_t launch_selector_score_tokens(const void* q_sel, const float* w, const
                                         int rows_per_seq, int l_cap, int d_s,
                                         const int32_t* seq_len, float* scores, hipStream_t s);
 
+hipError_t launch_selector_project(const void* h, const void* w_q, const void* w_k,
+                                   const void* w_w, const int32_t* pos, int rows, int d_model,
+                                   int h_s, int d_s, int rope_dim, float rope_base, void* q_out,
+                                   float* w_out, void* k_cache, int rows_per_seq, int l_cap,
+                                   hipStream_t s);
+hipError_t launch_selector_pool(const void* k_tok, void* k_pool, int n_seq, int l_cap,
+                                const int32_t* seq_len, const int32_t* first_block,
+                                int max_blocks, hipStream_t s);
+
 hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const int32_t* n_valid,
                                 float top_p, int k_max, int k_min, int n_sink, int n_recent,
                                 int32_t* idx, int32_t* count, float* nuc_mass, hipStream_t s);

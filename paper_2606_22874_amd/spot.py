@@ -28,7 +28,8 @@ KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2}
 BLK = 64
 
 SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score",
-           "spot_selector_score_tokens", "spot_select_blocks",
+           "spot_selector_score_tokens", "spot_selector_project", "spot_selector_pool",
+           "spot_select_blocks",
            "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
            "spot_sparse_prefill", "spot_decode_step_workspace_bytes", "spot_decode_step",
            "spot_probe_stream_read", "spot_probe_sink_words"]
@@ -63,6 +64,8 @@ def load(path: Optional[str] = None):
         L.spot_version.restype = ctypes.c_char_p
         L.spot_selector_score.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P, P]
         L.spot_selector_score_tokens.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P, P]
+        L.spot_selector_project.argtypes = [P, P, P, P, P, I, I, I, I, I, F, P, P, P, I, I, P]
+        L.spot_selector_pool.argtypes = [P, P, I, I, I, I, P, P, I, P]
         L.spot_select_blocks.argtypes = [P, I, I, P, F, I, I, I, I, P, P, P, P]
         L.spot_decode_workspace_bytes.argtypes = [I, I, I, I, I]
         L.spot_decode_workspace_bytes.restype = Z
@@ -76,7 +79,8 @@ def load(path: Optional[str] = None):
         L.spot_probe_stream_read.argtypes = [P, Z, P, P]
         L.spot_probe_stream_read.restype = ctypes.c_int32
         L.spot_probe_sink_words.restype = I
-        for name in ("spot_selector_score", "spot_selector_score_tokens", "spot_select_blocks", "spot_sparse_decode",
+        for name in ("spot_selector_score", "spot_selector_score_tokens", "spot_selector_project",
+                     "spot_selector_pool", "spot_select_blocks", "spot_sparse_decode",
                      "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step"):
             getattr(L, name).restype = ctypes.c_int32
         if path is None:
@@ -163,6 +167,38 @@ def spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_s
     _check("spot_selector_score_tokens", load().spot_selector_score_tokens(
         _ptr(q_sel), _ptr(w), _ptr(k_tok), _ptr(k_scale), f, n_seq, rows_per_seq, l_cap, h_s,
         d_s, _ptr(seq_len), _ptr(scores), _stream(stream)))
+
+
+def spot_selector_project(h, w_q, w_k, w_w, pos, rows, d_model, h_s, d_s, rope_dim, rope_base,
+                          q_out, w_out, k_cache, rows_per_seq, l_cap, stream=None):
+    n_out = h_s * d_s
+    _dev(h, "h", BF16, rows * d_model)
+    _dev(w_q, "w_q", BF16, n_out * d_model)
+    _dev(w_k, "w_k", BF16, n_out * d_model)
+    _dev(w_w, "w_w", BF16, h_s * d_model)
+    _dev(pos, "pos", I32, rows)
+    _dev(q_out, "q_out", BF16, rows * n_out)
+    _dev(w_out, "w_out", F32, rows * h_s)
+    _dev(k_cache, "k_cache", BF16, (rows // max(rows_per_seq, 1)) * l_cap * n_out)
+    _check("spot_selector_project", load().spot_selector_project(
+        _ptr(h), _ptr(w_q), _ptr(w_k), _ptr(w_w), _ptr(pos), rows, d_model, h_s, d_s, rope_dim,
+        rope_base, _ptr(q_out), _ptr(w_out), _ptr(k_cache), rows_per_seq, l_cap,
+        _stream(stream)))
+
+
+def spot_selector_pool(k_tok, k_pool, n_seq, l_cap, h_s, d_s, seq_len=None, first_block=None,
+                       max_blocks=None, stream=None):
+    _dev(k_tok, "k_tok", BF16, n_seq * l_cap * h_s * d_s)
+    _dev(k_pool, "k_pool", BF16, n_seq * (l_cap // 64) * h_s * d_s)
+    if seq_len is not None:
+        _dev(seq_len, "seq_len", I32, n_seq)
+    if first_block is not None:
+        _dev(first_block, "first_block", I32, n_seq)
+    if max_blocks is None:
+        max_blocks = l_cap // 64
+    _check("spot_selector_pool", load().spot_selector_pool(
+        _ptr(k_tok), _ptr(k_pool), n_seq, l_cap, h_s, d_s, _ptr(seq_len), _ptr(first_block),
+        max_blocks, _stream(stream)))
 
 
 def spot_select_blocks(scores, rows, nblk, n_valid, top_p, k_max, k_min, n_sink, n_recent, idx,

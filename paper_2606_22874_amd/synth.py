@@ -263,6 +263,21 @@ def selector_tokens(seed, B, L, Hs, ds, seq_len, rule=None, zipf_a=1.1, t0=16.0,
     return q_sel, w, k_tok
 
 
+def selector_frontend(seed, rows, d_model, Hs, ds):
+    """Hidden states and synthetic selector weights for the front end:
+    h [rows, d_model] ~ N(0, 1); W_q, W_k [Hs*ds, d_model] and W_w
+    [Hs, d_model] ~ N(0, 1/d_model) (so projections are of order 1); all BF16
+    bits.  Trained weights are not available; only the shapes matter to the
+    kernels."""
+    rng = np.random.default_rng([seed, 57])
+    sd = 1.0 / math.sqrt(d_model)
+    h = bf16_bits(rng.standard_normal((rows, d_model), dtype=np.float32))
+    wq = bf16_bits(rng.standard_normal((Hs * ds, d_model), dtype=np.float32) * np.float32(sd))
+    wk = bf16_bits(rng.standard_normal((Hs * ds, d_model), dtype=np.float32) * np.float32(sd))
+    ww = bf16_bits(rng.standard_normal((Hs, d_model), dtype=np.float32) * np.float32(sd))
+    return h, wq, wk, ww
+
+
 def selector_zipf(rng, B, nblk, Hs, ds, n_valid, rule: Rule, n_spikes=0,
                   zipf_a=1.1, t0=16.0, noise=0.06):
     """Pooled selector keys with a Zipf(zipf_a) relevance profile over blocks.

@@ -75,6 +75,34 @@ def test_validation_errors_before_launch(lib):
     assert tok(nz, nz, nz, None, 0, 1, 1, 4096, 16, 32, None, nz, None) == 3
     assert tok(nz, nz, nz, None, 5, 1, 1, 4096, 8, 64, None, nz, None) == 3
     assert tok(nz, nz, nz, None, 0, 0, 1, 4096, 8, 64, None, nz, None) == 0   # nothing to do
+    # front end: (h, w_q, w_k, w_w, pos, rows, d_model, h_s, d_s, rope_dim, rope_base, q_out,
+    # w_out, k_cache, rows_per_seq, l_cap, stream)
+    proj = lib.spot_selector_project
+
+    def pcall(**kw):
+        a = dict(h=nz, w_q=nz, w_k=nz, w_w=nz, pos=nz, rows=4, d_model=4096, h_s=4, d_s=128,
+                 rope_dim=64, rope_base=1e6, q_out=nz, w_out=nz, k_cache=nz, rows_per_seq=1,
+                 l_cap=4096, stream=None)
+        a.update(kw)
+        return proj(*a.values())
+
+    assert pcall(pos=None) == 1
+    assert pcall(k_cache=None) == 1
+    assert pcall(d_model=4100) == 2                 # not a multiple of 8
+    assert pcall(rows=5, rows_per_seq=2) == 2
+    assert pcall(h=P(24)) == 2                      # not 16-byte aligned
+    assert pcall(d_s=64) == 3                       # 4 x 64 != 512
+    assert pcall(rope_dim=130) == 3
+    assert pcall(rope_dim=63) == 3
+    assert pcall(rope_base=0.0) == 3
+    assert pcall(rope_base=float("nan")) == 3
+    assert pcall(rows=0) == 0
+    pool = lib.spot_selector_pool
+    assert pool(None, nz, 1, 4096, 4, 128, None, None, 1, None) == 1
+    assert pool(nz, nz, 1, 4000, 4, 128, None, None, 1, None) == 2
+    assert pool(nz, nz, 1, 4096, 4, 64, None, None, 1, None) == 3
+    assert pool(nz, nz, 1, 4096, 4, 128, None, None, 70000, None) == 3
+    assert pool(nz, nz, 1, 4096, 4, 128, None, None, 0, None) == 0
     # rules: NaN p, k_min > k_max, k_max < n_sink + n_recent, k_max < 1
     sel = lib.spot_select_blocks
     assert sel(nz, 1, 8, None, float("nan"), 4, 0, 1, 2, nz, nz, None, None) == 4

@@ -1,0 +1,188 @@
+"""Parity of the selector front end (projections with rotary embedding and
+the cache append; block pooling) with the FP64 oracle (needs an MI355X).
+
+Tolerances: a projected value g (FP32 products of BF16, rounded to BF16)
+against the oracle o: |g - o| <= 2^-8 |o| + 1e-5 S, with S the sum of
+|W_ji h_i| over the terms that make it up (the FP32 summation bound for
+4096-term dots, with margin); the weights w_out (FP32) to 1e-5 S.  Pooled
+keys: within one BF16 step (2^-8 relative) of the FP64 block mean, and
+bitwise equal to an FP32 token-order mean.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_22874_amd import spot, synth
+from paper_2606_22874_amd.synth import bf16_bits, bf16_value
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+DEV = "cuda:0"
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def bf(a):
+    return spot.to_device_bf16(a, DEV)
+
+
+def host_bf16(t):
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def abs_sums(h, w):
+    """S[r, j] = sum_i |W[j, i] h[r, i]|."""
+    return np.abs(bf16_value(h).astype(np.float64)) @ np.abs(bf16_value(w).astype(np.float64)).T
+
+
+def rot_sums(S, Hs, ds, rope_dim):
+    """Bound terms after the rotation: a rotated value mixes its pair."""
+    S = S.reshape(S.shape[0], Hs, ds).copy()
+    half = rope_dim // 2
+    both = S[..., :half] + S[..., half:rope_dim]
+    S[..., :half] = both
+    S[..., half:rope_dim] = both
+    return S
+
+
+def run_project(rows, d_model, Hs, ds, rope_dim, base, pos, rows_per_seq, l_cap, seed=1):
+    h, wq, wk, ww = synth.selector_frontend(seed, rows, d_model, Hs, ds)
+    n_seq = rows // rows_per_seq
+    q_out = torch.empty((rows, Hs, ds), dtype=torch.bfloat16, device=DEV)
+    w_out = torch.empty((rows, Hs), dtype=torch.float32, device=DEV)
+    cache = torch.zeros((n_seq, l_cap, Hs, ds), dtype=torch.bfloat16, device=DEV)
+    spot.spot_selector_project(bf(h), bf(wq), bf(wk), bf(ww), dev(np.asarray(pos, np.int32)),
+                               rows, d_model, Hs, ds, rope_dim, base, q_out, w_out, cache,
+                               rows_per_seq, l_cap)
+    torch.cuda.synchronize()
+    q_o, k_o, w_o = oracle.selector_project(h, wq, wk, ww, np.asarray(pos, np.int32), Hs, ds,
+                                            rope_dim=rope_dim, rope_base=base)
+    return (h, wq, wk, ww), (q_out, w_out, cache), (q_o, k_o, w_o)
+
+
+def check_bf16(g_bits, o, S):
+    g = bf16_value(g_bits).astype(np.float64)
+    err = np.abs(g - o)
+    bound = 2.0 ** -8 * np.abs(o) + 1e-5 * S
+    assert np.all(err <= bound), f"max excess {np.max(err - bound)}"
+
+
+CASES = [
+    # rows, d_model, Hs, ds, rope_dim, base, rows_per_seq, l_cap
+    (4, 4096, 4, 128, 64, 1.0e6, 1, 131072),     # decode, Qwen3-8B hidden size
+    (4, 4096, 8, 64, 32, 1.0e6, 1, 8192),
+    (3, 5120, 4, 128, 64, 1.0e6, 1, 4096),       # Qwen3-32B hidden size: two chunk passes
+    (20, 2560, 4, 128, 64, 1.0e4, 20, 64),       # prefill rows, two row passes
+    (6, 1000, 8, 64, 64, 500.0, 3, 128),         # d_model not a multiple of 512, all dims rotated
+    (2, 512, 4, 128, 0, 1.0e6, 1, 64),           # no rotary dims
+]
+
+
+@pytest.mark.parametrize("rows,d_model,Hs,ds,rope_dim,base,rps,l_cap", CASES)
+def test_project_parity(rows, d_model, Hs, ds, rope_dim, base, rps, l_cap):
+    print(f"[frontend] project rows={rows} d_model={d_model} {Hs}x{ds} rope {rope_dim}",
+          flush=True)
+    rng = np.random.default_rng(rows * d_model)
+    if rps == 1:
+        pos = rng.integers(0, l_cap, rows)
+        pos[0] = l_cap - 1
+    else:
+        pos = np.tile(np.arange(rps), rows // rps)
+    (h, wq, wk, ww), (q_out, w_out, cache), (q_o, k_o, w_o) = run_project(
+        rows, d_model, Hs, ds, rope_dim, base, pos, rps, l_cap)
+    Sq = rot_sums(abs_sums(h, wq), Hs, ds, rope_dim)
+    Sk = rot_sums(abs_sums(h, wk), Hs, ds, rope_dim)
+    check_bf16(host_bf16(q_out), q_o, Sq)
+    cache_h = host_bf16(cache)
+    k_g = np.stack([cache_h[r // rps, pos[r]] for r in range(rows)])
+    check_bf16(k_g, k_o, Sk)
+    Sw = abs_sums(h, ww)
+    assert np.all(np.abs(w_out.cpu().numpy() - w_o) <= 1e-5 * Sw)
+    # nothing else of the cache was written
+    mask = np.ones(cache_h.shape[:2], bool)
+    for r in range(rows):
+        mask[r // rps, pos[r]] = False
+    assert np.all(cache_h[mask] == 0)
+
+
+def test_project_skips_keys_outside_the_cache():
+    rows, l_cap = 4, 128
+    pos = np.array([5, -1, 128, 127], np.int32)
+    (h, wq, wk, ww), (q_out, w_out, cache), (q_o, k_o, w_o) = run_project(
+        rows, 1024, 4, 128, 64, 1.0e6, pos, 1, l_cap)
+    cache_h = host_bf16(cache)
+    assert np.all(cache_h[1] == 0) and np.all(cache_h[2] == 0)
+    assert np.any(cache_h[0, 5] != 0) and np.any(cache_h[3, 127] != 0)
+    # the queries are still produced at the given (even out-of-range) positions
+    check_bf16(host_bf16(q_out), q_o, rot_sums(abs_sums(h, wq), 4, 128, 64))
+
+
+def fp32_token_mean(k_tok, b, lo, hi):
+    acc = np.zeros(k_tok.shape[2:], np.float32)
+    for t in range(lo, hi):
+        acc += bf16_value(k_tok[b, t])
+    return bf16_bits(acc / np.float32(hi - lo))
+
+
+@pytest.mark.parametrize("n_seq,L,Hs,ds", [(3, 1024, 4, 128), (2, 4096, 8, 64)])
+def test_pool_parity(n_seq, L, Hs, ds):
+    rng = np.random.default_rng(L + n_seq)
+    k_tok = bf16_bits(rng.standard_normal((n_seq, L, Hs, ds), dtype=np.float32))
+    seq_len = np.array([L, L - 100, 1][:n_seq], np.int32)
+    pooled = torch.zeros((n_seq, L // 64, Hs, ds), dtype=torch.bfloat16, device=DEV)
+    spot.spot_selector_pool(bf(k_tok), pooled, n_seq, L, Hs, ds, dev(seq_len))
+    torch.cuda.synchronize()
+    g = host_bf16(pooled)
+    o = oracle.selector_pool(k_tok, seq_len)
+    gv = bf16_value(g).astype(np.float64)
+    nv = (seq_len + 63) // 64
+    for b in range(n_seq):
+        assert np.all(np.abs(gv[b, :nv[b]] - o[b, :nv[b]]) <= 2.0 ** -8 * np.abs(o[b, :nv[b]]))
+        assert np.all(g[b, nv[b]:] == 0)                      # blocks without tokens untouched
+        for j in (0, nv[b] - 1):
+            lo, hi = j * 64, min(j * 64 + 64, int(seq_len[b]))
+            np.testing.assert_array_equal(g[b, j], fp32_token_mean(k_tok, b, lo, hi))
+
+
+def test_decode_front_end_step():
+    """One decode step's front end: project the new token (append its key),
+    re-pool only its block, then score; against the oracle run on the same
+    cache contents."""
+    B, L, Hs, ds, d_model = 4, 8192, 8, 64, 4096
+    rng = np.random.default_rng(99)
+    k_tok = bf16_bits(rng.standard_normal((B, L, Hs, ds), dtype=np.float32))
+    seq_len = np.array([8192, 5000, 65, 64], np.int32)
+    pos = seq_len - 1
+    h, wq, wk, ww = synth.selector_frontend(7, B, d_model, Hs, ds)
+    cache = bf(k_tok)
+    pooled = torch.zeros((B, L // 64, Hs, ds), dtype=torch.bfloat16, device=DEV)
+    spot.spot_selector_pool(cache, pooled, B, L, Hs, ds, dev(seq_len))      # the prefill pooling
+    q_out = torch.empty((B, Hs, ds), dtype=torch.bfloat16, device=DEV)
+    w_out = torch.empty((B, Hs), dtype=torch.float32, device=DEV)
+    spot.spot_selector_project(bf(h), bf(wq), bf(wk), bf(ww), dev(pos), B, d_model, Hs, ds, 32,
+                               1.0e6, q_out, w_out, cache, 1, L)
+    spot.spot_selector_pool(cache, pooled, B, L, Hs, ds, dev(seq_len), dev(pos // 64), 1)
+    nv = (seq_len + 63) // 64
+    scores = spot.selector_score(q_out, w_out, pooled, n_valid=dev(nv), nblk=L // 64)
+    torch.cuda.synchronize()
+    cache_h = host_bf16(cache)
+    # the appended keys are the GPU's; everything downstream is checked on them
+    q_o, k_o, w_o = oracle.selector_project(h, wq, wk, ww, pos, Hs, ds, rope_dim=32,
+                                            rope_base=1.0e6)
+    check_bf16(np.stack([cache_h[b, pos[b]] for b in range(B)]), k_o,
+               rot_sums(abs_sums(h, wk), Hs, ds, 32))
+    pooled_o = oracle.selector_pool(cache_h, seq_len)
+    pv = bf16_value(host_bf16(pooled)).astype(np.float64)
+    for b in range(B):
+        assert np.all(np.abs(pv[b, :nv[b]] - pooled_o[b, :nv[b]]) <=
+                      2.0 ** -8 * np.abs(pooled_o[b, :nv[b]]))
+    s_o = oracle.selector_score(host_bf16(q_out), w_out.cpu().numpy(), host_bf16(pooled),
+                                n_valid=nv)
+    s_g = scores.cpu().numpy()
+    fin = np.isfinite(s_o)
+    assert np.array_equal(np.isfinite(s_g), fin)
+    assert np.all(np.abs(s_g[fin] - s_o[fin]) <= 1e-4 * np.abs(s_o[fin]) + 1e-6)
