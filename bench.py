@@ -334,6 +334,9 @@ def main():
                                                      mass, out, lse, ws, stream)
 
     if not args.no_extra:
+        result["selector_front_end"] = front_end_leg(args, torch, spot, synth, dev, timed, wl)
+
+    if not args.no_extra:
         del copies, bufs
         torch.cuda.empty_cache()
         result["config"]["smaller_workloads"] = small_decode_legs(args, torch, spot, synth, dev,
@@ -385,6 +388,75 @@ def static_topk_leg(args, torch, spot, dev, timed, wl, copies, q, q_sel, w, seq_
         del ws_k
     return {"workload": f"decode L={L} B={B}, static top-K (p >= 1, no reserved blocks)",
             "budgets": res}
+
+
+def front_end_leg(args, torch, spot, synth, dev, timed, wl):
+    """The selector front end of one decode step for the 4 sequences:
+    projections of the new token's hidden state (Qwen3-8B width 4096, 4 x 128
+    selector heads, rotary on 64 dims) with the key appended to the per-token
+    cache, then the pooled key of the block it landed in re-computed."""
+    B, L, Hs, ds, d_model = wl.B, wl.L, 4, 128, 4096
+    h, wq, wk, ww = synth.selector_frontend(SEED_TOKENS, B, d_model, Hs, ds)
+
+    def bf(a):
+        return spot.to_device_bf16(a, dev)
+
+    hd, wqd, wkd, wwd = bf(h), bf(wq), bf(wk), bf(ww)
+    pos = torch.from_numpy(wl.seq_len - 1).to(dev)
+    first = torch.from_numpy((wl.seq_len - 1) // 64).to(dev)
+    seq_len = torch.from_numpy(wl.seq_len).to(dev)
+    q_out = torch.empty((B, Hs, ds), dtype=torch.bfloat16, device=dev)
+    w_out = torch.empty((B, Hs), dtype=torch.float32, device=dev)
+    cache = torch.zeros((B, L, Hs, ds), dtype=torch.bfloat16, device=dev)
+    pooled = torch.zeros((B, L // 64, Hs, ds), dtype=torch.bfloat16, device=dev)
+    def project(st):
+        spot.spot_selector_project(hd, wqd, wkd, wwd, pos, B, d_model, Hs, ds, 64, 1.0e6, q_out,
+                                   w_out, cache, 1, L, st)
+
+    def pool(st):
+        spot.spot_selector_pool(cache, pooled, B, L, Hs, ds, seq_len, first, 1, st)
+
+    def both(st):
+        project(st)
+        pool(st)
+
+    # These launches last a few microseconds, less than the binding's host
+    # overhead per call, so they are timed as HIP graphs of 50 back-to-back
+    # launches (no host work between kernels), replayed.
+    def graph_ms(fn, n=50, reps=5):
+        for _ in range(3):
+            fn(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            st = torch.cuda.current_stream()
+            for _ in range(n):
+                fn(st)
+        g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / (n * reps)
+
+    pms = graph_ms(project)
+    qms = graph_ms(pool)
+    ms = graph_ms(both)
+    wbytes = wq.nbytes + wk.nbytes + ww.nbytes
+    log(f"[bench] selector front end: project {pms * 1e3:.1f} us, pool {qms * 1e3:.1f} us")
+    del cache, pooled
+    return {
+        "workload": f"decode B={B}: hidden {d_model} -> selector {Hs}x{ds} (RoPE 64 dims), "
+                    "key appended to the per-token cache, its block re-pooled",
+        "us_per_step": round(ms * 1e3, 2),
+        "project_us": round(pms * 1e3, 2),
+        "pool_us": round(qms * 1e3, 2),
+        "project_weight_bytes": int(wbytes),
+        "project_weight_gbs": round(wbytes / (pms * 1e-3) / 1e9, 1),
+    }
 
 
 def per_token_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, n_valid, idx,

@@ -112,8 +112,10 @@ spot_status spot_selector_project(const void *h, const void *w_q, const void *w_
  * query-block x key-block tiles of Section 2.1) holds the mean of the block's
  * token keys: for each sequence b and block j = first_block[b] + y,
  * y = 0 .. max_blocks-1,
- *     k_pool[b, j] = BF16( (sum over t in block j, t < seq_len[b], in token
- *                           order, of k_tok[b, t], in FP32) / count )
+ *     k_pool[b, j] = BF16( (sum over t in block j, t < seq_len[b], of
+ *                           k_tok[b, t], in FP32) / count )
+ * where the FP32 sum runs in token order within each 16-token quarter of the
+ * block and the four quarter sums are added in order (deterministic).
  * Blocks with no token below seq_len, or outside [0, l_cap/64), are left
  * untouched.  Decode re-pools only the block the new token fell in
  * (first_block = (seq_len - 1) / 64, max_blocks = 1); prefill pools all

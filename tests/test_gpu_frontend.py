@@ -6,7 +6,7 @@ against the oracle o: |g - o| <= 2^-8 |o| + 1e-5 S, with S the sum of
 |W_ji h_i| over the terms that make it up (the FP32 summation bound for
 4096-term dots, with margin); the weights w_out (FP32) to 1e-5 S.  Pooled
 keys: within one BF16 step (2^-8 relative) of the FP64 block mean, and
-bitwise equal to an FP32 token-order mean.
+bitwise equal to the documented FP32 summation order.
 """
 import numpy as np
 import pytest
@@ -121,11 +121,17 @@ def test_project_skips_keys_outside_the_cache():
     check_bf16(host_bf16(q_out), q_o, rot_sums(abs_sums(h, wq), 4, 128, 64))
 
 
-def fp32_token_mean(k_tok, b, lo, hi):
-    acc = np.zeros(k_tok.shape[2:], np.float32)
-    for t in range(lo, hi):
-        acc += bf16_value(k_tok[b, t])
-    return bf16_bits(acc / np.float32(hi - lo))
+def fp32_quarter_mean(k_tok, b, lo, hi):
+    """The documented FP32 order: token-order sums over the block's 16-token
+    quarters, the quarters added in order, one division."""
+    parts = []
+    for q in range(4):
+        acc = np.zeros(k_tok.shape[2:], np.float32)
+        for t in range(lo + 16 * q, min(lo + 16 * q + 16, hi)):
+            acc += bf16_value(k_tok[b, t])
+        parts.append(acc)
+    tot = ((parts[0] + parts[1]) + parts[2]) + parts[3]
+    return bf16_bits(tot / np.float32(hi - lo))
 
 
 @pytest.mark.parametrize("n_seq,L,Hs,ds", [(3, 1024, 4, 128), (2, 4096, 8, 64)])
@@ -145,7 +151,7 @@ def test_pool_parity(n_seq, L, Hs, ds):
         assert np.all(g[b, nv[b]:] == 0)                      # blocks without tokens untouched
         for j in (0, nv[b] - 1):
             lo, hi = j * 64, min(j * 64 + 64, int(seq_len[b]))
-            np.testing.assert_array_equal(g[b, j], fp32_token_mean(k_tok, b, lo, hi))
+            np.testing.assert_array_equal(g[b, j], fp32_quarter_mean(k_tok, b, lo, hi))
 
 
 def test_decode_front_end_step():
@@ -186,3 +192,39 @@ def test_decode_front_end_step():
     fin = np.isfinite(s_o)
     assert np.array_equal(np.isfinite(s_g), fin)
     assert np.all(np.abs(s_g[fin] - s_o[fin]) <= 1e-4 * np.abs(s_o[fin]) + 1e-6)
+
+
+def test_front_end_in_a_graph_matches_eager():
+    """Projection and pooling captured in a HIP graph: every replay (with
+    eager work and synchronisations between replays) gives the eager result."""
+    B, L, Hs, ds, d_model = 4, 4096, 4, 128, 4096
+    h, wq, wk, ww = synth.selector_frontend(5, B, d_model, Hs, ds)
+    hd, wqd, wkd, wwd = bf(h), bf(wq), bf(wk), bf(ww)
+    seq_len = np.array([4096, 3000, 64, 1], np.int32)
+    pos, first, sl = dev(seq_len - 1), dev((seq_len - 1) // 64), dev(seq_len)
+    outs = []
+    for _ in range(2):
+        outs.append((torch.empty((B, Hs, ds), dtype=torch.bfloat16, device=DEV),
+                     torch.empty((B, Hs), dtype=torch.float32, device=DEV),
+                     torch.zeros((B, L, Hs, ds), dtype=torch.bfloat16, device=DEV),
+                     torch.zeros((B, L // 64, Hs, ds), dtype=torch.bfloat16, device=DEV)))
+
+    def run(o, st):
+        spot.spot_selector_project(hd, wqd, wkd, wwd, pos, B, d_model, Hs, ds, 64, 1.0e6, o[0],
+                                   o[1], o[2], 1, L, st)
+        spot.spot_selector_pool(o[2], o[3], B, L, Hs, ds, sl, first, 1, st)
+
+    run(outs[0], torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run(outs[1], torch.cuda.current_stream())
+    for rep in range(3):
+        for t in outs[1]:
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs[0], outs[1]):
+            assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                               b.view(torch.int16) if b.dtype == torch.bfloat16 else b), rep
