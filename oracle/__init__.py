@@ -22,7 +22,7 @@ SRC = os.path.join(HERE, "spot_oracle.c")
 HDR = os.path.join(HERE, "spot_oracle.h")
 SO = os.path.join(HERE, "liboracle.so")
 
-KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2}
+KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2, "int8": 3, "mxfp8": 4}
 
 _lock = threading.Lock()
 _lib = None
@@ -92,7 +92,7 @@ def key_values(k_sel, k_scale=None, kfmt="bf16", n=None) -> np.ndarray:
     ks = np.ascontiguousarray(k_sel)
     sc = None if k_scale is None else np.ascontiguousarray(k_scale)
     if n is None:
-        n = ks.size if f == 0 else ks.size * 2
+        n = ks.size if f in (0, 3, 4) else ks.size * 2
     return np.array([L.oracle_key_value(_p(ks), _p(sc), f, i) for i in range(n)])
 
 
@@ -108,7 +108,7 @@ def selector_score(q_sel, w, k_sel, k_scale=None, kfmt="bf16", rows_per_seq=1,
     n_seq = rows // rows_per_seq
     k_sel = np.ascontiguousarray(k_sel)
     if nblk is None:
-        per = h_s * d_s if f == 0 else h_s * d_s // 2
+        per = h_s * d_s if f in (0, 3, 4) else h_s * d_s // 2
         nblk = k_sel.size // (n_seq * per)
     sc = None if k_scale is None else np.ascontiguousarray(k_scale)
     nv = None if n_valid is None else _c(n_valid, np.int32)
@@ -131,7 +131,7 @@ def selector_score_tokens(q_sel, w, k_tok, k_scale=None, kfmt="bf16", rows_per_s
     n_seq = rows // rows_per_seq
     k_tok = np.ascontiguousarray(k_tok)
     if l_cap is None:
-        per = h_s * d_s if f == 0 else h_s * d_s // 2
+        per = h_s * d_s if f in (0, 3, 4) else h_s * d_s // 2
         l_cap = k_tok.size // (n_seq * per)
     sc = None if k_scale is None else np.ascontiguousarray(k_scale)
     sl = None if seq_len is None else _c(seq_len, np.int32)

@@ -25,8 +25,9 @@
  *   dense attention ...... the full-attention baseline (Section 3)
  *
  * Stored formats are decoded exactly: BF16 and FP16 bit patterns, signed INT4
- * codes times an FP16 group scale, and OCP MXFP4 (E2M1 codes times an E8M0
- * power-of-two group scale), 32 elements per group (Section 5.3, Appendix G).
+ * and INT8 codes times an FP16 group scale, and OCP MXFP4 / MXFP8 (E2M1 or
+ * E4M3 codes times an E8M0 power-of-two group scale), 32 elements per group
+ * (Section 5.3, Appendix G).
  *
  * Readings taken where the paper is silent (each is listed in the design
  * notes with its reason): the score has no 1/sqrt(d) factor and temperature
@@ -95,6 +96,22 @@ static double e2m1_to_double(unsigned code) {
     return sign ? -v : v;
 }
 
+/* OCP MX v1.0 E4M3: sign bit 7, four exponent bits (bias 7), three mantissa
+ * bits; no infinities, S.1111.111 is NaN. */
+static double e4m3_to_double(unsigned code) {
+    int sign = (code >> 7) & 1;
+    int e = (code >> 3) & 15;
+    int m = code & 7;
+    double v;
+    if (e == 15 && m == 7)
+        v = NAN;
+    else if (e == 0)
+        v = ldexp((double)m, -9);
+    else
+        v = ldexp(8.0 + m, e - 10);
+    return sign ? -v : v;
+}
+
 /* OCP MX v1.0 E8M0: 2^(e - 127); 0xFF encodes NaN. */
 static double e8m0_to_double(uint8_t e) {
     return e == 0xFF ? NAN : ldexp(1.0, (int)e - 127);
@@ -103,6 +120,12 @@ static double e8m0_to_double(uint8_t e) {
 double oracle_key_value(const void *k_sel, const void *k_scale, int kfmt, int64_t el) {
     if (kfmt == ORACLE_KFMT_BF16)
         return bf16_to_double(((const uint16_t *)k_sel)[el]);
+    if (kfmt == ORACLE_KFMT_INT8)
+        return (double)((const int8_t *)k_sel)[el] *
+               f16_to_double(((const uint16_t *)k_scale)[el / 32]);
+    if (kfmt == ORACLE_KFMT_MXFP8)
+        return e4m3_to_double(((const uint8_t *)k_sel)[el]) *
+               e8m0_to_double(((const uint8_t *)k_scale)[el / 32]);
     uint8_t byte = ((const uint8_t *)k_sel)[el / 2];
     unsigned nib = (el & 1) ? (byte >> 4) : (byte & 15);
     if (kfmt == ORACLE_KFMT_INT4) {

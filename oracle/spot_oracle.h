@@ -20,6 +20,8 @@ extern "C" {
 #define ORACLE_KFMT_BF16 0
 #define ORACLE_KFMT_INT4 1   /* signed 4-bit codes, FP16 scale per 32 elements */
 #define ORACLE_KFMT_MXFP4 2  /* E2M1 codes, E8M0 scale per 32 elements        */
+#define ORACLE_KFMT_INT8 3   /* signed 8-bit codes, FP16 scale per 32 elements */
+#define ORACLE_KFMT_MXFP8 4  /* E4M3 codes, E8M0 scale per 32 elements        */
 
 void oracle_set_threads(int n);
 int oracle_get_threads(void);

@@ -409,6 +409,77 @@ def quantize_mxfp4_g32(k_bits: np.ndarray):
     return codes, e8
 
 
+def quantize_int8_g32(k_bits: np.ndarray):
+    """Symmetric INT8 with one FP16 scale per 32 consecutive elements.
+
+    scale = fp16_rne(amax / 127); code = clamp(rne(x / scale), -127, 127),
+    two's complement in a byte; an all-zero group gets scale 0 and codes 0.
+    Returns (codes uint8 [..., n], scales float16-bits uint16 [..., n/32]).
+    """
+    x = bf16_value(k_bits).astype(np.float64)
+    *lead, n = x.shape
+    assert n % 32 == 0
+    g = x.reshape(*lead, n // 32, 32)
+    amax = np.max(np.abs(g), axis=-1)
+    scale = (amax / 127.0).astype(np.float32).astype(np.float16)
+    sf = scale.astype(np.float64)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        c = np.where(sf[..., None] > 0, np.rint(g / sf[..., None]), 0.0)
+    c = np.clip(c, -127, 127).astype(np.int8).reshape(*lead, n)
+    return c.view(np.uint8), scale.view(np.uint16)
+
+
+def _e4m3_values() -> np.ndarray:
+    """Values of the non-negative finite OCP E4M3 codes 0 .. 126 (ascending)."""
+    v = []
+    for code in range(127):
+        e, m = code >> 3, code & 7
+        v.append(m / 8.0 * 2.0 ** -6 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7))
+    return np.array(v)
+
+
+E4M3_GRID = _e4m3_values()
+
+
+def _e4m3_rne(y: np.ndarray) -> np.ndarray:
+    """|y| -> E4M3 magnitude code (0 .. 126), nearest, ties to the even code,
+    saturating at 448."""
+    a = np.minimum(np.abs(y), 448.0)
+    hi = np.clip(np.searchsorted(E4M3_GRID, a), 1, 126)
+    lo = hi - 1
+    d_lo = a - E4M3_GRID[lo]
+    d_hi = E4M3_GRID[hi] - a
+    pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (hi % 2 == 0))
+    return np.where(pick_hi, hi, lo).astype(np.uint8)
+
+
+def quantize_mxfp8_g32(k_bits: np.ndarray):
+    """OCP MX v1.0 MXFP8 (E4M3): one E8M0 scale per 32 elements.
+
+    X = floor(log2(amax)) - 8 (8 = E4M3's max exponent), clamped to
+    [-127, 127]; E8M0 = X + 127; element code = E4M3_rne(x / 2^X) saturating
+    to +-448; amax = 0 gives E8M0 = 0 and zero codes.
+    Returns (codes uint8 [..., n], e8m0 uint8 [..., n/32]).
+    """
+    x = bf16_value(k_bits).astype(np.float64)
+    *lead, n = x.shape
+    assert n % 32 == 0
+    g = x.reshape(*lead, n // 32, 32)
+    amax = np.max(np.abs(g), axis=-1)
+    with np.errstate(divide="ignore"):
+        X = np.where(amax > 0, np.floor(np.log2(np.where(amax > 0, amax, 1.0))) - 8, -127)
+    X = np.clip(X, -127, 127).astype(np.int32)
+    e8 = (X + 127).astype(np.uint8)
+    y = g / np.ldexp(1.0, X)[..., None]
+    mag = _e4m3_rne(y)
+    sign = ((y < 0) & (mag > 0)).astype(np.uint8) << 7
+    return (mag | sign).reshape(*lead, n).astype(np.uint8), e8
+
+
+QUANTIZERS = {"int4": quantize_int4_g32, "mxfp4": quantize_mxfp4_g32,
+              "int8": quantize_int8_g32, "mxfp8": quantize_mxfp8_g32}
+
+
 # --------------------------------------------------------------------------
 # The five workloads
 # --------------------------------------------------------------------------

@@ -91,6 +91,59 @@ def test_key_decode_tables():
     np.testing.assert_array_equal(v, np.full(32, 0.5))
 
 
+def test_key_decode_tables_8bit():
+    """INT8 two's-complement bytes times the FP16 scale, and landmark codes of
+    the OCP MX v1.0 E4M3 format: 0x01 = 2^-9 (smallest subnormal), 0x08 =
+    2^-6 (smallest normal), 0x38 = 1, 0x3C = 1.5, 0x7E = 448 (largest), 0x7F
+    and 0xFF NaN, bit 7 the sign; E8M0 127 = 1."""
+    codes = np.arange(256, dtype=np.uint8)[:64]
+    v = oracle.key_values(codes, np.array([0x3C00, 0x3800], np.uint16), "int8", 64)
+    want = codes.astype(np.int8).astype(np.float64)
+    want[32:] *= 0.5
+    np.testing.assert_array_equal(v, want)
+    v = oracle.key_values(np.array([0x80, 0xFF, 0x7F, 0x01] * 8, np.uint8),
+                          np.array([0x3C00], np.uint16), "int8", 32)
+    np.testing.assert_array_equal(v[:4], [-128.0, -1.0, 127.0, 1.0])
+    marks = {0x00: 0.0, 0x01: 2.0 ** -9, 0x07: 7 * 2.0 ** -9, 0x08: 2.0 ** -6, 0x38: 1.0,
+             0x3C: 1.5, 0x40: 2.0, 0x7E: 448.0, 0xB8: -1.0, 0xFE: -448.0}
+    cs = np.array(list(marks) + [0] * (32 - len(marks)), np.uint8)
+    v = oracle.key_values(cs, np.array([127], np.uint8), "mxfp8", 32)
+    np.testing.assert_array_equal(v[:len(marks)], list(marks.values()))
+    v = oracle.key_values(np.array([0x7F, 0xFF] + [0] * 30, np.uint8),
+                          np.array([127], np.uint8), "mxfp8", 32)
+    assert np.isnan(v[0]) and np.isnan(v[1])
+    # the 127 finite non-negative codes are strictly increasing
+    v = oracle.key_values(np.arange(128, dtype=np.uint8), np.array([127] * 4, np.uint8),
+                          "mxfp8", 128)
+    assert np.all(np.diff(v[:127]) > 0)
+
+
+@pytest.mark.parametrize("kfmt", ["int8", "mxfp8"])
+def test_score_8bit_matches_bf16_when_exact(kfmt):
+    """8-bit codes times power-of-two scales are exact in BF16: scoring the
+    bytes and scoring BF16 keys with the decoded values agree exactly."""
+    rng = np.random.default_rng(53)
+    Hs, ds, nblk = 4, 128, 6
+    q = bf16_bits(rng.standard_normal((1, Hs, ds)).astype(np.float32))
+    w = rng.uniform(0, 1, (1, Hs)).astype(np.float32)
+    if kfmt == "int8":
+        codes = rng.integers(-128, 128, (1, nblk, Hs, ds)).astype(np.int8).view(np.uint8)
+        e = rng.integers(-6, 3, (1, nblk, Hs, ds // 32))
+        sc = np.ldexp(1.0, e).astype(np.float16)
+        vals = codes.view(np.int8) * np.repeat(sc.astype(np.float64), 32, axis=-1)
+        sc = sc.view(np.uint16)
+    else:
+        codes = rng.integers(0, 256, (1, nblk, Hs, ds)).astype(np.uint8)
+        codes[(codes & 0x7F) == 0x7F] = 0x3F          # no NaN codes
+        sc = rng.integers(120, 131, (1, nblk, Hs, ds // 32)).astype(np.uint8)
+        mag = np.array([0.0] + list(synth.E4M3_GRID[1:]) + [np.nan])
+        vals = np.where(codes & 0x80, -1.0, 1.0) * mag[codes & 0x7F] * \
+            np.repeat(np.ldexp(1.0, sc.astype(np.int64) - 127), 32, axis=-1)
+    s_q = oracle.selector_score(q, w, codes, sc, kfmt, nblk=nblk)
+    s_b = oracle.selector_score(q, w, bf16_bits(vals.astype(np.float32)))
+    np.testing.assert_array_equal(s_q, s_b)
+
+
 def test_score_invariants():
     rng = np.random.default_rng(11)
     Hs, ds, nblk = 4, 64, 9

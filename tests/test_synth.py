@@ -55,6 +55,46 @@ def test_int4_encoder():
     assert np.all(codes == 0) and np.all(scales == 0)
 
 
+def test_int8_encoder():
+    rng = np.random.default_rng(2)
+    x = bf16_bits(rng.standard_normal((50, 64)).astype(np.float32))
+    codes, scales = synth.quantize_int8_g32(x)
+    assert codes.shape == (50, 64) and scales.shape == (50, 2)
+    vals = oracle.key_values(codes, scales, "int8", x.size).reshape(50, 64)
+    xv = bf16_value(x).astype(np.float64)
+    sc = np.repeat(scales.view(np.float16).astype(np.float64), 32, axis=-1)
+    amax = np.repeat(np.abs(xv).reshape(50, 2, 32).max(-1), 32, axis=-1)
+    assert np.all(np.abs(vals - xv) <= sc / 2 + amax * 2.0 ** -10)
+    assert not np.any(codes.view(np.int8) == -128)   # codes stay within [-127, 127]
+    codes, scales = synth.quantize_int8_g32(np.zeros((1, 32), np.uint16))
+    assert np.all(codes == 0) and np.all(scales == 0)
+
+
+def test_mxfp8_encoder():
+    rng = np.random.default_rng(3)
+    x = bf16_bits(rng.standard_normal((50, 64)).astype(np.float32))
+    codes, e8 = synth.quantize_mxfp8_g32(x)
+    assert codes.shape == (50, 64) and e8.shape == (50, 2)
+    vals = oracle.key_values(codes, e8, "mxfp8", x.size).reshape(50, 64)
+    xv = bf16_value(x).astype(np.float64)
+    amax = np.repeat(np.abs(xv).reshape(50, 2, 32).max(-1), 32, axis=-1)
+    # E4M3 keeps 3 fraction bits: within half a step of 2^-3 relative, or of
+    # the smallest subnormal step (2^-9 of the scale) near zero
+    X = e8.astype(np.int64) - 127
+    s2 = np.repeat(np.ldexp(1.0, X), 32, axis=-1)
+    sat = np.abs(xv) / s2 > 448                       # OCP MX: saturate at the max
+    step = np.maximum(np.abs(xv) * 2.0 ** -3, amax * 2.0 ** -8 * 2.0 ** -9)
+    assert np.all(np.abs(vals - xv)[~sat] <= step[~sat] / 2 + 1e-30)
+    np.testing.assert_array_equal(vals[sat], np.sign(xv[sat]) * 448 * s2[sat])
+    # the group maximum lands in [256, 512) after the scale
+    top = np.abs(xv).reshape(50, 2, 32).max(-1) / np.ldexp(1.0, X)
+    assert np.all((top >= 256) & (top < 512))
+    assert np.all((codes & 0x7F) != 0x7F)            # no NaN codes
+    # ties go to the even code: 1 + 1/16 lies halfway between codes 0x38 and 0x39
+    c = synth._e4m3_rne(np.array([1.0625, 1.1875]))
+    assert list(c) == [0x38, 0x3A]
+
+
 def test_footprint_matches_paper():
     """Section 5.3: 4.50 GiB BF16 -> 1.27 GiB INT4 and 1.20 GiB FP4 (0.281x)."""
     ds = 64
