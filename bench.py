@@ -45,7 +45,7 @@ def parse():
                     help="skip the quantized-selector and smaller-workload decode timings")
     ap.add_argument("--tokens", action="store_true",
                     help="run the per-token selector leg even with --no-extra")
-    ap.add_argument("--fmt", default="bf16", choices=["bf16", "int4", "mxfp4"])
+    ap.add_argument("--fmt", default="bf16", choices=["bf16", "int4", "mxfp4", "int8", "mxfp8"])
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the block-sparse prefill leg (32K-token layer)")
     ap.add_argument("--prefill-iters", type=int, default=10)
@@ -118,18 +118,15 @@ def main():
     if args.fmt == "bf16":
         ksel_host, kscale_host = wl.k_sel, None
         sel_bytes = wl.k_sel.nbytes
-    elif args.fmt == "int4":
-        ksel_host, kscale_host = synth.quantize_int4_g32(wl.k_sel)
-        sel_bytes = ksel_host.nbytes + kscale_host.nbytes
     else:
-        ksel_host, kscale_host = synth.quantize_mxfp4_g32(wl.k_sel)
+        ksel_host, kscale_host = synth.QUANTIZERS[args.fmt](wl.k_sel)
         sel_bytes = ksel_host.nbytes + kscale_host.nbytes
 
     def dev_sel():
         if args.fmt == "bf16":
             return bf(ksel_host), None
         ks = torch.from_numpy(np.ascontiguousarray(ksel_host)).to(dev)
-        sc = kscale_host.view(np.int16) if args.fmt == "int4" else kscale_host
+        sc = kscale_host.view(np.int16) if args.fmt in ("int4", "int8") else kscale_host
         return ks, torch.from_numpy(np.ascontiguousarray(sc)).to(dev)
 
     q = bf(wl.q)
@@ -281,9 +278,9 @@ def main():
         # The same step with the 4-bit selector caches (INT4-g32 / MXFP4-g32,
         # quantized from the BF16 cache): fewer selector bytes, same K/V.
         quant = {}
-        for fmt, qfn in (("int4", synth.quantize_int4_g32), ("mxfp4", synth.quantize_mxfp4_g32)):
-            codes, scales = qfn(wl.k_sel)
-            sc = scales.view(np.int16) if fmt == "int4" else scales
+        for fmt in ("int4", "mxfp4", "int8", "mxfp8"):
+            codes, scales = synth.QUANTIZERS[fmt](wl.k_sel)
+            sc = scales.view(np.int16) if fmt in ("int4", "int8") else scales
             qsel = [(torch.from_numpy(np.ascontiguousarray(codes)).to(dev),
                      torch.from_numpy(np.ascontiguousarray(sc)).to(dev))
                     for _ in range(args.copies)]

@@ -52,11 +52,14 @@ typedef int32_t spot_status;
                                /* 16-byte aligned                                 */
 #define SPOT_ERR_HIP 6         /* the HIP runtime reported a launch error         */
 
-/* Storage formats of the selector key cache (Section 5.3, Appendix G:
- * group-32 microscale 4-bit formats alongside BF16). */
+/* Storage formats of the selector key cache (Section 5.3, Appendix G: INT8,
+ * FP8 and group-32 microscale 4-bit formats alongside BF16; here every
+ * quantized format carries one scale per 32 elements). */
 #define SPOT_KFMT_BF16 0
 #define SPOT_KFMT_INT4_G32 1  /* signed 4-bit codes, FP16 scale per 32 elements */
 #define SPOT_KFMT_MXFP4_G32 2 /* OCP MXFP4: E2M1 codes, E8M0 scale per 32       */
+#define SPOT_KFMT_INT8_G32 3  /* signed 8-bit codes, FP16 scale per 32 elements */
+#define SPOT_KFMT_MXFP8_G32 4 /* OCP MXFP8: E4M3 codes, E8M0 scale per 32       */
 
 /* Human-readable name of a status code (static storage). */
 const char *spot_status_str(spot_status s);

@@ -37,6 +37,11 @@ const char* spot_version(void) { return SPOT_VERSION_STR; }
 
 static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+static bool valid_kfmt(int kfmt) {
+  return kfmt == SPOT_KFMT_BF16 || kfmt == SPOT_KFMT_INT4_G32 || kfmt == SPOT_KFMT_MXFP4_G32 ||
+         kfmt == SPOT_KFMT_INT8_G32 || kfmt == SPOT_KFMT_MXFP8_G32;
+}
+
 spot_status spot_selector_project(const void* h, const void* w_q, const void* w_k,
                                   const void* w_w, const int32_t* pos, int rows, int d_model,
                                   int h_s, int d_s, int rope_dim, float rope_base, void* q_out,
@@ -78,8 +83,7 @@ spot_status spot_selector_score(const void* q_sel, const float* w, const void* k
                                 float* scores, void* stream) {
   if (!q_sel || !w || !k_sel || !scores) return SPOT_ERR_NULL;
   if (n_seq < 0 || rows_per_seq < 1 || nblk < 0 || h_s < 1 || d_s < 1) return SPOT_ERR_SHAPE;
-  if (kfmt != SPOT_KFMT_BF16 && kfmt != SPOT_KFMT_INT4_G32 && kfmt != SPOT_KFMT_MXFP4_G32)
-    return SPOT_ERR_UNSUPPORTED;
+  if (!valid_kfmt(kfmt)) return SPOT_ERR_UNSUPPORTED;
   if (kfmt != SPOT_KFMT_BF16 && !k_scale) return SPOT_ERR_NULL;
   if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
   if ((long long)n_seq * rows_per_seq > 0x7fffffffLL) return SPOT_ERR_SHAPE;
@@ -96,8 +100,7 @@ spot_status spot_selector_score_tokens(const void* q_sel, const float* w, const 
   if (!q_sel || !w || !k_tok || !scores) return SPOT_ERR_NULL;
   if (n_seq < 0 || rows_per_seq < 1 || l_cap < 0 || l_cap % kBlk || h_s < 1 || d_s < 1)
     return SPOT_ERR_SHAPE;
-  if (kfmt != SPOT_KFMT_BF16 && kfmt != SPOT_KFMT_INT4_G32 && kfmt != SPOT_KFMT_MXFP4_G32)
-    return SPOT_ERR_UNSUPPORTED;
+  if (!valid_kfmt(kfmt)) return SPOT_ERR_UNSUPPORTED;
   if (kfmt != SPOT_KFMT_BF16 && !k_scale) return SPOT_ERR_NULL;
   if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
   // Launch size: at most one workgroup per (row, block), padded to 8 blocks.
@@ -189,8 +192,7 @@ spot_status spot_decode_step(const void* q_sel, const float* w, const void* k_se
   spot_status st = check_decode(q, k, v, seq_len, out, batch, h_q, h_kv, d, l_cap);
   if (st != SPOT_OK) return st;
   if (!q_sel || !w || !k_sel || !scores || !idx || !count) return SPOT_ERR_NULL;
-  if (kfmt != SPOT_KFMT_BF16 && kfmt != SPOT_KFMT_INT4_G32 && kfmt != SPOT_KFMT_MXFP4_G32)
-    return SPOT_ERR_UNSUPPORTED;
+  if (!valid_kfmt(kfmt)) return SPOT_ERR_UNSUPPORTED;
   if (kfmt != SPOT_KFMT_BF16 && !k_scale) return SPOT_ERR_NULL;
   if (h_s < 1 || d_s < 1) return SPOT_ERR_SHAPE;
   if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;

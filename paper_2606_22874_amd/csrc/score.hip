@@ -158,6 +158,12 @@ hipError_t launch_selector_score(const void* q_sel, const float* w, const void* 
     case SPOT_KFMT_INT4_G32:
       return launch_fmt<SPOT_KFMT_INT4_G32>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk,
                                             n_valid, scores);
+    case SPOT_KFMT_INT8_G32:
+      return launch_fmt<SPOT_KFMT_INT8_G32>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk,
+                                            n_valid, scores);
+    case SPOT_KFMT_MXFP8_G32:
+      return launch_fmt<SPOT_KFMT_MXFP8_G32>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk,
+                                             n_valid, scores);
     default:
       return launch_fmt<SPOT_KFMT_MXFP4_G32>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk,
                                              n_valid, scores);

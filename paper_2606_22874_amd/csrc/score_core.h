@@ -3,9 +3,9 @@
 //   scores[r, j] = sum_h w[r,h] * ReLU(q_sel[r,h,:] . kbar[seq(r), j, h, :]).
 // The pooled key of one block is h_s * d_s = 512 elements.  One wavefront
 // covers a whole block with one load per lane: lane l owns elements
-// 8l .. 8l+7 (BF16: 16 bytes; 4-bit formats: 4 bytes of codes plus the group
-// scale of its 32-element group), so consecutive lanes read consecutive
-// bytes.  The head dot products are reduced over the LPH = d_s/8 lanes of a
+// 8l .. 8l+7 (BF16: 16 bytes; 8-bit formats: 8 bytes of codes, 4-bit
+// formats: 4 bytes, plus the scale of its 32-element group), so consecutive
+// lanes read consecutive bytes.  The head dot products are reduced over the LPH = d_s/8 lanes of a
 // head, passed through ReLU and weighted, then summed over heads -- all with
 // a fixed butterfly, so the result is deterministic.
 #pragma once
@@ -25,6 +25,7 @@ __device__ __forceinline__ float e8m0_to_f32(uint32_t e) {
 }
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Global loads, optionally non-temporal (NT: the line is not kept in the
 // caches -- for data streamed exactly once, which then does not evict
@@ -96,6 +97,56 @@ struct KeyLoad<SPOT_KFMT_MXFP4_G32> {
     const f32x2 v1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, 1.0f, 1);
     const f32x2 v2 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, 1.0f, 2);
     const f32x2 v3 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, 1.0f, 3);
+    float a = fmaf(qf[0], v0[0], 0.f);
+    a = fmaf(qf[1], v0[1], a);
+    a = fmaf(qf[2], v1[0], a);
+    a = fmaf(qf[3], v1[1], a);
+    a = fmaf(qf[4], v2[0], a);
+    a = fmaf(qf[5], v2[1], a);
+    a = fmaf(qf[6], v3[0], a);
+    a = fmaf(qf[7], v3[1], a);
+    return a * e8m0_to_f32(scale);
+  }
+};
+
+// INT8: 8 bytes of two's-complement codes and one FP16 scale.
+template <>
+struct KeyLoad<SPOT_KFMT_INT8_G32> {
+  u32x2 codes;
+  uint16_t scale;
+  template <bool NT = false>
+  __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t* ks, size_t blk, int lane) {
+    codes = ld<NT, u32x2>(kb + blk * 512 + lane * 8);
+    scale = ld<NT, uint16_t>(ks + (blk * 16 + (lane >> 2)) * 2);
+  }
+  __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
+    float a = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int code = (int)(codes[i >> 2] << (24 - 8 * (i & 3))) >> 24;  // sign-extend byte
+      a = fmaf(qf[i], (float)code, a);
+    }
+    return a * f16_to_f32(scale);
+  }
+};
+
+// MXFP8: 8 bytes of OCP E4M3 codes and one E8M0 scale.
+template <>
+struct KeyLoad<SPOT_KFMT_MXFP8_G32> {
+  u32x2 codes;
+  uint8_t scale;
+  template <bool NT = false>
+  __device__ __forceinline__ void load(const uint8_t* kb, const uint8_t* ks, size_t blk, int lane) {
+    codes = ld<NT, u32x2>(kb + blk * 512 + lane * 8);
+    scale = ld<NT, uint8_t>(ks + blk * 16 + (lane >> 2));
+  }
+  __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
+    // v_cvt_scalef32_pk_f32_fp8 (scale 1): the two E4M3 bytes of the low or
+    // high half-word -> their exact values; the E8M0 scale multiplies the sum.
+    const f32x2 v0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(codes[0], 1.0f, false);
+    const f32x2 v1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(codes[0], 1.0f, true);
+    const f32x2 v2 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(codes[1], 1.0f, false);
+    const f32x2 v3 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(codes[1], 1.0f, true);
     float a = fmaf(qf[0], v0[0], 0.f);
     a = fmaf(qf[1], v0[1], a);
     a = fmaf(qf[2], v1[0], a);

@@ -214,6 +214,14 @@ hipError_t launch_selector_score_tokens(const void* q_sel, const float* w, const
       return launch_tokens_fmt<SPOT_KFMT_INT4_G32>(lph, grid, s, q, w, k, ks, n_seq,
                                                    rows_per_seq, l_cap, nblk, runs, seq_len,
                                                    scores);
+    case SPOT_KFMT_INT8_G32:
+      return launch_tokens_fmt<SPOT_KFMT_INT8_G32>(lph, grid, s, q, w, k, ks, n_seq,
+                                                   rows_per_seq, l_cap, nblk, runs, seq_len,
+                                                   scores);
+    case SPOT_KFMT_MXFP8_G32:
+      return launch_tokens_fmt<SPOT_KFMT_MXFP8_G32>(lph, grid, s, q, w, k, ks, n_seq,
+                                                    rows_per_seq, l_cap, nblk, runs, seq_len,
+                                                    scores);
     default:
       return launch_tokens_fmt<SPOT_KFMT_MXFP4_G32>(lph, grid, s, q, w, k, ks, n_seq,
                                                     rows_per_seq, l_cap, nblk, runs, seq_len,

@@ -187,12 +187,20 @@ __device__ __forceinline__ void score_run_rt(const StepArgs& a, int row, int nv,
     switch (a.kfmt) {
       case SPOT_KFMT_BF16: score_run<SPOT_KFMT_BF16, 8>(a, row, nv, j0, jend, lane); break;
       case SPOT_KFMT_INT4_G32: score_run<SPOT_KFMT_INT4_G32, 8>(a, row, nv, j0, jend, lane); break;
+      case SPOT_KFMT_INT8_G32: score_run<SPOT_KFMT_INT8_G32, 8>(a, row, nv, j0, jend, lane); break;
+      case SPOT_KFMT_MXFP8_G32:
+        score_run<SPOT_KFMT_MXFP8_G32, 8>(a, row, nv, j0, jend, lane);
+        break;
       default: score_run<SPOT_KFMT_MXFP4_G32, 8>(a, row, nv, j0, jend, lane); break;
     }
   } else {
     switch (a.kfmt) {
       case SPOT_KFMT_BF16: score_run<SPOT_KFMT_BF16, 16>(a, row, nv, j0, jend, lane); break;
       case SPOT_KFMT_INT4_G32: score_run<SPOT_KFMT_INT4_G32, 16>(a, row, nv, j0, jend, lane); break;
+      case SPOT_KFMT_INT8_G32: score_run<SPOT_KFMT_INT8_G32, 16>(a, row, nv, j0, jend, lane); break;
+      case SPOT_KFMT_MXFP8_G32:
+        score_run<SPOT_KFMT_MXFP8_G32, 16>(a, row, nv, j0, jend, lane);
+        break;
       default: score_run<SPOT_KFMT_MXFP4_G32, 16>(a, row, nv, j0, jend, lane); break;
     }
   }

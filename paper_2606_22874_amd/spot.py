@@ -24,7 +24,7 @@ from . import build as _build
 SPOT_OK = 0
 STATUS = {0: "ok", 1: "null pointer", 2: "invalid shape", 3: "unsupported", 4: "invalid rule",
           5: "workspace", 6: "HIP launch error"}
-KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2}
+KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2, "int8": 3, "mxfp8": 4}
 BLK = 64
 
 SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score",
@@ -128,6 +128,17 @@ def _check(fn: str, st: int):
         raise SpotError(fn, st)
 
 
+def _sel_cache(k, k_scale, f, n_keys, h_s, d_s, name):
+    """Checks a selector key cache of n_keys keys in format f."""
+    if f == 0:
+        _dev(k, name, BF16, n_keys * h_s * d_s)
+        return
+    per = h_s * d_s if f in (3, 4) else h_s * d_s // 2      # 8-bit or 4-bit codes
+    _dev(k, name, U8, n_keys * per)
+    _dev(k_scale, "k_scale", (torch.float16, torch.int16) if f in (1, 3) else U8,
+         n_keys * h_s * d_s // 32)
+
+
 # ------------------------------------------------------------- C ABI calls
 def spot_selector_score(q_sel, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq, nblk, h_s, d_s,
                         n_valid, scores, stream=None):
@@ -135,12 +146,7 @@ def spot_selector_score(q_sel, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq, nbl
     f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
     _dev(q_sel, "q_sel", BF16, rows * h_s * d_s)
     _dev(w, "w", F32, rows * h_s)
-    if f == 0:
-        _dev(k_sel, "k_sel", BF16, n_seq * nblk * h_s * d_s)
-    else:
-        _dev(k_sel, "k_sel", U8, n_seq * nblk * h_s * d_s // 2)
-        _dev(k_scale, "k_scale", (torch.float16, torch.int16) if f == 1 else U8,
-             n_seq * nblk * h_s * d_s // 32)
+    _sel_cache(k_sel, k_scale, f, n_seq * nblk, h_s, d_s, "k_sel")
     if n_valid is not None:
         _dev(n_valid, "n_valid", I32, rows)
     _dev(scores, "scores", F32, rows * nblk)
@@ -155,12 +161,7 @@ def spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_s
     f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
     _dev(q_sel, "q_sel", BF16, rows * h_s * d_s)
     _dev(w, "w", F32, rows * h_s)
-    if f == 0:
-        _dev(k_tok, "k_tok", BF16, n_seq * l_cap * h_s * d_s)
-    else:
-        _dev(k_tok, "k_tok", U8, n_seq * l_cap * h_s * d_s // 2)
-        _dev(k_scale, "k_scale", (torch.float16, torch.int16) if f == 1 else U8,
-             n_seq * l_cap * h_s * d_s // 32)
+    _sel_cache(k_tok, k_scale, f, n_seq * l_cap, h_s, d_s, "k_tok")
     if seq_len is not None:
         _dev(seq_len, "seq_len", I32, rows)
     _dev(scores, "scores", F32, rows * (l_cap // 64))
@@ -279,11 +280,7 @@ def spot_decode_step(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k
     f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
     _dev(q_sel, "q_sel", BF16, batch * h_s * d_s)
     _dev(w, "w", F32, batch * h_s)
-    if f == 0:
-        _dev(k_sel, "k_sel", BF16, batch * nblk * h_s * d_s)
-    else:
-        _dev(k_sel, "k_sel", U8, batch * nblk * h_s * d_s // 2)
-        _dev(k_scale, "k_scale", None, batch * nblk * h_s * d_s // 32)
+    _sel_cache(k_sel, k_scale, f, batch * nblk, h_s, d_s, "k_sel")
     if n_valid is not None:
         _dev(n_valid, "n_valid", I32, batch)
     _dev(q, "q", BF16, batch * h_q * d)
@@ -322,7 +319,8 @@ def selector_score(q_sel, w, k_sel, k_scale=None, kfmt="bf16", rows_per_seq=1, n
     rows = q_sel.numel() // (h_s * d_s)
     n_seq = rows // rows_per_seq
     if nblk is None:
-        per = h_s * d_s if KFMT.get(kfmt, kfmt) == 0 else h_s * d_s // 2
+        f = KFMT.get(kfmt, kfmt)
+        per = h_s * d_s if f in (0, 3, 4) else h_s * d_s // 2
         nblk = k_sel.numel() // (n_seq * per)
     if out is None:
         out = torch.empty((rows, nblk), dtype=torch.float32, device=q_sel.device)
@@ -338,7 +336,8 @@ def selector_score_tokens(q_sel, w, k_tok, k_scale=None, kfmt="bf16", rows_per_s
     rows = q_sel.numel() // (h_s * d_s)
     n_seq = rows // rows_per_seq
     if l_cap is None:
-        per = h_s * d_s if KFMT.get(kfmt, kfmt) == 0 else h_s * d_s // 2
+        f = KFMT.get(kfmt, kfmt)
+        per = h_s * d_s if f in (0, 3, 4) else h_s * d_s // 2
         l_cap = k_tok.numel() // (n_seq * per)
     if out is None:
         out = torch.empty((rows, l_cap // 64), dtype=torch.float32, device=q_sel.device)

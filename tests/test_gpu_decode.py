@@ -54,10 +54,8 @@ def workload(i, **kw):
 
 
 def quantized(wl, fmt):
-    if fmt == "int4":
-        codes, scales = synth.quantize_int4_g32(wl.k_sel)
-        return codes, scales.view(np.uint16)
-    return synth.quantize_mxfp4_g32(wl.k_sel)
+    codes, scales = synth.QUANTIZERS[fmt](wl.k_sel)
+    return codes, (scales.view(np.uint16) if fmt in ("int4", "int8") else scales)
 
 
 def gpu_scores(wl, fmt="bf16"):
@@ -66,7 +64,7 @@ def gpu_scores(wl, fmt="bf16"):
     else:
         c, s = quantized(wl, fmt)
         k_sel = torch.from_numpy(c).to(DEV)
-        k_scale = (torch.from_numpy(s.view(np.int16)).to(DEV) if fmt == "int4"
+        k_scale = (torch.from_numpy(s.view(np.int16)).to(DEV) if fmt in ("int4", "int8")
                    else torch.from_numpy(s).to(DEV))
     out = spot.selector_score(bf(wl.q_sel), f32(wl.w), k_sel, k_scale, fmt,
                               n_valid=i32(wl.n_valid), nblk=wl.nblk)
@@ -106,7 +104,8 @@ def assert_out_close(out_g, lse_g, out_o, lse_o):
 
 # ------------------------------------------------------------------ scoring
 @pytest.mark.parametrize("cfg,fmt", [(1, "bf16"), (2, "bf16"), (3, "bf16"), (3, "int4"),
-                                     (3, "mxfp4"), (1, "int4"), (1, "mxfp4")])
+                                     (3, "mxfp4"), (1, "int4"), (1, "mxfp4"), (3, "int8"),
+                                     (3, "mxfp8"), (1, "int8"), (1, "mxfp8")])
 def test_selector_score_parity(cfg, fmt):
     wl = workload(cfg, backbone=False)
     assert_scores_close(gpu_scores(wl, fmt), oracle_scores(wl, fmt))
@@ -115,7 +114,7 @@ def test_selector_score_parity(cfg, fmt):
 def test_selector_score_ragged():
     # ragged seq_len (n_valid not a multiple of the 32-block workgroup chunk)
     wl = workload(2, B=5, L=8192, seq_len=(8192, 5000, 64, 1, 4097), backbone=False)
-    for fmt in ("bf16", "int4", "mxfp4"):
+    for fmt in ("bf16", "int4", "mxfp4", "int8", "mxfp8"):
         assert_scores_close(gpu_scores(wl, fmt), oracle_scores(wl, fmt))
 
 
@@ -225,7 +224,7 @@ def test_select_negative_zero_ties_positive_zero(nblk, k_max):
 
 
 @pytest.mark.parametrize("cfg,fmt", [(1, "bf16"), (2, "bf16"), (3, "bf16"), (3, "int4"),
-                                     (3, "mxfp4")])
+                                     (3, "mxfp4"), (3, "int8"), (3, "mxfp8")])
 def test_score_and_select_end_to_end(cfg, fmt):
     """GPU scores -> GPU selection vs oracle scores -> oracle selection."""
     wl = workload(cfg, backbone=False)

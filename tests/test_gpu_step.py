@@ -53,11 +53,9 @@ def workload(i, **kw):
 def selector(wl, fmt):
     if fmt == "bf16":
         return bf(wl.k_sel), None
-    if fmt == "int4":
-        c, s = synth.quantize_int4_g32(wl.k_sel)
-        return (torch.from_numpy(c).to(DEV),
-                torch.from_numpy(s.view(np.uint16).view(np.int16)).to(DEV))
-    c, s = synth.quantize_mxfp4_g32(wl.k_sel)
+    c, s = synth.QUANTIZERS[fmt](wl.k_sel)
+    if fmt in ("int4", "int8"):
+        s = s.view(np.uint16).view(np.int16)
     return torch.from_numpy(c).to(DEV), torch.from_numpy(s).to(DEV)
 
 
@@ -94,7 +92,7 @@ def assert_same(sep, fus):
 
 
 @pytest.mark.parametrize("cfg,fmt", [(1, "bf16"), (2, "bf16"), (3, "bf16"), (3, "int4"),
-                                     (3, "mxfp4")])
+                                     (3, "mxfp4"), (3, "int8"), (3, "mxfp8")])
 def test_step_matches_separate_calls(cfg, fmt):
     wl = workload(cfg)
     x = inputs(wl, fmt)

@@ -54,11 +54,8 @@ def inputs(seed, n_seq, rows_per_seq, L, Hs, ds, lens, fmt):
     w = w.reshape(n_seq * rows_per_seq, Hs)
     if fmt == "bf16":
         return q, w, k, None
-    if fmt == "int4":
-        c, s = synth.quantize_int4_g32(k)
-        return q, w, c, s.view(np.uint16)
-    c, s = synth.quantize_mxfp4_g32(k)
-    return q, w, c, s
+    c, s = synth.QUANTIZERS[fmt](k)
+    return q, w, c, (s.view(np.uint16) if fmt in ("int4", "int8") else s)
 
 
 def run_both(q, w, k, sc, fmt, rows_per_seq, L, lens):
@@ -67,7 +64,8 @@ def run_both(q, w, k, sc, fmt, rows_per_seq, L, lens):
     s_o = oracle.selector_score_tokens(q, w, k, sc, fmt, rows_per_seq=rows_per_seq,
                                        seq_len=sl_o, l_cap=L, h_s=Hs, d_s=ds)
     k_d = bf(k) if fmt == "bf16" else dev(k)
-    sc_d = None if sc is None else (dev(sc.view(np.int16)) if fmt == "int4" else dev(sc))
+    sc_d = None if sc is None else (dev(sc.view(np.int16)) if fmt in ("int4", "int8")
+                                    else dev(sc))
     sl_d = None if lens is None else dev(np.asarray(lens, np.int32))
     s_g = spot.selector_score_tokens(bf(q), dev(w), k_d, sc_d, fmt,
                                      rows_per_seq=rows_per_seq, seq_len=sl_d, l_cap=L)
@@ -87,6 +85,9 @@ CASES = [
     (2, 1, 4096, 4, 128, [4096, 4000], "mxfp4"),
     (2, 3, 2048, 4, 128, [2048, 1000, 64, 1500, 1501, 2047], "bf16"),  # rows share keys
     (3, 2, 1024, 8, 64, [1024, 700, 1, 2, 900, 1024], "int4"),
+    (2, 1, 4096, 4, 128, [4096, 2049], "int8"),
+    (2, 1, 4096, 8, 64, [3000, 4096], "mxfp8"),
+    (3, 2, 1024, 4, 128, [1024, 1, 700, 64, 1000, 65], "mxfp8"),
 ]
 
 
