@@ -57,6 +57,7 @@ def lib():
             L.oracle_key_value.argtypes = [P, P, I, ctypes.c_int64]
             L.oracle_key_value.restype = D
             L.oracle_selector_score.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P]
+            L.oracle_selector_score_qk.argtypes = [P, P, I, P, P, P, I, I, I, I, I, I, P, P]
             L.oracle_selector_score_tokens.argtypes = [P, P, P, P, I, I, I, I, I, I, I, P, P]
             L.oracle_selector_project.argtypes = [P, P, P, P, P, I, I, I, I, I, D, P, P, P]
             L.oracle_selector_pool.argtypes = [P, I, I, I, I, P, P]
@@ -115,6 +116,24 @@ def selector_score(q_sel, w, k_sel, k_scale=None, kfmt="bf16", rows_per_seq=1,
     out = np.empty((rows, nblk), dtype=np.float64)
     lib().oracle_selector_score(_p(q_sel), _p(w), _p(k_sel), _p(sc), f, n_seq, rows_per_seq,
                                 nblk, h_s, d_s, _p(nv), _p(out))
+    return out
+
+
+def selector_score_qk(q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt, rows, nblk, h_s, d_s,
+                      rows_per_seq=1, n_valid=None) -> np.ndarray:
+    """Block scores [rows, nblk] in float64 with quantized queries and keys."""
+    qf = KFMT[qfmt] if isinstance(qfmt, str) else int(qfmt)
+    kf = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
+    q = np.ascontiguousarray(q_sel)
+    qs = None if q_scale is None else np.ascontiguousarray(q_scale)
+    k = np.ascontiguousarray(k_sel)
+    ks = None if k_scale is None else np.ascontiguousarray(k_scale)
+    w = _c(w, np.float32)
+    nv = None if n_valid is None else _c(n_valid, np.int32)
+    out = np.empty((rows, nblk), dtype=np.float64)
+    lib().oracle_selector_score_qk(_p(q), _p(qs), qf, _p(w), _p(k), _p(ks), kf,
+                                   rows // rows_per_seq, rows_per_seq, nblk, h_s, d_s, _p(nv),
+                                   _p(out))
     return out
 
 

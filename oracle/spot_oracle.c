@@ -164,6 +164,38 @@ void oracle_selector_score(const uint16_t *q_sel, const float *w, const void *k_
     }
 }
 
+/* The same block score with the selector queries stored in a quantized
+ * format too (Section 5.3 and Appendix G quantize the queries as well as the
+ * key cache); qfmt/kfmt as oracle_key_value. */
+void oracle_selector_score_qk(const void *q_sel, const void *q_scale, int qfmt, const float *w,
+                              const void *k_sel, const void *k_scale, int kfmt, int n_seq,
+                              int rows_per_seq, int nblk, int h_s, int d_s,
+                              const int32_t *n_valid, double *scores) {
+    int rows = n_seq * rows_per_seq;
+#pragma omp parallel for schedule(dynamic) num_threads(oracle_get_threads())
+    for (int r = 0; r < rows; ++r) {
+        int seq = r / rows_per_seq;
+        int nv = n_valid ? n_valid[r] : nblk;
+        for (int j = 0; j < nblk; ++j) {
+            if (j >= nv) {
+                scores[(int64_t)r * nblk + j] = -INFINITY;
+                continue;
+            }
+            double s = 0.0;
+            for (int h = 0; h < h_s; ++h) {
+                int64_t kb = (((int64_t)seq * nblk + j) * h_s + h) * d_s;
+                int64_t qb = ((int64_t)r * h_s + h) * d_s;
+                double dot = 0.0;
+                for (int i = 0; i < d_s; ++i)
+                    dot += oracle_key_value(q_sel, q_scale, qfmt, qb + i) *
+                           oracle_key_value(k_sel, k_scale, kfmt, kb + i);
+                s += (double)w[(int64_t)r * h_s + h] * (dot > 0.0 ? dot : 0.0);
+            }
+            scores[(int64_t)r * nblk + j] = s;
+        }
+    }
+}
+
 /* Per-token selector with a per-block maximum (Section 2.3): each visible
  * token t gets the head-weighted ReLU score of Section 2.1 against its own
  * selector key, and a block's value is the largest score among its visible

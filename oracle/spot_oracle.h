@@ -41,6 +41,14 @@ void oracle_selector_score(const uint16_t *q_sel, const float *w, const void *k_
                            int nblk, int h_s, int d_s, const int32_t *n_valid,
                            double *scores);
 
+/* oracle_selector_score with the queries in a stored format as well:
+ * q_sel (and q_scale) in format qfmt laid out like the keys, [rows, h_s, d_s]
+ * elements (Section 5.3, Appendix G: queries and key cache quantized). */
+void oracle_selector_score_qk(const void *q_sel, const void *q_scale, int qfmt, const float *w,
+                              const void *k_sel, const void *k_scale, int kfmt, int n_seq,
+                              int rows_per_seq, int nblk, int h_s, int d_s,
+                              const int32_t *n_valid, double *scores);
+
 /* Per-token selector scores reduced to one value per block (Section 2.3:
  * sbar[r, b] = max over the tokens t of block b of s[r, t], with s the score
  * of Section 2.1 against each token's own selector key).

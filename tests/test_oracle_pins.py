@@ -144,6 +144,32 @@ def test_score_8bit_matches_bf16_when_exact(kfmt):
     np.testing.assert_array_equal(s_q, s_b)
 
 
+@pytest.mark.parametrize("fmt", ["mxfp4", "mxfp8"])
+def test_score_quantized_queries_match_bf16_when_exact(fmt):
+    """Queries stored as MX codes with power-of-two scales are exact in BF16:
+    scoring the coded queries against coded keys equals scoring BF16 copies
+    of both (the query and key decoders are independent of each other)."""
+    rng = np.random.default_rng(61)
+    rows, Hs, ds, nblk = 3, 4, 128, 5
+    q = bf16_bits(rng.standard_normal((rows, Hs, ds)).astype(np.float32))
+    k = bf16_bits(rng.standard_normal((1, nblk, Hs, ds)).astype(np.float32))
+    w = rng.uniform(0, 1, (rows, Hs)).astype(np.float32)
+    qc, qs = synth.QUANTIZERS[fmt](q)
+    kc, ks = synth.QUANTIZERS[fmt](k)
+    qv = oracle.key_values(qc, qs, fmt, q.size).reshape(q.shape)
+    kv = oracle.key_values(kc, ks, fmt, k.size).reshape(k.shape)
+    s_q = oracle.selector_score_qk(qc, qs, fmt, w, kc, ks, fmt, rows, nblk, Hs, ds,
+                                   rows_per_seq=rows)
+    s_b = oracle.selector_score(bf16_bits(qv.astype(np.float32)), w,
+                                bf16_bits(kv.astype(np.float32)), rows_per_seq=rows)
+    np.testing.assert_array_equal(s_q, s_b)
+    # BF16 queries through the general routine reduce to the plain score
+    s_plain = oracle.selector_score(q, w, kc, ks, fmt, rows_per_seq=rows, nblk=nblk)
+    np.testing.assert_array_equal(
+        oracle.selector_score_qk(q, None, "bf16", w, kc, ks, fmt, rows, nblk, Hs, ds,
+                                 rows_per_seq=rows), s_plain)
+
+
 def test_score_invariants():
     rng = np.random.default_rng(11)
     Hs, ds, nblk = 4, 64, 9
