@@ -170,6 +170,33 @@ spot_status spot_selector_score(const void *q_sel, const float *w, const void *k
                                 float *scores, void *stream);
 
 /*
+ * spot_selector_score_q -- block scores with quantized selector queries.
+ *
+ * Section 5.3 and Appendix G quantize the selector's queries as well as its
+ * key cache.  The score is that of spot_selector_score, with q_sel given as
+ * MX codes: qfmt SPOT_KFMT_MXFP4_G32 (E2M1 codes, two per byte, element 2i
+ * in the low nibble: uint8 [rows, h_s, d_s/2]) or SPOT_KFMT_MXFP8_G32 (E4M3
+ * codes, uint8 [rows, h_s, d_s]), with q_scale uint8 E8M0 [rows, h_s, d_s/32];
+ * qfmt SPOT_KFMT_BF16 is spot_selector_score itself (q_scale ignored).  Keys
+ * in any format.
+ *
+ * When queries and keys share one MX format, d_s == 128 and rows_per_seq is
+ * a multiple of 16 (prefill's query blocks), each head's tile product runs on
+ * the matrix cores' block-scaled instruction (v_mfma_scale_f32_16x16x128_f8f6f4:
+ * E2M1 or E4M3 operands, the E8M0 scales applied per 32-element group in
+ * hardware); otherwise the queries are decoded exactly in registers.  Both
+ * paths accumulate in FP32.
+ *
+ * Errors: SPOT_ERR_NULL (a pointer, q_scale, or k_scale for quantized keys),
+ * SPOT_ERR_SHAPE, SPOT_ERR_UNSUPPORTED (qfmt other than BF16/MXFP4/MXFP8, key
+ * format, head shape).
+ */
+spot_status spot_selector_score_q(const void *q_sel, const void *q_scale, int qfmt,
+                                  const float *w, const void *k_sel, const void *k_scale,
+                                  int kfmt, int n_seq, int rows_per_seq, int nblk, int h_s,
+                                  int d_s, const int32_t *n_valid, float *scores, void *stream);
+
+/*
  * spot_selector_score_tokens -- per-token selector, one value per block.
  *
  * Section 2.3: both selection modes rank a block by the largest per-token

@@ -93,6 +93,26 @@ spot_status spot_selector_score(const void* q_sel, const float* w, const void* k
                                         static_cast<hipStream_t>(stream)));
 }
 
+spot_status spot_selector_score_q(const void* q_sel, const void* q_scale, int qfmt,
+                                  const float* w, const void* k_sel, const void* k_scale,
+                                  int kfmt, int n_seq, int rows_per_seq, int nblk, int h_s,
+                                  int d_s, const int32_t* n_valid, float* scores, void* stream) {
+  if (qfmt == SPOT_KFMT_BF16)
+    return spot_selector_score(q_sel, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq, nblk, h_s,
+                               d_s, n_valid, scores, stream);
+  if (!q_sel || !w || !k_sel || !scores) return SPOT_ERR_NULL;
+  if (n_seq < 0 || rows_per_seq < 1 || nblk < 0 || h_s < 1 || d_s < 1) return SPOT_ERR_SHAPE;
+  if (qfmt != SPOT_KFMT_MXFP4_G32 && qfmt != SPOT_KFMT_MXFP8_G32) return SPOT_ERR_UNSUPPORTED;
+  if (!valid_kfmt(kfmt)) return SPOT_ERR_UNSUPPORTED;
+  if (!q_scale || (kfmt != SPOT_KFMT_BF16 && !k_scale)) return SPOT_ERR_NULL;
+  if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
+  if ((long long)n_seq * rows_per_seq > 0x7fffffffLL) return SPOT_ERR_SHAPE;
+  if (n_seq == 0 || nblk == 0) return SPOT_OK;
+  return from_hip(launch_selector_score_q(q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt, n_seq,
+                                          rows_per_seq, nblk, d_s, n_valid, scores,
+                                          static_cast<hipStream_t>(stream)));
+}
+
 spot_status spot_selector_score_tokens(const void* q_sel, const float* w, const void* k_tok,
                                        const void* k_scale, int kfmt, int n_seq,
                                        int rows_per_seq, int l_cap, int h_s, int d_s,

@@ -17,21 +17,24 @@ constexpr int kBlocksPerWG = kUnroll * kWavesPerWG;
 
 // grid: x = row (n_seq * rows_per_seq), y = chunk of kBlocksPerWG blocks;
 // wave w scores kUnroll consecutive blocks.
-template <int KFMT, int LPH>
-__global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__ q_sel,
+// QFMT: the queries' format (BF16, or MXFP4 / MXFP8 codes with q_scale).
+template <int KFMT, int LPH, int QFMT = SPOT_KFMT_BF16>
+__global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ q_sel,
                                                     const float* __restrict__ w,
                                                     const uint8_t* __restrict__ k_sel,
                                                     const uint8_t* __restrict__ k_scale,
                                                     int rows_per_seq, int nblk,
                                                     const int32_t* __restrict__ n_valid,
-                                                    float* __restrict__ scores) {
+                                                    float* __restrict__ scores,
+                                                    const uint8_t* __restrict__ q_scale) {
   const int row = blockIdx.x;
   const int j0 = blockIdx.y * kBlocksPerWG + (threadIdx.x >> 6) * kUnroll;
   int nv = n_valid ? n_valid[row] : nblk;
   nv = nv < 0 ? 0 : (nv > nblk ? nblk : nv);
   if (j0 >= nblk) return;
-  score_blocks<KFMT, LPH, kUnroll>(q_sel, w, k_sel, k_scale, row, row / rows_per_seq, nblk, nv,
-                                   j0, nblk, scores, nullptr, threadIdx.x & 63);
+  score_blocks<KFMT, LPH, kUnroll, QFMT>(q_sel, w, k_sel, k_scale, row, row / rows_per_seq, nblk,
+                                         nv, j0, nblk, scores, nullptr, threadIdx.x & 63,
+                                         q_scale);
 }
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -112,17 +115,130 @@ __global__ __launch_bounds__(256) void score_tile_kernel(
   }
 }
 
-template <int KFMT>
-hipError_t launch_fmt(int lph, dim3 grid, hipStream_t s, const uint16_t* q, const float* w,
+template <int KFMT, int QFMT = SPOT_KFMT_BF16>
+hipError_t launch_fmt(int lph, dim3 grid, hipStream_t s, const uint8_t* q, const float* w,
                       const uint8_t* k, const uint8_t* ks, int rows_per_seq, int nblk,
-                      const int32_t* nv, float* out) {
+                      const int32_t* nv, float* out, const uint8_t* qs = nullptr) {
   if (lph == 8)
-    hipLaunchKernelGGL((score_kernel<KFMT, 8>), grid, dim3(256), 0, s, q, w, k, ks, rows_per_seq,
-                       nblk, nv, out);
+    hipLaunchKernelGGL((score_kernel<KFMT, 8, QFMT>), grid, dim3(256), 0, s, q, w, k, ks,
+                       rows_per_seq, nblk, nv, out, qs);
   else
-    hipLaunchKernelGGL((score_kernel<KFMT, 16>), grid, dim3(256), 0, s, q, w, k, ks,
-                       rows_per_seq, nblk, nv, out);
+    hipLaunchKernelGGL((score_kernel<KFMT, 16, QFMT>), grid, dim3(256), 0, s, q, w, k, ks,
+                       rows_per_seq, nblk, nv, out, qs);
   return hipGetLastError();
+}
+
+// Row kernel for any key format with queries in format QFMT.
+template <int QFMT>
+hipError_t launch_row_q(int kfmt, int lph, dim3 grid, hipStream_t s, const uint8_t* q,
+                        const uint8_t* qs, const float* w, const uint8_t* k, const uint8_t* ks,
+                        int rows_per_seq, int nblk, const int32_t* nv, float* out) {
+  switch (kfmt) {
+    case SPOT_KFMT_BF16:
+      return launch_fmt<SPOT_KFMT_BF16, QFMT>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk, nv,
+                                              out, qs);
+    case SPOT_KFMT_INT4_G32:
+      return launch_fmt<SPOT_KFMT_INT4_G32, QFMT>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk,
+                                                  nv, out, qs);
+    case SPOT_KFMT_INT8_G32:
+      return launch_fmt<SPOT_KFMT_INT8_G32, QFMT>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk,
+                                                  nv, out, qs);
+    case SPOT_KFMT_MXFP8_G32:
+      return launch_fmt<SPOT_KFMT_MXFP8_G32, QFMT>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk,
+                                                   nv, out, qs);
+    default:
+      return launch_fmt<SPOT_KFMT_MXFP4_G32, QFMT>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk,
+                                                   nv, out, qs);
+  }
+}
+
+typedef int32_t i32x8_t __attribute__((ext_vector_type(8)));
+
+// Query-block x key-block tiles with queries and keys both in one MX format
+// (MXFP4 or MXFP8, one E8M0 scale per 32 elements) and d_s = 128: per head one
+// v_mfma_scale_f32_16x16x128_f8f6f4, the matrix cores applying both operands'
+// block scales.  Tiling as score_tile_kernel: one 16 x 16 tile per wave, 2 x 2
+// per workgroup.  A = Q_h: lane l holds query row l%16, dims 32(l/16) .. +31
+// of head h -- exactly one scale group, whose E8M0 byte the lane passes;
+// B = K_h^T likewise for key block l%16 (8-bit codes: see the operand
+// layout below).  D gives lane l rows 4(l/16)+i of key column l%16.
+template <int FMT>
+__global__ __launch_bounds__(256) void score_tile_mx_kernel(
+    const uint8_t* __restrict__ q, const uint8_t* __restrict__ qs, const float* __restrict__ w,
+    const uint8_t* __restrict__ k, const uint8_t* __restrict__ ks, int rows, int rows_per_seq,
+    int nblk, const int32_t* __restrict__ n_valid, float* __restrict__ scores) {
+  constexpr int HS = 4;                                        // 4 heads x 128 dims
+  constexpr bool FP4 = FMT == SPOT_KFMT_MXFP4_G32;
+  constexpr int RB = FP4 ? 256 : 512;                          // code bytes per row
+  constexpr int GB = FP4 ? 16 : 32;                            // code bytes per 32-group
+  constexpr int kFmtCode = FP4 ? 4 : 0;                        // E2M1 : E4M3
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r0 = blockIdx.x * 32 + (wave >> 1) * 16;
+  const int j0 = blockIdx.y * 32 + (wave & 1) * 16;
+  const int r16 = lane & 15, G = lane >> 4;
+  int nv[4];
+  int nv_max = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = r0 + 4 * G + i;
+    int v = r < rows ? (n_valid ? n_valid[r] : nblk) : 0;
+    v = v < 0 ? 0 : (v > nblk ? nblk : v);
+    nv[i] = v;
+    nv_max = max(nv_max, v);
+  }
+  nv_max = (int)wave_max_u((uint32_t)nv_max);
+  const int key = j0 + r16;
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  if (j0 < nv_max) {
+    // Rows past the end and keys past nblk read row / key 0 (in bounds);
+    // their results are never stored.
+    const int ra = min(r0 + r16, rows - 1);
+    const int seq = min(r0, rows - 1) / rows_per_seq;
+    const size_t kr = (size_t)seq * nblk + (key < nblk ? key : 0);
+    // Operand bytes of lane group G within a head: E2M1, 16 bytes = dims
+    // 32G .. 32G+31; E4M3, 32 bytes in two halves, dims 16G .. 16G+15 and
+    // 64+16G .. 64+16G+15 (the 8-bit operand layout).  Either way the lane's
+    // scale byte is that of the 32-dim group G.
+    const uint8_t* qa = q + (size_t)ra * RB + G * 16;
+    const uint8_t* kb = k + kr * RB + G * 16;
+    const float* wr = w + (size_t)(r0 + 4 * G) * HS;
+    i32x8_t A[HS], B[HS];
+    int sa[HS], sb[HS];
+#pragma unroll
+    for (int h = 0; h < HS; ++h) {
+      const u32x4 a0 = *reinterpret_cast<const u32x4*>(qa + h * 4 * GB);
+      const u32x4 b0 = *reinterpret_cast<const u32x4*>(kb + h * 4 * GB);
+      u32x4 a1 = {0u, 0u, 0u, 0u}, b1 = {0u, 0u, 0u, 0u};
+      if constexpr (!FP4) {
+        a1 = *reinterpret_cast<const u32x4*>(qa + h * 4 * GB + 64);
+        b1 = *reinterpret_cast<const u32x4*>(kb + h * 4 * GB + 64);
+      }
+      A[h] = i32x8_t{(int)a0[0], (int)a0[1], (int)a0[2], (int)a0[3],
+                     (int)a1[0], (int)a1[1], (int)a1[2], (int)a1[3]};
+      B[h] = i32x8_t{(int)b0[0], (int)b0[1], (int)b0[2], (int)b0[3],
+                     (int)b1[0], (int)b1[1], (int)b1[2], (int)b1[3]};
+      sa[h] = qs[(size_t)ra * 16 + h * 4 + G];
+      sb[h] = ks[kr * 16 + h * 4 + G];
+    }
+#pragma unroll
+    for (int h = 0; h < HS; ++h) {
+      const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
+      const f32x4_t sc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+          A[h], B[h], z, kFmtCode, kFmtCode, 0, sa[h], 0, sb[h]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float wi = r0 + 4 * G + i < rows ? wr[i * HS + h] : 0.f;
+        acc[i] = fmaf(wi, fmaxf(sc[i], 0.f), acc[i]);
+      }
+    }
+  }
+  if (key < nblk) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = r0 + 4 * G + i;
+      if (r < rows) scores[(size_t)r * nblk + key] = key < nv[i] ? acc[i] : -INFINITY;
+    }
+  }
 }
 
 }  // namespace
@@ -148,7 +264,7 @@ hipError_t launch_selector_score(const void* q_sel, const float* w, const void* 
   }
   dim3 grid(rows, (nblk + kBlocksPerWG - 1) / kBlocksPerWG);
   const int lph = d_s / 8;
-  auto q = static_cast<const uint16_t*>(q_sel);
+  auto q = static_cast<const uint8_t*>(q_sel);
   auto k = static_cast<const uint8_t*>(k_sel);
   auto ks = static_cast<const uint8_t*>(k_scale);
   switch (kfmt) {
@@ -168,6 +284,35 @@ hipError_t launch_selector_score(const void* q_sel, const float* w, const void* 
       return launch_fmt<SPOT_KFMT_MXFP4_G32>(lph, grid, s, q, w, k, ks, rows_per_seq, nblk,
                                              n_valid, scores);
   }
+}
+
+hipError_t launch_selector_score_q(const void* q_sel, const void* q_scale, int qfmt,
+                                   const float* w, const void* k_sel, const void* k_scale,
+                                   int kfmt, int n_seq, int rows_per_seq, int nblk, int d_s,
+                                   const int32_t* n_valid, float* scores, hipStream_t s) {
+  const int rows = n_seq * rows_per_seq;
+  auto q = static_cast<const uint8_t*>(q_sel);
+  auto qs = static_cast<const uint8_t*>(q_scale);
+  auto k = static_cast<const uint8_t*>(k_sel);
+  auto ks = static_cast<const uint8_t*>(k_scale);
+  if (qfmt == kfmt && (qfmt == SPOT_KFMT_MXFP4_G32 || qfmt == SPOT_KFMT_MXFP8_G32) &&
+      d_s == 128 && rows_per_seq > 1 && rows_per_seq % 16 == 0) {
+    const dim3 tgrid((rows + 31) / 32, (nblk + 31) / 32);
+    if (qfmt == SPOT_KFMT_MXFP4_G32)
+      hipLaunchKernelGGL((score_tile_mx_kernel<SPOT_KFMT_MXFP4_G32>), tgrid, dim3(256), 0, s, q,
+                         qs, w, k, ks, rows, rows_per_seq, nblk, n_valid, scores);
+    else
+      hipLaunchKernelGGL((score_tile_mx_kernel<SPOT_KFMT_MXFP8_G32>), tgrid, dim3(256), 0, s, q,
+                         qs, w, k, ks, rows, rows_per_seq, nblk, n_valid, scores);
+    return hipGetLastError();
+  }
+  const dim3 grid(rows, (nblk + kBlocksPerWG - 1) / kBlocksPerWG);
+  const int lph = d_s / 8;
+  if (qfmt == SPOT_KFMT_MXFP4_G32)
+    return launch_row_q<SPOT_KFMT_MXFP4_G32>(kfmt, lph, grid, s, q, qs, w, k, ks, rows_per_seq,
+                                             nblk, n_valid, scores);
+  return launch_row_q<SPOT_KFMT_MXFP8_G32>(kfmt, lph, grid, s, q, qs, w, k, ks, rows_per_seq,
+                                           nblk, n_valid, scores);
 }
 
 }  // namespace spot

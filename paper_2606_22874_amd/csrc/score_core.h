@@ -166,22 +166,63 @@ struct KeyLoad<SPOT_KFMT_MXFP8_G32> {
 // device scope (a reader in another workgroup of the same launch polls these
 // words: zero means not written yet).  Returns, in lane u < U, the score of
 // block j0 + u (-inf in the other lanes and past jend).
-template <int KFMT, int LPH, int U>
-__device__ __forceinline__ float score_blocks(const uint16_t* __restrict__ q_sel,
+// This lane's 8 query elements of row `row` (head lane / LPH, dims
+// 8*(lane % LPH) ..) as BF16 bits (qraw) and floats (qf).  Queries coded in
+// an MX format (E2M1 or E4M3 codes, one E8M0 scale per 32) are decoded
+// exactly; their values times a power of two fit BF16, so qraw holds them
+// exactly too.
+template <int QFMT>
+__device__ __forceinline__ void load_query(const uint8_t* __restrict__ q,
+                                           const uint8_t* __restrict__ q_scale, int row,
+                                           int lane, uint4& qraw, float (&qf)[8]) {
+  if constexpr (QFMT == SPOT_KFMT_BF16) {
+    qraw = *reinterpret_cast<const uint4*>(q + (size_t)row * 1024 + lane * 16);
+    qf[0] = bf16_lo(qraw.x); qf[1] = bf16_hi(qraw.x);
+    qf[2] = bf16_lo(qraw.y); qf[3] = bf16_hi(qraw.y);
+    qf[4] = bf16_lo(qraw.z); qf[5] = bf16_hi(qraw.z);
+    qf[6] = bf16_lo(qraw.w); qf[7] = bf16_hi(qraw.w);
+  } else {
+    static_assert(QFMT == SPOT_KFMT_MXFP4_G32 || QFMT == SPOT_KFMT_MXFP8_G32,
+                  "queries: BF16 or an MX format");
+    const float sf = e8m0_to_f32(q_scale[(size_t)row * 16 + (lane >> 2)]);
+    f32x2 v[4];
+    if constexpr (QFMT == SPOT_KFMT_MXFP4_G32) {
+      const uint32_t c = *reinterpret_cast<const uint32_t*>(q + (size_t)row * 256 + lane * 4);
+      v[0] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, sf, 0);
+      v[1] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, sf, 1);
+      v[2] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, sf, 2);
+      v[3] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, sf, 3);
+    } else {
+      const u32x2 c = *reinterpret_cast<const u32x2*>(q + (size_t)row * 512 + lane * 8);
+      v[0] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(c[0], sf, false);
+      v[1] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(c[0], sf, true);
+      v[2] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(c[1], sf, false);
+      v[3] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(c[1], sf, true);
+    }
+    uint32_t wd[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      qf[2 * i] = v[i][0];
+      qf[2 * i + 1] = v[i][1];
+      wd[i] = (__float_as_uint(v[i][0]) >> 16) | (__float_as_uint(v[i][1]) & 0xffff0000u);
+    }
+    qraw = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+  }
+}
+
+template <int KFMT, int LPH, int U, int QFMT = SPOT_KFMT_BF16>
+__device__ __forceinline__ float score_blocks(const void* __restrict__ q_sel,
                                              const float* __restrict__ w,
                                              const uint8_t* __restrict__ k_sel,
                                              const uint8_t* __restrict__ k_scale, int row,
                                              int seq, int nblk, int nv, int j0, int jend,
                                              float* __restrict__ scores,
-                                             uint32_t* __restrict__ rec, int lane) {
+                                             uint32_t* __restrict__ rec, int lane,
+                                             const uint8_t* __restrict__ q_scale = nullptr) {
   constexpr int kHeads = 64 / LPH;
-  // This lane's 8 query elements (head lane / LPH, dims 8*(lane % LPH) ..).
-  const uint4 qraw = *reinterpret_cast<const uint4*>(q_sel + (size_t)row * 512 + lane * 8);
+  uint4 qraw;
   float qf[8];
-  qf[0] = bf16_lo(qraw.x); qf[1] = bf16_hi(qraw.x);
-  qf[2] = bf16_lo(qraw.y); qf[3] = bf16_hi(qraw.y);
-  qf[4] = bf16_lo(qraw.z); qf[5] = bf16_hi(qraw.z);
-  qf[6] = bf16_lo(qraw.w); qf[7] = bf16_hi(qraw.w);
+  load_query<QFMT>(static_cast<const uint8_t*>(q_sel), q_scale, row, lane, qraw, qf);
   const float wh = w[(size_t)row * kHeads + lane / LPH];
 
   // Every slot loads (branch-free, so the loads of all U blocks fly

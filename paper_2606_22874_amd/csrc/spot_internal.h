@@ -131,6 +131,11 @@ hipError_t launch_selector_score(const void* q_sel, const float* w, const void* 
                                  int nblk, int h_s, int d_s, const int32_t* n_valid,
                                  float* scores, hipStream_t s);
 
+hipError_t launch_selector_score_q(const void* q_sel, const void* q_scale, int qfmt,
+                                   const float* w, const void* k_sel, const void* k_scale,
+                                   int kfmt, int n_seq, int rows_per_seq, int nblk, int d_s,
+                                   const int32_t* n_valid, float* scores, hipStream_t s);
+
 hipError_t launch_selector_score_tokens(const void* q_sel, const float* w, const void* k_tok,
                                         const void* k_scale, int kfmt, int n_seq,
                                         int rows_per_seq, int l_cap, int d_s,

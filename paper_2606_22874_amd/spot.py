@@ -28,7 +28,8 @@ KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2, "int8": 3, "mxfp8": 4}
 BLK = 64
 
 SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score",
-           "spot_selector_score_tokens", "spot_selector_project", "spot_selector_pool",
+           "spot_selector_score_q", "spot_selector_score_tokens", "spot_selector_project",
+           "spot_selector_pool",
            "spot_select_blocks",
            "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
            "spot_sparse_prefill", "spot_decode_step_workspace_bytes", "spot_decode_step",
@@ -64,6 +65,7 @@ def load(path: Optional[str] = None):
         L.spot_version.restype = ctypes.c_char_p
         L.spot_selector_score.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P, P]
         L.spot_selector_score_tokens.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P, P]
+        L.spot_selector_score_q.argtypes = [P, P, I, P, P, P, I, I, I, I, I, I, P, P, P]
         L.spot_selector_project.argtypes = [P, P, P, P, P, I, I, I, I, I, F, P, P, P, I, I, P]
         L.spot_selector_pool.argtypes = [P, P, I, I, I, I, P, P, I, P]
         L.spot_select_blocks.argtypes = [P, I, I, P, F, I, I, I, I, P, P, P, P]
@@ -79,7 +81,8 @@ def load(path: Optional[str] = None):
         L.spot_probe_stream_read.argtypes = [P, Z, P, P]
         L.spot_probe_stream_read.restype = ctypes.c_int32
         L.spot_probe_sink_words.restype = I
-        for name in ("spot_selector_score", "spot_selector_score_tokens", "spot_selector_project",
+        for name in ("spot_selector_score", "spot_selector_score_q", "spot_selector_score_tokens",
+                     "spot_selector_project",
                      "spot_selector_pool", "spot_select_blocks", "spot_sparse_decode",
                      "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step"):
             getattr(L, name).restype = ctypes.c_int32
@@ -153,6 +156,26 @@ def spot_selector_score(q_sel, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq, nbl
     _check("spot_selector_score", load().spot_selector_score(
         _ptr(q_sel), _ptr(w), _ptr(k_sel), _ptr(k_scale), f, n_seq, rows_per_seq, nblk, h_s,
         d_s, _ptr(n_valid), _ptr(scores), _stream(stream)))
+
+
+def spot_selector_score_q(q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq,
+                          nblk, h_s, d_s, n_valid, scores, stream=None):
+    rows = n_seq * rows_per_seq
+    qf = KFMT[qfmt] if isinstance(qfmt, str) else int(qfmt)
+    f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
+    if qf == 0:
+        _dev(q_sel, "q_sel", BF16, rows * h_s * d_s)
+    else:
+        _dev(q_sel, "q_sel", U8, rows * h_s * d_s // (2 if qf == 2 else 1))
+        _dev(q_scale, "q_scale", U8, rows * h_s * d_s // 32)
+    _dev(w, "w", F32, rows * h_s)
+    _sel_cache(k_sel, k_scale, f, n_seq * nblk, h_s, d_s, "k_sel")
+    if n_valid is not None:
+        _dev(n_valid, "n_valid", I32, rows)
+    _dev(scores, "scores", F32, rows * nblk)
+    _check("spot_selector_score_q", load().spot_selector_score_q(
+        _ptr(q_sel), _ptr(q_scale), qf, _ptr(w), _ptr(k_sel), _ptr(k_scale), f, n_seq,
+        rows_per_seq, nblk, h_s, d_s, _ptr(n_valid), _ptr(scores), _stream(stream)))
 
 
 def spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, h_s,

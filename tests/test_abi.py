@@ -64,6 +64,15 @@ def test_validation_errors_before_launch(lib):
     assert lib.spot_selector_score(nz, nz, nz, None, 0, 1, 1, 4, 8, 32, None, nz, None) == 3
     # quantized format without scales
     assert lib.spot_selector_score(nz, nz, nz, None, 1, 1, 1, 4, 8, 64, None, nz, None) == 1
+    # quantized queries: (q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt, n_seq, rows_per_seq,
+    # nblk, h_s, d_s, n_valid, scores, stream)
+    sq = lib.spot_selector_score_q
+    assert sq(nz, None, 2, nz, nz, nz, 2, 1, 1, 4, 4, 128, None, nz, None) == 1   # no q_scale
+    assert sq(nz, nz, 1, nz, nz, nz, 2, 1, 1, 4, 4, 128, None, nz, None) == 3     # INT4 queries
+    assert sq(nz, nz, 2, nz, nz, nz, 9, 1, 1, 4, 4, 128, None, nz, None) == 3     # key format
+    assert sq(nz, nz, 4, nz, nz, None, 3, 1, 1, 4, 4, 128, None, nz, None) == 1   # key scales
+    assert sq(nz, nz, 4, nz, nz, nz, 3, 1, 1, 4, 4, 64, None, nz, None) == 3      # 4 x 64
+    assert sq(nz, nz, 4, nz, nz, nz, 3, 0, 1, 4, 4, 128, None, nz, None) == 0
     # per-token scorer: (q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, h_s, d_s,
     # seq_len, scores, stream)
     tok = lib.spot_selector_score_tokens

@@ -356,3 +356,60 @@ def test_error_paths_leave_outputs_untouched():
     torch.cuda.synchronize()
     assert torch.all(out.float() == 7.0) and torch.all(lse == 7.0)
     assert torch.all(idx == 0) and int(cnt.item()) == 99
+
+
+# ------------------------------------------------------- quantized queries
+def _dev_scale(s, fmt):
+    return torch.from_numpy(np.ascontiguousarray(
+        s.view(np.uint16).view(np.int16) if fmt in ("int4", "int8") else s)).to(DEV)
+
+
+@pytest.mark.parametrize("B,nqb,Hs,ds,qfmt,kfmt", [
+    (2, 48, 4, 128, "mxfp4", "mxfp4"),     # block-scaled matrix cores
+    (1, 64, 4, 128, "mxfp8", "mxfp8"),     # block-scaled matrix cores
+    (2, 20, 4, 128, "mxfp4", "mxfp4"),     # 20 rows per sequence: row kernel
+    (2, 32, 8, 64, "mxfp8", "mxfp8"),      # d_s = 64: row kernel
+    (2, 32, 4, 128, "mxfp4", "bf16"),
+    (2, 32, 8, 64, "mxfp8", "int4"),
+    (1, 16, 4, 128, "mxfp4", "int8"),
+    (1, 16, 8, 64, "mxfp8", "mxfp4"),
+])
+def test_selector_score_quantized_queries(B, nqb, Hs, ds, qfmt, kfmt):
+    """Query-block x key-block scores with MX-coded queries, against the
+    oracle decoding the same codes (causal n_valid, several sequences)."""
+    print(f"[qscore] B={B} nqb={nqb} {Hs}x{ds} q={qfmt} k={kfmt}", flush=True)
+    rng = np.random.default_rng([B, nqb, Hs, ds])
+    q_sel, w, k_sel = synth.selector_prefill(rng, B, nqb, nqb, Hs, ds)
+    q_sel = q_sel.reshape(B * nqb, Hs, ds)
+    w = w.reshape(B * nqb, Hs)
+    n_valid = np.tile(np.arange(1, nqb + 1, dtype=np.int32), B)
+    qc, qs = synth.QUANTIZERS[qfmt](q_sel)
+    if kfmt == "bf16":
+        kc, ks = k_sel, None
+        kd, ksd = bf(k_sel), None
+    else:
+        kc, ks = synth.QUANTIZERS[kfmt](k_sel)
+        kd, ksd = torch.from_numpy(kc).to(DEV), _dev_scale(ks, kfmt)
+    s_o = oracle.selector_score_qk(qc, qs, qfmt, w, kc, ks, kfmt, B * nqb, nqb, Hs, ds,
+                                   rows_per_seq=nqb, n_valid=n_valid)
+    out = torch.empty((B * nqb, nqb), dtype=torch.float32, device=DEV)
+    spot.spot_selector_score_q(torch.from_numpy(qc).to(DEV), torch.from_numpy(qs).to(DEV), qfmt,
+                               f32(w), kd, ksd, kfmt, B, nqb, nqb, Hs, ds, i32(n_valid), out)
+    torch.cuda.synchronize()
+    assert_scores_close(out.cpu().numpy(), s_o)
+
+
+@pytest.mark.parametrize("qfmt", ["mxfp4", "mxfp8"])
+def test_decode_scores_quantized_queries(qfmt):
+    """Decode rows (one query per sequence) with MX-coded queries and the
+    128K-token workload's BF16 pooled keys."""
+    wl = workload(3, backbone=False)
+    qc, qs = synth.QUANTIZERS[qfmt](wl.q_sel)
+    s_o = oracle.selector_score_qk(qc, qs, qfmt, wl.w, wl.k_sel, None, "bf16", wl.B, wl.nblk,
+                                   wl.Hs, wl.ds, n_valid=wl.n_valid)
+    out = torch.empty((wl.B, wl.nblk), dtype=torch.float32, device=DEV)
+    spot.spot_selector_score_q(torch.from_numpy(qc).to(DEV), torch.from_numpy(qs).to(DEV), qfmt,
+                               f32(wl.w), bf(wl.k_sel), None, "bf16", wl.B, 1, wl.nblk, wl.Hs,
+                               wl.ds, i32(wl.n_valid), out)
+    torch.cuda.synchronize()
+    assert_scores_close(out.cpu().numpy(), s_o)
