@@ -343,6 +343,8 @@ def main():
         copies = bufs = None
         torch.cuda.empty_cache()
         result["prefill"] = prefill_leg(args, torch, spot, synth, dev, timed)
+        if not args.no_extra:
+            result["prefill"]["selector_formats"] = selector_format_leg(torch, spot, synth, dev)
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
@@ -387,6 +389,54 @@ def static_topk_leg(args, torch, spot, dev, timed, wl, copies, q, q_sel, w, seq_
             "budgets": res}
 
 
+def graph_ms(torch, fn, n=50, reps=5):
+    """Average time of fn(stream) captured n times in a HIP graph (no host
+    work between the kernels), over reps replays, in ms."""
+    for _ in range(3):
+        fn(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        st = torch.cuda.current_stream()
+        for _ in range(n):
+            fn(st)
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (n * reps)
+
+
+def selector_format_leg(torch, spot, synth, dev):
+    """Prefill selector tiles (one 32K-token sequence: 512 x 512 query-block x
+    key-block scores, causal) with the paper's 4 x 128 selector, BF16 and with
+    queries and keys both MXFP4 or MXFP8 on the block-scaled matrix cores."""
+    nqb, Hs, ds = 512, 4, 128
+    rng = np.random.default_rng(SEED_TOKENS)
+    q_sel, w, k_sel = synth.selector_prefill(rng, 1, nqb, nqb, Hs, ds)
+    q_sel = q_sel.reshape(nqb, Hs, ds)
+    w = torch.from_numpy(np.ascontiguousarray(w.reshape(nqb, Hs))).to(dev)
+    n_valid = torch.from_numpy(np.arange(1, nqb + 1, dtype=np.int32)).to(dev)
+    out = torch.empty((nqb, nqb), dtype=torch.float32, device=dev)
+    res = {}
+    qb, kb = spot.to_device_bf16(q_sel, dev), spot.to_device_bf16(k_sel, dev)
+    res["bf16"] = graph_ms(torch, lambda st: spot.spot_selector_score(
+        qb, w, kb, None, "bf16", 1, nqb, nqb, Hs, ds, n_valid, out, st)) * 1e3
+    for fmt in ("mxfp4", "mxfp8"):
+        qc, qs = synth.QUANTIZERS[fmt](q_sel)
+        kc, ks = synth.QUANTIZERS[fmt](k_sel)
+        t = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (qc, qs, kc, ks)]
+        res[fmt] = graph_ms(torch, lambda st, t=t, fmt=fmt: spot.spot_selector_score_q(
+            t[0], t[1], fmt, w, t[2], t[3], fmt, 1, nqb, nqb, Hs, ds, n_valid, out, st)) * 1e3
+    log("[bench] prefill selector 4x128: " + ", ".join(f"{k} {v:.1f} us" for k, v in res.items()))
+    return {"workload": "512 x 512 query-block x key-block selector tiles, 4 x 128 heads, causal",
+            "us": {k: round(v, 2) for k, v in res.items()}}
+
+
 def front_end_leg(args, torch, spot, synth, dev, timed, wl):
     """The selector front end of one decode step for the 4 sequences:
     projections of the new token's hidden state (Qwen3-8B width 4096, 4 x 128
@@ -418,30 +468,10 @@ def front_end_leg(args, torch, spot, synth, dev, timed, wl):
         pool(st)
 
     # These launches last a few microseconds, less than the binding's host
-    # overhead per call, so they are timed as HIP graphs of 50 back-to-back
-    # launches (no host work between kernels), replayed.
-    def graph_ms(fn, n=50, reps=5):
-        for _ in range(3):
-            fn(torch.cuda.current_stream())
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            st = torch.cuda.current_stream()
-            for _ in range(n):
-                fn(st)
-        g.replay()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(reps):
-            g.replay()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / (n * reps)
-
-    pms = graph_ms(project)
-    qms = graph_ms(pool)
-    ms = graph_ms(both)
+    # overhead per call, so they are timed as replayed HIP graphs.
+    pms = graph_ms(torch, project)
+    qms = graph_ms(torch, pool)
+    ms = graph_ms(torch, both)
     wbytes = wq.nbytes + wk.nbytes + ww.nbytes
     log(f"[bench] selector front end: project {pms * 1e3:.1f} us, pool {qms * 1e3:.1f} us")
     del cache, pooled
