@@ -10,7 +10,8 @@
  * as the block-sparse causal prefill over query blocks.
  * spot_selector_score_tokens replaces the first call when the selector cache
  * holds one key per token (block value = maximum of per-token scores,
- * Section 2.3).  Before them, spot_selector_project produces the step's
+ * Section 2.3), and spot_selector_score_q when the selector queries are
+ * stored in an MX format.  Before them, spot_selector_project produces the step's
  * selector query, weights and new cache key from the hidden state, and
  * spot_selector_pool refreshes the pooled key of the block it landed in.
  *

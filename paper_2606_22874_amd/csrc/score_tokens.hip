@@ -5,17 +5,19 @@
 //     sbar[r, b] = max_{t in b, t < seq_len[r]} sum_h w[r,h] ReLU(q[r,h,:] . k[seq(r), t, h, :]).
 //
 // The per-token cache is a streamed read (1 KiB per BF16 token), so the kernel
-// is bound by HBM and runs on the vector ALUs: one wavefront owns one 64-token
-// block.  Each lane reads the same 16 bytes (8 elements) of every token row,
-// so a load instruction moves one whole token row, coalesced.  Tokens are
+// is bound by HBM and runs on the vector ALUs: two wavefronts share a 64-token
+// block, 32 tokens each, and meet in LDS; the loads are non-temporal (read
+// once, they should not evict anything).  Each lane reads the same 16 bytes
+// (8 elements) of every token row, so a load instruction moves one whole
+// token row, coalesced.  Tokens are
 // taken 8 at a time; the 8 per-lane partial dot products are folded across
 // the LPH lanes of a head by a reduce-scatter (each butterfly step halves the
 // tokens a lane keeps and exchanges the other half with its partner), which
 // leaves every lane with the full head dot of one token in 7 exchanges where
 // per-token reductions would need 8 x log2(LPH).  The ReLU and weight follow,
 // then the head sum: inside a 16-lane row with one DPP move, across rows by a
-// second reduce-scatter over the block's 8 groups, once per block.  A final
-// wave maximum gives the block value.  Every exchange order is fixed, so the
+// second reduce-scatter over the wave's groups, once per wave.  A wave
+// maximum, then the maximum of the block's two waves, gives the block value.  Every exchange order is fixed, so the
 // result is deterministic.
 //
 // Token loads past the last visible token re-read that token (in bounds, in
