@@ -179,11 +179,133 @@ __global__ __launch_bounds__(256) void score_tokens_kernel(
   }
 }
 
+// 4-bit caches (INT4-g32, MXFP4-g32), 256 code bytes per token: a 16-byte
+// load per lane moves four tokens, so lane l takes token slot l/16 and the
+// 32-element scale group l%16 -- its 16 code bytes and its one scale.  The
+// lane keeps the 32 query elements of its group in registers.  Per load:
+// the group's dot, summed over the LG = d_s/32 lanes of a head (quad DPP
+// moves), ReLU and w_h, then over the heads of the 16-lane row by DPP row
+// rotations (rotating by 8, 4 (and 2) visits one lane of every head), which
+// leaves every lane of the row with its token's score.  Tokens past the last
+// visible one re-read it, as in score_tokens_kernel.
+template <int KFMT, int LG>
+__global__ __launch_bounds__(256) void score_tokens4_kernel(
+    const uint16_t* __restrict__ q_sel, const float* __restrict__ w,
+    const uint8_t* __restrict__ k_tok, const uint8_t* __restrict__ k_scale, int n_seq,
+    int rows_per_seq, int l_cap, int nblk, int runs, const int32_t* __restrict__ seq_len,
+    float* __restrict__ scores) {
+  constexpr int TPW = kTokTPW;               // tokens per wave
+  constexpr int NL = TPW / 4;                // loads per wave (4 tokens each)
+  constexpr int WPB = 64 / TPW;              // waves per block
+  constexpr int BPW = kTokWavesPerWG / WPB;  // blocks per workgroup
+  constexpr int kHeads = 16 / LG;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tq = lane >> 4, gi = lane & 15;
+  const int gsize = 8 * rows_per_seq;
+  const int id = blockIdx.x;
+  const int unit = (id / gsize) * 8 + (id & 7);
+  const int rr = (id % gsize) >> 3;
+  if (unit >= n_seq * runs) return;
+  const int seq = unit / runs;
+  const int j = (unit % runs) * BPW + wave / WPB;
+  const int row = seq * rows_per_seq + rr;
+  int len = seq_len ? seq_len[row] : l_cap;
+  len = len < 0 ? 0 : (len > l_cap ? l_cap : len);
+  const int t0 = j * 64 + (wave % WPB) * TPW;
+
+  float m = -INFINITY;
+  if (j < nblk && t0 < len) {
+    const int tlim = min(j * 64 + 64, len) - 1;
+    const size_t base = (size_t)seq * l_cap;
+    u32x4 code[NL];
+    uint32_t sc[NL];
+#pragma unroll
+    for (int u = 0; u < NL; ++u) {
+      const size_t t = base + min(t0 + 4 * u + tq, tlim);
+      code[u] = ld<true, u32x4>(k_tok + t * 256 + gi * 16);
+      if constexpr (KFMT == SPOT_KFMT_INT4_G32)
+        sc[u] = ld<true, uint16_t>(k_scale + (t * 16 + gi) * 2);
+      else
+        sc[u] = ld<true, uint8_t>(k_scale + t * 16 + gi);
+    }
+    float qf[32];
+    {
+      const u32x4* qp = reinterpret_cast<const u32x4*>(q_sel + (size_t)row * 512 + gi * 32);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const u32x4 x = qp[c];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          qf[8 * c + 2 * i] = bf16_lo(x[i]);
+          qf[8 * c + 2 * i + 1] = bf16_hi(x[i]);
+        }
+      }
+    }
+    const float wh = w[(size_t)row * kHeads + gi / LG];
+#pragma unroll
+    for (int u = 0; u < NL; ++u) {
+      float a = 0.f;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t wd = code[u][c];
+        if constexpr (KFMT == SPOT_KFMT_INT4_G32) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            a = fmaf(qf[8 * c + i], (float)((int)(wd << (28 - 4 * i)) >> 28), a);
+        } else {
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const f32x2 v = b == 0   ? __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd, 1.0f, 0)
+                            : b == 1 ? __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd, 1.0f, 1)
+                            : b == 2 ? __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd, 1.0f, 2)
+                                     : __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd, 1.0f, 3);
+            a = fmaf(qf[8 * c + 2 * b], v[0], a);
+            a = fmaf(qf[8 * c + 2 * b + 1], v[1], a);
+          }
+        }
+      }
+      a *= KFMT == SPOT_KFMT_INT4_G32 ? f16_to_f32((uint16_t)sc[u]) : e8m0_to_f32(sc[u]);
+      a += dpp_f<kDppQuadXor1>(a);
+      if constexpr (LG == 4) a += dpp_f<kDppQuadXor2>(a);
+      float d = wh * fmaxf(a, 0.f);
+      d += dpp_f<0x128>(d);                  // row_ror:8
+      d += dpp_f<0x124>(d);                  // row_ror:4
+      if constexpr (LG == 2) d += dpp_f<0x122>(d);   // row_ror:2
+      m = fmaxf(m, d);
+    }
+    m = wave_max(m);
+  }
+  float* dst = scores + (size_t)row * nblk + j;
+  if constexpr (WPB == 1) {
+    if (lane == 0 && j < nblk) *dst = m;
+  } else {
+    __shared__ float part[kTokWavesPerWG];
+    if (lane == 0) part[wave] = m;
+    __syncthreads();
+    if (lane == 0 && wave % WPB == 0 && j < nblk) {
+      float b = part[wave];
+#pragma unroll
+      for (int i = 1; i < WPB; ++i) b = fmaxf(b, part[wave + i]);
+      *dst = b;
+    }
+  }
+}
+
 template <int KFMT>
 hipError_t launch_tokens_fmt(int lph, dim3 grid, hipStream_t s, const uint16_t* q,
                              const float* w, const uint8_t* k, const uint8_t* ks, int n_seq,
                              int rows_per_seq, int l_cap, int nblk, int runs,
                              const int32_t* seq_len, float* out) {
+  if constexpr (KFMT == SPOT_KFMT_INT4_G32 || KFMT == SPOT_KFMT_MXFP4_G32) {
+    // lanes per head of the 4-bit kernel: d_s / 32 = lph / 4
+    if (lph == 8)
+      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 2>), grid, dim3(256), 0, s, q, w, k, ks,
+                         n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+    else
+      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 4>), grid, dim3(256), 0, s, q, w, k, ks,
+                         n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+    return hipGetLastError();
+  }
   if (lph == 8)
     hipLaunchKernelGGL((score_tokens_kernel<KFMT, 8, kTokTPW>), grid, dim3(256), 0, s, q, w, k, ks,
                        n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
