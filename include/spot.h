@@ -153,10 +153,12 @@ spot_status spot_selector_pool(const void *k_tok, void *k_pool, int n_seq, int l
  *  w        device, float [n_seq*rows_per_seq, h_s]
  *  k_sel    device, selector key cache, [n_seq, nblk, h_s, d_s] BF16 for
  *           SPOT_KFMT_BF16; for the 4-bit formats uint8 [n_seq, nblk, h_s, d_s/2]
- *           with element 2i in the low nibble of byte i
- *  k_scale  device, NULL for BF16; else [n_seq, nblk, h_s, d_s/32] of FP16
- *           (INT4: value = code * scale, code the nibble as two's complement)
- *           or uint8 E8M0 (MXFP4: value = E2M1(code) * 2^(e - 127))
+ *           with element 2i in the low nibble of byte i; for the 8-bit
+ *           formats uint8 [n_seq, nblk, h_s, d_s], one code per byte
+ *  k_scale  device, NULL for BF16; else [n_seq, nblk, h_s, d_s/32]: FP16 for
+ *           INT4 / INT8 (value = code * scale, the code a two's-complement
+ *           nibble / byte), uint8 E8M0 for MXFP4 / MXFP8 (value =
+ *           E2M1(code) or E4M3(code) times 2^(e - 127))
  *  n_valid  device int32 [rows] (blocks j >= n_valid[r] do not exist and score
  *           -inf) or NULL (every block valid)
  *  scores   device, float [rows, nblk]  (output)
@@ -212,10 +214,11 @@ spot_status spot_selector_score_q(const void *q_sel, const void *q_scale, int qf
  *  q_sel    device, BF16 [n_seq*rows_per_seq, h_s, d_s]
  *  w        device, float [n_seq*rows_per_seq, h_s]
  *  k_tok    device, per-token selector key cache, [n_seq, l_cap, h_s, d_s] BF16
- *           for SPOT_KFMT_BF16; for the 4-bit formats uint8
- *           [n_seq, l_cap, h_s, d_s/2], element 2i in the low nibble of byte i
- *  k_scale  device, NULL for BF16; else [n_seq, l_cap, h_s, d_s/32] FP16 (INT4)
- *           or uint8 E8M0 (MXFP4), as for spot_selector_score
+ *           for SPOT_KFMT_BF16; the quantized formats as for
+ *           spot_selector_score with one row per token instead of per block
+ *           (4-bit: [n_seq, l_cap, h_s, d_s/2] uint8; 8-bit: [.., d_s] uint8)
+ *  k_scale  device, NULL for BF16; else [n_seq, l_cap, h_s, d_s/32] (FP16 for
+ *           INT4 / INT8, uint8 E8M0 for MXFP4 / MXFP8)
  *  l_cap    tokens per sequence in the cache, a multiple of 64; nblk = l_cap/64
  *  seq_len  device int32 [rows]: row r sees tokens t < seq_len[r] (clamped to
  *           [0, l_cap]); NULL means every token is visible
