@@ -19,7 +19,9 @@
  *  - Pointers named as device arrays are caller-owned device memory; the
  *    library never allocates, frees, or synchronises, and keeps no state of
  *    its own between calls (the decode workspace carries completion counters
- *    that each call returns to zero).  Arrays are C-contiguous.  BF16 arrays hold bfloat16
+ *    that each call returns to zero).  Arrays are C-contiguous and start on
+ *    a 16-byte boundary (as every hipMalloc and torch allocation does; the
+ *    kernels read them with 16-byte vector loads).  BF16 arrays hold bfloat16
  *    values (2 bytes each).  A KV block is 64 consecutive tokens; the
  *    pooled selector key cache holds one key per block, the per-token cache
  *    one key per token.
