@@ -113,6 +113,8 @@ def _dev(t: torch.Tensor, name: str, dtypes, numel: Optional[int] = None):
         raise ValueError(f"{name} must be a device tensor")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+    if t.data_ptr() % 16:
+        raise ValueError(f"{name} must start on a 16-byte boundary")
     if dtypes is not None and t.dtype not in dtypes:
         raise ValueError(f"{name}: dtype {t.dtype} not in {dtypes}")
     if numel is not None and t.numel() < numel:
