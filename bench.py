@@ -5,14 +5,16 @@ One step = selector scoring of every KV block + dual top-p/top-K selection +
 block-sparse GQA decode attention, for all sequences of one layer, on the
 Qwen3-8B-shaped 128K-token workload (batch 4, 32 query / 8 KV heads, d = 128,
 2048 blocks of 64 tokens, p = 0.95, K_max = 128, 1 sink + 2 recent blocks).
-The headline value times spot_decode_step (all three stages in one launch);
-the three separate calls are timed too, with their per-stage times.
+The headline value times spot_decode_step (all three stages in one launch):
+the median of --repeats (5) runs of K back-to-back steps, each timed with HIP
+events on the launch stream.  The three separate calls are timed too, with
+their per-stage times.
 
 Inputs are resident in HBM before timing starts.  The timed loop rotates
 over NCOPY distinct copies of the KV cache and selector cache so that the
 256 MB last-level cache cannot serve repeated steps.  Prints one JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--repeats R] [--gpus 1] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -20,6 +22,7 @@ import argparse
 import hashlib
 import json
 import os
+import platform
 import re
 import sys
 import time
@@ -37,6 +40,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--copies", type=int, default=4)
+    ap.add_argument("--repeats", type=int, default=5,
+                    help="timed repeats of --steps steps; the headline is their median")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-dense", action="store_true", help="skip the dense decode baseline")
@@ -195,8 +200,9 @@ def main():
     torch.cuda.synchronize()
     counts = cnt.cpu().numpy()
 
-    log(f"[bench] timing {args.steps} steps")
-    ms = timed(step, args.steps)
+    log(f"[bench] timing {args.repeats} x {args.steps} steps")
+    rep_ms = [timed(step, args.steps) for _ in range(max(1, args.repeats))]
+    ms = float(np.median(rep_ms))
     sep_ms = timed(separate_step, args.steps)
     # Per-stage averages (same launch stream, back to back, rotating copies).
     attn_ms = timed(attend, args.steps)
@@ -244,6 +250,8 @@ def main():
                         "selector 8x64 pooled per 64-token block; p=0.95 K_max=128 sink 1 recent 2)",
             "selector_cache": args.fmt,
             "copies_rotated": args.copies,
+            "repeats": len(rep_ms),
+            "repeat_us_per_step": [round(r * 1e3, 2) for r in rep_ms],
             "mean_selected_blocks": float(counts.mean()),
             "bytes_per_step": step_bytes,
             "step_hbm_gbs": round(step_gbs, 1),
@@ -650,7 +658,7 @@ def prefill_leg(args, torch, spot, synth, dev, timed):
     tflops = mfma_flops / (attn_ms * 1e-3) / 1e12
     log(f"[bench] prefill: {step_ms:.3f} ms/layer; attention {attn_ms:.3f} ms "
         f"({tflops:.0f} TFLOP/s), score {score_ms * 1e3:.1f} us, select {select_ms * 1e3:.1f} us")
-    return {
+    res = {
         "workload": "prefill L=32768 B=1 (Qwen3-32B-shaped layer: 64 q / 8 kv heads, d=128; "
                     "selector 8x64 pooled per 64-token block; p=0.9 K_max=64 sink 1 recent 2)",
         "value": round(pw.L / (step_ms * 1e-3), 1), "unit": "tokens/s",
@@ -666,6 +674,63 @@ def prefill_leg(args, torch, spot, synth, dev, timed):
             "flops_per_launch": mfma_flops, "avg_launch_us": round(attn_ms * 1e3, 1),
         },
     }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = prefill_cpu_baseline(pw)
+    return res
+
+
+# Query blocks of the 512-block prefill layer on which the oracle is timed:
+# the first blocks (almost no history), powers of two minus one and plus
+# zero across the range, and the last blocks (the K_max cap binds).
+PREFILL_SAMPLE_QB = (0, 1, 2, 3, 31, 63, 64, 127, 191, 255, 256, 319, 383, 447, 510, 511)
+
+
+def prefill_cpu_baseline(pw):
+    """The FP64 oracle's prefill layer on the host cores: selector scores and
+    selection for all query blocks, attention on a fixed sample of query
+    blocks (all 64 heads), extrapolated to the layer."""
+    import oracle
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    oracle.set_threads(cores)
+    t0 = time.time()
+    s = oracle.selector_score(pw.q_sel, pw.w, pw.k_sel, rows_per_seq=pw.nblk,
+                              n_valid=pw.n_valid).astype(np.float32)
+    idx, cnt, _ = oracle.select_blocks(s.astype(np.float64), pw.rule, pw.n_valid)
+    sel_s = time.time() - t0
+    rows = np.asarray([r for r in PREFILL_SAMPLE_QB if r < pw.nblk], np.int32)
+    log(f"[bench] prefill cpu baseline: oracle attention on {rows.size} query blocks, "
+        f"{cores} threads")
+    t0 = time.time()
+    oracle.sparse_prefill(pw.q, pw.k, pw.v, idx, cnt, pw.sm_scale, rows)
+    attn_s = time.time() - t0
+    per_qb = attn_s / rows.size
+    per_tile = attn_s / max(1, int(cnt[rows].sum()))
+    layer_s = sel_s + per_tile * int(cnt.sum())
+    return {"value": round(pw.L / layer_s, 2), "unit": "tokens/s", "cores": oracle.get_threads(),
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "sample": f"selector scores + selection of all {pw.nblk} query blocks, then "
+                      f"attention (64 heads, FP64 C with OpenMP) on query blocks "
+                      f"{rows.tolist()}; the layer time extrapolates the sample's time per "
+                      f"selected tile to the layer's {int(cnt.sum())} tiles",
+            "selection_s": round(sel_s, 3),
+            "attention_s_per_qblock": round(per_qb, 4),
+            "attention_s_x512": round(per_qb * 512, 1),
+            "layer_s_extrapolated": round(layer_s, 1)}
+
+
+def cpu_model():
+    """The host processor's model name, as /proc/cpuinfo (and lscpu) give it."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
 
 
 def cpu_baseline(wl, budget_s):
@@ -700,7 +765,7 @@ def cpu_baseline(wl, budget_s):
             break
     oracle.set_threads(cores)
     return {"value": round(n / el, 4), "unit": "steps/s", "cores": used,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"{n} full decode steps (score + select + sparse attention, all 4 "
                       f"sequences) of the same workload, FP64 C with OpenMP",
             "single_thread_value": round(n1 / el1, 4),

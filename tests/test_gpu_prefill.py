@@ -15,6 +15,8 @@ import torch
 import oracle
 from paper_2606_22874_amd import spot, synth
 
+from selcheck import check_all
+
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
 
@@ -126,9 +128,27 @@ def c5():
     return _c5["wl"], _c5["idx"], _c5["cnt"]
 
 
+def test_prefill_full_size_selection_all_rows():
+    """Selector scores and the dual top-p / top-K selection of every one of
+    the 512 query blocks of the 32K-token layer, on the GPU, against the
+    oracle's scores and selection."""
+    wl, idx_o, cnt_o = c5()
+    nqb, rule = wl.nblk, wl.rule
+    s_o = oracle.selector_score(wl.q_sel, wl.w, wl.k_sel, rows_per_seq=nqb,
+                                n_valid=wl.n_valid).astype(np.float32)
+    s_g = spot.selector_score(bf(wl.q_sel), torch.from_numpy(wl.w).to(DEV), bf(wl.k_sel),
+                              rows_per_seq=nqb, n_valid=i32(wl.n_valid), nblk=nqb)
+    idx_g, cnt_g, _ = spot.select_blocks(s_g, rule, i32(wl.n_valid))
+    torch.cuda.synchronize()
+    print("[prefill] selection of all rows", check_all(
+        s_o, wl.n_valid, rule, idx_o, cnt_o, idx_g.cpu().numpy(), cnt_g.cpu().numpy()),
+        flush=True)
+
+
 def test_prefill_full_size_sampled_rows():
     """The 32K-token, 64/8-head layer with the oracle's selection; sampled rows
-    cover the first query blocks, the K_max-capped middle and the last block."""
+    are a fixed stratified set over the layer (first query blocks, powers of
+    two, the K_max-capped end), capped rows and a few random ones."""
     wl, idx, cnt = c5()
     assert cnt.max() == wl.rule.k_max          # the cap binds on some rows
     out_g, lse_g = spot.sparse_prefill(bf(wl.q), bf(wl.k), bf(wl.v), i32(idx), i32(cnt),
@@ -137,7 +157,8 @@ def test_prefill_full_size_sampled_rows():
     nqb = wl.nblk
     capped = np.flatnonzero(cnt == wl.rule.k_max)
     rng = np.random.default_rng(9)
-    rows = np.unique(np.concatenate([[0, 1, 2, 63, 64, nqb - 1], capped[:2],
+    stratified = [0, 1, 2, 3, 31, 63, 64, 127, 191, 255, 256, 319, 383, 447, 510, 511]
+    rows = np.unique(np.concatenate([stratified, [nqb - 1], capped[:2],
                                      rng.choice(nqb, 4, replace=False)])).astype(np.int32)
     print(f"[prefill] full size, rows {rows.tolist()}", flush=True)
     out_o, lse_o = oracle.sparse_prefill(wl.q, wl.k, wl.v, idx, cnt, wl.sm_scale, rows)
