@@ -68,6 +68,7 @@ STEP_SOURCES = ("step.hip", "decode_core.h", "score_core.h", "select_core.h", "s
 TOKENS_PROFILE = os.path.join(ROOT, "profiles", "score_tokens_L131072_B4.md")
 TOKENS_SOURCES = ("score_tokens.hip", "score_core.h", "spot_internal.h")
 SEED_TOKENS = 20260611
+QUANT_TOKENS = 2048      # tokens per sequence quantized for the per-token format timings
 
 
 def source_hash(files=STEP_SOURCES) -> str:
@@ -508,6 +509,7 @@ def per_token_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, 
     ws_ = torch.from_numpy(w_tok).to(dev)
     ktoks = [spot.to_device_bf16(k_tok, dev) for _ in range(2)]
     tok_bytes = k_tok.nbytes
+    k_head = np.ascontiguousarray(k_tok[:, :QUANT_TOKENS])
     del k_tok
     nblk = L // 64
     scores = torch.empty((B, nblk), dtype=torch.float32, device=dev)
@@ -534,6 +536,40 @@ def per_token_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, 
     log(f"[bench] per-token selector: score {sms * 1e3:.1f} us ({gbs:.0f} GB/s), "
         f"step {ms * 1e3:.1f} us")
     del ktoks
+    torch.cuda.empty_cache()
+
+    # The scorer alone over quantized per-token caches: the first QUANT_TOKENS
+    # tokens of each sequence quantized and repeated to L tokens (the encoders
+    # run on the host and would take minutes over all 512 Mi elements); four
+    # copies rotated, 0.6-1.1 GB in all, so the last-level cache cannot serve
+    # repeated launches.
+    fmts = {}
+    for fmt in ("int4", "mxfp4", "int8", "mxfp8"):
+        c, sc = synth.QUANTIZERS[fmt](k_head)
+        reps = L // QUANT_TOKENS
+        c = np.tile(c, (1, reps, 1, 1))
+        sc = np.tile(sc.view(np.int16) if fmt in ("int4", "int8") else sc, (1, reps, 1, 1))
+        nbytes = c.nbytes + sc.nbytes
+        c0 = torch.from_numpy(c).to(dev)
+        s0 = torch.from_numpy(sc).to(dev)
+        del c, sc
+        qcopies = [(c0, s0)] + [(c0.clone(), s0.clone()) for _ in range(3)]
+
+        def qscore(i, fmt=fmt, qcopies=qcopies):
+            kc, kscale = qcopies[i % len(qcopies)]
+            spot.spot_selector_score_tokens(qs, ws_, kc, kscale, fmt, B, 1, L, Hs, ds, seq_len,
+                                            scores, stream)
+
+        for i in range(args.warmup):
+            qscore(i)
+        qms = timed(qscore, args.steps)
+        qgbs = nbytes / (qms * 1e-3) / 1e9
+        kern = "score_tokens4_kernel" if fmt in ("int4", "mxfp4") else "score_tokens_kernel"
+        fmts[fmt] = {"kernel": kern, "us": round(qms * 1e3, 2), "bytes_per_launch": int(nbytes),
+                     "achieved_gbs": round(qgbs, 1), "frac": round(qgbs / HBM_PEAK_GBS, 4)}
+        log(f"[bench] per-token {fmt} scorer: {qms * 1e3:.1f} us ({qgbs:.0f} GB/s)")
+        del qcopies, c0, s0
+        torch.cuda.empty_cache()
     return {
         "workload": f"decode L={L} B={B}, per-token selector cache {Hs}x{ds} BF16 "
                     f"({tok_bytes >> 20} MiB), block value = max over its 64 tokens; "
@@ -550,6 +586,7 @@ def per_token_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, 
             "avg_launch_us": round(sms * 1e3, 2),
             "traffic": measured_traffic(TOKENS_PROFILE, TOKENS_SOURCES),
         },
+        "quantized_scorer": fmts,
     }
 
 

@@ -24,6 +24,22 @@ __device__ __forceinline__ float e8m0_to_f32(uint32_t e) {
   return e ? __uint_as_float(e << 23) : __uint_as_float(0x00400000u);
 }
 
+// Eight signed 4-bit codes of one word, nibble i (bits 4i .. 4i+3) holding
+// element i, as floats scaled by 1/16: v_cvt_off_f32_i4 turns the low four
+// bits of its operand into n / 16 (exact), and reading byte b of the word and
+// of the word rotated right by 4 picks nibbles 2b and 2b+1 with a byte select
+// on the operand, so the eight values cost nine instructions.  A sum of
+// q_i * (n_i / 16) scaled by 16 equals the sum of q_i * n_i bit for bit
+// (scaling by a power of two commutes with every rounding step).
+__device__ __forceinline__ void int4_sixteenths(uint32_t w, float (&v)[8]) {
+  const uint32_t odd = __builtin_amdgcn_alignbit(w, w, 4);
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    v[2 * b] = __builtin_amdgcn_cvt_off_f32_i4((int)((w >> (8 * b)) & 0xffu));
+    v[2 * b + 1] = __builtin_amdgcn_cvt_off_f32_i4((int)((odd >> (8 * b)) & 0xffu));
+  }
+}
+
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -69,13 +85,12 @@ struct KeyLoad<SPOT_KFMT_INT4_G32> {
     scale = ld<NT, uint16_t>(ks + (blk * 16 + (lane >> 2)) * 2);
   }
   __device__ __forceinline__ float dot(const uint4&, const float* qf) const {
+    float v[8];
+    int4_sixteenths(codes, v);
     float a = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int code = (int)(codes << (28 - 4 * i)) >> 28;  // sign-extend nibble i
-      a = fmaf(qf[i], (float)code, a);
-    }
-    return a * f16_to_f32(scale);
+    for (int i = 0; i < 8; ++i) a = fmaf(qf[i], v[i], a);
+    return a * 16.f * f16_to_f32(scale);
   }
 };
 

@@ -249,9 +249,10 @@ __global__ __launch_bounds__(256) void score_tokens4_kernel(
       for (int c = 0; c < 4; ++c) {
         const uint32_t wd = code[u][c];
         if constexpr (KFMT == SPOT_KFMT_INT4_G32) {
+          float v[8];
+          int4_sixteenths(wd, v);
 #pragma unroll
-          for (int i = 0; i < 8; ++i)
-            a = fmaf(qf[8 * c + i], (float)((int)(wd << (28 - 4 * i)) >> 28), a);
+          for (int i = 0; i < 8; ++i) a = fmaf(qf[8 * c + i], v[i], a);
         } else {
 #pragma unroll
           for (int b = 0; b < 4; ++b) {
@@ -264,7 +265,7 @@ __global__ __launch_bounds__(256) void score_tokens4_kernel(
           }
         }
       }
-      a *= KFMT == SPOT_KFMT_INT4_G32 ? f16_to_f32((uint16_t)sc[u]) : e8m0_to_f32(sc[u]);
+      a *= KFMT == SPOT_KFMT_INT4_G32 ? 16.f * f16_to_f32((uint16_t)sc[u]) : e8m0_to_f32(sc[u]);
       a += dpp_f<kDppQuadXor1>(a);
       if constexpr (LG == 4) a += dpp_f<kDppQuadXor2>(a);
       float d = wh * fmaxf(a, 0.f);
