@@ -5,8 +5,9 @@
 //     sbar[r, b] = max_{t in b, t < seq_len[r]} sum_h w[r,h] ReLU(q[r,h,:] . k[seq(r), t, h, :]).
 //
 // The per-token cache is a streamed read (1 KiB per BF16 token), so the kernel
-// is bound by HBM and runs on the vector ALUs: two wavefronts share a 64-token
-// block, 32 tokens each, and meet in LDS; the loads are non-temporal (read
+// is bound by HBM and runs on the vector ALUs: with BF16 keys two wavefronts
+// share a 64-token block, 32 tokens each, and meet in LDS (quantized keys: one
+// wave per block); the loads are non-temporal (read
 // once, they should not evict anything).  Each lane reads the same 16 bytes
 // (8 elements) of every token row, so a load instruction moves one whole
 // token row, coalesced.  Tokens are
@@ -17,8 +18,8 @@
 // per-token reductions would need 8 x log2(LPH).  The ReLU and weight follow,
 // then the head sum: inside a 16-lane row with one DPP move, across rows by a
 // second reduce-scatter over the wave's groups, once per wave.  A wave
-// maximum, then the maximum of the block's two waves, gives the block value.  Every exchange order is fixed, so the
-// result is deterministic.
+// maximum, then the maximum over the block's waves, gives the block value.
+// Every exchange order is fixed, so the result is deterministic.
 //
 // Token loads past the last visible token re-read that token (in bounds, in
 // cache); a duplicate of a visible token cannot change a maximum, so ragged
@@ -29,7 +30,13 @@ namespace spot {
 namespace {
 
 constexpr int kTokWavesPerWG = 4;
-constexpr int kTokTPW = 32;         // tokens per wave (two waves per block)
+constexpr int kTokTPW = 32;         // tokens per wave, BF16 keys (two waves per block)
+// Quantized keys decode with more ALU work per byte, and a wave that owns a
+// whole block (16 loads of 4 tokens in flight, 4-bit) overlaps its decode with
+// the loads of the others better than two half-block waves: measured 26.5 vs
+// 30.8 us (INT4) and 24.3 vs 28.4 us (MXFP4) over 4 x 131072 tokens.
+constexpr int kTok8TPW = 64;        // tokens per wave, 8-bit keys (one wave per block)
+constexpr int kTok4TPW = 64;        // tokens per wave, 4-bit keys (one wave per block)
 
 // Butterfly exchange partner moves, all DPP inside a 16-lane row: the partner
 // differs from the lane in the bit being folded (half-mirror 7 - i flips bit
@@ -188,13 +195,12 @@ __global__ __launch_bounds__(256) void score_tokens_kernel(
 // rotations (rotating by 8, 4 (and 2) visits one lane of every head), which
 // leaves every lane of the row with its token's score.  Tokens past the last
 // visible one re-read it, as in score_tokens_kernel.
-template <int KFMT, int LG>
+template <int KFMT, int LG, int TPW>
 __global__ __launch_bounds__(256) void score_tokens4_kernel(
     const uint16_t* __restrict__ q_sel, const float* __restrict__ w,
     const uint8_t* __restrict__ k_tok, const uint8_t* __restrict__ k_scale, int n_seq,
     int rows_per_seq, int l_cap, int nblk, int runs, const int32_t* __restrict__ seq_len,
     float* __restrict__ scores) {
-  constexpr int TPW = kTokTPW;               // tokens per wave
   constexpr int NL = TPW / 4;                // loads per wave (4 tokens each)
   constexpr int WPB = 64 / TPW;              // waves per block
   constexpr int BPW = kTokWavesPerWG / WPB;  // blocks per workgroup
@@ -292,26 +298,42 @@ __global__ __launch_bounds__(256) void score_tokens4_kernel(
   }
 }
 
+// Grid of a per-token launch: (n_seq x runs of the workgroup's blocks),
+// rounded up to a multiple of 8 units, times the query rows of a sequence.
+template <int TPW>
+int tok_runs(int nblk) {
+  constexpr int kBlocksPerWG = kTokWavesPerWG * TPW / 64;
+  return (nblk + kBlocksPerWG - 1) / kBlocksPerWG;
+}
+inline dim3 tok_grid(int n_seq, int runs, int rows_per_seq) {
+  const long long units = (long long)n_seq * runs;
+  return dim3((unsigned)(((units + 7) / 8) * 8 * rows_per_seq));
+}
+
 template <int KFMT>
-hipError_t launch_tokens_fmt(int lph, dim3 grid, hipStream_t s, const uint16_t* q,
-                             const float* w, const uint8_t* k, const uint8_t* ks, int n_seq,
-                             int rows_per_seq, int l_cap, int nblk, int runs,
-                             const int32_t* seq_len, float* out) {
+hipError_t launch_tokens_fmt(int lph, hipStream_t s, const uint16_t* q, const float* w,
+                             const uint8_t* k, const uint8_t* ks, int n_seq, int rows_per_seq,
+                             int l_cap, int nblk, const int32_t* seq_len, float* out) {
   if constexpr (KFMT == SPOT_KFMT_INT4_G32 || KFMT == SPOT_KFMT_MXFP4_G32) {
     // lanes per head of the 4-bit kernel: d_s / 32 = lph / 4
+    const int runs = tok_runs<kTok4TPW>(nblk);
+    const dim3 grid = tok_grid(n_seq, runs, rows_per_seq);
     if (lph == 8)
-      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 2>), grid, dim3(256), 0, s, q, w, k, ks,
-                         n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 2, kTok4TPW>), grid, dim3(256), 0, s, q, w,
+                         k, ks, n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
     else
-      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 4>), grid, dim3(256), 0, s, q, w, k, ks,
-                         n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 4, kTok4TPW>), grid, dim3(256), 0, s, q, w,
+                         k, ks, n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
     return hipGetLastError();
   }
+  constexpr int TPW = KFMT == SPOT_KFMT_BF16 ? kTokTPW : kTok8TPW;
+  const int runs = tok_runs<TPW>(nblk);
+  const dim3 grid = tok_grid(n_seq, runs, rows_per_seq);
   if (lph == 8)
-    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 8, kTokTPW>), grid, dim3(256), 0, s, q, w, k, ks,
+    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 8, TPW>), grid, dim3(256), 0, s, q, w, k, ks,
                        n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
   else
-    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 16, kTokTPW>), grid, dim3(256), 0, s, q, w, k, ks,
+    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 16, TPW>), grid, dim3(256), 0, s, q, w, k, ks,
                        n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
   return hipGetLastError();
 }
@@ -323,34 +345,26 @@ hipError_t launch_selector_score_tokens(const void* q_sel, const float* w, const
                                         int rows_per_seq, int l_cap, int d_s,
                                         const int32_t* seq_len, float* scores, hipStream_t s) {
   const int nblk = l_cap / kBlk;
-  constexpr int kBlocksPerWG = kTokWavesPerWG * kTokTPW / 64;
-  const int runs = (nblk + kBlocksPerWG - 1) / kBlocksPerWG;
-  const long long units = (long long)n_seq * runs;
-  const dim3 grid((unsigned)(((units + 7) / 8) * 8 * rows_per_seq));
   const int lph = d_s / 8;
   auto q = static_cast<const uint16_t*>(q_sel);
   auto k = static_cast<const uint8_t*>(k_tok);
   auto ks = static_cast<const uint8_t*>(k_scale);
   switch (kfmt) {
     case SPOT_KFMT_BF16:
-      return launch_tokens_fmt<SPOT_KFMT_BF16>(lph, grid, s, q, w, k, ks, n_seq, rows_per_seq,
-                                               l_cap, nblk, runs, seq_len, scores);
+      return launch_tokens_fmt<SPOT_KFMT_BF16>(lph, s, q, w, k, ks, n_seq, rows_per_seq, l_cap,
+                                               nblk, seq_len, scores);
     case SPOT_KFMT_INT4_G32:
-      return launch_tokens_fmt<SPOT_KFMT_INT4_G32>(lph, grid, s, q, w, k, ks, n_seq,
-                                                   rows_per_seq, l_cap, nblk, runs, seq_len,
-                                                   scores);
+      return launch_tokens_fmt<SPOT_KFMT_INT4_G32>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
+                                                   l_cap, nblk, seq_len, scores);
     case SPOT_KFMT_INT8_G32:
-      return launch_tokens_fmt<SPOT_KFMT_INT8_G32>(lph, grid, s, q, w, k, ks, n_seq,
-                                                   rows_per_seq, l_cap, nblk, runs, seq_len,
-                                                   scores);
+      return launch_tokens_fmt<SPOT_KFMT_INT8_G32>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
+                                                   l_cap, nblk, seq_len, scores);
     case SPOT_KFMT_MXFP8_G32:
-      return launch_tokens_fmt<SPOT_KFMT_MXFP8_G32>(lph, grid, s, q, w, k, ks, n_seq,
-                                                    rows_per_seq, l_cap, nblk, runs, seq_len,
-                                                    scores);
+      return launch_tokens_fmt<SPOT_KFMT_MXFP8_G32>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
+                                                    l_cap, nblk, seq_len, scores);
     default:
-      return launch_tokens_fmt<SPOT_KFMT_MXFP4_G32>(lph, grid, s, q, w, k, ks, n_seq,
-                                                    rows_per_seq, l_cap, nblk, runs, seq_len,
-                                                    scores);
+      return launch_tokens_fmt<SPOT_KFMT_MXFP4_G32>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
+                                                    l_cap, nblk, seq_len, scores);
   }
 }
 
