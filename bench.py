@@ -96,8 +96,9 @@ def measured_traffic(path=STEP_PROFILE, files=STEP_SOURCES):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the decode path "
-              "needs no cross-GPU exchange and this build measures a single device.",
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): it measures the "
+              "kernels on a single device's share of the work (a multi-GPU layout would "
+              "shard by sequence and KV head, with no exchange on the decode path).",
               file=sys.stderr)
         sys.exit(2)
 
