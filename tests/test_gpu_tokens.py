@@ -88,6 +88,15 @@ CASES = [
     (2, 1, 4096, 4, 128, [4096, 2049], "int8"),
     (2, 1, 4096, 8, 64, [3000, 4096], "mxfp8"),
     (3, 2, 1024, 4, 128, [1024, 1, 700, 64, 1000, 65], "mxfp8"),
+    # quantized keys run one wave per block, four blocks per workgroup: block
+    # counts that leave a workgroup's run partly empty (7 and 1 blocks)
+    (3, 1, 448, 4, 128, [448, 300, 0], "int4"),
+    (3, 1, 448, 8, 64, [447, 65, 448], "mxfp4"),
+    (2, 1, 448, 4, 128, [448, 129], "int8"),
+    (2, 1, 448, 8, 64, [63, 448], "mxfp8"),
+    (2, 1, 64, 4, 128, [64, 5], "mxfp4"),
+    (2, 3, 2048, 4, 128, [2048, 1000, 64, 1500, 1501, 2047], "mxfp4"),
+    (2, 3, 2048, 8, 64, [2048, 999, 1, 2000, 1501, 2048], "int8"),
 ]
 
 
