@@ -210,7 +210,7 @@ def test_score_tokens_closed_form(golden_dir):
         np.testing.assert_array_equal(s, expected)
 
 
-@pytest.mark.parametrize("kfmt", ["bf16", "int4", "mxfp4"])
+@pytest.mark.parametrize("kfmt", ["bf16", "int4", "mxfp4", "int8", "mxfp8"])
 def test_score_tokens_reduces_to_pooled_scores(kfmt):
     """With one token per block the per-token selector is the pinned block
     score with every token as its own block; a numpy maximum over groups of
@@ -220,8 +220,7 @@ def test_score_tokens_reduces_to_pooled_scores(kfmt):
     q = bf16_bits(rng.standard_normal((n_seq * rps, Hs, ds)).astype(np.float32))
     w = rng.uniform(0, 1, (n_seq * rps, Hs)).astype(np.float32)
     kb = bf16_bits(rng.standard_normal((n_seq, L, Hs, ds)).astype(np.float32))
-    k, sc = {"bf16": lambda b: (b, None), "int4": synth.quantize_int4_g32,
-             "mxfp4": synth.quantize_mxfp4_g32}[kfmt](kb)
+    k, sc = {"bf16": lambda b: (b, None), **synth.QUANTIZERS}[kfmt](kb)
     per_tok = oracle.selector_score(q, w, k, sc, kfmt, rows_per_seq=rps, nblk=L, h_s=Hs, d_s=ds)
     seq_len = np.array([L, 200, 129, 1], np.int32)
     s = oracle.selector_score_tokens(q, w, k, sc, kfmt, rows_per_seq=rps, seq_len=seq_len,
