@@ -17,10 +17,13 @@
  *
  * Conventions shared by every entry point:
  *  - Pointers named as device arrays are caller-owned device memory; the
- *    library never allocates, frees, or synchronises, and keeps no state of
- *    its own between calls (the decode workspace carries completion counters
- *    that each call returns to zero).  Arrays are C-contiguous and start on
- *    a 16-byte boundary (as every hipMalloc and torch allocation does; the
+ *    library never allocates or frees, synchronises only in
+ *    spot_decode_step_status, and between calls keeps only two process-wide
+ *    values of its own: a per-device cache of the fused step's occupancy
+ *    (the same number whichever call stores it) and the test hook of
+ *    spot_test_force_expiry.  The decode workspaces carry completion
+ *    counters and hand-off records that each call returns to zero.  Arrays
+ *    are C-contiguous and start on a 16-byte boundary (as every hipMalloc and torch allocation does; the
  *    kernels read them with 16-byte vector loads).  BF16 arrays hold bfloat16
  *    values (2 bytes each).  A KV block is 64 consecutive tokens; the
  *    pooled selector key cache holds one key per block, the per-token cache
@@ -54,6 +57,8 @@ typedef int32_t spot_status;
 #define SPOT_ERR_WORKSPACE 5   /* the workspace is missing, too small or not      */
                                /* 16-byte aligned                                 */
 #define SPOT_ERR_HIP 6         /* the HIP runtime reported a launch error         */
+#define SPOT_ERR_EXPIRED 7     /* a bounded wait of the fused decode step expired */
+                               /* (reported by spot_decode_step_status)           */
 
 /* Storage formats of the selector key cache (Section 5.3, Appendix G: INT8,
  * FP8 and group-32 microscale 4-bit formats alongside BF16; here every
@@ -323,35 +328,48 @@ spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
  * the ones they would produce.
  *
  * When h_q == 4 * h_kv, nblk <= 4096 and min(k_max, nblk) <= 512, the three
- * stages run as one launch whose grid fits the device at once: one
- * workgroup per sequence selects its blocks as soon as the sequence's
- * scores are in, and the attention workgroups start as soon as that
- * selection is published, with no kernel boundary in between (hand-offs
- * through self-flagging record words in the workspace, which each reader
- * clears again).  Otherwise (or when no such grid fits) the three stages are
- * launched one after the other on `stream`.  Either way the results are
- * deterministic; the fused path may split the attention over fewer
- * workgroups when fewer fit, which changes the FP32 summation order (not
- * the block set).  The fused grid is sized to the whole device: it assumes
- * no other kernel holds compute units for long while it runs (workgroups
- * that cannot start wait for others to drain).  Every wait inside it is
- * bounded (0.2 s), so the device never hangs; if a wait does expire, that
- * call's outputs are undefined and the workspace must be zero-filled again
- * before the next call.
+ * stages run as one launch: every workgroup scores a chunk of its
+ * sequence's blocks, then selects the sequence's blocks itself from the
+ * scores of all chunks, then attends to its share of them, with no kernel
+ * boundary in between (hand-offs through self-flagging record words in the
+ * workspace, which each reader clears again).  Otherwise (or when no such
+ * grid fits) the three stages are launched one after the other on `stream`.
+ * Either way the results are deterministic; the fused path may split the
+ * attention over fewer workgroups when fewer fit, which changes the FP32
+ * summation order (not the block set).
+ *
+ * Residency contract of the fused launch.  Its grid is sized to the number
+ * of workgroups the device holds at once, and workgroups wait for records
+ * written by others of the same launch: a sequence's workgroups wait for the
+ * scores of all h_kv * n_slot scoring workgroups of that sequence, and the
+ * last workgroup of each (sequence, KV head) pair waits for the attention
+ * partials of the pair's other workgroups.  A kernel on another stream that
+ * holds compute units (or a second fused step running concurrently) can keep
+ * some of these workgroups from starting.  Every wait is bounded (0.2 s), so
+ * the device never hangs.  When a wait expires, the waiting workgroup
+ * computes nothing on unwritten records: it attends to no block, count[b]
+ * of its sequence becomes -1, and a sticky expiry word in the workspace is
+ * set.  While that word is set, every later call on the workspace gives
+ * count = -1 for every sequence and zero outputs (idx and nuc_mass are left
+ * as they were) without waiting, until spot_decode_step_status() reports the
+ * expiry and zero-fills the workspace.  The word, not count, is
+ * authoritative: a sequence whose own workgroups finished can still show its
+ * real count in the call that expired.
  *
  *  scores   device float [batch, nblk]          (output)
  *  idx      device int32 [batch, k_max]         (output)
- *  count    device int32 [batch]                (output)
+ *  count    device int32 [batch]                (output; -1 after an expiry)
  *  nuc_mass device float [batch] or NULL        (output)
  *  out, lse as spot_sparse_decode               (output; lse may be NULL)
  *  ws       device, spot_decode_step_workspace_bytes(batch, h_q, h_kv, d,
  *           k_max) bytes, 16-byte aligned: the decode partials and counters
- *           laid out as for spot_sparse_decode, then (from the next 16-byte
- *           boundary) 4096 score record words per sequence and h_kv * k_max
- *           block list record words per sequence.  It must be zero-filled
- *           before its first use; every call leaves it ready for the next one
- *           (its counters and records return to zero).  Calls that share a
- *           workspace must not overlap in time.
+ *           laid out as for spot_sparse_decode (used when the stages run
+ *           separately), then (from the next 16-byte boundary) the fused
+ *           launch's partial records, election counters, expiry word and
+ *           4096 score record words per (sequence, KV head) pair.  It must be
+ *           zero-filled before its first use; every call leaves it ready for
+ *           the next one (its counters and records return to zero).  Calls
+ *           that share a workspace must not overlap in time.
  */
 size_t spot_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max);
 
@@ -365,10 +383,42 @@ spot_status spot_decode_step(const void *q_sel, const float *w, const void *k_se
                              float *lse, void *ws, size_t ws_bytes, void *stream);
 
 /*
- * spot_dense_decode -- the dense decode baseline: spot_sparse_decode with
- * every block < ceil(seq_len / 64) selected (full attention over the cache).
- * Same layouts; ws of spot_decode_workspace_bytes(batch, h_q, h_kv, d,
- * l_cap / 64) bytes, 16-byte aligned.
+ * spot_decode_step_status -- the expiry word of a fused-step workspace.
+ *
+ * Waits for `stream`, then reads the sticky expiry word that spot_decode_step
+ * sets when one of its bounded waits expires (see the residency contract
+ * above).  Returns SPOT_OK when it is clear.  When it is set, zero-fills the
+ * whole workspace (spot_decode_step_workspace_bytes for these sizes) on
+ * `stream`, waits for that, and returns SPOT_ERR_EXPIRED: the next
+ * spot_decode_step on the workspace runs normally again.  The sizes are
+ * those of the spot_decode_step calls that use ws.  Errors: SPOT_ERR_NULL,
+ * SPOT_ERR_SHAPE, SPOT_ERR_WORKSPACE (too small or misaligned), SPOT_ERR_HIP.
+ * This is the library's only synchronising call.
+ */
+spot_status spot_decode_step_status(void *ws, size_t ws_bytes, int batch, int h_q, int h_kv,
+                                    int d, int k_max, void *stream);
+
+/*
+ * spot_test_force_expiry -- test hook, not part of the attention path.
+ * While `on` is nonzero, every later fused spot_decode_step launch in this
+ * process behaves as if each workgroup's wait for its sequence's scores had
+ * expired at once (no waiting), so the expiry handling above can be tested
+ * with every kernel exiting normally.  Process-wide; not for concurrent use.
+ */
+void spot_test_force_expiry(int on);
+
+/*
+ * spot_dense_decode -- the dense decode baseline.  The paper's decode
+ * latency comparison (Section 3 names FlashAttention as the dense baseline;
+ * Section 4.2, Table 1 times it) sets the method against dense attention
+ * over every token of the cache.
+ * This call is spot_sparse_decode with every block < ceil(seq_len / 64)
+ * selected: for sequence b and query head h with KV head g = h / (h_q / h_kv),
+ *     out[b, h] = sum_{t < seq_len[b]} softmax_t(sm_scale * q[b,h] . k[b,g,t]) v[b,g,t].
+ * Same layouts, outputs, determinism and errors as spot_sparse_decode; ws of
+ * spot_decode_workspace_bytes(batch, h_q, h_kv, d, l_cap / 64) bytes,
+ * 16-byte aligned, zero-filled before first use (each call leaves it so).
+ * l_cap == 0 is SPOT_ERR_SHAPE.
  */
 spot_status spot_dense_decode(const void *q, const void *k, const void *v,
                               const int32_t *seq_len, int batch, int h_q, int h_kv, int d,

@@ -29,6 +29,7 @@ const char* spot_status_str(spot_status s) {
     case SPOT_ERR_RULE: return "invalid selection rule";
     case SPOT_ERR_WORKSPACE: return "workspace missing or too small";
     case SPOT_ERR_HIP: return "HIP launch error";
+    case SPOT_ERR_EXPIRED: return "a bounded wait of the fused decode step expired";
     default: return "unknown status";
   }
 }
@@ -245,6 +246,26 @@ spot_status spot_decode_step(const void* q_sel, const float* w, const void* k_se
                       sm_scale, out, lse, ws, s);
   return from_hip(e);
 }
+
+spot_status spot_decode_step_status(void* ws, size_t ws_bytes, int batch, int h_q, int h_kv,
+                                    int d, int k_max, void* stream) {
+  if (!ws) return SPOT_ERR_NULL;
+  if (batch < 1 || h_q < 1 || h_kv < 1 || d < 1 || k_max < 1) return SPOT_ERR_SHAPE;
+  const size_t need = step_workspace_bytes(batch, h_q, h_kv, d, k_max);
+  if (ws_bytes < need || misaligned(ws)) return SPOT_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint32_t word = 0;
+  const char* w = static_cast<const char*>(ws) + step_sticky_offset(batch, h_q, h_kv, k_max);
+  if (hipMemcpyAsync(&word, w, sizeof(word), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return SPOT_ERR_HIP;
+  if (word == 0u) return SPOT_OK;
+  if (hipMemsetAsync(ws, 0, need, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
+    return SPOT_ERR_HIP;
+  return SPOT_ERR_EXPIRED;
+}
+
+void spot_test_force_expiry(int on) { step_force_expiry(on); }
 
 spot_status spot_sparse_prefill(const void* q, const void* k, const void* v, int L,
                                 const int32_t* idx, const int32_t* count, int k_max, int batch,

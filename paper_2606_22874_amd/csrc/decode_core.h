@@ -89,6 +89,32 @@ __device__ __forceinline__ float group_sum(float v) {
   return v;
 }
 
+// Log-sum-exp merge of n <= 16 partials of query head bh held by one wave:
+// lane u < n has partial u's (m, l) in t, every lane has the partials'
+// output dims 2*lane, 2*lane+1 in o[u].  Writes out (BF16) and lse; fixed
+// order, so deterministic.
+__device__ __forceinline__ void merge_small(float2 t, const float2 (&o)[16], int n, size_t bh,
+                                            uint16_t* __restrict__ out, float* __restrict__ lse,
+                                            int lane) {
+  const float M = wave_max(t.y > 0.f ? t.x : -INFINITY);
+  const float wgt = t.y > 0.f ? exp2f(t.x - M) : 0.f;
+  const float L = wave_sum(t.y * wgt);
+  float o0 = 0.f, o1 = 0.f;
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    if (u < n) {
+      const float wt = readlane_f(wgt, u);
+      o0 = fmaf(o[u].x, wt, o0);
+      o1 = fmaf(o[u].y, wt, o1);
+    }
+  }
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  const uint32_t packed = (uint32_t)f32_to_bf16_rne(o0 * inv) |
+                          ((uint32_t)f32_to_bf16_rne(o1 * inv) << 16);
+  *reinterpret_cast<uint32_t*>(&out[bh * kD + 2 * lane]) = packed;
+  if (lse && lane == 0) lse[bh] = L > 0.f ? (M + log2f(L)) * 0.6931471805599453f : -INFINITY;
+}
+
 // Log-sum-exp merge of the n_split partials of query head bh by one wave
 // (lane = output dims 2*lane, 2*lane+1); fixed order, so deterministic.
 __device__ __forceinline__ void merge_head(const float* __restrict__ ws_o,
@@ -104,23 +130,7 @@ __device__ __forceinline__ void merge_head(const float* __restrict__ ws_o,
 #pragma unroll
     for (int u = 0; u < 16; ++u)
       if (u < n_split) o[u] = load_coherent(ob + (size_t)u * kD);
-    const float M = wave_max(t.y > 0.f ? t.x : -INFINITY);
-    const float wgt = t.y > 0.f ? exp2f(t.x - M) : 0.f;
-    const float L = wave_sum(t.y * wgt);
-    float o0 = 0.f, o1 = 0.f;
-#pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      if (u < n_split) {
-        const float wt = readlane_f(wgt, u);
-        o0 = fmaf(o[u].x, wt, o0);
-        o1 = fmaf(o[u].y, wt, o1);
-      }
-    }
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    const uint32_t packed = (uint32_t)f32_to_bf16_rne(o0 * inv) |
-                            ((uint32_t)f32_to_bf16_rne(o1 * inv) << 16);
-    *reinterpret_cast<uint32_t*>(&out[bh * kD + 2 * lane]) = packed;
-    if (lse && lane == 0) lse[bh] = L > 0.f ? (M + log2f(L)) * 0.6931471805599453f : -INFINITY;
+    merge_small(t, o, n_split, bh, out, lse, lane);
     return;
   }
   float M = -INFINITY;
@@ -248,51 +258,51 @@ struct ListFromIdx {
 };
 
 // ---------------------------------------------------------- the body
-// Workgroup (pair, slot): slot s takes its share of the pair's block list
-// (from `list`; DENSE: the s-th contiguous run of all valid blocks); wave w
-// processes token rows [w*T, (w+1)*T) of each of those blocks.  Returns true
-// in the workgroup that merged the pair's slots (the last one to finish).
-template <int G, bool DENSE, class List>
-__device__ __forceinline__ bool decode_body(
-    DecodeSmem<G>& sm, const List& list, int pair, int slot, const uint16_t* __restrict__ q,
-    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    const int32_t* __restrict__ seq_len, int h_q, int h_kv, int l_cap,
-    float scale_log2, int n_slot, float* __restrict__ ws_o, float* __restrict__ ws_ml,
-    unsigned* __restrict__ counters, uint16_t* __restrict__ out, float* __restrict__ lse) {
+// The G query heads of KV head g of sequence b: lane (h, t) of every wave
+// holds query head g*G + h (h = lane / T) as 64 packed BF16 pairs.
+template <int G>
+__device__ __forceinline__ void load_query_heads(uint32_t (&qv)[kD / 2],
+                                                 const uint16_t* __restrict__ q, int b, int g,
+                                                 int h_q) {
+  constexpr int T = 64 / G;
+  const int hh = __lane_id() / T;
+  const u32x4* qp = reinterpret_cast<const u32x4*>(q + ((size_t)b * h_q + g * G + hh) * kD);
+#pragma unroll
+  for (int i = 0; i < kD / 8; ++i) {
+    const u32x4 t = qp[i];
+    qv[4 * i + 0] = t.x; qv[4 * i + 1] = t.y; qv[4 * i + 2] = t.z; qv[4 * i + 3] = t.w;
+  }
+}
+
+// One workgroup's partial of one query head after its G waves are merged:
+// wave w holds head w of the group (M and L in every lane, output dims
+// 2*lane and 2*lane+1 in o0, o1).  L == 0 means no token was seen.
+struct HeadPartial {
+  float M, L, o0, o1;
+};
+
+// The block loop of a workgroup: blocks blk_of(0 .. n_local-1) of the KV
+// head whose caches start at kh / vh ([l_cap, 128] each), tokens below sl.
+// Wave w processes token rows [w*T, (w+1)*T) of every block; the G waves'
+// states are merged in LDS at the end (two barriers).  issued(n) is called
+// by every wave right after it issued the loads of block n, so a caller can
+// act once the last block's loads are in flight.
+template <int G, class BlkOf, class Issued>
+__device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
+                                                     const uint32_t (&qv)[kD / 2],
+                                                     const uint16_t* __restrict__ kh,
+                                                     const uint16_t* __restrict__ vh, int sl,
+                                                     int n_local, const BlkOf& blk_of,
+                                                     float scale_log2, const Issued& issued) {
   constexpr int T = 64 / G;               // token rows per wave per block
   constexpr int NLD = T * kD * 2 / 1024;  // 16-byte loads per lane per slice
   static_assert(NLD >= 1, "slice smaller than one wave load");
-  const int b = pair / h_kv, g = pair % h_kv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane / T, tt = lane % T;  // this lane's (head, token row)
-  unsigned* pc = pair_counters(counters, pair);
 
-  // This lane's query head (g*G + hh): 128 dims as packed BF16 pairs.
-  uint32_t qv[kD / 2];
-  {
-    const u32x4* qp = reinterpret_cast<const u32x4*>(q + ((size_t)b * h_q + g * G + hh) * kD);
-#pragma unroll
-    for (int i = 0; i < kD / 8; ++i) {
-      const u32x4 t = qp[i];
-      qv[4 * i + 0] = t.x; qv[4 * i + 1] = t.y; qv[4 * i + 2] = t.z; qv[4 * i + 3] = t.w;
-    }
-  }
-
-  const int sl = min(seq_len[b], l_cap);
-  const int nb_valid = (sl + kBlk - 1) / kBlk;
-  // DENSE: this workgroup's contiguous run [e0, e1) of the valid blocks.
-  const int bps = (nb_valid + n_slot - 1) / n_slot;
-  const int e0 = slot * bps;
-  const int e1 = min(e0 + bps, nb_valid);
-  if (!DENSE && wave == 0) {
-    const int n = list(sm.ids, b, g, slot, n_slot, nb_valid);
-    if (lane == 0) sm.n_local = n;
-  }
-
-  const size_t head_base = ((size_t)b * h_kv + g) * (size_t)l_cap * kD;
   // This wave's slice of a block starts at token row wave * T.
-  const uint16_t* kw = k + head_base + (size_t)wave * T * kD;
-  const uint16_t* vw = v + head_base + (size_t)wave * T * kD;
+  const uint16_t* kw = kh + (size_t)wave * T * kD;
+  const uint16_t* vw = vh + (size_t)wave * T * kD;
   auto& W = sm.wave[wave];
 
   // Register stages A and B hold the two blocks of the current chunk.
@@ -368,21 +378,29 @@ __device__ __forceinline__ bool decode_body(
     }
   };
 
-  __syncthreads();
-  const int n_local = DENSE ? max(e1 - e0, 0) : sm.n_local;
-  auto blk_of = [&](int n) { return DENSE ? e0 + n : sm.ids[n]; };
-
   // Two register stages: while block n is computed, blocks n+1 and n+2 are
   // loading.
-  if (n_local > 0) load_slice<NLD>(krA, vrA, kw, vw, blk_of(0), lane);
-  if (n_local > 1) load_slice<NLD>(krB, vrB, kw, vw, blk_of(1), lane);
+  if (n_local > 0) {
+    load_slice<NLD>(krA, vrA, kw, vw, blk_of(0), lane);
+    issued(0);
+  }
+  if (n_local > 1) {
+    load_slice<NLD>(krB, vrB, kw, vw, blk_of(1), lane);
+    issued(1);
+  }
   for (int n = 0; n < n_local; n += 2) {
     consume(krA, vrA);
-    if (n + 2 < n_local) load_slice<NLD>(krA, vrA, kw, vw, blk_of(n + 2), lane);
+    if (n + 2 < n_local) {
+      load_slice<NLD>(krA, vrA, kw, vw, blk_of(n + 2), lane);
+      issued(n + 2);
+    }
     compute(blk_of(n));
     if (n + 1 < n_local) {
       consume(krB, vrB);
-      if (n + 3 < n_local) load_slice<NLD>(krB, vrB, kw, vw, blk_of(n + 3), lane);
+      if (n + 3 < n_local) {
+        load_slice<NLD>(krB, vrB, kw, vw, blk_of(n + 3), lane);
+        issued(n + 3);
+      }
       compute(blk_of(n + 1));
     }
   }
@@ -398,6 +416,7 @@ __device__ __forceinline__ bool decode_body(
   for (int h = 0; h < G; ++h)
     *reinterpret_cast<float2*>(&sm.merge.o[wave][h][2 * lane]) = make_float2(acc[h][0], acc[h][1]);
   __syncthreads();
+  HeadPartial r;
   {
     const int h = wave;  // wave w merges head w of the group
     float M = -INFINITY;
@@ -416,9 +435,55 @@ __device__ __forceinline__ bool decode_body(
         o1 = fmaf(o.y, wgt, o1);
       }
     }
+    r = HeadPartial{M, L, o0, o1};
+  }
+  return r;
+}
+
+struct NoHook {
+  __device__ __forceinline__ void operator()(int) const {}
+};
+
+// Workgroup (pair, slot): slot s takes its share of the pair's block list
+// (from `list`; DENSE: the s-th contiguous run of all valid blocks); wave w
+// processes token rows [w*T, (w+1)*T) of each of those blocks.  The split
+// partials go to the workspace; the last workgroup of the pair to finish
+// (device-scope counter) merges them.  Returns true in that workgroup.
+template <int G, bool DENSE, class List>
+__device__ __forceinline__ bool decode_body(
+    DecodeSmem<G>& sm, const List& list, int pair, int slot, const uint16_t* __restrict__ q,
+    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    const int32_t* __restrict__ seq_len, int h_q, int h_kv, int l_cap,
+    float scale_log2, int n_slot, float* __restrict__ ws_o, float* __restrict__ ws_ml,
+    unsigned* __restrict__ counters, uint16_t* __restrict__ out, float* __restrict__ lse) {
+  const int b = pair / h_kv, g = pair % h_kv;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  unsigned* pc = pair_counters(counters, pair);
+
+  uint32_t qv[kD / 2];
+  load_query_heads<G>(qv, q, b, g, h_q);
+
+  const int sl = min(seq_len[b], l_cap);
+  const int nb_valid = (sl + kBlk - 1) / kBlk;
+  // DENSE: this workgroup's contiguous run [e0, e1) of the valid blocks.
+  const int bps = (nb_valid + n_slot - 1) / n_slot;
+  const int e0 = slot * bps;
+  const int e1 = min(e0 + bps, nb_valid);
+  if (!DENSE && wave == 0) {
+    const int n = list(sm.ids, b, g, slot, n_slot, nb_valid);
+    if (lane == 0) sm.n_local = n;
+  }
+  __syncthreads();
+  const int n_local = DENSE ? max(e1 - e0, 0) : sm.n_local;
+  const size_t head_base = ((size_t)b * h_kv + g) * (size_t)l_cap * kD;
+  auto blk_of = [&](int n) { return DENSE ? e0 + n : sm.ids[n]; };
+  const HeadPartial hp = attend_blocks<G>(sm, qv, k + head_base, v + head_base, sl, n_local,
+                                          blk_of, scale_log2, NoHook{});
+  {
+    const int h = wave;
     const size_t ps = ((size_t)b * h_q + g * G + h) * n_slot + slot;
-    store_coherent(&ws_o[ps * kD + 2 * lane], make_float2(o0, o1));
-    if (lane == 0) store_coherent(&ws_ml[ps * 2], make_float2(M, L));
+    store_coherent(&ws_o[ps * kD + 2 * lane], make_float2(hp.o0, hp.o1));
+    if (lane == 0) store_coherent(&ws_ml[ps * 2], make_float2(hp.M, hp.L));
   }
 
   // ---- the last workgroup of the pair merges all slots ----

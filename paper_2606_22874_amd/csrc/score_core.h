@@ -177,9 +177,10 @@ struct KeyLoad<SPOT_KFMT_MXFP8_G32> {
 // One wavefront scores blocks j0 .. min(j0 + U, jend) - 1 of query row `row`
 // (sequence `seq`), all key loads issued before any arithmetic; blocks at or
 // past nv score -inf.  A non-null rec (the row's record words, indexed by
-// block) also receives rec_word() of each valid block's score, stored at
-// device scope (a reader in another workgroup of the same launch polls these
-// words: zero means not written yet).  Returns, in lane u < U, the score of
+// block; rec_copies runs of them rec_stride words apart) also receives
+// rec_word() of each valid block's score in every run, stored at device
+// scope (readers in other workgroups of the same launch poll these words:
+// zero means not written yet).  Returns, in lane u < U, the score of
 // block j0 + u (-inf in the other lanes and past jend).
 // This lane's 8 query elements of row `row` (head lane / LPH, dims
 // 8*(lane % LPH) ..) as BF16 bits (qraw) and floats (qf).  Queries coded in
@@ -233,7 +234,8 @@ __device__ __forceinline__ float score_blocks(const void* __restrict__ q_sel,
                                              int seq, int nblk, int nv, int j0, int jend,
                                              float* __restrict__ scores,
                                              uint32_t* __restrict__ rec, int lane,
-                                             const uint8_t* __restrict__ q_scale = nullptr) {
+                                             const uint8_t* __restrict__ q_scale = nullptr,
+                                             int rec_copies = 1, size_t rec_stride = 0) {
   constexpr int kHeads = 64 / LPH;
   uint4 qraw;
   float qf[8];
@@ -263,8 +265,9 @@ __device__ __forceinline__ float score_blocks(const void* __restrict__ q_sel,
   const float val = lane < U && j < nv && j < jend ? res : -INFINITY;
   if (lane < U && j < jend) {
     if (rec && j < nv)
-      __hip_atomic_store(rec + j, rec_word(val), __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
+      for (int c = 0; c < rec_copies; ++c)
+        __hip_atomic_store(rec + c * rec_stride + j, rec_word(val), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     scores[(size_t)row * nblk + j] = val;
   }
   return val;

@@ -579,9 +579,12 @@ __global__ __launch_bounds__(kSelWG) void select_wg_kernel(
   const int row = blockIdx.x;
   int nv = n_valid ? n_valid[row] : nblk;
   nv = nv < 0 ? 0 : (nv > nblk ? nblk : nv);
-  select_row_wg<EPT, SPL>(sm, RowScores{scores + (size_t)row * nblk}, nblk, nv, top_p, k_max,
-                          k_min, n_sink, n_recent, idx_out + (size_t)row * k_max, count_out + row,
-                          mass_out ? mass_out + row : nullptr, IdRecords{nullptr, 0, 0});
+  const SelRow r = select_row_core<EPT, SPL>(sm, RowScores{scores + (size_t)row * nblk}, nv,
+                                             top_p, k_max, k_min, n_sink, n_recent);
+  int total;
+  const int pos = sel_positions(sm, r.fin, total);
+  sel_write<EPT>(idx_out + (size_t)row * k_max, count_out + row,
+                 mass_out ? mass_out + row : nullptr, k_max, r.fin, pos, total, r.mass);
 }
 
 }  // namespace

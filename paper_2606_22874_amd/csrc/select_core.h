@@ -91,8 +91,8 @@ __device__ __forceinline__ void bitonic_desc(uint64_t (&K)[SPL]) {
 }
 
 // ---------------------------------------------------------------------------
-// Workgroup (4 waves) selection for rows of 513 .. 4096 blocks, cap <= 512
-// (select_row_wg below): the single-wave kernel's rule with the element-wise
+// Workgroup (4 waves) selection for rows of up to 4096 blocks, cap <= 512
+// (select_row_core below): the single-wave kernel's rule with the element-wise
 // phases spread over 256 threads (EPT <= 16 consecutive ids each).
 constexpr int kSelWG = 256;
 
@@ -115,25 +115,18 @@ __device__ __forceinline__ int wg_excl_scan(int v, int* red, int& total) {
 }
 
 
-// Score source of select_row_wg: plain loads of a row of scores.  The fused
-// decode step substitutes a source that polls records written by other
-// workgroups of the same launch.
+// Score source of select_row_core: plain loads of a row of scores (never
+// fails).  The fused decode step substitutes a source that polls records
+// written by other workgroups of the same launch and fails when its bounded
+// wait expires.
 struct RowScores {
   const float* srow;
   template <int EPT>
-  __device__ __forceinline__ void operator()(float (&sv)[EPT], int j0, int nv) const {
+  __device__ __forceinline__ bool operator()(float (&sv)[EPT], int j0, int nv) const {
 #pragma unroll
     for (int e = 0; e < EPT; ++e) sv[e] = j0 + e < nv ? srow[j0 + e] : -INFINITY;
+    return true;
   }
-};
-
-// Optional copies of the selection for readers in other workgroups of the
-// same launch: `copies` runs of `len` words, word i of each run = id + 1 of
-// entry i, or 0xffffffff past the last entry (zero means not written yet).
-// Stored at device scope; base == nullptr publishes nothing.
-struct IdRecords {
-  uint32_t* base;
-  int len, copies;
 };
 
 constexpr int kValBins = 2048;   // value bins of the threshold search
@@ -152,10 +145,18 @@ struct SelWgSmem {
   float red_f[kSelWG / 64];
   float red_m[kSelWG / 64];       // survivors' mass partials
   int red_i[kSelWG / 64];
+  int red_bad[kSelWG / 64];       // per wave: a score source failed
   int gc[kSelWG / 64];            // threshold-bin members per wave
   int bc[4];
   uint64_t cut;
   float cut_mass;
+};
+
+// What select_row_core leaves in each thread (ids [tid*EPT, tid*EPT + EPT)).
+struct SelRow {
+  uint32_t fin;    // bit e: id tid*EPT + e is in S
+  float mass;      // nucleus mass (the same in every thread)
+  bool ok;         // false: the score source failed; fin = 0
 };
 
 // Packed rank key: higher score first, then lower block id; unique per id.
@@ -169,9 +170,8 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 }
 
 // Selection of one row by the whole 256-thread workgroup: src supplies the
-// row's scores (the first nv valid), out receives its k_max id slots, pub
-// optional device-scope copies.  Needs min(k_max, nblk) <= P = 64 * SPL
-// (<= 512) and pub.len <= k_max.  Every thread of the workgroup must call it.  Thread t owns the
+// row's scores (the first nv valid).  Needs min(k_max, nv) <= P = 64 * SPL
+// (<= 512).  Every thread of the workgroup must call it.  Thread t owns the
 // EPT consecutive ids [t*EPT, (t+1)*EPT).  Steps, with the workgroup barriers
 // in brackets:
 //  1. load; order-preserving keys of the residual candidates; residual max
@@ -191,20 +191,19 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 //     otherwise they are compacted [2], sorted in wave 0 by (score desc, id
 //     asc), prefix-summed and cut where the prefix first reaches top_p * Z,
 //     then floored by k_min [1];
-//  4. reserved + chosen ids are written in ascending order [1] (with
-//     record copies: [2]).
+// It returns, in every thread, the bits of its ids that belong to S (reserved
+// + chosen) and the nucleus mass; sel_positions / sel_write turn them into
+// the ascending id list [1].  A score source that fails (a bounded wait that
+// expired) makes the whole workgroup return ok = false with no ids.
 // Every reduction has a fixed order, so the result is deterministic.
 template <int EPT, int SPL, class Src>
-__device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src& src, int nblk,
-                                              int nv, float top_p, int k_max, int k_min,
-                                              int n_sink, int n_recent, int32_t* __restrict__ out,
-                                              int32_t* __restrict__ count_out,
-                                              float* __restrict__ mass_out, IdRecords pub) {
+__device__ __forceinline__ SelRow select_row_core(SelWgSmem<EPT, SPL>& sm, const Src& src,
+                                                  int nv, float top_p, int k_max, int k_min,
+                                                  int n_sink, int n_recent) {
   constexpr int NT = kSelWG, NW = NT / 64;
   constexpr int P = 64 * SPL;
   constexpr float kLog2e = 1.4426950408889634f;
   static_assert(EPT <= 16, "a thread's ids must fit one bit word");
-  (void)nblk;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sink_end = min(n_sink, nv);
   const int rec_start = max(0, nv - n_recent);
@@ -216,7 +215,7 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   // 1. scores, keys (0 = not a candidate), M and min
   SPOT_SEL_TS(0);
   float sv[EPT];
-  src(sv, j0, nv);
+  const bool src_ok = src(sv, j0, nv);
   static_assert(kValBins == NT * 8, "two 16-byte zero stores per thread");
   reinterpret_cast<uint4*>(sm.hist)[2 * tid] = make_uint4(0u, 0u, 0u, 0u);
   reinterpret_cast<uint4*>(sm.hist)[2 * tid + 1] = make_uint4(0u, 0u, 0u, 0u);
@@ -242,11 +241,19 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   }
   kmax = wave_max_u(kmax);
   kmin = wave_min_u(kmin);
+  const bool wave_bad = __ballot(!src_ok) != 0ull;
   if (lane == 0) {
     sm.red_u[wave][0] = kmax;
     sm.red_u[wave][1] = kmin;
+    sm.red_bad[wave] = wave_bad;
   }
   __syncthreads();
+  {
+    bool bad = false;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) bad = bad || sm.red_bad[w];
+    if (bad) return SelRow{0u, 0.f, false};   // uniform over the workgroup
+  }
   kmax = 0u;
   kmin = 0xffffffffu;
 #pragma unroll
@@ -518,46 +525,47 @@ __device__ __forceinline__ void select_row_wg(SelWgSmem<EPT, SPL>& sm, const Src
   }
   SPOT_SEL_TS(4);
 
-  // 4. write S = reserved u chosen, ascending: positions by a scan.  Each
-  // thread writes its own ids; with record copies to publish, the ids are
-  // staged in LDS first (at most 512: min(k_max, nblk) <= P) so that all
-  // threads share the copies' stores evenly.
-  const uint32_t fin = resv | chosen;
+  return SelRow{resv | chosen, mass, true};
+}
+
+// Position (in ascending block id) of the calling thread's first id of S and
+// |S| itself: a workgroup exclusive scan of the threads' counts (one barrier).
+template <int EPT, int SPL>
+__device__ __forceinline__ int sel_positions(SelWgSmem<EPT, SPL>& sm, uint32_t fin, int& total) {
+  constexpr int NW = kSelWG / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int mine = __popc(fin);
   const int incl = wave_incl_scan_i(mine);
   if (lane == 63) sm.red_i[wave] = incl;
   __syncthreads();
-  int pos = incl - mine, total = 0;
+  int pos = incl - mine;
+  total = 0;
 #pragma unroll
   for (int w = 0; w < NW; ++w) {
     const int t = sm.red_i[w];
     pos += w < wave ? t : 0;
     total += t;
   }
+  return pos;
+}
+
+// Writes the selection of one row: S in ascending block id into out[0,
+// k_max) (-1 past |S|), |S| and the nucleus mass.  Every thread of the
+// workgroup calls it with its own fin and position.
+template <int EPT>
+__device__ __forceinline__ void sel_write(int32_t* __restrict__ out, int32_t* __restrict__ count_out,
+                                          float* __restrict__ mass_out, int k_max, uint32_t fin,
+                                          int pos, int total, float mass) {
+  const int tid = threadIdx.x, j0 = tid * EPT;
   const int n_out = min(total, k_max);
-  if (pub.base) {
 #pragma unroll
-    for (int e = 0; e < EPT; ++e)
-      if (((fin >> e) & 1u) && pos < n_out && pos < kValBins) sm.hist[pos++] = (uint32_t)(j0 + e);
-    __syncthreads();
-    for (int i = tid; i < pub.len; i += NT) {
-      const uint32_t wd = i < n_out ? sm.hist[i] + 1u : 0xffffffffu;
-      for (int c = 0; c < pub.copies; ++c)
-        __hip_atomic_store(pub.base + (size_t)c * pub.len + i, wd, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-    }
-    for (int i = tid; i < k_max; i += NT) out[i] = i < n_out ? (int32_t)sm.hist[i] : -1;
-  } else {
-#pragma unroll
-    for (int e = 0; e < EPT; ++e)
-      if (((fin >> e) & 1u) && pos < n_out) out[pos++] = j0 + e;
-    for (int i = n_out + tid; i < k_max; i += NT) out[i] = -1;
-  }
+  for (int e = 0; e < EPT; ++e)
+    if (((fin >> e) & 1u) && pos < n_out) out[pos++] = j0 + e;
+  for (int i = n_out + tid; i < k_max; i += kSelWG) out[i] = -1;
   if (tid == 0) {
     *count_out = n_out;
     if (mass_out) *mass_out = mass;
   }
-  SPOT_SEL_TS(5);
 }
 
 }  // namespace spot

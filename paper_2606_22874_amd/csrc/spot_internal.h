@@ -158,6 +158,8 @@ int decode_num_splits(int batch, int h_kv, int max_blocks, int group);
 size_t decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_blocks);
 
 size_t step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max);
+size_t step_sticky_offset(int batch, int h_q, int h_kv, int k_max);
+void step_force_expiry(int on);
 bool step_fusable(int h_q, int h_kv, int nblk, int k_max);
 hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_sel,
                               const void* k_scale, int kfmt, int d_s, const int32_t* n_valid,

@@ -4,9 +4,10 @@
 // reserved, attend to the chosen blocks only).
 //
 // Separate launches pay a kernel boundary (completion, cache maintenance and
-// dispatch of the next grid, a few microseconds each) twice per step, and the
-// attention grid only starts fetching once its dispatch is done.  Here one
-// grid of n_pairs * n_slot workgroups runs
+// dispatch of the next grid, a few microseconds each) twice per step, and
+// the attention grid only starts fetching once its dispatch is done.  Here
+// one grid of n_pairs * n_slot workgroups (pair = (sequence b, KV head g),
+// slot s) runs
 //   1. scoring: the first kMaxScorers workgroups of each row (workgroup i
 //      serves row i % batch) score a contiguous run of its blocks; each
 //      score also goes out as a self-flagging record word;
@@ -14,24 +15,43 @@
 //      records (each thread its own ids, as they land), clears them, selects
 //      the row (the workgroup core shared with the stand-alone kernel) and
 //      publishes the block list as record words, one copy per KV head;
-//   3. attention: every workgroup polls the list records of its (sequence,
-//      KV head) share, clears them and runs its (pair, slot) of the split-KV
-//      decode (shared core).
+//   3. attention: every workgroup polls its share (entries s, s + n_slot,
+//      ...) of its pair's copy of the list, clears it and runs its part of
+//      the split-KV decode (shared core).  Right after it issued the loads of
+//      its last block, it bumps the pair's election counter: the workgroup
+//      that bumps it last merges the pair, so the election's round trip
+//      overlaps the last block.  Partials go out as self-flagging record
+//      words; the merger polls them, merges in slot order (deterministic)
+//      and clears them and the counter.
 // A record word is nonzero once written and its reader sets it back to zero,
-// so a hand-off costs one round trip to the device coherence point, there
-// are no flags or contended atomics, and the workspace is all zero again
-// when the launch ends.
+// so a hand-off needs no flag or fence, only polling readers, and the
+// workspace is all zero again when a launch ends.
 //
-// The waits need every workgroup of the grid to be resident at once: the
-// launcher sizes the grid to the occupancy-derived capacity of the device
-// (workgroups that cannot start right away because other work holds CUs
-// start when it drains, since nothing else depends on this grid).  Each wait
-// is also bounded in time (kWaitTicks of the 100 MHz real-time counter), so
-// a wait can never hang the device; an expired wait lets the workgroup
-// finish with whatever the records held.
+// Residency: every wait is for records written by other workgroups of the
+// same launch -- a row's selector waits for the row's scorers, every
+// workgroup for its row's selector, and a pair's merger for the pair's other
+// n_slot - 1 workgroups.  The launcher sizes the grid to the occupancy-derived
+// capacity of the device, so on an otherwise idle device all workgroups are
+// resident together; the scorers and selectors are the lowest workgroup ids
+// and start first.  A kernel holding compute units on another stream can
+// delay some of them; each wait is therefore bounded (wait_ticks of the
+// 100 MHz real-time counter).  An expired wait computes nothing on unwritten
+// records: that workgroup attends to no block (an expired selector publishes
+// an empty list), sets count[b] = -1 and a sticky error word in the
+// workspace.  A launch that finds the sticky word set does not wait at all
+// (count = -1 for every row, outputs zero) until spot_decode_step_status()
+// reports the expiry and zero-fills the workspace.
+#include <atomic>
+
 #include "decode_core.h"
 #include "score_core.h"
 #include "select_core.h"
+
+// Measurement hook: SPOT_STEP_TS(i) marks phase i of a workgroup (a
+// timeline build defines it; empty otherwise).
+#ifndef SPOT_STEP_TS
+#define SPOT_STEP_TS(i) ((void)0)
+#endif
 
 namespace spot {
 namespace {
@@ -43,6 +63,7 @@ constexpr int kScoreRun = 8;              // blocks per scoring call of one wave
                                           // stand-alone kernel's run: same code, same bits)
 constexpr int kMaxScorers = 64;           // scoring workgroups per row
 constexpr int kRecRow = 4096;             // score record words per row (the fused maximum)
+constexpr int kMaxSlots = 16;             // attention workgroups per pair (merge_small)
 constexpr uint64_t kWaitTicks = 20000000; // 0.2 s of the 100 MHz real-time counter
 
 struct StepArgs {
@@ -66,12 +87,15 @@ struct StepArgs {
   float* mass;
   uint16_t* out;
   float* lse;
-  float* ws_o;
-  float* ws_ml;
-  unsigned* pair_cnt;   // [batch * h_kv] split completion (decode merge)
-  uint32_t* srec;       // [batch, kRecRow] score records
-  uint32_t* irec;       // [batch, h_kv, rec_len] block list records
-  int rec_len;          // min(k_max, nblk)
+  uint32_t* part_o;    // [batch * h_q, n_slot, 128] partial o record words
+  uint32_t* part_ml;   // [batch * h_q, n_slot, 2] partial (m, l) record words
+  unsigned* elect;     // [batch * h_kv] merger election counters
+  uint32_t* sticky;    // expiry word (one per workspace)
+  uint32_t* srec;      // [batch, kRecRow] score records
+  uint32_t* irec;      // [batch * h_kv, rec_len] block list record copies, one per pair
+  int rec_len;         // min(k_max, nblk)
+  uint64_t wait_ticks;
+  int force_expire;    // test hook: every score wait gives up at once
 };
 
 __device__ __forceinline__ uint64_t now() { return __builtin_amdgcn_s_memrealtime(); }
@@ -84,93 +108,91 @@ template <typename W>
 __device__ __forceinline__ void store_rec(W* p, W v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ uint64_t rec_pair(float a, float b) {
+  return (uint64_t)rec_word(a) | ((uint64_t)rec_word(b) << 32);
+}
+__device__ __forceinline__ float2 rec_pair_value(uint64_t x) {
+  return make_float2(rec_value((uint32_t)x), rec_value((uint32_t)(x >> 32)));
+}
+__device__ __forceinline__ bool rec_pair_full(uint64_t x) {
+  return (uint32_t)x != 0u && (uint32_t)(x >> 32) != 0u;
+}
 
-// Score source of the selector: thread t polls the records of its own ids
-// [j0, j0 + EPT) until every valid one is written (two words per load; the
-// words past nv stay zero all launch).  clear_scores() zeroes them again
-// once the selection is done: a store issued here would hold up the
-// selection's next barrier until it completed.
+// Score source of the selection: thread t polls the records of its own ids
+// [j0, j0 + EPT) of the row until every valid one is written (two
+// words per load; the words past nv stay zero all launch).  Fails when the
+// wait expires, or at once when give_up is set.
 struct PolledScores {
-  uint32_t* rec;   // the row's kRecRow record words
+  const uint32_t* rec;
+  uint64_t ticks;
+  bool give_up;
   template <int EPT>
-  __device__ __forceinline__ void operator()(float (&sv)[EPT], int j0, int nv) const {
+  __device__ __forceinline__ bool operator()(float (&sv)[EPT], int j0, int nv) const {
     uint32_t wd[EPT];
 #pragma unroll
     for (int e = 0; e < EPT; ++e) wd[e] = 0u;
-    const uint64_t deadline = now() + kWaitTicks;
-    for (;;) {
-      bool all = true;
-      if constexpr (EPT % 2 == 0) {
-#pragma unroll
-        for (int e = 0; e < EPT; e += 2) {
-          const bool need = (j0 + e < nv && wd[e] == 0u) || (j0 + e + 1 < nv && wd[e + 1] == 0u);
-          if (need) {
-            const uint64_t x = load_rec(reinterpret_cast<const uint64_t*>(rec + j0 + e));
-            wd[e] = (uint32_t)x;
-            wd[e + 1] = (uint32_t)(x >> 32);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < EPT; ++e)
-          if (j0 + e < nv && wd[e] == 0u) wd[e] = load_rec(rec + j0 + e);
-      }
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) all = all && (j0 + e >= nv || wd[e] != 0u);
-      if (all || now() > deadline) break;
-      __builtin_amdgcn_s_sleep(1);
-    }
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) sv[e] = j0 + e < nv ? rec_value(wd[e]) : -INFINITY;
-  }
-};
-
-// Clears thread t's score records [j0, j0 + EPT) below nv (see PolledScores).
-template <int EPT>
-__device__ __forceinline__ void clear_scores(uint32_t* rec, int j0, int nv) {
-  if constexpr (EPT % 2 == 0) {
-#pragma unroll
-    for (int e = 0; e < EPT; e += 2)
-      if (j0 + e < nv) store_rec(reinterpret_cast<uint64_t*>(rec + j0 + e), (uint64_t)0);
-  } else {
-#pragma unroll
-    for (int e = 0; e < EPT; ++e)
-      if (j0 + e < nv) store_rec(rec + j0 + e, 0u);
-  }
-}
-
-// Block list source of an attention workgroup: entries slot, slot + n_slot,
-// ... of its (sequence, KV head) copy of the list records (the stand-alone
-// decode's share of the same list, in the same order), polled until written.
-// Called by wave 0; clear_list() zeroes the same words after the attention
-// (a store here would hold up the next workgroup barrier).
-struct PolledList {
-  const uint32_t* irec;
-  int h_kv, rec_len;
-  __device__ __forceinline__ int operator()(int* ids, int b, int g, int slot, int n_slot,
-                                            int nb_valid) const {
-    const int lane = __lane_id();
-    uint32_t* rec = const_cast<uint32_t*>(irec) + ((size_t)b * h_kv + g) * rec_len;
-    const uint64_t deadline = now() + kWaitTicks;
-    int cnt = 0;
-    for (int base = slot; base < rec_len; base += 64 * n_slot) {
-      const int e = base + lane * n_slot;
-      uint32_t wd = e < rec_len ? 0u : 0xffffffffu;
+    bool all = false;
+    if (!give_up) {
+      const uint64_t deadline = now() + ticks;
       for (;;) {
-        if (wd == 0u) wd = load_rec(rec + e);
-        if (__ballot(wd == 0u) == 0ull || now() > deadline) break;
+        if constexpr (EPT % 2 == 0) {
+#pragma unroll
+          for (int e = 0; e < EPT; e += 2) {
+            const bool need = (j0 + e < nv && wd[e] == 0u) || (j0 + e + 1 < nv && wd[e + 1] == 0u);
+            if (need) {
+              const uint64_t x = load_rec(reinterpret_cast<const uint64_t*>(rec + j0 + e));
+              wd[e] = (uint32_t)x;
+              wd[e + 1] = (uint32_t)(x >> 32);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < EPT; ++e)
+            if (j0 + e < nv && wd[e] == 0u) wd[e] = load_rec(rec + j0 + e);
+        }
+        all = true;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) all = all && (j0 + e >= nv || wd[e] != 0u);
+        if (all || now() > deadline) break;
         __builtin_amdgcn_s_sleep(1);
       }
-      const int j = wd == 0u || wd == 0xffffffffu ? -1 : (int)(wd - 1u);
-      cnt = append_ids(ids, cnt, j, nb_valid);
     }
-    return min(cnt, kMaxIds);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) sv[e] = j0 + e < nv && wd[e] != 0u ? rec_value(wd[e]) : -INFINITY;
+    return all;
   }
 };
 
-__device__ __forceinline__ void clear_list(uint32_t* irec, int h_kv, int rec_len, int b, int g,
-                                           int slot, int n_slot) {
-  uint32_t* rec = irec + ((size_t)b * h_kv + g) * rec_len;
+// Block list source of an attention workgroup: entries slot, slot + n_slot,
+// ... of its pair's copy of the list records (the stand-alone decode's share
+// of the same list, in the same order), polled by wave 0 until written; an id
+// at or past nb_valid is skipped.  Returns the share's length, or -1 when the
+// wait expired.  clear_list() zeroes the same words after the attention.
+__device__ __forceinline__ int poll_list(int* ids, const uint32_t* rec, int rec_len, int slot,
+                                         int n_slot, int nb_valid, uint64_t ticks) {
+  const int lane = __lane_id();
+  const uint64_t deadline = now() + ticks;
+  int cnt = 0;
+  bool expired = false;
+  for (int base = slot; base < rec_len; base += 64 * n_slot) {
+    const int e = base + lane * n_slot;
+    uint32_t wd = e < rec_len ? 0u : 0xffffffffu;
+    for (;;) {
+      if (wd == 0u) wd = load_rec(rec + e);
+      if (__ballot(wd == 0u) == 0ull) break;
+      if (now() > deadline) {
+        expired = true;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    const int j = wd == 0u || wd == 0xffffffffu ? -1 : (int)(wd - 1u);
+    cnt = append_ids(ids, cnt, j, nb_valid);
+  }
+  return expired ? -1 : min(cnt, kMaxIds);
+}
+
+__device__ __forceinline__ void clear_list(uint32_t* rec, int rec_len, int slot, int n_slot) {
   for (int e = slot + __lane_id() * n_slot; e < rec_len; e += 64 * n_slot) store_rec(rec + e, 0u);
 }
 
@@ -207,58 +229,187 @@ __device__ __forceinline__ void score_run_rt(const StepArgs& a, int row, int nv,
 }
 
 template <int EPT, int SPL>
+union StepSmem {
+  SelWgSmem<EPT, SPL> sel;
+  DecodeSmem<kStepG> dec;
+};
+
+template <int EPT, int SPL>
 __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
-  __shared__ union {
-    SelWgSmem<EPT, SPL> sel;
-    DecodeSmem<kStepG> dec;
-  } sm;
+  __shared__ StepSmem<EPT, SPL> sm;
+  // The block list and the per-workgroup flags of the decode layout lie past
+  // every field of the selection.
+  static_assert(offsetof(DecodeSmem<kStepG>, ids) >= sizeof(SelWgSmem<EPT, SPL>),
+                "decode list overlaps the selection storage");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wg = blockIdx.x, nwg = gridDim.x;
+  const int n_slot = a.n_slot;
+  const int pair = wg / n_slot, slot = wg % n_slot;
+  const int b = pair / a.h_kv, g = pair % a.h_kv;
+  const bool failed_before = load_rec(a.sticky) != 0u;
+  const int sl = min(a.seq_len[b], a.l_cap);
+  SPOT_STEP_TS(0);
 
   // ---- 1. scoring: row r = wg % B, by its first n_sc workgroups
   const int B = a.batch;
-  const int r = wg % B, c = wg / B;
-  const int n_sc = min(kMaxScorers, (nwg - r + B - 1) / B);   // scorers of row r
-  int nv = a.n_valid ? a.n_valid[r] : a.nblk;
-  nv = nv < 0 ? 0 : (nv > a.nblk ? a.nblk : nv);
-  if (c < n_sc) {
-    const int per = (a.nblk + n_sc - 1) / n_sc;
-    const int jb = c * per, je = min(jb + per, a.nblk);
-    for (int j0 = jb + wave * kScoreRun; j0 < je; j0 += kStepG * kScoreRun)
-      score_run_rt(a, r, nv, j0, je, lane);
+  {
+    const int r = wg % B, c = wg / B;
+    const int n_sc = min(kMaxScorers, (nwg - r + B - 1) / B);   // scorers of row r
+    if (c < n_sc) {
+      int nv = a.n_valid ? a.n_valid[r] : a.nblk;
+      nv = nv < 0 ? 0 : (nv > a.nblk ? a.nblk : nv);
+      const int per = (a.nblk + n_sc - 1) / n_sc;
+      const int jb = c * per, je = min(jb + per, a.nblk);
+      for (int j0 = jb + wave * kScoreRun; j0 < je; j0 += kStepG * kScoreRun)
+        score_run_rt(a, r, nv, j0, je, lane);
+    }
   }
+  SPOT_STEP_TS(1);
 
   // ---- 2. selection of row wg by workgroup wg (wg < B is scorer 0 of it)
   if (wg < B) {
-    select_row_wg<EPT, SPL>(sm.sel, PolledScores{a.srec + (size_t)wg * kRecRow}, a.nblk, nv,
-                            a.top_p, a.k_max, a.k_min, a.n_sink, a.n_recent,
-                            a.idx + (size_t)wg * a.k_max, a.count + wg,
-                            a.mass ? a.mass + wg : nullptr,
-                            IdRecords{a.irec + (size_t)wg * a.h_kv * a.rec_len, a.rec_len,
-                                      a.h_kv});
-    clear_scores<EPT>(a.srec + (size_t)wg * kRecRow, tid * EPT, nv);
-    // The selection's LDS is reused below: every wave's LDS accesses are
-    // done; no wait for the stores in flight.
-    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-    __builtin_amdgcn_s_barrier();
+    int nv = a.n_valid ? a.n_valid[wg] : a.nblk;
+    nv = nv < 0 ? 0 : (nv > a.nblk ? a.nblk : nv);
+    uint32_t* srec = a.srec + (size_t)wg * kRecRow;
+    const SelRow r = select_row_core<EPT, SPL>(
+        sm.sel, PolledScores{srec, a.wait_ticks, failed_before || a.force_expire != 0}, nv,
+        a.top_p, a.k_max, a.k_min, a.n_sink, a.n_recent);
+    int total;
+    int pos = sel_positions(sm.sel, r.fin, total);
+    SPOT_STEP_TS(2);
+    const int n_out = r.ok ? min(total, a.k_max) : 0;
+    if (r.ok) {
+      sel_write<EPT>(a.idx + (size_t)wg * a.k_max, a.count + wg, a.mass ? a.mass + wg : nullptr,
+                     a.k_max, r.fin, pos, total, r.mass);
+      // stage the list in LDS (ascending) so that every thread shares the
+      // copies' stores
+      const int j0 = tid * EPT;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e)
+        if (((r.fin >> e) & 1u) && pos < n_out) sm.sel.hist[pos++] = (uint32_t)(j0 + e);
+    } else if (tid == 0) {
+      // The wait expired (or an earlier one did): publish an empty list.
+      if (!failed_before) store_rec(a.sticky, 1u);
+      store_rec(a.count + wg, -1);
+    }
+    __syncthreads();
+    uint32_t* lst = a.irec + (size_t)wg * a.h_kv * a.rec_len;
+    for (int i = tid; i < a.rec_len; i += kSelWG) {
+      const uint32_t wd = i < n_out ? sm.sel.hist[i] + 1u : 0xffffffffu;
+      for (int c = 0; c < a.h_kv; ++c) store_rec(lst + (size_t)c * a.rec_len + i, wd);
+    }
+    // The selector is the score records' only reader.
+    for (int j = 2 * tid; j < nv; j += 2 * kSelWG)
+      store_rec(reinterpret_cast<uint64_t*>(srec + j), (uint64_t)0);
+    SPOT_STEP_TS(3);
+    __syncthreads();   // the selection's LDS is reused below
   }
 
-  // ---- 3. attention for (pair, slot) on the published block list
-  const int pair = wg / a.n_slot, slot = wg % a.n_slot;
-  decode_body<kStepG, false>(sm.dec, PolledList{a.irec, a.h_kv, a.rec_len}, pair, slot, a.q, a.k,
-                             a.v, a.seq_len, a.h_q, a.h_kv, a.l_cap, a.scale_log2, a.n_slot,
-                             a.ws_o, a.ws_ml, a.pair_cnt, a.out, a.lse);
-  if (wave == 0) clear_list(a.irec, a.h_kv, a.rec_len, pair / a.h_kv, pair % a.h_kv, slot, a.n_slot);
+  // ---- 3. attention on this workgroup's share of the published list
+  uint32_t* lrec = a.irec + (size_t)pair * a.rec_len;
+  const int nb_valid = (sl + kBlk - 1) / kBlk;
+  if (wave == 0) {
+    const int n = poll_list(sm.dec.ids, lrec, a.rec_len, slot, n_slot, nb_valid, a.wait_ticks);
+    if (lane == 0) sm.dec.n_local = n;
+  }
+  __syncthreads();
+  int n_local = sm.dec.n_local;
+  if (n_local < 0) {
+    n_local = 0;
+    if (tid == 0) {
+      store_rec(a.sticky, 1u);
+      store_rec(a.count + b, -1);
+    }
+  }
+  SPOT_STEP_TS(4);
+
+  uint32_t qv[kD / 2];
+  load_query_heads<kStepG>(qv, a.q, b, g, a.h_q);
+  const size_t head_base = ((size_t)b * a.h_kv + g) * (size_t)a.l_cap * kD;
+  unsigned elect_prev = 0u;
+  auto elect = [&](int n) {
+    if (n == n_local - 1 && tid == 0)
+      elect_prev = __hip_atomic_fetch_add(&a.elect[pair], 1u, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+  };
+  if (n_local == 0) elect(-1);
+  auto blk_of = [&](int n) { return sm.dec.ids[n]; };
+  const HeadPartial hp = attend_blocks<kStepG>(sm.dec, qv, a.k + head_base, a.v + head_base, sl,
+                                               n_local, blk_of, a.scale_log2, elect);
+  SPOT_STEP_TS(5);
+  if (wave == 0) clear_list(lrec, a.rec_len, slot, n_slot);
+  if (tid == 0) sm.dec.last = elect_prev == (unsigned)(n_slot - 1);
+  __syncthreads();
+  const size_t bh = (size_t)b * a.h_q + g * kStepG + wave;   // wave w: head w of the group
+  uint32_t* po = a.part_o + bh * n_slot * kD;
+  uint32_t* pml = a.part_ml + bh * n_slot * 2;
+  if (!sm.dec.last) {
+    store_rec(reinterpret_cast<uint64_t*>(po + (size_t)slot * kD + 2 * lane),
+              rec_pair(hp.o0, hp.o1));
+    if (lane == 0) store_rec(reinterpret_cast<uint64_t*>(pml + 2 * slot), rec_pair(hp.M, hp.L));
+    SPOT_STEP_TS(6);
+    return;
+  }
+
+  // ---- the merger: every workgroup of the pair has bumped the counter, so
+  // it is cleared; the other slots' partials are polled, merged in slot
+  // order and cleared.
+  if (tid == 0) store_rec(&a.elect[pair], 0u);
+  uint64_t t_raw = lane < n_slot && lane != slot
+                       ? load_rec(reinterpret_cast<const uint64_t*>(pml + 2 * lane))
+                       : rec_pair(hp.M, hp.L);
+  uint64_t o_raw[kMaxSlots];
+#pragma unroll
+  for (int u = 0; u < kMaxSlots; ++u)
+    o_raw[u] = u < n_slot && u != slot
+                   ? load_rec(reinterpret_cast<const uint64_t*>(po + (size_t)u * kD + 2 * lane))
+                   : rec_pair(hp.o0, hp.o1);
+  bool done = false;
+  const uint64_t deadline = now() + a.wait_ticks;
+  for (;;) {
+    bool full = rec_pair_full(t_raw);
+#pragma unroll
+    for (int u = 0; u < kMaxSlots; ++u) full = full && rec_pair_full(o_raw[u]);
+    done = __ballot(!full) == 0ull;
+    if (done || now() > deadline) break;
+    __builtin_amdgcn_s_sleep(1);
+    if (!rec_pair_full(t_raw))
+      t_raw = load_rec(reinterpret_cast<const uint64_t*>(pml + 2 * lane));
+#pragma unroll
+    for (int u = 0; u < kMaxSlots; ++u)
+      if (!rec_pair_full(o_raw[u]))
+        o_raw[u] = load_rec(reinterpret_cast<const uint64_t*>(po + (size_t)u * kD + 2 * lane));
+  }
+  if (!done && lane == 0) {
+    store_rec(a.sticky, 1u);
+    store_rec(a.count + b, -1);
+  }
+  // A partial that never arrived counts as empty (l = 0).
+  float2 t = rec_pair_full(t_raw) ? rec_pair_value(t_raw) : make_float2(-INFINITY, 0.f);
+  if (lane >= n_slot) t = make_float2(-INFINITY, 0.f);
+  float2 o[kMaxSlots];
+#pragma unroll
+  for (int u = 0; u < kMaxSlots; ++u)
+    o[u] = rec_pair_full(o_raw[u]) ? rec_pair_value(o_raw[u]) : make_float2(0.f, 0.f);
+  merge_small(t, o, n_slot, bh, a.out, a.lse, lane);
+  SPOT_STEP_TS(7);
+  if (lane < n_slot && lane != slot) store_rec(reinterpret_cast<uint64_t*>(pml + 2 * lane), (uint64_t)0);
+#pragma unroll
+  for (int u = 0; u < kMaxSlots; ++u)
+    if (u < n_slot && u != slot)
+      store_rec(reinterpret_cast<uint64_t*>(po + (size_t)u * kD + 2 * lane), (uint64_t)0);
 }
 
 // Workgroups of one step kernel that can be resident at once (per CU times
-// the CU count), queried once per device and instantiation and cached.
+// the CU count), queried once per device and instantiation.  The value only
+// depends on the device, so concurrent first calls store the same number.
 template <int EPT, int SPL>
 int step_capacity() {
-  static int cached[64] = {0};
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  if (cached[dev] > 0) return cached[dev];
+  const int c = cached[dev].load(std::memory_order_relaxed);
+  if (c > 0) return c;
   int per_cu = 0, cus = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
           &per_cu, reinterpret_cast<const void*>(&step_kernel<EPT, SPL>), 64 * kStepG, 0) !=
@@ -266,8 +417,8 @@ int step_capacity() {
     return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return 0;
-  cached[dev] = per_cu * cus;
-  return cached[dev];
+  cached[dev].store(per_cu * cus, std::memory_order_relaxed);
+  return per_cu * cus;
 }
 
 template <int EPT, int SPL>
@@ -280,18 +431,44 @@ hipError_t launch_step_t(StepArgs& a, int n_pairs, int n_slot_max, hipStream_t s
   return hipGetLastError();
 }
 
+// Workspace of the fused path, after the three-launch path's decode
+// workspace: partial o and (m, l) record words for up to kMaxSlots slots,
+// the election counters, the sticky word (16 bytes), the score records and
+// the block list record copies.
+struct StepLayout {
+  size_t part_o, part_ml, elect, sticky, srec, irec, total;
+  int n_slot_max;
+};
+
+StepLayout step_layout(int batch, int h_q, int h_kv, int k_max) {
+  StepLayout L;
+  const int ns = decode_num_splits(batch, h_kv, k_max, kStepG);
+  L.n_slot_max = ns < kMaxSlots ? ns : kMaxSlots;
+  const size_t heads = (size_t)batch * h_q;
+  L.part_o = (decode_workspace_bytes(batch, h_q, h_kv, kD, k_max) + 15) & ~(size_t)15;
+  L.part_ml = L.part_o + heads * L.n_slot_max * kD * 4;
+  L.elect = L.part_ml + heads * L.n_slot_max * 2 * 4;
+  L.sticky = (L.elect + (size_t)batch * h_kv * 4 + 15) & ~(size_t)15;
+  L.srec = L.sticky + 16;
+  L.irec = L.srec + (size_t)batch * kRecRow * 4;
+  L.total = L.irec + (size_t)batch * h_kv * k_max * 4;
+  return L;
+}
+
+std::atomic<int> g_force_expire{0};
+
 }  // namespace
 
-// Workspace: the split-decode partials and pair counters, then (16-byte
-// aligned) the score records [batch, kRecRow] and the list records
-// [batch, h_kv, min(k_max, nblk)] (sized for k_max).
-static size_t step_records_offset(int batch, int h_q, int h_kv, int d, int k_max) {
-  return (decode_workspace_bytes(batch, h_q, h_kv, d, k_max) + 15) & ~(size_t)15;
-}
 size_t step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max) {
-  return step_records_offset(batch, h_q, h_kv, d, k_max) +
-         (size_t)batch * (kRecRow + (size_t)h_kv * k_max) * sizeof(uint32_t);
+  (void)d;
+  return step_layout(batch, h_q, h_kv, k_max).total;
 }
+
+size_t step_sticky_offset(int batch, int h_q, int h_kv, int k_max) {
+  return step_layout(batch, h_q, h_kv, k_max).sticky;
+}
+
+void step_force_expiry(int on) { g_force_expire.store(on ? 1 : 0, std::memory_order_relaxed); }
 
 bool step_fusable(int h_q, int h_kv, int nblk, int k_max) {
   if (h_q != kStepG * h_kv || nblk < 1 || nblk > kRecRow) return false;
@@ -337,16 +514,19 @@ hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_s
   a.mass = nuc_mass;
   a.out = static_cast<uint16_t*>(out);
   a.lse = lse;
-  const int n_pairs = batch * h_kv;
-  const int n_slot_max = decode_num_splits(batch, h_kv, k_max, kStepG);
-  a.ws_o = static_cast<float*>(ws);
-  a.ws_ml = a.ws_o + (size_t)batch * h_q * n_slot_max * kD;
-  a.pair_cnt = reinterpret_cast<unsigned*>(a.ws_ml + (size_t)batch * h_q * n_slot_max * 2);
-  a.srec = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) +
-                                       step_records_offset(batch, h_q, h_kv, kD, k_max));
-  a.irec = a.srec + (size_t)batch * kRecRow;
+  const StepLayout L = step_layout(batch, h_q, h_kv, k_max);
+  char* base = static_cast<char*>(ws);
+  a.part_o = reinterpret_cast<uint32_t*>(base + L.part_o);
+  a.part_ml = reinterpret_cast<uint32_t*>(base + L.part_ml);
+  a.elect = reinterpret_cast<unsigned*>(base + L.elect);
+  a.sticky = reinterpret_cast<uint32_t*>(base + L.sticky);
+  a.srec = reinterpret_cast<uint32_t*>(base + L.srec);
+  a.irec = reinterpret_cast<uint32_t*>(base + L.irec);
   a.rec_len = k_max < a.nblk ? k_max : a.nblk;
-  // The partial buffers are laid out for n_slot_max; a smaller n_slot (when
+  a.wait_ticks = kWaitTicks;
+  a.force_expire = g_force_expire.load(std::memory_order_relaxed);
+  const int n_pairs = batch * h_kv;
+  // The partial records are laid out for n_slot_max; a smaller n_slot (when
   // fewer workgroups fit) uses a prefix of each head's run, indexed with the
   // actual n_slot -- the layout is [B, h_q, n_slot] either way.
   int P = 1;
@@ -356,7 +536,7 @@ hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_s
   const int ept = a.nblk <= 256 ? 1 : a.nblk <= 512 ? 2 : a.nblk <= 1024 ? 4
                 : a.nblk <= 2048 ? 8 : 16;
 #define SPOT_STEP_CASE(E, S) \
-  if (ept == E && spl == S) return launch_step_t<E, S>(a, n_pairs, n_slot_max, s);
+  if (ept == E && spl == S) return launch_step_t<E, S>(a, n_pairs, L.n_slot_max, s);
 #define SPOT_STEP_E(E) SPOT_STEP_CASE(E, 1) SPOT_STEP_CASE(E, 2) SPOT_STEP_CASE(E, 4) \
   SPOT_STEP_CASE(E, 8)
   SPOT_STEP_E(1)

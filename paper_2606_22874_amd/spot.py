@@ -23,7 +23,8 @@ from . import build as _build
 
 SPOT_OK = 0
 STATUS = {0: "ok", 1: "null pointer", 2: "invalid shape", 3: "unsupported", 4: "invalid rule",
-          5: "workspace", 6: "HIP launch error"}
+          5: "workspace", 6: "HIP launch error", 7: "fused-step wait expired"}
+SPOT_ERR_EXPIRED = 7
 KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2, "int8": 3, "mxfp8": 4}
 BLK = 64
 
@@ -33,6 +34,7 @@ SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score",
            "spot_select_blocks",
            "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
            "spot_sparse_prefill", "spot_decode_step_workspace_bytes", "spot_decode_step",
+           "spot_decode_step_status", "spot_test_force_expiry",
            "spot_probe_stream_read", "spot_probe_sink_words"]
 
 
@@ -78,13 +80,17 @@ def load(path: Optional[str] = None):
         L.spot_decode_step_workspace_bytes.restype = Z
         L.spot_decode_step.argtypes = [P, P, P, P, I, I, I, P, F, I, I, I, I, P, P, P, P, I, I,
                                        I, I, I, F, P, P, P, P, P, P, P, Z, P]
+        L.spot_decode_step_status.argtypes = [P, Z, I, I, I, I, I, P]
+        L.spot_test_force_expiry.argtypes = [I]
+        L.spot_test_force_expiry.restype = None
         L.spot_probe_stream_read.argtypes = [P, Z, P, P]
         L.spot_probe_stream_read.restype = ctypes.c_int32
         L.spot_probe_sink_words.restype = I
         for name in ("spot_selector_score", "spot_selector_score_q", "spot_selector_score_tokens",
                      "spot_selector_project",
                      "spot_selector_pool", "spot_select_blocks", "spot_sparse_decode",
-                     "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step"):
+                     "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step",
+                     "spot_decode_step_status"):
             getattr(L, name).restype = ctypes.c_int32
         if path is None:
             _lib = L
@@ -327,6 +333,22 @@ def spot_decode_step(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k
         batch, h_q, h_kv, d, l_cap, float(sm_scale), _ptr(scores), _ptr(idx), _ptr(count),
         _ptr(nuc_mass), _ptr(out), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def spot_decode_step_status(ws, batch, h_q, h_kv, d, k_max, stream=None) -> int:
+    """Status of a fused-step workspace: SPOT_OK, or SPOT_ERR_EXPIRED after a
+    bounded wait expired (the workspace is then zero-filled again).  Any other
+    status raises."""
+    _dev(ws, "ws", None)
+    st = load().spot_decode_step_status(_ptr(ws), ws.numel() * ws.element_size(), batch, h_q,
+                                        h_kv, d, k_max, _stream(stream))
+    if st not in (SPOT_OK, SPOT_ERR_EXPIRED):
+        raise SpotError("spot_decode_step_status", st)
+    return int(st)
+
+
+def spot_test_force_expiry(on: bool):
+    load().spot_test_force_expiry(1 if on else 0)
 
 
 def spot_probe_stream_read(buf, sink, stream=None):

@@ -32,6 +32,43 @@ def lib():
     return spot.load()
 
 
+# Declarations that are not steps of the method: names, sizes, status, the
+# measurement probe and the test hook.  Every other entry point must cite the
+# passage of the paper it implements in the comment block above it.
+UNCITED_HELPERS = ("spot_status_str", "spot_version", "spot_probe_stream_read",
+                   "spot_probe_sink_words", "spot_decode_workspace_bytes",
+                   "spot_decode_step_workspace_bytes", "spot_decode_step_status",
+                   "spot_test_force_expiry")
+CITATION = re.compile(r"\b(Section|Sections|Eqs?\.|Table|Appendix)\s+[A-Z0-9]")
+
+
+def declaration_comments():
+    """(name, comment block right above its declaration) for every entry point."""
+    out = []
+    for fn in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if not fn.endswith(".h"):
+            continue
+        text = open(os.path.join(ROOT, "include", fn)).read()
+        last_comment = ""
+        pos = 0
+        for m in re.finditer(r"/\*.*?\*/|\b(spot_\w+)\s*\(", text, flags=re.S):
+            if m.group(0).startswith("/*"):
+                last_comment = m.group(0)
+            else:
+                out.append((m.group(1), last_comment))
+            pos = m.end()
+    return out
+
+
+def test_every_entry_point_cites_the_paper():
+    decls = declaration_comments()
+    assert {n for n, _ in decls} == set(declared_functions())
+    for name, comment in decls:
+        if name in UNCITED_HELPERS:
+            continue
+        assert CITATION.search(comment), f"{name}: no Section/Eq./Table/Appendix citation"
+
+
 def test_header_declares_the_five_calls():
     names = declared_functions()
     for n in ("spot_selector_score", "spot_select_blocks", "spot_sparse_decode",
@@ -51,8 +88,9 @@ def test_exports_every_declared_symbol(lib):
 
 def test_version_and_status_strings(lib):
     assert b"gfx950" in lib.spot_version()
-    for s in range(7):
+    for s in range(8):
         assert lib.spot_status_str(s)
+    assert b"expired" in lib.spot_status_str(7)
 
 
 def test_validation_errors_before_launch(lib):
@@ -168,6 +206,16 @@ def test_validation_errors_before_launch(lib):
     # list records per sequence
     assert lib.spot_decode_step_workspace_bytes(4, 32, 8, 128, 128) >= \
         lib.spot_decode_workspace_bytes(4, 32, 8, 128, 128) + 4 * (4096 + 8 * 128) * 4
+
+
+def test_step_status_validation(lib):
+    P = ctypes.c_void_p
+    nz = P(16)   # never dereferenced: validation fails first
+    st = lib.spot_decode_step_status
+    assert st(None, 1 << 20, 4, 32, 8, 128, 128, None) == 1
+    assert st(nz, 1 << 20, 0, 32, 8, 128, 128, None) == 2
+    assert st(nz, 16, 4, 32, 8, 128, 128, None) == 5
+    assert st(P(24), 1 << 30, 4, 32, 8, 128, 128, None) == 5
 
 
 def test_workspace_size_query(lib):

@@ -80,12 +80,19 @@ def fused(x, wl, ws=None):
                             n_valid=x["n_valid"], sm_scale=wl.sm_scale, ws=ws)
 
 
-def assert_same(sep, fus):
+def assert_same(sep, fus, bitwise=False):
+    """Scores and block sets equal; with bitwise=True (same selection kernel
+    and the same attention split on both paths) every output bit for bit."""
     s0, i0, c0, m0, o0, l0 = sep
     s1, i1, c1, m1, o1, l1 = fus
     assert torch.equal(s0, s1), "scores differ"
     assert torch.equal(c0, c1), "counts differ"
     assert torch.equal(i0, i1), "block sets differ"
+    if bitwise:
+        assert torch.equal(m0, m1), "nucleus mass differs"
+        assert torch.equal(o0, o1), "outputs differ"
+        assert torch.equal(l0, l1), "lse differs"
+        return
     assert torch.allclose(m0, m1, rtol=1e-5, atol=1e-7), "nucleus mass differs"
     assert torch.max(torch.abs(o0.float() - o1.float())).item() <= 1e-2
     assert torch.max(torch.abs(l0 - l1)).item() <= 1e-4
@@ -100,7 +107,9 @@ def test_step_matches_separate_calls(cfg, fmt):
     sep = separate(x, wl)
     fus = fused(x, wl)
     torch.cuda.synchronize()
-    assert_same(sep, fus)
+    # 2048 blocks: both paths select with the workgroup core and split the
+    # attention 16 ways, so every output matches bit for bit.
+    assert_same(sep, fus, bitwise=(cfg == 3))
 
 
 def test_step_end_to_end_vs_oracle():
@@ -167,15 +176,55 @@ def test_step_repeated_calls_reset_workspace():
     torch.cuda.synchronize()
     for sep, fus in results:
         assert_same(sep, fus)
-    # Everything past the split partials -- one completion counter per
-    # (sequence, KV head) pair, then the score and block list records -- is
-    # back to zero.
+    # The fused launch's region (partial records, election counters, expiry
+    # word, score record copies) and the three-launch path's completion
+    # counters are back to zero.
     n_bytes = spot.spot_decode_step_workspace_bytes(wl.B, wl.Hq, wl.Hkv, wl.d, wl.rule.k_max)
     dec_bytes = spot.spot_decode_workspace_bytes(wl.B, wl.Hq, wl.Hkv, wl.d, wl.rule.k_max)
-    start = dec_bytes - 4 * wl.B * wl.Hkv
+    start = (dec_bytes + 15) // 16 * 16
     tail = ws[start:n_bytes].view(torch.int32)
-    assert tail.numel() >= wl.B * wl.Hkv + wl.B * 4096 + wl.B * wl.Hkv * wl.rule.k_max
+    assert tail.numel() >= wl.B * 4096 + wl.B * wl.Hkv * wl.rule.k_max + wl.B * wl.Hq * 16 * 130
     assert int(torch.count_nonzero(tail).item()) == 0
+    counters = ws[dec_bytes - 4 * wl.B * wl.Hkv:dec_bytes].view(torch.int32)
+    assert int(torch.count_nonzero(counters).item()) == 0
+    assert spot.spot_decode_step_status(ws, wl.B, wl.Hq, wl.Hkv, wl.d, wl.rule.k_max) == 0
+
+
+def test_step_expired_wait_is_reported():
+    """A fused step whose waits expire (forced from the host: every
+    workgroup's wait for its sequence's scores gives up at once, so every
+    kernel still exits normally) attends to nothing, reports count = -1 and
+    sets the workspace's expiry word; later calls on that workspace do the
+    same without waiting until spot_decode_step_status reports the expiry and
+    restores the workspace, after which a call equals the three separate
+    calls bit for bit."""
+    wl = workload(3)
+    x = inputs(wl, "bf16")
+    args = (wl.B, wl.Hq, wl.Hkv, wl.d, wl.rule.k_max)
+    ws = spot.step_workspace(*args, DEV)
+    sep = separate(x, wl)
+    print("[step] forced expiry", flush=True)
+    spot.spot_test_force_expiry(True)
+    try:
+        s1, _, c1, _, o1, l1 = fused(x, wl, ws)
+        torch.cuda.synchronize()
+    finally:
+        spot.spot_test_force_expiry(False)
+    assert torch.equal(s1, sep[0])                    # scoring never waits
+    assert torch.all(c1 == -1)
+    assert torch.all(o1.float() == 0) and torch.all(torch.isinf(l1))
+    # the word is sticky: a normal call on the same workspace does not wait
+    print("[step] call after the expiry", flush=True)
+    _, _, c2, _, o2, _ = fused(x, wl, ws)
+    torch.cuda.synchronize()
+    assert torch.all(c2 == -1) and torch.all(o2.float() == 0)
+    assert spot.spot_decode_step_status(ws, *args) == spot.SPOT_ERR_EXPIRED
+    assert int(torch.count_nonzero(ws).item()) == 0   # zero-filled again
+    assert spot.spot_decode_step_status(ws, *args) == 0
+    print("[step] normal call after the reset", flush=True)
+    fus = fused(x, wl, ws)
+    torch.cuda.synchronize()
+    assert_same(sep, fus, bitwise=True)
 
 
 def test_step_ragged_sequences():
