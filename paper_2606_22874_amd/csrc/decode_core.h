@@ -379,29 +379,67 @@ __device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
   };
 
   // Two register stages: while block n is computed, blocks n+1 and n+2 are
-  // loading.
-  if (n_local > 0) {
+  // loading.  The steady-state loop issues both prefetches unconditionally,
+  // so the compiler's wait before each stage's first use counts only that
+  // stage's loads (a conditional prefetch makes it wait for every load in
+  // flight, which serialises the stream); the last one or two blocks run
+  // after the loop.
+  int n = 0;
+  if (n_local >= 4) {
     load_slice<NLD>(krA, vrA, kw, vw, blk_of(0), lane);
     issued(0);
-  }
-  if (n_local > 1) {
     load_slice<NLD>(krB, vrB, kw, vw, blk_of(1), lane);
     issued(1);
-  }
-  for (int n = 0; n < n_local; n += 2) {
+    for (; n + 3 < n_local; n += 2) {
+      consume(krA, vrA);
+      load_slice<NLD>(krA, vrA, kw, vw, blk_of(n + 2), lane);
+      issued(n + 2);
+      compute(blk_of(n));
+      consume(krB, vrB);
+      load_slice<NLD>(krB, vrB, kw, vw, blk_of(n + 3), lane);
+      issued(n + 3);
+      compute(blk_of(n + 1));
+    }
+    // n_local - n is 2 or 3: blocks n and n + 1 are in flight
     consume(krA, vrA);
     if (n + 2 < n_local) {
       load_slice<NLD>(krA, vrA, kw, vw, blk_of(n + 2), lane);
       issued(n + 2);
     }
     compute(blk_of(n));
-    if (n + 1 < n_local) {
+    consume(krB, vrB);
+    compute(blk_of(n + 1));
+    if (n + 2 < n_local) {
+      consume(krA, vrA);
+      compute(blk_of(n + 2));
+    }
+  } else {
+    if (n_local > 0) {
+      load_slice<NLD>(krA, vrA, kw, vw, blk_of(0), lane);
+      issued(0);
+    }
+    if (n_local > 1) {
+      load_slice<NLD>(krB, vrB, kw, vw, blk_of(1), lane);
+      issued(1);
+    }
+    if (n_local > 2) {
+      consume(krA, vrA);
+      compute(blk_of(0));
+      load_slice<NLD>(krA, vrA, kw, vw, blk_of(2), lane);
+      issued(2);
       consume(krB, vrB);
-      if (n + 3 < n_local) {
-        load_slice<NLD>(krB, vrB, kw, vw, blk_of(n + 3), lane);
-        issued(n + 3);
+      compute(blk_of(1));
+      consume(krA, vrA);
+      compute(blk_of(2));
+    } else {
+      if (n_local > 0) {
+        consume(krA, vrA);
+        compute(blk_of(0));
       }
-      compute(blk_of(n + 1));
+      if (n_local > 1) {
+        consume(krB, vrB);
+        compute(blk_of(1));
+      }
     }
   }
 

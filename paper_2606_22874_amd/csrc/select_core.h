@@ -185,7 +185,9 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 //     candidates in better bins [1]; every wave ranks the members by
 //     counting and derives the
 //     packed cut key and the mass of the survivors.  The survivors are the
-//     candidates whose packed key reaches the cut.  A bin too crowded to
+//     candidates whose packed key reaches the cut (when the cap-th best
+//     candidate is the last of its bin, simply the candidates of that bin
+//     and the better ones, with no packing or ranking).  A bin too crowded to
 //     rank (heavy ties) falls back to an 8-bit radix select on the keys;
 //  3. below top_p * Z the cap binds and the survivors are the answer;
 //     otherwise they are compacted [2], sorted in wave 0 by (score desc, id
@@ -283,6 +285,8 @@ __device__ __forceinline__ SelRow select_row_core(SelWgSmem<EPT, SPL>& sm, const
   float msum = 0.f;
   bool have_msum = false;
   bool crowded = thresh;
+  bool by_bin = false;        // the survivors are exactly the candidates in bins <= b*
+  uint32_t surv_bin = 0u;
   if (thresh) {
     const float vhi = M, vlo = order_key_inv(kmin);
     const float span = vhi - vlo;
@@ -319,7 +323,14 @@ __device__ __forceinline__ SelRow select_row_core(SelWgSmem<EPT, SPL>& sm, const
       const int need = cap - __builtin_amdgcn_readlane(f_incl - fc, fb);
       const int in_bin = __builtin_amdgcn_readlane(fc, fb);
       SPOT_SEL_TS(7);
-      if (in_bin <= 64) {
+      if (in_bin == need) {
+        // The cap-th best candidate is the last of its bin: every candidate
+        // of the bin and of the better bins survives, no ranking needed.
+        crowded = false;
+        by_bin = true;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) surv_bin |= (uint32_t)(key[e] && bin[e] <= b_star) << e;
+      } else if (in_bin <= 64) {
         crowded = false;
         // each wave packs its members of the bin into its own run of s_K and
         // sums the mass of its candidates in better bins
@@ -430,12 +441,14 @@ __device__ __forceinline__ SelRow select_row_core(SelWgSmem<EPT, SPL>& sm, const
     kt = prefix;
     it = sm.bc[2];
   }
-  // survivor bits (key > kt, or key == kt and id <= it)
-  uint32_t surv = 0u;
+  // survivor bits (key > kt, or key == kt and id <= it; or by bin)
+  uint32_t surv = surv_bin;
+  if (!by_bin) {
 #pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    const bool sv_ = key[e] && (key[e] > kt || (key[e] == kt && j0 + e <= it));
-    surv |= (uint32_t)sv_ << e;
+    for (int e = 0; e < EPT; ++e) {
+      const bool sv_ = key[e] && (key[e] > kt || (key[e] == kt && j0 + e <= it));
+      surv |= (uint32_t)sv_ << e;
+    }
   }
   if (!have_msum) {
     float ms = 0.f;

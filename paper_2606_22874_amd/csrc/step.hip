@@ -92,8 +92,7 @@ struct StepArgs {
   unsigned* elect;     // [batch * h_kv] merger election counters
   uint32_t* sticky;    // expiry word (one per workspace)
   uint32_t* srec;      // [batch, kRecRow] score records
-  uint32_t* irec;      // [batch * h_kv, rec_len] block list record copies, one per pair
-  int rec_len;         // min(k_max, nblk)
+  uint32_t* brec;      // [batch * h_kv, kBitWords] selected-set bitmap copies, one per pair
   uint64_t wait_ticks;
   int force_expire;    // test hook: every score wait gives up at once
 };
@@ -154,7 +153,6 @@ struct PolledScores {
 #pragma unroll
         for (int e = 0; e < EPT; ++e) all = all && (j0 + e >= nv || wd[e] != 0u);
         if (all || now() > deadline) break;
-        __builtin_amdgcn_s_sleep(1);
       }
     }
 #pragma unroll
@@ -163,37 +161,69 @@ struct PolledScores {
   }
 };
 
-// Block list source of an attention workgroup: entries slot, slot + n_slot,
-// ... of its pair's copy of the list records (the stand-alone decode's share
-// of the same list, in the same order), polled by wave 0 until written; an id
-// at or past nb_valid is skipped.  Returns the share's length, or -1 when the
-// wait expired.  clear_list() zeroes the same words after the attention.
-__device__ __forceinline__ int poll_list(int* ids, const uint32_t* rec, int rec_len, int slot,
-                                         int n_slot, int nb_valid, uint64_t ticks) {
+// The selected set of a row travels as a bitmap: record word w holds the
+// bits of ids [16w, 16w + 16) in its low half and kBitFlag (so that every
+// written word is nonzero).  An attention workgroup's wave 0 polls its pair's
+// copy, scans the bit counts over the lanes and takes the entries slot, slot
+// + n_slot, ... of the ascending list whose ids lie below nb_valid (the
+// stand-alone decode's share of the same list, in the same order).  Returns
+// the share's length, or -1 when the wait expired.
+constexpr uint32_t kBitFlag = 0x10000u;
+constexpr int kBitWords = kRecRow / 16;   // bitmap words per copy
+
+__device__ __forceinline__ int poll_bitmap(int* ids, const uint32_t* rec, int nwords, int k_max,
+                                           int slot, int n_slot, int nb_valid, uint64_t ticks,
+                                           bool give_up) {
   const int lane = __lane_id();
-  const uint64_t deadline = now() + ticks;
-  int cnt = 0;
-  bool expired = false;
-  for (int base = slot; base < rec_len; base += 64 * n_slot) {
-    const int e = base + lane * n_slot;
-    uint32_t wd = e < rec_len ? 0u : 0xffffffffu;
+  // lane l: words [4l, 4l + 4), ids [64l, 64l + 64)
+  uint32_t wd[4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x) wd[x] = 4 * lane + x < nwords ? 0u : kBitFlag;
+  bool expired = give_up;
+  if (!give_up) {
+    const uint64_t deadline = now() + ticks;
     for (;;) {
-      if (wd == 0u) wd = load_rec(rec + e);
-      if (__ballot(wd == 0u) == 0ull) break;
+#pragma unroll
+      for (int x = 0; x < 4; x += 2) {
+        if (wd[x] == 0u || wd[x + 1] == 0u) {
+          const uint64_t v = load_rec(reinterpret_cast<const uint64_t*>(rec + 4 * lane + x));
+          if (wd[x] == 0u) wd[x] = (uint32_t)v;
+          if (wd[x + 1] == 0u) wd[x + 1] = (uint32_t)(v >> 32);
+        }
+      }
+      const bool mine = wd[0] && wd[1] && wd[2] && wd[3];
+      if (__ballot(!mine) == 0ull) break;
       if (now() > deadline) {
         expired = true;
         break;
       }
-      __builtin_amdgcn_s_sleep(1);
     }
-    const int j = wd == 0u || wd == 0xffffffffu ? -1 : (int)(wd - 1u);
-    cnt = append_ids(ids, cnt, j, nb_valid);
   }
-  return expired ? -1 : min(cnt, kMaxIds);
-}
-
-__device__ __forceinline__ void clear_list(uint32_t* rec, int rec_len, int slot, int n_slot) {
-  for (int e = slot + __lane_id() * n_slot; e < rec_len; e += 64 * n_slot) store_rec(rec + e, 0u);
+  if (expired) return -1;
+  uint64_t bits = 0;
+#pragma unroll
+  for (int x = 0; x < 4; ++x) bits |= (uint64_t)(wd[x] & 0xffffu) << (16 * x);
+  const int base_id = 64 * lane;
+  // entries below k_max and below nb_valid only (the list ascends, so the
+  // valid ids are a prefix of it)
+  const uint64_t valid = base_id >= nb_valid ? 0ull
+                         : nb_valid - base_id >= 64 ? ~0ull
+                                                    : (1ull << (nb_valid - base_id)) - 1ull;
+  const int cnt = __popcll(bits);
+  const int incl = wave_incl_scan_i(cnt);
+  int pos = incl - cnt;
+  const int total = min(__builtin_amdgcn_readlane(incl, 63), k_max);
+  const int n_ok = min(wave_sum_i(__popcll(bits & valid)), total);
+  while (bits) {
+    const int bit = __builtin_ctzll(bits);
+    bits &= bits - 1ull;
+    if (pos < n_ok && pos >= slot && (pos - slot) % n_slot == 0) {
+      const int kk = (pos - slot) / n_slot;
+      if (kk < kMaxIds) ids[kk] = base_id + bit;
+    }
+    ++pos;
+  }
+  return n_ok > slot ? min((n_ok - slot + n_slot - 1) / n_slot, kMaxIds) : 0;
 }
 
 template <int KFMT, int LPH>
@@ -274,29 +304,31 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
     const SelRow r = select_row_core<EPT, SPL>(
         sm.sel, PolledScores{srec, a.wait_ticks, failed_before || a.force_expire != 0}, nv,
         a.top_p, a.k_max, a.k_min, a.n_sink, a.n_recent);
-    int total;
-    int pos = sel_positions(sm.sel, r.fin, total);
     SPOT_STEP_TS(2);
-    const int n_out = r.ok ? min(total, a.k_max) : 0;
+    // Publish the set as a bitmap right away (the lanes of a 16-id word
+    // combine their bits with shuffles), then write idx / count / nuc_mass.
+    {
+      constexpr int K = 16 / EPT;   // threads per bitmap word
+      uint32_t wb = r.ok ? r.fin : 0u;
+#pragma unroll
+      for (int d = 1; d < K; d <<= 1) wb |= (uint32_t)__shfl_down((int)wb, d, 64) << (d * EPT);
+      const int nwords = (a.nblk + 15) / 16;
+      const int w = tid * EPT / 16;
+      if (tid % K == 0 && w < nwords) {
+        uint32_t* bm = a.brec + (size_t)wg * a.h_kv * kBitWords + w;
+        const uint32_t word = (wb & 0xffffu) | kBitFlag;
+        for (int c = 0; c < a.h_kv; ++c) store_rec(bm + (size_t)c * kBitWords, word);
+      }
+    }
+    int total;
+    const int pos = sel_positions(sm.sel, r.fin, total);
     if (r.ok) {
       sel_write<EPT>(a.idx + (size_t)wg * a.k_max, a.count + wg, a.mass ? a.mass + wg : nullptr,
                      a.k_max, r.fin, pos, total, r.mass);
-      // stage the list in LDS (ascending) so that every thread shares the
-      // copies' stores
-      const int j0 = tid * EPT;
-#pragma unroll
-      for (int e = 0; e < EPT; ++e)
-        if (((r.fin >> e) & 1u) && pos < n_out) sm.sel.hist[pos++] = (uint32_t)(j0 + e);
     } else if (tid == 0) {
-      // The wait expired (or an earlier one did): publish an empty list.
+      // The wait expired (or an earlier one did): an empty set was published.
       if (!failed_before) store_rec(a.sticky, 1u);
       store_rec(a.count + wg, -1);
-    }
-    __syncthreads();
-    uint32_t* lst = a.irec + (size_t)wg * a.h_kv * a.rec_len;
-    for (int i = tid; i < a.rec_len; i += kSelWG) {
-      const uint32_t wd = i < n_out ? sm.sel.hist[i] + 1u : 0xffffffffu;
-      for (int c = 0; c < a.h_kv; ++c) store_rec(lst + (size_t)c * a.rec_len + i, wd);
     }
     // The selector is the score records' only reader.
     for (int j = 2 * tid; j < nv; j += 2 * kSelWG)
@@ -305,11 +337,12 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
     __syncthreads();   // the selection's LDS is reused below
   }
 
-  // ---- 3. attention on this workgroup's share of the published list
-  uint32_t* lrec = a.irec + (size_t)pair * a.rec_len;
+  // ---- 3. attention on this workgroup's share of the published set
+  uint32_t* bmap = a.brec + (size_t)pair * kBitWords;
   const int nb_valid = (sl + kBlk - 1) / kBlk;
   if (wave == 0) {
-    const int n = poll_list(sm.dec.ids, lrec, a.rec_len, slot, n_slot, nb_valid, a.wait_ticks);
+    const int n = poll_bitmap(sm.dec.ids, bmap, (a.nblk + 15) / 16, a.k_max, slot, n_slot,
+                              nb_valid, a.wait_ticks, false);
     if (lane == 0) sm.dec.n_local = n;
   }
   __syncthreads();
@@ -337,7 +370,6 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
   const HeadPartial hp = attend_blocks<kStepG>(sm.dec, qv, a.k + head_base, a.v + head_base, sl,
                                                n_local, blk_of, a.scale_log2, elect);
   SPOT_STEP_TS(5);
-  if (wave == 0) clear_list(lrec, a.rec_len, slot, n_slot);
   if (tid == 0) sm.dec.last = elect_prev == (unsigned)(n_slot - 1);
   __syncthreads();
   const size_t bh = (size_t)b * a.h_q + g * kStepG + wave;   // wave w: head w of the group
@@ -351,10 +383,12 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
     return;
   }
 
-  // ---- the merger: every workgroup of the pair has bumped the counter, so
-  // it is cleared; the other slots' partials are polled, merged in slot
-  // order and cleared.
+  // ---- the merger: every workgroup of the pair has bumped the counter (so
+  // each has read the pair's bitmap): both are cleared; the other slots'
+  // partials are polled, merged in slot order and cleared.
   if (tid == 0) store_rec(&a.elect[pair], 0u);
+  for (int w = 2 * tid; w < (a.nblk + 15) / 16; w += 2 * kSelWG)
+    store_rec(reinterpret_cast<uint64_t*>(bmap + w), (uint64_t)0);
   uint64_t t_raw = lane < n_slot && lane != slot
                        ? load_rec(reinterpret_cast<const uint64_t*>(pml + 2 * lane))
                        : rec_pair(hp.M, hp.L);
@@ -434,9 +468,9 @@ hipError_t launch_step_t(StepArgs& a, int n_pairs, int n_slot_max, hipStream_t s
 // Workspace of the fused path, after the three-launch path's decode
 // workspace: partial o and (m, l) record words for up to kMaxSlots slots,
 // the election counters, the sticky word (16 bytes), the score records and
-// the block list record copies.
+// the selected-set bitmap copies.
 struct StepLayout {
-  size_t part_o, part_ml, elect, sticky, srec, irec, total;
+  size_t part_o, part_ml, elect, sticky, srec, brec, total;
   int n_slot_max;
 };
 
@@ -450,8 +484,8 @@ StepLayout step_layout(int batch, int h_q, int h_kv, int k_max) {
   L.elect = L.part_ml + heads * L.n_slot_max * 2 * 4;
   L.sticky = (L.elect + (size_t)batch * h_kv * 4 + 15) & ~(size_t)15;
   L.srec = L.sticky + 16;
-  L.irec = L.srec + (size_t)batch * kRecRow * 4;
-  L.total = L.irec + (size_t)batch * h_kv * k_max * 4;
+  L.brec = L.srec + (size_t)batch * kRecRow * 4;
+  L.total = L.brec + (size_t)batch * h_kv * kBitWords * 4;
   return L;
 }
 
@@ -521,8 +555,7 @@ hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_s
   a.elect = reinterpret_cast<unsigned*>(base + L.elect);
   a.sticky = reinterpret_cast<uint32_t*>(base + L.sticky);
   a.srec = reinterpret_cast<uint32_t*>(base + L.srec);
-  a.irec = reinterpret_cast<uint32_t*>(base + L.irec);
-  a.rec_len = k_max < a.nblk ? k_max : a.nblk;
+  a.brec = reinterpret_cast<uint32_t*>(base + L.brec);
   a.wait_ticks = kWaitTicks;
   a.force_expire = g_force_expire.load(std::memory_order_relaxed);
   const int n_pairs = batch * h_kv;
