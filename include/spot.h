@@ -383,6 +383,30 @@ spot_status spot_decode_step(const void *q_sel, const float *w, const void *k_se
                              float *lse, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * spot_decode_step_static -- spot_decode_step for callers that cannot
+ * allocate: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, outputs and results as spot_decode_step,
+ * without ws / ws_bytes: the workspace is an array of 8 MiB in the library's
+ * device memory, one per GPU, held until the process ends (the first call on
+ * a device looks it up and zero-fills it with a kernel on `stream`; every
+ * call leaves it zeroed again).  The call allocates and frees nothing.
+ * Errors: those of spot_decode_step, and SPOT_ERR_WORKSPACE when
+ * spot_decode_step_workspace_bytes(batch, h_q, h_kv, d, k_max) exceeds 8 MiB.
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on the same GPU (other streams, other threads) race and give undefined
+ * results.  Its expiry word is read and cleared by
+ * spot_decode_step_status(NULL, ...).
+ */
+spot_status spot_decode_step_static(const void *q_sel, const float *w, const void *k_sel,
+                                    const void *k_scale, int kfmt, int h_s, int d_s,
+                                    const int32_t *n_valid, float top_p, int k_max, int k_min,
+                                    int n_sink, int n_recent, const void *q, const void *k,
+                                    const void *v, const int32_t *seq_len, int batch, int h_q,
+                                    int h_kv, int d, int l_cap, float sm_scale, float *scores,
+                                    int32_t *idx, int32_t *count, float *nuc_mass, void *out,
+                                    float *lse, void *stream);
+
+/*
  * spot_decode_step_status -- the expiry word of a fused-step workspace.
  *
  * Waits for `stream`, then reads the sticky expiry word that spot_decode_step
@@ -391,8 +415,10 @@ spot_status spot_decode_step(const void *q_sel, const float *w, const void *k_se
  * whole workspace (spot_decode_step_workspace_bytes for these sizes) on
  * `stream`, waits for that, and returns SPOT_ERR_EXPIRED: the next
  * spot_decode_step on the workspace runs normally again.  The sizes are
- * those of the spot_decode_step calls that use ws.  Errors: SPOT_ERR_NULL,
- * SPOT_ERR_SHAPE, SPOT_ERR_WORKSPACE (too small or misaligned), SPOT_ERR_HIP.
+ * those of the spot_decode_step calls that use ws.  ws == NULL means the
+ * current device's array of spot_decode_step_static (SPOT_OK if that has not
+ * been used on the device).  Errors: SPOT_ERR_SHAPE, SPOT_ERR_WORKSPACE (too
+ * small or misaligned), SPOT_ERR_HIP.
  * This is the library's only synchronising call.
  */
 spot_status spot_decode_step_status(void *ws, size_t ws_bytes, int batch, int h_q, int h_kv,

@@ -202,14 +202,17 @@ size_t spot_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d, int
   return step_workspace_bytes(batch, h_q, h_kv, d, k_max);
 }
 
-spot_status spot_decode_step(const void* q_sel, const float* w, const void* k_sel,
+}  // extern "C"
+
+static spot_status decode_step_impl(const void* q_sel, const float* w, const void* k_sel,
                              const void* k_scale, int kfmt, int h_s, int d_s,
                              const int32_t* n_valid, float top_p, int k_max, int k_min,
                              int n_sink, int n_recent, const void* q, const void* k,
                              const void* v, const int32_t* seq_len, int batch, int h_q,
                              int h_kv, int d, int l_cap, float sm_scale, float* scores,
                              int32_t* idx, int32_t* count, float* nuc_mass, void* out,
-                             float* lse, void* ws, size_t ws_bytes, void* stream) {
+                             float* lse, void* ws, size_t ws_bytes, bool static_ws,
+                             void* stream) {
   spot_status st = check_decode(q, k, v, seq_len, out, batch, h_q, h_kv, d, l_cap);
   if (st != SPOT_OK) return st;
   if (!q_sel || !w || !k_sel || !scores || !idx || !count) return SPOT_ERR_NULL;
@@ -224,9 +227,16 @@ spot_status spot_decode_step(const void* q_sel, const float* w, const void* k_se
   const int nblk = l_cap / kBlk;
   if (nblk > 16384 || k_max > 4096) return SPOT_ERR_UNSUPPORTED;
   if (batch == 0) return SPOT_OK;
-  if (!ws || ws_bytes < step_workspace_bytes(batch, h_q, h_kv, d, k_max) || misaligned(ws))
-    return SPOT_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (static_ws) {
+    // the device's static scratch: no allocation, a size limit instead
+    if (step_workspace_bytes(batch, h_q, h_kv, d, k_max) > static_scratch_bytes())
+      return SPOT_ERR_WORKSPACE;
+    if (static_scratch(&ws, true, s) != hipSuccess) return SPOT_ERR_HIP;
+  } else if (!ws || ws_bytes < step_workspace_bytes(batch, h_q, h_kv, d, k_max) ||
+             misaligned(ws)) {
+    return SPOT_ERR_WORKSPACE;
+  }
   if (step_fusable(h_q, h_kv, nblk, k_max)) {
     const hipError_t e = launch_decode_step(q_sel, w, k_sel, k_scale, kfmt, d_s, n_valid, top_p,
                                             k_max, k_min, n_sink, n_recent, q, k, v, seq_len,
@@ -247,13 +257,47 @@ spot_status spot_decode_step(const void* q_sel, const float* w, const void* k_se
   return from_hip(e);
 }
 
+extern "C" {
+
+spot_status spot_decode_step(const void* q_sel, const float* w, const void* k_sel,
+                             const void* k_scale, int kfmt, int h_s, int d_s,
+                             const int32_t* n_valid, float top_p, int k_max, int k_min,
+                             int n_sink, int n_recent, const void* q, const void* k,
+                             const void* v, const int32_t* seq_len, int batch, int h_q,
+                             int h_kv, int d, int l_cap, float sm_scale, float* scores,
+                             int32_t* idx, int32_t* count, float* nuc_mass, void* out,
+                             float* lse, void* ws, size_t ws_bytes, void* stream) {
+  return decode_step_impl(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max, k_min,
+                          n_sink, n_recent, q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale,
+                          scores, idx, count, nuc_mass, out, lse, ws, ws_bytes, false, stream);
+}
+
+spot_status spot_decode_step_static(const void* q_sel, const float* w, const void* k_sel,
+                                    const void* k_scale, int kfmt, int h_s, int d_s,
+                                    const int32_t* n_valid, float top_p, int k_max, int k_min,
+                                    int n_sink, int n_recent, const void* q, const void* k,
+                                    const void* v, const int32_t* seq_len, int batch, int h_q,
+                                    int h_kv, int d, int l_cap, float sm_scale, float* scores,
+                                    int32_t* idx, int32_t* count, float* nuc_mass, void* out,
+                                    float* lse, void* stream) {
+  return decode_step_impl(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max, k_min,
+                          n_sink, n_recent, q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale,
+                          scores, idx, count, nuc_mass, out, lse, nullptr, 0, true, stream);
+}
+
 spot_status spot_decode_step_status(void* ws, size_t ws_bytes, int batch, int h_q, int h_kv,
                                     int d, int k_max, void* stream) {
-  if (!ws) return SPOT_ERR_NULL;
   if (batch < 1 || h_q < 1 || h_kv < 1 || d < 1 || k_max < 1) return SPOT_ERR_SHAPE;
   const size_t need = step_workspace_bytes(batch, h_q, h_kv, d, k_max);
-  if (ws_bytes < need || misaligned(ws)) return SPOT_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!ws) {
+    // the static scratch of spot_decode_step_static on the current device
+    if (need > static_scratch_bytes()) return SPOT_ERR_WORKSPACE;
+    if (static_scratch(&ws, false, s) != hipSuccess) return SPOT_ERR_HIP;
+    if (!ws) return SPOT_OK;   // never used on this device
+    ws_bytes = need;
+  }
+  if (ws_bytes < need || misaligned(ws)) return SPOT_ERR_WORKSPACE;
   uint32_t word = 0;
   const char* w = static_cast<const char*>(ws) + step_sticky_offset(batch, h_q, h_kv, k_max);
   if (hipMemcpyAsync(&word, w, sizeof(word), hipMemcpyDeviceToHost, s) != hipSuccess ||

@@ -160,6 +160,11 @@ size_t decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_block
 size_t step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max);
 size_t step_sticky_offset(int batch, int h_q, int h_kv, int k_max);
 void step_force_expiry(int on);
+size_t static_scratch_bytes();
+// Device address of the current device's static scratch; with setup, looked
+// up and zero-filled on `s` by the first call on the device (else NULL until
+// then).
+hipError_t static_scratch(void** out, bool setup, hipStream_t s);
 bool step_fusable(int h_q, int h_kv, int nblk, int k_max);
 hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_sel,
                               const void* k_scale, int kfmt, int d_s, const int32_t* n_valid,

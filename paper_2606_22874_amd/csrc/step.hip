@@ -42,6 +42,7 @@
 // (count = -1 for every row, outputs zero) until spot_decode_step_status()
 // reports the expiry and zero-fills the workspace.
 #include <atomic>
+#include <mutex>
 
 #include "decode_core.h"
 #include "score_core.h"
@@ -491,7 +492,54 @@ StepLayout step_layout(int batch, int h_q, int h_kv, int k_max) {
 
 std::atomic<int> g_force_expire{0};
 
+__global__ __launch_bounds__(256) void zero_fill_kernel(uint4* __restrict__ p, size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16;
+       i += (size_t)gridDim.x * blockDim.x)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
 }  // namespace
+
+// Workspace of spot_decode_step_static: one array per device, kept until the
+// process ends.  Host code never passes `scratch` itself to a kernel (in host
+// code the name is only a stand-in); it uses the device address that
+// hipGetSymbolAddress returns for the current device.
+constexpr size_t kStaticScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+std::atomic<void*> g_scratch_ptr[64];
+}  // namespace
+
+size_t static_scratch_bytes() { return kStaticScratchBytes; }
+
+hipError_t static_scratch(void** out, bool setup, hipStream_t s) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p || !setup) {
+    *out = p;
+    return hipSuccess;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    // Zero-filled once (a fill kernel, also safe inside a captured graph);
+    // every call leaves the array zeroed again.
+    hipLaunchKernelGGL(zero_fill_kernel, dim3(1024), dim3(256), 0, s, static_cast<uint4*>(p),
+                       kStaticScratchBytes / 16);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return hipSuccess;
+}
 
 size_t step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max) {
   (void)d;

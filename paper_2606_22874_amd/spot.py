@@ -34,7 +34,7 @@ SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score",
            "spot_select_blocks",
            "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
            "spot_sparse_prefill", "spot_decode_step_workspace_bytes", "spot_decode_step",
-           "spot_decode_step_status", "spot_test_force_expiry",
+           "spot_decode_step_static", "spot_decode_step_status", "spot_test_force_expiry",
            "spot_probe_stream_read", "spot_probe_sink_words"]
 
 
@@ -80,6 +80,8 @@ def load(path: Optional[str] = None):
         L.spot_decode_step_workspace_bytes.restype = Z
         L.spot_decode_step.argtypes = [P, P, P, P, I, I, I, P, F, I, I, I, I, P, P, P, P, I, I,
                                        I, I, I, F, P, P, P, P, P, P, P, Z, P]
+        L.spot_decode_step_static.argtypes = [P, P, P, P, I, I, I, P, F, I, I, I, I, P, P, P, P,
+                                              I, I, I, I, I, F, P, P, P, P, P, P, P]
         L.spot_decode_step_status.argtypes = [P, Z, I, I, I, I, I, P]
         L.spot_test_force_expiry.argtypes = [I]
         L.spot_test_force_expiry.restype = None
@@ -90,7 +92,7 @@ def load(path: Optional[str] = None):
                      "spot_selector_project",
                      "spot_selector_pool", "spot_select_blocks", "spot_sparse_decode",
                      "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step",
-                     "spot_decode_step_status"):
+                     "spot_decode_step_static", "spot_decode_step_status"):
             getattr(L, name).restype = ctypes.c_int32
         if path is None:
             _lib = L
@@ -335,13 +337,45 @@ def spot_decode_step(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k
         _stream(stream)))
 
 
+def spot_decode_step_static(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max,
+                            k_min, n_sink, n_recent, q, k, v, seq_len, batch, h_q, h_kv, d, l_cap,
+                            sm_scale, scores, idx, count, nuc_mass, out, lse, stream=None):
+    """spot_decode_step on the device's static scratch (no workspace argument)."""
+    nblk = l_cap // BLK
+    f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
+    _dev(q_sel, "q_sel", BF16, batch * h_s * d_s)
+    _dev(w, "w", F32, batch * h_s)
+    _sel_cache(k_sel, k_scale, f, batch * nblk, h_s, d_s, "k_sel")
+    if n_valid is not None:
+        _dev(n_valid, "n_valid", I32, batch)
+    _dev(q, "q", BF16, batch * h_q * d)
+    _dev(k, "k", BF16, batch * h_kv * l_cap * d)
+    _dev(v, "v", BF16, batch * h_kv * l_cap * d)
+    _dev(seq_len, "seq_len", I32, batch)
+    _dev(scores, "scores", F32, batch * nblk)
+    _dev(idx, "idx", I32, batch * k_max)
+    _dev(count, "count", I32, batch)
+    if nuc_mass is not None:
+        _dev(nuc_mass, "nuc_mass", F32, batch)
+    _dev(out, "out", BF16, batch * h_q * d)
+    if lse is not None:
+        _dev(lse, "lse", F32, batch * h_q)
+    _check("spot_decode_step_static", load().spot_decode_step_static(
+        _ptr(q_sel), _ptr(w), _ptr(k_sel), _ptr(k_scale), f, h_s, d_s, _ptr(n_valid),
+        float(top_p), k_max, k_min, n_sink, n_recent, _ptr(q), _ptr(k), _ptr(v), _ptr(seq_len),
+        batch, h_q, h_kv, d, l_cap, float(sm_scale), _ptr(scores), _ptr(idx), _ptr(count),
+        _ptr(nuc_mass), _ptr(out), _ptr(lse), _stream(stream)))
+
+
 def spot_decode_step_status(ws, batch, h_q, h_kv, d, k_max, stream=None) -> int:
-    """Status of a fused-step workspace: SPOT_OK, or SPOT_ERR_EXPIRED after a
-    bounded wait expired (the workspace is then zero-filled again).  Any other
-    status raises."""
-    _dev(ws, "ws", None)
-    st = load().spot_decode_step_status(_ptr(ws), ws.numel() * ws.element_size(), batch, h_q,
-                                        h_kv, d, k_max, _stream(stream))
+    """Status of a fused-step workspace (ws None: the device's static scratch
+    of spot_decode_step_static): SPOT_OK, or SPOT_ERR_EXPIRED after a bounded
+    wait expired (the workspace is then zero-filled again).  Any other status
+    raises."""
+    if ws is not None:
+        _dev(ws, "ws", None)
+    st = load().spot_decode_step_status(_ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                                        batch, h_q, h_kv, d, k_max, _stream(stream))
     if st not in (SPOT_OK, SPOT_ERR_EXPIRED):
         raise SpotError("spot_decode_step_status", st)
     return int(st)

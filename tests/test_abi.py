@@ -38,6 +38,7 @@ def lib():
 UNCITED_HELPERS = ("spot_status_str", "spot_version", "spot_probe_stream_read",
                    "spot_probe_sink_words", "spot_decode_workspace_bytes",
                    "spot_decode_step_workspace_bytes", "spot_decode_step_status",
+                   "spot_decode_step_static",
                    "spot_test_force_expiry")
 CITATION = re.compile(r"\b(Section|Sections|Eqs?\.|Table|Appendix)\s+[A-Z0-9]")
 
@@ -212,10 +213,21 @@ def test_step_status_validation(lib):
     P = ctypes.c_void_p
     nz = P(16)   # never dereferenced: validation fails first
     st = lib.spot_decode_step_status
-    assert st(None, 1 << 20, 4, 32, 8, 128, 128, None) == 1
     assert st(nz, 1 << 20, 0, 32, 8, 128, 128, None) == 2
     assert st(nz, 16, 4, 32, 8, 128, 128, None) == 5
     assert st(P(24), 1 << 30, 4, 32, 8, 128, 128, None) == 5
+
+
+def test_static_step_size_limit(lib):
+    """spot_decode_step_static rejects a workspace beyond its 8 MiB scratch
+    before touching the GPU."""
+    P = ctypes.c_void_p
+    nz = P(16)
+    a = [nz, nz, nz, None, 0, 8, 64, None, 0.9, 128, 0, 1, 2, nz, nz, nz, nz]
+    big = a + [512, 32, 8, 128, 131072, 0.1, nz, nz, nz, None, nz, None, None]
+    assert lib.spot_decode_step_workspace_bytes(512, 32, 8, 128, 128) > 8 << 20
+    assert lib.spot_decode_step_static(*big) == 5
+    assert lib.spot_decode_step_static(*(a[:1] + [None] + a[2:] + big[17:])) == 1
 
 
 def test_workspace_size_query(lib):
