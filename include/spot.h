@@ -328,33 +328,36 @@ spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
  * the ones they would produce.
  *
  * When h_q == 4 * h_kv, nblk <= 4096 and min(k_max, nblk) <= 512, the three
- * stages run as one launch: every workgroup scores a chunk of its
- * sequence's blocks, then selects the sequence's blocks itself from the
- * scores of all chunks, then attends to its share of them, with no kernel
- * boundary in between (hand-offs through self-flagging record words in the
- * workspace, which each reader clears again).  Otherwise (or when no such
- * grid fits) the three stages are launched one after the other on `stream`.
- * Either way the results are deterministic; the fused path may split the
- * attention over fewer workgroups when fewer fit, which changes the FP32
- * summation order (not the block set).
+ * stages run as one launch with no kernel boundary in between: the first
+ * workgroups score chunks of their sequence's blocks, one workgroup per
+ * sequence selects its blocks from the scores of all chunks and publishes
+ * the set, and every workgroup attends to its share of the set of its
+ * (sequence, KV head) pair; the last workgroup of a pair to finish merges
+ * the pair's partials.  The hand-offs go through self-flagging record words
+ * in the workspace, which each reader clears again.  Otherwise (or when no
+ * such grid fits) the three stages are launched one after the other on
+ * `stream`.  Either way the results are deterministic; the fused path may
+ * split the attention over fewer workgroups when fewer fit, which changes
+ * the FP32 summation order (not the block set).
  *
  * Residency contract of the fused launch.  Its grid is sized to the number
  * of workgroups the device holds at once, and workgroups wait for records
- * written by others of the same launch: a sequence's workgroups wait for the
- * scores of all h_kv * n_slot scoring workgroups of that sequence, and the
- * last workgroup of each (sequence, KV head) pair waits for the attention
- * partials of the pair's other workgroups.  A kernel on another stream that
- * holds compute units (or a second fused step running concurrently) can keep
- * some of these workgroups from starting.  Every wait is bounded (0.2 s), so
- * the device never hangs.  When a wait expires, the waiting workgroup
- * computes nothing on unwritten records: it attends to no block, count[b]
- * of its sequence becomes -1, and a sticky expiry word in the workspace is
- * set.  While that word is set, every later call on the workspace gives
- * count = -1 for every sequence and zero outputs (idx and nuc_mass are left
- * as they were) without waiting, until spot_decode_step_status() reports the
- * expiry and zero-fills the workspace.  The word, not count, is
- * authoritative: a sequence whose own workgroups finished can still show its
- * real count in the call that expired.
+ * written by others of the same launch: a sequence's selecting workgroup
+ * waits for the scores of the sequence's scoring workgroups, and every
+ * workgroup waits for its sequence's selected set.  (The merge waits for
+ * nothing: the last finisher reads partials already written.)  A kernel on
+ * another stream that holds compute units (or a second fused step running
+ * concurrently) can keep some of these workgroups from starting.  Every wait
+ * is bounded (0.2 s), so the device never hangs.  When a wait expires, the
+ * waiting workgroup computes nothing on unwritten records: it attends to no
+ * block, count[b] of its sequence becomes -1, and a sticky expiry word in
+ * the workspace is set.  While that word is set, every later call on the
+ * workspace gives count = -1 for every sequence and zero outputs (idx and
+ * nuc_mass are left as they were) without waiting, until
+ * spot_decode_step_status() reports the expiry and zero-fills the
+ * workspace.  The word, not count, is authoritative: a sequence whose own
+ * workgroups finished can still show its real count in the call that
+ * expired.
  *
  *  scores   device float [batch, nblk]          (output)
  *  idx      device int32 [batch, k_max]         (output)
@@ -365,11 +368,12 @@ spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
  *           k_max) bytes, 16-byte aligned: the decode partials and counters
  *           laid out as for spot_sparse_decode (used when the stages run
  *           separately), then (from the next 16-byte boundary) the fused
- *           launch's partial records, election counters, expiry word and
- *           4096 score record words per (sequence, KV head) pair.  It must be
- *           zero-filled before its first use; every call leaves it ready for
- *           the next one (its counters and records return to zero).  Calls
- *           that share a workspace must not overlap in time.
+ *           launch's partials, completion counters, expiry word, 4096
+ *           score record words per sequence and a 256-word bitmap per
+ *           (sequence, KV head) pair.  It must be zero-filled before its
+ *           first use; every call leaves it ready for the next one (its
+ *           counters, records and bitmaps return to zero).  Calls that share
+ *           a workspace must not overlap in time.
  */
 size_t spot_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max);
 

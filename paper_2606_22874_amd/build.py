@@ -30,6 +30,10 @@ HIPCC_FLAGS = [
     "-Wall", "-Wno-unused-function",
     "-Wno-pass-failed",   # large bitonic sorts keep their outer loops (no scratch)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # A single-lane atomic whose result is used later must not be rewritten
+    # into a wave-wide one: that rewrite waits for the result (and every
+    # load in flight) right after the atomic.
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-I", INCLUDE, "-I", CSRC,
 ]
 

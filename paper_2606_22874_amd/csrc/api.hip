@@ -179,7 +179,8 @@ spot_status spot_sparse_decode(const void* q, const void* k, const void* v,
   if (!ws || ws_bytes < decode_workspace_bytes(batch, h_q, h_kv, d, k_max) || misaligned(ws))
     return SPOT_ERR_WORKSPACE;
   return from_hip(launch_decode(false, q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv,
-                                l_cap, sm_scale, out, lse, ws, static_cast<hipStream_t>(stream)));
+                                l_cap, sm_scale, out, lse, ws, nullptr,
+                                static_cast<hipStream_t>(stream)));
 }
 
 spot_status spot_dense_decode(const void* q, const void* k, const void* v,
@@ -194,7 +195,8 @@ spot_status spot_dense_decode(const void* q, const void* k, const void* v,
       misaligned(ws))
     return SPOT_ERR_WORKSPACE;
   return from_hip(launch_decode(true, q, k, v, seq_len, nullptr, nullptr, 0, batch, h_q, h_kv,
-                                l_cap, sm_scale, out, lse, ws, static_cast<hipStream_t>(stream)));
+                                l_cap, sm_scale, out, lse, ws, nullptr,
+                                static_cast<hipStream_t>(stream)));
 }
 
 size_t spot_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max) {
@@ -230,8 +232,7 @@ static spot_status decode_step_impl(const void* q_sel, const float* w, const voi
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (static_ws) {
     // the device's static scratch: no allocation, a size limit instead
-    if (step_workspace_bytes(batch, h_q, h_kv, d, k_max) > static_scratch_bytes())
-      return SPOT_ERR_WORKSPACE;
+    if (!step_static_fits(batch, h_q, h_kv, k_max)) return SPOT_ERR_WORKSPACE;
     if (static_scratch(&ws, true, s) != hipSuccess) return SPOT_ERR_HIP;
   } else if (!ws || ws_bytes < step_workspace_bytes(batch, h_q, h_kv, d, k_max) ||
              misaligned(ws)) {
@@ -241,7 +242,7 @@ static spot_status decode_step_impl(const void* q_sel, const float* w, const voi
     const hipError_t e = launch_decode_step(q_sel, w, k_sel, k_scale, kfmt, d_s, n_valid, top_p,
                                             k_max, k_min, n_sink, n_recent, q, k, v, seq_len,
                                             batch, h_q, h_kv, l_cap, sm_scale, scores, idx,
-                                            count, nuc_mass, out, lse, ws, s);
+                                            count, nuc_mass, out, lse, ws, static_ws, s);
     if (e == hipSuccess) return SPOT_OK;
     if (e != hipErrorCooperativeLaunchTooLarge) return SPOT_ERR_HIP;
     (void)hipGetLastError();  // clear the refused launch; run the stages separately
@@ -251,9 +252,15 @@ static spot_status decode_step_impl(const void* q_sel, const float* w, const voi
   if (e == hipSuccess)
     e = launch_select_blocks(scores, batch, nblk, n_valid, top_p, k_max, k_min, n_sink,
                              n_recent, idx, count, nuc_mass, s);
-  if (e == hipSuccess)
+  if (e == hipSuccess) {
+    // the partials after the control region, the counters inside it
+    const StepWs L = static_ws ? step_static_layout(batch, h_q, h_kv, k_max)
+                               : step_layout(batch, h_q, h_kv, k_max, 0);
+    char* base = static_cast<char*>(ws);
     e = launch_decode(false, q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, l_cap,
-                      sm_scale, out, lse, ws, s);
+                      sm_scale, out, lse, base + L.part, reinterpret_cast<unsigned*>(base + L.cnt),
+                      s);
+  }
   return from_hip(e);
 }
 
@@ -288,18 +295,20 @@ spot_status spot_decode_step_static(const void* q_sel, const float* w, const voi
 spot_status spot_decode_step_status(void* ws, size_t ws_bytes, int batch, int h_q, int h_kv,
                                     int d, int k_max, void* stream) {
   if (batch < 1 || h_q < 1 || h_kv < 1 || d < 1 || k_max < 1) return SPOT_ERR_SHAPE;
-  const size_t need = step_workspace_bytes(batch, h_q, h_kv, d, k_max);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  StepWs L = step_layout(batch, h_q, h_kv, k_max, 0);
   if (!ws) {
     // the static scratch of spot_decode_step_static on the current device
-    if (need > static_scratch_bytes()) return SPOT_ERR_WORKSPACE;
+    if (!step_static_fits(batch, h_q, h_kv, k_max)) return SPOT_ERR_WORKSPACE;
     if (static_scratch(&ws, false, s) != hipSuccess) return SPOT_ERR_HIP;
     if (!ws) return SPOT_OK;   // never used on this device
-    ws_bytes = need;
+    L = step_static_layout(batch, h_q, h_kv, k_max);
+    ws_bytes = L.total;
   }
+  const size_t need = L.total;
   if (ws_bytes < need || misaligned(ws)) return SPOT_ERR_WORKSPACE;
   uint32_t word = 0;
-  const char* w = static_cast<const char*>(ws) + step_sticky_offset(batch, h_q, h_kv, k_max);
+  const char* w = static_cast<const char*>(ws) + L.sticky;
   if (hipMemcpyAsync(&word, w, sizeof(word), hipMemcpyDeviceToHost, s) != hipSuccess ||
       hipStreamSynchronize(s) != hipSuccess)
     return SPOT_ERR_HIP;

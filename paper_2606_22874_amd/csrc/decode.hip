@@ -53,14 +53,14 @@ size_t decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_block
 hipError_t launch_decode(bool dense, const void* q, const void* k, const void* v,
                          const int32_t* seq_len, const int32_t* idx, const int32_t* count,
                          int k_max, int batch, int h_q, int h_kv, int l_cap, float sm_scale,
-                         void* out, float* lse, void* ws, hipStream_t s) {
+                         void* out, float* lse, void* ws, unsigned* counters, hipStream_t s) {
   const int G = h_q / h_kv;
   const int max_blocks = dense ? l_cap / kBlk : k_max;
   const int n_slot = decode_num_splits(batch, h_kv, max_blocks, G);
   const int n_pairs = batch * h_kv;
   float* ws_o = static_cast<float*>(ws);
   float* ws_ml = ws_o + (size_t)batch * h_q * n_slot * kD;
-  unsigned* counters = reinterpret_cast<unsigned*>(ws_ml + (size_t)batch * h_q * n_slot * 2);
+  if (!counters) counters = reinterpret_cast<unsigned*>(ws_ml + (size_t)batch * h_q * n_slot * 2);
   auto o16 = static_cast<uint16_t*>(out);
   const float scale_log2 = sm_scale * kLog2e;
   dim3 grid(n_pairs * n_slot);

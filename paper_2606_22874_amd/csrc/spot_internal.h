@@ -157,8 +157,17 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
 int decode_num_splits(int batch, int h_kv, int max_blocks, int group);
 size_t decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_blocks);
 
+// Byte offsets in a decode step's workspace: the control region [0, ctrl)
+// (completion counters, expiry word, score records, bitmaps; zero between
+// calls) and the partials from `part` to `total`.
+struct StepWs {
+  size_t cnt, sticky, srec, brec, ctrl, part, total;
+};
+StepWs step_layout(int batch, int h_q, int h_kv, int k_max, size_t ctrl_cap);
 size_t step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max);
-size_t step_sticky_offset(int batch, int h_q, int h_kv, int k_max);
+// The layout of the static scratch: its partials start at a fixed offset.
+StepWs step_static_layout(int batch, int h_q, int h_kv, int k_max);
+bool step_static_fits(int batch, int h_q, int h_kv, int k_max);
 void step_force_expiry(int on);
 size_t static_scratch_bytes();
 // Device address of the current device's static scratch; with setup, looked
@@ -172,11 +181,14 @@ hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_s
                               const void* q, const void* k, const void* v,
                               const int32_t* seq_len, int batch, int h_q, int h_kv, int l_cap,
                               float sm_scale, float* scores, int32_t* idx, int32_t* count,
-                              float* nuc_mass, void* out, float* lse, void* ws, hipStream_t s);
+                              float* nuc_mass, void* out, float* lse, void* ws, bool static_ws,
+                              hipStream_t s);
+// ws holds the partials, then (when counters is NULL) the completion
+// counters, as decode_workspace_bytes lays them out.
 hipError_t launch_decode(bool dense, const void* q, const void* k, const void* v,
                          const int32_t* seq_len, const int32_t* idx, const int32_t* count,
                          int k_max, int batch, int h_q, int h_kv, int l_cap, float sm_scale,
-                         void* out, float* lse, void* ws, hipStream_t s);
+                         void* out, float* lse, void* ws, unsigned* counters, hipStream_t s);
 
 hipError_t launch_sparse_prefill(const void* q, const void* k, const void* v, int L,
                                  const int32_t* idx, const int32_t* count, int k_max,

@@ -12,35 +12,36 @@
 //      serves row i % batch) score a contiguous run of its blocks; each
 //      score also goes out as a self-flagging record word;
 //   2. selection: workgroup r (a scorer of row r) polls the row's score
-//      records (each thread its own ids, as they land), clears them, selects
-//      the row (the workgroup core shared with the stand-alone kernel) and
-//      publishes the block list as record words, one copy per KV head;
-//   3. attention: every workgroup polls its share (entries s, s + n_slot,
-//      ...) of its pair's copy of the list, clears it and runs its part of
-//      the split-KV decode (shared core).  Right after it issued the loads of
-//      its last block, it bumps the pair's election counter: the workgroup
-//      that bumps it last merges the pair, so the election's round trip
-//      overlaps the last block.  Partials go out as self-flagging record
-//      words; the merger polls them, merges in slot order (deterministic)
-//      and clears them and the counter.
+//      records (each thread its own ids, as they land), selects the row (the
+//      workgroup core shared with the stand-alone kernel), publishes the
+//      selected set as a bitmap (16 block bits and a flag bit per word, one
+//      copy per KV head), then writes idx / count / nuc_mass and clears the
+//      score records;
+//   3. attention: every workgroup polls its pair's bitmap copy, takes its
+//      share of the set (entries s, s + n_slot, ... in ascending block id:
+//      the stand-alone decode's share of the same list) and runs its part of
+//      the split-KV decode (shared core).  The partials go to the workspace;
+//      the last workgroup of the pair to finish (device-scope counter)
+//      merges them in slot order (deterministic), resets the counter and
+//      clears the bitmap, which every workgroup of the pair has read by then.
 // A record word is nonzero once written and its reader sets it back to zero,
-// so a hand-off needs no flag or fence, only polling readers, and the
-// workspace is all zero again when a launch ends.
+// so a hand-off needs no flag or fence, only polling readers; the records,
+// bitmaps and counters are all zero again when a launch ends.
 //
-// Residency: every wait is for records written by other workgroups of the
-// same launch -- a row's selector waits for the row's scorers, every
-// workgroup for its row's selector, and a pair's merger for the pair's other
-// n_slot - 1 workgroups.  The launcher sizes the grid to the occupancy-derived
-// capacity of the device, so on an otherwise idle device all workgroups are
-// resident together; the scorers and selectors are the lowest workgroup ids
-// and start first.  A kernel holding compute units on another stream can
-// delay some of them; each wait is therefore bounded (wait_ticks of the
-// 100 MHz real-time counter).  An expired wait computes nothing on unwritten
-// records: that workgroup attends to no block (an expired selector publishes
-// an empty list), sets count[b] = -1 and a sticky error word in the
-// workspace.  A launch that finds the sticky word set does not wait at all
-// (count = -1 for every row, outputs zero) until spot_decode_step_status()
-// reports the expiry and zero-fills the workspace.
+// Residency: a row's selector waits for the row's scorers, and every
+// workgroup waits for its row's selector; the merge waits for nothing (the
+// last finisher reads partials that are already written).  The launcher
+// sizes the grid to the occupancy-derived capacity of the device, so on an
+// otherwise idle device all workgroups are resident together; the scorers
+// and selectors are the lowest workgroup ids and start first.  A kernel
+// holding compute units on another stream can delay some of them; each wait
+// is therefore bounded (wait_ticks of the 100 MHz real-time counter).  An
+// expired wait computes nothing on unwritten records: that workgroup attends
+// to no block (an expired selector publishes an empty set), sets
+// count[b] = -1 and a sticky error word in the workspace.  A launch that
+// finds the sticky word set does not wait at all (count = -1 for every row,
+// outputs zero) until spot_decode_step_status() reports the expiry and
+// zero-fills the workspace.
 #include <atomic>
 #include <mutex>
 
@@ -88,9 +89,9 @@ struct StepArgs {
   float* mass;
   uint16_t* out;
   float* lse;
-  uint32_t* part_o;    // [batch * h_q, n_slot, 128] partial o record words
-  uint32_t* part_ml;   // [batch * h_q, n_slot, 2] partial (m, l) record words
-  unsigned* elect;     // [batch * h_kv] merger election counters
+  float* part_o;       // [batch * h_q, n_slot, 128] partial o
+  float* part_ml;      // [batch * h_q, n_slot, 2] partial (m, l)
+  unsigned* pair_cnt;  // [batch * h_kv] split completion counters
   uint32_t* sticky;    // expiry word (one per workspace)
   uint32_t* srec;      // [batch, kRecRow] score records
   uint32_t* brec;      // [batch * h_kv, kBitWords] selected-set bitmap copies, one per pair
@@ -107,15 +108,6 @@ __device__ __forceinline__ W load_rec(const W* p) {
 template <typename W>
 __device__ __forceinline__ void store_rec(W* p, W v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t rec_pair(float a, float b) {
-  return (uint64_t)rec_word(a) | ((uint64_t)rec_word(b) << 32);
-}
-__device__ __forceinline__ float2 rec_pair_value(uint64_t x) {
-  return make_float2(rec_value((uint32_t)x), rec_value((uint32_t)(x >> 32)));
-}
-__device__ __forceinline__ bool rec_pair_full(uint64_t x) {
-  return (uint32_t)x != 0u && (uint32_t)(x >> 32) != 0u;
 }
 
 // Score source of the selection: thread t polls the records of its own ids
@@ -360,79 +352,30 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
   uint32_t qv[kD / 2];
   load_query_heads<kStepG>(qv, a.q, b, g, a.h_q);
   const size_t head_base = ((size_t)b * a.h_kv + g) * (size_t)a.l_cap * kD;
-  unsigned elect_prev = 0u;
-  auto elect = [&](int n) {
-    if (n == n_local - 1 && tid == 0)
-      elect_prev = __hip_atomic_fetch_add(&a.elect[pair], 1u, __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
-  };
-  if (n_local == 0) elect(-1);
   auto blk_of = [&](int n) { return sm.dec.ids[n]; };
   const HeadPartial hp = attend_blocks<kStepG>(sm.dec, qv, a.k + head_base, a.v + head_base, sl,
-                                               n_local, blk_of, a.scale_log2, elect);
+                                               n_local, blk_of, a.scale_log2, NoHook{});
   SPOT_STEP_TS(5);
-  if (tid == 0) sm.dec.last = elect_prev == (unsigned)(n_slot - 1);
-  __syncthreads();
   const size_t bh = (size_t)b * a.h_q + g * kStepG + wave;   // wave w: head w of the group
-  uint32_t* po = a.part_o + bh * n_slot * kD;
-  uint32_t* pml = a.part_ml + bh * n_slot * 2;
-  if (!sm.dec.last) {
-    store_rec(reinterpret_cast<uint64_t*>(po + (size_t)slot * kD + 2 * lane),
-              rec_pair(hp.o0, hp.o1));
-    if (lane == 0) store_rec(reinterpret_cast<uint64_t*>(pml + 2 * slot), rec_pair(hp.M, hp.L));
-    SPOT_STEP_TS(6);
-    return;
-  }
+  store_coherent(&a.part_o[(bh * n_slot + slot) * kD + 2 * lane], make_float2(hp.o0, hp.o1));
+  if (lane == 0) store_coherent(&a.part_ml[(bh * n_slot + slot) * 2], make_float2(hp.M, hp.L));
 
-  // ---- the merger: every workgroup of the pair has bumped the counter (so
-  // each has read the pair's bitmap): both are cleared; the other slots'
-  // partials are polled, merged in slot order and cleared.
-  if (tid == 0) store_rec(&a.elect[pair], 0u);
+  // ---- the last workgroup of the pair to finish merges all slots
+  wait_stores();
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned prev = __hip_atomic_fetch_add(&a.pair_cnt[pair], 1u, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+    sm.dec.last = prev == (unsigned)(n_slot - 1);
+  }
+  __syncthreads();
+  SPOT_STEP_TS(6);
+  if (!sm.dec.last) return;
+  if (tid == 0) store_rec(&a.pair_cnt[pair], 0u);
   for (int w = 2 * tid; w < (a.nblk + 15) / 16; w += 2 * kSelWG)
     store_rec(reinterpret_cast<uint64_t*>(bmap + w), (uint64_t)0);
-  uint64_t t_raw = lane < n_slot && lane != slot
-                       ? load_rec(reinterpret_cast<const uint64_t*>(pml + 2 * lane))
-                       : rec_pair(hp.M, hp.L);
-  uint64_t o_raw[kMaxSlots];
-#pragma unroll
-  for (int u = 0; u < kMaxSlots; ++u)
-    o_raw[u] = u < n_slot && u != slot
-                   ? load_rec(reinterpret_cast<const uint64_t*>(po + (size_t)u * kD + 2 * lane))
-                   : rec_pair(hp.o0, hp.o1);
-  bool done = false;
-  const uint64_t deadline = now() + a.wait_ticks;
-  for (;;) {
-    bool full = rec_pair_full(t_raw);
-#pragma unroll
-    for (int u = 0; u < kMaxSlots; ++u) full = full && rec_pair_full(o_raw[u]);
-    done = __ballot(!full) == 0ull;
-    if (done || now() > deadline) break;
-    __builtin_amdgcn_s_sleep(1);
-    if (!rec_pair_full(t_raw))
-      t_raw = load_rec(reinterpret_cast<const uint64_t*>(pml + 2 * lane));
-#pragma unroll
-    for (int u = 0; u < kMaxSlots; ++u)
-      if (!rec_pair_full(o_raw[u]))
-        o_raw[u] = load_rec(reinterpret_cast<const uint64_t*>(po + (size_t)u * kD + 2 * lane));
-  }
-  if (!done && lane == 0) {
-    store_rec(a.sticky, 1u);
-    store_rec(a.count + b, -1);
-  }
-  // A partial that never arrived counts as empty (l = 0).
-  float2 t = rec_pair_full(t_raw) ? rec_pair_value(t_raw) : make_float2(-INFINITY, 0.f);
-  if (lane >= n_slot) t = make_float2(-INFINITY, 0.f);
-  float2 o[kMaxSlots];
-#pragma unroll
-  for (int u = 0; u < kMaxSlots; ++u)
-    o[u] = rec_pair_full(o_raw[u]) ? rec_pair_value(o_raw[u]) : make_float2(0.f, 0.f);
-  merge_small(t, o, n_slot, bh, a.out, a.lse, lane);
+  merge_head(a.part_o, a.part_ml, n_slot, bh, a.out, a.lse, lane);
   SPOT_STEP_TS(7);
-  if (lane < n_slot && lane != slot) store_rec(reinterpret_cast<uint64_t*>(pml + 2 * lane), (uint64_t)0);
-#pragma unroll
-  for (int u = 0; u < kMaxSlots; ++u)
-    if (u < n_slot && u != slot)
-      store_rec(reinterpret_cast<uint64_t*>(po + (size_t)u * kD + 2 * lane), (uint64_t)0);
 }
 
 // Workgroups of one step kernel that can be resident at once (per CU times
@@ -466,30 +409,6 @@ hipError_t launch_step_t(StepArgs& a, int n_pairs, int n_slot_max, hipStream_t s
   return hipGetLastError();
 }
 
-// Workspace of the fused path, after the three-launch path's decode
-// workspace: partial o and (m, l) record words for up to kMaxSlots slots,
-// the election counters, the sticky word (16 bytes), the score records and
-// the selected-set bitmap copies.
-struct StepLayout {
-  size_t part_o, part_ml, elect, sticky, srec, brec, total;
-  int n_slot_max;
-};
-
-StepLayout step_layout(int batch, int h_q, int h_kv, int k_max) {
-  StepLayout L;
-  const int ns = decode_num_splits(batch, h_kv, k_max, kStepG);
-  L.n_slot_max = ns < kMaxSlots ? ns : kMaxSlots;
-  const size_t heads = (size_t)batch * h_q;
-  L.part_o = (decode_workspace_bytes(batch, h_q, h_kv, kD, k_max) + 15) & ~(size_t)15;
-  L.part_ml = L.part_o + heads * L.n_slot_max * kD * 4;
-  L.elect = L.part_ml + heads * L.n_slot_max * 2 * 4;
-  L.sticky = (L.elect + (size_t)batch * h_kv * 4 + 15) & ~(size_t)15;
-  L.srec = L.sticky + 16;
-  L.brec = L.srec + (size_t)batch * kRecRow * 4;
-  L.total = L.brec + (size_t)batch * h_kv * kBitWords * 4;
-  return L;
-}
-
 std::atomic<int> g_force_expire{0};
 
 __global__ __launch_bounds__(256) void zero_fill_kernel(uint4* __restrict__ p, size_t n16) {
@@ -505,12 +424,36 @@ __global__ __launch_bounds__(256) void zero_fill_kernel(uint4* __restrict__ p, s
 // code the name is only a stand-in); it uses the device address that
 // hipGetSymbolAddress returns for the current device.
 constexpr size_t kStaticScratchBytes = (size_t)8 << 20;
+constexpr size_t kStaticCtrlBytes = (size_t)1 << 20;   // control region of every shape
 static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 namespace {
 std::mutex g_scratch_mu;
 std::atomic<void*> g_scratch_ptr[64];
 }  // namespace
+
+// Workspace of a decode step (both paths).  The control region comes first:
+// the split completion counters (one per pair, used by the fused launch and
+// by the separate decode alike), the expiry word (16 bytes), the score
+// records [batch, kRecRow] and the bitmap copies [batch * h_kv, kBitWords];
+// every call leaves it all zero.  The partials follow at `part`: o
+// [batch * h_q, ns, 128] then (m, l) [batch * h_q, ns, 2], ns being the
+// separate decode's split count (the fused launch indexes them with its own
+// n_slot <= ns); they hold data between calls.  ctrl_cap > 0 fixes where the
+// partials start, so that calls of any shape find zeros in their control
+// words; 0 puts them right after the control words.
+StepWs step_layout(int batch, int h_q, int h_kv, int k_max, size_t ctrl_cap) {
+  StepWs L;
+  L.cnt = 0;
+  L.sticky = ((size_t)batch * h_kv * 4 + 15) & ~(size_t)15;
+  L.srec = L.sticky + 16;
+  L.brec = L.srec + (size_t)batch * kRecRow * 4;
+  L.ctrl = (L.brec + (size_t)batch * h_kv * kBitWords * 4 + 255) & ~(size_t)255;
+  L.part = ctrl_cap > 0 ? ctrl_cap : L.ctrl;
+  const size_t ns = (size_t)decode_num_splits(batch, h_kv, k_max, h_q / h_kv);
+  L.total = L.part + (size_t)batch * h_q * ns * (kD + 2) * 4;
+  return L;
+}
 
 size_t static_scratch_bytes() { return kStaticScratchBytes; }
 
@@ -543,11 +486,16 @@ hipError_t static_scratch(void** out, bool setup, hipStream_t s) {
 
 size_t step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max) {
   (void)d;
-  return step_layout(batch, h_q, h_kv, k_max).total;
+  return step_layout(batch, h_q, h_kv, k_max, 0).total;
 }
 
-size_t step_sticky_offset(int batch, int h_q, int h_kv, int k_max) {
-  return step_layout(batch, h_q, h_kv, k_max).sticky;
+StepWs step_static_layout(int batch, int h_q, int h_kv, int k_max) {
+  return step_layout(batch, h_q, h_kv, k_max, kStaticCtrlBytes);
+}
+
+bool step_static_fits(int batch, int h_q, int h_kv, int k_max) {
+  const StepWs L = step_static_layout(batch, h_q, h_kv, k_max);
+  return L.ctrl <= kStaticCtrlBytes && L.total <= kStaticScratchBytes;
 }
 
 void step_force_expiry(int on) { g_force_expire.store(on ? 1 : 0, std::memory_order_relaxed); }
@@ -566,7 +514,8 @@ hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_s
                               const void* q, const void* k, const void* v,
                               const int32_t* seq_len, int batch, int h_q, int h_kv, int l_cap,
                               float sm_scale, float* scores, int32_t* idx, int32_t* count,
-                              float* nuc_mass, void* out, float* lse, void* ws, hipStream_t s) {
+                              float* nuc_mass, void* out, float* lse, void* ws, bool static_ws,
+                              hipStream_t s) {
   StepArgs a;
   a.q_sel = static_cast<const uint16_t*>(q_sel);
   a.w = w;
@@ -596,20 +545,23 @@ hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_s
   a.mass = nuc_mass;
   a.out = static_cast<uint16_t*>(out);
   a.lse = lse;
-  const StepLayout L = step_layout(batch, h_q, h_kv, k_max);
+  const StepWs L = static_ws ? step_static_layout(batch, h_q, h_kv, k_max)
+                            : step_layout(batch, h_q, h_kv, k_max, 0);
+  const int ns = decode_num_splits(batch, h_kv, k_max, kStepG);
+  const int n_slot_max = ns < kMaxSlots ? ns : kMaxSlots;
   char* base = static_cast<char*>(ws);
-  a.part_o = reinterpret_cast<uint32_t*>(base + L.part_o);
-  a.part_ml = reinterpret_cast<uint32_t*>(base + L.part_ml);
-  a.elect = reinterpret_cast<unsigned*>(base + L.elect);
+  a.part_o = reinterpret_cast<float*>(base + L.part);
+  a.part_ml = a.part_o + (size_t)batch * h_q * ns * kD;
+  a.pair_cnt = reinterpret_cast<unsigned*>(base + L.cnt);
   a.sticky = reinterpret_cast<uint32_t*>(base + L.sticky);
   a.srec = reinterpret_cast<uint32_t*>(base + L.srec);
   a.brec = reinterpret_cast<uint32_t*>(base + L.brec);
   a.wait_ticks = kWaitTicks;
   a.force_expire = g_force_expire.load(std::memory_order_relaxed);
   const int n_pairs = batch * h_kv;
-  // The partial records are laid out for n_slot_max; a smaller n_slot (when
-  // fewer workgroups fit) uses a prefix of each head's run, indexed with the
-  // actual n_slot -- the layout is [B, h_q, n_slot] either way.
+  // The partials are laid out for ns splits; the launch's n_slot (at most
+  // n_slot_max, fewer when fewer workgroups fit) uses a prefix of each
+  // head's run, indexed with the actual n_slot -- [B, h_q, n_slot] either way.
   int P = 1;
   const int cap = k_max < a.nblk ? k_max : a.nblk;
   while (P < cap) P <<= 1;
@@ -617,7 +569,7 @@ hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_s
   const int ept = a.nblk <= 256 ? 1 : a.nblk <= 512 ? 2 : a.nblk <= 1024 ? 4
                 : a.nblk <= 2048 ? 8 : 16;
 #define SPOT_STEP_CASE(E, S) \
-  if (ept == E && spl == S) return launch_step_t<E, S>(a, n_pairs, L.n_slot_max, s);
+  if (ept == E && spl == S) return launch_step_t<E, S>(a, n_pairs, n_slot_max, s);
 #define SPOT_STEP_E(E) SPOT_STEP_CASE(E, 1) SPOT_STEP_CASE(E, 2) SPOT_STEP_CASE(E, 4) \
   SPOT_STEP_CASE(E, 8)
   SPOT_STEP_E(1)

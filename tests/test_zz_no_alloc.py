@@ -4,7 +4,12 @@ caller workspace, through the C ABI (needs an MI355X).
 
 Both calls run the same kernels with the same work split, so every output
 must match bit for bit; this is checked on two calls in a row, the second with
-a smaller input, and the scratch must be left clean (status query)."""
+a smaller input, and the scratch must be left clean (status query).  A shape
+that runs the three stages as separate launches (k_max above the fused
+limit) leaves its partials in the scratch; a fused call after it must not be
+disturbed by them."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -52,4 +57,13 @@ def test_static_scratch_matches_workspace_twice():
     print("[no-alloc] 128K-token workload, batch 4", flush=True)
     both(synth.decode_config(3))
     print("[no-alloc] 8K-token workload, batch 2 (smaller)", flush=True)
+    both(synth.decode_config(2, B=2, L=8192))
+
+
+def test_static_scratch_after_separate_launches():
+    wl = synth.decode_config(2, B=1, L=65536)
+    wl = dataclasses.replace(wl, rule=dataclasses.replace(wl.rule, k_max=600))
+    print("[no-alloc] 64K-token workload, k_max 600 (separate launches)", flush=True)
+    both(wl)
+    print("[no-alloc] 8K-token workload, batch 2 (fused) after it", flush=True)
     both(synth.decode_config(2, B=2, L=8192))
