@@ -164,6 +164,28 @@ struct PolledScores {
 constexpr uint32_t kBitFlag = 0x10000u;
 constexpr int kBitWords = kRecRow / 16;   // bitmap words per copy
 
+// Position of the r-th (from 0) set bit of x; r < popcount(x).
+__device__ __forceinline__ int nth_set_bit(uint64_t x, int r) {
+  int base = 0;
+  uint32_t w = (uint32_t)x;
+  int c = __popc(w);
+  if (r >= c) {
+    r -= c;
+    w = (uint32_t)(x >> 32);
+    base = 32;
+  }
+#pragma unroll
+  for (int half = 16; half >= 1; half >>= 1) {
+    c = __popc(w & ((1u << half) - 1u));
+    if (r >= c) {
+      r -= c;
+      w >>= half;
+      base += half;
+    }
+  }
+  return base;
+}
+
 __device__ __forceinline__ int poll_bitmap(int* ids, const uint32_t* rec, int nwords, int k_max,
                                            int slot, int n_slot, int nb_valid, uint64_t ticks,
                                            bool give_up) {
@@ -204,17 +226,16 @@ __device__ __forceinline__ int poll_bitmap(int* ids, const uint32_t* rec, int nw
                                                     : (1ull << (nb_valid - base_id)) - 1ull;
   const int cnt = __popcll(bits);
   const int incl = wave_incl_scan_i(cnt);
-  int pos = incl - cnt;
+  const int pos = incl - cnt;             // list position of this lane's first id
   const int total = min(__builtin_amdgcn_readlane(incl, 63), k_max);
   const int n_ok = min(wave_sum_i(__popcll(bits & valid)), total);
-  while (bits) {
-    const int bit = __builtin_ctzll(bits);
-    bits &= bits - 1ull;
-    if (pos < n_ok && pos >= slot && (pos - slot) % n_slot == 0) {
-      const int kk = (pos - slot) / n_slot;
-      if (kk < kMaxIds) ids[kk] = base_id + bit;
-    }
-    ++pos;
+  // This lane's entries of the share: positions slot + kk * n_slot in
+  // [pos, min(pos + cnt, n_ok)), each the (position - pos)-th set bit.
+  const int end = min(pos + cnt, n_ok);
+  for (int kk = pos > slot ? (pos - slot + n_slot - 1) / n_slot : 0;; ++kk) {
+    const int p = slot + kk * n_slot;
+    if (p >= end || kk >= kMaxIds) break;
+    ids[kk] = base_id + nth_set_bit(bits, p - pos);
   }
   return n_ok > slot ? min((n_ok - slot + n_slot - 1) / n_slot, kMaxIds) : 0;
 }
