@@ -14,6 +14,16 @@ equals the oracle's, or when every difference is explained by one of:
 
 Whatever the exemption, the set must still contain every reserved block,
 respect k_max, and be a top-n set of the residual scores up to ``rel_tie``.
+Exempted rows must stay rare: check_all allows at most max(1, rows // 50)
+of them per call (2 %), so a systematic difference cannot hide behind the
+exemptions.
+
+Why these tolerances: the HIP path sums the exponentials in FP32 along a
+reduction tree of depth about 11 (8 per thread, 64 per wave, 4 waves), so
+the nucleus mass it compares with p carries a relative error of at most
+about 2 * 11 * 2^-24 = 1.3e-6 of Z (plus one ulp per v_exp_f32 term);
+mass_tol = 1e-5 leaves a factor of about 8 over that.  Scores are compared
+at 1e-4 relative, so two blocks closer than that may rank either way.
 """
 from __future__ import annotations
 
@@ -80,7 +90,7 @@ def check_row(scores, nv, rule, S_oracle, S_gpu, rel_tie=1e-4, mass_tol=1e-5):
     return "tie" if n_g == n_o else "mass"
 
 
-def check_all(scores, n_valid, rule, idx_o, cnt_o, idx_g, cnt_g, **kw):
+def check_all(scores, n_valid, rule, idx_o, cnt_o, idx_g, cnt_g, max_exempt=None, **kw):
     stats = {"exact": 0, "tie": 0, "mass": 0}
     for r in range(len(cnt_o)):
         g = idx_g[r, :cnt_g[r]]
@@ -91,4 +101,7 @@ def check_all(scores, n_valid, rule, idx_o, cnt_o, idx_g, cnt_g, **kw):
         except AssertionError as e:
             raise AssertionError(f"row {r}: {e}") from None
         stats[kind] += 1
+    if max_exempt is None:
+        max_exempt = max(1, len(cnt_o) // 50)
+    assert stats["tie"] + stats["mass"] <= max_exempt, f"too many exempted rows: {stats}"
     return stats

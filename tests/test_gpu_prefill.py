@@ -129,17 +129,26 @@ def c5():
 
 
 def test_prefill_full_size_selection_all_rows():
-    """Selector scores and the dual top-p / top-K selection of every one of
-    the 512 query blocks of the 32K-token layer, on the GPU, against the
-    oracle's scores and selection."""
+    """Selector scores (the query-block x key-block matrix-core kernel) and
+    the dual top-p / top-K selection of every one of the 512 query blocks of
+    the 32K-token layer, on the GPU, against the oracle: all 512 x 512
+    scores element by element (1e-4 relative), then the selection."""
     wl, idx_o, cnt_o = c5()
     nqb, rule = wl.nblk, wl.rule
-    s_o = oracle.selector_score(wl.q_sel, wl.w, wl.k_sel, rows_per_seq=nqb,
-                                n_valid=wl.n_valid).astype(np.float32)
+    s64 = oracle.selector_score(wl.q_sel, wl.w, wl.k_sel, rows_per_seq=nqb, n_valid=wl.n_valid)
+    s_o = s64.astype(np.float32)
     s_g = spot.selector_score(bf(wl.q_sel), torch.from_numpy(wl.w).to(DEV), bf(wl.k_sel),
                               rows_per_seq=nqb, n_valid=i32(wl.n_valid), nblk=nqb)
     idx_g, cnt_g, _ = spot.select_blocks(s_g, rule, i32(wl.n_valid))
     torch.cuda.synchronize()
+    g = s_g.cpu().numpy().astype(np.float64)
+    assert g.shape == (nqb, nqb)
+    fin = np.isfinite(s64)
+    assert np.array_equal(np.isfinite(g), fin) and np.all(g[~fin] == -np.inf)
+    assert fin.sum() == nqb * (nqb + 1) // 2          # causal: row qb has qb + 1 blocks
+    err = np.abs(g[fin] - s64[fin])
+    bound = 1e-4 * np.abs(s64[fin]) + 1e-6
+    assert np.all(err <= bound), f"max excess {np.max(err - bound)}"
     print("[prefill] selection of all rows", check_all(
         s_o, wl.n_valid, rule, idx_o, cnt_o, idx_g.cpu().numpy(), cnt_g.cpu().numpy()),
         flush=True)
