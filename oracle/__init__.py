@@ -6,7 +6,8 @@ and the HIP library never touches it.
 
 ``build()`` compiles the C file with gcc (OpenMP) into ``liboracle.so`` next
 to it; ``lib()`` builds on first use when the library is missing or older
-than its source.
+than its source.  ``SPOT_ORACLE_SO`` names another build of the same source
+to load instead (the sanitizer test uses it).
 """
 from __future__ import annotations
 
@@ -48,9 +49,12 @@ def lib():
     global _lib
     with _lock:
         if _lib is None:
-            if _stale():
-                build()
-            L = ctypes.CDLL(SO)
+            path = os.environ.get("SPOT_ORACLE_SO")
+            if not path:
+                path = SO
+                if _stale():
+                    build()
+            L = ctypes.CDLL(path)
             P, I, D = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
             L.oracle_set_threads.argtypes = [I]
             L.oracle_get_threads.restype = I
