@@ -183,23 +183,32 @@ spot_status spot_selector_score(const void *q_sel, const float *w, const void *k
  * spot_selector_score_q -- block scores with quantized selector queries.
  *
  * Section 5.3 and Appendix G quantize the selector's queries as well as its
- * key cache.  The score is that of spot_selector_score, with q_sel given as
- * MX codes: qfmt SPOT_KFMT_MXFP4_G32 (E2M1 codes, two per byte, element 2i
- * in the low nibble: uint8 [rows, h_s, d_s/2]) or SPOT_KFMT_MXFP8_G32 (E4M3
- * codes, uint8 [rows, h_s, d_s]), with q_scale uint8 E8M0 [rows, h_s, d_s/32];
- * qfmt SPOT_KFMT_BF16 is spot_selector_score itself (q_scale ignored).  Keys
- * in any format.
+ * key cache (INT8, INT4, FP8 and FP4).  The score is that of
+ * spot_selector_score, with q_sel given as codes in the layouts of the key
+ * cache formats (32-element groups along each row of h_s * d_s = 512):
+ *   qfmt SPOT_KFMT_INT4_G32  : uint8 [rows, h_s, d_s/2] two's-complement
+ *                              nibbles (element 2i low), q_scale FP16 bits
+ *                              uint16 [rows, h_s, d_s/32];
+ *   qfmt SPOT_KFMT_INT8_G32  : int8 [rows, h_s, d_s], q_scale as for INT4;
+ *   qfmt SPOT_KFMT_MXFP4_G32 : E2M1 codes, uint8 [rows, h_s, d_s/2] (element
+ *                              2i low), q_scale uint8 E8M0 [rows, h_s, d_s/32];
+ *   qfmt SPOT_KFMT_MXFP8_G32 : E4M3 codes, uint8 [rows, h_s, d_s], q_scale as
+ *                              for MXFP4;
+ * an element's value is code * scale of its group.  qfmt SPOT_KFMT_BF16 is
+ * spot_selector_score itself (q_scale ignored).  Keys in any format.
  *
  * When queries and keys share one MX format, d_s == 128 and rows_per_seq is
  * a multiple of 16 (prefill's query blocks), each head's tile product runs on
  * the matrix cores' block-scaled instruction (v_mfma_scale_f32_16x16x128_f8f6f4:
  * E2M1 or E4M3 operands, the E8M0 scales applied per 32-element group in
- * hardware); otherwise the queries are decoded exactly in registers.  Both
- * paths accumulate in FP32.
+ * hardware).  Otherwise MX queries are decoded exactly in registers, and
+ * integer queries enter the dot product as their integer codes, each lane's
+ * partial sum (8 elements of one group) then multiplied by the group's
+ * scale.  All paths accumulate in FP32.
  *
  * Errors: SPOT_ERR_NULL (a pointer, q_scale, or k_scale for quantized keys),
- * SPOT_ERR_SHAPE, SPOT_ERR_UNSUPPORTED (qfmt other than BF16/MXFP4/MXFP8, key
- * format, head shape).
+ * SPOT_ERR_SHAPE, SPOT_ERR_UNSUPPORTED (unknown query or key format, head
+ * shape).
  */
 spot_status spot_selector_score_q(const void *q_sel, const void *q_scale, int qfmt,
                                   const float *w, const void *k_sel, const void *k_scale,
@@ -385,6 +394,27 @@ spot_status spot_decode_step(const void *q_sel, const float *w, const void *k_se
                              int h_kv, int d, int l_cap, float sm_scale, float *scores,
                              int32_t *idx, int32_t *count, float *nuc_mass, void *out,
                              float *lse, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * spot_decode_step_q -- spot_decode_step with quantized selector queries
+ * (Section 5.3, Appendix G: the selector's queries are quantized to the
+ * precision of its key cache).  Arguments as spot_decode_step, plus q_scale
+ * and qfmt: qfmt SPOT_KFMT_BF16 is spot_decode_step itself (q_scale
+ * ignored); otherwise qfmt must equal kfmt and q_sel / q_scale hold the codes
+ * and scales in the layout spot_selector_score_q documents (rows = batch).
+ * The scores are those of spot_selector_score_q; selection and attention as
+ * in spot_decode_step, fused under the same conditions.
+ * Errors: those of spot_decode_step; SPOT_ERR_UNSUPPORTED when qfmt is
+ * neither BF16 nor kfmt, SPOT_ERR_NULL when q_scale is NULL for codes.
+ */
+spot_status spot_decode_step_q(const void *q_sel, const void *q_scale, int qfmt, const float *w,
+                               const void *k_sel, const void *k_scale, int kfmt, int h_s,
+                               int d_s, const int32_t *n_valid, float top_p, int k_max,
+                               int k_min, int n_sink, int n_recent, const void *q, const void *k,
+                               const void *v, const int32_t *seq_len, int batch, int h_q,
+                               int h_kv, int d, int l_cap, float sm_scale, float *scores,
+                               int32_t *idx, int32_t *count, float *nuc_mass, void *out,
+                               float *lse, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * spot_decode_step_static -- spot_decode_step for callers that cannot

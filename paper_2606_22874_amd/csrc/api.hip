@@ -103,8 +103,7 @@ spot_status spot_selector_score_q(const void* q_sel, const void* q_scale, int qf
                                d_s, n_valid, scores, stream);
   if (!q_sel || !w || !k_sel || !scores) return SPOT_ERR_NULL;
   if (n_seq < 0 || rows_per_seq < 1 || nblk < 0 || h_s < 1 || d_s < 1) return SPOT_ERR_SHAPE;
-  if (qfmt != SPOT_KFMT_MXFP4_G32 && qfmt != SPOT_KFMT_MXFP8_G32) return SPOT_ERR_UNSUPPORTED;
-  if (!valid_kfmt(kfmt)) return SPOT_ERR_UNSUPPORTED;
+  if (!valid_kfmt(qfmt) || !valid_kfmt(kfmt)) return SPOT_ERR_UNSUPPORTED;
   if (!q_scale || (kfmt != SPOT_KFMT_BF16 && !k_scale)) return SPOT_ERR_NULL;
   if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
   if ((long long)n_seq * rows_per_seq > 0x7fffffffLL) return SPOT_ERR_SHAPE;
@@ -206,7 +205,8 @@ size_t spot_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d, int
 
 }  // extern "C"
 
-static spot_status decode_step_impl(const void* q_sel, const float* w, const void* k_sel,
+static spot_status decode_step_impl(const void* q_sel, const void* q_scale, int qfmt,
+                             const float* w, const void* k_sel,
                              const void* k_scale, int kfmt, int h_s, int d_s,
                              const int32_t* n_valid, float top_p, int k_max, int k_min,
                              int n_sink, int n_recent, const void* q, const void* k,
@@ -219,7 +219,9 @@ static spot_status decode_step_impl(const void* q_sel, const float* w, const voi
   if (st != SPOT_OK) return st;
   if (!q_sel || !w || !k_sel || !scores || !idx || !count) return SPOT_ERR_NULL;
   if (!valid_kfmt(kfmt)) return SPOT_ERR_UNSUPPORTED;
+  if (qfmt != SPOT_KFMT_BF16 && qfmt != kfmt) return SPOT_ERR_UNSUPPORTED;
   if (kfmt != SPOT_KFMT_BF16 && !k_scale) return SPOT_ERR_NULL;
+  if (qfmt != SPOT_KFMT_BF16 && !q_scale) return SPOT_ERR_NULL;
   if (h_s < 1 || d_s < 1) return SPOT_ERR_SHAPE;
   if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
   if (l_cap == 0) return SPOT_ERR_SHAPE;
@@ -239,7 +241,8 @@ static spot_status decode_step_impl(const void* q_sel, const float* w, const voi
     return SPOT_ERR_WORKSPACE;
   }
   if (step_fusable(h_q, h_kv, nblk, k_max)) {
-    const hipError_t e = launch_decode_step(q_sel, w, k_sel, k_scale, kfmt, d_s, n_valid, top_p,
+    const hipError_t e = launch_decode_step(q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt, d_s,
+                                            n_valid, top_p,
                                             k_max, k_min, n_sink, n_recent, q, k, v, seq_len,
                                             batch, h_q, h_kv, l_cap, sm_scale, scores, idx,
                                             count, nuc_mass, out, lse, ws, static_ws, s);
@@ -247,8 +250,11 @@ static spot_status decode_step_impl(const void* q_sel, const float* w, const voi
     if (e != hipErrorCooperativeLaunchTooLarge) return SPOT_ERR_HIP;
     (void)hipGetLastError();  // clear the refused launch; run the stages separately
   }
-  hipError_t e = launch_selector_score(q_sel, w, k_sel, k_scale, kfmt, batch, 1, nblk, h_s, d_s,
-                                       n_valid, scores, s);
+  hipError_t e = qfmt == SPOT_KFMT_BF16
+                     ? launch_selector_score(q_sel, w, k_sel, k_scale, kfmt, batch, 1, nblk, h_s,
+                                             d_s, n_valid, scores, s)
+                     : launch_selector_score_q(q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt,
+                                               batch, 1, nblk, d_s, n_valid, scores, s);
   if (e == hipSuccess)
     e = launch_select_blocks(scores, batch, nblk, n_valid, top_p, k_max, k_min, n_sink,
                              n_recent, idx, count, nuc_mass, s);
@@ -274,9 +280,24 @@ spot_status spot_decode_step(const void* q_sel, const float* w, const void* k_se
                              int h_kv, int d, int l_cap, float sm_scale, float* scores,
                              int32_t* idx, int32_t* count, float* nuc_mass, void* out,
                              float* lse, void* ws, size_t ws_bytes, void* stream) {
-  return decode_step_impl(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max, k_min,
-                          n_sink, n_recent, q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale,
-                          scores, idx, count, nuc_mass, out, lse, ws, ws_bytes, false, stream);
+  return decode_step_impl(q_sel, nullptr, SPOT_KFMT_BF16, w, k_sel, k_scale, kfmt, h_s, d_s,
+                          n_valid, top_p, k_max, k_min, n_sink, n_recent, q, k, v, seq_len, batch,
+                          h_q, h_kv, d, l_cap, sm_scale, scores, idx, count, nuc_mass, out, lse,
+                          ws, ws_bytes, false, stream);
+}
+
+spot_status spot_decode_step_q(const void* q_sel, const void* q_scale, int qfmt, const float* w,
+                               const void* k_sel, const void* k_scale, int kfmt, int h_s,
+                               int d_s, const int32_t* n_valid, float top_p, int k_max,
+                               int k_min, int n_sink, int n_recent, const void* q, const void* k,
+                               const void* v, const int32_t* seq_len, int batch, int h_q,
+                               int h_kv, int d, int l_cap, float sm_scale, float* scores,
+                               int32_t* idx, int32_t* count, float* nuc_mass, void* out,
+                               float* lse, void* ws, size_t ws_bytes, void* stream) {
+  return decode_step_impl(q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid,
+                          top_p, k_max, k_min, n_sink, n_recent, q, k, v, seq_len, batch, h_q,
+                          h_kv, d, l_cap, sm_scale, scores, idx, count, nuc_mass, out, lse, ws,
+                          ws_bytes, false, stream);
 }
 
 spot_status spot_decode_step_static(const void* q_sel, const float* w, const void* k_sel,
@@ -287,9 +308,10 @@ spot_status spot_decode_step_static(const void* q_sel, const float* w, const voi
                                     int h_kv, int d, int l_cap, float sm_scale, float* scores,
                                     int32_t* idx, int32_t* count, float* nuc_mass, void* out,
                                     float* lse, void* stream) {
-  return decode_step_impl(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max, k_min,
-                          n_sink, n_recent, q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale,
-                          scores, idx, count, nuc_mass, out, lse, nullptr, 0, true, stream);
+  return decode_step_impl(q_sel, nullptr, SPOT_KFMT_BF16, w, k_sel, k_scale, kfmt, h_s, d_s,
+                          n_valid, top_p, k_max, k_min, n_sink, n_recent, q, k, v, seq_len, batch,
+                          h_q, h_kv, d, l_cap, sm_scale, scores, idx, count, nuc_mass, out, lse,
+                          nullptr, 0, true, stream);
 }
 
 spot_status spot_decode_step_status(void* ws, size_t ws_bytes, int batch, int h_q, int h_kv,

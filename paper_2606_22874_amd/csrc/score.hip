@@ -308,11 +308,20 @@ hipError_t launch_selector_score_q(const void* q_sel, const void* q_scale, int q
   }
   const dim3 grid(rows, (nblk + kBlocksPerWG - 1) / kBlocksPerWG);
   const int lph = d_s / 8;
-  if (qfmt == SPOT_KFMT_MXFP4_G32)
-    return launch_row_q<SPOT_KFMT_MXFP4_G32>(kfmt, lph, grid, s, q, qs, w, k, ks, rows_per_seq,
-                                             nblk, n_valid, scores);
-  return launch_row_q<SPOT_KFMT_MXFP8_G32>(kfmt, lph, grid, s, q, qs, w, k, ks, rows_per_seq,
-                                           nblk, n_valid, scores);
+  switch (qfmt) {
+    case SPOT_KFMT_MXFP4_G32:
+      return launch_row_q<SPOT_KFMT_MXFP4_G32>(kfmt, lph, grid, s, q, qs, w, k, ks, rows_per_seq,
+                                               nblk, n_valid, scores);
+    case SPOT_KFMT_MXFP8_G32:
+      return launch_row_q<SPOT_KFMT_MXFP8_G32>(kfmt, lph, grid, s, q, qs, w, k, ks, rows_per_seq,
+                                               nblk, n_valid, scores);
+    case SPOT_KFMT_INT4_G32:
+      return launch_row_q<SPOT_KFMT_INT4_G32>(kfmt, lph, grid, s, q, qs, w, k, ks, rows_per_seq,
+                                              nblk, n_valid, scores);
+    default:
+      return launch_row_q<SPOT_KFMT_INT8_G32>(kfmt, lph, grid, s, q, qs, w, k, ks, rows_per_seq,
+                                              nblk, n_valid, scores);
+  }
 }
 
 }  // namespace spot

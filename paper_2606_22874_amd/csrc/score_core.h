@@ -72,6 +72,17 @@ struct KeyLoad<SPOT_KFMT_BF16> {
     a = dot2_bf16(qraw.z, raw.z, a);
     return dot2_bf16(qraw.w, raw.w, a);
   }
+  // FP32 queries (integer query codes, which BF16 cannot hold exactly).
+  __device__ __forceinline__ float dot_f(const float* qf) const {
+    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+    float a = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      a = fmaf(qf[2 * i], bf16_lo(w[i]), a);
+      a = fmaf(qf[2 * i + 1], bf16_hi(w[i]), a);
+    }
+    return a;
+  }
 };
 
 // INT4: 4 bytes of codes (element 2i in the low nibble) and one FP16 scale.
@@ -92,6 +103,7 @@ struct KeyLoad<SPOT_KFMT_INT4_G32> {
     for (int i = 0; i < 8; ++i) a = fmaf(qf[i], v[i], a);
     return a * 16.f * f16_to_f32(scale);
   }
+  __device__ __forceinline__ float dot_f(const float* qf) const { return dot(uint4{}, qf); }
 };
 
 // MXFP4: 4 bytes of E2M1 codes and one E8M0 scale.
@@ -122,6 +134,7 @@ struct KeyLoad<SPOT_KFMT_MXFP4_G32> {
     a = fmaf(qf[7], v3[1], a);
     return a * e8m0_to_f32(scale);
   }
+  __device__ __forceinline__ float dot_f(const float* qf) const { return dot(uint4{}, qf); }
 };
 
 // INT8: 8 bytes of two's-complement codes and one FP16 scale.
@@ -143,6 +156,7 @@ struct KeyLoad<SPOT_KFMT_INT8_G32> {
     }
     return a * f16_to_f32(scale);
   }
+  __device__ __forceinline__ float dot_f(const float* qf) const { return dot(uint4{}, qf); }
 };
 
 // MXFP8: 8 bytes of OCP E4M3 codes and one E8M0 scale.
@@ -172,6 +186,7 @@ struct KeyLoad<SPOT_KFMT_MXFP8_G32> {
     a = fmaf(qf[7], v3[1], a);
     return a * e8m0_to_f32(scale);
   }
+  __device__ __forceinline__ float dot_f(const float* qf) const { return dot(uint4{}, qf); }
 };
 
 // One wavefront scores blocks j0 .. min(j0 + U, jend) - 1 of query row `row`
@@ -183,23 +198,38 @@ struct KeyLoad<SPOT_KFMT_MXFP8_G32> {
 // zero means not written yet).  Returns, in lane u < U, the score of
 // block j0 + u (-inf in the other lanes and past jend).
 // This lane's 8 query elements of row `row` (head lane / LPH, dims
-// 8*(lane % LPH) ..) as BF16 bits (qraw) and floats (qf).  Queries coded in
-// an MX format (E2M1 or E4M3 codes, one E8M0 scale per 32) are decoded
-// exactly; their values times a power of two fit BF16, so qraw holds them
-// exactly too.
+// 8*(lane % LPH) ..).  BF16 and MX queries: BF16 bits in qraw and floats in
+// qf, qsc = 1 (MX codes -- E2M1 or E4M3, one E8M0 scale per 32 -- times a
+// power of two fit BF16, so they are decoded exactly into both).  INT4 / INT8
+// queries (one FP16 scale per 32): the integer codes as floats in qf (exact)
+// and the group's scale in qsc, applied to the lane's partial dot product;
+// qraw is unused.
 template <int QFMT>
 __device__ __forceinline__ void load_query(const uint8_t* __restrict__ q,
                                            const uint8_t* __restrict__ q_scale, int row,
-                                           int lane, uint4& qraw, float (&qf)[8]) {
+                                           int lane, uint4& qraw, float (&qf)[8], float& qsc) {
+  qsc = 1.f;
   if constexpr (QFMT == SPOT_KFMT_BF16) {
     qraw = *reinterpret_cast<const uint4*>(q + (size_t)row * 1024 + lane * 16);
     qf[0] = bf16_lo(qraw.x); qf[1] = bf16_hi(qraw.x);
     qf[2] = bf16_lo(qraw.y); qf[3] = bf16_hi(qraw.y);
     qf[4] = bf16_lo(qraw.z); qf[5] = bf16_hi(qraw.z);
     qf[6] = bf16_lo(qraw.w); qf[7] = bf16_hi(qraw.w);
+  } else if constexpr (QFMT == SPOT_KFMT_INT4_G32 || QFMT == SPOT_KFMT_INT8_G32) {
+    qraw = make_uint4(0u, 0u, 0u, 0u);
+    qsc = f16_to_f32(*reinterpret_cast<const uint16_t*>(q_scale + ((size_t)row * 16 + (lane >> 2)) * 2));
+    if constexpr (QFMT == SPOT_KFMT_INT4_G32) {
+      const uint32_t c = *reinterpret_cast<const uint32_t*>(q + (size_t)row * 256 + lane * 4);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) qf[i] = (float)((int)(c << (28 - 4 * i)) >> 28);
+    } else {
+      const u32x2 c = *reinterpret_cast<const u32x2*>(q + (size_t)row * 512 + lane * 8);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) qf[i] = (float)((int)(c[i >> 2] << (24 - 8 * (i & 3))) >> 24);
+    }
   } else {
     static_assert(QFMT == SPOT_KFMT_MXFP4_G32 || QFMT == SPOT_KFMT_MXFP8_G32,
-                  "queries: BF16 or an MX format");
+                  "queries: BF16, INT4, INT8 or an MX format");
     const float sf = e8m0_to_f32(q_scale[(size_t)row * 16 + (lane >> 2)]);
     f32x2 v[4];
     if constexpr (QFMT == SPOT_KFMT_MXFP4_G32) {
@@ -237,9 +267,10 @@ __device__ __forceinline__ float score_blocks(const void* __restrict__ q_sel,
                                              const uint8_t* __restrict__ q_scale = nullptr,
                                              int rec_copies = 1, size_t rec_stride = 0) {
   constexpr int kHeads = 64 / LPH;
+  constexpr bool kIntQ = QFMT == SPOT_KFMT_INT4_G32 || QFMT == SPOT_KFMT_INT8_G32;
   uint4 qraw;
-  float qf[8];
-  load_query<QFMT>(static_cast<const uint8_t*>(q_sel), q_scale, row, lane, qraw, qf);
+  float qf[8], qsc;
+  load_query<QFMT>(static_cast<const uint8_t*>(q_sel), q_scale, row, lane, qraw, qf, qsc);
   const float wh = w[(size_t)row * kHeads + lane / LPH];
 
   // Every slot loads (branch-free, so the loads of all U blocks fly
@@ -253,7 +284,7 @@ __device__ __forceinline__ float score_blocks(const void* __restrict__ q_sel,
   float res = 0.f;
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    float part = key[u].dot(qraw, qf);
+    float part = kIntQ ? key[u].dot_f(qf) * qsc : key[u].dot(qraw, qf);
 #pragma unroll
     for (int off = 1; off < LPH; off <<= 1) part += __shfl_xor(part, off, 64);
     float v = wh * fmaxf(part, 0.f);

@@ -175,8 +175,9 @@ size_t static_scratch_bytes();
 // then).
 hipError_t static_scratch(void** out, bool setup, hipStream_t s);
 bool step_fusable(int h_q, int h_kv, int nblk, int k_max);
-hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_sel,
-                              const void* k_scale, int kfmt, int d_s, const int32_t* n_valid,
+hipError_t launch_decode_step(const void* q_sel, const void* q_scale, int qfmt, const float* w,
+                              const void* k_sel, const void* k_scale, int kfmt, int d_s,
+                              const int32_t* n_valid,
                               float top_p, int k_max, int k_min, int n_sink, int n_recent,
                               const void* q, const void* k, const void* v,
                               const int32_t* seq_len, int batch, int h_q, int h_kv, int l_cap,

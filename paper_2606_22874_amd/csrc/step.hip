@@ -69,7 +69,9 @@ constexpr int kMaxSlots = 16;             // attention workgroups per pair (merg
 constexpr uint64_t kWaitTicks = 20000000; // 0.2 s of the 100 MHz real-time counter
 
 struct StepArgs {
-  const uint16_t* q_sel;
+  const void* q_sel;       // BF16, or codes of the key cache's format (qfmt)
+  const uint8_t* q_scale;  // the query codes' scales (qfmt != BF16)
+  int qfmt;
   const float* w;
   const uint8_t* k_sel;
   const uint8_t* k_scale;
@@ -240,11 +242,17 @@ __device__ __forceinline__ int poll_bitmap(int* ids, const uint32_t* rec, int nw
   return n_ok > slot ? min((n_ok - slot + n_slot - 1) / n_slot, kMaxIds) : 0;
 }
 
+// Queries in BF16 or, when qfmt is not BF16, in the key cache's own format.
 template <int KFMT, int LPH>
 __device__ __forceinline__ void score_run(const StepArgs& a, int row, int nv, int j0, int jend,
                                           int lane) {
-  score_blocks<KFMT, LPH, kScoreRun>(a.q_sel, a.w, a.k_sel, a.k_scale, row, row, a.nblk, nv, j0,
-                                     jend, a.scores, a.srec + (size_t)row * kRecRow, lane);
+  uint32_t* rec = a.srec + (size_t)row * kRecRow;
+  if (KFMT == SPOT_KFMT_BF16 || a.qfmt == SPOT_KFMT_BF16)
+    score_blocks<KFMT, LPH, kScoreRun>(a.q_sel, a.w, a.k_sel, a.k_scale, row, row, a.nblk, nv,
+                                       j0, jend, a.scores, rec, lane);
+  else
+    score_blocks<KFMT, LPH, kScoreRun, KFMT>(a.q_sel, a.w, a.k_sel, a.k_scale, row, row, a.nblk,
+                                             nv, j0, jend, a.scores, rec, lane, a.q_scale);
 }
 
 __device__ __forceinline__ void score_run_rt(const StepArgs& a, int row, int nv, int j0, int jend,
@@ -529,8 +537,9 @@ bool step_fusable(int h_q, int h_kv, int nblk, int k_max) {
   return P <= 512;
 }
 
-hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_sel,
-                              const void* k_scale, int kfmt, int d_s, const int32_t* n_valid,
+hipError_t launch_decode_step(const void* q_sel, const void* q_scale, int qfmt, const float* w,
+                              const void* k_sel, const void* k_scale, int kfmt, int d_s,
+                              const int32_t* n_valid,
                               float top_p, int k_max, int k_min, int n_sink, int n_recent,
                               const void* q, const void* k, const void* v,
                               const int32_t* seq_len, int batch, int h_q, int h_kv, int l_cap,
@@ -538,7 +547,9 @@ hipError_t launch_decode_step(const void* q_sel, const float* w, const void* k_s
                               float* nuc_mass, void* out, float* lse, void* ws, bool static_ws,
                               hipStream_t s) {
   StepArgs a;
-  a.q_sel = static_cast<const uint16_t*>(q_sel);
+  a.q_sel = q_sel;
+  a.q_scale = static_cast<const uint8_t*>(q_scale);
+  a.qfmt = qfmt;
   a.w = w;
   a.k_sel = static_cast<const uint8_t*>(k_sel);
   a.k_scale = static_cast<const uint8_t*>(k_scale);

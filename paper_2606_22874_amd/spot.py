@@ -34,7 +34,8 @@ SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score",
            "spot_select_blocks",
            "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
            "spot_sparse_prefill", "spot_decode_step_workspace_bytes", "spot_decode_step",
-           "spot_decode_step_static", "spot_decode_step_status", "spot_test_force_expiry",
+           "spot_decode_step_q", "spot_decode_step_static", "spot_decode_step_status",
+           "spot_test_force_expiry",
            "spot_probe_stream_read", "spot_probe_sink_words"]
 
 
@@ -80,6 +81,8 @@ def load(path: Optional[str] = None):
         L.spot_decode_step_workspace_bytes.restype = Z
         L.spot_decode_step.argtypes = [P, P, P, P, I, I, I, P, F, I, I, I, I, P, P, P, P, I, I,
                                        I, I, I, F, P, P, P, P, P, P, P, Z, P]
+        L.spot_decode_step_q.argtypes = [P, P, I, P, P, P, I, I, I, P, F, I, I, I, I, P, P, P, P,
+                                         I, I, I, I, I, F, P, P, P, P, P, P, P, Z, P]
         L.spot_decode_step_static.argtypes = [P, P, P, P, I, I, I, P, F, I, I, I, I, P, P, P, P,
                                               I, I, I, I, I, F, P, P, P, P, P, P, P]
         L.spot_decode_step_status.argtypes = [P, Z, I, I, I, I, I, P]
@@ -92,7 +95,7 @@ def load(path: Optional[str] = None):
                      "spot_selector_project",
                      "spot_selector_pool", "spot_select_blocks", "spot_sparse_decode",
                      "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step",
-                     "spot_decode_step_static", "spot_decode_step_status"):
+                     "spot_decode_step_q", "spot_decode_step_static", "spot_decode_step_status"):
             getattr(L, name).restype = ctypes.c_int32
         if path is None:
             _lib = L
@@ -141,14 +144,14 @@ def _check(fn: str, st: int):
         raise SpotError(fn, st)
 
 
-def _sel_cache(k, k_scale, f, n_keys, h_s, d_s, name):
-    """Checks a selector key cache of n_keys keys in format f."""
+def _sel_cache(k, k_scale, f, n_keys, h_s, d_s, name, scale_name="k_scale"):
+    """Checks n_keys selector keys (or queries) of h_s * d_s elements in format f."""
     if f == 0:
         _dev(k, name, BF16, n_keys * h_s * d_s)
         return
     per = h_s * d_s if f in (3, 4) else h_s * d_s // 2      # 8-bit or 4-bit codes
-    _dev(k, name, U8, n_keys * per)
-    _dev(k_scale, "k_scale", (torch.float16, torch.int16) if f in (1, 3) else U8,
+    _dev(k, name, U8 + (torch.int8,), n_keys * per)
+    _dev(k_scale, scale_name, (torch.float16, torch.int16) if f in (1, 3) else U8,
          n_keys * h_s * d_s // 32)
 
 
@@ -173,11 +176,7 @@ def spot_selector_score_q(q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt, n_seq, 
     rows = n_seq * rows_per_seq
     qf = KFMT[qfmt] if isinstance(qfmt, str) else int(qfmt)
     f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
-    if qf == 0:
-        _dev(q_sel, "q_sel", BF16, rows * h_s * d_s)
-    else:
-        _dev(q_sel, "q_sel", U8, rows * h_s * d_s // (2 if qf == 2 else 1))
-        _dev(q_scale, "q_scale", U8, rows * h_s * d_s // 32)
+    _sel_cache(q_sel, q_scale, qf, rows, h_s, d_s, "q_sel", "q_scale")
     _dev(w, "w", F32, rows * h_s)
     _sel_cache(k_sel, k_scale, f, n_seq * nblk, h_s, d_s, "k_sel")
     if n_valid is not None:
@@ -308,10 +307,13 @@ def spot_decode_step_workspace_bytes(batch, h_q, h_kv, d, k_max) -> int:
 
 def spot_decode_step(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max, k_min,
                      n_sink, n_recent, q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale,
-                     scores, idx, count, nuc_mass, out, lse, ws, stream=None):
+                     scores, idx, count, nuc_mass, out, lse, ws, stream=None, q_scale=None,
+                     qfmt="bf16"):
+    """spot_decode_step, or spot_decode_step_q when qfmt is not BF16."""
     nblk = l_cap // BLK
     f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
-    _dev(q_sel, "q_sel", BF16, batch * h_s * d_s)
+    qf = KFMT[qfmt] if isinstance(qfmt, str) else int(qfmt)
+    _sel_cache(q_sel, q_scale, qf, batch, h_s, d_s, "q_sel", "q_scale")
     _dev(w, "w", F32, batch * h_s)
     _sel_cache(k_sel, k_scale, f, batch * nblk, h_s, d_s, "k_sel")
     if n_valid is not None:
@@ -329,12 +331,16 @@ def spot_decode_step(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k
     if lse is not None:
         _dev(lse, "lse", F32, batch * h_q)
     _dev(ws, "ws", None)
-    _check("spot_decode_step", load().spot_decode_step(
-        _ptr(q_sel), _ptr(w), _ptr(k_sel), _ptr(k_scale), f, h_s, d_s, _ptr(n_valid),
-        float(top_p), k_max, k_min, n_sink, n_recent, _ptr(q), _ptr(k), _ptr(v), _ptr(seq_len),
-        batch, h_q, h_kv, d, l_cap, float(sm_scale), _ptr(scores), _ptr(idx), _ptr(count),
-        _ptr(nuc_mass), _ptr(out), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
-        _stream(stream)))
+    rest = (f, h_s, d_s, _ptr(n_valid), float(top_p), k_max, k_min, n_sink, n_recent, _ptr(q),
+            _ptr(k), _ptr(v), _ptr(seq_len), batch, h_q, h_kv, d, l_cap, float(sm_scale),
+            _ptr(scores), _ptr(idx), _ptr(count), _ptr(nuc_mass), _ptr(out), _ptr(lse), _ptr(ws),
+            ws.numel() * ws.element_size(), _stream(stream))
+    if qf == 0:
+        _check("spot_decode_step", load().spot_decode_step(
+            _ptr(q_sel), _ptr(w), _ptr(k_sel), _ptr(k_scale), *rest))
+    else:
+        _check("spot_decode_step_q", load().spot_decode_step_q(
+            _ptr(q_sel), _ptr(q_scale), qf, _ptr(w), _ptr(k_sel), _ptr(k_scale), *rest))
 
 
 def spot_decode_step_static(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max,
@@ -500,11 +506,13 @@ def step_workspace(batch, h_q, h_kv, d, k_max, device="cuda"):
 
 
 def decode_step(q_sel, w, k_sel, q, k, v, seq_len, rule, k_scale=None, kfmt="bf16",
-                n_valid=None, sm_scale=None, ws=None, stream=None):
-    """One fused decode step: (scores, idx, count, nuc_mass, out, lse)."""
+                n_valid=None, sm_scale=None, ws=None, stream=None, q_scale=None, qfmt="bf16"):
+    """One fused decode step: (scores, idx, count, nuc_mass, out, lse).
+    Quantized queries (qfmt = kfmt, codes in q_sel) go through spot_decode_step_q."""
     batch, h_q, d = q.shape
     _, h_kv, l_cap, _ = k.shape
-    h_s, d_s = q_sel.shape[-2], q_sel.shape[-1]
+    qf = KFMT[qfmt] if isinstance(qfmt, str) else int(qfmt)
+    h_s, d_s = q_sel.shape[-2], q_sel.shape[-1] * (2 if qf in (1, 2) else 1)   # 4-bit codes
     nblk = l_cap // BLK
     dev = q.device
     sm_scale = 1.0 / math.sqrt(d) if sm_scale is None else sm_scale
@@ -518,7 +526,8 @@ def decode_step(q_sel, w, k_sel, q, k, v, seq_len, rule, k_scale=None, kfmt="bf1
         ws = step_workspace(batch, h_q, h_kv, d, rule.k_max, dev)
     spot_decode_step(q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, rule.top_p, rule.k_max,
                      rule.k_min, rule.n_sink, rule.n_recent, q, k, v, seq_len, batch, h_q, h_kv,
-                     d, l_cap, sm_scale, scores, idx, count, mass, out, lse, ws, stream)
+                     d, l_cap, sm_scale, scores, idx, count, mass, out, lse, ws, stream,
+                     q_scale=q_scale, qfmt=qfmt)
     return scores, idx, count, mass, out, lse
 
 

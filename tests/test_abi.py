@@ -107,11 +107,22 @@ def test_validation_errors_before_launch(lib):
     # nblk, h_s, d_s, n_valid, scores, stream)
     sq = lib.spot_selector_score_q
     assert sq(nz, None, 2, nz, nz, nz, 2, 1, 1, 4, 4, 128, None, nz, None) == 1   # no q_scale
-    assert sq(nz, nz, 1, nz, nz, nz, 2, 1, 1, 4, 4, 128, None, nz, None) == 3     # INT4 queries
+    assert sq(nz, nz, 7, nz, nz, nz, 2, 1, 1, 4, 4, 128, None, nz, None) == 3     # query format
+    assert sq(nz, None, 1, nz, nz, nz, 2, 1, 1, 4, 4, 128, None, nz, None) == 1   # INT4, no scale
     assert sq(nz, nz, 2, nz, nz, nz, 9, 1, 1, 4, 4, 128, None, nz, None) == 3     # key format
     assert sq(nz, nz, 4, nz, nz, None, 3, 1, 1, 4, 4, 128, None, nz, None) == 1   # key scales
     assert sq(nz, nz, 4, nz, nz, nz, 3, 1, 1, 4, 4, 64, None, nz, None) == 3      # 4 x 64
     assert sq(nz, nz, 4, nz, nz, nz, 3, 0, 1, 4, 4, 128, None, nz, None) == 0
+    # quantized decode step: queries in BF16 or the key cache's own format
+    # (q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max, k_min,
+    # n_sink, n_recent, q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale, scores, idx,
+    # count, nuc_mass, out, lse, ws, ws_bytes, stream)
+    dq = lib.spot_decode_step_q
+    tail = [4, 32, 8, 128, 131072, 0.1, nz, nz, nz, None, nz, None, nz, 1 << 30, None]
+    rule = [None, 0.9, 128, 0, 1, 2, nz, nz, nz, nz]
+    assert dq(nz, nz, 1, nz, nz, nz, 2, 8, 64, *rule, *tail) == 3      # INT4 queries, MXFP4 keys
+    assert dq(nz, None, 2, nz, nz, nz, 2, 8, 64, *rule, *tail) == 1    # codes without scales
+    assert dq(nz, nz, 9, nz, nz, nz, 9, 8, 64, *rule, *tail) == 3      # unknown format
     # per-token scorer: (q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, h_s, d_s,
     # seq_len, scores, stream)
     tok = lib.spot_selector_score_tokens

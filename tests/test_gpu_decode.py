@@ -373,10 +373,18 @@ def _dev_scale(s, fmt):
     (2, 32, 8, 64, "mxfp8", "int4"),
     (1, 16, 4, 128, "mxfp4", "int8"),
     (1, 16, 8, 64, "mxfp8", "mxfp4"),
+    (2, 32, 8, 64, "int4", "int4"),       # integer queries: row kernel, any key format
+    (2, 32, 4, 128, "int8", "int8"),
+    (2, 20, 8, 64, "int8", "bf16"),
+    (1, 16, 4, 128, "int4", "bf16"),
+    (2, 32, 8, 64, "int4", "mxfp4"),
+    (1, 16, 4, 128, "int8", "mxfp8"),
+    (1, 16, 8, 64, "int8", "int4"),
 ])
 def test_selector_score_quantized_queries(B, nqb, Hs, ds, qfmt, kfmt):
-    """Query-block x key-block scores with MX-coded queries, against the
-    oracle decoding the same codes (causal n_valid, several sequences)."""
+    """Query-block x key-block scores with coded queries (MX or integer),
+    against the oracle decoding the same codes (causal n_valid, several
+    sequences)."""
     print(f"[qscore] B={B} nqb={nqb} {Hs}x{ds} q={qfmt} k={kfmt}", flush=True)
     rng = np.random.default_rng([B, nqb, Hs, ds])
     q_sel, w, k_sel = synth.selector_prefill(rng, B, nqb, nqb, Hs, ds)
@@ -393,22 +401,22 @@ def test_selector_score_quantized_queries(B, nqb, Hs, ds, qfmt, kfmt):
     s_o = oracle.selector_score_qk(qc, qs, qfmt, w, kc, ks, kfmt, B * nqb, nqb, Hs, ds,
                                    rows_per_seq=nqb, n_valid=n_valid)
     out = torch.empty((B * nqb, nqb), dtype=torch.float32, device=DEV)
-    spot.spot_selector_score_q(torch.from_numpy(qc).to(DEV), torch.from_numpy(qs).to(DEV), qfmt,
+    spot.spot_selector_score_q(torch.from_numpy(qc).to(DEV), _dev_scale(qs, qfmt), qfmt,
                                f32(w), kd, ksd, kfmt, B, nqb, nqb, Hs, ds, i32(n_valid), out)
     torch.cuda.synchronize()
     assert_scores_close(out.cpu().numpy(), s_o)
 
 
-@pytest.mark.parametrize("qfmt", ["mxfp4", "mxfp8"])
+@pytest.mark.parametrize("qfmt", ["mxfp4", "mxfp8", "int4", "int8"])
 def test_decode_scores_quantized_queries(qfmt):
-    """Decode rows (one query per sequence) with MX-coded queries and the
+    """Decode rows (one query per sequence) with coded queries and the
     128K-token workload's BF16 pooled keys."""
     wl = workload(3, backbone=False)
     qc, qs = synth.QUANTIZERS[qfmt](wl.q_sel)
     s_o = oracle.selector_score_qk(qc, qs, qfmt, wl.w, wl.k_sel, None, "bf16", wl.B, wl.nblk,
                                    wl.Hs, wl.ds, n_valid=wl.n_valid)
     out = torch.empty((wl.B, wl.nblk), dtype=torch.float32, device=DEV)
-    spot.spot_selector_score_q(torch.from_numpy(qc).to(DEV), torch.from_numpy(qs).to(DEV), qfmt,
+    spot.spot_selector_score_q(torch.from_numpy(qc).to(DEV), _dev_scale(qs, qfmt), qfmt,
                                f32(wl.w), bf(wl.k_sel), None, "bf16", wl.B, 1, wl.nblk, wl.Hs,
                                wl.ds, i32(wl.n_valid), out)
     torch.cuda.synchronize()

@@ -112,6 +112,43 @@ def test_step_matches_separate_calls(cfg, fmt):
     assert_same(sep, fus, bitwise=(cfg == 3))
 
 
+@pytest.mark.parametrize("fmt", ["int4", "int8", "mxfp4", "mxfp8"])
+def test_step_quantized_queries(fmt):
+    """spot_decode_step_q: queries and the selector key cache in one quantized
+    format (the 128K-token workload).  The fused launch equals the separate
+    calls (spot_selector_score_q, selection, decode) bit for bit, and its
+    scores and selection match the oracle on the same codes."""
+    wl = workload(3)
+    x = inputs(wl, fmt)
+    qc, qs = synth.QUANTIZERS[fmt](wl.q_sel)
+    qs_dev = qs.view(np.uint16).view(np.int16) if fmt in ("int4", "int8") else qs
+    q_codes = torch.from_numpy(np.ascontiguousarray(qc)).to(DEV)
+    q_scale = torch.from_numpy(np.ascontiguousarray(qs_dev)).to(DEV)
+    print(f"[step] quantized queries {fmt}", flush=True)
+    s0 = torch.empty((wl.B, wl.nblk), dtype=torch.float32, device=DEV)
+    spot.spot_selector_score_q(q_codes, q_scale, fmt, x["w"], x["k_sel"], x["k_scale"], fmt,
+                               wl.B, 1, wl.nblk, wl.Hs, wl.ds, x["n_valid"], s0)
+    i0, c0, m0 = spot.select_blocks(s0, wl.rule, x["n_valid"])
+    o0, l0 = spot.sparse_decode(x["q"], x["k"], x["v"], x["seq_len"], i0, c0, wl.sm_scale)
+    fus = spot.decode_step(q_codes, x["w"], x["k_sel"], x["q"], x["k"], x["v"], x["seq_len"],
+                           wl.rule, k_scale=x["k_scale"], kfmt=fmt, n_valid=x["n_valid"],
+                           sm_scale=wl.sm_scale, q_scale=q_scale, qfmt=fmt)
+    torch.cuda.synchronize()
+    assert_same((s0, i0, c0, m0, o0, l0), fus, bitwise=True)
+    kc, ks = synth.QUANTIZERS[fmt](wl.k_sel)
+    s_o = oracle.selector_score_qk(qc, qs, fmt, wl.w, kc, ks, fmt, wl.B, wl.nblk, wl.Hs, wl.ds,
+                                   n_valid=wl.n_valid)
+    s = fus[0].cpu().numpy()
+    fin = np.isfinite(s_o)
+    assert np.array_equal(np.isfinite(s), fin)
+    assert np.all(np.abs(s[fin] - s_o[fin]) <= 1e-4 * np.abs(s_o[fin]) + 1e-6)
+    idx_o, cnt_o, _ = oracle.select_blocks(s_o.astype(np.float32).astype(np.float64), wl.rule,
+                                           wl.n_valid)
+    print("[step] selection vs oracle:",
+          check_all(s_o.astype(np.float32), wl.n_valid, wl.rule, idx_o, cnt_o,
+                    fus[1].cpu().numpy(), fus[2].cpu().numpy()))
+
+
 def test_step_end_to_end_vs_oracle():
     wl = workload(3)
     x = inputs(wl, "bf16")

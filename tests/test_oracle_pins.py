@@ -170,6 +170,39 @@ def test_score_quantized_queries_match_bf16_when_exact(fmt):
                                  rows_per_seq=rows), s_plain)
 
 
+@pytest.mark.parametrize("fmt", ["int4", "int8"])
+@pytest.mark.parametrize("kfmt", ["bf16", "int8", "mxfp4"])
+def test_score_integer_queries_match_bf16_when_exact(fmt, kfmt):
+    """Integer query codes with power-of-two FP16 scales are exact in BF16
+    (|code| <= 128 needs at most 8 significand bits): scoring the coded
+    queries equals scoring BF16 queries holding the decoded values, for keys
+    in several formats.  A wrong nibble order, sign extension, scale index or
+    a scale applied per head instead of per 32 elements breaks it."""
+    rng = np.random.default_rng(67)
+    rows, Hs, ds, nblk = 3, 8, 64, 6
+    lo, hi = (-8, 8) if fmt == "int4" else (-128, 128)
+    codes = rng.integers(lo, hi, (rows, Hs, ds))
+    e = rng.integers(-9, 4, (rows, Hs, ds // 32))
+    scale16 = np.ldexp(1.0, e).astype(np.float16)
+    vals = codes * np.repeat(scale16.astype(np.float64), 32, axis=-1)
+    if fmt == "int4":
+        nib = (codes & 0xF).astype(np.uint8)
+        qc = (nib[..., 0::2] | (nib[..., 1::2] << 4)).astype(np.uint8)
+    else:
+        qc = codes.astype(np.int8).view(np.uint8)
+    k = bf16_bits(rng.standard_normal((1, nblk, Hs, ds)).astype(np.float32))
+    w = rng.uniform(0, 1, (rows, Hs)).astype(np.float32)
+    if kfmt == "bf16":
+        kc, ks = k, None
+    else:
+        kc, ks = synth.QUANTIZERS[kfmt](k)
+    s_q = oracle.selector_score_qk(qc, scale16.view(np.uint16), fmt, w, kc, ks, kfmt, rows, nblk,
+                                   Hs, ds, rows_per_seq=rows)
+    s_b = oracle.selector_score_qk(bf16_bits(vals.astype(np.float32)), None, "bf16", w, kc, ks,
+                                   kfmt, rows, nblk, Hs, ds, rows_per_seq=rows)
+    np.testing.assert_array_equal(s_q, s_b)
+
+
 def test_score_invariants():
     rng = np.random.default_rng(11)
     Hs, ds, nblk = 4, 64, 9
