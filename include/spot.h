@@ -106,7 +106,8 @@ const char *spot_version(void);
  *
  * Supported: h_s * d_s == 512 with d_s in {64, 128}; rope_dim even, 0 <=
  * rope_dim <= d_s; rope_base > 0.  The arithmetic is FP32 (products of
- * BF16, fixed summation order) with the rotation angle in FP64.  Errors:
+ * BF16, fixed summation order); the rotation angle is formed and reduced
+ * modulo 2 pi in FP64, its sine and cosine taken in FP32.  Errors:
  * SPOT_ERR_NULL, SPOT_ERR_SHAPE (sizes, rows % rows_per_seq, alignment),
  * SPOT_ERR_UNSUPPORTED (head shape, rope_dim, rope_base).
  */
@@ -115,6 +116,33 @@ spot_status spot_selector_project(const void *h, const void *w_q, const void *w_
                                   int h_s, int d_s, int rope_dim, float rope_base, void *q_out,
                                   float *w_out, void *k_cache, int rows_per_seq, int l_cap,
                                   void *stream);
+
+/*
+ * spot_selector_project_pooled -- one decode step's selector front end in a
+ * single launch: spot_selector_project with one row per sequence
+ * (rows = n_seq, rows_per_seq = 1), then spot_selector_pool of the block the
+ * new key landed in (first_block = pos / 64, max_blocks = 1), with the same
+ * arithmetic and summation order, so q_out, w_out, k_cache and k_pool are
+ * bit for bit those of the two calls (Section 2.1: the new token's selector
+ * key joins the per-token cache and the pooled key of its block is the mean
+ * of the block's token keys).
+ *
+ *  pos      device int32 [n_seq]: the new token's position (no key stored or
+ *           pooled outside [0, l_cap))
+ *  seq_len  device int32 [n_seq] or NULL (pos + 1): tokens below it count in
+ *           the pooled mean
+ *  k_pool   device BF16 [n_seq, l_cap/64, h_s, d_s] (output), 16-byte aligned
+ *  the rest as spot_selector_project.
+ *
+ * Errors: those of spot_selector_project; SPOT_ERR_NULL for k_pool,
+ * SPOT_ERR_SHAPE when l_cap % 64 != 0.
+ */
+spot_status spot_selector_project_pooled(const void *h, const void *w_q, const void *w_k,
+                                         const void *w_w, const int32_t *pos,
+                                         const int32_t *seq_len, int n_seq, int d_model,
+                                         int h_s, int d_s, int rope_dim, float rope_base,
+                                         void *q_out, float *w_out, void *k_cache, void *k_pool,
+                                         int l_cap, void *stream);
 
 /*
  * spot_selector_pool -- block-pooled selector keys from the per-token cache.

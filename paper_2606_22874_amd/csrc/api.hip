@@ -61,7 +61,27 @@ spot_status spot_selector_project(const void* h, const void* w_q, const void* w_
   if (rows == 0) return SPOT_OK;
   return from_hip(launch_selector_project(h, w_q, w_k, w_w, pos, rows, d_model, h_s, d_s,
                                           rope_dim, rope_base, q_out, w_out, k_cache,
-                                          rows_per_seq, l_cap, static_cast<hipStream_t>(stream)));
+                                          rows_per_seq, l_cap, nullptr, nullptr,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+spot_status spot_selector_project_pooled(const void* h, const void* w_q, const void* w_k,
+                                         const void* w_w, const int32_t* pos,
+                                         const int32_t* seq_len, int n_seq, int d_model,
+                                         int h_s, int d_s, int rope_dim, float rope_base,
+                                         void* q_out, float* w_out, void* k_cache, void* k_pool,
+                                         int l_cap, void* stream) {
+  if (!k_pool) return SPOT_ERR_NULL;
+  if (l_cap % kBlk) return SPOT_ERR_SHAPE;
+  if (!aligned16(k_pool)) return SPOT_ERR_SHAPE;
+  const spot_status st = spot_selector_project(h, w_q, w_k, w_w, pos, 0, d_model, h_s, d_s,
+                                               rope_dim, rope_base, q_out, w_out, k_cache, 1,
+                                               l_cap, stream);   // validation only
+  if (st != SPOT_OK || n_seq == 0) return st;
+  if (n_seq < 0) return SPOT_ERR_SHAPE;
+  return from_hip(launch_selector_project(h, w_q, w_k, w_w, pos, n_seq, d_model, h_s, d_s,
+                                          rope_dim, rope_base, q_out, w_out, k_cache, 1, l_cap,
+                                          k_pool, seq_len, static_cast<hipStream_t>(stream)));
 }
 
 spot_status spot_selector_pool(const void* k_tok, void* k_pool, int n_seq, int l_cap, int h_s,

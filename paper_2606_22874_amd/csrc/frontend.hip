@@ -11,11 +11,14 @@
 // Projection at decode is a matrix-vector product per sequence, bound by
 // reading the weights (2 x 512 x d_model BF16 + the small W_w): each
 // workgroup owns one task -- two output rows of W_q or W_k that the rotation
-// pairs (or two neighbouring non-rotary rows), or two rows of W_w -- and its
-// 8 waves split d_model in 512-element chunks, so every weight byte is
-// loaded once with all of a workgroup's loads in flight together.  Hidden
+// pairs (or two neighbouring non-rotary rows), the first tasks also two rows
+// of W_w -- and its 8 waves split d_model in 512-element chunks, so every
+// weight byte is loaded once with all of a workgroup's loads in flight
+// together, and the 512 workgroups are resident at once.  Hidden
 // rows are re-read from L2 by every task.  Partial dots meet in LDS and are
 // summed in a fixed order (deterministic); one lane per row finishes.
+#include <cmath>
+
 #include "spot_internal.h"
 
 namespace spot {
@@ -30,32 +33,45 @@ __device__ __forceinline__ float dot8_bf16(const u32x4& a, const u32x4& b, float
   return dot2_bf16(a[3], b[3], c);
 }
 
-// Tasks: [0, n_out) pairs of W_q / W_k rows (n_out/2 each), then
-// ceil(h_s / 2) pairs of W_w rows.  Pair p of one head (d_s/2 pairs):
+// Tasks: n_out pairs of W_q / W_k rows (n_out/2 each); the first ceil(h_s/2)
+// tasks also take a pair of W_w rows, so that the grid (n_out = 512
+// workgroups of 8 waves) fits the device at once.  Pair p of one head (d_s/2 pairs):
 // p < rope_dim/2 -> dims (p, p + rope_dim/2), rotated; otherwise dims
 // (rope_dim + 2(p - rope_dim/2), +1), not rotated.
 // RP hidden rows per pass (4, 8 or 16): every pass loads its RP rows
 // without branches (rows past the end re-read the last row, in cache), so
 // all of a wave's loads are in flight together.
-template <int RP>
+// POOL (one row per sequence): a W_k task also pools its two dims of the
+// block each row's key lands in.  Wave w holds (row, dim) pairs w, w + 8, ..
+// of the pass with lane = token of the block: the other tokens' values are
+// loaded before the weights (and waited for only at the end), the new key's
+// value joins its lane, and each pair is summed in pool_kernel's order
+// exactly (16-token quarters in token order, then the quarters in order;
+// tokens at or past the block's count hold -0.0, the exact identity of
+// addition), so the pooled key is the one spot_selector_pool would compute
+// after the append.
+template <int RP, bool POOL>
 __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w_q,
     const uint16_t* __restrict__ w_k, const uint16_t* __restrict__ w_w,
     const int32_t* __restrict__ pos, int rows, int d_model, int h_s, int d_s, int rope_dim,
-    double rope_base, uint16_t* __restrict__ q_out, float* __restrict__ w_out,
-    uint16_t* __restrict__ k_cache, int rows_per_seq, int l_cap) {
-  __shared__ float part[kProjWaves][RP][2];
+    double rope_log2_base, uint16_t* __restrict__ q_out, float* __restrict__ w_out,
+    uint16_t* __restrict__ k_cache, int rows_per_seq, int l_cap,
+    uint16_t* __restrict__ k_pool, const int32_t* __restrict__ seq_len) {
+  __shared__ float part[kProjWaves][RP][4];   // [wave][row][row a, b, W_w c, d]
+  __shared__ float pool_new[POOL ? RP : 1][2];   // the new key's value, [row][dim a/b]
+  constexpr int kPairs = POOL ? (2 * RP + kProjWaves - 1) / kProjWaves : 1;   // per wave
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n_out = h_s * d_s;
   const int task = blockIdx.x;
   const int half = rope_dim / 2;
 
-  // This task's two weight rows and where their results go.
-  int kind, ra, rb, dim_a = 0, dim_b = 0, head = 0;
+  // This task's two weight rows and where their results go (dims a, b of
+  // q or k), plus W_w rows c, d for the first tasks.
+  int dim_a = 0, dim_b = 0, head = 0;
   bool rotate = false;
-  const uint16_t* wmat;
-  if (task < n_out) {
-    kind = task < n_out / 2 ? 0 : 1;               // 0: q, 1: k
+  const int kind = task < n_out / 2 ? 0 : 1;       // 0: q, 1: k
+  {
     const int p = task % (n_out / 2);
     head = p / (d_s / 2);
     const int pp = p % (d_s / 2);
@@ -67,49 +83,66 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
       dim_a = rope_dim + 2 * (pp - half);
       dim_b = dim_a + 1;
     }
-    ra = head * d_s + dim_a;
-    rb = head * d_s + dim_b;
-    wmat = kind == 0 ? w_q : w_k;
-  } else {
-    kind = 2;
-    ra = 2 * (task - n_out);
-    rb = min(ra + 1, h_s - 1);
-    wmat = w_w;
   }
-  const uint16_t* wa = wmat + (size_t)ra * d_model;
-  const uint16_t* wb = wmat + (size_t)rb * d_model;
-  // the pair's frequency (FP64), computed while the first loads are in flight
-  const double freq = rotate ? pow(rope_base, -2.0 * dim_a / rope_dim) : 0.0;
-
+  const uint16_t* wmat = kind == 0 ? w_q : w_k;
+  const uint16_t* wa = wmat + (size_t)(head * d_s + dim_a) * d_model;
+  const uint16_t* wb = wmat + (size_t)(head * d_s + dim_b) * d_model;
+  const bool with_w = task < (h_s + 1) / 2;
+  const int rc = 2 * task, rd = min(rc + 1, h_s - 1);
+  const uint16_t* wc = w_w + (size_t)(with_w ? rc : 0) * d_model;
+  const uint16_t* wd = w_w + (size_t)(with_w ? rd : 0) * d_model;
   for (int r0 = 0; r0 < rows; r0 += RP) {
     const int nr = min(RP, rows - r0);
-    // the finishing lane's (row r0 + lane) rotation, also ahead of the dots
-    float c_rot = 1.f, s_rot = 0.f;
-    int p_row = 0;
-    if (wave == 0 && lane < nr && kind != 2) {
-      p_row = pos[r0 + lane];
-      if (rotate) {
-        double sn, cs;
-        sincos((double)p_row * freq, &sn, &cs);   // pos up to ~1e6 times freq <= 1
-        c_rot = (float)cs;
-        s_rot = (float)sn;
+    // 1. the first chunk's weight and hidden loads go out first
+    int c = wave * 512 + lane * 8;
+    bool have = c < d_model;
+    u32x4 a, b, cw, dw, x[RP];
+    auto load_chunk = [&]() {
+      a = *reinterpret_cast<const u32x4*>(wa + c);
+      b = *reinterpret_cast<const u32x4*>(wb + c);
+      if (with_w) {
+        cw = *reinterpret_cast<const u32x4*>(wc + c);
+        dw = *reinterpret_cast<const u32x4*>(wd + c);
       }
-    }
-    float acc_a[RP], acc_b[RP];
-#pragma unroll
-    for (int i = 0; i < RP; ++i) acc_a[i] = acc_b[i] = 0.f;
-    for (int c = wave * 512 + lane * 8; c < d_model; c += kProjWaves * 512) {
-      const u32x4 a = *reinterpret_cast<const u32x4*>(wa + c);
-      const u32x4 b = *reinterpret_cast<const u32x4*>(wb + c);
-      u32x4 x[RP];
 #pragma unroll
       for (int i = 0; i < RP; ++i)
         x[i] = *reinterpret_cast<const u32x4*>(h + (size_t)min(r0 + i, rows - 1) * d_model + c);
+    };
+    if (have) load_chunk();
+    // 2. positions and, for pooling, the block's other tokens: their waits
+    // come later (the pooling positions are uniform scalar loads, whose wait
+    // does not hold up the vector loads above)
+    int p_row = 0;   // the finishing lane's (row r0 + lane) position
+    if (wave == 0 && lane < nr) p_row = pos[r0 + lane];
+    float pv[kPairs];   // POOL, W_k task: pair wave + 8m's value at token `lane`
+#pragma unroll
+    for (int m = 0; m < kPairs; ++m) {
+      pv[m] = -0.f;
+      const int pr = wave + kProjWaves * m, i = pr >> 1, sel = pr & 1;
+      if (POOL && kind == 1 && i < nr) {
+        const int r = r0 + i, p = pos[r];
+        if (p >= 0 && p < l_cap && lane != p % kBlk)
+          pv[m] = bf16_lo(k_cache[((size_t)r * l_cap + p / kBlk * kBlk + lane) * n_out +
+                                  head * d_s + (sel ? dim_b : dim_a)]);
+      }
+    }
+    // 3. the dot products, chunk by chunk
+    float acc_a[RP], acc_b[RP], acc_c[RP], acc_d[RP];
+#pragma unroll
+    for (int i = 0; i < RP; ++i) acc_a[i] = acc_b[i] = acc_c[i] = acc_d[i] = 0.f;
+    while (have) {
 #pragma unroll
       for (int i = 0; i < RP; ++i) {
         acc_a[i] = dot8_bf16(a, x[i], acc_a[i]);
         acc_b[i] = dot8_bf16(b, x[i], acc_b[i]);
+        if (with_w) {
+          acc_c[i] = dot8_bf16(cw, x[i], acc_c[i]);
+          acc_d[i] = dot8_bf16(dw, x[i], acc_d[i]);
+        }
       }
+      c += kProjWaves * 512;
+      have = c < d_model;
+      if (have) load_chunk();
     }
 #pragma unroll
     for (int i = 0; i < RP; ++i) {
@@ -119,23 +152,43 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
           part[wave][i][0] = sa;
           part[wave][i][1] = sb;
         }
+        if (with_w) {
+          const float sc = wave_sum(acc_c[i]), sd = wave_sum(acc_d[i]);
+          if (lane == 0) {
+            part[wave][i][2] = sc;
+            part[wave][i][3] = sd;
+          }
+        }
       }
     }
     __syncthreads();
     if (wave == 0 && lane < nr) {
       const int r = r0 + lane;
-      float A = 0.f, B = 0.f;
+      float A = 0.f, B = 0.f, C = 0.f, D = 0.f;
 #pragma unroll
       for (int w = 0; w < kProjWaves; ++w) {
         A += part[w][lane][0];
         B += part[w][lane][1];
+        if (with_w) {
+          C += part[w][lane][2];
+          D += part[w][lane][3];
+        }
       }
-      if (kind == 2) {
-        w_out[(size_t)r * h_s + ra] = A;
-        if (ra + 1 < h_s) w_out[(size_t)r * h_s + ra + 1] = B;
-      } else {
+      if (with_w) {
+        w_out[(size_t)r * h_s + rc] = C;
+        if (rc + 1 < h_s) w_out[(size_t)r * h_s + rc + 1] = D;
+      }
+      {
         const int p = p_row;
         if (rotate) {
+          // angle pos * base^(-2 dim_a / rope_dim) in FP64, reduced to
+          // [-pi, pi] in FP64 (two-part 2 pi), then sin and cos in FP32
+          const double theta = (double)p * exp2(-2.0 * dim_a / rope_dim * rope_log2_base);
+          const double k = rint(theta * 0.15915494309189535);   // 1 / (2 pi)
+          double red = fma(-k, 6.283185307179586, theta);       // 2 pi, high part
+          red = fma(-k, 2.4492935982947064e-16, red);           // 2 pi, low part
+          float s_rot, c_rot;
+          sincosf((float)red, &s_rot, &c_rot);
           const float A2 = A * c_rot - B * s_rot;
           const float B2 = B * c_rot + A * s_rot;
           A = A2;
@@ -150,12 +203,47 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
                     : nullptr;
         }
         if (dst) {
-          dst[head * d_s + dim_a] = f32_to_bf16_rne(A);
-          dst[head * d_s + dim_b] = f32_to_bf16_rne(B);
+          const uint16_t ha = f32_to_bf16_rne(A), hb = f32_to_bf16_rne(B);
+          dst[head * d_s + dim_a] = ha;
+          dst[head * d_s + dim_b] = hb;
+          if (POOL && kind == 1) {
+            pool_new[lane][0] = bf16_lo(ha);
+            pool_new[lane][1] = bf16_lo(hb);
+          }
         }
       }
     }
-    __syncthreads();   // part[] is reused by the next pass
+    __syncthreads();   // part[] is reused by the next pass; pool_new is complete
+    if (POOL && kind == 1) {
+#pragma unroll
+      for (int m = 0; m < kPairs; ++m) {
+        const int pr = wave + kProjWaves * m, i = pr >> 1, sel = pr & 1;
+        if (i >= nr) continue;
+        const int r = r0 + i, p = pos[r];
+        int len = seq_len ? seq_len[r] : p + 1;
+        len = len > l_cap ? l_cap : len;
+        const int lo = p / kBlk * kBlk, n = min(len - lo, kBlk);
+        if (p < 0 || p >= l_cap || n <= 0) continue;
+        float x = lane == p % kBlk ? pool_new[i][sel] : pv[m];
+        if (lane >= n) x = -0.f;
+        float q4[4];
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          float acc = 0.f;
+#pragma unroll
+          for (int u = 0; u < 16; ++u)
+            acc += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), qq * 16 + u));
+          q4[qq] = acc;
+        }
+        if (lane == 0) {
+          const float v = ((q4[0] + q4[1]) + q4[2]) + q4[3];
+          const int nblk = l_cap / kBlk;
+          k_pool[((size_t)r * nblk + p / kBlk) * n_out + head * d_s + (sel ? dim_b : dim_a)] =
+              f32_to_bf16_rne(v / (float)n);
+        }
+      }
+    }
+    if (POOL) __syncthreads();   // pool_new is reused by the next pass
   }
 }
 
@@ -225,22 +313,30 @@ hipError_t launch_selector_project(const void* h, const void* w_q, const void* w
                                    const void* w_w, const int32_t* pos, int rows, int d_model,
                                    int h_s, int d_s, int rope_dim, float rope_base, void* q_out,
                                    float* w_out, void* k_cache, int rows_per_seq, int l_cap,
-                                   hipStream_t s) {
-  const int tasks = h_s * d_s + (h_s + 1) / 2;
+                                   void* k_pool, const int32_t* seq_len, hipStream_t s) {
+  const int tasks = h_s * d_s;   // h_s * d_s / 2 >= ceil(h_s / 2) tasks carry the W_w rows
   auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, dim3(tasks), dim3(kProjWaves * 64), 0, s,
                        static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w_q),
                        static_cast<const uint16_t*>(w_k), static_cast<const uint16_t*>(w_w), pos,
-                       rows, d_model, h_s, d_s, rope_dim, (double)rope_base,
+                       rows, d_model, h_s, d_s, rope_dim, std::log2((double)rope_base),
                        static_cast<uint16_t*>(q_out), w_out, static_cast<uint16_t*>(k_cache),
-                       rows_per_seq, l_cap);
+                       rows_per_seq, l_cap, static_cast<uint16_t*>(k_pool), seq_len);
   };
-  if (rows <= 4)
-    go(project_kernel<4>);
-  else if (rows <= 8)
-    go(project_kernel<8>);
-  else
-    go(project_kernel<16>);
+  if (k_pool) {   // one row per sequence (the caller checks rows_per_seq == 1)
+    if (rows <= 4)
+      go(project_kernel<4, true>);
+    else if (rows <= 8)
+      go(project_kernel<8, true>);
+    else
+      go(project_kernel<16, true>);
+  } else if (rows <= 4) {
+    go(project_kernel<4, false>);
+  } else if (rows <= 8) {
+    go(project_kernel<8, false>);
+  } else {
+    go(project_kernel<16, false>);
+  }
   return hipGetLastError();
 }
 

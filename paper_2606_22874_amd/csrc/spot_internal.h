@@ -145,6 +145,7 @@ hipError_t launch_selector_project(const void* h, const void* w_q, const void* w
                                    const void* w_w, const int32_t* pos, int rows, int d_model,
                                    int h_s, int d_s, int rope_dim, float rope_base, void* q_out,
                                    float* w_out, void* k_cache, int rows_per_seq, int l_cap,
+                                   void* k_pool, const int32_t* seq_len,
                                    hipStream_t s);
 hipError_t launch_selector_pool(const void* k_tok, void* k_pool, int n_seq, int l_cap,
                                 const int32_t* seq_len, const int32_t* first_block,

@@ -30,7 +30,7 @@ BLK = 64
 
 SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score",
            "spot_selector_score_q", "spot_selector_score_tokens", "spot_selector_project",
-           "spot_selector_pool",
+           "spot_selector_project_pooled", "spot_selector_pool",
            "spot_select_blocks",
            "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
            "spot_sparse_prefill", "spot_decode_step_workspace_bytes", "spot_decode_step",
@@ -71,6 +71,8 @@ def load(path: Optional[str] = None):
         L.spot_selector_score_q.argtypes = [P, P, I, P, P, P, I, I, I, I, I, I, P, P, P]
         L.spot_selector_project.argtypes = [P, P, P, P, P, I, I, I, I, I, F, P, P, P, I, I, P]
         L.spot_selector_pool.argtypes = [P, P, I, I, I, I, P, P, I, P]
+        L.spot_selector_project_pooled.argtypes = [P, P, P, P, P, P, I, I, I, I, I, F, P, P, P,
+                                                   P, I, P]
         L.spot_select_blocks.argtypes = [P, I, I, P, F, I, I, I, I, P, P, P, P]
         L.spot_decode_workspace_bytes.argtypes = [I, I, I, I, I]
         L.spot_decode_workspace_bytes.restype = Z
@@ -92,7 +94,7 @@ def load(path: Optional[str] = None):
         L.spot_probe_stream_read.restype = ctypes.c_int32
         L.spot_probe_sink_words.restype = I
         for name in ("spot_selector_score", "spot_selector_score_q", "spot_selector_score_tokens",
-                     "spot_selector_project",
+                     "spot_selector_project", "spot_selector_project_pooled",
                      "spot_selector_pool", "spot_select_blocks", "spot_sparse_decode",
                      "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step",
                      "spot_decode_step_q", "spot_decode_step_static", "spot_decode_step_status"):
@@ -216,6 +218,27 @@ def spot_selector_project(h, w_q, w_k, w_w, pos, rows, d_model, h_s, d_s, rope_d
     _check("spot_selector_project", load().spot_selector_project(
         _ptr(h), _ptr(w_q), _ptr(w_k), _ptr(w_w), _ptr(pos), rows, d_model, h_s, d_s, rope_dim,
         rope_base, _ptr(q_out), _ptr(w_out), _ptr(k_cache), rows_per_seq, l_cap,
+        _stream(stream)))
+
+
+def spot_selector_project_pooled(h, w_q, w_k, w_w, pos, seq_len, n_seq, d_model, h_s, d_s,
+                                 rope_dim, rope_base, q_out, w_out, k_cache, k_pool, l_cap,
+                                 stream=None):
+    n_out = h_s * d_s
+    _dev(h, "h", BF16, n_seq * d_model)
+    _dev(w_q, "w_q", BF16, n_out * d_model)
+    _dev(w_k, "w_k", BF16, n_out * d_model)
+    _dev(w_w, "w_w", BF16, h_s * d_model)
+    _dev(pos, "pos", I32, n_seq)
+    if seq_len is not None:
+        _dev(seq_len, "seq_len", I32, n_seq)
+    _dev(q_out, "q_out", BF16, n_seq * n_out)
+    _dev(w_out, "w_out", F32, n_seq * h_s)
+    _dev(k_cache, "k_cache", BF16, n_seq * l_cap * n_out)
+    _dev(k_pool, "k_pool", BF16, n_seq * (l_cap // BLK) * n_out)
+    _check("spot_selector_project_pooled", load().spot_selector_project_pooled(
+        _ptr(h), _ptr(w_q), _ptr(w_k), _ptr(w_w), _ptr(pos), _ptr(seq_len), n_seq, d_model, h_s,
+        d_s, rope_dim, rope_base, _ptr(q_out), _ptr(w_out), _ptr(k_cache), _ptr(k_pool), l_cap,
         _stream(stream)))
 
 

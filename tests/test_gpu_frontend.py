@@ -194,6 +194,50 @@ def test_decode_front_end_step():
     assert np.all(np.abs(s_g[fin] - s_o[fin]) <= 1e-4 * np.abs(s_o[fin]) + 1e-6)
 
 
+@pytest.mark.parametrize("B,L,Hs,ds,rope_dim,with_len", [
+    (4, 8192, 8, 64, 32, True),       # decode, Qwen3-8B hidden size
+    (4, 32768, 4, 128, 64, False),    # seq_len = pos + 1
+    (9, 4096, 4, 128, 0, True),       # more rows than one pass (RP = 16 path)
+])
+def test_fused_front_end_equals_project_then_pool(B, L, Hs, ds, rope_dim, with_len):
+    """spot_selector_project_pooled gives exactly what spot_selector_project
+    followed by spot_selector_pool of the new token's block gives: queries,
+    weights, the cache and the whole pooled cache, bit for bit.  Positions
+    cover the first token of a block, the last, the middle, position 0, a
+    seq_len past pos (later tokens of the block count) and a position
+    outside the cache (nothing stored or pooled)."""
+    d_model = 4096
+    rng = np.random.default_rng([B, L, Hs])
+    k_tok = bf16_bits(rng.standard_normal((B, L, Hs, ds), dtype=np.float32))
+    pos = np.array([L - 1, 64, 127, 0, 5000 % L, 200, 63, L, 1000][:B], np.int32)
+    seq_len = np.minimum(pos + 1 + np.array([0, 0, 0, 0, 7, 0, 0, 0, 30][:B]), L).astype(np.int32)
+    h, wq, wk, ww = synth.selector_frontend(11, B, d_model, Hs, ds)
+    args = (bf(h), bf(wq), bf(wk), bf(ww))
+    pool0 = torch.zeros((B, L // 64, Hs, ds), dtype=torch.bfloat16, device=DEV)
+    spot.spot_selector_pool(bf(k_tok), pool0, B, L, Hs, ds, dev(np.minimum(pos, L)))
+    outs = []
+    for fused in (False, True):
+        q_out = torch.empty((B, Hs, ds), dtype=torch.bfloat16, device=DEV)
+        w_out = torch.empty((B, Hs), dtype=torch.float32, device=DEV)
+        cache, pooled = bf(k_tok), pool0.clone()
+        sl = dev(seq_len) if with_len else None
+        if fused:
+            spot.spot_selector_project_pooled(*args, dev(pos), sl, B, d_model, Hs, ds, rope_dim,
+                                              1.0e6, q_out, w_out, cache, pooled, L)
+        else:
+            spot.spot_selector_project(*args, dev(pos), B, d_model, Hs, ds, rope_dim, 1.0e6,
+                                       q_out, w_out, cache, 1, L)
+            spot.spot_selector_pool(cache, pooled, B, L, Hs, ds,
+                                    sl if with_len else dev(pos + 1), dev(pos // 64), 1)
+        outs.append((q_out, w_out, cache, pooled))
+    torch.cuda.synchronize()
+    for name, a, b in zip(("q_out", "w_out", "k_cache", "k_pool"), *outs):
+        if a.dtype == torch.bfloat16:
+            a, b = a.view(torch.int16), b.view(torch.int16)
+        assert torch.equal(a, b), name
+    assert not torch.equal(outs[1][3].view(torch.int16), pool0.view(torch.int16))
+
+
 def test_front_end_in_a_graph_matches_eager():
     """Projection and pooling captured in a HIP graph: every replay (with
     eager work and synchronisations between replays) gives the eager result."""
