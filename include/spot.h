@@ -402,15 +402,19 @@ spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
  *  nuc_mass device float [batch] or NULL        (output)
  *  out, lse as spot_sparse_decode               (output; lse may be NULL)
  *  ws       device, spot_decode_step_workspace_bytes(batch, h_q, h_kv, d,
- *           k_max) bytes, 16-byte aligned: the decode partials and counters
- *           laid out as for spot_sparse_decode (used when the stages run
- *           separately), then (from the next 16-byte boundary) the fused
- *           launch's partials, completion counters, expiry word, 4096
- *           score record words per sequence and a 256-word bitmap per
- *           (sequence, KV head) pair.  It must be zero-filled before its
- *           first use; every call leaves it ready for the next one (its
- *           counters, records and bitmaps return to zero).  Calls that share
- *           a workspace must not overlap in time.
+ *           k_max) bytes, 16-byte aligned: first a control region -- one
+ *           completion counter per (sequence, KV head) pair (used by the
+ *           fused launch and the separate decode alike), the expiry word
+ *           (16 bytes), 4096 score record words per sequence and a 256-word
+ *           bitmap per pair -- then, from a 256-byte boundary, the split
+ *           partials (o [batch, h_q, n_split, 128] then (m, l)
+ *           [batch, h_q, n_split, 2], FP32).  It must be zero-filled before its
+ *           first use; every call leaves it ready for the next call with
+ *           the same (batch, h_q, h_kv, k_max) (its counters, records and
+ *           bitmaps return to zero; the partials hold data).  Zero-fill it
+ *           again before using it for another such shape: the control words
+ *           of one shape can lie where another left partials.  Calls that
+ *           share a workspace must not overlap in time.
  */
 size_t spot_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d, int k_max);
 
