@@ -106,8 +106,9 @@ const char *spot_version(void);
  *
  * Supported: h_s * d_s == 512 with d_s in {64, 128}; rope_dim even, 0 <=
  * rope_dim <= d_s; rope_base > 0.  The arithmetic is FP32 (products of
- * BF16, fixed summation order); the rotation angle is formed and reduced
- * modulo 2 pi in FP64, its sine and cosine taken in FP32.  Errors:
+ * BF16, fixed summation order); the rotation angle (position times the
+ * pair's frequency rope_base^(-2i/rope_dim), both in FP64) is reduced modulo
+ * 2 pi in FP64, its sine and cosine taken in FP32.  Errors:
  * SPOT_ERR_NULL, SPOT_ERR_SHAPE (sizes, rows % rows_per_seq, alignment),
  * SPOT_ERR_UNSUPPORTED (head shape, rope_dim, rope_base).
  */
@@ -153,8 +154,9 @@ spot_status spot_selector_project_pooled(const void *h, const void *w_q, const v
  * y = 0 .. max_blocks-1,
  *     k_pool[b, j] = BF16( (sum over t in block j, t < seq_len[b], of
  *                           k_tok[b, t], in FP32) / count )
- * where the FP32 sum runs in token order within each 16-token quarter of the
- * block and the four quarter sums are added in order (deterministic).
+ * where each 16-token quarter of the block is summed in FP32 as a pairwise
+ * tree ((t0 + t1) + (t2 + t3), then groups of 4 and of 8; absent tokens count
+ * as -0.0) and the four quarter sums are added in order (deterministic).
  * Blocks with no token below seq_len, or outside [0, l_cap/64), are left
  * untouched.  Decode re-pools only the block the new token fell in
  * (first_block = (seq_len - 1) / 64, max_blocks = 1); prefill pools all

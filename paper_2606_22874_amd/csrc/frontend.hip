@@ -5,7 +5,7 @@
 //    q^I and w written out, k^I appended to the per-token selector cache at
 //    (sequence, position);
 //  * pool_kernel: the pooled selector key of a block, the mean of its
-//    existing tokens' keys (FP32 sums over 16-token quarters in token order,
+//    existing tokens' keys (FP32 pairwise sums over each 16-token quarter,
 //    the quarters added in order, then BF16).
 //
 // Projection at decode is a matrix-vector product per sequence, bound by
@@ -16,7 +16,17 @@
 // weight byte is loaded once with all of a workgroup's loads in flight
 // together, and the 512 workgroups are resident at once.  Hidden
 // rows are re-read from L2 by every task.  Partial dots meet in LDS and are
-// summed in a fixed order (deterministic); one lane per row finishes.
+// summed in a fixed order (deterministic); one lane per row finishes.  The
+// rotation angle only needs the position and the pair's frequency (FP64,
+// from the host), so it is formed while the weight loads are in flight.
+//
+// Pooled sums (pool_kernel, and project_kernel with POOL): each 16-token
+// quarter of the block is summed as a pairwise tree -- (t0 + t1) + (t2 + t3)
+// at the first two levels, then groups of 4 and 8 -- and the four quarter
+// sums are added in order; absent tokens count as -0.0, the exact identity
+// of addition.  With lane = token the tree is four DPP steps (adjacent lane,
+// lane pair, half-row mirror, row mirror; addition is commutative, so every
+// lane of a group holds the same sum).
 #include <cmath>
 
 #include "spot_internal.h"
@@ -25,6 +35,36 @@ namespace spot {
 namespace {
 
 constexpr int kProjWaves = 8;
+constexpr int kMaxRopePairs = 64;
+
+// base^(-2i / rope_dim) for the rotary pairs i < rope_dim / 2 (FP64).
+struct RopeFreq {
+  double f[kMaxRopePairs];
+};
+
+// Sum over each aligned group of 16 lanes as the pairwise tree above; every
+// lane of the group ends with the group's sum.
+template <int CTRL>
+__device__ __forceinline__ float dpp_add(float v) {
+  return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF,
+                                                        false));
+}
+__device__ __forceinline__ float quarter_tree_sum(float x) {
+  x = dpp_add<0xB1>(x);      // quad_perm [1, 0, 3, 2]: lane ^ 1
+  x = dpp_add<0x4E>(x);      // quad_perm [2, 3, 0, 1]: lane ^ 2
+  x = dpp_add<0x141>(x);     // row_half_mirror: the other group of 4 in the half row
+  return dpp_add<0x140>(x);  // row_mirror: the other half of the row
+}
+
+// The same tree over 16 values held by one lane.
+__device__ __forceinline__ float tree_sum16(const float (&t)[16]) {
+  float a[8], b[4];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) a[k] = t[2 * k] + t[2 * k + 1];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) b[k] = a[2 * k] + a[2 * k + 1];
+  return (b[0] + b[1]) + (b[2] + b[3]);
+}
 
 __device__ __forceinline__ float dot8_bf16(const u32x4& a, const u32x4& b, float c) {
   c = dot2_bf16(a[0], b[0], c);
@@ -55,7 +95,7 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w_q,
     const uint16_t* __restrict__ w_k, const uint16_t* __restrict__ w_w,
     const int32_t* __restrict__ pos, int rows, int d_model, int h_s, int d_s, int rope_dim,
-    double rope_log2_base, uint16_t* __restrict__ q_out, float* __restrict__ w_out,
+    RopeFreq freq, uint16_t* __restrict__ q_out, float* __restrict__ w_out,
     uint16_t* __restrict__ k_cache, int rows_per_seq, int l_cap,
     uint16_t* __restrict__ k_pool, const int32_t* __restrict__ seq_len) {
   __shared__ float part[kProjWaves][RP][4];   // [wave][row][row a, b, W_w c, d]
@@ -93,7 +133,10 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
   const uint16_t* wd = w_w + (size_t)(with_w ? rd : 0) * d_model;
   for (int r0 = 0; r0 < rows; r0 += RP) {
     const int nr = min(RP, rows - r0);
-    // 1. the first chunk's weight and hidden loads go out first
+    // 1. the finishing lane's (row r0 + lane) position, then the first
+    // chunk's weight and hidden loads
+    int p_row = 0;
+    if (wave == 0 && lane < nr) p_row = pos[r0 + lane];
     int c = wave * 512 + lane * 8;
     bool have = c < d_model;
     u32x4 a, b, cw, dw, x[RP];
@@ -109,11 +152,19 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
         x[i] = *reinterpret_cast<const u32x4*>(h + (size_t)min(r0 + i, rows - 1) * d_model + c);
     };
     if (have) load_chunk();
-    // 2. positions and, for pooling, the block's other tokens: their waits
-    // come later (the pooling positions are uniform scalar loads, whose wait
-    // does not hold up the vector loads above)
-    int p_row = 0;   // the finishing lane's (row r0 + lane) position
-    if (wave == 0 && lane < nr) p_row = pos[r0 + lane];
+    // 2. the rotation of the finishing lane's row: angle pos * freq in FP64,
+    // reduced to [-pi, pi] in FP64 (two-part 2 pi), sin and cos in FP32
+    float s_rot = 0.f, c_rot = 1.f;
+    if (rotate && wave == 0 && lane < nr) {
+      const double theta = (double)p_row * freq.f[dim_a];
+      const double k = rint(theta * 0.15915494309189535);   // 1 / (2 pi)
+      double red = fma(-k, 6.283185307179586, theta);       // 2 pi, high part
+      red = fma(-k, 2.4492935982947064e-16, red);           // 2 pi, low part
+      sincosf((float)red, &s_rot, &c_rot);
+    }
+    // 3. for pooling, the block's other tokens: their waits come later (the
+    // pooling positions are uniform scalar loads, whose wait does not hold
+    // up the vector loads above)
     float pv[kPairs];   // POOL, W_k task: pair wave + 8m's value at token `lane`
 #pragma unroll
     for (int m = 0; m < kPairs; ++m) {
@@ -126,7 +177,7 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
                                   head * d_s + (sel ? dim_b : dim_a)]);
       }
     }
-    // 3. the dot products, chunk by chunk
+    // 4. the dot products, chunk by chunk
     float acc_a[RP], acc_b[RP], acc_c[RP], acc_d[RP];
 #pragma unroll
     for (int i = 0; i < RP; ++i) acc_a[i] = acc_b[i] = acc_c[i] = acc_d[i] = 0.f;
@@ -181,14 +232,6 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
       {
         const int p = p_row;
         if (rotate) {
-          // angle pos * base^(-2 dim_a / rope_dim) in FP64, reduced to
-          // [-pi, pi] in FP64 (two-part 2 pi), then sin and cos in FP32
-          const double theta = (double)p * exp2(-2.0 * dim_a / rope_dim * rope_log2_base);
-          const double k = rint(theta * 0.15915494309189535);   // 1 / (2 pi)
-          double red = fma(-k, 6.283185307179586, theta);       // 2 pi, high part
-          red = fma(-k, 2.4492935982947064e-16, red);           // 2 pi, low part
-          float s_rot, c_rot;
-          sincosf((float)red, &s_rot, &c_rot);
           const float A2 = A * c_rot - B * s_rot;
           const float B2 = B * c_rot + A * s_rot;
           A = A2;
@@ -226,15 +269,11 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
         if (p < 0 || p >= l_cap || n <= 0) continue;
         float x = lane == p % kBlk ? pool_new[i][sel] : pv[m];
         if (lane >= n) x = -0.f;
+        x = quarter_tree_sum(x);
         float q4[4];
 #pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-          float acc = 0.f;
-#pragma unroll
-          for (int u = 0; u < 16; ++u)
-            acc += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), qq * 16 + u));
-          q4[qq] = acc;
-        }
+        for (int qq = 0; qq < 4; ++qq)
+          q4[qq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), qq * 16));
         if (lane == 0) {
           const float v = ((q4[0] + q4[1]) + q4[2]) + q4[3];
           const int nblk = l_cap / kBlk;
@@ -249,9 +288,9 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
 
 // One workgroup of 4 waves per (sequence, block to pool): block
 // j = first_block[b] + y.  Wave w sums tokens [16w, 16w + 16) of the block
-// (all 16 rows in flight), lane l elements 8l .. 8l+7, in token order; the
-// four partial sums are added in wave order, divided by the token count and
-// rounded to BF16.
+// (all 16 rows in flight), lane l elements 8l .. 8l+7, as the pairwise tree;
+// the four partial sums are added in wave order, divided by the token count
+// and rounded to BF16.
 __global__ __launch_bounds__(256) void pool_kernel(const uint16_t* __restrict__ k_tok,
                                                    uint16_t* __restrict__ k_pool, int l_cap,
                                                    const int32_t* __restrict__ seq_len,
@@ -269,7 +308,7 @@ __global__ __launch_bounds__(256) void pool_kernel(const uint16_t* __restrict__ 
   const int t0 = wave * 16;
   float acc[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  for (int e = 0; e < 8; ++e) acc[e] = -0.f;
   if (t0 < n) {
     const uint16_t* src = k_tok + ((size_t)b * l_cap + lo) * 512 + lane * 8;
     u32x4 x[16];
@@ -277,14 +316,14 @@ __global__ __launch_bounds__(256) void pool_kernel(const uint16_t* __restrict__ 
     for (int u = 0; u < 16; ++u)
       x[u] = *reinterpret_cast<const u32x4*>(src + (size_t)min(t0 + u, n - 1) * 512);
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      if (t0 + u < n) {
+    for (int e = 0; e < 8; ++e) {
+      float t[16];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          acc[2 * i] += bf16_lo(x[u][i]);
-          acc[2 * i + 1] += bf16_hi(x[u][i]);
-        }
+      for (int u = 0; u < 16; ++u) {
+        const uint32_t wd = x[u][e >> 1];
+        t[u] = t0 + u < n ? ((e & 1) ? bf16_hi(wd) : bf16_lo(wd)) : -0.f;
       }
+      acc[e] = tree_sum16(t);
     }
   }
 #pragma unroll
@@ -315,11 +354,16 @@ hipError_t launch_selector_project(const void* h, const void* w_q, const void* w
                                    float* w_out, void* k_cache, int rows_per_seq, int l_cap,
                                    void* k_pool, const int32_t* seq_len, hipStream_t s) {
   const int tasks = h_s * d_s;   // h_s * d_s / 2 >= ceil(h_s / 2) tasks carry the W_w rows
+  if (rope_dim / 2 > kMaxRopePairs) return hipErrorInvalidValue;
+  RopeFreq freq;
+  const double lb = std::log2((double)rope_base);
+  for (int i = 0; i < kMaxRopePairs; ++i)
+    freq.f[i] = i < rope_dim / 2 ? std::exp2(-2.0 * i / rope_dim * lb) : 0.0;
   auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, dim3(tasks), dim3(kProjWaves * 64), 0, s,
                        static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w_q),
                        static_cast<const uint16_t*>(w_k), static_cast<const uint16_t*>(w_w), pos,
-                       rows, d_model, h_s, d_s, rope_dim, std::log2((double)rope_base),
+                       rows, d_model, h_s, d_s, rope_dim, freq,
                        static_cast<uint16_t*>(q_out), w_out, static_cast<uint16_t*>(k_cache),
                        rows_per_seq, l_cap, static_cast<uint16_t*>(k_pool), seq_len);
   };

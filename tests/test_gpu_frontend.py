@@ -122,14 +122,17 @@ def test_project_skips_keys_outside_the_cache():
 
 
 def fp32_quarter_mean(k_tok, b, lo, hi):
-    """The documented FP32 order: token-order sums over the block's 16-token
-    quarters, the quarters added in order, one division."""
+    """The documented FP32 order: each 16-token quarter of the block summed
+    as a pairwise tree ((t0 + t1) + (t2 + t3), then groups of 4 and 8; absent
+    tokens -0.0), the quarters added in order, one division."""
+    zero = np.full(k_tok.shape[2:], -0.0, np.float32)
     parts = []
     for q in range(4):
-        acc = np.zeros(k_tok.shape[2:], np.float32)
-        for t in range(lo + 16 * q, min(lo + 16 * q + 16, hi)):
-            acc += bf16_value(k_tok[b, t])
-        parts.append(acc)
+        vals = [bf16_value(k_tok[b, t]).astype(np.float32) if t < hi else zero
+                for t in range(lo + 16 * q, lo + 16 * q + 16)]
+        while len(vals) > 1:
+            vals = [vals[2 * i] + vals[2 * i + 1] for i in range(len(vals) // 2)]
+        parts.append(vals[0])
     tot = ((parts[0] + parts[1]) + parts[2]) + parts[3]
     return bf16_bits(tot / np.float32(hi - lo))
 
