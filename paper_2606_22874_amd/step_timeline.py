@@ -1,14 +1,17 @@
 """Per-phase timeline of the fused decode step (measurement tool).
 
-    python -m paper_2606_22874_amd.step_timeline [--cfg 3] [--trials 6]
+    python -m paper_2606_22874_amd.step_timeline [--cfg 3] [--trials 6] [--burst 1]
 
 Builds ``libspot_timeline.so`` (next to libspot.so) -- the library with the step kernel
 compiled from ``csrc/step_timeline.hip`` (step.hip with its phase hooks
 stamping the device's 100 MHz real-time counter) -- then runs the decode
 workload (default: 131072 tokens, batch 4), times 200 back-to-back fused
-steps, and stamps ``--trials`` single launches.  It prints, as markdown, the
-median over the trials of each phase's time in microseconds since the first
-workgroup of the launch started.  Needs an MI355X.
+steps, and stamps ``--trials`` launches: with ``--burst 1`` each one starts
+on an idle device, with ``--burst N`` it is the last of N back-to-back
+launches (the regime bench.py times; every launch overwrites the stamps).
+It prints, as markdown, the median over the trials of each phase's time in
+microseconds since the first workgroup of the launch started.  Needs an
+MI355X.
 """
 from __future__ import annotations
 
@@ -22,6 +25,7 @@ import numpy as np
 from . import build as B
 
 TIMELINE_SO = os.path.join(B.PKG, "libspot_timeline.so")
+SCORERS_PER_ROW = 64   # the step kernel's scoring workgroups per row
 TIMELINE_SRC = "step_timeline.hip"
 
 
@@ -48,7 +52,7 @@ def _pct(x, q):
     return float(np.percentile(x, q)) if len(x) else float("nan")
 
 
-def run(cfg: int = 3, trials: int = 6) -> dict:
+def run(cfg: int = 3, trials: int = 6, burst: int = 1) -> dict:
     import torch
 
     from . import spot, synth
@@ -104,7 +108,8 @@ def run(cfg: int = 3, trials: int = 6) -> dict:
         if lib.spot_timeline_clear() != 0:
             raise RuntimeError("spot_timeline_clear failed")
         torch.cuda.synchronize()
-        step(t + 1)
+        for i in range(burst):
+            step(t + 1 + i)
         torch.cuda.synchronize()
         if lib.spot_timeline_read(ts.ctypes.data, sel.ctypes.data, xcc.ctypes.data) != 0:
             raise RuntimeError("spot_timeline_read failed")
@@ -114,9 +119,11 @@ def run(cfg: int = 3, trials: int = 6) -> dict:
         x_ = xcc[:n]
         g0 = t_[:, 0].min()
         us = lambda v: (np.asarray(v, np.int64) - g0) * 0.01   # noqa: E731
-        scorer = t_[:, 1] > t_[:, 0]
+        # workgroup i scores for row i % B when i / B is below the per-row count
+        # (every workgroup stamps phase 1; only these did scoring before it)
+        scorer = np.arange(n) // B_ < min(SCORERS_PER_ROW, n // B_)
         selector = np.arange(n) < B_
-        merged = t_[:, 7] > 0
+        merged = t_[:, 7] > t_[:, 6]   # stamped by this launch's merge
         end = np.where(merged, t_[:, 7], t_[:, 6])
         r = {
             "workgroups": n,
@@ -146,6 +153,7 @@ def run(cfg: int = 3, trials: int = 6) -> dict:
            for k in rows[0]}
     med["us_per_step_untraced"] = us_per_step
     med["trials"] = trials
+    med["burst"] = burst
     return med
 
 
@@ -173,14 +181,18 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--cfg", type=int, default=3)
     ap.add_argument("--trials", type=int, default=6)
+    ap.add_argument("--burst", type=int, default=1,
+                    help="stamp the last of this many back-to-back launches")
     ap.add_argument("--no-build", action="store_true")
     args = ap.parse_args()
     if not args.no_build or not os.path.exists(TIMELINE_SO):
         build()
-    m = run(args.cfg, args.trials)
+    m = run(args.cfg, args.trials, max(args.burst, 1))
+    start = ("the launch starts on an idle device" if m["burst"] == 1 else
+             f"the last of {m['burst']} back-to-back launches")
     print(f"decode workload {args.cfg}: {m['workgroups']:.0f} workgroups; "
           f"{m['us_per_step_untraced']:.2f} us per step (timeline build, 200 steps, "
-          f"HIP events)\n")
+          f"HIP events); stamped: {start}\n")
     print(table(m))
 
 
