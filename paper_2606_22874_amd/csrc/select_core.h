@@ -146,10 +146,16 @@ struct SelWgSmem {
   float red_m[kSelWG / 64];       // survivors' mass partials
   int red_i[kSelWG / 64];
   int red_bad[kSelWG / 64];       // per wave: a score source failed
-  int gc[kSelWG / 64];            // threshold-bin members per wave
+  int gc[kSelWG / 64];            // threshold-bin members / survivors per wave
   int bc[4];
   uint64_t cut;
   float cut_mass;
+  // nucleus without a sort (cap <= 64); separate from s_K and gc, which the
+  // threshold-bin ranking may still be reading when a wave gets here
+  uint64_t s_sk[64];              // survivors' packed rank keys, in block order
+  float s_pe[64];                 // their exp(s - M)
+  int part_rk[kSelWG / 64][64];   // per wave: better survivors of its run, per survivor
+  float part_mb[kSelWG / 64][64]; // per wave: their mass, per survivor
 };
 
 // What select_row_core leaves in each thread (ids [tid*EPT, tid*EPT + EPT)).
@@ -190,9 +196,15 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
 //     and the better ones, with no packing or ranking).  A bin too crowded to
 //     rank (heavy ties) falls back to an 8-bit radix select on the keys;
 //  3. below top_p * Z the cap binds and the survivors are the answer;
-//     otherwise they are compacted [2], sorted in wave 0 by (score desc, id
-//     asc), prefix-summed and cut where the prefix first reaches top_p * Z,
-//     then floored by k_min [1];
+//     otherwise the survivors are ranked by (score desc, id asc) and cut
+//     where the prefix mass first reaches top_p * Z, then floored by k_min:
+//     the survivors are compacted in block order [2]; up to 64 of them are
+//     ranked without sorting -- wave w compares every survivor with
+//     survivors 16w .. 16w+15 (how many are better, and their mass) [1],
+//     and every wave adds the four parts in order and takes the same cut (a
+//     survivor is in the nucleus when the mass of the better survivors is
+//     still below top_p * Z); more are sorted in wave 0, prefix-summed and
+//     cut [1];
 // It returns, in every thread, the bits of its ids that belong to S (reserved
 // + chosen) and the nucleus mass; sel_positions / sel_write turn them into
 // the ascending id list [1].  A score source that fails (a bounded wait that
@@ -476,7 +488,78 @@ __device__ __forceinline__ SelRow select_row_core(SelWgSmem<EPT, SPL>& sm, const
   if (n >= 0 && n_reserved + n < k_min) n = min(k_min - n_reserved, cap);
   uint32_t chosen = n == 0 ? 0u : surv;
   float mass = n > 0 && Z > 0.f ? msum / Z : 0.f;
-  if (n < 0 || (n > 0 && n < cap)) {
+  if ((n < 0 || (n > 0 && n < cap)) && cap <= 64) {
+    // survivors (exactly cap <= 64 of them) ranked without a sort,
+    // compacted in block order
+    int run;
+    int slot = wg_excl_scan(__popc(surv), sm.red_i, run);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      if ((surv >> e) & 1u) {
+        sm.s_sk[slot] = rank_key(key[e], j0 + e);
+        sm.s_pe[slot] = pe[e];
+        ++slot;
+      }
+    }
+    __syncthreads();
+    SPOT_SEL_TS(5);
+    // lane i holds survivor i
+    const bool real = lane < run;
+    const uint64_t mine = real ? sm.s_sk[lane] : 0ull;
+    const float pmine = real ? sm.s_pe[lane] : 0.f;
+    {
+      // survivors [16 w, 16 w + 16) against survivor `lane`, in order, eight
+      // per batch of LDS reads
+      int rk = 0;
+      float mb = 0.f;
+#pragma unroll
+      for (int jb = 16 * wave; jb < 16 * wave + 16; jb += 8) {
+        uint64_t kk[8];
+        float pp[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          kk[u] = sm.s_sk[jb + u];
+          pp[u] = sm.s_pe[jb + u];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const bool better = jb + u < run && kk[u] > mine;
+          rk += better ? 1 : 0;
+          mb += better ? pp[u] : 0.f;
+        }
+      }
+      sm.part_rk[wave][lane] = rk;
+      sm.part_mb[wave][lane] = mb;
+    }
+    __syncthreads();
+    SPOT_SEL_TS(9);
+    int rk = 0;
+    float mb = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      rk += sm.part_rk[w][lane];
+      mb += sm.part_mb[w][lane];
+    }
+    int nn = n;
+    if (nn < 0) {
+      nn = __popcll(__ballot(real && mb < pz));
+      if (n_reserved + nn < k_min) nn = min(k_min - n_reserved, cap);
+    }
+    nn = min(max(nn, 1), run);
+    const uint64_t at = __ballot(real && rk == nn - 1);
+    const int src = at ? __builtin_ctzll(at) : 0;
+    const uint64_t kc = readlane_u64(mine, src);
+    const float m_at = readlane_f(mb + pmine, src);
+    mass = Z > 0.f ? m_at / Z : 0.f;
+    const uint32_t ck = (uint32_t)(kc >> 32);
+    const int ci = (int)(0xffffffffu - (uint32_t)kc);
+    chosen = 0u;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const bool ch = ((surv >> e) & 1u) && (key[e] > ck || (key[e] == ck && j0 + e <= ci));
+      chosen |= (uint32_t)ch << e;
+    }
+  } else if (n < 0 || (n > 0 && n < cap)) {
     // survivors (exactly cap of them) in rank order: compact, sort, cut
     int total;
     int pos = wg_excl_scan(__popc(surv), sm.red_i, total);
@@ -535,6 +618,7 @@ __device__ __forceinline__ SelRow select_row_core(SelWgSmem<EPT, SPL>& sm, const
       const bool ch = ((surv >> e) & 1u) && (key[e] > ck || (key[e] == ck && j0 + e <= ci));
       chosen |= (uint32_t)ch << e;
     }
+  
   }
   SPOT_SEL_TS(4);
 

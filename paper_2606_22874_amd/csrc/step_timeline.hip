@@ -9,7 +9,9 @@
 //                (the pair's last workgroup);
 //   selection    0 core entered, 1 this wave's scores in, 2 every wave's
 //                scores in (after the first barrier), 6 histogram, 7 bin
-//                scan, 8 members packed, 3 survivors, 4 core done.
+//                scan, 8 members packed, 3 survivors, 5 survivors packed
+//                and 9 ranked (the nucleus cut of at most 64 survivors),
+//                4 core done.
 // Everything else is step.hip compiled unchanged; paper_2606_22874_amd/
 // step_timeline.py links this object with the library's other objects.
 #include <hip/hip_runtime.h>
