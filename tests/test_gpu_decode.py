@@ -161,6 +161,13 @@ SELECT_CASES = [
     (8, 4096, Rule(1.0, 3000, 0, 0, 0), "ragged"),      # static top-K, cap above 2048
     (8, 2048, Rule(0.999, 1000, 0, 1, 2), None),        # nucleus under a 1000-block cap
     (4, 2048, Rule(0.0, 900, 600, 1, 2), None),         # k_min floor of 600 blocks
+    # long rows, small caps: the cut inside at most 64 survivors is ranked by
+    # counting, above 64 by the sort
+    (8, 2048, Rule(0.9, 64, 0, 1, 2), None),            # cap 61
+    (8, 1024, Rule(0.5, 67, 0, 1, 2), "ragged"),        # cap 64: the last counted
+    (8, 1024, Rule(0.5, 68, 0, 1, 2), "ragged"),        # cap 65: the first sorted
+    (8, 2048, Rule(0.3, 40, 30, 1, 2), None),           # k_min floor under a cap of 37
+    (8, 600, Rule(0.2, 20, 0, 2, 3), None),             # short nucleus, cap 15
 ]
 
 
@@ -189,12 +196,13 @@ def test_select_parity_same_scores(case):
     np.testing.assert_allclose(mass_g.cpu().numpy()[exact], mass_o[exact], atol=2e-5)
 
 
-def test_select_deterministic_and_ties():
-    """Exact ties break toward the lower block id; repeated runs are bitwise equal."""
+@pytest.mark.parametrize("rule", [Rule(0.9, 100, 0, 1, 2), Rule(0.02, 40, 0, 1, 2)])
+def test_select_deterministic_and_ties(rule):
+    """Exact ties break toward the lower block id; repeated runs are bitwise
+    equal (a cap of 97 that binds; a cut inside 37 tied survivors)."""
     rows, nblk = 32, 2048
     s = np.zeros((rows, nblk), np.float32)
     s[:, ::7] = 1.0                       # many exactly equal maxima
-    rule = Rule(0.9, 100, 0, 1, 2)
     idx_o, cnt_o, _ = oracle.select_blocks(s.astype(np.float64), rule)
     a = spot.select_blocks(f32(s), rule)
     b = spot.select_blocks(f32(s), rule)
@@ -205,7 +213,8 @@ def test_select_deterministic_and_ties():
     np.testing.assert_array_equal(a[1].cpu().numpy(), cnt_o)
 
 
-@pytest.mark.parametrize("nblk,k_max", [(300, 100), (2048, 100), (2048, 1500), (8192, 700)])
+@pytest.mark.parametrize("nblk,k_max", [(300, 100), (2048, 100), (2048, 40), (2048, 1500),
+                                        (8192, 700)])
 def test_select_negative_zero_ties_positive_zero(nblk, k_max):
     """-0.0 and +0.0 are the same score: a cut through a run of zeros of
     both signs takes the lower ids, whatever their sign (every selection
