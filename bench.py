@@ -714,11 +714,18 @@ def prefill_leg(args, torch, spot, synth, dev, timed):
     for i in range(2):
         score(i), select(i), attend(i)
     torch.cuda.synchronize()
+    # The layer and its stages are timed in three interleaved rounds and each
+    # figure is the median of its rounds (the ~3 ms prefill launches vary by
+    # several percent from one loop to the next).
     n = args.prefill_iters
-    attn_ms = timed(attend, n)
-    score_ms = timed(score, n)
-    select_ms = timed(select, n)
-    step_ms = timed(lambda i: (score(i), select(i), attend(i)), n)
+    rounds = {"attn": [], "score": [], "select": [], "step": []}
+    for _ in range(3):
+        rounds["step"].append(timed(lambda i: (score(i), select(i), attend(i)), n))
+        rounds["attn"].append(timed(attend, n))
+        rounds["score"].append(timed(score, n))
+        rounds["select"].append(timed(select, n))
+    med = {k: float(np.median(v)) for k, v in rounds.items()}
+    attn_ms, score_ms, select_ms, step_ms = med["attn"], med["score"], med["select"], med["step"]
 
     ids = idx.cpu().numpy()
     c = cnt.cpu().numpy()
@@ -752,8 +759,11 @@ def prefill_leg(args, torch, spot, synth, dev, timed):
             "issued_flops_per_launch": mfma_flops,
             "issued_tflops": round(issued_tflops, 1),
             "avg_launch_us": round(attn_ms * 1e3, 1),
-            "avg_launch_timing": "HIP events around back-to-back launches on the launch stream",
+            "avg_launch_timing": "HIP events around back-to-back launches on the launch "
+                                 "stream; median of three interleaved rounds",
         },
+        "round_ms": {"layer": [round(x, 4) for x in rounds["step"]],
+                     "attention": [round(x, 4) for x in rounds["attn"]]},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = prefill_cpu_baseline(pw)
