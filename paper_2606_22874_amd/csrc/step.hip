@@ -84,6 +84,7 @@ struct StepArgs {
   const uint16_t* v;
   const int32_t* seq_len;
   int batch, h_q, h_kv, l_cap, nblk, n_slot;
+  int slot_div;        // ceil(2^18 / n_slot): x / n_slot == (x * slot_div) >> 18 below 2^14
   float scale_log2;
   float* scores;
   int32_t* idx;
@@ -189,8 +190,8 @@ __device__ __forceinline__ int nth_set_bit(uint64_t x, int r) {
 }
 
 __device__ __forceinline__ int poll_bitmap(int* ids, const uint32_t* rec, int nwords, int k_max,
-                                           int slot, int n_slot, int nb_valid, uint64_t ticks,
-                                           bool give_up) {
+                                           int slot, int n_slot, int slot_div, int nb_valid,
+                                           uint64_t ticks, bool give_up) {
   const int lane = __lane_id();
   // lane l: words [4l, 4l + 4), ids [64l, 64l + 64)
   uint32_t wd[4];
@@ -230,16 +231,21 @@ __device__ __forceinline__ int poll_bitmap(int* ids, const uint32_t* rec, int nw
   const int incl = wave_incl_scan_i(cnt);
   const int pos = incl - cnt;             // list position of this lane's first id
   const int total = min(__builtin_amdgcn_readlane(incl, 63), k_max);
-  const int n_ok = min(wave_sum_i(__popcll(bits & valid)), total);
+  // set bits below nb_valid: the list position of id nb_valid (the lane that
+  // holds it adds its own bits below it)
+  const int lv = min(nb_valid >> 6, 63);
+  const int n_ok = min(__builtin_amdgcn_readlane(incl - cnt + __popcll(bits & valid), lv), total);
   // This lane's entries of the share: positions slot + kk * n_slot in
   // [pos, min(pos + cnt, n_ok)), each the (position - pos)-th set bit.
+  // Divisions by n_slot are a multiply and a shift (positions stay below
+  // 2^14, where that is exact).
   const int end = min(pos + cnt, n_ok);
-  for (int kk = pos > slot ? (pos - slot + n_slot - 1) / n_slot : 0;; ++kk) {
+  for (int kk = pos > slot ? ((pos - slot + n_slot - 1) * slot_div) >> 18 : 0;; ++kk) {
     const int p = slot + kk * n_slot;
     if (p >= end || kk >= kMaxIds) break;
     ids[kk] = base_id + nth_set_bit(bits, p - pos);
   }
-  return n_ok > slot ? min((n_ok - slot + n_slot - 1) / n_slot, kMaxIds) : 0;
+  return n_ok > slot ? min(((n_ok - slot + n_slot - 1) * slot_div) >> 18, kMaxIds) : 0;
 }
 
 // Queries in BF16 or, when qfmt is not BF16, in the key cache's own format.
@@ -364,7 +370,7 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
   const int nb_valid = (sl + kBlk - 1) / kBlk;
   if (wave == 0) {
     const int n = poll_bitmap(sm.dec.ids, bmap, (a.nblk + 15) / 16, a.k_max, slot, n_slot,
-                              nb_valid, a.wait_ticks, false);
+                              a.slot_div, nb_valid, a.wait_ticks, false);
     if (lane == 0) sm.dec.n_local = n;
   }
   __syncthreads();
@@ -433,6 +439,7 @@ hipError_t launch_step_t(StepArgs& a, int n_pairs, int n_slot_max, hipStream_t s
   const int cap = step_capacity<EPT, SPL>();
   if (cap < n_pairs) return hipErrorCooperativeLaunchTooLarge;
   a.n_slot = n_slot_max < cap / n_pairs ? n_slot_max : cap / n_pairs;
+  a.slot_div = ((1 << 18) + a.n_slot - 1) / a.n_slot;
   hipLaunchKernelGGL((step_kernel<EPT, SPL>), dim3(n_pairs * a.n_slot), dim3(64 * kStepG), 0, s,
                      a);
   return hipGetLastError();
