@@ -208,7 +208,9 @@ def select_blocks(scores, rule, n_valid=None):
     return idx, cnt, mass
 
 
-def sparse_decode(q, k, v, seq_len, idx, count, sm_scale):
+def sparse_decode(q, k, v, seq_len, idx, count, sm_scale, blk=64):
+    """Attention over the tokens of the selected blocks of blk tokens each
+    (Section 2): [B, h_q, d] outputs and [B, h_q] log-sum-exps in float64."""
     q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
     B, h_q, d = q.shape
     _, h_kv, l_cap, _ = k.shape
@@ -218,7 +220,7 @@ def sparse_decode(q, k, v, seq_len, idx, count, sm_scale):
     out = np.empty((B, h_q, d), dtype=np.float64)
     lse = np.empty((B, h_q), dtype=np.float64)
     lib().oracle_sparse_decode(_p(q), _p(k), _p(v), _p(sl), _p(idx), _p(cnt), idx.shape[1], B,
-                               h_q, h_kv, d, l_cap, 64, float(sm_scale), _p(out), _p(lse))
+                               h_q, h_kv, d, l_cap, int(blk), float(sm_scale), _p(out), _p(lse))
     return out, lse
 
 

@@ -218,15 +218,17 @@ def selector_planted(rng, B, L, Hs, ds, seq_len, n_planted=4, cosine=0.8):
 
 
 def selector_tokens(seed, B, L, Hs, ds, seq_len, rule=None, zipf_a=1.1, t0=16.0,
-                    noise=0.06):
+                    noise=0.06, blk=BLK):
     """Per-token selector inputs with the Zipf relevance profile of
-    ``selector_zipf`` carried by one token per block.
+    ``selector_zipf`` carried by one token per block of ``blk`` tokens (64,
+    the KV block, or 16, the paper's selector block).
 
     Returns q_sel [B, Hs, ds] (N(0, I/ds) draws, so |q_h| is about 1),
     w [B, Hs] ~ U(0, 1) and k_tok [B, L, Hs, ds] (BF16 bits).  Every token key
     is N(0, I) (filled in parallel in runs of up to 4096 tokens), which gives
     background token scores of order sum_h w_h.  In each residual block (not
-    a sink or recency block of ``rule``) one visible "lead" token, at a random
+    a sink or recency block of ``rule``, counted in blocks of ``blk``) one
+    visible "lead" token, at a random
     position, is replaced by a key whose dot product with each head's query is
     T_j / sum_h w_h + N(0, noise^2), with T_j = t0 - zipf_a * ln(rank_j) for a
     random permutation rank of 1..n_res; its other directions are N(0, I).
@@ -246,13 +248,13 @@ def selector_tokens(seed, B, L, Hs, ds, seq_len, rule=None, zipf_a=1.1, t0=16.0,
     k_tok = normal_bf16(seed, 4, (B, L // run, run * Hs * ds)).reshape(B, L, Hs, ds)
     for b in range(B):
         n = int(min(max(int(seq_len[b]), 0), L))
-        nv = (n + BLK - 1) // BLK
+        nv = (n + blk - 1) // blk
         res = np.flatnonzero(~_reserved_mask(nv, rule.n_sink, rule.n_recent))
         if len(res) == 0:
             continue
         T = t0 - zipf_a * np.log(rng.permutation(len(res)) + 1.0)
-        lo = res * BLK
-        pos = lo + (rng.random(len(res)) * (np.minimum(lo + BLK, n) - lo)).astype(np.int64)
+        lo = res * blk
+        pos = lo + (rng.random(len(res)) * (np.minimum(lo + blk, n) - lo)).astype(np.int64)
         z = rng.standard_normal((len(res), Hs, ds))
         along = np.sum(z * qhat[b][None], axis=-1)
         perp = z - along[..., None] * qhat[b][None]

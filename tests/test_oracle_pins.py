@@ -243,19 +243,22 @@ def test_score_tokens_closed_form(golden_dir):
         np.testing.assert_array_equal(s, expected)
 
 
+@pytest.mark.parametrize("blk", [64, 16])
 @pytest.mark.parametrize("kfmt", ["bf16", "int4", "mxfp4", "int8", "mxfp8"])
-def test_score_tokens_reduces_to_pooled_scores(kfmt):
+def test_score_tokens_reduces_to_pooled_scores(kfmt, blk):
     """With one token per block the per-token selector is the pinned block
     score with every token as its own block; a numpy maximum over groups of
-    tokens then gives the per-block value, with hidden tokens left out."""
+    tokens then gives the per-block value, with hidden tokens left out.  Both
+    the 64-token KV block and the paper's 16-token selector block
+    (Appendix A)."""
     rng = np.random.default_rng(23)
-    n_seq, rps, Hs, ds, L, blk = 2, 2, 4, 128, 320, 64
+    n_seq, rps, Hs, ds, L = 2, 2, 4, 128, 320
     q = bf16_bits(rng.standard_normal((n_seq * rps, Hs, ds)).astype(np.float32))
     w = rng.uniform(0, 1, (n_seq * rps, Hs)).astype(np.float32)
     kb = bf16_bits(rng.standard_normal((n_seq, L, Hs, ds)).astype(np.float32))
     k, sc = {"bf16": lambda b: (b, None), **synth.QUANTIZERS}[kfmt](kb)
     per_tok = oracle.selector_score(q, w, k, sc, kfmt, rows_per_seq=rps, nblk=L, h_s=Hs, d_s=ds)
-    seq_len = np.array([L, 200, 129, 1], np.int32)
+    seq_len = np.array([L, 200, 129, 1] if blk == 64 else [L, 200, 17, 15], np.int32)
     s = oracle.selector_score_tokens(q, w, k, sc, kfmt, rows_per_seq=rps, seq_len=seq_len,
                                      l_cap=L, blk=blk, h_s=Hs, d_s=ds)
     for r in range(n_seq * rps):
@@ -270,6 +273,24 @@ def test_score_tokens_reduces_to_pooled_scores(kfmt):
     s_all = oracle.selector_score_tokens(q, w, k, sc, kfmt, rows_per_seq=rps, l_cap=L, blk=blk,
                                          h_s=Hs, d_s=ds)
     np.testing.assert_array_equal(s_p, s_all)
+
+
+def test_score_tokens_16_token_blocks_nest_in_64():
+    """A 64-token block's value is the largest of its four 16-token blocks'
+    values (a maximum over a union), hidden tokens and empty blocks included."""
+    rng = np.random.default_rng(27)
+    n_seq, Hs, ds, L = 3, 4, 128, 384
+    q = bf16_bits(rng.standard_normal((n_seq, Hs, ds)).astype(np.float32))
+    w = rng.uniform(0, 1, (n_seq, Hs)).astype(np.float32)
+    k = bf16_bits(rng.standard_normal((n_seq, L, Hs, ds)).astype(np.float32))
+    seq_len = np.array([L, 145, 16], np.int32)
+    s16 = oracle.selector_score_tokens(q, w, k, seq_len=seq_len, blk=16)
+    s64 = oracle.selector_score_tokens(q, w, k, seq_len=seq_len, blk=64)
+    assert s16.shape == (n_seq, L // 16) and s64.shape == (n_seq, L // 64)
+    np.testing.assert_array_equal(s64, s16.reshape(n_seq, L // 64, 4).max(axis=2))
+    # a 16-token block with no visible token does not exist
+    assert np.all(s16[1, 10:] == -np.inf) and np.isfinite(s16[1, 9])
+    assert np.all(s16[2, 1:] == -np.inf) and np.isfinite(s16[2, 0])
 
 
 def test_score_tokens_of_repeated_key_is_pooled_score():
@@ -608,6 +629,42 @@ def test_sparse_is_lse_merge_of_partition():
     om = (np.exp(l1 - lm)[..., None] * o1 + np.exp(l2 - lm)[..., None] * o2)
     np.testing.assert_allclose(l, lm, rtol=1e-12)
     np.testing.assert_allclose(o, om, rtol=1e-10, atol=1e-13)
+
+
+def test_sparse_decode_16_token_blocks():
+    """Blocks of 16 tokens (the paper's selector block, Appendix A): the
+    attended tokens are those t < seq_len with t // 16 in S, checked against
+    numpy attention over exactly that token list; ids that are negative or
+    start at or past seq_len select nothing; and taking the four quarters of
+    some 64-token blocks is the 64-token result on those blocks."""
+    rng = np.random.default_rng(43)
+    B, Hq, Hkv, d, L = 2, 8, 2, 128, 512
+    q, k, v = _rand_decode(rng, B, Hq, Hkv, d, L)
+    scale = 1 / math.sqrt(d)
+    seq_len = np.array([512, 203], np.int32)
+    idx = np.array([[0, 3, 7, 17, 31, -1],      # 31 is the last block of sequence 0
+                    [1, 12, 13, -5, 29, 30]], np.int32)   # 12: tokens 192..202 only
+    cnt = np.array([5, 6], np.int32)
+    out, lse = oracle.sparse_decode(q, k, v, seq_len, idx, cnt, scale, blk=16)
+    G = Hq // Hkv
+    for b in range(B):
+        S = {int(j) for j in idx[b, :cnt[b]] if j >= 0}
+        toks = [t for t in range(int(seq_len[b])) if t // 16 in S]
+        for h in range(Hq):
+            o, l = _numpy_attention(_f(q[b, h]), _f(k[b, h // G, toks]), _f(v[b, h // G, toks]),
+                                    scale)
+            np.testing.assert_allclose(out[b, h], o, rtol=1e-10, atol=1e-13)
+            assert abs(lse[b, h] - l) < 1e-10
+    S64 = np.array([[0, 2, 5, -1], [1, 3, -1, -1]], np.int32)
+    c64 = np.array([3, 2], np.int32)
+    quarters = np.array([[4 * j + u for j in row[:c] for u in range(4)] + [-1] * 4
+                         for row, c in zip(S64, c64)], dtype=object)
+    n16 = max(len(r) for r in quarters)
+    S16 = np.array([list(r) + [-1] * (n16 - len(r)) for r in quarters], np.int32)
+    o64, l64 = oracle.sparse_decode(q, k, v, seq_len, S64, c64, scale)
+    o16, l16 = oracle.sparse_decode(q, k, v, seq_len, S16, 4 * c64, scale, blk=16)
+    np.testing.assert_array_equal(o16, o64)
+    np.testing.assert_array_equal(l16, l64)
 
 
 def test_gqa_head_mapping():
