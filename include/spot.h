@@ -10,7 +10,8 @@
  * as the block-sparse causal prefill over query blocks.
  * spot_selector_score_tokens replaces the first call when the selector cache
  * holds one key per token (block value = maximum of per-token scores,
- * Section 2.3), and spot_selector_score_q when the selector queries are
+ * Section 2.3; spot_selector_score_tokens_blk and spot_sparse_decode_blk take
+ * the paper's 16-token selector block), and spot_selector_score_q when the selector queries are
  * stored in an MX format.  Before them, spot_selector_project produces the step's
  * selector query, weights and new cache key from the hidden state, and
  * spot_selector_pool refreshes the pooled key of the block it landed in.
@@ -283,6 +284,32 @@ spot_status spot_selector_score_tokens(const void *q_sel, const float *w, const 
                                        const int32_t *seq_len, float *scores, void *stream);
 
 /*
+ * spot_selector_score_tokens_blk -- the per-token selector with blocks of
+ * blk tokens: the paper's selector block of 16 tokens (Appendix A,
+ * hyper-parameter table: block size 16) or the 64-token KV block.
+ *
+ * Section 2.3 as for spot_selector_score_tokens, with blocks of blk tokens:
+ *     scores[r, b] = max_{blk*b <= t < min(blk*b + blk, seq_len[r])} (token score of t)
+ * and -inf for a block with no visible token; nblk = l_cap / blk, and
+ * spot_select_blocks takes the result with n_valid[r] = ceil(seq_len[r] /
+ * blk).  Arguments, layouts and errors as for spot_selector_score_tokens (l_cap
+ * a multiple of 64 in both cases), plus
+ *
+ *  blk      16 or 64 (spot_selector_score_tokens is blk = 64); anything else
+ *           is SPOT_ERR_UNSUPPORTED
+ *  scores   device, float [rows, l_cap / blk] (output)
+ *
+ * The key stream is the same as with 64-token blocks; each 16-token block's
+ * maximum is taken over the same per-token scores, so the 64-token value of
+ * a block is the largest of its four 16-token values, bit for bit.
+ */
+spot_status spot_selector_score_tokens_blk(const void *q_sel, const float *w, const void *k_tok,
+                                           const void *k_scale, int kfmt, int n_seq,
+                                           int rows_per_seq, int l_cap, int blk, int h_s,
+                                           int d_s, const int32_t *seq_len, float *scores,
+                                           void *stream);
+
+/*
  * spot_select_blocks -- dual top-p / static top-K block selection.
  *
  * Section 2.3 (Eqs. select-topk, select-nucleus, select-topp).  Per row r,
@@ -345,8 +372,11 @@ size_t spot_decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_
  *           spot_decode_workspace_bytes(batch, h_q, h_kv, d, k_max) bytes,
  *           16-byte aligned.  It must be zero-filled before its first use;
  *           every call leaves it ready for the next one (its completion
- *           counters return to zero).  Calls that may overlap in time need
- *           separate workspaces.
+ *           counters return to zero).  Where the counters lie depends on
+ *           batch, h_q, h_kv and k_max (not on the block size of
+ *           spot_sparse_decode_blk), so a workspace reused with other
+ *           sizes must be zero-filled again first.  Calls that may overlap
+ *           in time need separate workspaces.
  *
  * Supported: d == 128, h_q / h_kv in {1, 2, 4, 8}.
  */
@@ -355,6 +385,31 @@ spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
                                int k_max, int batch, int h_q, int h_kv, int d, int l_cap,
                                float sm_scale, void *out, float *lse, void *ws, size_t ws_bytes,
                                void *stream);
+
+/*
+ * spot_sparse_decode_blk -- spot_sparse_decode over blocks of blk tokens:
+ * the paper's 16-token selector block (Appendix A) or the 64-token KV block.
+ *
+ * Section 2 and the method figure, with T = { t < seq_len[b] : t / blk in
+ * S_b }: the layer attends to the tokens of the selected blocks of blk
+ * tokens each.  Arguments, layouts, workspace and errors as for
+ * spot_sparse_decode (which is blk = 64); idx holds ids of blk-token
+ * blocks, and entries that are negative or start at or past seq_len are
+ * skipped.
+ *
+ *  blk      16 or 64; anything else is SPOT_ERR_UNSUPPORTED
+ *  ws       at least spot_decode_workspace_bytes(batch, h_q, h_kv, d, k_max)
+ *           bytes, as for spot_sparse_decode
+ *
+ * With 16-token blocks each wave of a workgroup streams one 16-row slice of
+ * a block per step, the same 4 KiB contiguous K and V reads as with 64-token
+ * blocks, so the HBM stream is unchanged.
+ */
+spot_status spot_sparse_decode_blk(const void *q, const void *k, const void *v,
+                                   const int32_t *seq_len, const int32_t *idx,
+                                   const int32_t *count, int k_max, int blk, int batch, int h_q,
+                                   int h_kv, int d, int l_cap, float sm_scale, void *out,
+                                   float *lse, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * spot_decode_step -- one decode step of the whole method for every sequence:

@@ -133,14 +133,14 @@ spot_status spot_selector_score_q(const void* q_sel, const void* q_scale, int qf
                                           static_cast<hipStream_t>(stream)));
 }
 
-spot_status spot_selector_score_tokens(const void* q_sel, const float* w, const void* k_tok,
-                                       const void* k_scale, int kfmt, int n_seq,
-                                       int rows_per_seq, int l_cap, int h_s, int d_s,
-                                       const int32_t* seq_len, float* scores, void* stream) {
+spot_status spot_selector_score_tokens_blk(const void* q_sel, const float* w, const void* k_tok,
+                                           const void* k_scale, int kfmt, int n_seq,
+                                           int rows_per_seq, int l_cap, int blk, int h_s, int d_s,
+                                           const int32_t* seq_len, float* scores, void* stream) {
   if (!q_sel || !w || !k_tok || !scores) return SPOT_ERR_NULL;
   if (n_seq < 0 || rows_per_seq < 1 || l_cap < 0 || l_cap % kBlk || h_s < 1 || d_s < 1)
     return SPOT_ERR_SHAPE;
-  if (!valid_kfmt(kfmt)) return SPOT_ERR_UNSUPPORTED;
+  if (!valid_kfmt(kfmt) || (blk != 16 && blk != kBlk)) return SPOT_ERR_UNSUPPORTED;
   if (kfmt != SPOT_KFMT_BF16 && !k_scale) return SPOT_ERR_NULL;
   if (h_s * d_s != 512 || (d_s != 64 && d_s != 128)) return SPOT_ERR_UNSUPPORTED;
   // Launch size: at most one workgroup per (row, block), padded to 8 blocks.
@@ -148,8 +148,16 @@ spot_status spot_selector_score_tokens(const void* q_sel, const float* w, const 
     return SPOT_ERR_SHAPE;
   if (n_seq == 0 || l_cap == 0) return SPOT_OK;
   return from_hip(launch_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq,
-                                               rows_per_seq, l_cap, d_s, seq_len, scores,
+                                               rows_per_seq, l_cap, blk, d_s, seq_len, scores,
                                                static_cast<hipStream_t>(stream)));
+}
+
+spot_status spot_selector_score_tokens(const void* q_sel, const float* w, const void* k_tok,
+                                       const void* k_scale, int kfmt, int n_seq,
+                                       int rows_per_seq, int l_cap, int h_s, int d_s,
+                                       const int32_t* seq_len, float* scores, void* stream) {
+  return spot_selector_score_tokens_blk(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq,
+                                        l_cap, kBlk, h_s, d_s, seq_len, scores, stream);
 }
 
 spot_status spot_select_blocks(const float* scores, int rows, int nblk, const int32_t* n_valid,
@@ -185,21 +193,31 @@ static spot_status check_decode(const void* q, const void* k, const void* v,
   return SPOT_OK;
 }
 
+spot_status spot_sparse_decode_blk(const void* q, const void* k, const void* v,
+                                   const int32_t* seq_len, const int32_t* idx,
+                                   const int32_t* count, int k_max, int blk, int batch, int h_q,
+                                   int h_kv, int d, int l_cap, float sm_scale, void* out,
+                                   float* lse, void* ws, size_t ws_bytes, void* stream) {
+  spot_status st = check_decode(q, k, v, seq_len, out, batch, h_q, h_kv, d, l_cap);
+  if (st != SPOT_OK) return st;
+  if (!idx || !count) return SPOT_ERR_NULL;
+  if (k_max < 1) return SPOT_ERR_SHAPE;
+  if (blk != 16 && blk != kBlk) return SPOT_ERR_UNSUPPORTED;
+  if (batch == 0) return SPOT_OK;
+  if (!ws || ws_bytes < decode_workspace_bytes(batch, h_q, h_kv, d, k_max) || misaligned(ws))
+    return SPOT_ERR_WORKSPACE;
+  return from_hip(launch_decode(false, q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv,
+                                l_cap, blk, sm_scale, out, lse, ws, nullptr,
+                                static_cast<hipStream_t>(stream)));
+}
+
 spot_status spot_sparse_decode(const void* q, const void* k, const void* v,
                                const int32_t* seq_len, const int32_t* idx, const int32_t* count,
                                int k_max, int batch, int h_q, int h_kv, int d, int l_cap,
                                float sm_scale, void* out, float* lse, void* ws, size_t ws_bytes,
                                void* stream) {
-  spot_status st = check_decode(q, k, v, seq_len, out, batch, h_q, h_kv, d, l_cap);
-  if (st != SPOT_OK) return st;
-  if (!idx || !count) return SPOT_ERR_NULL;
-  if (k_max < 1) return SPOT_ERR_SHAPE;
-  if (batch == 0) return SPOT_OK;
-  if (!ws || ws_bytes < decode_workspace_bytes(batch, h_q, h_kv, d, k_max) || misaligned(ws))
-    return SPOT_ERR_WORKSPACE;
-  return from_hip(launch_decode(false, q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv,
-                                l_cap, sm_scale, out, lse, ws, nullptr,
-                                static_cast<hipStream_t>(stream)));
+  return spot_sparse_decode_blk(q, k, v, seq_len, idx, count, k_max, kBlk, batch, h_q, h_kv, d,
+                                l_cap, sm_scale, out, lse, ws, ws_bytes, stream);
 }
 
 spot_status spot_dense_decode(const void* q, const void* k, const void* v,
@@ -214,7 +232,7 @@ spot_status spot_dense_decode(const void* q, const void* k, const void* v,
       misaligned(ws))
     return SPOT_ERR_WORKSPACE;
   return from_hip(launch_decode(true, q, k, v, seq_len, nullptr, nullptr, 0, batch, h_q, h_kv,
-                                l_cap, sm_scale, out, lse, ws, nullptr,
+                                l_cap, kBlk, sm_scale, out, lse, ws, nullptr,
                                 static_cast<hipStream_t>(stream)));
 }
 
@@ -283,7 +301,7 @@ static spot_status decode_step_impl(const void* q_sel, const void* q_scale, int 
     const StepWs L = static_ws ? step_static_layout(batch, h_q, h_kv, k_max)
                                : step_layout(batch, h_q, h_kv, k_max, 0);
     char* base = static_cast<char*>(ws);
-    e = launch_decode(false, q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, l_cap,
+    e = launch_decode(false, q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, l_cap, kBlk,
                       sm_scale, out, lse, base + L.part, reinterpret_cast<unsigned*>(base + L.cnt),
                       s);
   }

@@ -8,8 +8,9 @@ namespace {
 using namespace dec;
 
 // Grid: n_pairs * n_slot workgroups; workgroup i serves pair i / n_slot with
-// slot i % n_slot.
-template <int G, bool DENSE>
+// slot i % n_slot.  SB: tokens per selected block (64, or 16 for the paper's
+// selector block; sparse only).
+template <int G, bool DENSE, int SB = kBlk>
 __global__ __launch_bounds__(64 * G, waves_per_eu(G)) void decode_split_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ seq_len,
@@ -18,23 +19,26 @@ __global__ __launch_bounds__(64 * G, waves_per_eu(G)) void decode_split_kernel(
     float* __restrict__ ws_ml, unsigned* __restrict__ counters, uint16_t* __restrict__ out,
     float* __restrict__ lse) {
   __shared__ DecodeSmem<G> sm;
-  decode_body<G, DENSE>(sm, ListFromIdx{idx, count, k_max}, blockIdx.x / n_slot,
-                        blockIdx.x % n_slot, q, k, v, seq_len, h_q, h_kv, l_cap, scale_log2,
-                        n_slot, ws_o, ws_ml, counters, out, lse);
+  decode_body<G, DENSE, ListFromIdx, SB>(sm, ListFromIdx{idx, count, k_max},
+                                         blockIdx.x / n_slot, blockIdx.x % n_slot, q, k, v,
+                                         seq_len, h_q, h_kv, l_cap, scale_log2, n_slot, ws_o,
+                                         ws_ml, counters, out, lse);
 }
 
 }  // namespace
 
 // Workgroups per (sequence, KV head) pair: aim for ~2048 waves over the grid
 // (8 per CU, so the whole grid is resident at once), at least one, and at
-// least two list entries per workgroup.
+// least two list entries per workgroup (with blocks of 16 tokens: two
+// virtual blocks of four entries).  Never more than with per_virtual = 1, so
+// a workspace sized for 64-token blocks fits.
 #ifndef SPOT_DECODE_WAVE_TARGET
 #define SPOT_DECODE_WAVE_TARGET 2048
 #endif
-int decode_num_splits(int batch, int h_kv, int max_blocks, int group) {
+int decode_num_splits(int batch, int h_kv, int max_blocks, int group, int per_virtual) {
   const int pairs = batch * h_kv;
   int n = (SPOT_DECODE_WAVE_TARGET / group + pairs - 1) / pairs;
-  const int by_len = (max_blocks + 1) / 2;
+  const int by_len = ((max_blocks + per_virtual - 1) / per_virtual + 1) / 2;
   if (n > by_len) n = by_len;
   const int min_for_ids = (max_blocks + kMaxIds - 1) / kMaxIds;  // entries per WG <= kMaxIds
   if (n < min_for_ids) n = min_for_ids;
@@ -45,22 +49,27 @@ int decode_num_splits(int batch, int h_kv, int max_blocks, int group) {
 // then one completion counter per (sequence, KV head) pair.
 size_t decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_blocks) {
   const int G = h_q / h_kv;
-  const size_t ns = (size_t)decode_num_splits(batch, h_kv, max_blocks, G);
+  const size_t ns = (size_t)decode_num_splits(batch, h_kv, max_blocks, G, 1);
   return (size_t)batch * h_q * ns * ((size_t)d + 2) * sizeof(float) +
          (size_t)batch * h_kv * sizeof(unsigned);
 }
 
 hipError_t launch_decode(bool dense, const void* q, const void* k, const void* v,
                          const int32_t* seq_len, const int32_t* idx, const int32_t* count,
-                         int k_max, int batch, int h_q, int h_kv, int l_cap, float sm_scale,
-                         void* out, float* lse, void* ws, unsigned* counters, hipStream_t s) {
+                         int k_max, int batch, int h_q, int h_kv, int l_cap, int blk,
+                         float sm_scale, void* out, float* lse, void* ws, unsigned* counters,
+                         hipStream_t s) {
   const int G = h_q / h_kv;
+  const bool b16 = !dense && blk == 16;
   const int max_blocks = dense ? l_cap / kBlk : k_max;
-  const int n_slot = decode_num_splits(batch, h_kv, max_blocks, G);
+  const int n_slot = decode_num_splits(batch, h_kv, max_blocks, G, b16 ? 4 : 1);
+  // The workspace layout follows the 64-token split count (never smaller),
+  // so the completion counters sit at the same place for either block size.
+  const int n_lay = decode_num_splits(batch, h_kv, max_blocks, G, 1);
   const int n_pairs = batch * h_kv;
   float* ws_o = static_cast<float*>(ws);
-  float* ws_ml = ws_o + (size_t)batch * h_q * n_slot * kD;
-  if (!counters) counters = reinterpret_cast<unsigned*>(ws_ml + (size_t)batch * h_q * n_slot * 2);
+  float* ws_ml = ws_o + (size_t)batch * h_q * n_lay * kD;
+  if (!counters) counters = reinterpret_cast<unsigned*>(ws_ml + (size_t)batch * h_q * n_lay * 2);
   auto o16 = static_cast<uint16_t*>(out);
   const float scale_log2 = sm_scale * kLog2e;
   dim3 grid(n_pairs * n_slot);
@@ -69,7 +78,11 @@ hipError_t launch_decode(bool dense, const void* q, const void* k, const void* v
   auto vv = static_cast<const uint16_t*>(v);
 #define SPOT_DECODE_CASE(GG)                                                                   \
   if (G == GG) {                                                                               \
-    if (dense)                                                                                 \
+    if (b16)                                                                                   \
+      hipLaunchKernelGGL((decode_split_kernel<GG, false, 16>), grid, dim3(64 * GG), 0, s, qq,  \
+                         kk, vv, seq_len, idx, count, k_max, h_q, h_kv, l_cap, scale_log2,     \
+                         n_slot, ws_o, ws_ml, counters, o16, lse);                             \
+    else if (dense)                                                                            \
       hipLaunchKernelGGL((decode_split_kernel<GG, true>), grid, dim3(64 * GG), 0, s, qq, kk,   \
                          vv, seq_len, idx, count, k_max, h_q, h_kv, l_cap, scale_log2,         \
                          n_slot, ws_o, ws_ml, counters, o16, lse);                             \

@@ -21,6 +21,13 @@
 //     (DPP reductions), lane-local running sums;
 //   * P.V: lane = pair of output dims, all G heads, probabilities broadcast
 //     from LDS.
+// Blocks of 16 tokens (SB = 16, the paper's selector block): the loop runs
+// over "virtual blocks" of four consecutive entries of the workgroup's list
+// (the last one padded with -1), and wave row r of virtual block n is row
+// (wT + r) % 16 of entry 4n + (wT + r) / 16 -- the same slice shapes, loads
+// and LDS layout, with a per-row token address; rows of a padding entry are
+// masked like rows past seq_len.  Each wave keeps its own softmax state, so
+// which tokens a wave sees does not matter to the merge.
 // After the block loop the G waves' (m, l, o) states are merged in LDS into
 // one partial per head; the last split to finish for a (sequence, KV head)
 // merges all splits with log-sum-exp weights, rounds to BF16 and resets the
@@ -39,6 +46,7 @@ constexpr int kKRow = kD + 8;    // padded K row in LDS (272 bytes)
 constexpr int waves_per_eu(int G) { return G >= 4 ? 2 : 1; }
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMaxIds = 512;     // max list entries per workgroup
+static_assert(kMaxIds % 4 == 0, "16-token blocks pad the list to whole virtual blocks");
 
 // ------------------------------------------------ coherent split partials
 // Split partials cross workgroups that may run on different XCDs (each with
@@ -286,8 +294,9 @@ struct HeadPartial {
 // Wave w processes token rows [w*T, (w+1)*T) of every block; the G waves'
 // states are merged in LDS at the end (two barriers).  issued(n) is called
 // by every wave right after it issued the loads of block n, so a caller can
-// act once the last block's loads are in flight.
-template <int G, class BlkOf, class Issued>
+// act once the last block's loads are in flight.  SB = 16: n_local counts
+// virtual blocks, and blk_of(e) is list entry e (-1 for padding).
+template <int G, int SB = kBlk, class BlkOf, class Issued>
 __device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
                                                      const uint32_t (&qv)[kD / 2],
                                                      const uint16_t* __restrict__ kh,
@@ -297,6 +306,7 @@ __device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
   constexpr int T = 64 / G;               // token rows per wave per block
   constexpr int NLD = T * kD * 2 / 1024;  // 16-byte loads per lane per slice
   static_assert(NLD >= 1, "slice smaller than one wave load");
+  static_assert(SB == kBlk || SB == 16, "blocks of 64 or 16 tokens");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane / T, tt = lane % T;  // this lane's (head, token row)
 
@@ -304,6 +314,34 @@ __device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
   const uint16_t* kw = kh + (size_t)wave * T * kD;
   const uint16_t* vw = vh + (size_t)wave * T * kD;
   auto& W = sm.wave[wave];
+
+  // Loads of (virtual) block n into a register stage; 16-byte chunk
+  // c = i * 64 + lane is row c / 16, column chunk c % 16 of the wave's slice.
+  auto load = [&](u32x4 (&kr)[NLD], u32x4 (&vr)[NLD], int n) {
+    if constexpr (SB == kBlk) {
+      load_slice<NLD>(kr, vr, kw, vw, blk_of(n), lane);
+    } else {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        const int wr = wave * T + 4 * i + (lane >> 4);
+        const int id = blk_of(4 * n + (wr >> 4));
+        const size_t off = (size_t)(id < 0 ? 0 : id * SB + (wr & (SB - 1))) * kD + (lane & 15) * 8;
+        kr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kh + off));
+        vr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vh + off));
+      }
+    }
+  };
+  // This lane's token (row tt of the wave's slice) in (virtual) block n; -1
+  // for a padding entry.
+  auto tok_of = [&](int n) {
+    if constexpr (SB == kBlk) {
+      return blk_of(n) * kBlk + wave * T + tt;
+    } else {
+      const int wr = wave * T + tt;
+      const int id = blk_of(4 * n + (wr >> 4));
+      return id < 0 ? -1 : id * SB + (wr & (SB - 1));
+    }
+  };
 
   // Register stages A and B hold the two blocks of the current chunk.
   u32x4 krA[NLD], vrA[NLD], krB[NLD], vrB[NLD];
@@ -322,7 +360,7 @@ __device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
     }
     wave_lds_sync();
   };
-  auto compute = [&](int blk) {
+  auto compute = [&](int tok) {
     // Q.K for (head hh, token row tt)
     const u32x4* krow = reinterpret_cast<const u32x4*>(&W.k[tt * kKRow]);
     float s = 0.f;
@@ -334,7 +372,7 @@ __device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
       s = dot2_bf16(qv[4 * i + 2], kk.z, s);
       s = dot2_bf16(qv[4 * i + 3], kk.w, s);
     }
-    const bool tok_ok = blk * kBlk + wave * T + tt < sl;
+    const bool tok_ok = (SB == kBlk || tok >= 0) && tok < sl;
     const float x = tok_ok ? s * scale_log2 : -INFINITY;
     const float m_new = fmaxf(m_run, group_max<T>(x));
     // A slice whose rows all lie past seq_len leaves the state unchanged.
@@ -386,59 +424,59 @@ __device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
   // after the loop.
   int n = 0;
   if (n_local >= 4) {
-    load_slice<NLD>(krA, vrA, kw, vw, blk_of(0), lane);
+    load(krA, vrA, 0);
     issued(0);
-    load_slice<NLD>(krB, vrB, kw, vw, blk_of(1), lane);
+    load(krB, vrB, 1);
     issued(1);
     for (; n + 3 < n_local; n += 2) {
       consume(krA, vrA);
-      load_slice<NLD>(krA, vrA, kw, vw, blk_of(n + 2), lane);
+      load(krA, vrA, n + 2);
       issued(n + 2);
-      compute(blk_of(n));
+      compute(tok_of(n));
       consume(krB, vrB);
-      load_slice<NLD>(krB, vrB, kw, vw, blk_of(n + 3), lane);
+      load(krB, vrB, n + 3);
       issued(n + 3);
-      compute(blk_of(n + 1));
+      compute(tok_of(n + 1));
     }
     // n_local - n is 2 or 3: blocks n and n + 1 are in flight
     consume(krA, vrA);
     if (n + 2 < n_local) {
-      load_slice<NLD>(krA, vrA, kw, vw, blk_of(n + 2), lane);
+      load(krA, vrA, n + 2);
       issued(n + 2);
     }
-    compute(blk_of(n));
+    compute(tok_of(n));
     consume(krB, vrB);
-    compute(blk_of(n + 1));
+    compute(tok_of(n + 1));
     if (n + 2 < n_local) {
       consume(krA, vrA);
-      compute(blk_of(n + 2));
+      compute(tok_of(n + 2));
     }
   } else {
     if (n_local > 0) {
-      load_slice<NLD>(krA, vrA, kw, vw, blk_of(0), lane);
+      load(krA, vrA, 0);
       issued(0);
     }
     if (n_local > 1) {
-      load_slice<NLD>(krB, vrB, kw, vw, blk_of(1), lane);
+      load(krB, vrB, 1);
       issued(1);
     }
     if (n_local > 2) {
       consume(krA, vrA);
-      compute(blk_of(0));
-      load_slice<NLD>(krA, vrA, kw, vw, blk_of(2), lane);
+      compute(tok_of(0));
+      load(krA, vrA, 2);
       issued(2);
       consume(krB, vrB);
-      compute(blk_of(1));
+      compute(tok_of(1));
       consume(krA, vrA);
-      compute(blk_of(2));
+      compute(tok_of(2));
     } else {
       if (n_local > 0) {
         consume(krA, vrA);
-        compute(blk_of(0));
+        compute(tok_of(0));
       }
       if (n_local > 1) {
         consume(krB, vrB);
-        compute(blk_of(1));
+        compute(tok_of(1));
       }
     }
   }
@@ -487,7 +525,7 @@ struct NoHook {
 // processes token rows [w*T, (w+1)*T) of each of those blocks.  The split
 // partials go to the workspace; the last workgroup of the pair to finish
 // (device-scope counter) merges them.  Returns true in that workgroup.
-template <int G, bool DENSE, class List>
+template <int G, bool DENSE, class List, int SB = kBlk>
 __device__ __forceinline__ bool decode_body(
     DecodeSmem<G>& sm, const List& list, int pair, int slot, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
@@ -502,21 +540,26 @@ __device__ __forceinline__ bool decode_body(
   load_query_heads<G>(qv, q, b, g, h_q);
 
   const int sl = min(seq_len[b], l_cap);
-  const int nb_valid = (sl + kBlk - 1) / kBlk;
+  const int nb_valid = (sl + SB - 1) / SB;
   // DENSE: this workgroup's contiguous run [e0, e1) of the valid blocks.
   const int bps = (nb_valid + n_slot - 1) / n_slot;
   const int e0 = slot * bps;
   const int e1 = min(e0 + bps, nb_valid);
   if (!DENSE && wave == 0) {
-    const int n = list(sm.ids, b, g, slot, n_slot, nb_valid);
+    int n = list(sm.ids, b, g, slot, n_slot, nb_valid);
+    if constexpr (SB != kBlk) {
+      // pad the last virtual block of four entries (kMaxIds is a multiple of 4)
+      if (lane < 3 && n + lane < ((n + 3) & ~3)) sm.ids[n + lane] = -1;
+      n = (n + 3) / 4;
+    }
     if (lane == 0) sm.n_local = n;
   }
   __syncthreads();
   const int n_local = DENSE ? max(e1 - e0, 0) : sm.n_local;
   const size_t head_base = ((size_t)b * h_kv + g) * (size_t)l_cap * kD;
   auto blk_of = [&](int n) { return DENSE ? e0 + n : sm.ids[n]; };
-  const HeadPartial hp = attend_blocks<G>(sm, qv, k + head_base, v + head_base, sl, n_local,
-                                          blk_of, scale_log2, NoHook{});
+  const HeadPartial hp = attend_blocks<G, SB>(sm, qv, k + head_base, v + head_base, sl,
+                                              n_local, blk_of, scale_log2, NoHook{});
   {
     const int h = wave;
     const size_t ps = ((size_t)b * h_q + g * G + h) * n_slot + slot;

@@ -24,6 +24,16 @@
 // Token loads past the last visible token re-read that token (in bounds, in
 // cache); a duplicate of a visible token cannot change a maximum, so ragged
 // blocks need no masking.
+//
+// Blocks of 16 tokens (SB = 16, the paper's selector block, Appendix A): the
+// kernels walk the same 64-token spans and keep one maximum per 16-token
+// block instead of one per span.  The folds above leave each lane with the
+// scores of tokens from one 16-token block, so a block's value is the
+// maximum over the lanes that hold its tokens (every copy of a score
+// included, as in the 64-token maximum, so that both block sizes pick the
+// largest of the same values); a 16-token block whose first token is not
+// visible gets -inf (it may have been handed duplicates of an earlier
+// block's last token).
 #include "score_core.h"
 
 namespace spot {
@@ -87,6 +97,31 @@ __device__ __forceinline__ float rows_sum_max(const float (&y)[G], int lane) {
   }
 }
 
+__device__ __forceinline__ float row_max16(float v) {
+  v = fmaxf(v, dpp_f<kDppQuadXor1>(v));
+  v = fmaxf(v, dpp_f<kDppQuadXor2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  return fmaxf(v, dpp_f<kDppMirror>(v));
+}
+
+// Per-16-token-block maxima of a wave's G groups of 8 tokens after the head
+// sums.  G = 4 (32 tokens): rows_sum_max leaves lane l with group
+// 2 bit4(l) + bit5(l), so 16-token block bit4(l) of the wave; G = 8 (64
+// tokens): it leaves the larger of groups 4 bit4 + 2 bit5 + {0, 1}, i.e.
+// 16-token block 2 bit4 + bit5, the same for every lane of a 16-lane row.
+// Returns that block's maximum in every lane.
+template <int G>
+__device__ __forceinline__ float sub16_max(const float (&y)[G], int lane) {
+  float c = row_max16(rows_sum_max<G>(y, lane));
+  if constexpr (G == 4) c = fmaxf(c, __shfl_xor(c, 32, 64));
+  return c;
+}
+// Which of the wave's 16-token blocks lane l holds after sub16_max.
+template <int G>
+__device__ __forceinline__ int sub16_of_lane(int lane) {
+  return G == 4 ? (lane >> 4) & 1 : 2 * ((lane >> 4) & 1) + (lane >> 5);
+}
+
 // TPW tokens per wavefront (16, 32 or 64): a block is shared by 64 / TPW
 // waves of one workgroup, whose partial maxima meet in LDS.
 //
@@ -95,7 +130,7 @@ __device__ __forceinline__ float rows_sum_max(const float (&y)[G], int lane) {
 // ids go round-robin over the 8 XCDs, so the rows that read the same keys
 // are given ids 8 apart -- the same XCD, hence the same L2 -- and
 // consecutive units alternate XCDs.
-template <int KFMT, int LPH, int TPW>
+template <int KFMT, int LPH, int TPW, int SB>
 __global__ __launch_bounds__(256) void score_tokens_kernel(
     const uint16_t* __restrict__ q_sel, const float* __restrict__ w,
     const uint8_t* __restrict__ k_tok, const uint8_t* __restrict__ k_scale, int n_seq,
@@ -105,6 +140,8 @@ __global__ __launch_bounds__(256) void score_tokens_kernel(
   constexpr int G = TPW / 8;                 // groups of 8 tokens per wave
   constexpr int WPB = 64 / TPW;              // waves per block
   constexpr int BPW = kTokWavesPerWG / WPB;  // blocks per workgroup
+  static_assert(SB == 64 || (SB == 16 && (G == 4 || G == 8)),
+                "16-token blocks need 32 or 64 tokens per wave");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gsize = 8 * rows_per_seq;
   const int id = blockIdx.x;
@@ -112,7 +149,7 @@ __global__ __launch_bounds__(256) void score_tokens_kernel(
   const int rr = (id % gsize) >> 3;
   if (unit >= n_seq * runs) return;
   const int seq = unit / runs;
-  const int j = (unit % runs) * BPW + wave / WPB;
+  const int j = (unit % runs) * BPW + wave / WPB;   // 64-token span
   const int row = seq * rows_per_seq + rr;
   int len = seq_len ? seq_len[row] : l_cap;
   len = len < 0 ? 0 : (len > l_cap ? l_cap : len);
@@ -168,7 +205,18 @@ __global__ __launch_bounds__(256) void score_tokens_kernel(
       }
       y[g] = d;
     }
-    m = wave_max(rows_sum_max<G>(y, lane));
+    if constexpr (SB == 64)
+      m = wave_max(rows_sum_max<G>(y, lane));
+    else
+      m = sub16_max<G>(y, lane);
+  }
+  if constexpr (SB == 16) {
+    // 16-token block J = the wave's first one + sub16_of_lane; one writer
+    // lane per block (lanes 0, 16 (, 32, 48)).
+    const int J = t0 / 16 + sub16_of_lane<G>(lane);
+    if ((lane & 15) == 0 && (G == 8 || lane < 32) && j < nblk)
+      scores[(size_t)row * nblk * 4 + J] = J * 16 < len ? m : -INFINITY;
+    return;
   }
   float* dst = scores + (size_t)row * nblk + j;
   if constexpr (WPB == 1) {
@@ -195,7 +243,7 @@ __global__ __launch_bounds__(256) void score_tokens_kernel(
 // rotations (rotating by 8, 4 (and 2) visits one lane of every head), which
 // leaves every lane of the row with its token's score.  Tokens past the last
 // visible one re-read it, as in score_tokens_kernel.
-template <int KFMT, int LG, int TPW>
+template <int KFMT, int LG, int TPW, int SB>
 __global__ __launch_bounds__(256) void score_tokens4_kernel(
     const uint16_t* __restrict__ q_sel, const float* __restrict__ w,
     const uint8_t* __restrict__ k_tok, const uint8_t* __restrict__ k_scale, int n_seq,
@@ -218,8 +266,10 @@ __global__ __launch_bounds__(256) void score_tokens4_kernel(
   int len = seq_len ? seq_len[row] : l_cap;
   len = len < 0 ? 0 : (len > l_cap ? l_cap : len);
   const int t0 = j * 64 + (wave % WPB) * TPW;
+  static_assert(SB == 64 || (SB == 16 && TPW == 64), "16-token blocks: one wave per span");
 
   float m = -INFINITY;
+  float ms[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};   // SB == 16
   if (j < nblk && t0 < len) {
     const int tlim = min(j * 64 + 64, len) - 1;
     const size_t base = (size_t)seq * l_cap;
@@ -278,9 +328,30 @@ __global__ __launch_bounds__(256) void score_tokens4_kernel(
       d += dpp_f<0x128>(d);                  // row_ror:8
       d += dpp_f<0x124>(d);                  // row_ror:4
       if constexpr (LG == 2) d += dpp_f<0x122>(d);   // row_ror:2
-      m = fmaxf(m, d);
+      if constexpr (SB == 64)
+        m = fmaxf(m, d);
+      else
+        ms[u >> 2] = fmaxf(ms[u >> 2], d);   // loads 4s .. 4s+3: tokens 16s .. 16s+15
     }
-    m = wave_max(m);
+    if constexpr (SB == 64) {
+      m = wave_max(m);
+    } else {
+      // Row tq holds token slot tq's scores, but its lanes may hold them
+      // rounded differently (the head sums may contract into fused
+      // multiply-adds that start from a different lane's term), so each
+      // block's maximum is taken over the whole wave, as wave_max does for
+      // 64-token blocks: both then pick the largest of the same values.
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4) ms[s4] = wave_max(ms[s4]);
+    }
+  }
+  if constexpr (SB == 16) {
+    if (lane < 4 && j < nblk) {
+      const float v = lane == 0 ? ms[0] : lane == 1 ? ms[1] : lane == 2 ? ms[2] : ms[3];
+      const int J = 4 * j + lane;
+      scores[(size_t)row * nblk * 4 + J] = J * 16 < len ? v : -INFINITY;
+    }
+    return;
   }
   float* dst = scores + (size_t)row * nblk + j;
   if constexpr (WPB == 1) {
@@ -310,7 +381,8 @@ inline dim3 tok_grid(int n_seq, int runs, int rows_per_seq) {
   return dim3((unsigned)(((units + 7) / 8) * 8 * rows_per_seq));
 }
 
-template <int KFMT>
+// nblk counts 64-token spans; with SB = 16 a row has 4 nblk output values.
+template <int KFMT, int SB>
 hipError_t launch_tokens_fmt(int lph, hipStream_t s, const uint16_t* q, const float* w,
                              const uint8_t* k, const uint8_t* ks, int n_seq, int rows_per_seq,
                              int l_cap, int nblk, const int32_t* seq_len, float* out) {
@@ -319,53 +391,64 @@ hipError_t launch_tokens_fmt(int lph, hipStream_t s, const uint16_t* q, const fl
     const int runs = tok_runs<kTok4TPW>(nblk);
     const dim3 grid = tok_grid(n_seq, runs, rows_per_seq);
     if (lph == 8)
-      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 2, kTok4TPW>), grid, dim3(256), 0, s, q, w,
-                         k, ks, n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 2, kTok4TPW, SB>), grid, dim3(256), 0, s, q,
+                         w, k, ks, n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
     else
-      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 4, kTok4TPW>), grid, dim3(256), 0, s, q, w,
-                         k, ks, n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+      hipLaunchKernelGGL((score_tokens4_kernel<KFMT, 4, kTok4TPW, SB>), grid, dim3(256), 0, s, q,
+                         w, k, ks, n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
     return hipGetLastError();
   }
   constexpr int TPW = KFMT == SPOT_KFMT_BF16 ? kTokTPW : kTok8TPW;
   const int runs = tok_runs<TPW>(nblk);
   const dim3 grid = tok_grid(n_seq, runs, rows_per_seq);
   if (lph == 8)
-    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 8, TPW>), grid, dim3(256), 0, s, q, w, k, ks,
-                       n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 8, TPW, SB>), grid, dim3(256), 0, s, q, w, k,
+                       ks, n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
   else
-    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 16, TPW>), grid, dim3(256), 0, s, q, w, k, ks,
-                       n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
+    hipLaunchKernelGGL((score_tokens_kernel<KFMT, 16, TPW, SB>), grid, dim3(256), 0, s, q, w, k,
+                       ks, n_seq, rows_per_seq, l_cap, nblk, runs, seq_len, out);
   return hipGetLastError();
+}
+
+template <int SB>
+hipError_t launch_tokens_sb(int kfmt, int lph, hipStream_t s, const uint16_t* q, const float* w,
+                            const uint8_t* k, const uint8_t* ks, int n_seq, int rows_per_seq,
+                            int l_cap, int nblk, const int32_t* seq_len, float* out) {
+  switch (kfmt) {
+    case SPOT_KFMT_BF16:
+      return launch_tokens_fmt<SPOT_KFMT_BF16, SB>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
+                                                   l_cap, nblk, seq_len, out);
+    case SPOT_KFMT_INT4_G32:
+      return launch_tokens_fmt<SPOT_KFMT_INT4_G32, SB>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
+                                                       l_cap, nblk, seq_len, out);
+    case SPOT_KFMT_INT8_G32:
+      return launch_tokens_fmt<SPOT_KFMT_INT8_G32, SB>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
+                                                       l_cap, nblk, seq_len, out);
+    case SPOT_KFMT_MXFP8_G32:
+      return launch_tokens_fmt<SPOT_KFMT_MXFP8_G32, SB>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
+                                                        l_cap, nblk, seq_len, out);
+    default:
+      return launch_tokens_fmt<SPOT_KFMT_MXFP4_G32, SB>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
+                                                        l_cap, nblk, seq_len, out);
+  }
 }
 
 }  // namespace
 
 hipError_t launch_selector_score_tokens(const void* q_sel, const float* w, const void* k_tok,
                                         const void* k_scale, int kfmt, int n_seq,
-                                        int rows_per_seq, int l_cap, int d_s,
+                                        int rows_per_seq, int l_cap, int blk, int d_s,
                                         const int32_t* seq_len, float* scores, hipStream_t s) {
-  const int nblk = l_cap / kBlk;
+  const int nblk = l_cap / kBlk;   // 64-token spans
   const int lph = d_s / 8;
   auto q = static_cast<const uint16_t*>(q_sel);
   auto k = static_cast<const uint8_t*>(k_tok);
   auto ks = static_cast<const uint8_t*>(k_scale);
-  switch (kfmt) {
-    case SPOT_KFMT_BF16:
-      return launch_tokens_fmt<SPOT_KFMT_BF16>(lph, s, q, w, k, ks, n_seq, rows_per_seq, l_cap,
-                                               nblk, seq_len, scores);
-    case SPOT_KFMT_INT4_G32:
-      return launch_tokens_fmt<SPOT_KFMT_INT4_G32>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
-                                                   l_cap, nblk, seq_len, scores);
-    case SPOT_KFMT_INT8_G32:
-      return launch_tokens_fmt<SPOT_KFMT_INT8_G32>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
-                                                   l_cap, nblk, seq_len, scores);
-    case SPOT_KFMT_MXFP8_G32:
-      return launch_tokens_fmt<SPOT_KFMT_MXFP8_G32>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
-                                                    l_cap, nblk, seq_len, scores);
-    default:
-      return launch_tokens_fmt<SPOT_KFMT_MXFP4_G32>(lph, s, q, w, k, ks, n_seq, rows_per_seq,
-                                                    l_cap, nblk, seq_len, scores);
-  }
+  if (blk == 16)
+    return launch_tokens_sb<16>(kfmt, lph, s, q, w, k, ks, n_seq, rows_per_seq, l_cap, nblk,
+                                seq_len, scores);
+  return launch_tokens_sb<64>(kfmt, lph, s, q, w, k, ks, n_seq, rows_per_seq, l_cap, nblk,
+                              seq_len, scores);
 }
 
 }  // namespace spot

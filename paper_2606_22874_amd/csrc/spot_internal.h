@@ -138,7 +138,7 @@ hipError_t launch_selector_score_q(const void* q_sel, const void* q_scale, int q
 
 hipError_t launch_selector_score_tokens(const void* q_sel, const float* w, const void* k_tok,
                                         const void* k_scale, int kfmt, int n_seq,
-                                        int rows_per_seq, int l_cap, int d_s,
+                                        int rows_per_seq, int l_cap, int blk, int d_s,
                                         const int32_t* seq_len, float* scores, hipStream_t s);
 
 hipError_t launch_selector_project(const void* h, const void* w_q, const void* w_k,
@@ -155,7 +155,8 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
                                 float top_p, int k_max, int k_min, int n_sink, int n_recent,
                                 int32_t* idx, int32_t* count, float* nuc_mass, hipStream_t s);
 
-int decode_num_splits(int batch, int h_kv, int max_blocks, int group);
+// per_virtual: list entries per loop step (1; 4 for 16-token blocks)
+int decode_num_splits(int batch, int h_kv, int max_blocks, int group, int per_virtual = 1);
 size_t decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_blocks);
 
 // Byte offsets in a decode step's workspace: the control region [0, ctrl)
@@ -189,8 +190,9 @@ hipError_t launch_decode_step(const void* q_sel, const void* q_scale, int qfmt, 
 // counters, as decode_workspace_bytes lays them out.
 hipError_t launch_decode(bool dense, const void* q, const void* k, const void* v,
                          const int32_t* seq_len, const int32_t* idx, const int32_t* count,
-                         int k_max, int batch, int h_q, int h_kv, int l_cap, float sm_scale,
-                         void* out, float* lse, void* ws, unsigned* counters, hipStream_t s);
+                         int k_max, int batch, int h_q, int h_kv, int l_cap, int blk,
+                         float sm_scale, void* out, float* lse, void* ws, unsigned* counters,
+                         hipStream_t s);
 
 hipError_t launch_sparse_prefill(const void* q, const void* k, const void* v, int L,
                                  const int32_t* idx, const int32_t* count, int k_max,

@@ -29,10 +29,12 @@ KFMT = {"bf16": 0, "int4": 1, "mxfp4": 2, "int8": 3, "mxfp8": 4}
 BLK = 64
 
 SYMBOLS = ["spot_status_str", "spot_version", "spot_selector_score",
-           "spot_selector_score_q", "spot_selector_score_tokens", "spot_selector_project",
+           "spot_selector_score_q", "spot_selector_score_tokens",
+           "spot_selector_score_tokens_blk", "spot_selector_project",
            "spot_selector_project_pooled", "spot_selector_pool",
            "spot_select_blocks",
-           "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_dense_decode",
+           "spot_decode_workspace_bytes", "spot_sparse_decode", "spot_sparse_decode_blk",
+           "spot_dense_decode",
            "spot_sparse_prefill", "spot_decode_step_workspace_bytes", "spot_decode_step",
            "spot_decode_step_q", "spot_decode_step_static", "spot_decode_step_status",
            "spot_test_force_expiry",
@@ -68,6 +70,7 @@ def load(path: Optional[str] = None):
         L.spot_version.restype = ctypes.c_char_p
         L.spot_selector_score.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P, P]
         L.spot_selector_score_tokens.argtypes = [P, P, P, P, I, I, I, I, I, I, P, P, P]
+        L.spot_selector_score_tokens_blk.argtypes = [P, P, P, P, I, I, I, I, I, I, I, P, P, P]
         L.spot_selector_score_q.argtypes = [P, P, I, P, P, P, I, I, I, I, I, I, P, P, P]
         L.spot_selector_project.argtypes = [P, P, P, P, P, I, I, I, I, I, F, P, P, P, I, I, P]
         L.spot_selector_pool.argtypes = [P, P, I, I, I, I, P, P, I, P]
@@ -77,6 +80,8 @@ def load(path: Optional[str] = None):
         L.spot_decode_workspace_bytes.argtypes = [I, I, I, I, I]
         L.spot_decode_workspace_bytes.restype = Z
         L.spot_sparse_decode.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, P, P, P, Z, P]
+        L.spot_sparse_decode_blk.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, I, F, P, P, P,
+                                             Z, P]
         L.spot_dense_decode.argtypes = [P, P, P, P, I, I, I, I, I, F, P, P, P, Z, P]
         L.spot_sparse_prefill.argtypes = [P, P, P, I, P, P, I, I, I, I, I, F, P, P, P]
         L.spot_decode_step_workspace_bytes.argtypes = [I, I, I, I, I]
@@ -94,8 +99,10 @@ def load(path: Optional[str] = None):
         L.spot_probe_stream_read.restype = ctypes.c_int32
         L.spot_probe_sink_words.restype = I
         for name in ("spot_selector_score", "spot_selector_score_q", "spot_selector_score_tokens",
+                     "spot_selector_score_tokens_blk",
                      "spot_selector_project", "spot_selector_project_pooled",
                      "spot_selector_pool", "spot_select_blocks", "spot_sparse_decode",
+                     "spot_sparse_decode_blk",
                      "spot_dense_decode", "spot_sparse_prefill", "spot_decode_step",
                      "spot_decode_step_q", "spot_decode_step_static", "spot_decode_step_status"):
             getattr(L, name).restype = ctypes.c_int32
@@ -189,8 +196,8 @@ def spot_selector_score_q(q_sel, q_scale, qfmt, w, k_sel, k_scale, kfmt, n_seq, 
         rows_per_seq, nblk, h_s, d_s, _ptr(n_valid), _ptr(scores), _stream(stream)))
 
 
-def spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, h_s,
-                               d_s, seq_len, scores, stream=None):
+def _tokens_args(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, blk, h_s, d_s,
+                 seq_len, scores):
     rows = n_seq * rows_per_seq
     f = KFMT[kfmt] if isinstance(kfmt, str) else int(kfmt)
     _dev(q_sel, "q_sel", BF16, rows * h_s * d_s)
@@ -198,10 +205,26 @@ def spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_s
     _sel_cache(k_tok, k_scale, f, n_seq * l_cap, h_s, d_s, "k_tok")
     if seq_len is not None:
         _dev(seq_len, "seq_len", I32, rows)
-    _dev(scores, "scores", F32, rows * (l_cap // 64))
+    _dev(scores, "scores", F32, rows * (l_cap // blk))
+    return f
+
+
+def spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, h_s,
+                               d_s, seq_len, scores, stream=None):
+    f = _tokens_args(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, 64, h_s, d_s,
+                     seq_len, scores)
     _check("spot_selector_score_tokens", load().spot_selector_score_tokens(
         _ptr(q_sel), _ptr(w), _ptr(k_tok), _ptr(k_scale), f, n_seq, rows_per_seq, l_cap, h_s,
         d_s, _ptr(seq_len), _ptr(scores), _stream(stream)))
+
+
+def spot_selector_score_tokens_blk(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap,
+                                   blk, h_s, d_s, seq_len, scores, stream=None):
+    f = _tokens_args(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, blk, h_s, d_s,
+                     seq_len, scores)
+    _check("spot_selector_score_tokens_blk", load().spot_selector_score_tokens_blk(
+        _ptr(q_sel), _ptr(w), _ptr(k_tok), _ptr(k_scale), f, n_seq, rows_per_seq, l_cap, blk,
+        h_s, d_s, _ptr(seq_len), _ptr(scores), _stream(stream)))
 
 
 def spot_selector_project(h, w_q, w_k, w_w, pos, rows, d_model, h_s, d_s, rope_dim, rope_base,
@@ -277,6 +300,23 @@ def spot_decode_workspace_bytes(batch, h_q, h_kv, d, max_blocks) -> int:
 
 def spot_sparse_decode(q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, d, l_cap,
                        sm_scale, out, lse, ws, stream=None):
+    _decode_args(q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, d, l_cap, out, lse, ws)
+    _check("spot_sparse_decode", load().spot_sparse_decode(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(seq_len), _ptr(idx), _ptr(count), k_max, batch, h_q,
+        h_kv, d, l_cap, float(sm_scale), _ptr(out), _ptr(lse), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def spot_sparse_decode_blk(q, k, v, seq_len, idx, count, k_max, blk, batch, h_q, h_kv, d, l_cap,
+                           sm_scale, out, lse, ws, stream=None):
+    _decode_args(q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, d, l_cap, out, lse, ws)
+    _check("spot_sparse_decode_blk", load().spot_sparse_decode_blk(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(seq_len), _ptr(idx), _ptr(count), k_max, blk, batch,
+        h_q, h_kv, d, l_cap, float(sm_scale), _ptr(out), _ptr(lse), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def _decode_args(q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, d, l_cap, out, lse, ws):
     _dev(q, "q", BF16, batch * h_q * d)
     _dev(k, "k", BF16, batch * h_kv * l_cap * d)
     _dev(v, "v", BF16, batch * h_kv * l_cap * d)
@@ -287,10 +327,6 @@ def spot_sparse_decode(q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, d,
     if lse is not None:
         _dev(lse, "lse", F32, batch * h_q)
     _dev(ws, "ws", None)
-    _check("spot_sparse_decode", load().spot_sparse_decode(
-        _ptr(q), _ptr(k), _ptr(v), _ptr(seq_len), _ptr(idx), _ptr(count), k_max, batch, h_q,
-        h_kv, d, l_cap, float(sm_scale), _ptr(out), _ptr(lse), _ptr(ws),
-        ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def spot_dense_decode(q, k, v, seq_len, batch, h_q, h_kv, d, l_cap, sm_scale, out, lse, ws,
@@ -440,8 +476,9 @@ def selector_score(q_sel, w, k_sel, k_scale=None, kfmt="bf16", rows_per_seq=1, n
 
 
 def selector_score_tokens(q_sel, w, k_tok, k_scale=None, kfmt="bf16", rows_per_seq=1,
-                          seq_len=None, l_cap=None, out=None, stream=None):
-    """Per-block maximum of per-token scores [rows, l_cap // 64] float32."""
+                          seq_len=None, l_cap=None, out=None, stream=None, blk=64):
+    """Per-block maximum of per-token scores [rows, l_cap // blk] float32
+    (blocks of 64 tokens, or 16: the paper's selector block)."""
     h_s, d_s = q_sel.shape[-2], q_sel.shape[-1]
     rows = q_sel.numel() // (h_s * d_s)
     n_seq = rows // rows_per_seq
@@ -450,9 +487,13 @@ def selector_score_tokens(q_sel, w, k_tok, k_scale=None, kfmt="bf16", rows_per_s
         per = h_s * d_s if f in (0, 3, 4) else h_s * d_s // 2
         l_cap = k_tok.numel() // (n_seq * per)
     if out is None:
-        out = torch.empty((rows, l_cap // 64), dtype=torch.float32, device=q_sel.device)
-    spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap, h_s,
-                               d_s, seq_len, out, stream)
+        out = torch.empty((rows, l_cap // blk), dtype=torch.float32, device=q_sel.device)
+    if blk == 64:
+        spot_selector_score_tokens(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq, l_cap,
+                                   h_s, d_s, seq_len, out, stream)
+    else:
+        spot_selector_score_tokens_blk(q_sel, w, k_tok, k_scale, kfmt, n_seq, rows_per_seq,
+                                       l_cap, blk, h_s, d_s, seq_len, out, stream)
     return out
 
 
@@ -477,7 +518,9 @@ def decode_workspace(batch, h_q, h_kv, d, max_blocks, device="cuda"):
 
 
 def sparse_decode(q, k, v, seq_len, idx, count, sm_scale=None, out=None, lse=None, ws=None,
-                  stream=None):
+                  stream=None, blk=64):
+    """Attention over the selected blocks of blk tokens (64, or 16: the
+    paper's selector block); returns (out [batch, h_q, d] BF16, lse)."""
     batch, h_q, d = q.shape
     _, h_kv, l_cap, _ = k.shape
     k_max = idx.shape[-1]
@@ -488,8 +531,12 @@ def sparse_decode(q, k, v, seq_len, idx, count, sm_scale=None, out=None, lse=Non
         lse = torch.empty((batch, h_q), dtype=torch.float32, device=q.device)
     if ws is None:
         ws = decode_workspace(batch, h_q, h_kv, d, k_max, q.device)
-    spot_sparse_decode(q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, d, l_cap,
-                       sm_scale, out, lse, ws, stream)
+    if blk == 64:
+        spot_sparse_decode(q, k, v, seq_len, idx, count, k_max, batch, h_q, h_kv, d, l_cap,
+                           sm_scale, out, lse, ws, stream)
+    else:
+        spot_sparse_decode_blk(q, k, v, seq_len, idx, count, k_max, blk, batch, h_q, h_kv, d,
+                               l_cap, sm_scale, out, lse, ws, stream)
     return out, lse
 
 
