@@ -574,6 +574,8 @@ def per_token_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, 
         f"step {ms * 1e3:.1f} us")
     del ktoks
     torch.cuda.empty_cache()
+    block16 = block16_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, out, lse,
+                          stream)
 
     # The scorer alone over quantized per-token caches: the first QUANT_TOKENS
     # tokens of each sequence quantized and repeated to L tokens (the encoders
@@ -624,6 +626,78 @@ def per_token_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, 
             "traffic": measured_traffic(TOKENS_PROFILE, TOKENS_SOURCES),
         },
         "quantized_scorer": fmts,
+        "block16": block16,
+    }
+
+
+def block16_leg(args, torch, spot, synth, dev, timed, wl, copies, q, seq_len, out, lse, stream):
+    """The per-token decode step with the paper's 16-token selector block
+    (Appendix A): the same 4 x 128 per-token cache and KV layer, block value =
+    maximum over 16 tokens, dual top-p / top-K over L / 16 blocks with the
+    same token budget as the 64-token workload (K_max = 512 blocks = 8192
+    tokens, 4 sink + 8 recent blocks = 64 + 128 tokens), attention over the
+    selected 16-token blocks; three launches."""
+    B, L = wl.B, wl.L
+    Hs, ds, blk = 4, 128, 16
+    rule = synth.Rule(wl.rule.top_p, 512, 0, 4, 8)
+    log("[bench] 16-token blocks: generating the per-token cache (one lead token per block)")
+    q_tok, w_tok, k_tok = synth.selector_tokens(SEED_TOKENS + 1, B, L, Hs, ds, wl.seq_len,
+                                                rule=rule, blk=blk)
+    qs = spot.to_device_bf16(q_tok, dev)
+    ws_ = torch.from_numpy(w_tok).to(dev)
+    ktoks = [spot.to_device_bf16(k_tok, dev) for _ in range(2)]
+    tok_bytes = k_tok.nbytes
+    del k_tok
+    nb = L // blk
+    nv = torch.from_numpy(((wl.seq_len + blk - 1) // blk).astype(np.int32)).to(dev)
+    scores = torch.empty((B, nb), dtype=torch.float32, device=dev)
+    idx = torch.empty((B, rule.k_max), dtype=torch.int32, device=dev)
+    cnt = torch.empty(B, dtype=torch.int32, device=dev)
+    mass = torch.empty(B, dtype=torch.float32, device=dev)
+    ws = spot.decode_workspace(B, wl.Hq, wl.Hkv, wl.d, rule.k_max, dev)
+
+    def score(c):
+        spot.spot_selector_score_tokens_blk(qs, ws_, ktoks[c % 2], None, "bf16", B, 1, L, blk,
+                                            Hs, ds, seq_len, scores, stream)
+
+    def select(c):
+        spot.spot_select_blocks(scores, B, nb, nv, rule.top_p, rule.k_max, rule.k_min,
+                                rule.n_sink, rule.n_recent, idx, cnt, mass, stream)
+
+    def attend(c):
+        k, v, _, _ = copies[c % len(copies)]
+        spot.spot_sparse_decode_blk(q, k, v, seq_len, idx, cnt, rule.k_max, blk, B, wl.Hq,
+                                    wl.Hkv, wl.d, L, wl.sm_scale, out, lse, ws, stream)
+
+    def step(c):
+        score(c)
+        select(c)
+        attend(c)
+
+    for i in range(args.warmup):
+        step(i)
+    ms = timed(step, args.steps)
+    s_ms, sel_ms, att_ms = timed(score, args.steps), timed(select, args.steps), \
+        timed(attend, args.steps)
+    counts = cnt.cpu().numpy()
+    attn_bytes = int(counts.sum()) * blk * wl.Hkv * wl.d * 4
+    log(f"[bench] 16-token blocks: step {ms * 1e3:.1f} us (score {s_ms * 1e3:.1f}, select "
+        f"{sel_ms * 1e3:.1f}, attention {att_ms * 1e3:.1f}), {counts.mean():.0f} blocks")
+    del ktoks
+    torch.cuda.empty_cache()
+    return {
+        "workload": f"decode L={L} B={B}, per-token selector cache {Hs}x{ds} BF16 "
+                    f"({tok_bytes >> 20} MiB), block of {blk} tokens = max over its tokens; "
+                    f"p={rule.top_p} K_max={rule.k_max} blocks, {rule.n_sink} sink + "
+                    f"{rule.n_recent} recent blocks",
+        "us_per_step": round(ms * 1e3, 2),
+        "steps_per_s": round(1e3 / ms, 1),
+        "stage_us": {"score": round(s_ms * 1e3, 2), "select": round(sel_ms * 1e3, 2),
+                     "attention": round(att_ms * 1e3, 2)},
+        "mean_selected_blocks": float(counts.mean()),
+        "bytes_per_step": int(tok_bytes + attn_bytes),
+        "hbm_frac": round((tok_bytes + attn_bytes) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "attention_gbs": round(attn_bytes / (att_ms * 1e-3) / 1e9, 1),
     }
 
 

@@ -3,7 +3,7 @@
 //
 // Three kernels, chosen by row length and cap (one row per workgroup):
 //  * rows of up to 512 blocks: one wavefront (select_wave_kernel);
-//  * 513 .. 4096 blocks: one 256-thread workgroup (select_wg_kernel, its body
+//  * 513 .. 8192 blocks: one 256-thread workgroup (select_wg_kernel, its body
 //    in select_core.h, shared with the fused decode step), for caps up to
 //    1024 and, when top_p >= 1 (static top-K: no survivor sort), any cap;
 //  * longer rows or larger caps: the 256-thread sort-based select_kernel.
@@ -568,7 +568,7 @@ __global__ __launch_bounds__(64) void select_wave_kernel(
 }
 
 // Workgroup selection kernel: one 256-thread workgroup per row (rows of
-// 513 .. 4096 blocks, cap <= 512).
+// 513 .. 8192 blocks, cap <= 512).
 template <int EPT, int SPL>
 __global__ __launch_bounds__(kSelWG) void select_wg_kernel(
     const float* __restrict__ scores, int nblk, const int32_t* __restrict__ n_valid,
@@ -579,8 +579,15 @@ __global__ __launch_bounds__(kSelWG) void select_wg_kernel(
   const int row = blockIdx.x;
   int nv = n_valid ? n_valid[row] : nblk;
   nv = nv < 0 ? 0 : (nv > nblk ? nblk : nv);
-  const SelRow r = select_row_core<EPT, SPL>(sm, RowScores{scores + (size_t)row * nblk}, nv,
-                                             top_p, k_max, k_min, n_sink, n_recent);
+  SelRow r;
+  if constexpr (EPT >= 16) {
+    __shared__ alignas(16) float stage[kSelWG * EPT];
+    r = select_row_core<EPT, SPL>(sm, StagedRowScores{scores + (size_t)row * nblk, stage}, nv,
+                                  top_p, k_max, k_min, n_sink, n_recent);
+  } else {
+    r = select_row_core<EPT, SPL>(sm, RowScores{scores + (size_t)row * nblk}, nv, top_p, k_max,
+                                  k_min, n_sink, n_recent);
+  }
   int total;
   const int pos = sel_positions(sm, r.fin, total);
   sel_write<EPT>(idx_out + (size_t)row * k_max, count_out + row,
@@ -603,8 +610,8 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
   // are never sorted and the survivor buffer (64 * SPL keys) does not bound
   // the cap: static top-K at any budget runs on the 512-key instantiation.
   const int spl_wg = top_p >= 1.f && spl > 8 ? 8 : spl;
-  if (nblk > 512 && nblk <= 4096 && spl_wg <= 16) {
-    const int e2 = nblk <= 1024 ? 4 : nblk <= 2048 ? 8 : 16;
+  if (nblk > 512 && nblk <= 8192 && spl_wg <= 16) {
+    const int e2 = nblk <= 1024 ? 4 : nblk <= 2048 ? 8 : nblk <= 4096 ? 16 : 32;
 #define SPOT_SELECT_WG(E, S)                                                                    \
     if (e2 == E && spl_wg == S) {                                                             \
       hipLaunchKernelGGL((select_wg_kernel<E, S>), grid, dim3(kSelWG), 0, s, scores, nblk,    \
@@ -618,6 +625,7 @@ hipError_t launch_select_blocks(const float* scores, int rows, int nblk, const i
     SPOT_SELECT_WG_E(4)
     SPOT_SELECT_WG_E(8)
     SPOT_SELECT_WG_E(16)
+    SPOT_SELECT_WG_E(32)
 #undef SPOT_SELECT_WG_E
 #undef SPOT_SELECT_WG
   }

@@ -129,6 +129,44 @@ struct RowScores {
   }
 };
 
+// The same row through LDS, for long rows: a thread owns EPT consecutive
+// ids, so loading them directly makes every wave-wide load touch 64 cache
+// lines (one per lane, each line requested again for every element) -- with
+// 32 ids per thread that took ~6 us per row.  Here each wave loads its own
+// 64 * EPT scores lane-contiguously (two lines per load), parks them in its
+// part of stage[] and reads its threads' runs back; only the wave's own
+// lanes touch its part, so no workgroup barrier is needed.
+struct StagedRowScores {
+  const float* srow;
+  float* stage;   // kSelWG * EPT floats of LDS
+  template <int EPT>
+  __device__ __forceinline__ bool operator()(float (&sv)[EPT], int j0, int nv) const {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wbase = j0 - lane * EPT;          // the wave's first id
+    float* st = stage + wave * 64 * EPT;
+    float v[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+      const int j = wbase + 64 * i + lane;
+      v[i] = j < nv ? srow[j] : -INFINITY;
+    }
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) st[64 * i + lane] = v[i];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int e = 0; e < EPT; e += 4) {
+      const float4 x = *reinterpret_cast<const float4*>(&st[lane * EPT + e]);
+      sv[e] = x.x;
+      sv[e + 1] = x.y;
+      sv[e + 2] = x.z;
+      sv[e + 3] = x.w;
+    }
+    return true;
+  }
+};
+
 constexpr int kValBins = 2048;   // value bins of the threshold search
 
 #ifndef SPOT_SEL_TS
@@ -217,7 +255,7 @@ __device__ __forceinline__ SelRow select_row_core(SelWgSmem<EPT, SPL>& sm, const
   constexpr int NT = kSelWG, NW = NT / 64;
   constexpr int P = 64 * SPL;
   constexpr float kLog2e = 1.4426950408889634f;
-  static_assert(EPT <= 16, "a thread's ids must fit one bit word");
+  static_assert(EPT <= 32, "a thread's ids must fit one 32-bit word");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sink_end = min(n_sink, nv);
   const int rec_start = max(0, nv - n_recent);

@@ -168,6 +168,11 @@ SELECT_CASES = [
     (8, 1024, Rule(0.5, 68, 0, 1, 2), "ragged"),        # cap 65: the first sorted
     (8, 2048, Rule(0.3, 40, 30, 1, 2), None),           # k_min floor under a cap of 37
     (8, 600, Rule(0.2, 20, 0, 2, 3), None),             # short nucleus, cap 15
+    # rows of 16-token blocks (128K tokens: 8192 blocks) on the workgroup kernel
+    (4, 8192, Rule(0.95, 512, 0, 4, 8), None),          # the paper's block, 8192-token budget
+    (8, 8192, Rule(0.9, 64, 0, 4, 8), "ragged"),        # counted cut
+    (4, 8192, Rule(1.0, 2048, 0, 0, 0), None),          # static top-K
+    (4, 6000, Rule(0.5, 1000, 0, 1, 2), "ragged"),      # 1000-block cap
 ]
 
 
@@ -214,7 +219,7 @@ def test_select_deterministic_and_ties(rule):
 
 
 @pytest.mark.parametrize("nblk,k_max", [(300, 100), (2048, 100), (2048, 40), (2048, 1500),
-                                        (8192, 700)])
+                                        (8192, 700), (16384, 700)])
 def test_select_negative_zero_ties_positive_zero(nblk, k_max):
     """-0.0 and +0.0 are the same score: a cut through a run of zeros of
     both signs takes the lower ids, whatever their sign (every selection
