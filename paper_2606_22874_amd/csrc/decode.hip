@@ -11,7 +11,7 @@ using namespace dec;
 // slot i % n_slot.  SB: tokens per selected block (64, or 16 for the paper's
 // selector block; sparse only).
 template <int G, bool DENSE, int SB = kBlk>
-__global__ __launch_bounds__(64 * G, waves_per_eu(G)) void decode_split_kernel(
+__global__ __launch_bounds__(64 * kDecWaves, 2) void decode_split_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ seq_len,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ count, int k_max, int h_q,
@@ -28,7 +28,8 @@ __global__ __launch_bounds__(64 * G, waves_per_eu(G)) void decode_split_kernel(
 }  // namespace
 
 // Workgroups per (sequence, KV head) pair: aim for ~2048 waves over the grid
-// (8 per CU, so the whole grid is resident at once), at least one, and at
+// (8 per CU, so the whole grid is resident at once; 4 waves per workgroup
+// whatever the group size), at least one, and at
 // least two list entries per workgroup (with blocks of 16 tokens: two
 // virtual blocks of four entries).  Never more than with per_virtual = 1, so
 // a workspace sized for 64-token blocks fits.
@@ -37,7 +38,8 @@ __global__ __launch_bounds__(64 * G, waves_per_eu(G)) void decode_split_kernel(
 #endif
 int decode_num_splits(int batch, int h_kv, int max_blocks, int group, int per_virtual) {
   const int pairs = batch * h_kv;
-  int n = (SPOT_DECODE_WAVE_TARGET / group + pairs - 1) / pairs;
+  (void)group;
+  int n = (SPOT_DECODE_WAVE_TARGET / kDecWaves + pairs - 1) / pairs;
   const int by_len = ((max_blocks + per_virtual - 1) / per_virtual + 1) / 2;
   if (n > by_len) n = by_len;
   const int min_for_ids = (max_blocks + kMaxIds - 1) / kMaxIds;  // entries per WG <= kMaxIds
@@ -76,26 +78,25 @@ hipError_t launch_decode(bool dense, const void* q, const void* k, const void* v
   auto qq = static_cast<const uint16_t*>(q);
   auto kk = static_cast<const uint16_t*>(k);
   auto vv = static_cast<const uint16_t*>(v);
-#define SPOT_DECODE_CASE(GG)                                                                   \
-  if (G == GG) {                                                                               \
-    if (b16)                                                                                   \
-      hipLaunchKernelGGL((decode_split_kernel<GG, false, 16>), grid, dim3(64 * GG), 0, s, qq,  \
-                         kk, vv, seq_len, idx, count, k_max, h_q, h_kv, l_cap, scale_log2,     \
-                         n_slot, ws_o, ws_ml, counters, o16, lse);                             \
-    else if (dense)                                                                            \
-      hipLaunchKernelGGL((decode_split_kernel<GG, true>), grid, dim3(64 * GG), 0, s, qq, kk,   \
-                         vv, seq_len, idx, count, k_max, h_q, h_kv, l_cap, scale_log2,         \
-                         n_slot, ws_o, ws_ml, counters, o16, lse);                             \
-    else                                                                                       \
-      hipLaunchKernelGGL((decode_split_kernel<GG, false>), grid, dim3(64 * GG), 0, s, qq, kk,  \
-                         vv, seq_len, idx, count, k_max, h_q, h_kv, l_cap, scale_log2,         \
-                         n_slot, ws_o, ws_ml, counters, o16, lse);                             \
+#define SPOT_DECODE_LAUNCH(...)                                                               \
+  hipLaunchKernelGGL((decode_split_kernel<__VA_ARGS__>), grid, dim3(64 * kDecWaves), 0, s, qq, \
+                     kk, vv, seq_len, idx, count, k_max, h_q, h_kv, l_cap, scale_log2, n_slot,  \
+                     ws_o, ws_ml, counters, o16, lse)
+#define SPOT_DECODE_CASE(GG)                 \
+  if (G == GG) {                             \
+    if (b16)                                 \
+      SPOT_DECODE_LAUNCH(GG, false, 16);     \
+    else if (dense)                          \
+      SPOT_DECODE_LAUNCH(GG, true);          \
+    else                                     \
+      SPOT_DECODE_LAUNCH(GG, false);         \
   }
   SPOT_DECODE_CASE(1)
   SPOT_DECODE_CASE(2)
   SPOT_DECODE_CASE(4)
   SPOT_DECODE_CASE(8)
 #undef SPOT_DECODE_CASE
+#undef SPOT_DECODE_LAUNCH
   return hipGetLastError();
 }
 

@@ -8,27 +8,34 @@
 // Work split: grid (n_split, h_kv, batch).  A workgroup owns every n_split-th
 // entry of its sequence's block list and the whole GQA group of G query
 // heads of one KV head, so every K/V byte is read from HBM exactly once.  The
-// workgroup has G waves; wave w owns token rows [w*T, (w+1)*T) (T = 64/G) of
-// every 64-token block, and its lanes are (head h, token t) = (lane / T,
-// lane % T):
-//   * each wave streams its own contiguous T-row slices of K and V (16-byte
-//     coalesced loads, the next block's slice already in flight in registers)
-//     through a wave-private LDS region -- no workgroup barrier per block;
-//   * Q.K: lane (h, t) takes the full 128-dim dot product of query head h with
-//     key row t using packed BF16 dot2; the G lanes reading the same key row
-//     are served by one LDS broadcast;
-//   * online softmax per head in the log2 domain over the T lanes of the head
-//     (DPP reductions), lane-local running sums;
-//   * P.V: lane = pair of output dims, all G heads, probabilities broadcast
-//     from LDS.
+// workgroup has 4 waves; wave w owns token rows [16w, 16w+16) of every
+// 64-token block and keeps its own online-softmax state per head.  Per block
+// a wave's arithmetic is two small matrix products on the matrix cores, run
+// transposed so that the scores never leave the registers (the GQA group's
+// heads are the 16 columns of each tile, G of them real):
+//   S^T = K Q^T       4 v_mfma_f32_16x16x32_bf16: the wave's 16 K rows are
+//                     the A operand straight from global memory (16-byte
+//                     loads), Q^T the B operand held for the whole loop;
+//   online softmax    per head = per lane column: block maximum over the 4
+//                     rows a lane holds and the 4 lane groups (two lane
+//                     swaps), a lazy rescale (only when a maximum grows by
+//                     more than 2^kLazy), exponentials in the log2 domain;
+//   O^T += V^T P^T    8 v_mfma_f32_16x16x16_bf16: P^T goes from the score
+//                     accumulators straight into the B operand (rounded to
+//                     BF16), V^T comes from the wave's V rows in LDS through
+//                     the transposing read ds_read_b64_tr_b16.
+// The C layout of a 16x16 tile gives lane l the rows 4(l/16)..4(l/16)+3 of
+// column l%16; the A/B layouts give lane l the consecutive k entries of row
+// (A) or column (B) l%16 starting at k = 8(l/16) (16x16x32) or 4(l/16)
+// (16x16x16).  The next two blocks' K and V rows are in flight in registers
+// while one is computed.
 // Blocks of 16 tokens (SB = 16, the paper's selector block): the loop runs
 // over "virtual blocks" of four consecutive entries of the workgroup's list
-// (the last one padded with -1), and wave row r of virtual block n is row
-// (wT + r) % 16 of entry 4n + (wT + r) / 16 -- the same slice shapes, loads
-// and LDS layout, with a per-row token address; rows of a padding entry are
-// masked like rows past seq_len.  Each wave keeps its own softmax state, so
-// which tokens a wave sees does not matter to the merge.
-// After the block loop the G waves' (m, l, o) states are merged in LDS into
+// (the last one padded with -1), and wave w takes entry 4n + w of virtual
+// block n -- the same 16-row loads; rows of a padding entry are masked like
+// rows past seq_len.  Each wave keeps its own softmax state, so which
+// tokens a wave sees does not matter to the merge.
+// After the block loop the 4 waves' (m, l, O) states are merged in LDS into
 // one partial per head; the last split to finish for a (sequence, KV head)
 // merges all splits with log-sum-exp weights, rounds to BF16 and resets the
 // completion counter, so the whole call is one kernel launch.
@@ -42,8 +49,6 @@ namespace dec {
 
 constexpr int kD = 128;
 constexpr int kKRow = kD + 8;    // padded K row in LDS (272 bytes)
-// Occupancy target in waves per SIMD (caps VGPRs without spilling).
-constexpr int waves_per_eu(int G) { return G >= 4 ? 2 : 1; }
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMaxIds = 512;     // max list entries per workgroup
 static_assert(kMaxIds % 4 == 0, "16-token blocks pad the list to whole virtual blocks");
@@ -71,30 +76,6 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// ------------------------------------------- reductions over T-lane groups
-// Max / sum over the T consecutive lanes of a group (T in {8, 16, 32, 64});
-// every lane of the group receives the result.
-template <int T>
-__device__ __forceinline__ float group_max(float v) {
-  v = fmaxf(v, dpp_f<kDppQuadXor1>(v));
-  v = fmaxf(v, dpp_f<kDppQuadXor2>(v));
-  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
-  if (T >= 16) v = fmaxf(v, dpp_f<kDppMirror>(v));
-  if (T >= 32) v = fmaxf(v, __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F)));
-  if (T >= 64) v = fmaxf(readlane_f(v, 0), readlane_f(v, 32));
-  return v;
-}
-template <int T>
-__device__ __forceinline__ float group_sum(float v) {
-  v += dpp_f<kDppQuadXor1>(v);
-  v += dpp_f<kDppQuadXor2>(v);
-  v += dpp_f<kDppHalfMirror>(v);
-  if (T >= 16) v += dpp_f<kDppMirror>(v);
-  if (T >= 32) v += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F));
-  if (T >= 64) v = readlane_f(v, 0) + readlane_f(v, 32);
-  return v;
 }
 
 // Log-sum-exp merge of n <= 16 partials of query head bh held by one wave:
@@ -189,36 +170,26 @@ __device__ __forceinline__ void merge_head(const float* __restrict__ ws_o,
   if (lse && lane == 0) lse[bh] = L > 0.f ? (M + log2f(L)) * 0.6931471805599453f : -INFINITY;
 }
 
-// One T-row slice of a block's K and of its V (contiguous T x 256 bytes each)
-// into registers: 16-byte chunk c = i * 64 + lane.
-template <int NLD>
-__device__ __forceinline__ void load_slice(u32x4 (&kr)[NLD], u32x4 (&vr)[NLD],
-                                           const uint16_t* __restrict__ kw,
-                                           const uint16_t* __restrict__ vw, int blk, int lane) {
-  const size_t base = (size_t)blk * kBlk * kD;
-#pragma unroll
-  for (int i = 0; i < NLD; ++i) {
-    const int c = i * 64 + lane;
-    kr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kw + base + c * 8));
-    vr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vw + base + c * 8));
-  }
-}
-
 // ---------------------------------------------------------- LDS layout
+constexpr int kDecWaves = 4;         // waves per workgroup (16 token rows each)
+constexpr int kVRowBytes = kD * 2;   // one V row, 256 bytes
+constexpr float kLazy = 8.f;         // rescale only when a maximum grows by more (log2)
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
 template <int G>
 struct DecodeSmem {
-  static constexpr int T = 64 / G;                    // token rows per wave
-  struct Wave {
-    uint16_t k[T * kKRow];                            // K slice, padded rows
-    uint16_t v[T * kD];                               // V slice
-    float p[T][G];                                    // probabilities [token][head]
-  };
+  static_assert(G >= 1 && G <= 16, "the heads of a group are the columns of a 16x16 tile");
   struct Merge {
-    float ml[G][G][2];                                // [wave][head] (m, l)
-    float o[G][G][kD];                                // [wave][head][dim]
+    float ml[kDecWaves][G][2];                        // [wave][head] (m, l)
+    alignas(16) float o[kDecWaves][G][kD];            // [wave][head][dim]
   };
   union {
-    Wave wave[G];
+    alignas(16) unsigned char v[kDecWaves][16 * kVRowBytes];   // each wave's V rows
     Merge merge;
   };
   int ids[kMaxIds];
@@ -266,153 +237,175 @@ struct ListFromIdx {
 };
 
 // ---------------------------------------------------------- the body
-// The G query heads of KV head g of sequence b: lane (h, t) of every wave
-// holds query head g*G + h (h = lane / T) as 64 packed BF16 pairs.
-template <int G>
-__device__ __forceinline__ void load_query_heads(uint32_t (&qv)[kD / 2],
-                                                 const uint16_t* __restrict__ q, int b, int g,
-                                                 int h_q) {
-  constexpr int T = 64 / G;
-  const int hh = __lane_id() / T;
-  const u32x4* qp = reinterpret_cast<const u32x4*>(q + ((size_t)b * h_q + g * G + hh) * kD);
-#pragma unroll
-  for (int i = 0; i < kD / 8; ++i) {
-    const u32x4 t = qp[i];
-    qv[4 * i + 0] = t.x; qv[4 * i + 1] = t.y; qv[4 * i + 2] = t.z; qv[4 * i + 3] = t.w;
-  }
+// Physical 16-byte chunk of logical chunk c of V row r in LDS: the
+// transposing read takes 8 bytes from each of 8 rows at the same column per
+// half wave, so rows r and r + 1 .. r + 7 must land in different bank
+// groups; XOR with 2 (r % 8) moves the chunk pairs apart and keeps each
+// pair's two chunks adjacent.
+__device__ __forceinline__ int swz_v(int r, int c) { return c ^ ((r & 7) << 1); }
+
+// Two floats -> packed BF16 pair, round to nearest even.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
 }
 
-// One workgroup's partial of one query head after its G waves are merged:
-// wave w holds head w of the group (M and L in every lane, output dims
-// 2*lane and 2*lane+1 in o0, o1).  L == 0 means no token was seen.
+// Cross-lane partner values without LDS: the lane swaps exchange the two
+// halves / the odd-even 16-lane rows of a register.
+__device__ __forceinline__ float lanes_max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float lanes_max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float lanes_sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float lanes_sum_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Q^T as the B operand of S^T = K Q^T: lane l holds query head l%16 of the
+// group (zero past G), dims 32 kc + 8(l/16) .. +8 for kc = 0 .. 3.
+struct QueryFrag {
+  bf16x8_t q[4];
+};
+template <int G>
+__device__ __forceinline__ QueryFrag load_query_heads(const uint16_t* __restrict__ q, int b,
+                                                      int g, int h_q) {
+  const int lane = __lane_id(), hh = lane & 15, kg = lane >> 4;
+  QueryFrag f;
+#pragma unroll
+  for (int kc = 0; kc < 4; ++kc) {
+    u32x4 t = {0u, 0u, 0u, 0u};
+    if (hh < G)
+      t = *reinterpret_cast<const u32x4*>(q + ((size_t)b * h_q + g * G + hh) * kD + 32 * kc +
+                                          8 * kg);
+    f.q[kc] = __builtin_bit_cast(bf16x8_t, t);
+  }
+  return f;
+}
+
+// One workgroup's partial of one query head after its 4 waves are merged:
+// M and L in every lane, output dims 2*lane and 2*lane+1 in o0, o1.  L == 0
+// means no token was seen.
 struct HeadPartial {
   float M, L, o0, o1;
+};
+// The partials a wave holds after the merge: heads wave + 4j (j < HPW) of the
+// group; entries for heads >= G are unused.
+template <int G>
+struct Partials {
+  static constexpr int HPW = (G + kDecWaves - 1) / kDecWaves;
+  HeadPartial h[HPW];
 };
 
 // The block loop of a workgroup: blocks blk_of(0 .. n_local-1) of the KV
 // head whose caches start at kh / vh ([l_cap, 128] each), tokens below sl.
-// Wave w processes token rows [w*T, (w+1)*T) of every block; the G waves'
+// Wave w processes token rows [16w, 16w+16) of every block; the 4 waves'
 // states are merged in LDS at the end (two barriers).  issued(n) is called
 // by every wave right after it issued the loads of block n, so a caller can
 // act once the last block's loads are in flight.  SB = 16: n_local counts
 // virtual blocks, and blk_of(e) is list entry e (-1 for padding).
 template <int G, int SB = kBlk, class BlkOf, class Issued>
-__device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
-                                                     const uint32_t (&qv)[kD / 2],
+__device__ __forceinline__ Partials<G> attend_blocks(DecodeSmem<G>& sm, const QueryFrag& qf,
                                                      const uint16_t* __restrict__ kh,
                                                      const uint16_t* __restrict__ vh, int sl,
                                                      int n_local, const BlkOf& blk_of,
                                                      float scale_log2, const Issued& issued) {
-  constexpr int T = 64 / G;               // token rows per wave per block
-  constexpr int NLD = T * kD * 2 / 1024;  // 16-byte loads per lane per slice
-  static_assert(NLD >= 1, "slice smaller than one wave load");
   static_assert(SB == kBlk || SB == 16, "blocks of 64 or 16 tokens");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int hh = lane / T, tt = lane % T;  // this lane's (head, token row)
+  const int r16 = lane & 15, kg = lane >> 4;   // tile column / row, lane group
+  unsigned char* vs = sm.v[wave];
 
-  // This wave's slice of a block starts at token row wave * T.
-  const uint16_t* kw = kh + (size_t)wave * T * kD;
-  const uint16_t* vw = vh + (size_t)wave * T * kD;
-  auto& W = sm.wave[wave];
-
-  // Loads of (virtual) block n into a register stage; 16-byte chunk
-  // c = i * 64 + lane is row c / 16, column chunk c % 16 of the wave's slice.
-  auto load = [&](u32x4 (&kr)[NLD], u32x4 (&vr)[NLD], int n) {
+  // First token of this wave's 16 rows in (virtual) block n; -1 for padding.
+  auto base_tok = [&](int n) -> int {
     if constexpr (SB == kBlk) {
-      load_slice<NLD>(kr, vr, kw, vw, blk_of(n), lane);
+      return blk_of(n) * kBlk + wave * 16;
     } else {
+      const int id = blk_of(4 * n + wave);
+      return id < 0 ? -1 : id * SB;
+    }
+  };
+  // K rows in the A layout of 16x16x32 (row r16, dims 32 kc + 8 kg .. +8) and
+  // V rows lane-contiguously (load i: row 4i + kg, chunk r16).
+  auto load = [&](u32x4 (&kr)[4], u32x4 (&vr)[4], int n) {
+    const int tb = max(base_tok(n), 0);
+    const uint16_t* kp = kh + (size_t)(tb + r16) * kD + 8 * kg;
+    const uint16_t* vp = vh + (size_t)tb * kD + lane * 8;
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) {
-        const int wr = wave * T + 4 * i + (lane >> 4);
-        const int id = blk_of(4 * n + (wr >> 4));
-        const size_t off = (size_t)(id < 0 ? 0 : id * SB + (wr & (SB - 1))) * kD + (lane & 15) * 8;
-        kr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kh + off));
-        vr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vh + off));
-      }
-    }
-  };
-  // This lane's token (row tt of the wave's slice) in (virtual) block n; -1
-  // for a padding entry.
-  auto tok_of = [&](int n) {
-    if constexpr (SB == kBlk) {
-      return blk_of(n) * kBlk + wave * T + tt;
-    } else {
-      const int wr = wave * T + tt;
-      const int id = blk_of(4 * n + (wr >> 4));
-      return id < 0 ? -1 : id * SB + (wr & (SB - 1));
-    }
+    for (int kc = 0; kc < 4; ++kc)
+      kr[kc] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kp + 32 * kc));
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      vr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vp + i * 512));
   };
 
-  // Register stages A and B hold the two blocks of the current chunk.
-  u32x4 krA[NLD], vrA[NLD], krB[NLD], vrB[NLD];
+  u32x4 krA[4], vrA[4], krB[4], vrB[4];
+  f32x4_t o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_lane = 0.f;
-  float acc[G][2];
-#pragma unroll
-  for (int h = 0; h < G; ++h) acc[h][0] = acc[h][1] = 0.f;
 
-  auto consume = [&](const u32x4 (&kr)[NLD], const u32x4 (&vr)[NLD]) {
-    wave_lds_sync();  // this wave's reads of the previous slice are issued
+  // V rows of the stage into the wave's LDS rows (swizzled), then S^T.
+  auto front = [&](const u32x4 (&kr)[4], const u32x4 (&vr)[4]) -> f32x4_t {
+    wave_lds_sync();  // this wave's reads of the previous rows are issued
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int c = i * 64 + lane;
-      *reinterpret_cast<u32x4*>(&W.k[(c >> 4) * kKRow + (c & 15) * 8]) = kr[i];
-      *reinterpret_cast<u32x4*>(&W.v[c * 8]) = vr[i];
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * i + kg;
+      *reinterpret_cast<u32x4*>(vs + r * kVRowBytes + (swz_v(r, r16) << 4)) = vr[i];
     }
+    f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc)
+      s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[kc]), qf.q[kc],
+                                                  s, 0, 0, 0);
     wave_lds_sync();
+    return s;
   };
-  auto compute = [&](int tok) {
-    // Q.K for (head hh, token row tt)
-    const u32x4* krow = reinterpret_cast<const u32x4*>(&W.k[tt * kKRow]);
-    float s = 0.f;
+  // Softmax of the block's scores and O^T += V^T P^T.
+  auto back = [&](int n, f32x4_t s) {
+    const int tb = base_tok(n);
+    float x[4];
 #pragma unroll
-    for (int i = 0; i < kD / 8; ++i) {
-      const u32x4 kk = krow[i];
-      s = dot2_bf16(qv[4 * i + 0], kk.x, s);
-      s = dot2_bf16(qv[4 * i + 1], kk.y, s);
-      s = dot2_bf16(qv[4 * i + 2], kk.z, s);
-      s = dot2_bf16(qv[4 * i + 3], kk.w, s);
+    for (int i = 0; i < 4; ++i) {
+      const int t = tb + 4 * kg + i;
+      x[i] = tb >= 0 && t < sl ? s[i] * scale_log2 : -INFINITY;
     }
-    const bool tok_ok = (SB == kBlk || tok >= 0) && tok < sl;
-    const float x = tok_ok ? s * scale_log2 : -INFINITY;
-    const float m_new = fmaxf(m_run, group_max<T>(x));
-    // A slice whose rows all lie past seq_len leaves the state unchanged.
-    const bool live = m_new > -INFINITY;
-    const float pr = live ? exp2f(x - m_new) : 0.f;
-    const float alpha = live ? exp2f(m_run - m_new) : 1.f;
-    m_run = m_new;
-    l_lane = l_lane * alpha + pr;
-    W.p[tt][hh] = pr;
-    float al[G];
+    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    mx = lanes_max_xor32(lanes_max_xor16(mx));          // the head's block maximum
+    if (__ballot(mx > m_run + kLazy) != 0ull) {           // some head's maximum grew
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
+      l_lane *= alpha;
 #pragma unroll
-    for (int h = 0; h < G; ++h) al[h] = readlane_f(alpha, h * T);
-    wave_lds_sync();
-
-    // P.V: lane = output dims 2*lane, 2*lane+1 for every head of the group
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      acc[h][0] *= al[h];
-      acc[h][1] *= al[h];
+      for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
+      m_run = m_new;
     }
-#pragma unroll 4
-    for (int t = 0; t < T; ++t) {
-      float pt[G];
-      if constexpr (G >= 4) {
+    float p[4];
 #pragma unroll
-        for (int h4 = 0; h4 < G; h4 += 4) {
-          const float4 p4 = *reinterpret_cast<const float4*>(&W.p[t][h4]);
-          pt[h4] = p4.x; pt[h4 + 1] = p4.y; pt[h4 + 2] = p4.z; pt[h4 + 3] = p4.w;
-        }
-      } else {
+    for (int i = 0; i < 4; ++i) p[i] = x[i] == -INFINITY ? 0.f : exp2f(x[i] - m_run);
+    l_lane += (p[0] + p[1]) + (p[2] + p[3]);
+    const s16x4_t pb =
+        __builtin_bit_cast(s16x4_t, u32x2_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])});
+    // V^T fragment of d tile dt: lane (kg, r16) addresses row 4 kg + r16/4,
+    // columns 16 dt + 4 (r16 % 4) .. +3 and receives column 16 dt + r16 of
+    // rows 4 kg .. 4 kg + 3.
+    const int vr_row = 4 * kg + (r16 >> 2);
+    const unsigned char* vrow = vs + vr_row * kVRowBytes + (r16 & 1) * 8;
 #pragma unroll
-        for (int h = 0; h < G; ++h) pt[h] = W.p[t][h];
-      }
-      const uint32_t vv = *reinterpret_cast<const uint32_t*>(&W.v[t * kD + 2 * lane]);
-      const float v0 = bf16_lo(vv), v1 = bf16_hi(vv);
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        acc[h][0] = fmaf(pt[h], v0, acc[h][0]);
-        acc[h][1] = fmaf(pt[h], v1, acc[h][1]);
-      }
+    for (int dt = 0; dt < 8; ++dt) {
+      const int c = 2 * dt + ((r16 & 3) >> 1);
+      const s16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4_t*)(vrow + (swz_v(vr_row, c) << 4)));
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pb, o[dt], 0, 0, 0);
     }
   };
 
@@ -429,27 +422,27 @@ __device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
     load(krB, vrB, 1);
     issued(1);
     for (; n + 3 < n_local; n += 2) {
-      consume(krA, vrA);
+      f32x4_t s = front(krA, vrA);
       load(krA, vrA, n + 2);
       issued(n + 2);
-      compute(tok_of(n));
-      consume(krB, vrB);
+      back(n, s);
+      s = front(krB, vrB);
       load(krB, vrB, n + 3);
       issued(n + 3);
-      compute(tok_of(n + 1));
+      back(n + 1, s);
     }
     // n_local - n is 2 or 3: blocks n and n + 1 are in flight
-    consume(krA, vrA);
+    f32x4_t s = front(krA, vrA);
     if (n + 2 < n_local) {
       load(krA, vrA, n + 2);
       issued(n + 2);
     }
-    compute(tok_of(n));
-    consume(krB, vrB);
-    compute(tok_of(n + 1));
+    back(n, s);
+    s = front(krB, vrB);
+    back(n + 1, s);
     if (n + 2 < n_local) {
-      consume(krA, vrA);
-      compute(tok_of(n + 2));
+      s = front(krA, vrA);
+      back(n + 2, s);
     }
   } else {
     if (n_local > 0) {
@@ -461,57 +454,55 @@ __device__ __forceinline__ HeadPartial attend_blocks(DecodeSmem<G>& sm,
       issued(1);
     }
     if (n_local > 2) {
-      consume(krA, vrA);
-      compute(tok_of(0));
+      f32x4_t s = front(krA, vrA);
       load(krA, vrA, 2);
       issued(2);
-      consume(krB, vrB);
-      compute(tok_of(1));
-      consume(krA, vrA);
-      compute(tok_of(2));
+      back(0, s);
+      s = front(krB, vrB);
+      back(1, s);
+      s = front(krA, vrA);
+      back(2, s);
     } else {
-      if (n_local > 0) {
-        consume(krA, vrA);
-        compute(tok_of(0));
-      }
-      if (n_local > 1) {
-        consume(krB, vrB);
-        compute(tok_of(1));
-      }
+      if (n_local > 0) back(0, front(krA, vrA));
+      if (n_local > 1) back(1, front(krB, vrB));
     }
   }
 
-  // ---- merge the G waves (token slices) into one partial per head ----
-  const float l_grp = group_sum<T>(l_lane);
-  __syncthreads();  // every wave is done with its slice buffers (aliased below)
-  if (tt == 0) {
-    sm.merge.ml[wave][hh][0] = m_run;
-    sm.merge.ml[wave][hh][1] = l_grp;
+  // ---- merge the 4 waves into one partial per head ----
+  const float l_head = lanes_sum_xor32(lanes_sum_xor16(l_lane));   // column r16's sum
+  __syncthreads();  // every wave is done with its V rows (aliased below)
+  if (r16 < G) {
+    if (kg == 0) {
+      sm.merge.ml[wave][r16][0] = m_run;
+      sm.merge.ml[wave][r16][1] = l_head;
+    }
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt)
+      *reinterpret_cast<f32x4_t*>(&sm.merge.o[wave][r16][16 * dt + 4 * kg]) = o[dt];
   }
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-    *reinterpret_cast<float2*>(&sm.merge.o[wave][h][2 * lane]) = make_float2(acc[h][0], acc[h][1]);
   __syncthreads();
-  HeadPartial r;
-  {
-    const int h = wave;  // wave w merges head w of the group
-    float M = -INFINITY;
+  Partials<G> r;
 #pragma unroll
-    for (int w = 0; w < G; ++w)
-      if (sm.merge.ml[w][h][1] > 0.f) M = fmaxf(M, sm.merge.ml[w][h][0]);
-    float L = 0.f, o0 = 0.f, o1 = 0.f;
-    if (M > -INFINITY) {
+  for (int j = 0; j < Partials<G>::HPW; ++j) {
+    const int h = wave + kDecWaves * j;   // this wave merges head h of the group
+    float M = -INFINITY, L = 0.f, o0 = 0.f, o1 = 0.f;
+    if (h < G) {
 #pragma unroll
-      for (int w = 0; w < G; ++w) {
-        const float lw = sm.merge.ml[w][h][1];
-        const float wgt = lw > 0.f ? exp2f(sm.merge.ml[w][h][0] - M) : 0.f;
-        L = fmaf(lw, wgt, L);
-        const float2 o = *reinterpret_cast<const float2*>(&sm.merge.o[w][h][2 * lane]);
-        o0 = fmaf(o.x, wgt, o0);
-        o1 = fmaf(o.y, wgt, o1);
+      for (int w = 0; w < kDecWaves; ++w)
+        if (sm.merge.ml[w][h][1] > 0.f) M = fmaxf(M, sm.merge.ml[w][h][0]);
+      if (M > -INFINITY) {
+#pragma unroll
+        for (int w = 0; w < kDecWaves; ++w) {
+          const float lw = sm.merge.ml[w][h][1];
+          const float wgt = lw > 0.f ? exp2f(sm.merge.ml[w][h][0] - M) : 0.f;
+          L = fmaf(lw, wgt, L);
+          const float2 ov = *reinterpret_cast<const float2*>(&sm.merge.o[w][h][2 * lane]);
+          o0 = fmaf(ov.x, wgt, o0);
+          o1 = fmaf(ov.y, wgt, o1);
+        }
       }
     }
-    r = HeadPartial{M, L, o0, o1};
+    r.h[j] = HeadPartial{M, L, o0, o1};
   }
   return r;
 }
@@ -536,8 +527,7 @@ __device__ __forceinline__ bool decode_body(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   unsigned* pc = pair_counters(counters, pair);
 
-  uint32_t qv[kD / 2];
-  load_query_heads<G>(qv, q, b, g, h_q);
+  const QueryFrag qf = load_query_heads<G>(q, b, g, h_q);
 
   const int sl = min(seq_len[b], l_cap);
   const int nb_valid = (sl + SB - 1) / SB;
@@ -558,13 +548,16 @@ __device__ __forceinline__ bool decode_body(
   const int n_local = DENSE ? max(e1 - e0, 0) : sm.n_local;
   const size_t head_base = ((size_t)b * h_kv + g) * (size_t)l_cap * kD;
   auto blk_of = [&](int n) { return DENSE ? e0 + n : sm.ids[n]; };
-  const HeadPartial hp = attend_blocks<G, SB>(sm, qv, k + head_base, v + head_base, sl,
+  const Partials<G> hp = attend_blocks<G, SB>(sm, qf, k + head_base, v + head_base, sl,
                                               n_local, blk_of, scale_log2, NoHook{});
-  {
-    const int h = wave;
-    const size_t ps = ((size_t)b * h_q + g * G + h) * n_slot + slot;
-    store_coherent(&ws_o[ps * kD + 2 * lane], make_float2(hp.o0, hp.o1));
-    if (lane == 0) store_coherent(&ws_ml[ps * 2], make_float2(hp.M, hp.L));
+#pragma unroll
+  for (int j = 0; j < Partials<G>::HPW; ++j) {
+    const int h = wave + kDecWaves * j;
+    if (h < G) {
+      const size_t ps = ((size_t)b * h_q + g * G + h) * n_slot + slot;
+      store_coherent(&ws_o[ps * kD + 2 * lane], make_float2(hp.h[j].o0, hp.h[j].o1));
+      if (lane == 0) store_coherent(&ws_ml[ps * 2], make_float2(hp.h[j].M, hp.h[j].L));
+    }
   }
 
   // ---- the last workgroup of the pair merges all slots ----
@@ -577,7 +570,11 @@ __device__ __forceinline__ bool decode_body(
   }
   __syncthreads();
   if (!sm.last) return false;
-  merge_head(ws_o, ws_ml, n_slot, (size_t)b * h_q + g * G + wave, out, lse, lane);
+#pragma unroll
+  for (int j = 0; j < Partials<G>::HPW; ++j) {
+    const int h = wave + kDecWaves * j;
+    if (h < G) merge_head(ws_o, ws_ml, n_slot, (size_t)b * h_q + g * G + h, out, lse, lane);
+  }
   if (tid == 0) __hip_atomic_store(&pc[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   return true;
 }

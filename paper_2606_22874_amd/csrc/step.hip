@@ -384,12 +384,11 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
   }
   SPOT_STEP_TS(4);
 
-  uint32_t qv[kD / 2];
-  load_query_heads<kStepG>(qv, a.q, b, g, a.h_q);
+  const QueryFrag qf = load_query_heads<kStepG>(a.q, b, g, a.h_q);
   const size_t head_base = ((size_t)b * a.h_kv + g) * (size_t)a.l_cap * kD;
   auto blk_of = [&](int n) { return sm.dec.ids[n]; };
-  const HeadPartial hp = attend_blocks<kStepG>(sm.dec, qv, a.k + head_base, a.v + head_base, sl,
-                                               n_local, blk_of, a.scale_log2, NoHook{});
+  const HeadPartial hp = attend_blocks<kStepG>(sm.dec, qf, a.k + head_base, a.v + head_base, sl,
+                                               n_local, blk_of, a.scale_log2, NoHook{}).h[0];
   SPOT_STEP_TS(5);
   const size_t bh = (size_t)b * a.h_q + g * kStepG + wave;   // wave w: head w of the group
   store_coherent(&a.part_o[(bh * n_slot + slot) * kD + 2 * lane], make_float2(hp.o0, hp.o1));
