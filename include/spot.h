@@ -378,7 +378,8 @@ size_t spot_decode_workspace_bytes(int batch, int h_q, int h_kv, int d, int max_
  *           sizes must be zero-filled again first.  Calls that may overlap
  *           in time need separate workspaces.
  *
- * Supported: d == 128, h_q / h_kv in {1, 2, 4, 8}.
+ * Supported: d == 128, h_q a multiple of h_kv with h_q / h_kv <= 16 (the
+ * group's heads are the columns of the 16-wide matrix tiles).
  */
 spot_status spot_sparse_decode(const void *q, const void *k, const void *v,
                                const int32_t *seq_len, const int32_t *idx, const int32_t *count,
@@ -421,13 +422,13 @@ spot_status spot_sparse_decode_blk(const void *q, const void *k, const void *v,
  * three calls, and the outputs (scores, idx, count, nuc_mass, out, lse) are
  * the ones they would produce.
  *
- * When h_q == 4 * h_kv, nblk <= 4096 and min(k_max, nblk) <= 512, the three
- * stages run as one launch with no kernel boundary in between: the first
- * workgroups score chunks of their sequence's blocks, one workgroup per
- * sequence selects its blocks from the scores of all chunks and publishes
- * the set, and every workgroup attends to its share of the set of its
- * (sequence, KV head) pair; the last workgroup of a pair to finish merges
- * the pair's partials.  The hand-offs go through self-flagging record words
+ * When h_q is 4 or 8 times h_kv, nblk <= 4096 and min(k_max, nblk) <= 512,
+ * the three stages run as one launch with no kernel boundary in between: the
+ * first workgroups score chunks of their sequence's blocks, one workgroup
+ * per sequence selects its blocks from the scores of all chunks and
+ * publishes the set, and every workgroup attends to its share of the set of
+ * its (sequence, KV head) pair; the last workgroup of a pair to finish
+ * merges the pair's partials.  The hand-offs go through self-flagging record words
  * in the workspace, which each reader clears again.  Otherwise (or when no
  * such grid fits) the three stages are launched one after the other on
  * `stream`.  Either way the results are deterministic; the fused path may

@@ -10,7 +10,16 @@ namespace {
 
 spot_status from_hip(hipError_t e) { return e == hipSuccess ? SPOT_OK : SPOT_ERR_HIP; }
 
+// Decode: any group up to 16 query heads per KV head (the group is the
+// columns of a 16-wide matrix tile).
 bool supported_group(int h_q, int h_kv) {
+  if (h_kv < 1 || h_q < h_kv || h_q % h_kv) return false;
+  return h_q / h_kv <= kMaxGroupSize;
+}
+
+// Prefill: a workgroup takes up to four heads of a group, so groups of
+// 1, 2, 4 or 8.
+bool supported_prefill_group(int h_q, int h_kv) {
   if (h_kv < 1 || h_q < h_kv || h_q % h_kv) return false;
   const int g = h_q / h_kv;
   return g == 1 || g == 2 || g == 4 || g == 8;
@@ -386,7 +395,8 @@ spot_status spot_sparse_prefill(const void* q, const void* k, const void* v, int
                                 void* stream) {
   if (!q || !k || !v || !idx || !count || !out) return SPOT_ERR_NULL;
   if (L < 0 || L % kBlk || batch < 0 || k_max < 1 || h_q < 1 || h_kv < 1) return SPOT_ERR_SHAPE;
-  if (d != 128 || !supported_group(h_q, h_kv) || k_max > 4096) return SPOT_ERR_UNSUPPORTED;
+  if (d != 128 || !supported_prefill_group(h_q, h_kv) || k_max > 4096)
+    return SPOT_ERR_UNSUPPORTED;
   if (!(sm_scale > 0.f) || sm_scale > 3.0e38f) return SPOT_ERR_UNSUPPORTED;
   if ((long long)batch * (L / kBlk) * h_kv > 0x0fffffffLL) return SPOT_ERR_SHAPE;
   if (batch == 0 || L == 0) return SPOT_OK;

@@ -83,18 +83,22 @@ hipError_t launch_decode(bool dense, const void* q, const void* k, const void* v
                      kk, vv, seq_len, idx, count, k_max, h_q, h_kv, l_cap, scale_log2, n_slot,  \
                      ws_o, ws_ml, counters, o16, lse)
 #define SPOT_DECODE_CASE(GG)                 \
-  if (G == GG) {                             \
+  case GG:                                   \
     if (b16)                                 \
       SPOT_DECODE_LAUNCH(GG, false, 16);     \
     else if (dense)                          \
       SPOT_DECODE_LAUNCH(GG, true);          \
     else                                     \
       SPOT_DECODE_LAUNCH(GG, false);         \
+    break;
+  // every group of up to 16 query heads per KV head (the tile's columns)
+  switch (G) {
+    SPOT_DECODE_CASE(1) SPOT_DECODE_CASE(2) SPOT_DECODE_CASE(3) SPOT_DECODE_CASE(4)
+    SPOT_DECODE_CASE(5) SPOT_DECODE_CASE(6) SPOT_DECODE_CASE(7) SPOT_DECODE_CASE(8)
+    SPOT_DECODE_CASE(9) SPOT_DECODE_CASE(10) SPOT_DECODE_CASE(11) SPOT_DECODE_CASE(12)
+    SPOT_DECODE_CASE(13) SPOT_DECODE_CASE(14) SPOT_DECODE_CASE(15) SPOT_DECODE_CASE(16)
+    default: return hipErrorInvalidValue;
   }
-  SPOT_DECODE_CASE(1)
-  SPOT_DECODE_CASE(2)
-  SPOT_DECODE_CASE(4)
-  SPOT_DECODE_CASE(8)
 #undef SPOT_DECODE_CASE
 #undef SPOT_DECODE_LAUNCH
   return hipGetLastError();

@@ -10,6 +10,7 @@ namespace spot {
 
 constexpr int kBlk = 64;      // tokens per KV block
 constexpr int kWave = 64;     // CDNA wavefront width
+constexpr int kMaxGroupSize = 16;   // query heads per KV head of the decode paths
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));

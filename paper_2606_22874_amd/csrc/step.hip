@@ -60,7 +60,6 @@ namespace {
 
 using namespace dec;
 
-constexpr int kStepG = 4;                 // GQA group of the fused path (256 threads)
 constexpr int kScoreRun = 8;              // blocks per scoring call of one wave (the
                                           // stand-alone kernel's run: same code, same bits)
 constexpr int kMaxScorers = 64;           // scoring workgroups per row
@@ -286,18 +285,20 @@ __device__ __forceinline__ void score_run_rt(const StepArgs& a, int row, int nv,
   }
 }
 
-template <int EPT, int SPL>
+template <int EPT, int SPL, int G>
 union StepSmem {
   SelWgSmem<EPT, SPL> sel;
-  DecodeSmem<kStepG> dec;
+  DecodeSmem<G> dec;
 };
 
-template <int EPT, int SPL>
-__global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
-  __shared__ StepSmem<EPT, SPL> sm;
+// G: query heads per KV head (4 or 8), a compile-time constant of the
+// attention core; 4 waves (256 threads) either way.
+template <int EPT, int SPL, int G>
+__global__ __launch_bounds__(64 * kDecWaves, 2) void step_kernel(StepArgs a) {
+  __shared__ StepSmem<EPT, SPL, G> sm;
   // The block list and the per-workgroup flags of the decode layout lie past
   // every field of the selection.
-  static_assert(offsetof(DecodeSmem<kStepG>, ids) >= sizeof(SelWgSmem<EPT, SPL>),
+  static_assert(offsetof(DecodeSmem<G>, ids) >= sizeof(SelWgSmem<EPT, SPL>),
                 "decode list overlaps the selection storage");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wg = blockIdx.x, nwg = gridDim.x;
@@ -318,7 +319,7 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
       nv = nv < 0 ? 0 : (nv > a.nblk ? a.nblk : nv);
       const int per = (a.nblk + n_sc - 1) / n_sc;
       const int jb = c * per, je = min(jb + per, a.nblk);
-      for (int j0 = jb + wave * kScoreRun; j0 < je; j0 += kStepG * kScoreRun)
+      for (int j0 = jb + wave * kScoreRun; j0 < je; j0 += kDecWaves * kScoreRun)
         score_run_rt(a, r, nv, j0, je, lane);
     }
   }
@@ -384,15 +385,21 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
   }
   SPOT_STEP_TS(4);
 
-  const QueryFrag qf = load_query_heads<kStepG>(a.q, b, g, a.h_q);
+  const QueryFrag qf = load_query_heads<G>(a.q, b, g, a.h_q);
   const size_t head_base = ((size_t)b * a.h_kv + g) * (size_t)a.l_cap * kD;
   auto blk_of = [&](int n) { return sm.dec.ids[n]; };
-  const HeadPartial hp = attend_blocks<kStepG>(sm.dec, qf, a.k + head_base, a.v + head_base, sl,
-                                               n_local, blk_of, a.scale_log2, NoHook{}).h[0];
+  const Partials<G> hp = attend_blocks<G>(sm.dec, qf, a.k + head_base, a.v + head_base, sl,
+                                           n_local, blk_of, a.scale_log2, NoHook{});
   SPOT_STEP_TS(5);
-  const size_t bh = (size_t)b * a.h_q + g * kStepG + wave;   // wave w: head w of the group
-  store_coherent(&a.part_o[(bh * n_slot + slot) * kD + 2 * lane], make_float2(hp.o0, hp.o1));
-  if (lane == 0) store_coherent(&a.part_ml[(bh * n_slot + slot) * 2], make_float2(hp.M, hp.L));
+  // wave w holds heads w, w + 4, ... of the group
+#pragma unroll
+  for (int jh = 0; jh < Partials<G>::HPW; ++jh) {
+    const size_t bh = (size_t)b * a.h_q + g * G + wave + kDecWaves * jh;
+    store_coherent(&a.part_o[(bh * n_slot + slot) * kD + 2 * lane],
+                   make_float2(hp.h[jh].o0, hp.h[jh].o1));
+    if (lane == 0)
+      store_coherent(&a.part_ml[(bh * n_slot + slot) * 2], make_float2(hp.h[jh].M, hp.h[jh].L));
+  }
 
   // ---- the last workgroup of the pair to finish merges all slots
   wait_stores();
@@ -408,14 +415,17 @@ __global__ __launch_bounds__(64 * kStepG, 2) void step_kernel(StepArgs a) {
   if (tid == 0) store_rec(&a.pair_cnt[pair], 0u);
   for (int w = 2 * tid; w < (a.nblk + 15) / 16; w += 2 * kSelWG)
     store_rec(reinterpret_cast<uint64_t*>(bmap + w), (uint64_t)0);
-  merge_head(a.part_o, a.part_ml, n_slot, bh, a.out, a.lse, lane);
+#pragma unroll
+  for (int jh = 0; jh < Partials<G>::HPW; ++jh)
+    merge_head(a.part_o, a.part_ml, n_slot, (size_t)b * a.h_q + g * G + wave + kDecWaves * jh,
+               a.out, a.lse, lane);
   SPOT_STEP_TS(7);
 }
 
 // Workgroups of one step kernel that can be resident at once (per CU times
 // the CU count), queried once per device and instantiation.  The value only
 // depends on the device, so concurrent first calls store the same number.
-template <int EPT, int SPL>
+template <int EPT, int SPL, int G>
 int step_capacity() {
   static std::atomic<int> cached[64];
   int dev = 0;
@@ -424,7 +434,7 @@ int step_capacity() {
   if (c > 0) return c;
   int per_cu = 0, cus = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &per_cu, reinterpret_cast<const void*>(&step_kernel<EPT, SPL>), 64 * kStepG, 0) !=
+          &per_cu, reinterpret_cast<const void*>(&step_kernel<EPT, SPL, G>), 64 * kDecWaves, 0) !=
       hipSuccess)
     return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -433,13 +443,13 @@ int step_capacity() {
   return per_cu * cus;
 }
 
-template <int EPT, int SPL>
+template <int EPT, int SPL, int G>
 hipError_t launch_step_t(StepArgs& a, int n_pairs, int n_slot_max, hipStream_t s) {
-  const int cap = step_capacity<EPT, SPL>();
+  const int cap = step_capacity<EPT, SPL, G>();
   if (cap < n_pairs) return hipErrorCooperativeLaunchTooLarge;
   a.n_slot = n_slot_max < cap / n_pairs ? n_slot_max : cap / n_pairs;
   a.slot_div = ((1 << 18) + a.n_slot - 1) / a.n_slot;
-  hipLaunchKernelGGL((step_kernel<EPT, SPL>), dim3(n_pairs * a.n_slot), dim3(64 * kStepG), 0, s,
+  hipLaunchKernelGGL((step_kernel<EPT, SPL, G>), dim3(n_pairs * a.n_slot), dim3(64 * kDecWaves), 0, s,
                      a);
   return hipGetLastError();
 }
@@ -536,7 +546,10 @@ bool step_static_fits(int batch, int h_q, int h_kv, int k_max) {
 void step_force_expiry(int on) { g_force_expire.store(on ? 1 : 0, std::memory_order_relaxed); }
 
 bool step_fusable(int h_q, int h_kv, int nblk, int k_max) {
-  if (h_q != kStepG * h_kv || nblk < 1 || nblk > kRecRow) return false;
+  // groups of 4 or 8 query heads per KV head (the fused kernel is compiled
+  // for those two; other groups run the three stages as separate launches)
+  if (h_kv < 1 || (h_q != 4 * h_kv && h_q != 8 * h_kv) || nblk < 1 || nblk > kRecRow)
+    return false;
   int P = 1;
   const int cap = k_max < nblk ? k_max : nblk;
   while (P < cap) P <<= 1;
@@ -585,7 +598,7 @@ hipError_t launch_decode_step(const void* q_sel, const void* q_scale, int qfmt, 
   a.lse = lse;
   const StepWs L = static_ws ? step_static_layout(batch, h_q, h_kv, k_max)
                             : step_layout(batch, h_q, h_kv, k_max, 0);
-  const int ns = decode_num_splits(batch, h_kv, k_max, kStepG);
+  const int ns = decode_num_splits(batch, h_kv, k_max, h_q / h_kv);
   const int n_slot_max = ns < kMaxSlots ? ns : kMaxSlots;
   char* base = static_cast<char*>(ws);
   a.part_o = reinterpret_cast<float*>(base + L.part);
@@ -606,8 +619,10 @@ hipError_t launch_decode_step(const void* q_sel, const void* q_scale, int qfmt, 
   const int spl = P <= 64 ? 1 : P / 64;
   const int ept = a.nblk <= 256 ? 1 : a.nblk <= 512 ? 2 : a.nblk <= 1024 ? 4
                 : a.nblk <= 2048 ? 8 : 16;
-#define SPOT_STEP_CASE(E, S) \
-  if (ept == E && spl == S) return launch_step_t<E, S>(a, n_pairs, n_slot_max, s);
+#define SPOT_STEP_CASE(E, S)                                           \
+  if (ept == E && spl == S)                                            \
+    return h_q == 8 * h_kv ? launch_step_t<E, S, 8>(a, n_pairs, n_slot_max, s) \
+                           : launch_step_t<E, S, 4>(a, n_pairs, n_slot_max, s);
 #define SPOT_STEP_E(E) SPOT_STEP_CASE(E, 1) SPOT_STEP_CASE(E, 2) SPOT_STEP_CASE(E, 4) \
   SPOT_STEP_CASE(E, 8)
   SPOT_STEP_E(1)

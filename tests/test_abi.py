@@ -172,7 +172,9 @@ def test_validation_errors_before_launch(lib):
     # decode: d != 128, bad GQA group, l_cap not a multiple of 64, no workspace
     dec = lib.spot_sparse_decode
     assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 32, 8, 64, 4096, 0.1, nz, None, nz, 1 << 20, None) == 3
-    assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 24, 8, 128, 4096, 0.1, nz, None, nz, 1 << 20, None) == 3
+    # groups: more than 16 query heads per KV head, or h_q not a multiple of h_kv
+    assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 136, 8, 128, 4096, 0.1, nz, None, nz, 1 << 20, None) == 3
+    assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 20, 8, 128, 4096, 0.1, nz, None, nz, 1 << 20, None) == 3
     assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 32, 8, 128, 4000, 0.1, nz, None, nz, 1 << 20, None) == 2
     assert dec(nz, nz, nz, nz, nz, nz, 4, 1, 32, 8, 128, 4096, 0.1, nz, None, nz, 0, None) == 5
     assert dec(nz, nz, nz, nz, None, nz, 4, 1, 32, 8, 128, 4096, 0.1, nz, None, nz, 1 << 20, None) == 1
@@ -185,6 +187,7 @@ def test_validation_errors_before_launch(lib):
     assert pre(nz, nz, nz, 100, nz, nz, 4, 1, 64, 8, 128, 0.1, nz, None, None) == 2
     assert pre(nz, nz, nz, 128, nz, nz, 4, 1, 64, 8, 96, 0.1, nz, None, None) == 3
     assert pre(nz, nz, nz, 128, nz, nz, 5000, 1, 64, 8, 128, 0.1, nz, None, None) == 3
+    assert pre(nz, nz, nz, 128, nz, nz, 4, 1, 24, 8, 128, 0.1, nz, None, None) == 3   # group 3
     for bad_scale in (0.0, -0.1, float("nan"), float("inf")):
         assert pre(nz, nz, nz, 128, nz, nz, 4, 1, 64, 8, 128, bad_scale, nz, None, None) == 3
     # fused step: (q_sel, w, k_sel, k_scale, kfmt, h_s, d_s, n_valid, top_p, k_max, k_min,

@@ -297,6 +297,35 @@ def test_sparse_decode_ragged_and_bad_ids():
     assert torch.all(out_g.float() == 0) and torch.all(torch.isinf(lse_g))
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(6, 2), (10, 2), (24, 4), (32, 2), (48, 4)])
+def test_sparse_decode_group_sizes(Hq, Hkv):
+    """Groups other than 1, 2, 4, 8 query heads per KV head (3, 5, 6, 16, 12):
+    the group's heads are the columns of the 16-wide matrix tiles."""
+    B, L, d = 3, 4096, 128
+    print(f"[decode] Hq={Hq} Hkv={Hkv}", flush=True)
+    q, k, v = synth._backbone_decode(960 + Hq, B, L, Hq, Hkv, d)
+    seq_len = np.array([4096, 2500, 65], np.int32)
+    rng = np.random.default_rng(Hq)
+    k_max = 40
+    idx = np.full((B, k_max), -1, np.int32)
+    cnt = np.zeros(B, np.int32)
+    for b in range(B):
+        nv = int((seq_len[b] + 63) // 64)
+        row = rng.permutation(nv)[: min(nv, 37)]
+        idx[b, :len(row)] = row
+        cnt[b] = len(row)
+    scale = 1 / np.sqrt(d)
+    out_o, lse_o = oracle.sparse_decode(q, k, v, seq_len, idx, cnt, scale)
+    out_g, lse_g = spot.sparse_decode(bf(q), bf(k), bf(v), i32(seq_len), i32(idx), i32(cnt),
+                                      scale)
+    torch.cuda.synchronize()
+    assert_out_close(out_g, lse_g, out_o, lse_o)
+    out_o, lse_o = oracle.dense_decode(q, k, v, seq_len, scale)
+    out_g, lse_g = spot.dense_decode(bf(q), bf(k), bf(v), i32(seq_len), scale)
+    torch.cuda.synchronize()
+    assert_out_close(out_g, lse_g, out_o, lse_o)
+
+
 @pytest.mark.parametrize("cfg,B,L", [(1, None, None), (2, 2, 8192), (2, 3, 4160)])
 def test_dense_decode_parity(cfg, B, L):
     kw = {} if B is None else {"B": B, "L": L, "seq_len": tuple([L, L - 37, 64][:B])}

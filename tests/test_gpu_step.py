@@ -270,17 +270,32 @@ def test_step_ragged_sequences():
     assert_same(sep, fus)
 
 
-def test_step_fallback_shapes():
-    """Shapes outside the fused path (GQA group 8, 8192 blocks) run the three
-    stages one after the other and give the separate calls' results."""
-    wl = workload(2, B=2, L=8192)
+@pytest.mark.parametrize("G", [1, 2, 5, 8, 16])
+def test_step_group_sizes(G):
+    """spot_decode_step at other GQA group sizes (G query heads per KV head,
+    up to the 16 columns of a matrix tile): G = 8 (64 / 8 heads) runs fused,
+    the others as three launches; the separate calls' results, and the
+    attention outputs against the oracle on the selected set."""
+    wl = workload(2, B=2, L=8192, seq_len=(8192, 5001))
     x = inputs(wl, "bf16")
-    # GQA group 8: 64 query heads over the same 8 KV heads.
-    x8 = dict(x, q=bf(synth.normal_bf16(77, 1, (wl.B, 64, wl.d))))
-    sep = separate(x8, wl)
-    fus = fused(x8, wl)
+    q = synth.normal_bf16(70 + G, 1, (wl.B, 8 * G, wl.d))
+    xg = dict(x, q=bf(q))
+    print(f"[step] group {G}", flush=True)
+    sep = separate(xg, wl)
+    fus = fused(xg, wl)
     torch.cuda.synchronize()
     assert_same(sep, fus)
+    idx, cnt = fus[1].cpu().numpy(), fus[2].cpu().numpy()
+    out_o, lse_o = oracle.sparse_decode(q, wl.k, wl.v, wl.seq_len, idx, cnt, wl.sm_scale)
+    g = fus[4].float().cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(g - out_o)) <= 2e-2
+    assert np.linalg.norm(g - out_o) / np.linalg.norm(out_o) <= 1e-2
+    assert np.max(np.abs(fus[5].cpu().numpy() - lse_o)) <= 2e-3
+
+
+def test_step_fallback_shapes():
+    """Shapes outside the fused path (8192 blocks) run the three stages one
+    after the other and give the separate calls' results."""
     # 8192 blocks (L = 524288) exceed the fused selection core: k_max 256.
     wl_long = synth.decode_config(3, B=1, L=524288, backbone=False)
     rule = Rule(0.95, 256, 0, 1, 2)
