@@ -340,6 +340,33 @@ def main():
             log(f"[bench] {fmt} selector cache and queries: {qqms * 1e3:.1f} us/step")
         result["config"]["quantized_selector"] = quant
 
+    if not args.no_extra and args.fmt == "bf16":
+        # The same layer with 64 query heads over the 8 KV heads (GQA group 8,
+        # the Qwen3-32B shape): the fused step compiled for groups of 8.
+        hq8 = 8 * Hkv
+        q8 = bf(synth.normal_bf16(SEED_TOKENS + 8, 1, (B, hq8, d)))
+        out8 = torch.empty((B, hq8, d), dtype=torch.bfloat16, device=dev)
+        lse8 = torch.empty((B, hq8), dtype=torch.float32, device=dev)
+        ws8 = spot.step_workspace(B, hq8, Hkv, d, rule.k_max, dev)
+
+        def step8(c):
+            k, v, ks, sc = copies[c % len(copies)]
+            spot.spot_decode_step(q_sel, w, ks, sc, args.fmt, wl.Hs, wl.ds, n_valid, rule.top_p,
+                                  rule.k_max, rule.k_min, rule.n_sink, rule.n_recent, q8, k, v,
+                                  seq_len, B, hq8, Hkv, d, L, wl.sm_scale, scores, idx, cnt, mass,
+                                  out8, lse8, ws8, stream)
+
+        for i in range(args.warmup):
+            step8(i)
+        g8ms = timed(step8, args.steps)
+        result["config"]["group8_step"] = {
+            "workload": f"decode L={L} B={B}, 64 q / 8 kv heads (GQA group 8), selector and "
+                        "rule as above; spot_decode_step, one launch",
+            "us_per_step": round(g8ms * 1e3, 2), "steps_per_s": round(1e3 / g8ms, 1),
+            "bytes_per_step": step_bytes,
+            "hbm_frac": round(step_bytes / (g8ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"[bench] group-8 step (64 q heads): {g8ms * 1e3:.1f} us/step")
+
     if not args.no_dense:
         wsd = spot.decode_workspace(B, Hq, Hkv, d, nblk, dev)
 
