@@ -48,7 +48,6 @@ namespace dec {
 
 
 constexpr int kD = 128;
-constexpr int kKRow = kD + 8;    // padded K row in LDS (272 bytes)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMaxIds = 512;     // max list entries per workgroup
 static_assert(kMaxIds % 4 == 0, "16-token blocks pad the list to whole virtual blocks");
@@ -513,7 +512,7 @@ struct NoHook {
 
 // Workgroup (pair, slot): slot s takes its share of the pair's block list
 // (from `list`; DENSE: the s-th contiguous run of all valid blocks); wave w
-// processes token rows [w*T, (w+1)*T) of each of those blocks.  The split
+// processes token rows [16w, 16w+16) of each of those blocks.  The split
 // partials go to the workspace; the last workgroup of the pair to finish
 // (device-scope counter) merges them.  Returns true in that workgroup.
 template <int G, bool DENSE, class List, int SB = kBlk>
