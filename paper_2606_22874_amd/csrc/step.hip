@@ -545,10 +545,18 @@ bool step_static_fits(int batch, int h_q, int h_kv, int k_max) {
 
 void step_force_expiry(int on) { g_force_expire.store(on ? 1 : 0, std::memory_order_relaxed); }
 
+// Groups the fused kernel is compiled for: 4 and 8 query heads per KV head
+// (a build that defines SPOT_STEP_GROUP4_ONLY, the phase-stamping timeline
+// build, only 4); other groups run the three stages as separate launches.
+#ifdef SPOT_STEP_GROUP4_ONLY
+constexpr bool kStepGroup8 = false;
+#else
+constexpr bool kStepGroup8 = true;
+#endif
+
 bool step_fusable(int h_q, int h_kv, int nblk, int k_max) {
-  // groups of 4 or 8 query heads per KV head (the fused kernel is compiled
-  // for those two; other groups run the three stages as separate launches)
-  if (h_kv < 1 || (h_q != 4 * h_kv && h_q != 8 * h_kv) || nblk < 1 || nblk > kRecRow)
+  if (h_kv < 1 || (h_q != 4 * h_kv && !(kStepGroup8 && h_q == 8 * h_kv)) || nblk < 1 ||
+      nblk > kRecRow)
     return false;
   int P = 1;
   const int cap = k_max < nblk ? k_max : nblk;
@@ -619,10 +627,15 @@ hipError_t launch_decode_step(const void* q_sel, const void* q_scale, int qfmt, 
   const int spl = P <= 64 ? 1 : P / 64;
   const int ept = a.nblk <= 256 ? 1 : a.nblk <= 512 ? 2 : a.nblk <= 1024 ? 4
                 : a.nblk <= 2048 ? 8 : 16;
-#define SPOT_STEP_CASE(E, S)                                           \
-  if (ept == E && spl == S)                                            \
-    return h_q == 8 * h_kv ? launch_step_t<E, S, 8>(a, n_pairs, n_slot_max, s) \
+#ifdef SPOT_STEP_GROUP4_ONLY
+#define SPOT_STEP_CASE(E, S) \
+  if (ept == E && spl == S) return launch_step_t<E, S, 4>(a, n_pairs, n_slot_max, s);
+#else
+#define SPOT_STEP_CASE(E, S)                                                         \
+  if (ept == E && spl == S)                                                          \
+    return h_q == 8 * h_kv ? launch_step_t<E, S, 8>(a, n_pairs, n_slot_max, s)       \
                            : launch_step_t<E, S, 4>(a, n_pairs, n_slot_max, s);
+#endif
 #define SPOT_STEP_E(E) SPOT_STEP_CASE(E, 1) SPOT_STEP_CASE(E, 2) SPOT_STEP_CASE(E, 4) \
   SPOT_STEP_CASE(E, 8)
   SPOT_STEP_E(1)
