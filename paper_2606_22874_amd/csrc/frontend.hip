@@ -12,13 +12,21 @@
 // reading the weights (2 x 512 x d_model BF16 + the small W_w): each
 // workgroup owns one task -- two output rows of W_q or W_k that the rotation
 // pairs (or two neighbouring non-rotary rows), the first tasks also two rows
-// of W_w -- and its 8 waves split d_model in 512-element chunks, so every
-// weight byte is loaded once with all of a workgroup's loads in flight
-// together, and the 512 workgroups are resident at once.  Hidden
-// rows are re-read from L2 by every task.  Partial dots meet in LDS and are
-// summed in a fixed order (deterministic); one lane per row finishes.  The
+// of W_w -- and its 4 waves split d_model in passes of 4 x CH chunks of 512
+// elements (one pass at d_model = 4096), every chunk's weight and hidden
+// loads issued before the first product, so every weight byte is loaded once
+// with all of a wave's loads in flight together, and the 512 workgroups are
+// resident at once (a grid row per pass of RP hidden rows).  Hidden rows are
+// re-read from L2 by every task.  Partial
+// dots meet in LDS and are summed in a fixed order (deterministic); one lane
+// per row finishes.  The rows' positions (and lengths) are the first loads
+// of a pass, so that nothing after them waits for a late scalar load; the
 // rotation angle only needs the position and the pair's frequency (FP64,
 // from the host), so it is formed while the weight loads are in flight.
+// (Against 8 waves of one chunk, with the positions read where they are
+// used and loads behind branches, this takes 3.8 instead of 4.9 us for the
+// B = 4, d_model = 4096 decode projection, and 4.5 instead of 6.0 us with
+// the pooling, replayed in a HIP graph.)
 //
 // Pooled sums (pool_kernel, and project_kernel with POOL): each 16-token
 // quarter of the block is summed as a pairwise tree -- (t0 + t1) + (t2 + t3)
@@ -34,7 +42,7 @@
 namespace spot {
 namespace {
 
-constexpr int kProjWaves = 8;
+constexpr int kProjWaves = 4;
 constexpr int kMaxRopePairs = 64;
 
 // base^(-2i / rope_dim) for the rotary pairs i < rope_dim / 2 (FP64).
@@ -75,125 +83,141 @@ __device__ __forceinline__ float dot8_bf16(const u32x4& a, const u32x4& b, float
 
 // Tasks: n_out pairs of W_q / W_k rows (n_out/2 each); the first ceil(h_s/2)
 // tasks also take a pair of W_w rows, so that the grid (n_out = 512
-// workgroups of 8 waves) fits the device at once.  Pair p of one head (d_s/2 pairs):
+// workgroups of 4 waves) fits the device at once.  Pair p of one head (d_s/2 pairs):
 // p < rope_dim/2 -> dims (p, p + rope_dim/2), rotated; otherwise dims
 // (rope_dim + 2(p - rope_dim/2), +1), not rotated.
-// RP hidden rows per pass (4, 8 or 16): every pass loads its RP rows
+// RP hidden rows per row pass (4, 8 or 16): every pass loads its RP rows
 // without branches (rows past the end re-read the last row, in cache), so
-// all of a wave's loads are in flight together.
+// all of a wave's loads are in flight together.  CH chunks of 512 elements
+// per wave and d pass; lanes past d_model load nothing and add zeros.
 // POOL (one row per sequence): a W_k task also pools its two dims of the
-// block each row's key lands in.  Wave w holds (row, dim) pairs w, w + 8, ..
-// of the pass with lane = token of the block: the other tokens' values are
-// loaded before the weights (and waited for only at the end), the new key's
-// value joins its lane, and each pair is summed in pool_kernel's order
-// exactly (16-token quarters in token order, then the quarters in order;
-// tokens at or past the block's count hold -0.0, the exact identity of
-// addition), so the pooled key is the one spot_selector_pool would compute
-// after the append.
-template <int RP, bool POOL>
+// block each row's key lands in.  Wave w gathers rows w, w + 4, .. of the
+// pass, both dims (one 4-byte load when they are neighbours), with lane =
+// token of the block: the loads go out after the first d pass's weight
+// loads and are waited for only at the end; the new key's value joins its
+// lane, and each dim is summed in pool_kernel's order exactly (16-token
+// quarters in token order, then the quarters in order; tokens at or past
+// the block's count hold -0.0, the exact identity of addition), so the
+// pooled key is the one spot_selector_pool would compute after the append.
+template <int RP, int CH, bool POOL>
 __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
     const uint16_t* __restrict__ h, const uint16_t* __restrict__ w_q,
     const uint16_t* __restrict__ w_k, const uint16_t* __restrict__ w_w,
     const int32_t* __restrict__ pos, int rows, int d_model, int h_s, int d_s, int rope_dim,
     RopeFreq freq, uint16_t* __restrict__ q_out, float* __restrict__ w_out,
     uint16_t* __restrict__ k_cache, int rows_per_seq, int l_cap,
-    uint16_t* __restrict__ k_pool, const int32_t* __restrict__ seq_len) {
+    uint16_t* __restrict__ k_pool, const int32_t* __restrict__ seq_len, int row_base) {
+  static_assert(RP >= kProjWaves && (RP & (RP - 1)) == 0, "RP: a power of two >= the waves");
   __shared__ float part[kProjWaves][RP][4];   // [wave][row][row a, b, W_w c, d]
   __shared__ float pool_new[POOL ? RP : 1][2];   // the new key's value, [row][dim a/b]
-  constexpr int kPairs = POOL ? (2 * RP + kProjWaves - 1) / kProjWaves : 1;   // per wave
+  constexpr int kRows = POOL ? RP / kProjWaves : 1;   // rows gathered per wave
+  constexpr int kPass = kProjWaves * 512 * CH;        // d elements per pass
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // Row pass blockIdx.y (RP rows from row_base + RP * blockIdx.y).
+  // 1. every lane: position and length (the position again without
+  // seq_len) of row r0 + lane % RP (the last row for lanes past the end),
+  // the first loads; lane r of wave 0 finishes row r0 + r, wave w gathers
+  // rows r0 + w + 4m.  Every load is unconditional (addresses clamped into
+  // their buffers, unused values masked where they are used), so that no
+  // branch join makes a wave wait for a load before it issues the next ones.
+  const int r0 = row_base + (int)blockIdx.y * RP;
+  const int nr = min(RP, rows - r0);
+  const int lr = r0 + min(lane & (RP - 1), nr - 1);
+  const int pos_l = pos[lr];
+  const int len_l = (seq_len ? seq_len : pos)[lr];
+
+  // This task's two weight rows and where their results go (dims a, b of
+  // q or k), plus W_w rows c, d for the first tasks.  n_out (512) and the
+  // d_s / 2 pairs of a head are powers of two.
   const int n_out = h_s * d_s;
   const int task = blockIdx.x;
   const int half = rope_dim / 2;
-
-  // This task's two weight rows and where their results go (dims a, b of
-  // q or k), plus W_w rows c, d for the first tasks.
-  int dim_a = 0, dim_b = 0, head = 0;
-  bool rotate = false;
-  const int kind = task < n_out / 2 ? 0 : 1;       // 0: q, 1: k
-  {
-    const int p = task % (n_out / 2);
-    head = p / (d_s / 2);
-    const int pp = p % (d_s / 2);
-    if (pp < half) {
-      dim_a = pp;
-      dim_b = pp + half;
-      rotate = true;
-    } else {
-      dim_a = rope_dim + 2 * (pp - half);
-      dim_b = dim_a + 1;
-    }
-  }
+  // 0: q, 1: k; with pooling the k tasks, which also gather and pool, are
+  // dispatched first
+  const int kind = (task < (n_out >> 1)) == POOL ? 1 : 0;
+  const int p_task = task & ((n_out >> 1) - 1);
+  const int head = p_task >> __builtin_ctz(d_s >> 1);
+  const int pp = p_task & ((d_s >> 1) - 1);
+  const bool rotate = pp < half;
+  const int dim_a = rotate ? pp : rope_dim + 2 * (pp - half);
+  const int dim_b = rotate ? pp + half : dim_a + 1;
+  const bool pool_task = POOL && kind == 1;
   const uint16_t* wmat = kind == 0 ? w_q : w_k;
   const uint16_t* wa = wmat + (size_t)(head * d_s + dim_a) * d_model;
   const uint16_t* wb = wmat + (size_t)(head * d_s + dim_b) * d_model;
-  const bool with_w = task < (h_s + 1) / 2;
-  const int rc = 2 * task, rd = min(rc + 1, h_s - 1);
+  // W_w rows ride on the first q tasks (with pooling, the k tasks are the
+  // heavier ones)
+  const int wt = task - (POOL ? n_out >> 1 : 0);
+  const bool with_w = wt >= 0 && wt < (h_s + 1) / 2;
+  const int rc = with_w ? 2 * wt : 0, rd = min(rc + 1, h_s - 1);
   const uint16_t* wc = w_w + (size_t)(with_w ? rc : 0) * d_model;
   const uint16_t* wd = w_w + (size_t)(with_w ? rd : 0) * d_model;
-  for (int r0 = 0; r0 < rows; r0 += RP) {
-    const int nr = min(RP, rows - r0);
-    // 1. the finishing lane's (row r0 + lane) position, then the first
-    // chunk's weight and hidden loads
-    int p_row = 0;
-    if (wave == 0 && lane < nr) p_row = pos[r0 + lane];
-    int c = wave * 512 + lane * 8;
-    bool have = c < d_model;
-    u32x4 a, b, cw, dw, x[RP];
-    auto load_chunk = [&]() {
-      a = *reinterpret_cast<const u32x4*>(wa + c);
-      b = *reinterpret_cast<const u32x4*>(wb + c);
-      if (with_w) {
-        cw = *reinterpret_cast<const u32x4*>(wc + c);
-        dw = *reinterpret_cast<const u32x4*>(wd + c);
-      }
-#pragma unroll
-      for (int i = 0; i < RP; ++i)
-        x[i] = *reinterpret_cast<const u32x4*>(h + (size_t)min(r0 + i, rows - 1) * d_model + c);
-    };
-    if (have) load_chunk();
-    // 2. the rotation of the finishing lane's row: angle pos * freq in FP64,
-    // reduced to [-pi, pi] in FP64 (two-part 2 pi), sin and cos in FP32
-    float s_rot = 0.f, c_rot = 1.f;
-    if (rotate && wave == 0 && lane < nr) {
-      const double theta = (double)p_row * freq.f[dim_a];
-      const double k = rint(theta * 0.15915494309189535);   // 1 / (2 pi)
-      double red = fma(-k, 6.283185307179586, theta);       // 2 pi, high part
-      red = fma(-k, 2.4492935982947064e-16, red);           // 2 pi, low part
-      sincosf((float)red, &s_rot, &c_rot);
-    }
-    // 3. for pooling, the block's other tokens: their waits come later (the
-    // pooling positions are uniform scalar loads, whose wait does not hold
-    // up the vector loads above)
-    float pv[kPairs];   // POOL, W_k task: pair wave + 8m's value at token `lane`
-#pragma unroll
-    for (int m = 0; m < kPairs; ++m) {
-      pv[m] = -0.f;
-      const int pr = wave + kProjWaves * m, i = pr >> 1, sel = pr & 1;
-      if (POOL && kind == 1 && i < nr) {
-        const int r = r0 + i, p = pos[r];
-        if (p >= 0 && p < l_cap && lane != p % kBlk)
-          pv[m] = bf16_lo(k_cache[((size_t)r * l_cap + p / kBlk * kBlk + lane) * n_out +
-                                  head * d_s + (sel ? dim_b : dim_a)]);
-      }
-    }
-    // 4. the dot products, chunk by chunk
+  {
+    // the finishing lane's sequence
+    const int seq_l = rows_per_seq == 1 ? lr : lr / rows_per_seq;
     float acc_a[RP], acc_b[RP], acc_c[RP], acc_d[RP];
 #pragma unroll
     for (int i = 0; i < RP; ++i) acc_a[i] = acc_b[i] = acc_c[i] = acc_d[i] = 0.f;
-    while (have) {
+    uint16_t pga[kRows], pgb[kRows];   // POOL, W_k task: row w + 4m's dims at token `lane`
+    float s_rot = 0.f, c_rot = 1.f;
+    for (int c0 = 0; c0 < d_model; c0 += kPass) {
+      // 2. this pass's weight and hidden loads, all in flight together
+      // (chunks past d_model re-read the last 8 elements and are skipped)
+      u32x4 a[CH], b[CH], cw[CH], dw[CH], x[CH][RP];
 #pragma unroll
-      for (int i = 0; i < RP; ++i) {
-        acc_a[i] = dot8_bf16(a, x[i], acc_a[i]);
-        acc_b[i] = dot8_bf16(b, x[i], acc_b[i]);
+      for (int cc = 0; cc < CH; ++cc) {
+        const int c = min(c0 + (cc * kProjWaves + wave) * 512 + lane * 8, d_model - 8);
+        a[cc] = *reinterpret_cast<const u32x4*>(wa + c);
+        b[cc] = *reinterpret_cast<const u32x4*>(wb + c);
         if (with_w) {
-          acc_c[i] = dot8_bf16(cw, x[i], acc_c[i]);
-          acc_d[i] = dot8_bf16(dw, x[i], acc_d[i]);
+          cw[cc] = *reinterpret_cast<const u32x4*>(wc + c);
+          dw[cc] = *reinterpret_cast<const u32x4*>(wd + c);
+        }
+#pragma unroll
+        for (int i = 0; i < RP; ++i)
+          x[cc][i] = *reinterpret_cast<const u32x4*>(
+              h + (size_t)min(r0 + i, rows - 1) * d_model + c);
+      }
+      if (c0 == 0) {
+        // 3. pooling: the block's tokens at both dims (waited for at the
+        // end); tasks and rows without pooling read one cache word
+#pragma unroll
+        for (int m = 0; m < kRows; ++m) {
+          const int i = wave + kProjWaves * m;
+          const int p = __builtin_amdgcn_readlane(pos_l, min(i, nr - 1));
+          const bool live = pool_task && i < nr && p >= 0 && p < l_cap;
+          const uint16_t* src =
+              live ? k_cache + ((size_t)(r0 + i) * l_cap + p / kBlk * kBlk + lane) * n_out +
+                         head * d_s
+                   : k_cache;
+          pga[m] = src[dim_a];
+          pgb[m] = src[dim_b];
+        }
+        // 4. the rotation of the finishing lane's row: angle pos * freq in
+        // FP64, reduced to [-pi, pi] in FP64 (two-part 2 pi), sin and cos in
+        // FP32
+        if (rotate && wave == 0 && lane < nr) {
+          const double theta = (double)pos_l * freq.f[dim_a];
+          const double k = rint(theta * 0.15915494309189535);   // 1 / (2 pi)
+          double red = fma(-k, 6.283185307179586, theta);       // 2 pi, high part
+          red = fma(-k, 2.4492935982947064e-16, red);           // 2 pi, low part
+          sincosf((float)red, &s_rot, &c_rot);
         }
       }
-      c += kProjWaves * 512;
-      have = c < d_model;
-      if (have) load_chunk();
+      // 5. the dot products of this pass
+#pragma unroll
+      for (int cc = 0; cc < CH; ++cc) {
+        if (c0 + (cc * kProjWaves + wave) * 512 + lane * 8 >= d_model) continue;
+#pragma unroll
+        for (int i = 0; i < RP; ++i) {
+          acc_a[i] = dot8_bf16(a[cc], x[cc][i], acc_a[i]);
+          acc_b[i] = dot8_bf16(b[cc], x[cc][i], acc_b[i]);
+          if (with_w) {
+            acc_c[i] = dot8_bf16(cw[cc], x[cc][i], acc_c[i]);
+            acc_d[i] = dot8_bf16(dw[cc], x[cc][i], acc_d[i]);
+          }
+        }
+      }
     }
 #pragma unroll
     for (int i = 0; i < RP; ++i) {
@@ -230,7 +254,7 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
         if (rc + 1 < h_s) w_out[(size_t)r * h_s + rc + 1] = D;
       }
       {
-        const int p = p_row;
+        const int p = pos_l;
         if (rotate) {
           const float A2 = A * c_rot - B * s_rot;
           const float B2 = B * c_rot + A * s_rot;
@@ -242,47 +266,50 @@ __global__ __launch_bounds__(kProjWaves * 64) void project_kernel(
           dst = q_out + (size_t)r * n_out;
         } else {
           dst = (p >= 0 && p < l_cap)
-                    ? k_cache + ((size_t)(r / rows_per_seq) * l_cap + p) * n_out
+                    ? k_cache + ((size_t)seq_l * l_cap + p) * n_out
                     : nullptr;
         }
         if (dst) {
           const uint16_t ha = f32_to_bf16_rne(A), hb = f32_to_bf16_rne(B);
           dst[head * d_s + dim_a] = ha;
           dst[head * d_s + dim_b] = hb;
-          if (POOL && kind == 1) {
+          if (pool_task) {
             pool_new[lane][0] = bf16_lo(ha);
             pool_new[lane][1] = bf16_lo(hb);
           }
         }
       }
     }
-    __syncthreads();   // part[] is reused by the next pass; pool_new is complete
-    if (POOL && kind == 1) {
+    if (pool_task) __syncthreads();   // pool_new is complete
+    if (pool_task) {
 #pragma unroll
-      for (int m = 0; m < kPairs; ++m) {
-        const int pr = wave + kProjWaves * m, i = pr >> 1, sel = pr & 1;
+      for (int m = 0; m < kRows; ++m) {
+        const int i = wave + kProjWaves * m;
         if (i >= nr) continue;
-        const int r = r0 + i, p = pos[r];
-        int len = seq_len ? seq_len[r] : p + 1;
+        const int p = __builtin_amdgcn_readlane(pos_l, i);
+        int len = seq_len ? __builtin_amdgcn_readlane(len_l, i) : p + 1;
         len = len > l_cap ? l_cap : len;
         const int lo = p / kBlk * kBlk, n = min(len - lo, kBlk);
         if (p < 0 || p >= l_cap || n <= 0) continue;
-        float x = lane == p % kBlk ? pool_new[i][sel] : pv[m];
-        if (lane >= n) x = -0.f;
-        x = quarter_tree_sum(x);
-        float q4[4];
+        const int r = r0 + i;
 #pragma unroll
-        for (int qq = 0; qq < 4; ++qq)
-          q4[qq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), qq * 16));
-        if (lane == 0) {
-          const float v = ((q4[0] + q4[1]) + q4[2]) + q4[3];
-          const int nblk = l_cap / kBlk;
-          k_pool[((size_t)r * nblk + p / kBlk) * n_out + head * d_s + (sel ? dim_b : dim_a)] =
-              f32_to_bf16_rne(v / (float)n);
+        for (int sel = 0; sel < 2; ++sel) {
+          float x = lane == p % kBlk ? pool_new[i][sel] : bf16_lo(sel ? pgb[m] : pga[m]);
+          if (lane >= n) x = -0.f;
+          x = quarter_tree_sum(x);
+          float q4[4];
+#pragma unroll
+          for (int qq = 0; qq < 4; ++qq)
+            q4[qq] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), qq * 16));
+          if (lane == 0) {
+            const float v = ((q4[0] + q4[1]) + q4[2]) + q4[3];
+            const int nblk = l_cap / kBlk;
+            k_pool[((size_t)r * nblk + p / kBlk) * n_out + head * d_s + (sel ? dim_b : dim_a)] =
+                f32_to_bf16_rne(v / (float)n);
+          }
         }
       }
     }
-    if (POOL) __syncthreads();   // pool_new is reused by the next pass
   }
 }
 
@@ -359,27 +386,35 @@ hipError_t launch_selector_project(const void* h, const void* w_q, const void* w
   const double lb = std::log2((double)rope_base);
   for (int i = 0; i < kMaxRopePairs; ++i)
     freq.f[i] = i < rope_dim / 2 ? std::exp2(-2.0 * i / rope_dim * lb) : 0.0;
-  auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, dim3(tasks), dim3(kProjWaves * 64), 0, s,
-                       static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w_q),
-                       static_cast<const uint16_t*>(w_k), static_cast<const uint16_t*>(w_w), pos,
-                       rows, d_model, h_s, d_s, rope_dim, freq,
-                       static_cast<uint16_t*>(q_out), w_out, static_cast<uint16_t*>(k_cache),
-                       rows_per_seq, l_cap, static_cast<uint16_t*>(k_pool), seq_len);
-  };
-  if (k_pool) {   // one row per sequence (the caller checks rows_per_seq == 1)
-    if (rows <= 4)
-      go(project_kernel<4, true>);
-    else if (rows <= 8)
-      go(project_kernel<8, true>);
-    else
-      go(project_kernel<16, true>);
-  } else if (rows <= 4) {
-    go(project_kernel<4, false>);
-  } else if (rows <= 8) {
-    go(project_kernel<8, false>);
-  } else {
-    go(project_kernel<16, false>);
+  const int rp = rows <= 4 ? 4 : (rows <= 8 ? 8 : 16);
+  const int passes = (rows + rp - 1) / rp;
+  // one row pass per workgroup row; more than 65535 passes take more launches
+  for (int p0 = 0; p0 < passes; p0 += 65535) {
+    const dim3 grid(tasks, passes - p0 < 65535 ? passes - p0 : 65535);
+    auto go = [&](auto kern) {
+      hipLaunchKernelGGL(kern, grid, dim3(kProjWaves * 64), 0, s,
+                         static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w_q),
+                         static_cast<const uint16_t*>(w_k), static_cast<const uint16_t*>(w_w),
+                         pos, rows, d_model, h_s, d_s, rope_dim, freq,
+                         static_cast<uint16_t*>(q_out), w_out, static_cast<uint16_t*>(k_cache),
+                         rows_per_seq, l_cap, static_cast<uint16_t*>(k_pool), seq_len, p0 * rp);
+    };
+    if (k_pool) {   // one row per sequence (the caller checks rows_per_seq == 1)
+      if (rp == 4)
+        go(project_kernel<4, 2, true>);
+      else if (rp == 8)
+        go(project_kernel<8, 2, true>);
+      else
+        go(project_kernel<16, 1, true>);
+    } else if (rp == 4) {
+      go(project_kernel<4, 2, false>);
+    } else if (rp == 8) {
+      go(project_kernel<8, 2, false>);
+    } else {
+      go(project_kernel<16, 1, false>);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
   return hipGetLastError();
 }
