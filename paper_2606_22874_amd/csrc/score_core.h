@@ -195,8 +195,9 @@ struct KeyLoad<SPOT_KFMT_MXFP8_G32> {
 // block; rec_copies runs of them rec_stride words apart) also receives
 // rec_word() of each valid block's score in every run, stored at device
 // scope (readers in other workgroups of the same launch poll these words:
-// zero means not written yet).  Returns, in lane u < U, the score of
-// block j0 + u (-inf in the other lanes and past jend).
+// zero means not written yet).  A null `scores` stores no scores.  Returns,
+// in lane u < U, the score of block j0 + u (-inf in the other lanes and past
+// jend).
 // This lane's 8 query elements of row `row` (head lane / LPH, dims
 // 8*(lane % LPH) ..).  BF16 and MX queries: BF16 bits in qraw and floats in
 // qf, qsc = 1 (MX codes -- E2M1 or E4M3, one E8M0 scale per 32 -- times a
@@ -256,6 +257,43 @@ __device__ __forceinline__ void load_query(const uint8_t* __restrict__ q,
   }
 }
 
+// Butterfly step of the score reductions: x + (x of lane l ^ OFF) in every
+// lane (both lanes of a pair form the same sum, addition being commutative).
+// Without LDS: quad permutes for 1 and 2; for 4 and 8 the half-row and row
+// mirrors, whose partner lane holds the same value as lane l ^ OFF once the
+// groups of OFF lanes are summed; the lane-swap instructions for 16 and 32.
+template <int OFF>
+__device__ __forceinline__ float xor_add(float x) {
+#pragma clang fp contract(off)
+  if constexpr (OFF == 1) {
+    return x + dpp_f<kDppQuadXor1>(x);
+  } else if constexpr (OFF == 2) {
+    return x + dpp_f<kDppQuadXor2>(x);
+  } else if constexpr (OFF == 4) {
+    return x + dpp_f<kDppHalfMirror>(x);
+  } else if constexpr (OFF == 8) {
+    return x + dpp_f<kDppMirror>(x);
+  } else if constexpr (OFF == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  } else {
+    static_assert(OFF == 32, "lane offsets 1 .. 32");
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+}
+// Sum over aligned groups of END lanes, given groups of FROM lanes already
+// summed (every lane of a group holding the same value).
+template <int FROM, int END>
+__device__ __forceinline__ float xor_sum(float x) {
+  if constexpr (FROM >= END)
+    return x;
+  else
+    return xor_sum<FROM * 2, END>(xor_add<FROM>(x));
+}
+
 template <int KFMT, int LPH, int U, int QFMT = SPOT_KFMT_BF16>
 __device__ __forceinline__ float score_blocks(const void* __restrict__ q_sel,
                                              const float* __restrict__ w,
@@ -266,6 +304,11 @@ __device__ __forceinline__ float score_blocks(const void* __restrict__ q_sel,
                                              uint32_t* __restrict__ rec, int lane,
                                              const uint8_t* __restrict__ q_scale = nullptr,
                                              int rec_copies = 1, size_t rec_stride = 0) {
+  // No product is fused into a following addition: whether the compiler
+  // fuses one depends on the code around the call (it did for some runs
+  // of 8 blocks and not for runs of 16), and every caller must get the same
+  // bits for a block, whatever its run.
+#pragma clang fp contract(off)
   constexpr int kHeads = 64 / LPH;
   constexpr bool kIntQ = QFMT == SPOT_KFMT_INT4_G32 || QFMT == SPOT_KFMT_INT8_G32;
   uint4 qraw;
@@ -285,11 +328,9 @@ __device__ __forceinline__ float score_blocks(const void* __restrict__ q_sel,
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     float part = kIntQ ? key[u].dot_f(qf) * qsc : key[u].dot(qraw, qf);
-#pragma unroll
-    for (int off = 1; off < LPH; off <<= 1) part += __shfl_xor(part, off, 64);
+    part = xor_sum<1, LPH>(part);
     float v = wh * fmaxf(part, 0.f);
-#pragma unroll
-    for (int off = LPH; off < 64; off <<= 1) v += __shfl_xor(v, off, 64);
+    v = xor_sum<LPH, 64>(v);
     if (lane == u) res = v;
   }
   const int j = j0 + lane;
@@ -299,7 +340,7 @@ __device__ __forceinline__ float score_blocks(const void* __restrict__ q_sel,
       for (int c = 0; c < rec_copies; ++c)
         __hip_atomic_store(rec + c * rec_stride + j, rec_word(val), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
-    scores[(size_t)row * nblk + j] = val;
+    if (scores) scores[(size_t)row * nblk + j] = val;
   }
   return val;
 }
