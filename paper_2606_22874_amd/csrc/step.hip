@@ -422,6 +422,182 @@ __global__ __launch_bounds__(64 * kDecWaves, 2) void step_kernel(StepArgs a) {
   SPOT_STEP_TS(7);
 }
 
+// ---- Short rows: a step whose rows have at most kSmallBlocks blocks.  The
+// two hand-offs of step_kernel (scores to the selector, the set to the
+// attention workgroups) cost ~1.5 us each, more than scoring a short row
+// takes, so here every workgroup of a sequence scores the whole row itself
+// (the row's selector cache is at most 128 KiB and stays in L2), keeps the
+// scores in LDS, runs the same selection core on them and takes its share
+// of the ascending list directly; only workgroup (KV head 0, slot 0) of the
+// sequence writes the scores, idx, count and nucleus mass.  Scores, set and
+// split are those of step_kernel (same scoring code, same selection core,
+// same n_slot), so the results are the same bits.  No workgroup waits for
+// another (the last finisher of a pair merges, as in step_kernel); the
+// expiry word keeps its meaning: a launch that finds it set (or the forced
+// expiry of the tests) selects nothing and reports count = -1.
+constexpr int kSmallBlocks = 128;
+constexpr int kSmallRun = 16;   // blocks per scoring call of one wave
+
+// Score source of the short-row kernel: the row's scores in LDS; fails at
+// once (no ids) when give_up is set.
+struct LdsRowScores {
+  const float* s;
+  bool give_up;
+  template <int EPT>
+  __device__ __forceinline__ bool operator()(float (&sv)[EPT], int j0, int nv) const {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) sv[e] = !give_up && j0 + e < nv ? s[j0 + e] : -INFINITY;
+    return !give_up;
+  }
+};
+
+template <int KFMT, int LPH>
+__device__ __forceinline__ float score_small(const StepArgs& a, int row, int nv, int j0,
+                                             float* scores, int lane) {
+  if (KFMT == SPOT_KFMT_BF16 || a.qfmt == SPOT_KFMT_BF16)
+    return score_blocks<KFMT, LPH, kSmallRun>(a.q_sel, a.w, a.k_sel, a.k_scale, row, row,
+                                              a.nblk, nv, j0, a.nblk, scores, nullptr, lane);
+  return score_blocks<KFMT, LPH, kSmallRun, KFMT>(a.q_sel, a.w, a.k_sel, a.k_scale, row, row,
+                                                  a.nblk, nv, j0, a.nblk, scores, nullptr, lane,
+                                                  a.q_scale);
+}
+
+__device__ __forceinline__ float score_small_rt(const StepArgs& a, int row, int nv, int j0,
+                                                float* scores, int lane) {
+  if (a.lph == 8) {
+    switch (a.kfmt) {
+      case SPOT_KFMT_BF16: return score_small<SPOT_KFMT_BF16, 8>(a, row, nv, j0, scores, lane);
+      case SPOT_KFMT_INT4_G32:
+        return score_small<SPOT_KFMT_INT4_G32, 8>(a, row, nv, j0, scores, lane);
+      case SPOT_KFMT_INT8_G32:
+        return score_small<SPOT_KFMT_INT8_G32, 8>(a, row, nv, j0, scores, lane);
+      case SPOT_KFMT_MXFP8_G32:
+        return score_small<SPOT_KFMT_MXFP8_G32, 8>(a, row, nv, j0, scores, lane);
+      default: return score_small<SPOT_KFMT_MXFP4_G32, 8>(a, row, nv, j0, scores, lane);
+    }
+  }
+  switch (a.kfmt) {
+    case SPOT_KFMT_BF16: return score_small<SPOT_KFMT_BF16, 16>(a, row, nv, j0, scores, lane);
+    case SPOT_KFMT_INT4_G32:
+      return score_small<SPOT_KFMT_INT4_G32, 16>(a, row, nv, j0, scores, lane);
+    case SPOT_KFMT_INT8_G32:
+      return score_small<SPOT_KFMT_INT8_G32, 16>(a, row, nv, j0, scores, lane);
+    case SPOT_KFMT_MXFP8_G32:
+      return score_small<SPOT_KFMT_MXFP8_G32, 16>(a, row, nv, j0, scores, lane);
+    default: return score_small<SPOT_KFMT_MXFP4_G32, 16>(a, row, nv, j0, scores, lane);
+  }
+}
+
+// One id per thread (EPT = 1: nblk <= kSmallBlocks < 256).
+template <int SPL, int G>
+__global__ __launch_bounds__(64 * kDecWaves, 2) void step_small_kernel(StepArgs a) {
+  constexpr int EPT = 1;
+  __shared__ StepSmem<EPT, SPL, G> sm;
+  __shared__ float sc[kSmallBlocks];
+  static_assert(offsetof(DecodeSmem<G>, ids) >= sizeof(SelWgSmem<EPT, SPL>),
+                "decode list overlaps the selection storage");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_slot = a.n_slot;
+  const int pair = blockIdx.x / n_slot, slot = blockIdx.x % n_slot;
+  const int b = pair / a.h_kv, g = pair % a.h_kv;
+  const bool failed_before = load_rec(a.sticky) != 0u;
+  const int sl = min(a.seq_len[b], a.l_cap);
+  const bool writer = g == 0 && slot == 0;
+  int nv = a.n_valid ? a.n_valid[b] : a.nblk;
+  nv = nv < 0 ? 0 : (nv > a.nblk ? a.nblk : nv);
+  SPOT_STEP_TS(0);
+
+  // The attention's query fragment goes out first; it waits in registers.
+  const QueryFrag qf = load_query_heads<G>(a.q, b, g, a.h_q);
+
+  // ---- 1. scoring: the whole row, runs of kSmallRun blocks per wave.  The
+  // key loads do not wait for n_valid (every block of the row is in the
+  // cache); scores past it become -inf here, as score_blocks makes them.
+  for (int j0 = wave * kSmallRun; j0 < a.nblk; j0 += kDecWaves * kSmallRun) {
+    const float v = score_small_rt(a, b, a.nblk, j0, nullptr, lane);
+    const int j = j0 + lane;
+    if (lane < kSmallRun && j < a.nblk) sc[j] = j < nv ? v : -INFINITY;
+  }
+  __syncthreads();
+  if (writer)
+    for (int j = tid; j < a.nblk; j += kSelWG) a.scores[(size_t)b * a.nblk + j] = sc[j];
+  SPOT_STEP_TS(1);
+
+  // ---- 2. selection, then this workgroup's share of the list
+  const SelRow r = select_row_core<EPT, SPL>(
+      sm.sel, LdsRowScores{sc, failed_before || a.force_expire != 0}, nv, a.top_p, a.k_max,
+      a.k_min, a.n_sink, a.n_recent);
+  SPOT_STEP_TS(2);
+  int total;
+  const int pos = sel_positions(sm.sel, r.fin, total);
+  if (writer) {
+    if (r.ok) {
+      sel_write<EPT>(a.idx + (size_t)b * a.k_max, a.count + b, a.mass ? a.mass + b : nullptr,
+                     a.k_max, r.fin, pos, total, r.mass);
+    } else if (tid == 0) {
+      if (!failed_before) store_rec(a.sticky, 1u);
+      store_rec(a.count + b, -1);
+    }
+  }
+  // The list is S in ascending id, cut at k_max entries; the ids below
+  // nb_valid are a prefix of it, [0, n_ok), n_ok read off thread nb_valid's
+  // position (nb_valid <= nblk < 256).  Entries slot, slot + n_slot, ...
+  // of that prefix are the share (as the stand-alone decode takes them).
+  const int nb_valid = (sl + kBlk - 1) / kBlk;
+  const int n_entries = min(total, a.k_max);
+  if (tid == nb_valid) {
+    const int n_ok = min(pos, n_entries);
+    sm.dec.n_local = n_ok > slot ? min((n_ok - slot + n_slot - 1) / n_slot, kMaxIds) : 0;
+  }
+  if ((r.fin & 1u) && tid < nb_valid && pos < n_entries && pos >= slot &&
+      (pos - slot) % n_slot == 0 && (pos - slot) / n_slot < kMaxIds)
+    sm.dec.ids[(pos - slot) / n_slot] = tid;
+  __syncthreads();
+  const int n_local = sm.dec.n_local;
+  SPOT_STEP_TS(3);
+  SPOT_STEP_TS(4);
+
+  // ---- 3. attention on the share, partials, the last finisher merges
+  const size_t head_base = ((size_t)b * a.h_kv + g) * (size_t)a.l_cap * kD;
+  auto blk_of = [&](int n) { return sm.dec.ids[n]; };
+  const Partials<G> hp = attend_blocks<G>(sm.dec, qf, a.k + head_base, a.v + head_base, sl,
+                                           n_local, blk_of, a.scale_log2, NoHook{});
+  SPOT_STEP_TS(5);
+#pragma unroll
+  for (int jh = 0; jh < Partials<G>::HPW; ++jh) {
+    const size_t bh = (size_t)b * a.h_q + g * G + wave + kDecWaves * jh;
+    store_coherent(&a.part_o[(bh * n_slot + slot) * kD + 2 * lane],
+                   make_float2(hp.h[jh].o0, hp.h[jh].o1));
+    if (lane == 0)
+      store_coherent(&a.part_ml[(bh * n_slot + slot) * 2], make_float2(hp.h[jh].M, hp.h[jh].L));
+  }
+  wait_stores();
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned prev = __hip_atomic_fetch_add(&a.pair_cnt[pair], 1u, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+    sm.dec.last = prev == (unsigned)(n_slot - 1);
+  }
+  __syncthreads();
+  SPOT_STEP_TS(6);
+  if (!sm.dec.last) return;
+  if (tid == 0) store_rec(&a.pair_cnt[pair], 0u);
+#pragma unroll
+  for (int jh = 0; jh < Partials<G>::HPW; ++jh)
+    merge_head(a.part_o, a.part_ml, n_slot, (size_t)b * a.h_q + g * G + wave + kDecWaves * jh,
+               a.out, a.lse, lane);
+  SPOT_STEP_TS(7);
+}
+
+template <int SPL, int G>
+hipError_t launch_small_t(StepArgs& a, int n_pairs, int n_slot_max, hipStream_t s) {
+  a.n_slot = n_slot_max;
+  a.slot_div = ((1 << 18) + a.n_slot - 1) / a.n_slot;
+  hipLaunchKernelGGL((step_small_kernel<SPL, G>), dim3(n_pairs * a.n_slot), dim3(64 * kDecWaves),
+                     0, s, a);
+  return hipGetLastError();
+}
+
 // Workgroups of one step kernel that can be resident at once (per CU times
 // the CU count), queried once per device and instantiation.  The value only
 // depends on the device, so concurrent first calls store the same number.
@@ -625,6 +801,18 @@ hipError_t launch_decode_step(const void* q_sel, const void* q_scale, int qfmt, 
   const int cap = k_max < a.nblk ? k_max : a.nblk;
   while (P < cap) P <<= 1;
   const int spl = P <= 64 ? 1 : P / 64;
+  if (a.nblk <= kSmallBlocks) {   // P <= 128
+#ifdef SPOT_STEP_GROUP4_ONLY
+    return spl == 1 ? launch_small_t<1, 4>(a, n_pairs, n_slot_max, s)
+                    : launch_small_t<2, 4>(a, n_pairs, n_slot_max, s);
+#else
+    if (h_q == 8 * h_kv)
+      return spl == 1 ? launch_small_t<1, 8>(a, n_pairs, n_slot_max, s)
+                      : launch_small_t<2, 8>(a, n_pairs, n_slot_max, s);
+    return spl == 1 ? launch_small_t<1, 4>(a, n_pairs, n_slot_max, s)
+                    : launch_small_t<2, 4>(a, n_pairs, n_slot_max, s);
+#endif
+  }
   const int ept = a.nblk <= 256 ? 1 : a.nblk <= 512 ? 2 : a.nblk <= 1024 ? 4
                 : a.nblk <= 2048 ? 8 : 16;
 #ifdef SPOT_STEP_GROUP4_ONLY

@@ -224,15 +224,18 @@ def test_step_repeated_calls_reset_workspace():
     assert spot.spot_decode_step_status(ws, wl.B, wl.Hq, wl.Hkv, wl.d, wl.rule.k_max) == 0
 
 
-def test_step_expired_wait_is_reported():
+@pytest.mark.parametrize("cfg", [3, 1])
+def test_step_expired_wait_is_reported(cfg):
     """A fused step whose waits expire (forced from the host: every
     workgroup's wait for its sequence's scores gives up at once, so every
     kernel still exits normally) attends to nothing, reports count = -1 and
     sets the workspace's expiry word; later calls on that workspace do the
     same without waiting until spot_decode_step_status reports the expiry and
     restores the workspace, after which a call equals the three separate
-    calls bit for bit."""
-    wl = workload(3)
+    calls bit for bit.  Workload 1 (64 blocks per row) runs the short-row
+    kernel, which waits for nothing but honours the forced expiry and the
+    expiry word the same way."""
+    wl = workload(cfg)
     x = inputs(wl, "bf16")
     args = (wl.B, wl.Hq, wl.Hkv, wl.d, wl.rule.k_max)
     ws = spot.step_workspace(*args, DEV)
@@ -258,7 +261,41 @@ def test_step_expired_wait_is_reported():
     print("[step] normal call after the reset", flush=True)
     fus = fused(x, wl, ws)
     torch.cuda.synchronize()
-    assert_same(sep, fus, bitwise=True)
+    assert_same(sep, fus, bitwise=(cfg == 3))
+
+
+SHORT_ROWS = [
+    dict(i=1),                                            # 4096 tokens, batch 1: 64 blocks
+    dict(i=2, B=3, L=8192, seq_len=(8192, 100, 4097)),    # 128 blocks, ragged
+    dict(i=2, B=2, L=2048, seq_len=(2048, 1)),            # 32 blocks, fewer than k_max
+]
+
+
+@pytest.mark.parametrize("case", range(len(SHORT_ROWS)))
+@pytest.mark.parametrize("fmt", ["bf16", "int4", "mxfp8"])
+def test_step_short_rows(case, fmt):
+    """Rows of at most 128 blocks take the short-row kernel: every workgroup
+    of a sequence scores and selects the sequence itself.  Scores, block sets
+    and counts equal the separate calls bit for bit (the same scoring code;
+    the selection rule decides the same set), the outputs too where both
+    paths split the attention alike (batch 1), the nucleus mass to FP32
+    rounding; and the outputs match the oracle's attention on that set."""
+    kw = dict(SHORT_ROWS[case])
+    wl = workload(kw.pop("i"), **kw)
+    assert wl.nblk <= 128
+    x = inputs(wl, fmt)
+    print(f"[step] short rows {SHORT_ROWS[case]} {fmt}", flush=True)
+    sep = separate(x, wl)
+    fus = fused(x, wl)
+    torch.cuda.synchronize()
+    assert_same(sep, fus)
+    if wl.B == 1:
+        assert torch.equal(sep[4], fus[4]) and torch.equal(sep[5], fus[5])
+    idx, cnt = fus[1].cpu().numpy(), fus[2].cpu().numpy()
+    out_o, lse_o = oracle.sparse_decode(wl.q, wl.k, wl.v, wl.seq_len, idx, cnt, wl.sm_scale)
+    g = fus[4].float().cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(g - out_o)) <= 2e-2
+    assert np.linalg.norm(g - out_o) / max(np.linalg.norm(out_o), 1e-30) <= 1e-2
 
 
 def test_step_ragged_sequences():
