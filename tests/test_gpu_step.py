@@ -113,12 +113,16 @@ def test_step_matches_separate_calls(cfg, fmt):
 
 
 @pytest.mark.parametrize("fmt", ["int4", "int8", "mxfp4", "mxfp8"])
-def test_step_quantized_queries(fmt):
+@pytest.mark.parametrize("cfg", [3, 1])
+def test_step_quantized_queries(fmt, cfg):
     """spot_decode_step_q: queries and the selector key cache in one quantized
-    format (the 128K-token workload).  The fused launch equals the separate
-    calls (spot_selector_score_q, selection, decode) bit for bit, and its
-    scores and selection match the oracle on the same codes."""
-    wl = workload(3)
+    format (the 128K-token workload; and 4K tokens, batch 1, on the short-row
+    kernel).  The fused launch equals the separate calls
+    (spot_selector_score_q, selection, decode) bit for bit (at 4K tokens the
+    nucleus mass to FP32 rounding: the separate selection of short rows is
+    the one-wave kernel), and its scores and selection match the oracle on
+    the same codes."""
+    wl = workload(cfg)
     x = inputs(wl, fmt)
     qc, qs = synth.QUANTIZERS[fmt](wl.q_sel)
     qs_dev = qs.view(np.uint16).view(np.int16) if fmt in ("int4", "int8") else qs
@@ -134,7 +138,8 @@ def test_step_quantized_queries(fmt):
                            wl.rule, k_scale=x["k_scale"], kfmt=fmt, n_valid=x["n_valid"],
                            sm_scale=wl.sm_scale, q_scale=q_scale, qfmt=fmt)
     torch.cuda.synchronize()
-    assert_same((s0, i0, c0, m0, o0, l0), fus, bitwise=True)
+    assert_same((s0, i0, c0, m0, o0, l0), fus, bitwise=(cfg == 3))
+    assert torch.equal(o0, fus[4]) and torch.equal(l0, fus[5])
     kc, ks = synth.QUANTIZERS[fmt](wl.k_sel)
     s_o = oracle.selector_score_qk(qc, qs, fmt, wl.w, kc, ks, fmt, wl.B, wl.nblk, wl.Hs, wl.ds,
                                    n_valid=wl.n_valid)
