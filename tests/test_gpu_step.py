@@ -273,6 +273,7 @@ SHORT_ROWS = [
     dict(i=1),                                            # 4096 tokens, batch 1: 64 blocks
     dict(i=2, B=3, L=8192, seq_len=(8192, 100, 4097)),    # 128 blocks, ragged
     dict(i=2, B=2, L=2048, seq_len=(2048, 1)),            # 32 blocks, fewer than k_max
+    dict(i=2, B=2, L=6400, seq_len=(6400, 3001)),         # 100 blocks: a partial scoring run
 ]
 
 
