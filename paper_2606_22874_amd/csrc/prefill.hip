@@ -68,8 +68,10 @@ __device__ __forceinline__ void stage_tile(const uint16_t* __restrict__ src, uns
     const int p = base + lane;
     const int r = p >> 4, pc = p & 15;
     const int lc = IS_K ? swz_k(r, pc) : swz_v(r, pc);
-    __builtin_amdgcn_global_load_lds(src + r * kD + lc * 8, (lds_void*)(dst + base * 16), 16, 0,
-                                     0);
+    // unsigned lane offset: with a uniform src the load takes a scalar base
+    // and a 32-bit offset instead of 64-bit lane addresses
+    const uint32_t off = (uint32_t)(r * kD + lc * 8);
+    __builtin_amdgcn_global_load_lds(src + off, (lds_void*)(dst + base * 16), 16, 0, 0);
   }
 }
 
@@ -365,7 +367,12 @@ __global__ __launch_bounds__(64 * W) void prefill_kernel(
 
   const uint16_t* kg = k + (int64_t)(b * h_kv + g) * L * kD;
   const uint16_t* vg = v + (int64_t)(b * h_kv + g) * L * kD;
-  auto blk = [](const uint16_t* base, int j) { return base + (int64_t)j * kBlk * kD; };
+  // The block id read from LDS is the same in every lane; readfirstlane
+  // makes the tile's base address scalar, so the tile copies below take the
+  // scalar-base form with a 32-bit lane offset.
+  auto blk = [](const uint16_t* base, int j) {
+    return base + (int64_t)__builtin_amdgcn_readfirstlane(j) * kBlk * kD;
+  };
 
   // Ping-pong schedule.  The waves form two groups, 0..W/2-1 and W/2..W-1,
   // so the two waves sharing a SIMD belong to different groups.  A wave in
