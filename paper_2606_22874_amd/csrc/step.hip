@@ -429,10 +429,12 @@ __global__ __launch_bounds__(64 * kDecWaves, 2) void step_kernel(StepArgs a) {
 // (the row's selector cache is at most 128 KiB and stays in L2), keeps the
 // scores in LDS, runs the same selection core on them and takes its share
 // of the ascending list directly; only workgroup (KV head 0, slot 0) of the
-// sequence writes the scores, idx, count and nucleus mass.  Scores, set and
-// split are those of step_kernel (same scoring code, same selection core,
-// same n_slot), so the results are the same bits.  No workgroup waits for
-// another (the last finisher of a pair merges, as in step_kernel); the
+// sequence writes the scores, idx, count and nucleus mass.  Scores and set
+// are those of step_kernel (same scoring code, same selection core) and the
+// split is the stand-alone decode's (at most 16 workgroups per pair, with no
+// residency cap, since nothing waits), so the results are the same bits as
+// step_kernel's wherever its own split is not capped.  No workgroup waits
+// for another (the last finisher of a pair merges, as in step_kernel); the
 // expiry word keeps its meaning: a launch that finds it set (or the forced
 // expiry of the tests) selects nothing and reports count = -1.
 constexpr int kSmallBlocks = 128;
